@@ -1,0 +1,96 @@
+"""Block compositions of the oracle, with the storage rounding points of the
+GPU path: every tensor that one GPU kernel writes and another reads is rounded
+to the storage dtype here at the same point; all arithmetic inside a step is
+float64.  The final outputs are returned unrounded except where the step
+itself stores them.
+
+TEST INFRASTRUCTURE ONLY (see the package docstring).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from . import ops
+from .numerics import store
+
+
+PAIR_ORDER_BLOCK = ("bcast", "lin", "att_row", "tri_out", "trans", "single")
+PAIR_ORDER_STACK = ("bcast", "tri_out", "tri_in", "att_row", "att_col", "trans", "single")
+
+
+def pair_block(s, lengths, p, dims, order, z=None, dtype="bf16"):
+    """One single-pair-single block (Eq. running-block generalised with the
+    Pairformer-style steps of Sec. 4.3).
+
+    s       [sum N, C_s] single track;  z: [sum N^2, C_z] pair state or None.
+    p       weights (see the input generator), dims: dict(c_z, heads, head_dim).
+    order   sequence of steps:
+      bcast    z = [z +] bcast(u, v), [u|v] = s W_uv^T + b_uv     (Eq. running-block l.1)
+      lin      z = LN(z) W^T + b                                   (Sec. 3.3)
+      att_row  [q|k|v|beta] = LN(z) W^T + b; o = attention axis 0; z += o W_o^T + b_o
+      att_col  the same around the ending node (axis 1)
+      tri_out  [a|b] = LN(z) W^T + b; z += triangle_outgoing(a, b)
+      tri_in   [a|b] = LN(z) W^T + b; z += triangle_incoming(a, b)
+      trans    z = z + SwiGLU(LN(z))                                (Eq. running-block l.2)
+      single   m = mean_b z[.,b];  s = s + m W_s^T + b_s            (Eq. running-block l.3)
+    Returns (s, z, trace) where trace maps step names to intermediate values.
+    """
+    C, H, d = dims["c_z"], dims["heads"], dims["head_dim"]
+    st = lambda t: store(t, dtype)          # noqa: E731
+    trace = {}
+    s = np.asarray(s, np.float64)
+    for step in order:
+        if step == "bcast":
+            uv = st(ops.layernorm_linear(s, p["uv.w"], p["uv.b"]))
+            trace["uv"] = uv
+            z = st(ops.pair_broadcast(uv[:, :C], uv[:, C:], lengths, z_in=z))
+        elif step == "lin":
+            z = st(ops.layernorm_linear(z, p["lin.w"], p["lin.b"], ln=(p["lin.ln_g"], p["lin.ln_b"])))
+        elif step in ("att_row", "att_col"):
+            key = step
+            proj = ops.layernorm_linear(z, p[key + ".w"], p[key + ".b"],
+                                        ln=(p[key + ".ln_g"], p[key + ".ln_b"]))
+            q, k, v = st(proj[:, :C]), st(proj[:, C:2 * C]), st(proj[:, 2 * C:3 * C])
+            beta = st(proj[:, 3 * C:3 * C + H])
+            o = st(ops.pair_row_attention(q, k, v, beta, lengths, H, d,
+                                          axis=0 if step == "att_row" else 1))
+            trace[step + ".o"] = o
+            z = st(ops.layernorm_linear(o, p[key + ".wo"], p[key + ".bo"],
+                                        epilogue="residual", residual=z))
+        elif step in ("tri_out", "tri_in"):
+            ab = st(ops.layernorm_linear(z, p[step + ".w"], p[step + ".b"],
+                                         ln=(p[step + ".ln_g"], p[step + ".ln_b"])))
+            t = ops.triangle_mul(ab[:, :C], ab[:, C:], lengths,
+                                 "outgoing" if step == "tri_out" else "incoming")
+            z = st(z + t)
+        elif step == "trans":
+            z = st(ops.layernorm_linear(z, p["trans.w"], p["trans.b"],
+                                        ln=(p["trans.ln_g"], p["trans.ln_b"]),
+                                        epilogue="swiglu_residual",
+                                        w2=p["trans.w2"], b2=p["trans.b2"]))
+        elif step == "single":
+            m = ops.segment_reduce(z, lengths, "pair_cols", "mean")   # stored fp32
+            trace["col_mean"] = m
+            s = st(ops.layernorm_linear(m, p["single.w"], p["single.b"],
+                                        epilogue="residual", residual=s))
+        else:
+            raise ValueError(f"unknown step {step!r}")
+        trace[step] = z
+    return s, z, trace
+
+
+def encoder_layer(x, lengths, p, heads, head_dim, dtype="bf16"):
+    """Pre-LayerNorm Transformer encoder layer on packed tokens followed by a
+    per-sample mean pool (the 1-D token path: Sec. 3.3 "Attention through
+    packed blocks"; BERT-Base shape of Appendix C).
+    Returns (x_out, pooled, trace)."""
+    st = lambda t: store(t, dtype)          # noqa: E731
+    c = heads * head_dim
+    x = np.asarray(x, np.float64)
+    qkv = st(ops.layernorm_linear(x, p["qkv.w"], p["qkv.b"], ln=(p["ln1_g"], p["ln1_b"])))
+    o = st(ops.attention_1d(qkv[:, :c], qkv[:, c:2 * c], qkv[:, 2 * c:], lengths, heads, head_dim))
+    x = st(ops.layernorm_linear(o, p["o.w"], p["o.b"], epilogue="residual", residual=x))
+    h = st(ops.layernorm_linear(x, p["ffn1.w"], p["ffn1.b"], ln=(p["ln2_g"], p["ln2_b"]), epilogue="gelu"))
+    x = st(ops.layernorm_linear(h, p["ffn2.w"], p["ffn2.b"], epilogue="residual", residual=x))
+    pooled = ops.segment_reduce(x, lengths, "samples", "mean")
+    return x, pooled, {"qkv": qkv, "o": o, "h": h}

@@ -1,0 +1,179 @@
+"""Seeded synthetic workloads: length vectors, activations and weights.
+
+This module only draws random numbers and describes workload shapes.  It holds
+none of the packed-tensor arithmetic, so the GPU path and the CPU oracle can be
+fed byte-identical inputs without sharing any of the computation.
+
+Length distributions follow the pair workloads of the paper's evaluation
+(square pair regimes of Table "regimes", Appendix C) and a BERT-Base-shaped
+token batch (IMDB / BERT, Appendix C, B=64); no dataset is read.  Values are
+drawn in float64, converted to float32 and, for bf16 workloads, snapped to the
+nearest bf16 value (round to nearest even) so that every input is exactly
+representable in the storage type of both sides.
+"""
+from __future__ import annotations
+
+import zlib
+from dataclasses import dataclass, field
+
+import numpy as np
+
+__all__ = [
+    "Workload", "WORKLOADS", "lengths_for", "tensor_rng", "snap_bf16",
+    "pair_block_params", "encoder_layer_params", "normal",
+]
+
+
+@dataclass(frozen=True)
+class Workload:
+    """One synthetic workload: batch geometry, widths and storage dtype."""
+    name: str
+    kind: str                  # "pair" (pair block / stack) or "tokens"
+    batch: int
+    dist: tuple                # ("uniform", lo, hi) or ("lognormal", mu, sigma, lo, hi)
+    seed: int
+    dtype: str                 # "f32" or "bf16"
+    c_s: int = 0               # single width
+    c_z: int = 0               # pair width
+    heads: int = 0
+    head_dim: int = 0
+    hidden: int = 0            # transition / FFN hidden width
+    blocks: int = 1
+    transition: bool = True
+    tri_incoming: bool = False
+    col_attention: bool = False
+    single_update: bool = True
+    gains: dict = field(default_factory=dict, compare=False, hash=False)
+
+
+def _pair_gains(n_max: int, blocks: int = 1) -> dict:
+    # Gains keep every bf16 tensor that crosses a kernel boundary well inside
+    # |v| < 4 (std <= ~0.6), so that the bf16 half-ulp stays <= 2^-8.
+    damp = 1.0 / np.sqrt(blocks)
+    return {
+        "uv": 0.35 * damp,        # z = u_a + v_b has std ~0.5
+        "lin": 0.5,               # LayerNorm+Linear that replaces z
+        "qkv": 0.5, "bias": 0.6,  # attention projections
+        "o": 0.5 * damp,          # attention output projection (residual)
+        # a, b std g so that t = sum_k a b has std ~0.3 for N = n_max
+        "ab": float(np.sqrt(0.3 / np.sqrt(n_max))) * np.sqrt(damp),
+        "gu": 1.0, "d": 0.25 * damp,   # SwiGLU transition
+        "s": 0.5,                 # single update from the column mean
+    }
+
+
+WORKLOADS = {
+    w.name: w for w in [
+        Workload("pair_tiny_f32_b4", "pair", 4, ("uniform", 4, 16), 0, "f32",
+                 c_s=32, c_z=16, heads=2, head_dim=8, hidden=64,
+                 transition=False, gains=_pair_gains(16)),
+        Workload("pair_b8_n208_224_bf16", "pair", 8, ("uniform", 208, 224), 0, "bf16",
+                 c_s=384, c_z=128, heads=4, head_dim=32, hidden=512,
+                 gains=_pair_gains(224)),
+        Workload("pair_b8_n32_512_bf16", "pair", 8, ("uniform", 32, 512), 1, "bf16",
+                 c_s=384, c_z=128, heads=4, head_dim=32, hidden=512,
+                 gains=_pair_gains(512)),
+        Workload("pairformer4_b16_lognormal192_bf16", "pair", 16,
+                 ("lognormal", 192.0, 0.6, 16, 768), 0, "bf16",
+                 c_s=384, c_z=128, heads=4, head_dim=32, hidden=512, blocks=4,
+                 tri_incoming=True, col_attention=True,
+                 gains=_pair_gains(768, blocks=4)),
+        Workload("tokens_b64_lognormal230_bf16", "tokens", 64,
+                 ("lognormal", 230.0, 0.5, 16, 512), 0, "bf16",
+                 c_s=768, heads=12, head_dim=64, hidden=3072,
+                 gains={"qkv": 0.5, "o": 0.5, "ffn1": 0.5, "ffn2": 0.5}),
+    ]
+}
+
+
+def lengths_for(w: Workload) -> np.ndarray:
+    """Per-sample lengths N_i (int32) of a workload, from its own seed."""
+    rng = np.random.default_rng(w.seed)
+    if w.dist[0] == "uniform":
+        _, lo, hi = w.dist
+        n = rng.integers(lo, hi, size=w.batch, endpoint=True)
+    elif w.dist[0] == "lognormal":
+        _, mu, sigma, lo, hi = w.dist
+        n = np.clip(np.rint(rng.lognormal(np.log(mu), sigma, size=w.batch)), lo, hi)
+    else:
+        raise ValueError(f"unknown length distribution {w.dist[0]!r}")
+    return np.asarray(n, dtype=np.int32)
+
+
+def tensor_rng(seed: int, name: str) -> np.random.Generator:
+    """An independent generator per named tensor, stable across runs."""
+    return np.random.default_rng(np.random.SeedSequence([seed, zlib.crc32(name.encode())]))
+
+
+def snap_bf16(x: np.ndarray) -> np.ndarray:
+    """Nearest bf16 value (round to nearest, ties to even), returned as float32."""
+    f = np.ascontiguousarray(x, dtype=np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
+    out = u.astype(np.uint32).view(np.float32)
+    return np.where(np.isnan(f), f, out)
+
+
+def normal(seed: int, name: str, shape, scale: float = 1.0, dtype: str = "f32",
+           loc: float = 0.0) -> np.ndarray:
+    """loc + scale * N(0,1) draws for one named tensor, stored as float32."""
+    x = (loc + scale * tensor_rng(seed, name).standard_normal(shape)).astype(np.float32)
+    return snap_bf16(x) if dtype == "bf16" else x
+
+
+def _linear(seed, name, n_out, n_in, gain, dtype):
+    w = normal(seed, name + ".w", (n_out, n_in), gain / np.sqrt(n_in), dtype)
+    b = normal(seed, name + ".b", (n_out,), 0.1 * gain)          # fp32 always
+    return w, b
+
+
+def _ln(seed, name, c):
+    return (normal(seed, name + ".gamma", (c,), 0.1, loc=1.0),
+            normal(seed, name + ".beta", (c,), 0.1))
+
+
+def pair_block_params(w: Workload, block: int = 0, seed: int | None = None) -> dict:
+    """Random-init weights of one pair block (see the block recipe in the
+    oracle).  Matrices are [out, in] (y = x W^T + b), stored in the workload
+    dtype; biases and LayerNorm affine parameters are float32."""
+    seed = w.seed if seed is None else seed
+    g, dt, cz, cs, H = w.gains, w.dtype, w.c_z, w.c_s, w.heads
+    p = {}
+    pre = f"blk{block}."
+    p["uv.w"], p["uv.b"] = _linear(seed, pre + "uv", 2 * cz, cs, g["uv"], dt)
+    if block == 0:
+        p["lin.ln_g"], p["lin.ln_b"] = _ln(seed, pre + "lin", cz)
+        p["lin.w"], p["lin.b"] = _linear(seed, pre + "lin", cz, cz, g["lin"], dt)
+    attn = ["row"] + (["col"] if w.col_attention else [])
+    for a in attn:
+        p[f"att_{a}.ln_g"], p[f"att_{a}.ln_b"] = _ln(seed, pre + "att_" + a, cz)
+        wq, bq = _linear(seed, pre + f"att_{a}.qkv", 3 * cz, cz, g["qkv"], dt)
+        wb, bb = _linear(seed, pre + f"att_{a}.bias", H, cz, g["bias"], dt)
+        p[f"att_{a}.w"] = np.concatenate([wq, wb], 0)
+        p[f"att_{a}.b"] = np.concatenate([bq, bb], 0)
+        p[f"att_{a}.wo"], p[f"att_{a}.bo"] = _linear(seed, pre + f"att_{a}.o", cz, cz, g["o"], dt)
+    tri = ["out"] + (["in"] if w.tri_incoming else [])
+    for t in tri:
+        p[f"tri_{t}.ln_g"], p[f"tri_{t}.ln_b"] = _ln(seed, pre + "tri_" + t, cz)
+        p[f"tri_{t}.w"], p[f"tri_{t}.b"] = _linear(seed, pre + f"tri_{t}", 2 * cz, cz, g["ab"], dt)
+    if w.transition:
+        p["trans.ln_g"], p["trans.ln_b"] = _ln(seed, pre + "trans", cz)
+        p["trans.w"], p["trans.b"] = _linear(seed, pre + "trans.gu", 2 * w.hidden, cz, g["gu"], dt)
+        p["trans.w2"], p["trans.b2"] = _linear(seed, pre + "trans.d", cz, w.hidden, g["d"], dt)
+    if w.single_update:
+        p["single.w"], p["single.b"] = _linear(seed, pre + "single", cs, cz, g["s"], dt)
+    return p
+
+
+def encoder_layer_params(w: Workload, seed: int | None = None) -> dict:
+    """Random-init weights of one pre-LayerNorm encoder layer (token path)."""
+    seed = w.seed if seed is None else seed
+    g, dt, c = w.gains, w.dtype, w.c_s
+    p = {}
+    p["ln1_g"], p["ln1_b"] = _ln(seed, "enc.ln1", c)
+    p["qkv.w"], p["qkv.b"] = _linear(seed, "enc.qkv", 3 * c, c, g["qkv"], dt)
+    p["o.w"], p["o.b"] = _linear(seed, "enc.o", c, c, g["o"], dt)
+    p["ln2_g"], p["ln2_b"] = _ln(seed, "enc.ln2", c)
+    p["ffn1.w"], p["ffn1.b"] = _linear(seed, "enc.ffn1", w.hidden, c, g["ffn1"], dt)
+    p["ffn2.w"], p["ffn2.b"] = _linear(seed, "enc.ffn2", c, w.hidden, g["ffn2"], dt)
+    return p

@@ -1,0 +1,150 @@
+"""Block-level pins: the packed oracle blocks equal independent masked padded
+computations on the valid cells (Sec. 3.3 and the reference-semantics contract
+of Appendix A), and the token path equals torch's own pre-LayerNorm encoder
+layer on a padded batch with a key padding mask."""
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+from oracle import blocks, layout
+from paper_2609_30379_amd import synth
+
+
+def _params(c_s, c_z, H, hidden, seed, transition=True, cols=True, tri_in=True):
+    w = synth.Workload("t", "pair", 1, ("uniform", 1, 1), seed, "f32", c_s=c_s, c_z=c_z, heads=H,
+                       head_dim=c_z // H, hidden=hidden, transition=transition,
+                       tri_incoming=tri_in, col_attention=cols, gains=synth._pair_gains(8))
+    return synth.pair_block_params(w, block=0, seed=seed)
+
+
+def _padded_pair_block(s, L, p, H, d, order, z=None):
+    """Padded reference on [B, N, N, C] with torch ops; padded keys are masked
+    and padded a/b cells zeroed, so only valid cells are meaningful."""
+    T = lambda x: torch.from_numpy(np.asarray(x, np.float64))   # noqa: E731
+    B, N, C = len(L), max(L), H * d
+    o1 = layout.single_offsets(L)
+    sp = torch.zeros(B, N, s.shape[1], dtype=torch.float64)
+    for i, n in enumerate(L):
+        sp[i, :n] = T(s[o1[i]:o1[i + 1]])
+    valid = torch.zeros(B, N, dtype=torch.bool)
+    for i, n in enumerate(L):
+        valid[i, :n] = True
+    cellmask = valid[:, :, None] & valid[:, None, :]
+
+    def lnlin(x, key):
+        return F.linear(F.layer_norm(x, (x.shape[-1],), T(p[key + ".ln_g"]), T(p[key + ".ln_b"]), 1e-5),
+                        T(p[key + ".w"]), T(p[key + ".b"]))
+
+    def att(zz, key):
+        proj = lnlin(zz, key)
+        q = proj[..., :C].reshape(B, N, N, H, d)
+        k = proj[..., C:2 * C].reshape(B, N, N, H, d)
+        v = proj[..., 2 * C:3 * C].reshape(B, N, N, H, d)
+        bias = proj[..., 3 * C:3 * C + H]                         # [B, j, k, H]
+        logits = torch.einsum("brjhd,brkhd->brhjk", q, k) / np.sqrt(d) + bias.permute(0, 3, 1, 2)[:, None]
+        logits = logits.masked_fill(~valid[:, None, None, None, :], float("-inf"))
+        o = torch.einsum("brhjk,brkhd->brjhd", torch.softmax(logits, -1), v).reshape(B, N, N, C)
+        return zz + F.linear(o, T(p[key + ".wo"]), T(p[key + ".bo"]))
+
+    for step in order:
+        if step == "bcast":
+            uv = F.linear(sp, T(p["uv.w"]), T(p["uv.b"]))
+            zz = uv[..., :C][:, :, None, :] + uv[..., C:][:, None, :, :]
+            z = zz if z is None else z + zz
+        elif step == "lin":
+            z = lnlin(z, "lin")
+        elif step == "att_row":
+            z = att(z, "att_row")
+        elif step == "att_col":
+            z = att(z.transpose(1, 2), "att_col").transpose(1, 2)
+        elif step in ("tri_out", "tri_in"):
+            ab = lnlin(z, step) * cellmask[..., None]
+            a, b = ab[..., :C], ab[..., C:]
+            eq = "bxkc,bykc->bxyc" if step == "tri_out" else "bkxc,bkyc->bxyc"
+            z = z + torch.einsum(eq, a, b)
+        elif step == "trans":
+            xn = F.layer_norm(z, (C,), T(p["trans.ln_g"]), T(p["trans.ln_b"]), 1e-5)
+            gu = F.linear(xn, T(p["trans.w"]), T(p["trans.b"]))
+            Fh = gu.shape[-1] // 2
+            z = z + F.linear(F.silu(gu[..., :Fh]) * gu[..., Fh:], T(p["trans.w2"]), T(p["trans.b2"]))
+        elif step == "single":
+            n = torch.tensor(L, dtype=torch.float64).clamp(min=1)[:, None, None]
+            m = (z * valid[:, None, :, None]).sum(2) / n
+            sp = sp + F.linear(m, T(p["single.w"]), T(p["single.b"]))
+    zs = np.concatenate([z[i, :n, :n].reshape(n * n, C).numpy() for i, n in enumerate(L)])
+    ss = np.concatenate([sp[i, :n].numpy() for i, n in enumerate(L)])
+    return ss, zs
+
+
+@pytest.mark.parametrize("L,order", [
+    ([5, 3, 1, 4], blocks.PAIR_ORDER_BLOCK),
+    ([4, 6, 2], blocks.PAIR_ORDER_STACK),
+    ([3, 3, 3], blocks.PAIR_ORDER_BLOCK),     # all-equal lengths: ordinary dense batching
+])
+def test_pair_block_equals_masked_padded(L, order):
+    c_s, c_z, H = 12, 8, 2
+    p = _params(c_s, c_z, H, 16, seed=7)
+    s = synth.normal(7, "s", (sum(L), c_s))
+    dims = dict(c_z=c_z, heads=H, head_dim=c_z // H)
+    s_o, z_o, _ = blocks.pair_block(s, L, p, dims, order, dtype="f32")
+    s_r, z_r = _padded_pair_block(s, L, p, H, c_z // H, order)
+    np.testing.assert_allclose(z_o, z_r, rtol=1e-10, atol=1e-10)
+    np.testing.assert_allclose(s_o, s_r, rtol=1e-10, atol=1e-10)
+    assert z_o.shape[0] == layout.pair_offsets(L)[-1]
+
+
+def test_pair_block_accumulates_into_existing_state():
+    L, c_s, c_z, H = [3, 2], 6, 4, 2
+    p = _params(c_s, c_z, H, 8, seed=3)
+    s = synth.normal(3, "s", (5, c_s))
+    z0 = synth.normal(3, "z", (13, c_z))
+    dims = dict(c_z=c_z, heads=H, head_dim=2)
+    _, z_a, _ = blocks.pair_block(s, L, p, dims, ("bcast",), z=z0, dtype="f32")
+    _, z_b, _ = blocks.pair_block(s, L, p, dims, ("bcast",), dtype="f32")
+    np.testing.assert_allclose(z_a, z_b + z0, rtol=1e-13, atol=1e-13)
+
+
+def test_bf16_storage_points_round():
+    L = [3, 2]
+    p = _params(6, 4, 2, 8, seed=5)
+    s = synth.normal(5, "s", (5, 6), dtype="bf16")
+    _, z, tr = blocks.pair_block(s, L, p, dict(c_z=4, heads=2, head_dim=2), ("bcast", "lin"), dtype="bf16")
+    from oracle.numerics import round_bf16
+    assert np.array_equal(z, round_bf16(z))
+    assert np.array_equal(tr["uv"], round_bf16(tr["uv"]))
+
+
+def test_encoder_layer_matches_torch_encoder_layer(torch_cpu):
+    L, H, d, hidden = [5, 1, 7, 3], 2, 4, 24
+    c = H * d
+    w = synth.Workload("t", "tokens", 4, ("uniform", 1, 1), 2, "f32", c_s=c, heads=H, head_dim=d,
+                       hidden=hidden, gains={"qkv": 1.0, "o": 1.0, "ffn1": 1.0, "ffn2": 1.0})
+    p = synth.encoder_layer_params(w, seed=2)
+    x = synth.normal(2, "x", (sum(L), c))
+    xo, pooled, _ = blocks.encoder_layer(x, L, p, H, d, dtype="f32")
+
+    layer = torch.nn.TransformerEncoderLayer(c, H, hidden, dropout=0.0, activation="gelu",
+                                             batch_first=True, norm_first=True, dtype=torch.float64)
+    sd = {
+        "self_attn.in_proj_weight": p["qkv.w"], "self_attn.in_proj_bias": p["qkv.b"],
+        "self_attn.out_proj.weight": p["o.w"], "self_attn.out_proj.bias": p["o.b"],
+        "linear1.weight": p["ffn1.w"], "linear1.bias": p["ffn1.b"],
+        "linear2.weight": p["ffn2.w"], "linear2.bias": p["ffn2.b"],
+        "norm1.weight": p["ln1_g"], "norm1.bias": p["ln1_b"],
+        "norm2.weight": p["ln2_g"], "norm2.bias": p["ln2_b"],
+    }
+    layer.load_state_dict({k: torch.from_numpy(np.asarray(v, np.float64)) for k, v in sd.items()})
+    layer.eval()
+    B, N = len(L), max(L)
+    o = layout.single_offsets(L)
+    xp = torch.zeros(B, N, c, dtype=torch.float64)
+    pad = torch.ones(B, N, dtype=torch.bool)
+    for i, n in enumerate(L):
+        xp[i, :n] = torch.from_numpy(x[o[i]:o[i + 1]].astype(np.float64))
+        pad[i, :n] = False
+    with torch.no_grad():
+        ref = layer(xp, src_key_padding_mask=pad).numpy()
+    ref_packed = np.concatenate([ref[i, :n] for i, n in enumerate(L)])
+    np.testing.assert_allclose(xo, ref_packed, rtol=1e-10, atol=1e-10)
+    np.testing.assert_allclose(pooled, np.stack([ref[i, :n].mean(0) for i, n in enumerate(L)]), rtol=1e-10, atol=1e-10)

@@ -1,0 +1,102 @@
+"""The pins must be able to fail: plant plausible mistakes in the oracle (on the
+CPU only) and check that at least one pin catches each of them."""
+import numpy as np
+import pytest
+
+import oracle.ops as ops
+import oracle.numerics as numerics
+from oracle import layout
+from tests import test_oracle_ops as T_ops
+from tests import test_oracle_blocks as T_blk
+from tests import test_oracle_layout as T_lay
+
+
+def _fails(fn, *a, **k):
+    try:
+        fn(*a, **k)
+    except AssertionError:
+        return True
+    return False
+
+
+def _mut_broadcast_swapped(u, v, lengths, z_in=None):
+    return _orig["pair_broadcast"](v, u, lengths, z_in)
+
+
+def _mut_ln_unbiased(x, gamma, beta, eps=1e-5):
+    x = np.asarray(x, np.float64)
+    return (x - x.mean(-1, keepdims=True)) / np.sqrt(x.var(-1, ddof=1, keepdims=True) + eps) * gamma + beta
+
+
+def _mut_attention_bias_transposed(q, k, v, bias, lengths, heads, head_dim, axis=0, scale=None):
+    if bias is not None:
+        bias = np.array(bias, np.float64)
+        for off, n in zip(layout.pair_offsets(lengths), lengths):
+            blk = bias[off:off + n * n].reshape(n, n, -1)
+            bias[off:off + n * n] = blk.transpose(1, 0, 2).reshape(n * n, -1)
+    return _orig["pair_row_attention"](q, k, v, bias, lengths, heads, head_dim, axis, scale)
+
+
+def _mut_attention_no_scale(q, k, v, bias, lengths, heads, head_dim, axis=0, scale=None):
+    return _orig["pair_row_attention"](q, k, v, bias, lengths, heads, head_dim, axis, 1.0)
+
+
+def _mut_triangle_transposed(a, b, lengths, direction="outgoing"):
+    return _orig["triangle_mul"](b, a, lengths, direction)
+
+
+def _mut_triangle_direction(a, b, lengths, direction="outgoing"):
+    other = {"outgoing": "incoming", "incoming": "outgoing"}[direction]
+    return _orig["triangle_mul"](a, b, lengths, other)
+
+
+def _mut_reduce_rows(x, lengths, level="pair_cols", op="sum"):
+    if level != "pair_cols":
+        return _orig["segment_reduce"](x, lengths, level, op)
+    outs = []
+    for off, n in zip(layout.pair_offsets(lengths), lengths):
+        P = np.asarray(x[off:off + n * n], np.float64).reshape(n, n, -1)
+        Y = P.sum(axis=0)                       # reduces over rows instead of columns
+        outs.append(Y / n if op == "mean" and n else Y)
+    return np.concatenate(outs, 0)
+
+
+def _mut_pair_offsets(lengths):
+    return layout.offsets([int(n) * int(n) + (1 if i == 0 else 0) for i, n in enumerate(lengths)])
+
+
+_orig = {k: getattr(ops, k) for k in ("pair_broadcast", "pair_row_attention", "triangle_mul", "segment_reduce")}
+
+MUTANTS = [
+    ("broadcast_swapped", ops, "pair_broadcast", _mut_broadcast_swapped,
+     [(T_ops.test_broadcast_worked_example, ())]),
+    ("layernorm_unbiased", numerics, "layernorm", _mut_ln_unbiased,
+     [(T_ops.test_layernorm_linear_brute_force, ())]),
+    ("attention_bias_transposed", ops, "pair_row_attention", _mut_attention_bias_transposed,
+     [(T_ops.test_attention_brute_force, ()), (T_ops.test_attention_dominant_bias_selects_value, ())]),
+    ("attention_no_scale", ops, "pair_row_attention", _mut_attention_no_scale,
+     [(T_ops.test_attention_brute_force, ())]),
+    ("triangle_operands_swapped", ops, "triangle_mul", _mut_triangle_transposed,
+     [(T_ops.test_triangle_masked_padded_and_brute_force, ())]),
+    ("triangle_direction", ops, "triangle_mul", _mut_triangle_direction,
+     [(T_ops.test_triangle_masked_padded_and_brute_force, ())]),
+    ("reduce_over_rows", ops, "segment_reduce", _mut_reduce_rows,
+     [(T_ops.test_pair_column_sum_equation, ())]),
+    ("pair_offsets_off_by_one", layout, "pair_offsets", _mut_pair_offsets,
+     [(T_lay.test_worked_example_offsets_and_splits, ())]),
+]
+
+
+@pytest.mark.parametrize("name,mod,attr,mutant,pins", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_catch_planted_mistake(monkeypatch, name, mod, attr, mutant, pins):
+    monkeypatch.setattr(mod, attr, mutant)
+    if mod is numerics:          # ops imported the name directly
+        monkeypatch.setattr(ops, attr, mutant)
+    caught = [_fails(fn, *args) for fn, args in pins]
+    assert any(caught), f"no pin caught the planted mistake {name}"
+
+
+def test_padded_block_pin_catches_a_triangle_mistake(monkeypatch):
+    monkeypatch.setattr(ops, "triangle_mul", _mut_triangle_transposed)
+    from oracle import blocks
+    assert _fails(T_blk.test_pair_block_equals_masked_padded, [4, 6, 2], blocks.PAIR_ORDER_STACK)
