@@ -1,0 +1,177 @@
+#!/usr/bin/env python3
+"""Benchmark of the packed pair-state hot path on one MI355X.
+
+One step = one pass of the whole pair block over the batch: single
+projections, pair broadcast, LayerNorm+Linear, row attention with pair bias
+(projection, attention, output projection + residual), triangle update
+(projection + contraction), SwiGLU transition, and the column mean back to the
+single track.  Default workload: B=8 near-uniform lengths 208..224, C_s=384,
+C_z=128, 4 heads x 32, transition 128->512->128, bf16 with fp32 accumulation.
+
+Prints one JSON line (see the fields below).  --gpus N > 1 is rejected: the
+path runs on one GPU.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "valid pair positions/sec per pair block (1 MI355X) + % HBM / MFMA roofline"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 matrix cores, TFLOP/s
+F32_PEAK_TFLOPS = 157.3        # fp32 vector
+
+
+def op_costs(w, L):
+    """Algorithmic HBM bytes and flops per launch of every op of one block
+    (bf16 storage = 2 bytes; every tensor read or written once)."""
+    R = sum(n * n for n in L)
+    S = sum(L)
+    N3 = sum(n ** 3 for n in L)
+    C, Cs, H, d, F = w.c_z, w.c_s, w.heads, w.head_dim, w.hidden
+    e = 2 if w.dtype == "bf16" else 4
+    c = {
+        "single_proj": (S * (Cs + 2 * C) * e, 2 * S * Cs * 2 * C),
+        "pair_broadcast": (R * C * e + 2 * S * C * e, R * C),
+        "ln_linear": (R * 2 * C * e, 2 * R * C * C),
+        "attn_proj": (R * (C + 3 * C + H) * e, 2 * R * C * (3 * C + H)),
+        "attention_row": (R * (4 * H * d + H) * e, 4 * H * d * N3),
+        "attention_col": (R * (4 * H * d + H) * e, 4 * H * d * N3),
+        "attn_out_residual": (R * 3 * C * e, 2 * R * C * C),
+        "tri_proj": (R * 3 * C * e, 2 * R * C * 2 * C),
+        "triangle_out": (R * 4 * C * e, 2 * C * N3),
+        "triangle_in": (R * 4 * C * e, 2 * C * N3),
+        "transition": (R * 2 * C * e, 2 * R * (C * 2 * F + F * C)),
+        "segment_mean": (R * C * e + S * C * 4, R * C),
+        "single_update": (S * (C * 4 + 2 * Cs * e), 2 * S * C * Cs),
+    }
+    return c
+
+
+def roofline_for(name, bytes_, flops, us, dtype):
+    """Bound = whichever of HBM time and matrix-core time is longer."""
+    peak_f = BF16_PEAK_TFLOPS if dtype == "bf16" else F32_PEAK_TFLOPS
+    t_hbm = bytes_ / (HBM_PEAK_GBS * 1e9)
+    t_mma = flops / (peak_f * 1e12)
+    if t_mma > t_hbm:
+        ach = flops / (us * 1e-6) / 1e12
+        return {"kernel": name, "bound": "mfma", "achieved": round(ach, 2), "peak": peak_f, "unit": "TFLOP/s",
+                "frac": round(ach / peak_f, 4), "traffic": None}
+    ach = bytes_ / (us * 1e-6) / 1e9
+    return {"kernel": name, "bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None}
+
+
+def cpu_baseline(w, run, budget_s: float = 30.0):
+    """The CPU oracle timed on this host: one pass of the same pair block over
+    one sample of the workload (the smallest), pair positions per second."""
+    import numpy as np
+    from oracle import blocks as OB
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    i = int(np.argmin(run.lengths))
+    n = run.lengths[i]
+    eta = int(np.sum(run.lengths[:i]))
+    dims = dict(c_z=w.c_z, heads=w.heads, head_dim=w.head_dim)
+    s = run.s_init[eta:eta + n]
+    t0 = time.perf_counter()
+    z = None
+    for b in range(w.blocks):
+        steps = w.steps if b == 0 else tuple(t for t in w.steps if t != "lin")
+        s, z, _ = OB.pair_block(s, [n], run.params[b], dims, steps, z=z, dtype=w.dtype)
+    dt = time.perf_counter() - t0
+    return {"value": round(n * n * w.blocks / dt, 1), "unit": "pair positions/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"sample {i} of the batch (N={n}, {n * n} pair positions), one pass of the block "
+                      f"({w.blocks} block(s)) in float64 NumPy, {dt:.1f} s; host has {os.cpu_count()} CPUs"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="pair_b8_n208_224_bf16")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--kernels", action="store_true", help="also print the per-op breakdown to stderr")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this path runs on one GPU; --gpus {args.gpus} is not supported "
+              "(samples are independent, see the sharding notes in the design document)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_30379_amd import binding, blocks, synth
+    binding.load()
+    w = synth.WORKLOADS[args.workload]
+    if w.kind != "pair":
+        raise SystemExit("bench.py times the pair workloads")
+    torch.cuda.set_device(0)
+    run = blocks.PairRun(w)
+    L = run.lengths
+    R = sum(n * n for n in L)
+
+    for _ in range(args.warmup):
+        run.step()
+    torch.cuda.synchronize()
+
+    # timed region: per-op events on the launch stream, wall clock around it
+    tm = blocks.OpTimer()
+    blocks.timer = tm
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record()
+    for _ in range(args.steps):
+        run.step()
+    ev1.record()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    blocks.timer = None
+    ms = (t1 - t0) * 1e3 / args.steps
+    ms_dev = ev0.elapsed_time(ev1) / args.steps
+    per_op = tm.summary()                            # {op: (launches, mean us)}
+
+    costs = op_costs(w, L)
+    total_us = {k: n * us / args.steps for k, (n, us) in per_op.items()}
+    dominant = max(total_us, key=total_us.get)
+    n_launch, us_launch = per_op[dominant]
+    rl = roofline_for(dominant, costs[dominant][0], costs[dominant][1], us_launch, w.dtype)
+    rl["us_per_launch"] = round(us_launch, 2)
+    kernels = {}
+    for k, (n, us) in per_op.items():
+        r = roofline_for(k, costs[k][0], costs[k][1], us, w.dtype)
+        kernels[k] = {"us": round(us, 2), "launches_per_step": n // args.steps, "bound": r["bound"],
+                      "frac": r["frac"]}
+
+    out = {
+        "metric": METRIC, "value": round(w.blocks * R / (ms * 1e-3), 1), "unit": "pair positions/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "device_ms_per_step": round(ms_dev, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": w.name, "batch": w.batch, "lengths": L, "sum_n": sum(L), "sum_n2": R,
+                   "c_s": w.c_s, "c_z": w.c_z, "heads": w.heads, "head_dim": w.head_dim, "hidden": w.hidden,
+                   "blocks": w.blocks, "steps_per_block": list(w.steps)},
+        "roofline": rl,
+        "kernels": kernels,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, run)
+    if args.kernels:
+        for k, v in sorted(kernels.items(), key=lambda kv: -kv[1]["us"] * kv[1]["launches_per_step"]):
+            print(f"{k:20s} {v['us']:9.2f} us x{v['launches_per_step']}  {v['bound']} frac {v['frac']:.3f}",
+                  file=sys.stderr)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

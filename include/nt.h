@@ -1,0 +1,277 @@
+/*
+ * nt.h -- C ABI of the packed multi-ragged pair-state library for MI355X
+ * (gfx950).
+ *
+ * The library computes on packed values plus tensor-backed partitions, the
+ * representation of "DanLing NestedTensor: Composable Multi-Ragged Tensors for
+ * Deep Learning" (Sec. 3.1): a batch of B individually dense elements is
+ * stored as one value buffer whose leading axis concatenates every sample's
+ * ragged prefix, with sample offsets o (o_0 = 0, o_{i+1} - o_i = p_i,
+ * o_B = T; Appendix A) held on the host and mirrored on the device.
+ *
+ * Packed layouts used by the calls below (all row-major, elements not bytes):
+ *   singles      [sum_i N_i, C]        row eta_i + a         (eta = cu_seqlens)
+ *   square pairs [sum_i N_i^2, C]      row o_i + a N_i + b   (Eq. coordinate)
+ *   pair-padded channel-major operands of the triangle update: channel c of
+ *                cell (i,a,b) at c*ld + P_i + a n8_i + b, where n8_i = N_i
+ *                rounded up to a multiple of 8 and P_i = sum_{j<i} N_j n8_j
+ *                (every operand row starts 16-byte aligned; entries b >= N_i
+ *                are padding and never read as data); the transposed variant
+ *                stores cell (i,a,b) at c*ld + P_i + b n8_i + a
+ *   head-major pair bias: [H][sum_i N_i^2], head h of cell at h*ld + cell
+ * Row strides ("ld_*") are in elements and let callers address column slices
+ * of a wider buffer (e.g. u and v inside one [sum N, 2C] projection).
+ *
+ * Ownership: every value buffer is a device pointer owned by the caller; op
+ * calls never allocate, free or retain them.  An nt_layout and its device
+ * mirrors are owned by the library from nt_from_* until nt_layout_destroy;
+ * the caller must not destroy a layout while work that uses it is queued.
+ *
+ * Streams: every op enqueues asynchronously on the caller's HIP stream
+ * (NULL = the default stream) and returns without synchronising.  Only
+ * nt_from_* copies host->device (stream-ordered).
+ *
+ * Errors: every call returns an nt_status; nothing aborts or throws across the
+ * ABI.  All argument checks run on the host before any launch; on an error no
+ * work is enqueued and nt_last_error() (thread-local, valid until the next
+ * call on the same thread) describes it.  Device pointers must be 16-byte
+ * aligned and row strides multiples of 8 elements (bf16) or 4 (f32) unless a
+ * call says otherwise.
+ */
+#ifndef NT_H
+#define NT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct nt_layout nt_layout;          /* opaque, library-owned */
+
+typedef enum {
+  NT_OK = 0,
+  NT_ERR_INVALID_ARG = -1,     /* null pointer, bad size, misalignment, bad enum */
+  NT_ERR_LAYOUT_MISMATCH = -2, /* operands with different logical partitions   */
+  NT_ERR_OVERFLOW = -3,        /* a packed extent does not fit int32            */
+  NT_ERR_UNSUPPORTED = -4,     /* valid request outside the implemented shapes  */
+  NT_ERR_HIP = -5,             /* HIP runtime or launch failure                 */
+  NT_ERR_OOM = -6              /* device allocation of layout mirrors failed    */
+} nt_status;
+
+typedef enum { NT_F32 = 0, NT_BF16 = 1 } nt_dtype;
+
+typedef enum {
+  NT_EPI_NONE = 0,             /* y = LN(x) W^T + b                                  */
+  NT_EPI_RESIDUAL = 1,         /* y = residual + LN(x) W^T + b                       */
+  NT_EPI_SWIGLU_RESIDUAL = 2,  /* y = residual + (silu(g) * u) W2^T + b2,
+                                  [g|u] = LN(x) W^T + b (W stacks W_gate; W_up)       */
+  NT_EPI_GELU = 3              /* y = gelu(LN(x) W^T + b), exact erf form            */
+} nt_epilogue;
+
+typedef enum { NT_LEVEL_SINGLES = 0, NT_LEVEL_PAIRS = 1 } nt_level;
+
+/* Layout of the columns that nt_layernorm_linear routes to y_tail. */
+typedef enum {
+  NT_TAIL_CHANNEL_MAJOR = 0,   /* column j of row r at j*ld_tail + r               */
+  NT_TAIL_PAIR_PADDED = 1,     /* pair-padded channel-major (needs a pair layout)  */
+  NT_TAIL_PAIR_PADDED_T = 2    /* transposed pair-padded channel-major             */
+} nt_tail_layout;
+
+enum { NT_LAYOUT_HOST_ONLY = 1u };           /* nt_from_*: no device mirrors */
+
+/* Host arrays a layout exposes through nt_layout_host_array(). */
+typedef enum {
+  NT_ARR_LENGTHS = 0,          /* N_i, [B]                                      */
+  NT_ARR_CU_SEQLENS = 1,       /* single offsets eta, [B+1]                     */
+  NT_ARR_CU_PAIRS = 2,         /* square-pair offsets o, [B+1]                  */
+  NT_ARR_ROW_SPLITS2 = 3,      /* level-2 pair row splits, [1 + sum N_i]        */
+  NT_ARR_ROW_SAMPLE = 4,       /* sample id of every single row, [sum N_i]      */
+  NT_ARR_ATTN_WORK = 5,        /* pair-row work map (sample, row) pairs, XCD-ordered */
+  NT_ARR_TRI_WORK = 6,         /* triangle tile map (sample, x-tile, y-tile, 0) quads */
+  NT_ARR_SEQ_WORK = 7,         /* 1-D attention map (sample, query block) pairs */
+  NT_ARR_CU_PAD = 8            /* P_i offsets of pair-padded operands, [B+1]    */
+} nt_array;
+
+typedef struct {
+  int32_t batch;               /* B                                             */
+  int32_t max_len;             /* max_i N_i                                     */
+  int64_t sum_n;               /* sum_i N_i    (rows of a single tensor)         */
+  int64_t sum_n2;              /* sum_i N_i^2  (rows of a square pair tensor)    */
+  int64_t sum_n3;              /* sum_i N_i^3  (work of the pair contractions)   */
+  int64_t sum_pad;             /* sum_i N_i n8_i (channel stride of pair-padded operands) */
+  const int32_t* d_cu_seqlens; /* device mirrors (NULL for host-only layouts)   */
+  const int32_t* d_cu_pairs;
+  const int32_t* d_row_splits2;
+} nt_layout_info_t;
+
+/* ---------------------------------------------------------------- layouts
+ * Partitions of a batch of square pair states, built from the per-sample
+ * lengths N_i (Sec. 3.1 "Structural metadata"; Fig. "representation"):
+ * single offsets eta (cu_seqlens), pair offsets o with p_i = N_i^2, the
+ * level-2 row splits o_i + a N_i (1 + sum N_i entries), and the tile-to-sample
+ * work maps the kernels launch from, so that no wavefront crosses a sample
+ * boundary.  Zero-length samples are allowed (Appendix A: zero-volume
+ * elements have coincident offsets).
+ *   lengths   host, [batch], each >= 0.            batch >= 1.
+ *   flags     0, or NT_LAYOUT_HOST_ONLY to build host arrays only (no device
+ *             memory is touched; op calls then reject the layout).
+ *   stream    HIP stream for the host->device copies of the mirrors.
+ *   out       receives the new layout.
+ * Errors: NT_ERR_INVALID_ARG (null, batch < 1, negative length),
+ *         NT_ERR_OVERFLOW (sum N_i^2 or sum N_i does not fit int32),
+ *         NT_ERR_OOM / NT_ERR_HIP (device mirrors).                          */
+nt_status nt_from_lengths(const int32_t* lengths, int32_t batch, uint32_t flags,
+                          void* stream, nt_layout** out);
+
+/* Same from single offsets (cu_seqlens, host, [batch+1]); they must satisfy
+ * o_0 = 0 and be non-decreasing (Appendix A, "Structural invariants"),
+ * otherwise NT_ERR_INVALID_ARG.                                              */
+nt_status nt_from_offsets(const int32_t* cu_seqlens, int32_t batch, uint32_t flags,
+                          void* stream, nt_layout** out);
+
+/* Frees the layout and its device mirrors (NULL is accepted).  Waits for the
+ * device to finish using the mirrors (hipFree semantics).                    */
+nt_status nt_layout_destroy(nt_layout* layout);
+
+nt_status nt_layout_info(const nt_layout* layout, nt_layout_info_t* info);
+
+/* Host copy of one metadata array (pointer valid for the layout's lifetime);
+ * *count receives the number of int32 entries.                              */
+nt_status nt_layout_host_array(const nt_layout* layout, nt_array which,
+                               const int32_t** data, int64_t* count);
+
+/* 1 if the two layouts describe the same logical partition (equal length
+ * vectors), else 0.  Equal packed totals are not enough: (2,6) and (3,4)
+ * pairs both hold twelve rows but are incompatible (Sec. 3.2).              */
+int32_t nt_layouts_compatible(const nt_layout* a, const nt_layout* b);
+
+/* ---------------------------------------------------------------- broadcast
+ * Pair construction by broadcasting (Eq. running-block, first line; Sec. 3.2
+ * "Creating axes through broadcasting"): for every sample i and a, b < N_i
+ *     z[o_i + a N_i + b, c] (+)= u[eta_i + a, c] + v[eta_i + b, c]
+ * computed in fp32 and rounded once to the storage dtype.
+ *   C          channels (> 0).
+ *   u, v       singles [sum N, C] with row strides ld_u, ld_v (may alias).
+ *   z          pairs [sum N^2, C] with row stride ld_z (must not alias u/v).
+ *   accumulate 0: z is overwritten; 1: z is read and the sum added to it.
+ *   dtype      NT_F32 or NT_BF16 for u, v and z.
+ * Errors: NT_ERR_INVALID_ARG.                                                */
+nt_status nt_pair_broadcast(const nt_layout* layout, int32_t C,
+                            const void* u, int64_t ld_u, const void* v, int64_t ld_v,
+                            void* z, int64_t ld_z, int32_t accumulate,
+                            nt_dtype dtype, void* stream);
+
+/* ---------------------------------------------------------------- LN + Linear
+ * Feature transform on packed rows (Sec. 3.3: V' = V W^T + b, normalisation on
+ * each row's feature tail; rows are independent, so one launch covers every
+ * sample):  y = epilogue(LN(x; gamma, beta, eps) W^T + b).
+ * LayerNorm uses the biased variance with statistics in fp32.  bf16 runs on
+ * matrix cores (bf16 operands, fp32 accumulation); f32 runs in fp32 FMA.      */
+typedef struct {
+  int64_t rows;                /* R >= 0                                         */
+  int32_t c_in;                /* K (multiple of 8)                               */
+  int32_t c_out;               /* N: output width (for SwiGLU: the residual width) */
+  nt_dtype dtype;              /* dtype of W, W2, residual and y                  */
+  const void* x;               /* [R, K] row stride ldx                           */
+  int64_t ldx;
+  nt_dtype x_dtype;            /* x may be f32 when dtype is bf16 (e.g. a reduce output) */
+  const float* ln_gamma;       /* [K] or NULL (no LayerNorm); ln_beta NULL = 0    */
+  const float* ln_beta;
+  float ln_eps;
+  const void* w;               /* [N_w, K] row-major; N_w = N, or 2F for SwiGLU    */
+  const float* bias;           /* [N_w] or NULL                                   */
+  nt_epilogue epilogue;
+  int32_t hidden;              /* F for SwiGLU (multiple of 32), else 0           */
+  const void* w2;              /* SwiGLU down projection [N, F], else NULL        */
+  const float* bias2;          /* [N] or NULL                                     */
+  const void* residual;        /* [R, N - n_tail] row stride ld_residual (added to the
+                                  main columns only); NULL = x for SwiGLU          */
+  int64_t ld_residual;
+  void* y;                     /* [R, N - n_tail] row stride ldy (may alias residual) */
+  int64_t ldy;
+  int32_t n_tail;              /* last n_tail output columns go to y_tail instead */
+  void* y_tail;                /* [n_tail][ld_tail], arranged as tail_layout says  */
+  int64_t ld_tail;
+  nt_tail_layout tail_layout;
+  const nt_layout* layout;     /* optional: rows must equal the layout's row count */
+  nt_level level;              /*   at this level                               */
+  const nt_layout* residual_layout;  /* optional: must be compatible with layout */
+} nt_linear_args;
+
+/* Errors: NT_ERR_INVALID_ARG, NT_ERR_LAYOUT_MISMATCH (residual_layout differs
+ * from layout, or rows differ from the layout's count), NT_ERR_UNSUPPORTED
+ * (bf16 SwiGLU unless x is bf16, K == N in {64, 128, 256} and F % 32 == 0;
+ * f32 SwiGLU with K > 1024 or F > 4096; n_tail with SwiGLU; a pair-padded
+ * tail without a pair layout).  ln_gamma/ln_beta must be 16-byte aligned.    */
+nt_status nt_layernorm_linear(const nt_linear_args* args, void* stream);
+
+/* ---------------------------------------------------------------- attention
+ * Segmented softmax attention, one launch over the whole batch.
+ *   axis 0  row attention with pair bias around the starting node: for sample
+ *           i, pair row r, query j, head h
+ *             o[cell(r,j),h] = sum_k softmax_k(scale q[cell(r,j),h].k[cell(r,k),h]
+ *                                              + bias[h][cell(j,k)]) v[cell(r,k),h]
+ *   axis 1  the same around the ending node: axis 0 applied to each sample's
+ *           transpose (q, k, v and the bias read at cell(b,a) for (a,b)).
+ *   axis 2  1-D variable-length self-attention over the tokens of each sample
+ *           (Sec. 3.3 "Attention through packed blocks"); bias must be NULL.
+ * cell(a,b) = o_i + a N_i + b.  Pair attention follows the Pairformer's
+ * triangle attention cited in Sec. 4.3 (reading: no gating, no mask).
+ *   heads, head_dim  H and d; d in {8 (f32 only), 32, 64}; H*d <= ld_qkv.
+ *   q, k, v  [rows, H*d] with common row stride ld_qkv (may be slices of one
+ *            buffer); rows = sum N^2 (axes 0/1) or sum N (axis 2).
+ *   bias     head-major [H][ld_bias] or NULL (axes 0/1).
+ *   scale    softmax scale (e.g. 1/sqrt(d)).
+ *   o        [rows, H*d] row stride ld_o.
+ * Errors: NT_ERR_INVALID_ARG, NT_ERR_UNSUPPORTED (d, or N_i beyond the
+ * on-chip limit: 1024 for d=32, 512 for d=64).                               */
+nt_status nt_pair_row_attention(const nt_layout* layout, int32_t axis,
+                                int32_t heads, int32_t head_dim,
+                                const void* q, const void* k, const void* v, int64_t ld_qkv,
+                                const void* bias, int64_t ld_bias, float scale,
+                                void* o, int64_t ld_o, nt_dtype dtype, void* stream);
+
+/* ---------------------------------------------------------------- triangle
+ * Triangle multiplicative update, channelwise (Sec. 4.3, after the AlphaFold 3
+ * Pairformer; reading: no gates, no output projection), accumulated into z:
+ *   direction 0 (outgoing)  z[cell(x,y),c] += sum_k a_c[x,k] b_c[y,k]
+ *   direction 1 (incoming)  z[cell(x,y),c] += sum_k a_c[k,x] b_c[k,y]
+ * a, b are pair-padded channel-major with channel stride ld_ab (>= sum_pad):
+ * for direction 0 in the plain variant (a_c[x,k] at c*ld_ab + P_i + x n8_i + k),
+ * for direction 1 in the transposed variant (a_c[k,x] at c*ld_ab + P_i + x n8_i + k),
+ * which is what nt_layernorm_linear writes with NT_TAIL_PAIR_PADDED(_T); the
+ * incoming update is then the outgoing contraction of the transposes.  z is the
+ * channel-last pair state [sum N^2, C] with row stride ld_z.  One ragged grouped
+ * GEMM over all samples and channels; fp32 accumulation, z rounded once.
+ * Errors: NT_ERR_INVALID_ARG (C not a multiple of 32 for bf16).              */
+nt_status nt_triangle_mul(const nt_layout* layout, int32_t direction, int32_t C,
+                          const void* a, const void* b, int64_t ld_ab,
+                          void* z, int64_t ld_z, nt_dtype dtype, void* stream);
+
+/* ---------------------------------------------------------------- reduce
+ * Reductions that consume a ragged axis, with fp32 accumulation and fp32
+ * output, one launch, no atomics:
+ *   level NT_LEVEL_PAIRS   (pair columns, Eq. pair-reduction)
+ *       y[eta_i + a, c] = sum_b x[o_i + a N_i + b, c]     (op 1: / N_i)
+ *   level NT_LEVEL_SINGLES (complete reduction within each element, Appendix A)
+ *       y[i, c] = sum_t x[eta_i + t, c]                    (op 1: / N_i;
+ *       an empty sample gives 0 for the sum and NaN for the mean)
+ *   op       0 sum, 1 mean.
+ *   x        [rows, C] row stride ld_x, dtype x_dtype.   y: fp32, row stride ld_y.
+ * Errors: NT_ERR_INVALID_ARG.                                                */
+nt_status nt_segment_reduce(const nt_layout* layout, nt_level level, int32_t op, int32_t C,
+                            const void* x, int64_t ld_x, nt_dtype x_dtype,
+                            float* y, int64_t ld_y, void* stream);
+
+/* Thread-local description of the last error on this thread. */
+const char* nt_last_error(void);
+
+/* Library version string. */
+const char* nt_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NT_H */

@@ -1,8 +1,10 @@
 """Block compositions of the oracle, with the storage rounding points of the
-GPU path: every tensor that one GPU kernel writes and another reads is rounded
-to the storage dtype here at the same point; all arithmetic inside a step is
-float64.  The final outputs are returned unrounded except where the step
-itself stores them.
+bf16 execution: the paper measures with BF16 parameters and inputs (Sec. 4.1
+"Measurement"), so every tensor a step produces is a bf16 value -- the
+normalised features entering a projection, the gated SwiGLU hidden, every
+projection output and every pair/single state.  Those points are rounded here
+(numerics.store); all arithmetic between them is float64.  For the fp32
+workloads nothing is rounded.
 
 TEST INFRASTRUCTURE ONLY (see the package docstring).
 """
@@ -11,7 +13,21 @@ from __future__ import annotations
 import numpy as np
 
 from . import ops
-from .numerics import store
+from .numerics import gelu, layernorm, linear, silu, store
+
+
+def _ln_linear(x, w, b, ln, st):
+    """LN(x) stored in the working precision, then V W^T + b (Sec. 3.3)."""
+    return linear(st(layernorm(x, *ln)), w, b)
+
+
+def _swiglu(x, p, st):
+    """x + SwiGLU(LN(x)) with bf16 storage of LN(x) and of the gated hidden
+    (Eq. running-block, second line)."""
+    gu = _ln_linear(x, p["trans.w"], p["trans.b"], (p["trans.ln_g"], p["trans.ln_b"]), st)
+    F = gu.shape[1] // 2
+    h = st(silu(gu[:, :F]) * gu[:, F:])
+    return x + linear(h, p["trans.w2"], p["trans.b2"])
 
 
 PAIR_ORDER_BLOCK = ("bcast", "lin", "att_row", "tri_out", "trans", "single")
@@ -41,38 +57,31 @@ def pair_block(s, lengths, p, dims, order, z=None, dtype="bf16"):
     s = np.asarray(s, np.float64)
     for step in order:
         if step == "bcast":
-            uv = st(ops.layernorm_linear(s, p["uv.w"], p["uv.b"]))
+            uv = st(linear(s, p["uv.w"], p["uv.b"]))
             trace["uv"] = uv
             z = st(ops.pair_broadcast(uv[:, :C], uv[:, C:], lengths, z_in=z))
         elif step == "lin":
-            z = st(ops.layernorm_linear(z, p["lin.w"], p["lin.b"], ln=(p["lin.ln_g"], p["lin.ln_b"])))
+            z = st(_ln_linear(z, p["lin.w"], p["lin.b"], (p["lin.ln_g"], p["lin.ln_b"]), st))
         elif step in ("att_row", "att_col"):
             key = step
-            proj = ops.layernorm_linear(z, p[key + ".w"], p[key + ".b"],
-                                        ln=(p[key + ".ln_g"], p[key + ".ln_b"]))
+            proj = _ln_linear(z, p[key + ".w"], p[key + ".b"], (p[key + ".ln_g"], p[key + ".ln_b"]), st)
             q, k, v = st(proj[:, :C]), st(proj[:, C:2 * C]), st(proj[:, 2 * C:3 * C])
             beta = st(proj[:, 3 * C:3 * C + H])
             o = st(ops.pair_row_attention(q, k, v, beta, lengths, H, d,
                                           axis=0 if step == "att_row" else 1))
             trace[step + ".o"] = o
-            z = st(ops.layernorm_linear(o, p[key + ".wo"], p[key + ".bo"],
-                                        epilogue="residual", residual=z))
+            z = st(z + linear(o, p[key + ".wo"], p[key + ".bo"]))
         elif step in ("tri_out", "tri_in"):
-            ab = st(ops.layernorm_linear(z, p[step + ".w"], p[step + ".b"],
-                                         ln=(p[step + ".ln_g"], p[step + ".ln_b"])))
+            ab = st(_ln_linear(z, p[step + ".w"], p[step + ".b"], (p[step + ".ln_g"], p[step + ".ln_b"]), st))
             t = ops.triangle_mul(ab[:, :C], ab[:, C:], lengths,
                                  "outgoing" if step == "tri_out" else "incoming")
             z = st(z + t)
         elif step == "trans":
-            z = st(ops.layernorm_linear(z, p["trans.w"], p["trans.b"],
-                                        ln=(p["trans.ln_g"], p["trans.ln_b"]),
-                                        epilogue="swiglu_residual",
-                                        w2=p["trans.w2"], b2=p["trans.b2"]))
+            z = st(_swiglu(z, p, st))
         elif step == "single":
-            m = ops.segment_reduce(z, lengths, "pair_cols", "mean")   # stored fp32
+            m = ops.segment_reduce(z, lengths, "pair_cols", "mean")
             trace["col_mean"] = m
-            s = st(ops.layernorm_linear(m, p["single.w"], p["single.b"],
-                                        epilogue="residual", residual=s))
+            s = st(s + linear(st(m), p["single.w"], p["single.b"]))
         else:
             raise ValueError(f"unknown step {step!r}")
         trace[step] = z
@@ -87,10 +96,10 @@ def encoder_layer(x, lengths, p, heads, head_dim, dtype="bf16"):
     st = lambda t: store(t, dtype)          # noqa: E731
     c = heads * head_dim
     x = np.asarray(x, np.float64)
-    qkv = st(ops.layernorm_linear(x, p["qkv.w"], p["qkv.b"], ln=(p["ln1_g"], p["ln1_b"])))
+    qkv = st(_ln_linear(x, p["qkv.w"], p["qkv.b"], (p["ln1_g"], p["ln1_b"]), st))
     o = st(ops.attention_1d(qkv[:, :c], qkv[:, c:2 * c], qkv[:, 2 * c:], lengths, heads, head_dim))
-    x = st(ops.layernorm_linear(o, p["o.w"], p["o.b"], epilogue="residual", residual=x))
-    h = st(ops.layernorm_linear(x, p["ffn1.w"], p["ffn1.b"], ln=(p["ln2_g"], p["ln2_b"]), epilogue="gelu"))
-    x = st(ops.layernorm_linear(h, p["ffn2.w"], p["ffn2.b"], epilogue="residual", residual=x))
+    x = st(x + linear(o, p["o.w"], p["o.b"]))
+    h = st(gelu(_ln_linear(x, p["ffn1.w"], p["ffn1.b"], (p["ln2_g"], p["ln2_b"]), st)))
+    x = st(x + linear(h, p["ffn2.w"], p["ffn2.b"]))
     pooled = ops.segment_reduce(x, lengths, "samples", "mean")
     return x, pooled, {"qkv": qkv, "o": o, "h": h}

@@ -1,0 +1,228 @@
+"""Thin ctypes binding of libnt.so (include/nt.h).
+
+Argument marshalling only: every computation runs in the HIP kernels behind
+the C ABI.  torch supplies device memory and the current HIP stream.  The
+library must have been built (paper_2609_30379_amd.build); nothing here falls
+back to any other implementation.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libnt.so")
+
+NT_OK, NT_ERR_INVALID_ARG, NT_ERR_LAYOUT_MISMATCH, NT_ERR_OVERFLOW, NT_ERR_UNSUPPORTED, NT_ERR_HIP, NT_ERR_OOM = \
+    0, -1, -2, -3, -4, -5, -6
+NT_F32, NT_BF16 = 0, 1
+EPILOGUES = {"none": 0, "residual": 1, "swiglu_residual": 2, "gelu": 3}
+LEVELS = {"singles": 0, "pairs": 1}
+TAILS = {"channel_major": 0, "pair_padded": 1, "pair_padded_t": 2}
+ARRAYS = {"lengths": 0, "cu_seqlens": 1, "cu_pairs": 2, "row_splits2": 3, "row_sample": 4,
+          "attn_work": 5, "tri_work": 6, "seq_work": 7, "cu_pad": 8}
+NT_LAYOUT_HOST_ONLY = 1
+
+
+class NtError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"nt status {status}: {msg}")
+        self.status = status
+
+
+class LayoutInfo(C.Structure):
+    _fields_ = [("batch", C.c_int32), ("max_len", C.c_int32), ("sum_n", C.c_int64), ("sum_n2", C.c_int64),
+                ("sum_n3", C.c_int64), ("sum_pad", C.c_int64), ("d_cu_seqlens", C.c_void_p),
+                ("d_cu_pairs", C.c_void_p), ("d_row_splits2", C.c_void_p)]
+
+
+class LinearArgs(C.Structure):
+    _fields_ = [("rows", C.c_int64), ("c_in", C.c_int32), ("c_out", C.c_int32), ("dtype", C.c_int),
+                ("x", C.c_void_p), ("ldx", C.c_int64), ("x_dtype", C.c_int),
+                ("ln_gamma", C.c_void_p), ("ln_beta", C.c_void_p), ("ln_eps", C.c_float),
+                ("w", C.c_void_p), ("bias", C.c_void_p), ("epilogue", C.c_int),
+                ("hidden", C.c_int32), ("w2", C.c_void_p), ("bias2", C.c_void_p),
+                ("residual", C.c_void_p), ("ld_residual", C.c_int64),
+                ("y", C.c_void_p), ("ldy", C.c_int64),
+                ("n_tail", C.c_int32), ("y_tail", C.c_void_p), ("ld_tail", C.c_int64), ("tail_layout", C.c_int),
+                ("layout", C.c_void_p), ("level", C.c_int), ("residual_layout", C.c_void_p)]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Loads libnt.so once; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build it with `python -m paper_2609_30379_amd.build`")
+    lib = C.CDLL(path)
+    vp, i32, i64, f32 = C.c_void_p, C.c_int32, C.c_int64, C.c_float
+    sig = {
+        "nt_from_lengths": [vp, i32, C.c_uint32, vp, C.POINTER(vp)],
+        "nt_from_offsets": [vp, i32, C.c_uint32, vp, C.POINTER(vp)],
+        "nt_layout_destroy": [vp],
+        "nt_layout_info": [vp, C.POINTER(LayoutInfo)],
+        "nt_layout_host_array": [vp, C.c_int, C.POINTER(C.POINTER(i32)), C.POINTER(i64)],
+        "nt_layouts_compatible": [vp, vp],
+        "nt_pair_broadcast": [vp, i32, vp, i64, vp, i64, vp, i64, i32, C.c_int, vp],
+        "nt_layernorm_linear": [C.POINTER(LinearArgs), vp],
+        "nt_pair_row_attention": [vp, i32, i32, i32, vp, vp, vp, i64, vp, i64, f32, vp, i64, C.c_int, vp],
+        "nt_triangle_mul": [vp, i32, i32, vp, vp, i64, vp, i64, C.c_int, vp],
+        "nt_segment_reduce": [vp, C.c_int, i32, i32, vp, i64, C.c_int, vp, i64, vp],
+        "nt_last_error": [],
+        "nt_version": [],
+    }
+    for name, args in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = C.c_char_p if name in ("nt_last_error", "nt_version") else C.c_int
+    _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status != NT_OK:
+        raise NtError(status, load().nt_last_error().decode())
+
+
+def _stream():
+    import torch
+    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dtype(t) -> int:
+    import torch
+    if t.dtype == torch.bfloat16:
+        return NT_BF16
+    if t.dtype == torch.float32:
+        return NT_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _mat(t, name):
+    """(device pointer, row stride in elements) of a 2-D device tensor with unit column stride."""
+    if t is None:
+        return None, 0
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dim() != 2 or (t.size(1) > 1 and t.stride(1) != 1):
+        raise ValueError(f"{name} must be 2-D with contiguous rows")
+    return C.c_void_p(t.data_ptr()), int(t.stride(0)) if t.size(0) > 1 else int(t.size(1))
+
+
+def _ptr(t):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+class NestedLayout:
+    """Partitions of a batch of square pair states (nt_from_lengths)."""
+
+    def __init__(self, lengths, host_only: bool = False, offsets: bool = False):
+        lib = load()
+        arr = np.ascontiguousarray(np.asarray(lengths, dtype=np.int32))
+        self._arr = arr
+        handle = C.c_void_p()
+        flags = NT_LAYOUT_HOST_ONLY if host_only else 0
+        stream = None if host_only else _stream()
+        batch = len(arr) - 1 if offsets else len(arr)
+        fn = lib.nt_from_offsets if offsets else lib.nt_from_lengths
+        _check(fn(arr.ctypes.data_as(C.c_void_p), batch, flags, stream, C.byref(handle)))
+        self.handle = handle
+        info = LayoutInfo()
+        _check(lib.nt_layout_info(handle, C.byref(info)))
+        self.batch, self.max_len = info.batch, info.max_len
+        self.sum_n, self.sum_n2, self.sum_n3, self.sum_pad = info.sum_n, info.sum_n2, info.sum_n3, info.sum_pad
+
+    def host_array(self, name: str) -> np.ndarray:
+        ptr, count = C.POINTER(C.c_int32)(), C.c_int64()
+        _check(load().nt_layout_host_array(self.handle, ARRAYS[name], C.byref(ptr), C.byref(count)))
+        return np.ctypeslib.as_array(ptr, shape=(count.value,)).copy() if count.value else np.zeros(0, np.int32)
+
+    def compatible(self, other: "NestedLayout") -> bool:
+        return bool(load().nt_layouts_compatible(self.handle, other.handle))
+
+    def close(self):
+        if getattr(self, "handle", None) is not None and self.handle.value:
+            _check(load().nt_layout_destroy(self.handle))
+            self.handle = C.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def nt_pair_broadcast(layout: NestedLayout, u, v, z, accumulate: bool = False):
+    pu, ldu = _mat(u, "u")
+    pv, ldv = _mat(v, "v")
+    pz, ldz = _mat(z, "z")
+    _check(load().nt_pair_broadcast(layout.handle, int(z.size(1)), pu, ldu, pv, ldv, pz, ldz,
+                                    int(accumulate), _dtype(z), _stream()))
+    return z
+
+
+def nt_layernorm_linear(x, w, bias, y, ln=None, eps: float = 1e-5, epilogue: str = "none", w2=None, bias2=None,
+                        hidden: int = 0, residual=None, n_tail: int = 0, y_tail=None,
+                        tail_layout: str = "channel_major", layout: NestedLayout | None = None,
+                        level: str = "pairs", residual_layout: NestedLayout | None = None, c_out: int | None = None):
+    a = LinearArgs()
+    px, ldx = _mat(x, "x")
+    a.rows, a.c_in = int(x.size(0)), int(x.size(1))
+    a.c_out = int(c_out if c_out is not None else (w2.size(0) if epilogue == "swiglu_residual" else w.size(0)))
+    a.dtype, a.x, a.ldx, a.x_dtype = _dtype(w), px, ldx, _dtype(x)
+    if ln is not None:
+        a.ln_gamma, a.ln_beta = _ptr(ln[0]), _ptr(ln[1])
+    a.ln_eps = eps
+    a.w, a.bias, a.epilogue = _ptr(w), _ptr(bias), EPILOGUES[epilogue]
+    a.hidden, a.w2, a.bias2 = int(hidden), _ptr(w2), _ptr(bias2)
+    a.residual, a.ld_residual = _mat(residual, "residual")
+    a.y, a.ldy = _mat(y, "y")
+    a.n_tail = int(n_tail)
+    a.y_tail, a.ld_tail = (_ptr(y_tail), int(y_tail.stride(0))) if y_tail is not None else (None, 0)
+    a.tail_layout = TAILS[tail_layout]
+    a.layout = layout.handle if layout is not None else None
+    a.level = LEVELS[level]
+    a.residual_layout = residual_layout.handle if residual_layout is not None else None
+    _check(load().nt_layernorm_linear(C.byref(a), _stream()))
+    return y
+
+
+def nt_pair_row_attention(layout: NestedLayout, axis: int, heads: int, head_dim: int, q, k, v, o,
+                          bias=None, scale: float | None = None):
+    pq, ld = _mat(q, "q")
+    pk, ldk = _mat(k, "k")
+    pv, ldv = _mat(v, "v")
+    if not (ld == ldk == ldv):
+        raise ValueError("q, k and v must share one row stride")
+    po, ldo = _mat(o, "o")
+    pb, ldb = (_ptr(bias), int(bias.stride(0))) if bias is not None else (None, 0)
+    scale = 1.0 / float(np.sqrt(head_dim)) if scale is None else float(scale)
+    _check(load().nt_pair_row_attention(layout.handle, int(axis), int(heads), int(head_dim), pq, pk, pv, ld,
+                                        pb, ldb, scale, po, ldo, _dtype(q), _stream()))
+    return o
+
+
+def nt_triangle_mul(layout: NestedLayout, direction: int, a, b, z):
+    """a, b: pair-padded channel-major operands [C, >= sum_pad] (rows = channels)."""
+    pz, ldz = _mat(z, "z")
+    _check(load().nt_triangle_mul(layout.handle, int(direction), int(z.size(1)), _ptr(a), _ptr(b),
+                                  int(a.stride(0)), pz, ldz, _dtype(z), _stream()))
+    return z
+
+
+def nt_segment_reduce(layout: NestedLayout, level: str, op: str, x, y):
+    px, ldx = _mat(x, "x")
+    py, ldy = _mat(y, "y")
+    _check(load().nt_segment_reduce(layout.handle, LEVELS[level], {"sum": 0, "mean": 1}[op], int(x.size(1)),
+                                    px, ldx, _dtype(x), py, ldy, _stream()))
+    return y
+
+
+def version() -> str:
+    return load().nt_version().decode()

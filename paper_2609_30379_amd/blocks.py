@@ -1,0 +1,243 @@
+"""Block compositions on the GPU path: every step is one call into libnt.so.
+
+pair block      the single-pair-single block of Eq. running-block, extended with
+                the Pairformer-style steps of Sec. 4.3 (row/column attention
+                with pair bias, outgoing/incoming triangle update, SwiGLU
+                transition), over a packed [sum N_i^2, C] pair state.
+encoder layer   a pre-LayerNorm encoder layer on packed [sum N_i, C] tokens
+                with segmented attention and a per-sample mean pool.
+
+Workspaces are allocated once per (layout, dims); a step allocates nothing.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import torch
+
+from . import binding as B
+
+ORDER_BLOCK = ("bcast", "lin", "att_row", "tri_out", "trans", "single")
+ORDER_STACK = ("bcast", "tri_out", "tri_in", "att_row", "att_col", "trans", "single")
+
+
+def _round8(n: int) -> int:
+    return (int(n) + 7) // 8 * 8
+
+
+class OpTimer:
+    """Records a pair of events on the current stream around every op of a
+    block, to attribute device time per op (used by the benchmark)."""
+
+    def __init__(self):
+        self.events = []          # (name, start, end)
+
+    def __call__(self, name):
+        return _OpSpan(self, name)
+
+    def summary(self):
+        """{op: (launches, mean microseconds)} after a device synchronisation."""
+        torch.cuda.synchronize()
+        acc = {}
+        for name, a, b in self.events:
+            n, t = acc.get(name, (0, 0.0))
+            acc[name] = (n + 1, t + a.elapsed_time(b) * 1e3)
+        return {k: (n, t / n) for k, (n, t) in acc.items()}
+
+
+class _OpSpan:
+    def __init__(self, timer, name):
+        self.timer, self.name = timer, name
+
+    def __enter__(self):
+        self.a = torch.cuda.Event(enable_timing=True)
+        self.b = torch.cuda.Event(enable_timing=True)
+        self.a.record()
+
+    def __exit__(self, *exc):
+        self.b.record()
+        self.timer.events.append((self.name, self.a, self.b))
+
+
+class _NoSpan:
+    def __enter__(self):
+        return None
+
+    def __exit__(self, *exc):
+        return False
+
+
+_NOSPAN = _NoSpan()
+timer = None                      # set to an OpTimer to record per-op events
+
+
+def _op(name):
+    return timer(name) if timer is not None else _NOSPAN
+
+
+def to_device(params: dict, dtype: str, device="cuda") -> dict:
+    """Weights as device tensors: matrices in the storage dtype, vectors in fp32."""
+    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    out = {}
+    for k, v in params.items():
+        t = torch.from_numpy(np.ascontiguousarray(v))
+        out[k] = t.to(device=device, dtype=td if t.dim() == 2 else torch.float32).contiguous()
+    return out
+
+
+class PairWorkspace:
+    """Device buffers of one pair block for a given layout and widths."""
+
+    def __init__(self, layout: B.NestedLayout, c_s: int, c_z: int, heads: int, dtype: str, device="cuda"):
+        td = torch.bfloat16 if dtype == "bf16" else torch.float32
+        R, S = layout.sum_n2, layout.sum_n
+        self.td = td
+        self.uv = torch.empty((S, 2 * c_z), dtype=td, device=device)
+        self.z = [torch.empty((R, c_z), dtype=td, device=device) for _ in range(2)]
+        self.qkv = torch.empty((R, 3 * c_z), dtype=td, device=device)
+        self.bias = torch.empty((heads, max(_round8(R), 8)), dtype=td, device=device)
+        self.o = torch.empty((R, c_z), dtype=td, device=device)
+        self.ab = torch.empty((2 * c_z, max(_round8(layout.sum_pad), 8)), dtype=td, device=device)
+        self.m = torch.empty((S, c_z), dtype=torch.float32, device=device)
+        self.cur = 0
+
+
+def pair_block(layout: B.NestedLayout, s, W: dict, dims: dict, order, ws: PairWorkspace, z=None):
+    """Runs one pair block.  s ([sum N, C_s]) is updated in place by the
+    "single" step; returns the pair state tensor (a workspace buffer, or z)."""
+    C, H, d = dims["c_z"], dims["heads"], dims["head_dim"]
+    for step in order:
+        if step == "bcast":
+            with _op("single_proj"):
+                B.nt_layernorm_linear(s, W["uv.w"], W["uv.b"], ws.uv, layout=layout, level="singles")
+            acc = z is not None
+            z = ws.z[ws.cur] if z is None else z
+            with _op("pair_broadcast"):
+                B.nt_pair_broadcast(layout, ws.uv[:, :C], ws.uv[:, C:], z, accumulate=acc)
+        elif step == "lin":
+            out = ws.z[1 - ws.cur] if z is ws.z[ws.cur] else ws.z[ws.cur]
+            with _op("ln_linear"):
+                B.nt_layernorm_linear(z, W["lin.w"], W["lin.b"], out, ln=(W["lin.ln_g"], W["lin.ln_b"]),
+                                      layout=layout, level="pairs")
+            if out is ws.z[1 - ws.cur]:
+                ws.cur = 1 - ws.cur
+            z = out
+        elif step in ("att_row", "att_col"):
+            with _op("attn_proj"):
+                B.nt_layernorm_linear(z, W[step + ".w"], W[step + ".b"], ws.qkv,
+                                      ln=(W[step + ".ln_g"], W[step + ".ln_b"]), n_tail=H, y_tail=ws.bias,
+                                      tail_layout="channel_major", layout=layout, level="pairs")
+            with _op("attention_" + step[4:]):
+                B.nt_pair_row_attention(layout, 0 if step == "att_row" else 1, H, d, ws.qkv[:, :C],
+                                        ws.qkv[:, C:2 * C], ws.qkv[:, 2 * C:], ws.o, bias=ws.bias)
+            with _op("attn_out_residual"):
+                B.nt_layernorm_linear(ws.o, W[step + ".wo"], W[step + ".bo"], z, epilogue="residual", residual=z,
+                                      layout=layout, level="pairs", residual_layout=layout)
+        elif step in ("tri_out", "tri_in"):
+            with _op("tri_proj"):
+                B.nt_layernorm_linear(z, W[step + ".w"], W[step + ".b"], None,
+                                      ln=(W[step + ".ln_g"], W[step + ".ln_b"]), n_tail=2 * C, y_tail=ws.ab,
+                                      tail_layout="pair_padded" if step == "tri_out" else "pair_padded_t",
+                                      layout=layout, level="pairs", c_out=2 * C)
+            with _op("triangle_" + step[4:]):
+                B.nt_triangle_mul(layout, 0 if step == "tri_out" else 1, ws.ab[:C], ws.ab[C:], z)
+        elif step == "trans":
+            with _op("transition"):
+                B.nt_layernorm_linear(z, W["trans.w"], W["trans.b"], z, ln=(W["trans.ln_g"], W["trans.ln_b"]),
+                                      epilogue="swiglu_residual", w2=W["trans.w2"], bias2=W["trans.b2"],
+                                      hidden=W["trans.w2"].shape[1], layout=layout, level="pairs")
+        elif step == "single":
+            with _op("segment_mean"):
+                B.nt_segment_reduce(layout, "pairs", "mean", z, ws.m)
+            with _op("single_update"):
+                B.nt_layernorm_linear(ws.m, W["single.w"], W["single.b"], s, epilogue="residual", residual=s,
+                                      layout=layout, level="singles", residual_layout=layout)
+        else:
+            raise ValueError(f"unknown step {step!r}")
+    return z
+
+
+class TokenWorkspace:
+    def __init__(self, layout: B.NestedLayout, c: int, hidden: int, dtype: str, device="cuda"):
+        td = torch.bfloat16 if dtype == "bf16" else torch.float32
+        T = layout.sum_n
+        self.qkv = torch.empty((T, 3 * c), dtype=td, device=device)
+        self.o = torch.empty((T, c), dtype=td, device=device)
+        self.h = torch.empty((T, hidden), dtype=td, device=device)
+        self.pooled = torch.empty((layout.batch, c), dtype=torch.float32, device=device)
+
+
+def encoder_layer(layout: B.NestedLayout, x, W: dict, heads: int, head_dim: int, ws: TokenWorkspace):
+    """Pre-LN encoder layer on packed tokens, in place on x; returns the pooled means."""
+    c = heads * head_dim
+    with _op("qkv_proj"):
+        B.nt_layernorm_linear(x, W["qkv.w"], W["qkv.b"], ws.qkv, ln=(W["ln1_g"], W["ln1_b"]),
+                              layout=layout, level="singles")
+    with _op("attention_1d"):
+        B.nt_pair_row_attention(layout, 2, heads, head_dim, ws.qkv[:, :c], ws.qkv[:, c:2 * c], ws.qkv[:, 2 * c:],
+                                ws.o, scale=1.0 / math.sqrt(head_dim))
+    with _op("out_proj_residual"):
+        B.nt_layernorm_linear(ws.o, W["o.w"], W["o.b"], x, epilogue="residual", residual=x, layout=layout,
+                              level="singles")
+    with _op("ffn_up_gelu"):
+        B.nt_layernorm_linear(x, W["ffn1.w"], W["ffn1.b"], ws.h, ln=(W["ln2_g"], W["ln2_b"]), epilogue="gelu",
+                              layout=layout, level="singles")
+    with _op("ffn_down_residual"):
+        B.nt_layernorm_linear(ws.h, W["ffn2.w"], W["ffn2.b"], x, epilogue="residual", residual=x, layout=layout,
+                              level="singles")
+    with _op("sample_mean"):
+        B.nt_segment_reduce(layout, "singles", "mean", x, ws.pooled)
+    return ws.pooled
+
+
+class PairRun:
+    """A pair workload prepared on the device: layout, weights of every block,
+    the initial single track and the workspaces.  step() runs all blocks."""
+
+    def __init__(self, w, lengths=None, device="cuda"):
+        from . import synth
+        self.w = w
+        self.lengths = [int(n) for n in (synth.lengths_for(w) if lengths is None else lengths)]
+        self.layout = B.NestedLayout(self.lengths)
+        self.dims = dict(c_z=w.c_z, heads=w.heads, head_dim=w.head_dim)
+        self.params = [synth.pair_block_params(w, block=b) for b in range(w.blocks)]
+        self.W = [to_device(p, w.dtype, device) for p in self.params]
+        self.s_init = synth.normal(w.seed, "s", (sum(self.lengths), w.c_s), 1.0, w.dtype)
+        td = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+        self.s0 = torch.from_numpy(self.s_init).to(device=device, dtype=td)
+        self.s = self.s0.clone()
+        self.ws = PairWorkspace(self.layout, w.c_s, w.c_z, w.heads, w.dtype, device)
+        self.z = None
+
+    def step(self):
+        self.s.copy_(self.s0)
+        z = None
+        for b in range(self.w.blocks):
+            steps = self.w.steps if b == 0 else tuple(t for t in self.w.steps if t != "lin")
+            z = pair_block(self.layout, self.s, self.W[b], self.dims, steps, self.ws, z=z)
+        self.z = z
+        return self.s, z
+
+
+class TokenRun:
+    """The token-path workload prepared on the device; step() runs one encoder
+    layer and the per-sample mean pool."""
+
+    def __init__(self, w, lengths=None, device="cuda"):
+        from . import synth
+        self.w = w
+        self.lengths = [int(n) for n in (synth.lengths_for(w) if lengths is None else lengths)]
+        self.layout = B.NestedLayout(self.lengths)
+        self.params = synth.encoder_layer_params(w)
+        self.W = to_device(self.params, w.dtype, device)
+        self.x_init = synth.normal(w.seed, "x", (sum(self.lengths), w.c_s), 0.5, w.dtype)
+        td = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+        self.x0 = torch.from_numpy(self.x_init).to(device=device, dtype=td)
+        self.x = self.x0.clone()
+        self.ws = TokenWorkspace(self.layout, w.c_s, w.hidden, w.dtype, device)
+
+    def step(self):
+        self.x.copy_(self.x0)
+        pooled = encoder_layer(self.layout, self.x, self.W, self.w.heads, self.w.head_dim, self.ws)
+        return self.x, pooled

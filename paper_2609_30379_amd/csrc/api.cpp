@@ -1,0 +1,319 @@
+// C ABI entry points (include/nt.h): argument validation on the host, layout
+// lifetime, and dispatch to the kernel launchers.  No entry point throws,
+// aborts or synchronises the device.
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "nt_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int vec_elems(nt_dtype t) { return t == NT_BF16 ? 8 : 4; }
+
+bool valid_dtype(nt_dtype t) { return t == NT_F32 || t == NT_BF16; }
+
+nt_status check_hip(hipError_t e, const char* what) {
+  if (e == hipSuccess) return NT_OK;
+  return nt::fail(NT_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+nt_status need_device(const nt_layout* L) {
+  if (!L) return nt::fail(NT_ERR_INVALID_ARG, "layout is NULL");
+  if (!L->has_device) return nt::fail(NT_ERR_INVALID_ARG, "layout was built host-only; it has no device mirrors");
+  return NT_OK;
+}
+
+bool same_partition(const nt_layout* a, const nt_layout* b) {
+  return a == b || (a && b && a->lengths == b->lengths);
+}
+
+nt_status upload(nt_layout* L, hipStream_t s) {
+  struct Part { const std::vector<int32_t>* v; const int32_t** dst; };
+  Part parts[] = {
+      {&L->lengths, &L->d_lengths},       {&L->cu_seqlens, &L->d_cu_seqlens},
+      {&L->cu_pairs, &L->d_cu_pairs},     {&L->cu_pad, &L->d_cu_pad},
+      {&L->row_splits2, &L->d_row_splits2}, {&L->row_sample, &L->d_row_sample},
+      {&L->attn_work, &L->d_attn_work},   {&L->tri_work, &L->d_tri_work},
+      {&L->seq_work, &L->d_seq_work},
+  };
+  size_t total = 0;
+  for (auto& p : parts) total += (p.v->size() * sizeof(int32_t) + 255) / 256 * 256;
+  std::vector<int32_t> staging(total / sizeof(int32_t), 0);
+  if (hipGetDevice(&L->device) != hipSuccess) return nt::fail(NT_ERR_HIP, "hipGetDevice failed");
+  hipError_t e = hipMalloc(&L->d_base, total);
+  if (e != hipSuccess) {
+    L->d_base = nullptr;
+    return nt::fail(e == hipErrorOutOfMemory ? NT_ERR_OOM : NT_ERR_HIP,
+                    std::string("hipMalloc of layout mirrors: ") + hipGetErrorString(e));
+  }
+  size_t off = 0;
+  for (auto& p : parts) {
+    std::memcpy(staging.data() + off / sizeof(int32_t), p.v->data(), p.v->size() * sizeof(int32_t));
+    *p.dst = reinterpret_cast<const int32_t*>(static_cast<char*>(L->d_base) + off);
+    off += (p.v->size() * sizeof(int32_t) + 255) / 256 * 256;
+  }
+  e = hipMemcpyAsync(L->d_base, staging.data(), total, hipMemcpyHostToDevice, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);   // staging is a local buffer
+  if (e != hipSuccess) return check_hip(e, "copy of layout mirrors");
+  L->has_device = true;
+  return NT_OK;
+}
+
+nt_status build(const int32_t* lengths, int32_t batch, uint32_t flags, void* stream, nt_layout** out) {
+  if (!out) return nt::fail(NT_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (flags & ~(uint32_t)NT_LAYOUT_HOST_ONLY) return nt::fail(NT_ERR_INVALID_ARG, "unknown flags");
+  nt_layout* L = new (std::nothrow) nt_layout();
+  if (!L) return nt::fail(NT_ERR_OOM, "host allocation failed");
+  nt_status st = nt::plan_layout(lengths, batch, L);
+  if (st == NT_OK && !(flags & NT_LAYOUT_HOST_ONLY)) st = upload(L, static_cast<hipStream_t>(stream));
+  if (st != NT_OK) {
+    nt_layout_destroy(L);
+    return st;
+  }
+  *out = L;
+  return NT_OK;
+}
+
+}  // namespace
+
+namespace nt {
+nt_status fail(nt_status s, const std::string& msg) {
+  g_last_error = msg;
+  return s;
+}
+}  // namespace nt
+
+extern "C" {
+
+const char* nt_last_error(void) { return g_last_error.c_str(); }
+
+const char* nt_version(void) { return "nt-mi355x 0.1 (gfx950)"; }
+
+nt_status nt_from_lengths(const int32_t* lengths, int32_t batch, uint32_t flags, void* stream,
+                          nt_layout** out) {
+  g_last_error.clear();
+  return build(lengths, batch, flags, stream, out);
+}
+
+nt_status nt_from_offsets(const int32_t* cu_seqlens, int32_t batch, uint32_t flags, void* stream,
+                          nt_layout** out) {
+  g_last_error.clear();
+  if (!cu_seqlens) return nt::fail(NT_ERR_INVALID_ARG, "cu_seqlens is NULL");
+  if (batch < 1) return nt::fail(NT_ERR_INVALID_ARG, "batch must be >= 1");
+  if (cu_seqlens[0] != 0) return nt::fail(NT_ERR_INVALID_ARG, "offsets must start at 0");
+  std::vector<int32_t> lengths(batch);
+  for (int32_t i = 0; i < batch; ++i) {
+    if (cu_seqlens[i + 1] < cu_seqlens[i])
+      return nt::fail(NT_ERR_INVALID_ARG, "offsets must be non-decreasing (sample " + std::to_string(i) + ")");
+    lengths[i] = cu_seqlens[i + 1] - cu_seqlens[i];
+  }
+  return build(lengths.data(), batch, flags, stream, out);
+}
+
+nt_status nt_layout_destroy(nt_layout* L) {
+  if (!L) return NT_OK;
+  nt_status st = NT_OK;
+  if (L->d_base) {
+    if (hipFree(L->d_base) != hipSuccess) st = nt::fail(NT_ERR_HIP, "hipFree of layout mirrors failed");
+  }
+  delete L;
+  return st;
+}
+
+nt_status nt_layout_info(const nt_layout* L, nt_layout_info_t* info) {
+  g_last_error.clear();
+  if (!L || !info) return nt::fail(NT_ERR_INVALID_ARG, "NULL argument");
+  info->batch = L->batch;
+  info->max_len = L->max_len;
+  info->sum_n = L->sum_n;
+  info->sum_n2 = L->sum_n2;
+  info->sum_n3 = L->sum_n3;
+  info->sum_pad = L->sum_pad;
+  info->d_cu_seqlens = L->d_cu_seqlens;
+  info->d_cu_pairs = L->d_cu_pairs;
+  info->d_row_splits2 = L->d_row_splits2;
+  return NT_OK;
+}
+
+nt_status nt_layout_host_array(const nt_layout* L, nt_array which, const int32_t** data, int64_t* count) {
+  g_last_error.clear();
+  if (!L || !data || !count) return nt::fail(NT_ERR_INVALID_ARG, "NULL argument");
+  const std::vector<int32_t>* v = nullptr;
+  switch (which) {
+    case NT_ARR_LENGTHS: v = &L->lengths; break;
+    case NT_ARR_CU_SEQLENS: v = &L->cu_seqlens; break;
+    case NT_ARR_CU_PAIRS: v = &L->cu_pairs; break;
+    case NT_ARR_ROW_SPLITS2: v = &L->row_splits2; break;
+    case NT_ARR_ROW_SAMPLE: v = &L->row_sample; break;
+    case NT_ARR_ATTN_WORK: v = &L->attn_work; break;
+    case NT_ARR_TRI_WORK: v = &L->tri_work; break;
+    case NT_ARR_SEQ_WORK: v = &L->seq_work; break;
+    case NT_ARR_CU_PAD: v = &L->cu_pad; break;
+    default: return nt::fail(NT_ERR_INVALID_ARG, "unknown array id");
+  }
+  *data = v->data();
+  *count = (int64_t)v->size();
+  return NT_OK;
+}
+
+int32_t nt_layouts_compatible(const nt_layout* a, const nt_layout* b) {
+  return (a && b && same_partition(a, b)) ? 1 : 0;
+}
+
+nt_status nt_pair_broadcast(const nt_layout* L, int32_t C, const void* u, int64_t ld_u, const void* v,
+                            int64_t ld_v, void* z, int64_t ld_z, int32_t accumulate, nt_dtype dtype,
+                            void* stream) {
+  g_last_error.clear();
+  if (nt_status st = need_device(L)) return st;
+  if (!valid_dtype(dtype)) return nt::fail(NT_ERR_INVALID_ARG, "dtype must be NT_F32 or NT_BF16");
+  if (C <= 0) return nt::fail(NT_ERR_INVALID_ARG, "C must be > 0");
+  if (accumulate != 0 && accumulate != 1) return nt::fail(NT_ERR_INVALID_ARG, "accumulate must be 0 or 1");
+  const int ve = vec_elems(dtype);
+  if (C % ve) return nt::fail(NT_ERR_INVALID_ARG, "C must be a multiple of " + std::to_string(ve));
+  if (L->sum_n2 == 0) return NT_OK;
+  if (!u || !v || !z) return nt::fail(NT_ERR_INVALID_ARG, "u, v and z must be non-NULL");
+  if (!aligned16(u) || !aligned16(v) || !aligned16(z)) return nt::fail(NT_ERR_INVALID_ARG, "pointers must be 16-byte aligned");
+  if (ld_u < C || ld_v < C || ld_z < C || ld_u % ve || ld_v % ve || ld_z % ve)
+    return nt::fail(NT_ERR_INVALID_ARG, "row strides must be >= C and multiples of the vector width");
+  return check_hip(nt::launch_pair_broadcast(*L, C, u, ld_u, v, ld_v, z, ld_z, accumulate, dtype,
+                                             static_cast<hipStream_t>(stream)),
+                   "nt_pair_broadcast launch");
+}
+
+nt_status nt_segment_reduce(const nt_layout* L, nt_level level, int32_t op, int32_t C, const void* x,
+                            int64_t ld_x, nt_dtype x_dtype, float* y, int64_t ld_y, void* stream) {
+  g_last_error.clear();
+  if (nt_status st = need_device(L)) return st;
+  if (level != NT_LEVEL_SINGLES && level != NT_LEVEL_PAIRS) return nt::fail(NT_ERR_INVALID_ARG, "bad level");
+  if (op != 0 && op != 1) return nt::fail(NT_ERR_INVALID_ARG, "op must be 0 (sum) or 1 (mean)");
+  if (!valid_dtype(x_dtype)) return nt::fail(NT_ERR_INVALID_ARG, "bad dtype");
+  if (C <= 0) return nt::fail(NT_ERR_INVALID_ARG, "C must be > 0");
+  const int ve = vec_elems(x_dtype);
+  if (C % ve || ld_x % ve || ld_x < C) return nt::fail(NT_ERR_INVALID_ARG, "C and ld_x must be multiples of the vector width, ld_x >= C");
+  if (ld_y < C || ld_y % 4) return nt::fail(NT_ERR_INVALID_ARG, "ld_y must be >= C and a multiple of 4");
+  const int64_t out_rows = level == NT_LEVEL_PAIRS ? L->sum_n : L->batch;
+  if (out_rows == 0) return NT_OK;
+  if (!y) return nt::fail(NT_ERR_INVALID_ARG, "y is NULL");
+  if (!x && (level == NT_LEVEL_PAIRS ? L->sum_n2 : L->sum_n) > 0) return nt::fail(NT_ERR_INVALID_ARG, "x is NULL");
+  if ((x && !aligned16(x)) || !aligned16(y)) return nt::fail(NT_ERR_INVALID_ARG, "pointers must be 16-byte aligned");
+  return check_hip(nt::launch_segment_reduce(*L, level, op, C, x, ld_x, x_dtype, y, ld_y,
+                                             static_cast<hipStream_t>(stream)),
+                   "nt_segment_reduce launch");
+}
+
+nt_status nt_layernorm_linear(const nt_linear_args* a, void* stream) {
+  g_last_error.clear();
+  if (!a) return nt::fail(NT_ERR_INVALID_ARG, "args is NULL");
+  if (!valid_dtype(a->dtype) || !valid_dtype(a->x_dtype)) return nt::fail(NT_ERR_INVALID_ARG, "bad dtype");
+  if (a->dtype == NT_F32 && a->x_dtype != NT_F32) return nt::fail(NT_ERR_INVALID_ARG, "f32 weights need f32 input");
+  if (a->rows < 0 || a->c_in <= 0 || a->c_out <= 0) return nt::fail(NT_ERR_INVALID_ARG, "bad sizes");
+  if (a->rows > INT32_MAX) return nt::fail(NT_ERR_OVERFLOW, "rows exceed int32");
+  if (a->c_in % 8) return nt::fail(NT_ERR_INVALID_ARG, "c_in must be a multiple of 8");
+  if (a->epilogue < NT_EPI_NONE || a->epilogue > NT_EPI_GELU) return nt::fail(NT_ERR_INVALID_ARG, "bad epilogue");
+  if (a->ln_beta && !a->ln_gamma) return nt::fail(NT_ERR_INVALID_ARG, "ln_beta without ln_gamma");
+  if (a->ln_gamma && !(a->ln_eps >= 0.f)) return nt::fail(NT_ERR_INVALID_ARG, "ln_eps must be >= 0");
+  const bool swiglu = a->epilogue == NT_EPI_SWIGLU_RESIDUAL;
+  const int vx = vec_elems(a->x_dtype), vy = vec_elems(a->dtype);
+  if (a->ldx < a->c_in || a->ldx % vx) return nt::fail(NT_ERR_INVALID_ARG, "ldx must be >= c_in and a multiple of the vector width");
+  if (a->n_tail < 0 || a->n_tail > a->c_out) return nt::fail(NT_ERR_INVALID_ARG, "n_tail out of range");
+  if (a->tail_layout < NT_TAIL_CHANNEL_MAJOR || a->tail_layout > NT_TAIL_PAIR_PADDED_T)
+    return nt::fail(NT_ERR_INVALID_ARG, "bad tail_layout");
+  const int n_main = a->c_out - a->n_tail;
+  if (a->layout) {
+    if (!a->layout->has_device && a->n_tail && a->tail_layout != NT_TAIL_CHANNEL_MAJOR)
+      return nt::fail(NT_ERR_INVALID_ARG, "pair-padded tails need a layout with device mirrors");
+    const int64_t expect = a->level == NT_LEVEL_PAIRS ? a->layout->sum_n2 : a->layout->sum_n;
+    if (a->level != NT_LEVEL_PAIRS && a->level != NT_LEVEL_SINGLES) return nt::fail(NT_ERR_INVALID_ARG, "bad level");
+    if (expect != a->rows) return nt::fail(NT_ERR_LAYOUT_MISMATCH, "rows differ from the layout's row count");
+  }
+  if (a->residual_layout && !same_partition(a->layout, a->residual_layout))
+    return nt::fail(NT_ERR_LAYOUT_MISMATCH, "residual has a different logical partition than x");
+  if (a->n_tail && a->tail_layout != NT_TAIL_CHANNEL_MAJOR &&
+      (!a->layout || a->level != NT_LEVEL_PAIRS))
+    return nt::fail(NT_ERR_UNSUPPORTED, "pair-padded tail output needs a pair-level layout");
+  if (swiglu) {
+    if (a->dtype == NT_BF16 && (a->c_in != a->c_out || (a->c_in != 64 && a->c_in != 128 && a->c_in != 256) ||
+                                a->hidden <= 0 || a->hidden % 32 || a->x_dtype != NT_BF16))
+      return nt::fail(NT_ERR_UNSUPPORTED, "bf16 SwiGLU needs bf16 x, c_in == c_out in {64, 128, 256} and hidden % 32 == 0");
+    if (a->dtype == NT_F32 && (a->c_in > 1024 || a->hidden <= 0 || a->hidden > 4096))
+      return nt::fail(NT_ERR_UNSUPPORTED, "f32 SwiGLU needs c_in <= 1024 and 0 < hidden <= 4096");
+    if (a->n_tail) return nt::fail(NT_ERR_UNSUPPORTED, "SwiGLU has no tail output");
+    if (!a->w2) return nt::fail(NT_ERR_INVALID_ARG, "SwiGLU needs w2");
+    if (!a->residual && a->c_out != a->c_in) return nt::fail(NT_ERR_INVALID_ARG, "SwiGLU without residual needs c_out == c_in");
+    if (!a->residual && a->x_dtype != a->dtype) return nt::fail(NT_ERR_INVALID_ARG, "SwiGLU residual = x needs x in the output dtype");
+  }
+  if (a->dtype == NT_F32 && !swiglu && a->c_in > 4096) return nt::fail(NT_ERR_UNSUPPORTED, "f32 path needs c_in <= 4096");
+  if (a->epilogue == NT_EPI_RESIDUAL && !a->residual) return nt::fail(NT_ERR_INVALID_ARG, "residual epilogue needs residual");
+  if (a->rows == 0) return NT_OK;
+  if (!a->x || !a->w) return nt::fail(NT_ERR_INVALID_ARG, "x and w must be non-NULL");
+  if (n_main > 0 && !a->y) return nt::fail(NT_ERR_INVALID_ARG, "y is NULL");
+  if (a->n_tail > 0 && !a->y_tail) return nt::fail(NT_ERR_INVALID_ARG, "y_tail is NULL");
+  if ((a->ln_gamma && !aligned16(a->ln_gamma)) || (a->ln_beta && !aligned16(a->ln_beta)))
+    return nt::fail(NT_ERR_INVALID_ARG, "ln_gamma and ln_beta must be 16-byte aligned");
+  if (!aligned16(a->x) || !aligned16(a->w) || (a->y && !aligned16(a->y)) || (a->residual && !aligned16(a->residual)) ||
+      (a->w2 && !aligned16(a->w2)) || (a->y_tail && !aligned16(a->y_tail)))
+    return nt::fail(NT_ERR_INVALID_ARG, "pointers must be 16-byte aligned");
+  if (n_main > 0 && (a->ldy < n_main || a->ldy % vy)) return nt::fail(NT_ERR_INVALID_ARG, "ldy must be >= the main width and a multiple of the vector width");
+  if (a->residual && (a->ld_residual < n_main || a->ld_residual % vy)) return nt::fail(NT_ERR_INVALID_ARG, "bad ld_residual");
+  if (a->n_tail > 0) {
+    const int64_t need = a->tail_layout == NT_TAIL_CHANNEL_MAJOR ? a->rows : a->layout->sum_pad;
+    if (a->ld_tail < need) return nt::fail(NT_ERR_INVALID_ARG, "ld_tail is smaller than the tail's row extent");
+  }
+  nt::LinearPlan p{a, a->tail_layout, a->layout};
+  return check_hip(nt::launch_linear(p, static_cast<hipStream_t>(stream)), "nt_layernorm_linear launch");
+}
+
+nt_status nt_pair_row_attention(const nt_layout* L, int32_t axis, int32_t H, int32_t D, const void* q,
+                                const void* k, const void* v, int64_t ld_qkv, const void* bias,
+                                int64_t ld_bias, float scale, void* o, int64_t ld_o, nt_dtype dtype,
+                                void* stream) {
+  g_last_error.clear();
+  if (nt_status st = need_device(L)) return st;
+  if (axis < 0 || axis > 2) return nt::fail(NT_ERR_INVALID_ARG, "axis must be 0, 1 or 2");
+  if (!valid_dtype(dtype)) return nt::fail(NT_ERR_INVALID_ARG, "bad dtype");
+  if (H <= 0 || D <= 0) return nt::fail(NT_ERR_INVALID_ARG, "heads and head_dim must be > 0");
+  if (dtype == NT_BF16 && D != 32 && D != 64) return nt::fail(NT_ERR_UNSUPPORTED, "bf16 attention supports head_dim 32 or 64");
+  if (dtype == NT_F32 && D != 8 && D != 16 && D != 32 && D != 64) return nt::fail(NT_ERR_UNSUPPORTED, "f32 attention supports head_dim 8, 16, 32 or 64");
+  if (axis == 2 && bias) return nt::fail(NT_ERR_INVALID_ARG, "1-D attention takes no pair bias");
+  const int ve = vec_elems(dtype);
+  if ((int64_t)H * D > ld_qkv || ld_qkv % ve || (int64_t)H * D > ld_o || ld_o % ve)
+    return nt::fail(NT_ERR_INVALID_ARG, "row strides must hold H*head_dim and be multiples of the vector width");
+  const int lim = dtype == NT_F32 ? 4096 : (D == 32 ? nt::kAttnMaxLenD32 : nt::kAttnMaxLenD64);
+  if (L->max_len > lim) return nt::fail(NT_ERR_UNSUPPORTED, "a sample is longer than the attention limit " + std::to_string(lim));
+  const int64_t rows = axis == 2 ? L->sum_n : L->sum_n2;
+  if (bias && ld_bias < rows) return nt::fail(NT_ERR_INVALID_ARG, "ld_bias must be >= the pair row count");
+  if (rows == 0) return NT_OK;
+  if (!q || !k || !v || !o) return nt::fail(NT_ERR_INVALID_ARG, "q, k, v and o must be non-NULL");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || (bias && (reinterpret_cast<uintptr_t>(bias) & 3u)))
+    return nt::fail(NT_ERR_INVALID_ARG, "q, k, v, o must be 16-byte aligned, bias 4-byte aligned");
+  if (!(scale == scale)) return nt::fail(NT_ERR_INVALID_ARG, "scale is NaN");
+  return check_hip(nt::launch_attention(*L, axis, H, D, q, k, v, ld_qkv, bias, ld_bias, scale, o, ld_o, dtype,
+                                        static_cast<hipStream_t>(stream)),
+                   "nt_pair_row_attention launch");
+}
+
+nt_status nt_triangle_mul(const nt_layout* L, int32_t direction, int32_t C, const void* a, const void* b,
+                          int64_t ld_ab, void* z, int64_t ld_z, nt_dtype dtype, void* stream) {
+  g_last_error.clear();
+  if (nt_status st = need_device(L)) return st;
+  if (direction != 0 && direction != 1) return nt::fail(NT_ERR_INVALID_ARG, "direction must be 0 or 1");
+  if (!valid_dtype(dtype)) return nt::fail(NT_ERR_INVALID_ARG, "bad dtype");
+  if (C <= 0) return nt::fail(NT_ERR_INVALID_ARG, "C must be > 0");
+  if (dtype == NT_BF16 && C % 32) return nt::fail(NT_ERR_INVALID_ARG, "bf16 triangle needs C % 32 == 0");
+  const int ve = vec_elems(dtype);
+  if (ld_z < C || ld_z % ve) return nt::fail(NT_ERR_INVALID_ARG, "ld_z must be >= C and a multiple of the vector width");
+  if (ld_ab < L->sum_pad || ld_ab % 8) return nt::fail(NT_ERR_INVALID_ARG, "ld_ab must be >= sum_pad and a multiple of 8");
+  if (L->sum_n2 == 0) return NT_OK;
+  if (!a || !b || !z) return nt::fail(NT_ERR_INVALID_ARG, "a, b and z must be non-NULL");
+  if (!aligned16(a) || !aligned16(b) || !aligned16(z)) return nt::fail(NT_ERR_INVALID_ARG, "pointers must be 16-byte aligned");
+  return check_hip(nt::launch_triangle(*L, C, a, b, ld_ab, z, ld_z, dtype, static_cast<hipStream_t>(stream)),
+                   "nt_triangle_mul launch");
+}
+
+}  // extern "C"

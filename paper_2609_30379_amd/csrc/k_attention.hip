@@ -1,0 +1,275 @@
+// Segmented softmax attention over packed buffers, one launch for the batch.
+//
+// A segment is one pair row (axis 0: cells (i, r, *)), one pair column
+// (axis 1: cells (i, *, r)) or one sample's tokens (axis 2).  The workgroup
+// for (segment, head) stages the segment's keys and transposed values in LDS
+// once; each wave then runs 16-query tiles through an online softmax over
+// 64-key chunks on matrix cores:
+//   S^T = K Q^T       lane (g, q) holds scores of keys 16t + 4g + i for query q,
+//                     so the running max/sum of a query live in one lane column
+//   O^T += V^T P^T    P is taken from the S^T registers as the B operand
+//                     (keys {4g..4g+3} of two 16-key tiles), no shuffles.
+#include "nt_device.h"
+#include "nt_internal.h"
+
+namespace nt {
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+struct AttnArgs {
+  int axis, H;
+  const bf16* q;
+  const bf16* k;
+  const bf16* v;
+  int64_t ld_qkv;
+  const bf16* bias;
+  int64_t ld_bias;
+  float scale_log2;      // softmax scale * log2(e)
+  bf16* o;
+  int64_t ld_o;
+  const int32_t* work;   // (sample, row) or (sample, query block) pairs
+  const int32_t* cu_seqlens;
+  const int32_t* cu_pairs;
+  int vstride;           // LDS row stride of V^T (elements)
+};
+
+struct Seg {
+  int n;                 // keys in the segment
+  int64_t base, step;    // packed row of element t: base + t * step
+  int q_begin, q_end;
+  int64_t cu;            // pair offset of the sample (bias addressing)
+};
+
+template <typename A>
+__device__ __forceinline__ bool segment_of(const A& p, Seg& s) {
+  const int i = p.work[2 * blockIdx.x], r = p.work[2 * blockIdx.x + 1];
+  if (i < 0) return false;
+  if (p.axis == 2) {
+    s.n = p.cu_seqlens[i + 1] - p.cu_seqlens[i];
+    s.base = p.cu_seqlens[i];
+    s.step = 1;
+    s.q_begin = r * kSeqQBlock;
+    s.q_end = min(s.n, s.q_begin + kSeqQBlock);
+    s.cu = 0;
+  } else {
+    s.n = p.cu_seqlens[i + 1] - p.cu_seqlens[i];
+    s.cu = p.cu_pairs[i];
+    s.base = p.axis == 0 ? s.cu + (int64_t)r * s.n : s.cu + r;
+    s.step = p.axis == 0 ? 1 : s.n;
+    s.q_begin = 0;
+    s.q_end = s.n;
+  }
+  return true;
+}
+
+template <int D>
+__global__ void __launch_bounds__(256) attention_mfma_kernel(AttnArgs p) {
+  extern __shared__ __attribute__((aligned(16))) bf16 lds[];
+  constexpr int KS = D + 8;                    // LDS stride of K rows (bf16)
+  constexpr int DV = D / 8;                    // 16-byte vectors per head row
+  Seg sg;
+  if (!segment_of(p, sg)) return;
+  const int h = blockIdx.y;
+  const int n = sg.n;
+  const int npad = (n + 63) & ~63;
+  bf16* Ks = lds;                              // [npad][KS]
+  bf16* Vt = lds + (size_t)npad * KS;          // [D][vstride]
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, g = lane >> 4;
+
+  // ---- stage keys (row-major) and values (transposed) of this head -------
+  for (int c = tid; c < npad * DV; c += 256) {
+    const int key = c / DV, dc = (c % DV) * 8;
+    uint4 kk = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
+    if (key < n) {
+      const int64_t row = sg.base + (int64_t)key * sg.step;
+      kk = *reinterpret_cast<const uint4*>(p.k + row * p.ld_qkv + h * D + dc);
+      vv = *reinterpret_cast<const uint4*>(p.v + row * p.ld_qkv + h * D + dc);
+    }
+    *reinterpret_cast<uint4*>(&Ks[key * KS + dc]) = kk;
+    const bf16x8 vb = *reinterpret_cast<const bf16x8*>(&vv);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) Vt[(dc + j) * p.vstride + key] = vb[j];
+  }
+  __syncthreads();
+
+  for (int qt = sg.q_begin / 16 + wave; qt * 16 < sg.q_end; qt += 4) {
+    const int qi = qt * 16 + l16;
+    const bool qvalid = qi < sg.q_end;
+    const int64_t qrow = sg.base + (int64_t)qi * sg.step;
+    bf16x8 qf[D / 32];
+#pragma unroll
+    for (int dd = 0; dd < D / 32; ++dd) {
+      if (qvalid) qf[dd] = *reinterpret_cast<const bf16x8*>(p.q + qrow * p.ld_qkv + h * D + dd * 32 + g * 8);
+      else qf[dd] = bf16x8{};
+    }
+    float m_run = -INFINITY, l_run = 0.f;
+    f32x4 O[D / 16];
+#pragma unroll
+    for (int dt = 0; dt < D / 16; ++dt) O[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const bf16* brow = nullptr;                // bias row of this query (axis 0)
+    if (p.bias && qvalid) brow = p.bias + (int64_t)h * p.ld_bias + sg.cu + (p.axis == 0 ? (int64_t)qi * n : qi);
+
+    for (int kc = 0; kc < npad; kc += 64) {
+      f32x4 s[4];
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt) {
+        s[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int dd = 0; dd < D / 32; ++dd) {
+          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Ks[(kc + kt * 16 + l16) * KS + dd * 32 + g * 8]);
+          s[kt] = mfma16(kf, qf[dd], s[kt]);
+        }
+      }
+      float x[4][4];
+      float mloc = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int key = kc + kt * 16 + 4 * g + i;
+          float t = s[kt][i] * p.scale_log2;
+          if (brow && key < n) t += (float)brow[p.axis == 0 ? (int64_t)key : (int64_t)key * n] * kLog2e;
+          t = key < n ? t : -INFINITY;
+          x[kt][i] = t;
+          mloc = fmaxf(mloc, t);
+        }
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+      const float m_new = fmaxf(m_run, mloc);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt) O[dt] *= alpha;
+      bf16x8 pf[2];
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float e = __builtin_amdgcn_exp2f(x[kt][i] - m_new);
+          l_run += e;
+          pf[kt >> 1][(kt & 1) * 4 + i] = (bf16)e;
+        }
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt)
+#pragma unroll
+        for (int pp = 0; pp < 2; ++pp) {
+          const bf16* vr = &Vt[(dt * 16 + l16) * p.vstride + kc + pp * 32 + 4 * g];
+          const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vr);
+          const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vr + 16);
+          const bf16x8 vf = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+          O[dt] = mfma16(vf, pf[pp], O[dt]);
+        }
+    }
+    l_run += __shfl_xor(l_run, 16, 64);
+    l_run += __shfl_xor(l_run, 32, 64);
+    if (qvalid) {
+      const float inv = 1.f / l_run;
+      bf16* orow = p.o + qrow * p.ld_o + h * D;
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt) {
+        bf16x4 ov;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) ov[i] = (bf16)(O[dt][i] * inv);
+        *reinterpret_cast<bf16x4*>(orow + dt * 16 + 4 * g) = ov;
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------- fp32 path
+struct AttnF32Args {
+  int axis, H;
+  const float* q;
+  const float* k;
+  const float* v;
+  int64_t ld_qkv;
+  const float* bias;
+  int64_t ld_bias;
+  float scale;
+  float* o;
+  int64_t ld_o;
+  const int32_t* work;
+  const int32_t* cu_seqlens;
+  const int32_t* cu_pairs;
+};
+
+// Exact two-pass softmax per query in fp32: one thread per query.
+template <int D>
+__global__ void __launch_bounds__(256) attention_f32_kernel(AttnF32Args p) {
+  Seg sg;
+  if (!segment_of(p, sg)) return;
+  const int h = blockIdx.y, n = sg.n;
+  for (int qi = sg.q_begin + (int)threadIdx.x; qi < sg.q_end; qi += 256) {
+    const int64_t qrow = sg.base + (int64_t)qi * sg.step;
+    float qv[D];
+#pragma unroll
+    for (int d = 0; d < D; ++d) qv[d] = p.q[qrow * p.ld_qkv + h * D + d];
+    const float* brow = p.bias ? p.bias + (int64_t)h * p.ld_bias + sg.cu + (p.axis == 0 ? (int64_t)qi * n : qi) : nullptr;
+    auto logit = [&](int key) {
+      const int64_t krow = sg.base + (int64_t)key * sg.step;
+      float s = 0.f;
+#pragma unroll
+      for (int d = 0; d < D; ++d) s = fmaf(qv[d], p.k[krow * p.ld_qkv + h * D + d], s);
+      s *= p.scale;
+      if (brow) s += brow[p.axis == 0 ? (int64_t)key : (int64_t)key * n];
+      return s;
+    };
+    float mx = -INFINITY;
+    for (int key = 0; key < n; ++key) mx = fmaxf(mx, logit(key));
+    float sum = 0.f, acc[D];
+#pragma unroll
+    for (int d = 0; d < D; ++d) acc[d] = 0.f;
+    for (int key = 0; key < n; ++key) {
+      const float e = expf(logit(key) - mx);
+      sum += e;
+      const int64_t krow = sg.base + (int64_t)key * sg.step;
+#pragma unroll
+      for (int d = 0; d < D; ++d) acc[d] = fmaf(e, p.v[krow * p.ld_qkv + h * D + d], acc[d]);
+    }
+#pragma unroll
+    for (int d = 0; d < D; ++d) p.o[qrow * p.ld_o + h * D + d] = acc[d] / sum;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_attention(const nt_layout& L, int axis, int H, int D, const void* q, const void* k,
+                            const void* v, int64_t ld_qkv, const void* bias, int64_t ld_bias, float scale,
+                            void* o, int64_t ld_o, nt_dtype dtype, hipStream_t s) {
+  const int32_t* work = axis == 2 ? L.d_seq_work : L.d_attn_work;
+  const int64_t items = axis == 2 ? L.seq_items() : L.attn_items();
+  if (items == 0) return hipSuccess;
+  const dim3 grid((unsigned)items, (unsigned)H), block(256);
+  if (dtype == NT_F32) {
+    AttnF32Args a{axis, H, (const float*)q, (const float*)k, (const float*)v, ld_qkv, (const float*)bias,
+                  ld_bias, scale, (float*)o, ld_o, work, L.d_cu_seqlens, L.d_cu_pairs};
+    switch (D) {
+      case 8: attention_f32_kernel<8><<<grid, block, 0, s>>>(a); break;
+      case 16: attention_f32_kernel<16><<<grid, block, 0, s>>>(a); break;
+      case 32: attention_f32_kernel<32><<<grid, block, 0, s>>>(a); break;
+      case 64: attention_f32_kernel<64><<<grid, block, 0, s>>>(a); break;
+      default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+  }
+  const int npad = (L.max_len + 63) & ~63;
+  const int vstride = npad + 8;
+  AttnArgs a{axis, H, (const bf16*)q, (const bf16*)k, (const bf16*)v, ld_qkv, (const bf16*)bias, ld_bias,
+             scale * kLog2e, (bf16*)o, ld_o, work, L.d_cu_seqlens, L.d_cu_pairs, vstride};
+  const size_t smem = sizeof(bf16) * ((size_t)npad * (D + 8) + (size_t)D * vstride);
+  if (D == 32) {
+    if (smem > 65536) hipFuncSetAttribute((const void*)attention_mfma_kernel<32>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    attention_mfma_kernel<32><<<grid, block, smem, s>>>(a);
+  } else if (D == 64) {
+    if (smem > 65536) hipFuncSetAttribute((const void*)attention_mfma_kernel<64>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    attention_mfma_kernel<64><<<grid, block, smem, s>>>(a);
+  } else {
+    return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace nt

@@ -1,0 +1,606 @@
+// LayerNorm + Linear on packed rows (Sec. 3.3: V' = V W^T + b, with the
+// normalisation acting on each row's feature tail).  Rows are independent, so
+// every launch covers the whole ragged batch as one dense [R, K] x [K, N].
+//
+// bf16 path: matrix cores (v_mfma_f32_16x16x32_bf16), computed transposed as
+// D^T = W X^T so that each lane ends up owning four consecutive output
+// channels of one row, which the fused epilogues (bias, residual, GELU,
+// channel-major tails) consume without a shuffle.
+#include "nt_device.h"
+#include "nt_internal.h"
+
+namespace nt {
+namespace {
+
+constexpr int BM = 128, BN = 128, BK = 32;
+constexpr int SK = BK + 8;          // LDS row stride (bf16): 80 bytes, keeps b128 reads spread
+
+struct LinArgs {
+  int rows, K, N, n_main;
+  const void* x;
+  int64_t ldx;
+  const float* gamma;
+  const float* beta;
+  float eps;
+  const bf16* w;
+  const float* bias;
+  const bf16* res;
+  int64_t ld_res;
+  bf16* y;
+  int64_t ldy;
+  bf16* y_tail;
+  int64_t ld_tail;
+  int tail_mode;
+  const int32_t* row_splits2;
+  const int32_t* row_sample;
+  const int32_t* cu_seqlens;
+  const int32_t* cu_pad;
+  int sum_n;
+  int mblocks, nblocks;
+};
+
+// Position of packed pair row m (cell (i, x, k)) in a pair-padded channel-major
+// block: P_i + x n8_i + k, or P_i + k n8_i + x when transposed.
+__device__ __forceinline__ int64_t pair_padded_pos(const LinArgs& p, int m) {
+  int lo = 0, hi = p.sum_n - 1;               // largest eta with row_splits2[eta] <= m
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (p.row_splits2[mid] <= m) lo = mid; else hi = mid - 1;
+  }
+  const int i = p.row_sample[lo];
+  const int n = p.cu_seqlens[i + 1] - p.cu_seqlens[i];
+  const int n8 = (n + 7) & ~7;
+  const int x = lo - p.cu_seqlens[i];
+  const int k = m - p.row_splits2[lo];
+  return (int64_t)p.cu_pad[i] + (p.tail_mode == kTailPairPadded ? (int64_t)x * n8 + k : (int64_t)k * n8 + x);
+}
+
+__device__ __forceinline__ float gelu_erf(float v) { return 0.5f * v * (1.f + erff(v * 0.70710678118654752f)); }
+
+// Raw (unnormalised) global data of one k-step, held in registers while the
+// previous step computes.
+template <typename XT> struct XStage;
+template <> struct XStage<bf16> { uint4 d[2]; };
+template <> struct XStage<float> { float4 d[4]; };
+
+template <typename XT, int EPI>
+__global__ void __launch_bounds__(256) linear_mfma_kernel(LinArgs p) {
+  __shared__ __attribute__((aligned(16))) bf16 Xs[BM * SK];
+  __shared__ __attribute__((aligned(16))) bf16 Ws[BN * SK];
+  __shared__ float s_mean[BM], s_rstd[BM];
+
+  // XCD-aware tile order: the n-blocks of one row block run back to back on
+  // the same XCD (workgroups are dispatched round-robin over 8 XCDs), so the
+  // row block is fetched into one L2 once.
+  const int id = blockIdx.x;
+  const int xcd = id % kXcds, kq = id / kXcds;
+  const int nb = kq % p.nblocks;
+  const int mb = (kq / p.nblocks) * kXcds + xcd;
+  if (mb >= p.mblocks) return;
+  const int m0 = mb * BM, n0 = nb * BN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, g = lane >> 4;
+  const XT* x = static_cast<const XT*>(p.x);
+  constexpr int VX = Vec<XT>::N;
+
+  // ---- LayerNorm statistics: 16 lanes per row, two passes, fp32 ----------
+  if (p.gamma) {
+    for (int rr = tid >> 4; rr < BM; rr += 16) {
+      const int m = m0 + rr;
+      float mean = 0.f, rstd = 0.f;
+      if (m < p.rows) {
+        const XT* row = x + (int64_t)m * p.ldx;
+        float s = 0.f;
+        for (int k = l16 * VX; k < p.K; k += 16 * VX) {
+          Vec<XT> t; t.load(row + k);
+#pragma unroll
+          for (int j = 0; j < VX; ++j) s += t.v[j];
+        }
+        mean = group_sum<16>(s) / (float)p.K;
+        float q = 0.f;
+        for (int k = l16 * VX; k < p.K; k += 16 * VX) {
+          Vec<XT> t; t.load(row + k);
+#pragma unroll
+          for (int j = 0; j < VX; ++j) { const float d = t.v[j] - mean; q += d * d; }
+        }
+        rstd = rsqrtf(group_sum<16>(q) / (float)p.K + p.eps);
+      }
+      if (l16 == 0) { s_mean[rr] = mean; s_rstd[rr] = rstd; }
+    }
+  }
+
+  // ---- staging: thread t owns row t/2 and 16 consecutive k ----------------
+  const int srow = tid >> 1, skh = (tid & 1) * 16;
+  const int xm = m0 + srow, wn = n0 + srow;
+  XStage<XT> xs;
+  uint4 wsr[2];
+  auto load_step = [&](int k0) {
+#pragma unroll
+    for (int c = 0; c < 16 / VX; ++c) {
+      const int k = k0 + skh + c * VX;
+      if (xm < p.rows && k < p.K) {
+        if constexpr (VX == 8) xs.d[c] = *reinterpret_cast<const uint4*>(x + (int64_t)xm * p.ldx + k);
+        else xs.d[c] = *reinterpret_cast<const float4*>(x + (int64_t)xm * p.ldx + k);
+      } else {
+        if constexpr (VX == 8) xs.d[c] = make_uint4(0, 0, 0, 0);
+        else xs.d[c] = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const int k = k0 + skh + c * 8;
+      wsr[c] = (wn < p.N && k < p.K) ? *reinterpret_cast<const uint4*>(p.w + (int64_t)wn * p.K + k)
+                                     : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto store_step = [&](int k0) {
+    float v[16];
+    if constexpr (VX == 8) {
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const uint32_t w4[4] = {xs.d[c].x, xs.d[c].y, xs.d[c].z, xs.d[c].w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          v[c * 8 + 2 * j] = __uint_as_float(w4[j] << 16);
+          v[c * 8 + 2 * j + 1] = __uint_as_float(w4[j] & 0xffff0000u);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        v[4 * c] = xs.d[c].x; v[4 * c + 1] = xs.d[c].y; v[4 * c + 2] = xs.d[c].z; v[4 * c + 3] = xs.d[c].w;
+      }
+    }
+    if (p.gamma) {
+      const float mu = s_mean[srow], rs = s_rstd[srow];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int k = k0 + skh + 4 * c;
+        if (k < p.K) {
+          const float4 ga = *reinterpret_cast<const float4*>(p.gamma + k);
+          const float4 be = p.beta ? *reinterpret_cast<const float4*>(p.beta + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+          v[4 * c + 0] = (v[4 * c + 0] - mu) * rs * ga.x + be.x;
+          v[4 * c + 1] = (v[4 * c + 1] - mu) * rs * ga.y + be.y;
+          v[4 * c + 2] = (v[4 * c + 2] - mu) * rs * ga.z + be.z;
+          v[4 * c + 3] = (v[4 * c + 3] - mu) * rs * ga.w + be.w;
+        } else {
+          v[4 * c] = v[4 * c + 1] = v[4 * c + 2] = v[4 * c + 3] = 0.f;
+        }
+      }
+      if (xm >= p.rows) {
+#pragma unroll
+        for (int j = 0; j < 16; ++j) v[j] = 0.f;
+      }
+    }
+    bf16x8 lo, hi;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) { lo[j] = (bf16)v[j]; hi[j] = (bf16)v[8 + j]; }
+    *reinterpret_cast<bf16x8*>(&Xs[srow * SK + skh]) = lo;
+    *reinterpret_cast<bf16x8*>(&Xs[srow * SK + skh + 8]) = hi;
+    *reinterpret_cast<uint4*>(&Ws[srow * SK + skh]) = wsr[0];
+    *reinterpret_cast<uint4*>(&Ws[srow * SK + skh + 8]) = wsr[1];
+  };
+
+  const int wn_off = (wave >> 1) * 64, wm_off = (wave & 1) * 64;
+  const bool wave_active = n0 + wn_off < p.N;
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  __syncthreads();                 // statistics visible
+  load_step(0);
+  store_step(0);
+  __syncthreads();
+  for (int k0 = 0; k0 < p.K; k0 += BK) {
+    const bool more = k0 + BK < p.K;
+    if (more) load_step(k0 + BK);
+    if (wave_active) {
+      bf16x8 af[4], bfr[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        af[t] = *reinterpret_cast<const bf16x8*>(&Ws[(wn_off + t * 16 + l16) * SK + g * 8]);
+        bfr[t] = *reinterpret_cast<const bf16x8*>(&Xs[(wm_off + t * 16 + l16) * SK + g * 8]);
+      }
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) acc[a][b] = mfma16(af[a], bfr[b], acc[a][b]);
+    }
+    __syncthreads();
+    if (more) {
+      store_step(k0 + BK);
+      __syncthreads();
+    }
+  }
+  if (!wave_active) return;
+
+  // ---- epilogue: lane owns channels n..n+3 of row m for every (a, b) tile --
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    const int m = m0 + wm_off + b * 16 + l16;
+    if (m >= p.rows) continue;
+    int64_t tpos = m;
+    if (p.y_tail && p.tail_mode != kTailChannelMajor && n0 + BN > p.n_main) tpos = pair_padded_pos(p, m);
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+      const int n = n0 + wn_off + a * 16 + g * 4;
+      if (n >= p.N) continue;
+      float r[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        r[i] = acc[a][b][i] + ((p.bias && n + i < p.N) ? p.bias[n + i] : 0.f);
+        if constexpr (EPI == NT_EPI_GELU) r[i] = gelu_erf(r[i]);
+      }
+      if (n + 4 <= p.n_main) {
+        if constexpr (EPI == NT_EPI_RESIDUAL) {
+          const uint2 rr = *reinterpret_cast<const uint2*>(p.res + (int64_t)m * p.ld_res + n);
+          r[0] += __uint_as_float(rr.x << 16); r[1] += __uint_as_float(rr.x & 0xffff0000u);
+          r[2] += __uint_as_float(rr.y << 16); r[3] += __uint_as_float(rr.y & 0xffff0000u);
+        }
+        bf16x4 o;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[i] = (bf16)r[i];
+        *reinterpret_cast<bf16x4*>(p.y + (int64_t)m * p.ldy + n) = o;
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int nn = n + i;
+          if (nn >= p.N) break;
+          if (nn < p.n_main) {
+            float v = r[i];
+            if constexpr (EPI == NT_EPI_RESIDUAL) v += (float)p.res[(int64_t)m * p.ld_res + nn];
+            p.y[(int64_t)m * p.ldy + nn] = (bf16)v;
+          } else {
+            p.y_tail[(int64_t)(nn - p.n_main) * p.ld_tail + tpos] = (bf16)r[i];
+          }
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------- SwiGLU
+// Pre-normalised SwiGLU transition (Eq. running-block, second line):
+//   y = res + (silu(LN(x) Wg^T + bg) * (LN(x) Wu^T + bu)) Wd^T + bd.
+// One workgroup owns 64*MT rows; each wave keeps its normalised rows as
+// matrix-core B fragments in registers, walks the hidden width in chunks of
+// 32, and feeds the gated hidden chunk straight from the first product's
+// accumulators into the second product (same lane layout), so the hidden
+// activations never leave registers.
+struct SwiArgs {
+  int rows, K, F, N;
+  const bf16* x;
+  int64_t ldx;
+  const float* gamma;
+  const float* beta;
+  float eps;
+  const bf16* w;       // [2F, K]: gate rows then up rows
+  const float* bias;   // [2F] or NULL
+  const bf16* w2;      // [N, F]
+  const float* bias2;  // [N] or NULL
+  const bf16* res;
+  int64_t ld_res;
+  bf16* y;
+  int64_t ldy;
+};
+
+template <int MT, int K, int N>
+__global__ void __launch_bounds__(256) swiglu_kernel(SwiArgs p) {
+  constexpr int RW = 4 * MT * 16;                 // rows per workgroup
+  constexpr int KMAX = K, NMAX = N;
+  constexpr int SD = 32 + 8;                      // LDS stride of the down-projection chunk
+  constexpr int SKW = K + 8, SKX = K + 8;         // LDS strides of weight / normalised rows
+  extern __shared__ __attribute__((aligned(16))) bf16 smem[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, g = lane >> 4;
+  const int m0 = blockIdx.x * RW;
+
+  // ---- prologue: LayerNorm of the workgroup's rows into LDS --------------
+  bf16* Xn = smem;                                 // [RW][SKX]
+  for (int rr = tid >> 4; rr < RW; rr += 16) {
+    const int m = m0 + rr;
+    float v[2][8];
+    float s = 0.f;
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const int k = (l16 + 16 * c) * 8;
+      if (m < p.rows && k < K) {
+        Vec<bf16> t; t.load(p.x + (int64_t)m * p.ldx + k);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) { v[c][j] = t.v[j]; s += t.v[j]; }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[c][j] = 0.f;
+      }
+    }
+    const float mean = group_sum<16>(s) / (float)K;
+    float q = 0.f;
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const int k = (l16 + 16 * c) * 8;
+      if (k < K) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) { const float d = v[c][j] - mean; q += d * d; }
+      }
+    }
+    const float rstd = rsqrtf(group_sum<16>(q) / (float)K + p.eps);
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const int k = (l16 + 16 * c) * 8;
+      if (k < K) {
+        bf16x8 o;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          float t = (v[c][j] - mean) * rstd;
+          if (p.gamma) t = t * p.gamma[k + j] + (p.beta ? p.beta[k + j] : 0.f);
+          o[j] = (bf16)(m < p.rows ? t : 0.f);
+        }
+        *reinterpret_cast<bf16x8*>(&Xn[rr * SKX + k]) = o;
+      }
+    }
+  }
+  __syncthreads();
+  constexpr int KT = K / 32;
+  bf16x8 xf[MT][KMAX / 32];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int kk = 0; kk < KMAX / 32; ++kk)
+      if (kk < KT) xf[mt][kk] = *reinterpret_cast<const bf16x8*>(&Xn[(wave * MT * 16 + mt * 16 + l16) * SKX + kk * 32 + g * 8]);
+  __syncthreads();                                 // Xn is reused for weight chunks
+
+  bf16* Wg = smem;                                 // [32][SKW]
+  bf16* Wu = smem + 32 * SKW;                      // [32][SKW]
+  bf16* Wd = smem + 64 * SKW;                      // [N][SD]
+  constexpr int NT = N / 16;
+  f32x4 accY[NMAX / 16][MT];
+#pragma unroll
+  for (int a = 0; a < NMAX / 16; ++a)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) accY[a][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // staging assignment: gate/up chunks = 64 rows x K/8 vectors, down chunk = N rows x 4 vectors
+  constexpr int gu_vecs = 64 * (K / 8), d_vecs = N * 4;
+  for (int f0 = 0; f0 < p.F; f0 += 32) {
+    for (int t = tid; t < gu_vecs; t += 256) {
+      const int r = t / (K / 8), kc = (t % (K / 8)) * 8;
+      const int wrow = r < 32 ? f0 + r : p.F + f0 + (r - 32);
+      const uint4 d = *reinterpret_cast<const uint4*>(p.w + (int64_t)wrow * K + kc);
+      *reinterpret_cast<uint4*>(&smem[r * SKW + kc]) = d;
+    }
+    for (int t = tid; t < d_vecs; t += 256) {
+      const int n = t >> 2, fc = (t & 3) * 8;
+      const uint4 d = *reinterpret_cast<const uint4*>(p.w2 + (int64_t)n * p.F + f0 + fc);
+      *reinterpret_cast<uint4*>(&Wd[n * SD + fc]) = d;
+    }
+    __syncthreads();
+
+    f32x4 accG[2][MT], accU[2][MT];
+#pragma unroll
+    for (int ft = 0; ft < 2; ++ft)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) { accG[ft][mt] = f32x4{0.f, 0.f, 0.f, 0.f}; accU[ft][mt] = accG[ft][mt]; }
+#pragma unroll
+    for (int kk = 0; kk < KMAX / 32; ++kk) {
+      if (kk >= KT) break;
+#pragma unroll
+      for (int ft = 0; ft < 2; ++ft) {
+        const bf16x8 ag = *reinterpret_cast<const bf16x8*>(&Wg[(ft * 16 + l16) * SKW + kk * 32 + g * 8]);
+        const bf16x8 au = *reinterpret_cast<const bf16x8*>(&Wu[(ft * 16 + l16) * SKW + kk * 32 + g * 8]);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          accG[ft][mt] = mfma16(ag, xf[mt][kk], accG[ft][mt]);
+          accU[ft][mt] = mfma16(au, xf[mt][kk], accU[ft][mt]);
+        }
+      }
+    }
+    // gated hidden chunk, in the B-operand layout of the second product:
+    // element j < 4 is hidden f0 + 4g + j, element j >= 4 is f0 + 16 + 4g + (j-4)
+    float bgv[8], buv[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int f = f0 + (j < 4 ? 4 * g + j : 16 + 4 * g + (j - 4));
+      bgv[j] = p.bias ? p.bias[f] : 0.f;
+      buv[j] = p.bias ? p.bias[p.F + f] : 0.f;
+    }
+    bf16x8 hv[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int ft = j >> 2, i = j & 3;
+        const float gv = accG[ft][mt][i] + bgv[j];
+        const float uv = accU[ft][mt][i] + buv[j];
+        hv[mt][j] = (bf16)(gv / (1.f + __expf(-gv)) * uv);
+      }
+#pragma unroll
+    for (int a = 0; a < NMAX / 16; ++a) {
+      if (a >= NT) break;
+      const bf16x4 lo = *reinterpret_cast<const bf16x4*>(&Wd[(a * 16 + l16) * SD + 4 * g]);
+      const bf16x4 hi = *reinterpret_cast<const bf16x4*>(&Wd[(a * 16 + l16) * SD + 16 + 4 * g]);
+      const bf16x8 ad = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) accY[a][mt] = mfma16(ad, hv[mt], accY[a][mt]);
+    }
+    __syncthreads();
+  }
+
+  // ---- epilogue: residual + bias, lane owns channels n..n+3 of row m ------
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    const int m = m0 + wave * MT * 16 + mt * 16 + l16;
+    if (m >= p.rows) continue;
+#pragma unroll
+    for (int a = 0; a < NMAX / 16; ++a) {
+      if (a >= NT) break;
+      const int n = a * 16 + 4 * g;
+      const uint2 rr = *reinterpret_cast<const uint2*>(p.res + (int64_t)m * p.ld_res + n);
+      const float rv[4] = {__uint_as_float(rr.x << 16), __uint_as_float(rr.x & 0xffff0000u),
+                           __uint_as_float(rr.y << 16), __uint_as_float(rr.y & 0xffff0000u)};
+      bf16x4 o;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) o[i] = (bf16)(accY[a][mt][i] + (p.bias2 ? p.bias2[n + i] : 0.f) + rv[i]);
+      *reinterpret_cast<bf16x4*>(p.y + (int64_t)m * p.ldy + n) = o;
+    }
+  }
+}
+
+// ---------------------------------------------------------------- fp32 path
+// Plain fp32 FMA path (used by the fp32 workloads): RB rows per workgroup, one
+// wave normalises each row into LDS, then threads compute output channels.
+constexpr int RB = 4;
+
+struct F32Args {
+  int rows, K, N, n_main, F, epi;
+  const float* x;
+  int64_t ldx;
+  const float* gamma;
+  const float* beta;
+  float eps;
+  const float* w;
+  const float* bias;
+  const float* w2;
+  const float* bias2;
+  const float* res;
+  int64_t ld_res;
+  float* y;
+  int64_t ldy;
+  float* y_tail;
+  int64_t ld_tail;
+  LinArgs pair;         // only the pair-padded tail fields are used
+};
+
+__global__ void __launch_bounds__(256) linear_f32_kernel(F32Args p) {
+  extern __shared__ float fsm[];
+  float* xs = fsm;                      // [RB][K]
+  float* hs = fsm + RB * p.K;           // [RB][F] (SwiGLU only)
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int m0 = blockIdx.x * RB;
+  {
+    const int r = wave, m = m0 + r;
+    if (m < p.rows) {
+      const float* row = p.x + (int64_t)m * p.ldx;
+      float mean = 0.f, rstd = 1.f;
+      if (p.gamma) {
+        float s = 0.f;
+        for (int k = lane; k < p.K; k += 64) s += row[k];
+        mean = group_sum<64>(s) / (float)p.K;
+        float q = 0.f;
+        for (int k = lane; k < p.K; k += 64) { const float d = row[k] - mean; q += d * d; }
+        rstd = 1.f / sqrtf(group_sum<64>(q) / (float)p.K + p.eps);
+      }
+      for (int k = lane; k < p.K; k += 64)
+        xs[r * p.K + k] = p.gamma ? (row[k] - mean) * rstd * p.gamma[k] + (p.beta ? p.beta[k] : 0.f) : row[k];
+    }
+  }
+  __syncthreads();
+  if (p.epi == NT_EPI_SWIGLU_RESIDUAL) {
+    for (int idx = tid; idx < RB * p.F; idx += 256) {
+      const int r = idx / p.F, f = idx % p.F;
+      if (m0 + r >= p.rows) continue;
+      float gsum = p.bias ? p.bias[f] : 0.f, usum = p.bias ? p.bias[p.F + f] : 0.f;
+      const float* wg = p.w + (int64_t)f * p.K;
+      const float* wu = p.w + (int64_t)(p.F + f) * p.K;
+      for (int k = 0; k < p.K; ++k) { gsum = fmaf(xs[r * p.K + k], wg[k], gsum); usum = fmaf(xs[r * p.K + k], wu[k], usum); }
+      hs[r * p.F + f] = gsum / (1.f + expf(-gsum)) * usum;
+    }
+    __syncthreads();
+    for (int idx = tid; idx < RB * p.N; idx += 256) {
+      const int r = idx / p.N, n = idx % p.N, m = m0 + r;
+      if (m >= p.rows) continue;
+      float s = p.bias2 ? p.bias2[n] : 0.f;
+      const float* wd = p.w2 + (int64_t)n * p.F;
+      for (int f = 0; f < p.F; ++f) s = fmaf(hs[r * p.F + f], wd[f], s);
+      p.y[(int64_t)m * p.ldy + n] = p.res[(int64_t)m * p.ld_res + n] + s;
+    }
+    return;
+  }
+  for (int idx = tid; idx < RB * p.N; idx += 256) {
+    const int r = idx / p.N, n = idx % p.N, m = m0 + r;
+    if (m >= p.rows) continue;
+    float s = p.bias ? p.bias[n] : 0.f;
+    const float* wr = p.w + (int64_t)n * p.K;
+    for (int k = 0; k < p.K; ++k) s = fmaf(xs[r * p.K + k], wr[k], s);
+    if (p.epi == NT_EPI_GELU) s = 0.5f * s * (1.f + erff(s * 0.70710678118654752f));
+    if (n < p.n_main) {
+      if (p.epi == NT_EPI_RESIDUAL) s += p.res[(int64_t)m * p.ld_res + n];
+      p.y[(int64_t)m * p.ldy + n] = s;
+    } else {
+      const int64_t pos = p.pair.tail_mode == kTailChannelMajor ? (int64_t)m : pair_padded_pos(p.pair, m);
+      p.y_tail[(int64_t)(n - p.n_main) * p.ld_tail + pos] = s;
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
+  const nt_linear_args& a = *plan.a;
+  const int rows = (int)a.rows;
+  if (rows == 0) return hipSuccess;
+  LinArgs p{};
+  p.rows = rows; p.K = a.c_in; p.N = a.c_out; p.n_main = a.c_out - a.n_tail;
+  p.x = a.x; p.ldx = a.ldx; p.gamma = a.ln_gamma; p.beta = a.ln_beta; p.eps = a.ln_eps;
+  p.w = (const bf16*)a.w; p.bias = a.bias;
+  p.res = (const bf16*)a.residual; p.ld_res = a.ld_residual;
+  p.y = (bf16*)a.y; p.ldy = a.ldy;
+  p.y_tail = (bf16*)a.y_tail; p.ld_tail = a.ld_tail; p.tail_mode = plan.tail_mode;
+  if (plan.layout && plan.layout->has_device) {
+    p.row_splits2 = plan.layout->d_row_splits2; p.row_sample = plan.layout->d_row_sample;
+    p.cu_seqlens = plan.layout->d_cu_seqlens; p.cu_pad = plan.layout->d_cu_pad;
+    p.sum_n = (int)plan.layout->sum_n;
+  }
+  if (a.n_tail == 0) p.y_tail = nullptr;
+
+  if (a.dtype == NT_F32) {
+    F32Args f{};
+    f.rows = rows; f.K = a.c_in; f.N = a.c_out; f.n_main = p.n_main; f.F = a.hidden; f.epi = a.epilogue;
+    f.x = (const float*)a.x; f.ldx = a.ldx; f.gamma = a.ln_gamma; f.beta = a.ln_beta; f.eps = a.ln_eps;
+    f.w = (const float*)a.w; f.bias = a.bias; f.w2 = (const float*)a.w2; f.bias2 = a.bias2;
+    f.res = a.residual ? (const float*)a.residual : (const float*)a.x;
+    f.ld_res = a.residual ? a.ld_residual : a.ldx;
+    f.y = (float*)a.y; f.ldy = a.ldy; f.y_tail = (float*)a.y_tail; f.ld_tail = a.ld_tail; f.pair = p;
+    const size_t smem = sizeof(float) * RB * ((size_t)a.c_in + (a.epilogue == NT_EPI_SWIGLU_RESIDUAL ? a.hidden : 0));
+    linear_f32_kernel<<<dim3((rows + RB - 1) / RB), dim3(256), smem, s>>>(f);
+    return hipGetLastError();
+  }
+
+  if (a.epilogue == NT_EPI_SWIGLU_RESIDUAL) {
+    SwiArgs w{};
+    w.rows = rows; w.K = a.c_in; w.F = a.hidden; w.N = a.c_out;
+    w.x = (const bf16*)a.x; w.ldx = a.ldx; w.gamma = a.ln_gamma; w.beta = a.ln_beta; w.eps = a.ln_eps;
+    w.w = (const bf16*)a.w; w.bias = a.bias; w.w2 = (const bf16*)a.w2; w.bias2 = a.bias2;
+    w.res = a.residual ? (const bf16*)a.residual : (const bf16*)a.x;
+    w.ld_res = a.residual ? a.ld_residual : a.ldx;
+    w.y = (bf16*)a.y; w.ldy = a.ldy;
+    constexpr int MT = 2;
+    const int rw = 4 * MT * 16;
+    const size_t xn = (size_t)rw * (a.c_in + 8);
+    const size_t wc = (size_t)64 * (a.c_in + 8) + (size_t)a.c_out * 40;
+    const size_t smem = sizeof(bf16) * (xn > wc ? xn : wc);
+    const dim3 grid((rows + rw - 1) / rw);
+    if (a.c_in == 64 && a.c_out == 64) swiglu_kernel<MT, 64, 64><<<grid, dim3(256), smem, s>>>(w);
+    else if (a.c_in == 128 && a.c_out == 128) swiglu_kernel<MT, 128, 128><<<grid, dim3(256), smem, s>>>(w);
+    else if (a.c_in == 256 && a.c_out == 256) swiglu_kernel<MT, 256, 256><<<grid, dim3(256), smem, s>>>(w);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
+  }
+
+  p.mblocks = (rows + BM - 1) / BM;
+  p.nblocks = (a.c_out + BN - 1) / BN;
+  const unsigned grid = (unsigned)(((p.mblocks + kXcds - 1) / kXcds) * kXcds * p.nblocks);
+  const bool xf32 = a.x_dtype == NT_F32;
+#define NT_LAUNCH_LIN(XT, EPI) linear_mfma_kernel<XT, EPI><<<dim3(grid), dim3(256), 0, s>>>(p)
+  switch (a.epilogue) {
+    case NT_EPI_NONE: if (xf32) NT_LAUNCH_LIN(float, NT_EPI_NONE); else NT_LAUNCH_LIN(bf16, NT_EPI_NONE); break;
+    case NT_EPI_RESIDUAL: if (xf32) NT_LAUNCH_LIN(float, NT_EPI_RESIDUAL); else NT_LAUNCH_LIN(bf16, NT_EPI_RESIDUAL); break;
+    case NT_EPI_GELU: if (xf32) NT_LAUNCH_LIN(float, NT_EPI_GELU); else NT_LAUNCH_LIN(bf16, NT_EPI_GELU); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef NT_LAUNCH_LIN
+  return hipGetLastError();
+}
+
+}  // namespace nt

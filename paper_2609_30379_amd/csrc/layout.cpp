@@ -1,0 +1,153 @@
+// Layout planner: partitions and tile-to-sample work maps of a batch of square
+// pair states (Sec. 3.1 "Structural metadata", Fig. "representation",
+// Appendix A "Structural invariants"), built on the host from the per-sample
+// lengths.  Pure C++: the same code is exercised by host-only layouts.
+#include <algorithm>
+#include <array>
+#include <climits>
+#include <numeric>
+
+#include "nt_internal.h"
+
+namespace nt {
+namespace {
+
+// Orders work items for launch so that the item at position p is executed by
+// XCD p % 8 (MI355X dispatches workgroups of one launch round-robin over its
+// 8 XCDs).  Items of one sample are kept on as few XCDs as possible, so
+// per-sample operands (pair bias, triangle rows) are reused from one L2, and
+// the summed cost per XCD is balanced.  Idle positions are filled with -1.
+template <int W>
+std::vector<int32_t> xcd_order(const std::vector<std::array<int32_t, W>>& items,
+                               const std::vector<double>& cost) {
+  const size_t n = items.size();
+  std::vector<size_t> idx(n);
+  std::iota(idx.begin(), idx.end(), 0);
+  // per-sample totals; items arrive grouped by sample (field 0)
+  std::vector<double> sample_cost;
+  for (size_t t = 0; t < n; ++t) {
+    const int32_t s = items[t][0];
+    if ((int32_t)sample_cost.size() <= s) sample_cost.resize(s + 1, 0.0);
+    sample_cost[s] += cost[t];
+  }
+  std::stable_sort(idx.begin(), idx.end(), [&](size_t a, size_t b) {
+    const double ca = sample_cost[items[a][0]], cb = sample_cost[items[b][0]];
+    if (ca != cb) return ca > cb;
+    return items[a][0] < items[b][0];
+  });
+  double total = 0.0;
+  for (double c : cost) total += c;
+  const double quota = total / kXcds;
+  std::array<std::vector<size_t>, kXcds> q;
+  std::array<double, kXcds> load{};
+  int x = 0;
+  for (size_t t : idx) {
+    if (x < kXcds - 1 && load[x] >= quota * (1.0 - 1e-12) && load[x] > 0.0) ++x;
+    q[x].push_back(t);
+    load[x] += cost[t];
+  }
+  size_t depth = 0;
+  for (auto& v : q) {
+    std::stable_sort(v.begin(), v.end(), [&](size_t a, size_t b) { return cost[a] > cost[b]; });
+    depth = std::max(depth, v.size());
+  }
+  std::vector<int32_t> out(depth * kXcds * W, -1);
+  for (size_t k = 0; k < depth; ++k)
+    for (int xx = 0; xx < kXcds; ++xx)
+      if (k < q[xx].size()) {
+        const auto& it = items[q[xx][k]];
+        for (int f = 0; f < W; ++f) out[(k * kXcds + xx) * W + f] = it[f];
+      }
+  return out;
+}
+
+}  // namespace
+
+nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L) {
+  if (!lengths) return fail(NT_ERR_INVALID_ARG, "lengths is NULL");
+  if (batch < 1) return fail(NT_ERR_INVALID_ARG, "batch must be >= 1");
+  L->batch = batch;
+  L->lengths.assign(lengths, lengths + batch);
+  L->cu_seqlens.assign(batch + 1, 0);
+  L->cu_pairs.assign(batch + 1, 0);
+  L->cu_pad.assign(batch + 1, 0);
+  int64_t sn = 0, sn2 = 0, sn3 = 0, spad = 0;
+  int32_t mx = 0;
+  for (int32_t i = 0; i < batch; ++i) {
+    const int64_t n = lengths[i];
+    if (n < 0) return fail(NT_ERR_INVALID_ARG, "negative length at sample " + std::to_string(i));
+    sn += n;
+    sn2 += n * n;
+    sn3 += n * n * n;
+    spad += n * ((n + 7) / 8 * 8);
+    if (sn > INT32_MAX || sn2 > INT32_MAX || spad > INT32_MAX)
+      return fail(NT_ERR_OVERFLOW, "packed pair extent exceeds int32 at sample " + std::to_string(i));
+    L->cu_seqlens[i + 1] = (int32_t)sn;
+    L->cu_pairs[i + 1] = (int32_t)sn2;
+    L->cu_pad[i + 1] = (int32_t)spad;
+    mx = std::max<int32_t>(mx, (int32_t)n);
+  }
+  L->sum_n = sn;
+  L->sum_n2 = sn2;
+  L->sum_n3 = sn3;
+  L->sum_pad = spad;
+  L->max_len = mx;
+
+  // level-2 row splits: o_i + a N_i for every pair row, then the total
+  L->row_splits2.assign(sn + 1, 0);
+  L->row_sample.assign(sn, 0);
+  for (int32_t i = 0; i < batch; ++i) {
+    const int32_t n = lengths[i];
+    for (int32_t a = 0; a < n; ++a) {
+      const int64_t eta = (int64_t)L->cu_seqlens[i] + a;
+      L->row_splits2[eta] = L->cu_pairs[i] + a * n;
+      L->row_sample[eta] = i;
+    }
+  }
+  L->row_splits2[sn] = (int32_t)sn2;
+
+  // pair-row attention: one item per (sample, pair row), cost N_i^2
+  {
+    std::vector<std::array<int32_t, 2>> items;
+    std::vector<double> cost;
+    items.reserve(sn);
+    for (int32_t i = 0; i < batch; ++i)
+      for (int32_t r = 0; r < lengths[i]; ++r) {
+        items.push_back({i, r});
+        cost.push_back((double)lengths[i] * lengths[i]);
+      }
+    L->attn_work = xcd_order<2>(items, cost);
+  }
+  // triangle: one item per (sample, 32x32 output tile), cost = valid x * valid y * N
+  {
+    std::vector<std::array<int32_t, 4>> items;
+    std::vector<double> cost;
+    for (int32_t i = 0; i < batch; ++i) {
+      const int32_t n = lengths[i], nt = (n + kTriTile - 1) / kTriTile;
+      for (int32_t xt = 0; xt < nt; ++xt)
+        for (int32_t yt = 0; yt < nt; ++yt) {
+          items.push_back({i, xt, yt, 0});
+          const double vx = std::min(kTriTile, n - xt * kTriTile);
+          const double vy = std::min(kTriTile, n - yt * kTriTile);
+          cost.push_back(vx * vy * n);
+        }
+    }
+    L->tri_work = xcd_order<4>(items, cost);
+  }
+  // 1-D attention: one item per (sample, block of kSeqQBlock queries), cost = queries * N_i
+  {
+    std::vector<std::array<int32_t, 2>> items;
+    std::vector<double> cost;
+    for (int32_t i = 0; i < batch; ++i) {
+      const int32_t n = lengths[i];
+      for (int32_t qb = 0; qb * kSeqQBlock < n; ++qb) {
+        items.push_back({i, qb});
+        cost.push_back((double)std::min(kSeqQBlock, n - qb * kSeqQBlock) * n);
+      }
+    }
+    L->seq_work = xcd_order<2>(items, cost);
+  }
+  return NT_OK;
+}
+
+}  // namespace nt

@@ -1,0 +1,99 @@
+// Host-side internals shared by the C ABI, the layout planner and the kernel
+// launchers.  Not part of the public interface.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "nt.h"
+
+namespace nt {
+
+constexpr int kXcds = 8;          // MI355X: 8 XCDs, workgroups dispatched round-robin
+constexpr int kTriTile = 32;      // triangle output tile: 32 x 32 cells
+constexpr int kSeqQBlock = 64;    // 1-D attention: queries per workgroup
+
+// Attention limits imposed by staging a whole key segment in LDS.
+constexpr int kAttnMaxLenD32 = 1024;
+constexpr int kAttnMaxLenD64 = 512;
+
+}  // namespace nt
+
+// Opaque layout object (see nt.h).  Host arrays are the canonical copies;
+// device mirrors live in one allocation.
+struct nt_layout {
+  int32_t batch = 0;
+  int32_t max_len = 0;
+  int64_t sum_n = 0, sum_n2 = 0, sum_n3 = 0;
+  int64_t sum_pad = 0;             // sum_i N_i * round_up(N_i, 8)
+
+  std::vector<int32_t> lengths;      // [B]
+  std::vector<int32_t> cu_seqlens;   // [B+1]
+  std::vector<int32_t> cu_pairs;     // [B+1]
+  std::vector<int32_t> cu_pad;       // [B+1] offsets of the padded channel-major operand blocks
+  std::vector<int32_t> row_splits2;  // [sum N + 1]
+  std::vector<int32_t> row_sample;   // [sum N]
+  std::vector<int32_t> attn_work;    // pairs (sample, row); count multiple of 8; (-1,-1) = idle
+  std::vector<int32_t> tri_work;     // quads (sample, xt, yt, 0); count multiple of 8
+  std::vector<int32_t> seq_work;     // pairs (sample, query block); count multiple of 8
+
+  bool has_device = false;
+  int device = -1;
+  void* d_base = nullptr;
+  const int32_t* d_lengths = nullptr;
+  const int32_t* d_cu_seqlens = nullptr;
+  const int32_t* d_cu_pairs = nullptr;
+  const int32_t* d_cu_pad = nullptr;
+  const int32_t* d_row_splits2 = nullptr;
+  const int32_t* d_row_sample = nullptr;
+  const int32_t* d_attn_work = nullptr;
+  const int32_t* d_tri_work = nullptr;
+  const int32_t* d_seq_work = nullptr;
+
+  int64_t attn_items() const { return (int64_t)attn_work.size() / 2; }
+  int64_t tri_items() const { return (int64_t)tri_work.size() / 4; }
+  int64_t seq_items() const { return (int64_t)seq_work.size() / 2; }
+};
+
+namespace nt {
+
+// Sets the thread-local error message and returns the status.
+nt_status fail(nt_status s, const std::string& msg);
+
+// ---- kernel launchers (return hipGetLastError() after the launch) ----------
+
+hipError_t launch_pair_broadcast(const nt_layout& L, int C, const void* u, int64_t ld_u,
+                                 const void* v, int64_t ld_v, void* z, int64_t ld_z,
+                                 int accumulate, nt_dtype dtype, hipStream_t s);
+
+hipError_t launch_segment_reduce(const nt_layout& L, nt_level level, int op, int C,
+                                 const void* x, int64_t ld_x, nt_dtype x_dtype,
+                                 float* y, int64_t ld_y, hipStream_t s);
+
+// Tail output modes of the projection (columns routed to y_tail).
+enum TailMode { kTailChannelMajor = 0, kTailPairPadded = 1, kTailPairPaddedT = 2 };
+
+struct LinearPlan {
+  const nt_linear_args* a;
+  int tail_mode;
+  const nt_layout* layout;   // for pair-padded tail modes
+};
+hipError_t launch_linear(const LinearPlan& p, hipStream_t s);
+
+hipError_t launch_attention(const nt_layout& L, int axis, int H, int D,
+                            const void* q, const void* k, const void* v, int64_t ld_qkv,
+                            const void* bias, int64_t ld_bias, float scale,
+                            void* o, int64_t ld_o, nt_dtype dtype, hipStream_t s);
+
+hipError_t launch_triangle(const nt_layout& L, int C, const void* a, const void* b,
+                           int64_t ld_ab, void* z, int64_t ld_z, nt_dtype dtype,
+                           hipStream_t s);
+
+// Host-side planner (pure C++; no HIP calls).  Fills every host array of the
+// layout from the lengths, or returns an error status.
+nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L);
+
+}  // namespace nt

@@ -44,6 +44,7 @@ class Workload:
     col_attention: bool = False
     single_update: bool = True
     gains: dict = field(default_factory=dict, compare=False, hash=False)
+    steps: tuple = ()          # ordered steps of one block (pair workloads)
 
 
 def _pair_gains(n_max: int, blocks: int = 1) -> dict:
@@ -55,29 +56,39 @@ def _pair_gains(n_max: int, blocks: int = 1) -> dict:
         "lin": 0.5,               # LayerNorm+Linear that replaces z
         "qkv": 0.5, "bias": 0.6,  # attention projections
         "o": 0.5 * damp,          # attention output projection (residual)
-        # a, b std g so that t = sum_k a b has std ~0.3 for N = n_max
-        "ab": float(np.sqrt(0.3 / np.sqrt(n_max))) * np.sqrt(damp),
+        # pair states built by broadcasting are rank-structured, so the
+        # triangle sum over k is coherent and grows like N: a, b get gain
+        # sqrt(0.3 / n_max) to keep t = sum_k a b of order 0.3
+        "ab": float(np.sqrt(0.3 / n_max)) * np.sqrt(damp),
         "gu": 1.0, "d": 0.25 * damp,   # SwiGLU transition
         "s": 0.5,                 # single update from the column mean
     }
 
 
+# Block step sequences: the tiny block (broadcast, LayerNorm+Linear, row
+# attention, triangle), the single pair block (plus the SwiGLU transition) and
+# the Pairformer-style stack block; every block ends with the column mean back
+# to the single track (Eq. running-block, third line).
+_TINY = ("bcast", "lin", "att_row", "tri_out", "single")
+_BLOCK = ("bcast", "lin", "att_row", "tri_out", "trans", "single")
+_STACK = ("bcast", "tri_out", "tri_in", "att_row", "att_col", "trans", "single")
+
 WORKLOADS = {
     w.name: w for w in [
         Workload("pair_tiny_f32_b4", "pair", 4, ("uniform", 4, 16), 0, "f32",
                  c_s=32, c_z=16, heads=2, head_dim=8, hidden=64,
-                 transition=False, gains=_pair_gains(16)),
+                 transition=False, gains=_pair_gains(16), steps=_TINY),
         Workload("pair_b8_n208_224_bf16", "pair", 8, ("uniform", 208, 224), 0, "bf16",
                  c_s=384, c_z=128, heads=4, head_dim=32, hidden=512,
-                 gains=_pair_gains(224)),
+                 gains=_pair_gains(224), steps=_BLOCK),
         Workload("pair_b8_n32_512_bf16", "pair", 8, ("uniform", 32, 512), 1, "bf16",
                  c_s=384, c_z=128, heads=4, head_dim=32, hidden=512,
-                 gains=_pair_gains(512)),
+                 gains=_pair_gains(512), steps=_BLOCK),
         Workload("pairformer4_b16_lognormal192_bf16", "pair", 16,
                  ("lognormal", 192.0, 0.6, 16, 768), 0, "bf16",
                  c_s=384, c_z=128, heads=4, head_dim=32, hidden=512, blocks=4,
                  tri_incoming=True, col_attention=True,
-                 gains=_pair_gains(768, blocks=4)),
+                 gains=_pair_gains(768, blocks=4), steps=_STACK),
         Workload("tokens_b64_lognormal230_bf16", "tokens", 64,
                  ("lognormal", 230.0, 0.5, 16, 512), 0, "bf16",
                  c_s=768, heads=12, head_dim=64, hidden=3072,

@@ -1,0 +1,156 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads and
+exports every declared symbol, host-only layouts match the oracle's offsets bit
+for bit, the work maps cover every item exactly once with balanced XCD loads,
+and argument errors are reported before any device work."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import layout as OL
+from paper_2609_30379_amd import binding as B
+from paper_2609_30379_amd import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return B.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    hdr = open(os.path.join(ROOT, "include", "nt.h")).read()
+    names = set(re.findall(r"^\s*(?:nt_status|int32_t|const char\*)\s+(nt_\w+)\s*\(", hdr, re.M))
+    assert len(names) >= 12
+    for n in sorted(names):
+        assert hasattr(lib, n), f"libnt.so does not export {n}"
+    assert B.version().startswith("nt-mi355x")
+
+
+LENGTH_CASES = [[2, 3], [15, 12, 10, 7], [5, 0, 1, 37, 64, 3, 70], [0], [1], [0, 0, 4]]
+
+
+@pytest.mark.parametrize("L", LENGTH_CASES + [synth.lengths_for(w).tolist() for w in synth.WORKLOADS.values()])
+def test_host_layout_matches_oracle(L):
+    lay = B.NestedLayout(L, host_only=True)
+    assert lay.host_array("lengths").tolist() == list(L)
+    assert lay.host_array("cu_seqlens").tolist() == OL.single_offsets(L).tolist()
+    assert lay.host_array("cu_pairs").tolist() == OL.pair_offsets(L).tolist()
+    assert lay.host_array("row_splits2").tolist() == OL.pair_row_splits(L)[1].tolist()
+    n8 = [(n + 7) // 8 * 8 for n in L]
+    assert lay.host_array("cu_pad").tolist() == OL.offsets([n * m for n, m in zip(L, n8)]).tolist()
+    rs = lay.host_array("row_sample")
+    assert rs.tolist() == [i for i, n in enumerate(L) for _ in range(n)]
+    assert (lay.sum_n, lay.sum_n2, lay.sum_n3) == (sum(L), sum(n * n for n in L), sum(n ** 3 for n in L))
+    assert lay.max_len == max(L)
+
+
+def _xcd_loads(items, cost):
+    loads = np.zeros(8)
+    for p, it in enumerate(items):
+        if it[0] >= 0:
+            loads[p % 8] += cost(it)
+    return loads
+
+
+@pytest.mark.parametrize("L", [[15, 12, 10, 7], [259, 278, 395, 489, 48, 101, 427, 488], [5, 0, 1, 37, 64, 3, 70],
+                               synth.lengths_for(synth.WORKLOADS["pairformer4_b16_lognormal192_bf16"]).tolist()])
+def test_work_maps_cover_each_item_once(L):
+    lay = B.NestedLayout(L, host_only=True)
+    att = lay.host_array("attn_work").reshape(-1, 2)
+    assert len(att) % 8 == 0
+    got = sorted(map(tuple, att[att[:, 0] >= 0].tolist()))
+    assert got == sorted((i, r) for i, n in enumerate(L) for r in range(n))
+    tri = lay.host_array("tri_work").reshape(-1, 4)
+    assert len(tri) % 8 == 0
+    got = sorted(map(tuple, tri[tri[:, 0] >= 0, :3].tolist()))
+    T = 32
+    assert got == sorted((i, x, y) for i, n in enumerate(L) for x in range(-(-n // T)) for y in range(-(-n // T)))
+    seq = lay.host_array("seq_work").reshape(-1, 2)
+    got = sorted(map(tuple, seq[seq[:, 0] >= 0].tolist()))
+    assert got == sorted((i, q) for i, n in enumerate(L) for q in range(-(-n // 64)))
+    # balanced XCD loads: no XCD above the mean by more than one sample's largest item
+    loads = _xcd_loads(att.tolist(), lambda it: L[it[0]] ** 2)
+    assert loads.max() - loads.mean() <= max(L) ** 2 + 1e-9
+
+
+def test_uniform_batch_puts_each_sample_on_its_own_xcd():
+    L = synth.lengths_for(synth.WORKLOADS["pair_b8_n208_224_bf16"]).tolist()
+    att = B.NestedLayout(L, host_only=True).host_array("attn_work").reshape(-1, 2)
+    xcd_samples = [set(att[p::8, 0].tolist()) - {-1} for p in range(8)]
+    assert all(len(s) <= 2 for s in xcd_samples)
+
+
+def test_layout_errors():
+    with pytest.raises(B.NtError) as e:
+        B.NestedLayout([3, -1], host_only=True)
+    assert e.value.status == B.NT_ERR_INVALID_ARG
+    with pytest.raises(B.NtError) as e:
+        B.NestedLayout([46341], host_only=True)            # 46341^2 > INT32_MAX
+    assert e.value.status == B.NT_ERR_OVERFLOW
+    with pytest.raises(B.NtError) as e:
+        B.NestedLayout([], host_only=True)
+    assert e.value.status == B.NT_ERR_INVALID_ARG
+    with pytest.raises(B.NtError) as e:
+        B.NestedLayout([0, 3, 2], host_only=True, offsets=True)   # decreasing offsets
+    assert e.value.status == B.NT_ERR_INVALID_ARG
+    with pytest.raises(B.NtError):
+        B.NestedLayout([1, 3, 5], host_only=True, offsets=True)   # o_0 != 0
+    lay = B.NestedLayout([0, 2, 5], host_only=True, offsets=True)
+    assert lay.host_array("lengths").tolist() == [2, 3]
+
+
+def test_compatibility_distinguishes_equal_totals():
+    # (3,4) and (4,3) hold the same 7 singles and 25 pair cells but differ per sample
+    a = B.NestedLayout([3, 4], host_only=True)
+    b = B.NestedLayout([4, 3], host_only=True)
+    c = B.NestedLayout([3, 4], host_only=True)
+    assert (a.sum_n, a.sum_n2) == (b.sum_n, b.sum_n2)
+    assert not a.compatible(b)
+    assert a.compatible(c)
+
+
+def _linear_args(**kw):
+    a = B.LinearArgs()
+    a.rows, a.c_in, a.c_out, a.dtype, a.x_dtype = 16, 16, 16, B.NT_BF16, B.NT_BF16
+    a.x, a.w, a.y = C.c_void_p(0x1000), C.c_void_p(0x2000), C.c_void_p(0x3000)
+    a.ldx, a.ldy = 16, 16
+    for k, v in kw.items():
+        setattr(a, k, v)
+    return a
+
+
+def test_op_argument_errors_need_no_device(lib):
+    host = B.NestedLayout([3, 4], host_only=True)
+    other = B.NestedLayout([4, 3], host_only=True)
+    # op calls reject host-only layouts before touching the device
+    st = lib.nt_pair_broadcast(host.handle, 8, C.c_void_p(16), 8, C.c_void_p(16), 8, C.c_void_p(16), 8, 0, B.NT_BF16, None)
+    assert st == B.NT_ERR_INVALID_ARG and b"host-only" in lib.nt_last_error()
+    st = lib.nt_triangle_mul(host.handle, 0, 32, None, None, 0, None, 32, B.NT_BF16, None)
+    assert st == B.NT_ERR_INVALID_ARG
+    st = lib.nt_segment_reduce(None, 1, 0, 8, None, 8, B.NT_BF16, None, 8, None)
+    assert st == B.NT_ERR_INVALID_ARG
+    # LayerNorm+Linear validation
+    cases = [
+        (dict(c_in=12), B.NT_ERR_INVALID_ARG),                            # K not a multiple of 8
+        (dict(epilogue=7), B.NT_ERR_INVALID_ARG),
+        (dict(x=C.c_void_p(0x1002)), B.NT_ERR_INVALID_ARG),               # misaligned
+        (dict(epilogue=1), B.NT_ERR_INVALID_ARG),                         # residual missing
+        (dict(epilogue=2, hidden=64, w2=C.c_void_p(0x4000), c_in=96, c_out=96, ldx=96, ldy=96), B.NT_ERR_UNSUPPORTED),
+        (dict(n_tail=4, y_tail=C.c_void_p(0x5000), ld_tail=16, tail_layout=1), B.NT_ERR_UNSUPPORTED),
+        (dict(rows=25, layout=host.handle, level=1, residual_layout=other.handle,
+              residual=C.c_void_p(0x6000), ld_residual=16, epilogue=1), B.NT_ERR_LAYOUT_MISMATCH),
+        (dict(rows=24, layout=host.handle, level=1), B.NT_ERR_LAYOUT_MISMATCH),
+        (dict(dtype=B.NT_F32, x_dtype=B.NT_BF16), B.NT_ERR_INVALID_ARG),
+        (dict(ldy=4), B.NT_ERR_INVALID_ARG),
+    ]
+    for kw, want in cases:
+        a = _linear_args(**kw)
+        assert lib.nt_layernorm_linear(C.byref(a), None) == want, (kw, lib.nt_last_error())
+    # attention validation
+    dev = B.NestedLayout([2, 3], host_only=True)
+    assert lib.nt_pair_row_attention(dev.handle, 0, 4, 32, None, None, None, 384, None, 0, 1.0, None, 128,
+                                     B.NT_BF16, None) == B.NT_ERR_INVALID_ARG    # host-only layout

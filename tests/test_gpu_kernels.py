@@ -1,0 +1,244 @@
+"""Per-kernel parity of the HIP path (through the C ABI) against the CPU oracle
+on identical seeded inputs.  Shapes span several tiles, ragged tails, empty
+and length-1 samples."""
+import numpy as np
+import pytest
+
+from oracle import ops as O
+from paper_2609_30379_amd import synth
+from tests.gpu_util import check, dev, host, pair_padded, unpad_pair
+
+pytestmark = pytest.mark.gpu
+
+LENGTHS = {
+    "tiny": [15, 12, 10, 7],
+    "ragged": [5, 0, 1, 37, 64, 3, 70],
+    "one": [1],
+}
+
+
+@pytest.fixture(scope="module")
+def B():
+    from paper_2609_30379_amd import binding
+    binding.load()
+    return binding
+
+
+def _layout(B, L):
+    return B.NestedLayout(L)
+
+
+def _n(seed, name, shape, scale=1.0, dtype="bf16"):
+    return synth.normal(seed, name, shape, scale, dtype)
+
+
+# ------------------------------------------------------------------ broadcast
+@pytest.mark.parametrize("lname", list(LENGTHS))
+@pytest.mark.parametrize("dtype,C", [("bf16", 128), ("bf16", 64), ("f32", 16)])
+@pytest.mark.parametrize("accumulate", [False, True])
+def test_pair_broadcast(B, lname, dtype, C, accumulate):
+    L = LENGTHS[lname]
+    lay = _layout(B, L)
+    S, R = sum(L), sum(n * n for n in L)
+    uv = _n(1, "uv", (S, 2 * C), 0.6, dtype)
+    z0 = _n(2, "z0", (R, C), 0.6, dtype)
+    uvd = dev(uv, dtype)
+    z = dev(z0, dtype)
+    B.nt_pair_broadcast(lay, uvd[:, :C], uvd[:, C:], z, accumulate=accumulate)
+    ref = O.pair_broadcast(uv[:, :C], uv[:, C:], L, z_in=z0 if accumulate else None)
+    check(host(z), ref, dtype, f"broadcast {lname} {dtype} C={C} acc={accumulate}")
+
+
+def test_pair_broadcast_full_size(B):
+    w = synth.WORKLOADS["pair_b8_n208_224_bf16"]
+    L = synth.lengths_for(w).tolist()
+    lay = _layout(B, L)
+    S, R, C = sum(L), sum(n * n for n in L), w.c_z
+    uv = _n(3, "uv", (S, 2 * C), 0.5)
+    uvd = dev(uv, "bf16")
+    import torch
+    z = torch.empty((R, C), dtype=torch.bfloat16, device="cuda")
+    B.nt_pair_broadcast(lay, uvd[:, :C], uvd[:, C:], z)
+    check(host(z), O.pair_broadcast(uv[:, :C], uv[:, C:], L), "bf16", "broadcast full size")
+
+
+# ------------------------------------------------------------------ reduce
+@pytest.mark.parametrize("lname", list(LENGTHS))
+@pytest.mark.parametrize("dtype,C", [("bf16", 128), ("bf16", 768), ("f32", 16), ("f32", 36)])
+@pytest.mark.parametrize("level", ["pairs", "singles"])
+@pytest.mark.parametrize("op", ["sum", "mean"])
+def test_segment_reduce(B, lname, dtype, C, level, op):
+    import torch
+    L = LENGTHS[lname]
+    lay = _layout(B, L)
+    rows = sum(n * n for n in L) if level == "pairs" else sum(L)
+    out_rows = sum(L) if level == "pairs" else len(L)
+    x = _n(4, "x", (rows, C), 0.7, dtype)
+    y = torch.full((out_rows, C), 123.0, dtype=torch.float32, device="cuda")
+    B.nt_segment_reduce(lay, level, op, dev(x, dtype), y)
+    ref = O.segment_reduce(x, L, "pair_cols" if level == "pairs" else "samples", op)
+    check(host(y), ref, "f32", f"reduce {lname} {level} {op} {dtype}", equal_nan=True)
+
+
+def test_segment_reduce_empty_sample_mean_is_nan(B):
+    import torch
+    lay = _layout(B, [3, 0, 2])
+    x = dev(np.ones((5, 8)), "bf16")
+    y = torch.zeros((3, 8), dtype=torch.float32, device="cuda")
+    B.nt_segment_reduce(lay, "singles", "mean", x, y)
+    out = host(y)
+    assert np.all(out[0] == 1.0) and np.all(np.isnan(out[1])) and np.all(out[2] == 1.0)
+    B.nt_segment_reduce(lay, "singles", "sum", x, y)
+    assert np.all(host(y)[1] == 0.0)
+
+
+# ------------------------------------------------------------------ LN + Linear
+LIN_CASES = [
+    # rows, K, N, ln, epilogue, x dtype, dtype, n_tail
+    (1000, 128, 128, True, "none", "bf16", "bf16", 0),
+    (777, 128, 388, True, "none", "bf16", "bf16", 4),
+    (300, 384, 256, False, "none", "bf16", "bf16", 0),
+    (600, 768, 2304, True, "none", "bf16", "bf16", 0),
+    (600, 768, 3072, True, "gelu", "bf16", "bf16", 0),
+    (600, 3072, 768, False, "residual", "bf16", "bf16", 0),
+    (300, 128, 384, False, "residual", "f32", "bf16", 0),
+    (129, 136, 40, True, "residual", "bf16", "bf16", 0),
+    (100, 16, 50, True, "none", "f32", "f32", 2),
+    (100, 32, 32, False, "residual", "f32", "f32", 0),
+    (100, 16, 16, True, "gelu", "f32", "f32", 0),
+]
+
+
+@pytest.mark.parametrize("R,K,N,ln,epi,xdt,dtype,n_tail", LIN_CASES)
+def test_layernorm_linear(B, R, K, N, ln, epi, xdt, dtype, n_tail):
+    import torch
+    x = _n(5, "x", (R, K), 0.5, xdt)
+    w = _n(6, "w", (N, K), 0.5 / np.sqrt(K), dtype)
+    b = _n(7, "b", (N,), 0.1, "f32")
+    g = _n(8, "g", (K,), 0.1, "f32") + 1.0
+    be = _n(9, "be", (K,), 0.1, "f32")
+    res = _n(10, "res", (R, N - n_tail), 0.5, dtype) if epi == "residual" else None
+    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    y = torch.full((R, N - n_tail), float("nan"), dtype=td, device="cuda")
+    yt = torch.full((max(n_tail, 1), R + 8), float("nan"), dtype=td, device="cuda") if n_tail else None
+    B.nt_layernorm_linear(dev(x, xdt), dev(w, dtype), dev(b, "f32"), y,
+                          ln=(dev(g, "f32"), dev(be, "f32")) if ln else None, epilogue=epi,
+                          residual=dev(res, dtype) if res is not None else None, n_tail=n_tail, y_tail=yt)
+    ref = O.layernorm_linear(x, w, b, ln=(g, be) if ln else None,
+                             epilogue=epi if epi != "residual" else "none")
+    main = ref[:, :N - n_tail] + (res if res is not None else 0.0)
+    check(host(y), main, dtype, f"linear main {R}x{K}->{N} {epi}")
+    if n_tail:
+        check(host(yt)[:, :R].T, ref[:, N - n_tail:], dtype, "linear tail")
+
+
+@pytest.mark.parametrize("transposed", [False, True])
+@pytest.mark.parametrize("dtype,C", [("bf16", 64), ("f32", 16)])
+def test_layernorm_linear_pair_padded_tail(B, transposed, dtype, C):
+    import torch
+    L = LENGTHS["ragged"]
+    lay = _layout(B, L)
+    R = sum(n * n for n in L)
+    x = _n(11, "x", (R, C), 0.5, dtype)
+    w = _n(12, "w", (2 * C, C), 0.5 / np.sqrt(C), dtype)
+    b = _n(13, "b", (2 * C,), 0.1, "f32")
+    g, be = _n(14, "g", (C,), 0.1, "f32") + 1, _n(15, "be", (C,), 0.1, "f32")
+    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    ld = (lay.sum_pad + 7) // 8 * 8
+    yt = torch.full((2 * C, ld), float("nan"), dtype=td, device="cuda")
+    B.nt_layernorm_linear(dev(x, dtype), dev(w, dtype), dev(b, "f32"), None, ln=(dev(g, "f32"), dev(be, "f32")),
+                          n_tail=2 * C, y_tail=yt, tail_layout="pair_padded_t" if transposed else "pair_padded",
+                          layout=lay, level="pairs", c_out=2 * C)
+    ref = O.layernorm_linear(x, w, b, ln=(g, be))
+    check(unpad_pair(host(yt), L, transposed), ref, dtype, "pair-padded tail")
+
+
+@pytest.mark.parametrize("R,K,F,dtype", [(1000, 128, 512, "bf16"), (333, 64, 256, "bf16"), (65, 256, 96, "bf16"),
+                                         (100, 16, 64, "f32")])
+def test_swiglu_transition(B, R, K, F, dtype):
+    import torch
+    x = _n(16, "x", (R, K), 0.5, dtype)
+    w = _n(17, "w", (2 * F, K), 1.0 / np.sqrt(K), dtype)
+    b = _n(18, "b", (2 * F,), 0.1, "f32")
+    w2 = _n(19, "w2", (K, F), 0.25 / np.sqrt(F), dtype)
+    b2 = _n(20, "b2", (K,), 0.1, "f32")
+    g, be = _n(21, "g", (K,), 0.1, "f32") + 1, _n(22, "be", (K,), 0.1, "f32")
+    xd = dev(x, dtype)
+    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    y = torch.full((R, K), float("nan"), dtype=td, device="cuda")
+    B.nt_layernorm_linear(xd, dev(w, dtype), dev(b, "f32"), y, ln=(dev(g, "f32"), dev(be, "f32")),
+                          epilogue="swiglu_residual", w2=dev(w2, dtype), bias2=dev(b2, "f32"), hidden=F)
+    ref = O.layernorm_linear(x, w, b, ln=(g, be), epilogue="swiglu_residual", w2=w2, b2=b2)
+    check(host(y), ref, dtype, f"swiglu {R}x{K} F={F}")
+    # in place (y aliases x), as the pair block runs it
+    B.nt_layernorm_linear(xd, dev(w, dtype), dev(b, "f32"), xd, ln=(dev(g, "f32"), dev(be, "f32")),
+                          epilogue="swiglu_residual", w2=dev(w2, dtype), bias2=dev(b2, "f32"), hidden=F)
+    check(host(xd), ref, dtype, "swiglu in place")
+
+
+# ------------------------------------------------------------------ attention
+ATT_LENGTHS = [5, 0, 1, 37, 64, 3, 70, 130, 17]
+
+
+def _head_major(bias_cells):
+    return np.ascontiguousarray(bias_cells.T)
+
+
+@pytest.mark.parametrize("axis", [0, 1])
+@pytest.mark.parametrize("dtype,H,D", [("bf16", 4, 32), ("bf16", 2, 64), ("f32", 2, 8)])
+def test_pair_attention(B, axis, dtype, H, D):
+    import torch
+    L = ATT_LENGTHS if dtype == "bf16" else LENGTHS["tiny"]
+    lay = _layout(B, L)
+    R = sum(n * n for n in L)
+    qkv = _n(23, "qkv", (R, 3 * H * D), 1.0, dtype)
+    qkv[:, 2 * H * D:] *= 0.5
+    if dtype == "bf16":
+        qkv = synth.snap_bf16(qkv)
+    bias = _n(24, "bias", (R, H), 1.0, dtype)
+    qd = dev(qkv, dtype)
+    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    o = torch.full((R, H * D), float("nan"), dtype=td, device="cuda")
+    c = H * D
+    B.nt_pair_row_attention(lay, axis, H, D, qd[:, :c], qd[:, c:2 * c], qd[:, 2 * c:], o,
+                            bias=dev(_head_major(bias), dtype))
+    ref = O.pair_row_attention(qkv[:, :c], qkv[:, c:2 * c], qkv[:, 2 * c:], bias, L, H, D, axis=axis)
+    check(host(o), ref, dtype, f"pair attention axis {axis} {dtype}")
+
+
+@pytest.mark.parametrize("dtype,H,D,L", [("bf16", 3, 64, [1, 5, 64, 65, 130, 512, 0, 200]),
+                                         ("bf16", 2, 32, [33, 1, 97]),
+                                         ("f32", 2, 8, [15, 12, 10, 7, 0, 1])])
+def test_attention_1d(B, dtype, H, D, L):
+    import torch
+    lay = _layout(B, L)
+    T = sum(L)
+    c = H * D
+    qkv = _n(25, "qkv", (T, 3 * c), 1.0, dtype)
+    qd = dev(qkv, dtype)
+    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    o = torch.full((T, c), float("nan"), dtype=td, device="cuda")
+    B.nt_pair_row_attention(lay, 2, H, D, qd[:, :c], qd[:, c:2 * c], qd[:, 2 * c:], o)
+    ref = O.attention_1d(qkv[:, :c], qkv[:, c:2 * c], qkv[:, 2 * c:], L, H, D)
+    check(host(o), ref, dtype, f"1-D attention {dtype}")
+
+
+# ------------------------------------------------------------------ triangle
+@pytest.mark.parametrize("direction", [0, 1])
+@pytest.mark.parametrize("dtype,C,lname", [("bf16", 64, "ragged"), ("bf16", 32, "tiny"), ("f32", 16, "tiny"),
+                                           ("f32", 16, "ragged")])
+def test_triangle(B, direction, dtype, C, lname):
+    L = LENGTHS[lname]
+    lay = _layout(B, L)
+    R = sum(n * n for n in L)
+    a = _n(26, "a", (R, C), 0.3, dtype)
+    b = _n(27, "b", (R, C), 0.3, dtype)
+    z0 = _n(28, "z0", (R, C), 0.5, dtype)
+    tr = direction == 1
+    ld = (lay.sum_pad + 7) // 8 * 8
+    ap = dev(pair_padded(a, L, tr, ld, fill=np.nan), dtype)
+    bp = dev(pair_padded(b, L, tr, ld, fill=np.nan), dtype)
+    z = dev(z0, dtype)
+    B.nt_triangle_mul(lay, direction, ap, bp, z)
+    ref = z0 + O.triangle_mul(a, b, L, "outgoing" if direction == 0 else "incoming")
+    check(host(z), ref, dtype, f"triangle dir {direction} {dtype} {lname}")
