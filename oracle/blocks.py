@@ -34,7 +34,7 @@ PAIR_ORDER_BLOCK = ("bcast", "lin", "att_row", "tri_out", "trans", "single")
 PAIR_ORDER_STACK = ("bcast", "tri_out", "tri_in", "att_row", "att_col", "trans", "single")
 
 
-def pair_block(s, lengths, p, dims, order, z=None, dtype="bf16"):
+def pair_block(s, lengths, p, dims, order, z=None, dtype="bf16", round_last=True):
     """One single-pair-single block (Eq. running-block generalised with the
     Pairformer-style steps of Sec. 4.3).
 
@@ -49,49 +49,55 @@ def pair_block(s, lengths, p, dims, order, z=None, dtype="bf16"):
       tri_in   [a|b] = LN(z) W^T + b; z += triangle_incoming(a, b)
       trans    z = z + SwiGLU(LN(z))                                (Eq. running-block l.2)
       single   m = mean_b z[.,b];  s = s + m W_s^T + b_s            (Eq. running-block l.3)
+    round_last=False returns the output of the final step unrounded (the
+    exact value the last store of the GPU path rounds); every value a later
+    step consumes is still stored.
     Returns (s, z, trace) where trace maps step names to intermediate values.
     """
     C, H, d = dims["c_z"], dims["heads"], dims["head_dim"]
-    st = lambda t: store(t, dtype)          # noqa: E731
+    keep = lambda t: store(t, dtype)        # noqa: E731
     trace = {}
     s = np.asarray(s, np.float64)
-    for step in order:
+    for k, step in enumerate(order):
+        last = k == len(order) - 1
+        st = keep if (round_last or not last) else (lambda t: np.asarray(t, np.float64))
         if step == "bcast":
-            uv = st(linear(s, p["uv.w"], p["uv.b"]))
+            uv = keep(linear(s, p["uv.w"], p["uv.b"]))
             trace["uv"] = uv
             z = st(ops.pair_broadcast(uv[:, :C], uv[:, C:], lengths, z_in=z))
         elif step == "lin":
-            z = st(_ln_linear(z, p["lin.w"], p["lin.b"], (p["lin.ln_g"], p["lin.ln_b"]), st))
+            z = st(_ln_linear(z, p["lin.w"], p["lin.b"], (p["lin.ln_g"], p["lin.ln_b"]), keep))
         elif step in ("att_row", "att_col"):
             key = step
-            proj = _ln_linear(z, p[key + ".w"], p[key + ".b"], (p[key + ".ln_g"], p[key + ".ln_b"]), st)
-            q, k, v = st(proj[:, :C]), st(proj[:, C:2 * C]), st(proj[:, 2 * C:3 * C])
-            beta = st(proj[:, 3 * C:3 * C + H])
-            o = st(ops.pair_row_attention(q, k, v, beta, lengths, H, d,
-                                          axis=0 if step == "att_row" else 1))
+            proj = _ln_linear(z, p[key + ".w"], p[key + ".b"], (p[key + ".ln_g"], p[key + ".ln_b"]), keep)
+            q, kk, v = keep(proj[:, :C]), keep(proj[:, C:2 * C]), keep(proj[:, 2 * C:3 * C])
+            beta = keep(proj[:, 3 * C:3 * C + H])
+            o = keep(ops.pair_row_attention(q, kk, v, beta, lengths, H, d,
+                                            axis=0 if step == "att_row" else 1))
             trace[step + ".o"] = o
             z = st(z + linear(o, p[key + ".wo"], p[key + ".bo"]))
         elif step in ("tri_out", "tri_in"):
-            ab = st(_ln_linear(z, p[step + ".w"], p[step + ".b"], (p[step + ".ln_g"], p[step + ".ln_b"]), st))
+            ab = keep(_ln_linear(z, p[step + ".w"], p[step + ".b"], (p[step + ".ln_g"], p[step + ".ln_b"]), keep))
             t = ops.triangle_mul(ab[:, :C], ab[:, C:], lengths,
                                  "outgoing" if step == "tri_out" else "incoming")
             z = st(z + t)
         elif step == "trans":
-            z = st(_swiglu(z, p, st))
+            z = st(_swiglu(z, p, keep))
         elif step == "single":
             m = ops.segment_reduce(z, lengths, "pair_cols", "mean")
             trace["col_mean"] = m
-            s = st(s + linear(st(m), p["single.w"], p["single.b"]))
+            s = st(s + linear(keep(m), p["single.w"], p["single.b"]))
         else:
             raise ValueError(f"unknown step {step!r}")
         trace[step] = z
     return s, z, trace
 
 
-def encoder_layer(x, lengths, p, heads, head_dim, dtype="bf16"):
+def encoder_layer(x, lengths, p, heads, head_dim, dtype="bf16", round_last=True):
     """Pre-LayerNorm Transformer encoder layer on packed tokens followed by a
     per-sample mean pool (the 1-D token path: Sec. 3.3 "Attention through
-    packed blocks"; BERT-Base shape of Appendix C).
+    packed blocks"; BERT-Base shape of Appendix C).  The pool reads the stored
+    layer output; round_last=False returns that output unrounded.
     Returns (x_out, pooled, trace)."""
     st = lambda t: store(t, dtype)          # noqa: E731
     c = heads * head_dim
@@ -100,6 +106,7 @@ def encoder_layer(x, lengths, p, heads, head_dim, dtype="bf16"):
     o = st(ops.attention_1d(qkv[:, :c], qkv[:, c:2 * c], qkv[:, 2 * c:], lengths, heads, head_dim))
     x = st(x + linear(o, p["o.w"], p["o.b"]))
     h = st(gelu(_ln_linear(x, p["ffn1.w"], p["ffn1.b"], (p["ln2_g"], p["ln2_b"]), st)))
-    x = st(x + linear(h, p["ffn2.w"], p["ffn2.b"]))
+    x_exact = x + linear(h, p["ffn2.w"], p["ffn2.b"])
+    x = st(x_exact)
     pooled = ops.segment_reduce(x, lengths, "samples", "mean")
-    return x, pooled, {"qkv": qkv, "o": o, "h": h}
+    return (x if round_last else x_exact), pooled, {"qkv": qkv, "o": o, "h": h}

@@ -203,7 +203,7 @@ class PairRun:
         self.dims = dict(c_z=w.c_z, heads=w.heads, head_dim=w.head_dim)
         self.params = [synth.pair_block_params(w, block=b) for b in range(w.blocks)]
         self.W = [to_device(p, w.dtype, device) for p in self.params]
-        self.s_init = synth.normal(w.seed, "s", (sum(self.lengths), w.c_s), 1.0, w.dtype)
+        self.s_init = synth.normal(w.seed, "s", (sum(self.lengths), w.c_s), w.s_scale, w.dtype)
         td = torch.bfloat16 if w.dtype == "bf16" else torch.float32
         self.s0 = torch.from_numpy(self.s_init).to(device=device, dtype=td)
         self.s = self.s0.clone()

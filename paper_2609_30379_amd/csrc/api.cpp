@@ -39,7 +39,9 @@ nt_status upload(nt_layout* L, hipStream_t s) {
       {&L->cu_pairs, &L->d_cu_pairs},     {&L->cu_pad, &L->d_cu_pad},
       {&L->row_splits2, &L->d_row_splits2}, {&L->row_sample, &L->d_row_sample},
       {&L->attn_work, &L->d_attn_work},   {&L->tri_work, &L->d_tri_work},
-      {&L->seq_work, &L->d_seq_work},
+      {&L->seq_work, &L->d_seq_work},     {&L->prow_base, &L->d_prow_base},
+      {&L->prow_tbase, &L->d_prow_tbase}, {&L->prow_n8, &L->d_prow_n8},
+      {&L->blk_prow, &L->d_blk_prow},
   };
   size_t total = 0;
   for (auto& p : parts) total += (p.v->size() * sizeof(int32_t) + 255) / 256 * 256;

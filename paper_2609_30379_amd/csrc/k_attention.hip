@@ -110,6 +110,7 @@ __global__ void __launch_bounds__(256) attention_mfma_kernel(AttnArgs p) {
     for (int dt = 0; dt < D / 16; ++dt) O[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
     const bf16* brow = nullptr;                // bias row of this query (axis 0)
     if (p.bias && qvalid) brow = p.bias + (int64_t)h * p.ld_bias + sg.cu + (p.axis == 0 ? (int64_t)qi * n : qi);
+    const int64_t bstep = p.axis == 0 ? 1 : n;
 
     for (int kc = 0; kc < npad; kc += 64) {
       f32x4 s[4];
@@ -130,7 +131,7 @@ __global__ void __launch_bounds__(256) attention_mfma_kernel(AttnArgs p) {
         for (int i = 0; i < 4; ++i) {
           const int key = kc + kt * 16 + 4 * g + i;
           float t = s[kt][i] * p.scale_log2;
-          if (brow && key < n) t += (float)brow[p.axis == 0 ? (int64_t)key : (int64_t)key * n] * kLog2e;
+          if (brow && key < n) t += (float)brow[(int64_t)key * bstep] * kLog2e;
           t = key < n ? t : -INFINITY;
           x[kt][i] = t;
           mloc = fmaxf(mloc, t);

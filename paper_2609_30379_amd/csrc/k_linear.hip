@@ -37,6 +37,10 @@ struct LinArgs {
   const int32_t* cu_pad;
   int sum_n;
   int mblocks, nblocks;
+  const int32_t* prow_base;   // pair-row tables of the pair-padded tail layouts
+  const int32_t* prow_tbase;
+  const int32_t* prow_n8;
+  const int32_t* blk_prow;
 };
 
 // Position of packed pair row m (cell (i, x, k)) in a pair-padded channel-major
@@ -60,8 +64,25 @@ __device__ __forceinline__ float gelu_erf(float v) { return 0.5f * v * (1.f + er
 // Raw (unnormalised) global data of one k-step, held in registers while the
 // previous step computes.
 template <typename XT> struct XStage;
-template <> struct XStage<bf16> { uint4 d[2]; };
-template <> struct XStage<float> { float4 d[4]; };
+template <> struct XStage<bf16> {
+  using T = uint4;
+  uint4 d[2];
+  static __device__ __forceinline__ uint4 zero() { return make_uint4(0, 0, 0, 0); }
+  static __device__ __forceinline__ void unpack(const uint4& t, float* o) {
+    const uint32_t w4[4] = {t.x, t.y, t.z, t.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      o[2 * j] = __uint_as_float(w4[j] << 16);
+      o[2 * j + 1] = __uint_as_float(w4[j] & 0xffff0000u);
+    }
+  }
+};
+template <> struct XStage<float> {
+  using T = float4;
+  float4 d[4];
+  static __device__ __forceinline__ float4 zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
+  static __device__ __forceinline__ void unpack(const float4& t, float* o) { o[0] = t.x; o[1] = t.y; o[2] = t.z; o[3] = t.w; }
+};
 
 template <typename XT, int EPI>
 __global__ void __launch_bounds__(256) linear_mfma_kernel(LinArgs p) {
@@ -261,6 +282,208 @@ __global__ void __launch_bounds__(256) linear_mfma_kernel(LinArgs p) {
   }
 }
 
+// ---------------------------------------------------------------- K-resident
+// For the pair path (K <= 256) one workgroup owns a 128-row tile and all
+// output columns: the whole normalised tile and one 128-column weight block
+// sit in LDS after a single global round trip, LayerNorm statistics come from
+// registers (two threads per row), and the next weight block is prefetched
+// into registers while the current one runs on the matrix cores.  Rows of a
+// pair-level input are cells; their pair-padded tail offsets come from the
+// per-pair-row tables (first pair row of the tile from blk_prow, the tile's
+// row splits cached in LDS).
+template <typename XT, int EPI, int K>
+__global__ void __launch_bounds__(256) linear_res_kernel(LinArgs p) {
+  constexpr int SKR = K + 8;
+  constexpr int VX = Vec<XT>::N;
+  constexpr int HALF = K / 2;
+  constexpr int NV = HALF / VX;               // x vectors per thread
+  constexpr int WV = K / 16;                  // weight vectors per thread per block
+  __shared__ __attribute__((aligned(16))) bf16 Xs[BM * SKR];
+  __shared__ __attribute__((aligned(16))) bf16 Ws[BN * SKR];
+  __shared__ int32_t rs[BM + 1];
+  const int mb = blockIdx.x;
+  const int m0 = mb * BM;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, g = lane >> 4;
+  const XT* x = static_cast<const XT*>(p.x);
+
+  // ---- issue every global load of the tile and the first weight block ----
+  const int r = tid >> 1, hh = tid & 1, xm = m0 + r;
+  using XV = typename XStage<XT>::T;
+  XV xr[NV];
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    if (xm < p.rows) xr[v] = *reinterpret_cast<const XV*>(x + (int64_t)xm * p.ldx + hh * HALF + v * VX);
+    else xr[v] = XStage<XT>::zero();
+  }
+  uint4 wr[WV];
+  auto load_w = [&](int n0) {
+#pragma unroll
+    for (int j = 0; j < WV; ++j) {
+      const int c = tid + 256 * j, wrow = c / (K / 8), wcol = (c % (K / 8)) * 8;
+      wr[j] = (n0 + wrow < p.N) ? *reinterpret_cast<const uint4*>(p.w + (int64_t)(n0 + wrow) * K + wcol)
+                                : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto store_w = [&]() {
+#pragma unroll
+    for (int j = 0; j < WV; ++j) {
+      const int c = tid + 256 * j, wrow = c / (K / 8), wcol = (c % (K / 8)) * 8;
+      *reinterpret_cast<uint4*>(&Ws[wrow * SKR + wcol]) = wr[j];
+    }
+  };
+  load_w(0);
+  const bool padded_tail = p.y_tail && p.tail_mode != kTailChannelMajor;
+  int eta0 = 0;
+  if (padded_tail) {
+    eta0 = p.blk_prow[mb];
+    for (int j = tid; j <= BM; j += 256) rs[j] = p.row_splits2[min(eta0 + j, p.sum_n)];
+  }
+
+  // ---- LayerNorm from the raw registers, normalised bf16 tile into LDS ----
+  float mean = 0.f, rstd = 1.f;
+  if (p.gamma) {
+    float s = 0.f;
+#pragma unroll
+    for (int vv = 0; vv < NV; ++vv) {
+      float t[VX];
+      XStage<XT>::unpack(xr[vv], t);
+#pragma unroll
+      for (int e = 0; e < VX; ++e) s += t[e];
+    }
+    s += __shfl_xor(s, 1, 64);
+    mean = s / (float)K;
+    float q = 0.f;
+#pragma unroll
+    for (int vv = 0; vv < NV; ++vv) {
+      float t[VX];
+      XStage<XT>::unpack(xr[vv], t);
+#pragma unroll
+      for (int e = 0; e < VX; ++e) { const float d = t[e] - mean; q += d * d; }
+    }
+    q += __shfl_xor(q, 1, 64);
+    rstd = xm < p.rows ? rsqrtf(q / (float)K + p.eps) : 0.f;
+  }
+#pragma unroll
+  for (int j = 0; j < HALF; j += 8) {
+    float t[8];
+    XStage<XT>::unpack(xr[j / VX], t);
+    if constexpr (VX == 4) XStage<XT>::unpack(xr[j / VX + 1], t + 4);
+    if (p.gamma) {
+#pragma unroll
+      for (int e = 0; e < 8; e += 4) {
+        const float4 ga = *reinterpret_cast<const float4*>(p.gamma + hh * HALF + j + e);
+        const float4 be = p.beta ? *reinterpret_cast<const float4*>(p.beta + hh * HALF + j + e)
+                                 : make_float4(0.f, 0.f, 0.f, 0.f);
+        t[e] = (t[e] - mean) * rstd * ga.x + be.x;
+        t[e + 1] = (t[e + 1] - mean) * rstd * ga.y + be.y;
+        t[e + 2] = (t[e + 2] - mean) * rstd * ga.z + be.z;
+        t[e + 3] = (t[e + 3] - mean) * rstd * ga.w + be.w;
+      }
+      if (xm >= p.rows) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) t[e] = 0.f;
+      }
+    }
+    bf16x8 o;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = (bf16)t[e];
+    *reinterpret_cast<bf16x8*>(&Xs[r * SKR + hh * HALF + j]) = o;
+  }
+  store_w();
+  __syncthreads();
+
+  // pair-padded offsets of the lane's four rows
+  const int wn_off = (wave >> 1) * 64, wm_off = (wave & 1) * 64;
+  int32_t tpos[4];
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    const int m = m0 + wm_off + b * 16 + l16;
+    tpos[b] = m;
+    if (padded_tail && m < p.rows) {
+      int lo = 0, hi = min(BM, p.sum_n - eta0) - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (rs[mid] <= m) lo = mid; else hi = mid - 1;
+      }
+      const int eta = eta0 + lo, kk = m - rs[lo];
+      tpos[b] = p.tail_mode == kTailPairPadded ? p.prow_base[eta] + kk : p.prow_tbase[eta] + kk * p.prow_n8[eta];
+    }
+  }
+
+  for (int n0 = 0; n0 < p.N; n0 += BN) {
+    const bool more = n0 + BN < p.N;
+    if (more) load_w(n0 + BN);
+    f32x4 acc[4][4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int b = 0; b < 4; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const bool wave_active = n0 + wn_off < p.N;
+    if (wave_active) {
+#pragma unroll
+      for (int kk = 0; kk < K / 32; ++kk) {
+        bf16x8 af[4], bfr[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          af[t] = *reinterpret_cast<const bf16x8*>(&Ws[(wn_off + t * 16 + l16) * SKR + kk * 32 + g * 8]);
+          bfr[t] = *reinterpret_cast<const bf16x8*>(&Xs[(wm_off + t * 16 + l16) * SKR + kk * 32 + g * 8]);
+        }
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+          for (int b = 0; b < 4; ++b) acc[a][b] = mfma16(af[a], bfr[b], acc[a][b]);
+      }
+      // epilogue: lane owns channels n..n+3 of row m for every (a, b) tile
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const int m = m0 + wm_off + b * 16 + l16;
+        if (m >= p.rows) continue;
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+          const int n = n0 + wn_off + a * 16 + g * 4;
+          if (n >= p.N) continue;
+          float rr[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            rr[i] = acc[a][b][i] + ((p.bias && n + i < p.N) ? p.bias[n + i] : 0.f);
+            if constexpr (EPI == NT_EPI_GELU) rr[i] = gelu_erf(rr[i]);
+          }
+          if (n + 4 <= p.n_main) {
+            if constexpr (EPI == NT_EPI_RESIDUAL) {
+              const uint2 q2 = *reinterpret_cast<const uint2*>(p.res + (int64_t)m * p.ld_res + n);
+              rr[0] += __uint_as_float(q2.x << 16); rr[1] += __uint_as_float(q2.x & 0xffff0000u);
+              rr[2] += __uint_as_float(q2.y << 16); rr[3] += __uint_as_float(q2.y & 0xffff0000u);
+            }
+            bf16x4 o;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) o[i] = (bf16)rr[i];
+            *reinterpret_cast<bf16x4*>(p.y + (int64_t)m * p.ldy + n) = o;
+          } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int nn = n + i;
+              if (nn >= p.N) break;
+              if (nn < p.n_main) {
+                float val = rr[i];
+                if constexpr (EPI == NT_EPI_RESIDUAL) val += (float)p.res[(int64_t)m * p.ld_res + nn];
+                p.y[(int64_t)m * p.ldy + nn] = (bf16)val;
+              } else {
+                p.y_tail[(int64_t)(nn - p.n_main) * p.ld_tail + tpos[b]] = (bf16)rr[i];
+              }
+            }
+          }
+        }
+      }
+    }
+    if (more) {
+      __syncthreads();
+      store_w();
+      __syncthreads();
+    }
+  }
+}
+
 // ---------------------------------------------------------------- SwiGLU
 // Pre-normalised SwiGLU transition (Eq. running-block, second line):
 //   y = res + (silu(LN(x) Wg^T + bg) * (LN(x) Wu^T + bu)) Wd^T + bd.
@@ -298,18 +521,32 @@ __global__ void __launch_bounds__(256) swiglu_kernel(SwiArgs p) {
   const int m0 = blockIdx.x * RW;
 
   // ---- prologue: LayerNorm of the workgroup's rows into LDS --------------
+  // 16 lanes per row; every load of the workgroup's rows is issued first.
   bf16* Xn = smem;                                 // [RW][SKX]
-  for (int rr = tid >> 4; rr < RW; rr += 16) {
+  constexpr int KC = (K + 127) / 128;              // 16-byte vectors per lane per row
+  uint4 raw[RW / 16][KC];
+#pragma unroll
+  for (int it = 0; it < RW / 16; ++it) {
+    const int m = m0 + (tid >> 4) + 16 * it;
+#pragma unroll
+    for (int c = 0; c < KC; ++c) {
+      const int k = (l16 + 16 * c) * 8;
+      raw[it][c] = (m < p.rows && k < K) ? *reinterpret_cast<const uint4*>(p.x + (int64_t)m * p.ldx + k)
+                                         : make_uint4(0, 0, 0, 0);
+    }
+  }
+#pragma unroll
+  for (int it = 0; it < RW / 16; ++it) {
+    const int rr = (tid >> 4) + 16 * it;
     const int m = m0 + rr;
     float v[2][8];
     float s = 0.f;
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
-      const int k = (l16 + 16 * c) * 8;
-      if (m < p.rows && k < K) {
-        Vec<bf16> t; t.load(p.x + (int64_t)m * p.ldx + k);
+      if (c < KC) {
+        XStage<bf16>::unpack(raw[it][c], v[c]);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) { v[c][j] = t.v[j]; s += t.v[j]; }
+        for (int j = 0; j < 8; ++j) s += v[c][j];
       } else {
 #pragma unroll
         for (int j = 0; j < 8; ++j) v[c][j] = 0.f;
@@ -551,6 +788,8 @@ hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
     p.row_splits2 = plan.layout->d_row_splits2; p.row_sample = plan.layout->d_row_sample;
     p.cu_seqlens = plan.layout->d_cu_seqlens; p.cu_pad = plan.layout->d_cu_pad;
     p.sum_n = (int)plan.layout->sum_n;
+    p.prow_base = plan.layout->d_prow_base; p.prow_tbase = plan.layout->d_prow_tbase;
+    p.prow_n8 = plan.layout->d_prow_n8; p.blk_prow = plan.layout->d_blk_prow;
   }
   if (a.n_tail == 0) p.y_tail = nullptr;
 
@@ -590,6 +829,24 @@ hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
 
   p.mblocks = (rows + BM - 1) / BM;
   p.nblocks = (a.c_out + BN - 1) / BN;
+  const bool xf = a.x_dtype == NT_F32;
+  if (a.c_in == 64 || a.c_in == 128 || a.c_in == 256) {
+    const dim3 g1((unsigned)p.mblocks), b1(256);
+#define NT_RES(XT, EPI, KK) linear_res_kernel<XT, EPI, KK><<<g1, b1, 0, s>>>(p)
+#define NT_RES_K(XT, EPI) \
+    do { if (a.c_in == 64) NT_RES(XT, EPI, 64); else if (a.c_in == 128) NT_RES(XT, EPI, 128); else NT_RES(XT, EPI, 256); } while (0)
+#define NT_RES_X(EPI) do { if (xf) NT_RES_K(float, EPI); else NT_RES_K(bf16, EPI); } while (0)
+    switch (a.epilogue) {
+      case NT_EPI_NONE: NT_RES_X(NT_EPI_NONE); break;
+      case NT_EPI_RESIDUAL: NT_RES_X(NT_EPI_RESIDUAL); break;
+      case NT_EPI_GELU: NT_RES_X(NT_EPI_GELU); break;
+      default: return hipErrorInvalidValue;
+    }
+#undef NT_RES_X
+#undef NT_RES_K
+#undef NT_RES
+    return hipGetLastError();
+  }
   const unsigned grid = (unsigned)(((p.mblocks + kXcds - 1) / kXcds) * kXcds * p.nblocks);
   const bool xf32 = a.x_dtype == NT_F32;
 #define NT_LAUNCH_LIN(XT, EPI) linear_mfma_kernel<XT, EPI><<<dim3(grid), dim3(256), 0, s>>>(p)

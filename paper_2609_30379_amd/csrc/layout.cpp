@@ -106,6 +106,28 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L) {
   }
   L->row_splits2[sn] = (int32_t)sn2;
 
+  // pair-padded operand addressing per pair row, and the first pair row of
+  // every kLinRows-cell block of the pair tensor (projection row tiles)
+  L->prow_base.assign(sn, 0);
+  L->prow_tbase.assign(sn, 0);
+  L->prow_n8.assign(sn, 0);
+  for (int32_t i = 0; i < batch; ++i) {
+    const int32_t n = lengths[i], n8 = (n + 7) / 8 * 8;
+    for (int32_t a = 0; a < n; ++a) {
+      const int64_t eta = (int64_t)L->cu_seqlens[i] + a;
+      L->prow_base[eta] = L->cu_pad[i] + a * n8;
+      L->prow_tbase[eta] = L->cu_pad[i] + a;
+      L->prow_n8[eta] = n8;
+    }
+  }
+  const int64_t nblk = (sn2 + kLinRows - 1) / kLinRows;
+  L->blk_prow.assign(nblk, 0);
+  for (int64_t b = 0, eta = 0; b < nblk; ++b) {
+    const int64_t m = b * kLinRows;
+    while (eta + 1 < sn && L->row_splits2[eta + 1] <= m) ++eta;
+    L->blk_prow[b] = (int32_t)eta;
+  }
+
   // pair-row attention: one item per (sample, pair row), cost N_i^2
   {
     std::vector<std::array<int32_t, 2>> items;

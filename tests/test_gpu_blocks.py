@@ -26,7 +26,8 @@ def _oracle_pair(w, run, samples):
         z = None
         for b in range(w.blocks):
             steps = w.steps if b == 0 else tuple(t for t in w.steps if t != "lin")
-            s, z, _ = OB.pair_block(s, [n], run.params[b], dims, steps, z=z, dtype=w.dtype)
+            s, z, _ = OB.pair_block(s, [n], run.params[b], dims, steps, z=z, dtype=w.dtype,
+                                    round_last=b < w.blocks - 1)
         out[i] = (s, z)
     return out
 
@@ -80,6 +81,7 @@ def test_token_workload():
     for i in (12, 47, 1):
         n = run.lengths[i]
         print(f"  sample {i} N={n}", flush=True)
-        xr, pr, _ = OB2.encoder_layer(run.x_init[eta[i]:eta[i + 1]], [n], run.params, w.heads, w.head_dim, w.dtype)
+        xr, pr, _ = OB2.encoder_layer(run.x_init[eta[i]:eta[i + 1]], [n], run.params, w.heads, w.head_dim, w.dtype,
+                                      round_last=False)
         check(xg[eta[i]:eta[i + 1]], xr, "bf16", f"token layer x sample {i}")
         check(pg[i:i + 1], pr, "bf16", f"token pooled sample {i}")
