@@ -41,7 +41,7 @@ nt_status upload(nt_layout* L, hipStream_t s) {
       {&L->attn_work, &L->d_attn_work},   {&L->tri_work, &L->d_tri_work},
       {&L->seq_work, &L->d_seq_work},     {&L->prow_base, &L->d_prow_base},
       {&L->prow_tbase, &L->d_prow_tbase}, {&L->prow_n8, &L->d_prow_n8},
-      {&L->blk_prow, &L->d_blk_prow},
+      {&L->blk_prow, &L->d_blk_prow},     {&L->pattn_work, &L->d_pattn_work},
   };
   size_t total = 0;
   for (auto& p : parts) total += (p.v->size() * sizeof(int32_t) + 255) / 256 * 256;

@@ -291,9 +291,13 @@ __global__ void __launch_bounds__(256) linear_mfma_kernel(LinArgs p) {
 // pair-level input are cells; their pair-padded tail offsets come from the
 // per-pair-row tables (first pair row of the tile from blk_prow, the tile's
 // row splits cached in LDS).
+// LDS row stride (elements) for 16-byte fragment reads of a K-wide bf16 tile:
+// conflict-free when the stride is 8 (mod 64) dwords, i.e. 16 (mod 128) elements.
+template <int K> constexpr int frag_stride() { return K + ((16 - K % 128) + 128) % 128; }
+
 template <typename XT, int EPI, int K>
 __global__ void __launch_bounds__(256) linear_res_kernel(LinArgs p) {
-  constexpr int SKR = K + 8;
+  constexpr int SKR = frag_stride<K>();
   constexpr int VX = Vec<XT>::N;
   constexpr int HALF = K / 2;
   constexpr int NV = HALF / VX;               // x vectors per thread
@@ -513,8 +517,8 @@ template <int MT, int K, int N>
 __global__ void __launch_bounds__(256) swiglu_kernel(SwiArgs p) {
   constexpr int RW = 4 * MT * 16;                 // rows per workgroup
   constexpr int KMAX = K, NMAX = N;
-  constexpr int SD = 32 + 8;                      // LDS stride of the down-projection chunk
-  constexpr int SKW = K + 8, SKX = K + 8;         // LDS strides of weight / normalised rows
+  constexpr int SD = 36;                          // down-projection chunk: 8-byte reads, 2 (mod 4) dwords
+  constexpr int SKW = frag_stride<K>(), SKX = frag_stride<K>();   // 16-byte fragment rows
   extern __shared__ __attribute__((aligned(16))) bf16 smem[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, g = lane >> 4;
@@ -610,7 +614,8 @@ __global__ void __launch_bounds__(256) swiglu_kernel(SwiArgs p) {
     for (int t = tid; t < d_vecs; t += 256) {
       const int n = t >> 2, fc = (t & 3) * 8;
       const uint4 d = *reinterpret_cast<const uint4*>(p.w2 + (int64_t)n * p.F + f0 + fc);
-      *reinterpret_cast<uint4*>(&Wd[n * SD + fc]) = d;
+      *reinterpret_cast<uint2*>(&Wd[n * SD + fc]) = make_uint2(d.x, d.y);     // rows are 8-byte aligned
+      *reinterpret_cast<uint2*>(&Wd[n * SD + fc + 4]) = make_uint2(d.z, d.w);
     }
     __syncthreads();
 
@@ -816,8 +821,9 @@ hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
     w.y = (bf16*)a.y; w.ldy = a.ldy;
     constexpr int MT = 2;
     const int rw = 4 * MT * 16;
-    const size_t xn = (size_t)rw * (a.c_in + 8);
-    const size_t wc = (size_t)64 * (a.c_in + 8) + (size_t)a.c_out * 40;
+    const int sk = a.c_in + ((16 - a.c_in % 128) + 128) % 128;
+    const size_t xn = (size_t)rw * sk;
+    const size_t wc = (size_t)64 * sk + (size_t)a.c_out * 36;
     const size_t smem = sizeof(bf16) * (xn > wc ? xn : wc);
     const dim3 grid((rows + rw - 1) / rw);
     if (a.c_in == 64 && a.c_out == 64) swiglu_kernel<MT, 64, 64><<<grid, dim3(256), smem, s>>>(w);

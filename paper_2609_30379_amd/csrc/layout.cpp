@@ -140,6 +140,23 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L) {
       }
     L->attn_work = xcd_order<2>(items, cost);
   }
+  // pair attention, bias-resident form: one item per (sample, block of kAttnQB
+  // queries, group of kAttnRG pair rows); the query blocks of one row group are
+  // generated next to each other so they run back to back on one XCD and share
+  // the rows' keys and values in its L2
+  {
+    std::vector<std::array<int32_t, 4>> items;
+    std::vector<double> cost;
+    for (int32_t i = 0; i < batch; ++i) {
+      const int32_t n = lengths[i];
+      for (int32_t rg = 0; rg * kAttnRG < n; ++rg)
+        for (int32_t jb = 0; jb * kAttnQB < n; ++jb) {
+          items.push_back({i, jb, rg, 0});
+          cost.push_back((double)std::min(kAttnRG, n - rg * kAttnRG) * std::min(kAttnQB, n - jb * kAttnQB) * n);
+        }
+    }
+    L->pattn_work = xcd_order<4>(items, cost);
+  }
   // triangle: one item per (sample, 32x32 output tile), cost = valid x * valid y * N
   {
     std::vector<std::array<int32_t, 4>> items;

@@ -16,6 +16,9 @@ constexpr int kXcds = 8;          // MI355X: 8 XCDs, workgroups dispatched round
 constexpr int kTriTile = 32;      // triangle output tile: 32 x 32 cells
 constexpr int kSeqQBlock = 64;    // 1-D attention: queries per workgroup
 constexpr int kLinRows = 128;     // rows per projection workgroup (pair-row table granularity)
+constexpr int kAttnQB = 64;       // pair attention: queries per workgroup
+constexpr int kAttnRG = 16;       // pair attention: pair rows per workgroup
+constexpr int kAttnFastMaxLen = 512;  // pair attention with the bias tile resident in LDS
 
 // Attention limits imposed by staging a whole key segment in LDS.
 constexpr int kAttnMaxLenD32 = 1024;
@@ -40,6 +43,7 @@ struct nt_layout {
   std::vector<int32_t> attn_work;    // pairs (sample, row); count multiple of 8; (-1,-1) = idle
   std::vector<int32_t> tri_work;     // quads (sample, xt, yt, 0); count multiple of 8
   std::vector<int32_t> seq_work;     // pairs (sample, query block); count multiple of 8
+  std::vector<int32_t> pattn_work;   // quads (sample, query block, row group, 0); count multiple of 8
   std::vector<int32_t> prow_base;    // [sum N] P_i + a n8_i: padded offset of pair row (i, a)
   std::vector<int32_t> prow_tbase;   // [sum N] P_i + a: transposed padded offset of row (i, a)
   std::vector<int32_t> prow_n8;      // [sum N] n8_i
@@ -57,6 +61,7 @@ struct nt_layout {
   const int32_t* d_attn_work = nullptr;
   const int32_t* d_tri_work = nullptr;
   const int32_t* d_seq_work = nullptr;
+  const int32_t* d_pattn_work = nullptr;
   const int32_t* d_prow_base = nullptr;
   const int32_t* d_prow_tbase = nullptr;
   const int32_t* d_prow_n8 = nullptr;
@@ -65,6 +70,7 @@ struct nt_layout {
   int64_t attn_items() const { return (int64_t)attn_work.size() / 2; }
   int64_t tri_items() const { return (int64_t)tri_work.size() / 4; }
   int64_t seq_items() const { return (int64_t)seq_work.size() / 2; }
+  int64_t pattn_items() const { return (int64_t)pattn_work.size() / 4; }
 };
 
 namespace nt {

@@ -185,10 +185,13 @@ def _head_major(bias_cells):
 
 
 @pytest.mark.parametrize("axis", [0, 1])
-@pytest.mark.parametrize("dtype,H,D", [("bf16", 4, 32), ("bf16", 2, 64), ("f32", 2, 8)])
-def test_pair_attention(B, axis, dtype, H, D):
+@pytest.mark.parametrize("dtype,H,D,lset", [("bf16", 4, 32, "att"), ("bf16", 2, 64, "att"), ("f32", 2, 8, "tiny"),
+                                            ("bf16", 2, 32, "long")])
+def test_pair_attention(B, axis, dtype, H, D, lset):
     import torch
-    L = ATT_LENGTHS if dtype == "bf16" else LENGTHS["tiny"]
+    # "att" takes the bias-resident path for head_dim 32; "long" (a sample
+    # above 512) and head_dim 64 take the per-row path
+    L = {"att": ATT_LENGTHS, "tiny": LENGTHS["tiny"], "long": [530, 7, 64]}[lset]
     lay = _layout(B, L)
     R = sum(n * n for n in L)
     qkv = _n(23, "qkv", (R, 3 * H * D), 1.0, dtype)
