@@ -6,6 +6,8 @@
 // D^T = W X^T so that each lane ends up owning four consecutive output
 // channels of one row, which the fused epilogues (bias, residual, GELU,
 // channel-major tails) consume without a shuffle.
+#include <algorithm>
+
 #include "nt_device.h"
 #include "nt_internal.h"
 
@@ -41,6 +43,9 @@ struct LinArgs {
   const int32_t* prow_tbase;
   const int32_t* prow_n8;
   const int32_t* blk_prow;
+  const int32_t* cu_pairs;    // sample tables of the streaming kernel's pair-padded tails
+  int batch;
+  int wc, ntiles;             // streaming kernel: waves along the columns, 64-row tiles
 };
 
 // Position of packed pair row m (cell (i, x, k)) in a pair-padded channel-major
@@ -488,6 +493,221 @@ __global__ void __launch_bounds__(256) linear_res_kernel(LinArgs p) {
   }
 }
 
+// ---------------------------------------------------------------- streaming
+// Persistent projection for K in {64, 128} and up to 512 output columns (the
+// pair path).  The product is HBM-bound, so the kernel is organised around
+// keeping loads in flight: every workgroup stays resident and walks 64-row
+// tiles; the weights of each wave's output columns live in registers for the
+// whole launch; while one tile is on the matrix cores the next tile's rows
+// (and its residual) are already loading into registers, and the normalised
+// tiles alternate between two LDS buffers, so one barrier per tile suffices.
+// The eight waves split a tile as (row groups) x (column groups): a wave owns
+// column tiles wcol + wc*t and 16-row subtiles u with u % (8/wc) == wrow.
+constexpr int kStreamRows = 64;
+constexpr int kStreamThreads = 512;
+constexpr int kStreamMaxSamples = 1024;   // sample tables cached in LDS for pair-padded tails
+
+// Pair-padded position of packed pair cell m (Eq. coordinate inverted with the
+// sample tables): sample i by binary search over the pair offsets, then
+// (a, b) = divmod(m - o_i, N_i).
+__device__ __forceinline__ int32_t padded_pos_lds(const int32_t* cp, const int32_t* len, const int32_t* pad,
+                                                  int batch, int m, bool transposed) {
+  int lo = 0, hi = batch - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (cp[mid] <= m) lo = mid; else hi = mid - 1;
+  }
+  const int n = len[lo], local = m - cp[lo], n8 = (n + 7) & ~7;
+  int a = (int)((float)local / (float)n);
+  int b = local - a * n;
+  if (b < 0) { --a; b += n; } else if (b >= n) { ++a; b -= n; }
+  return pad[lo] + (transposed ? b * n8 + a : a * n8 + b);
+}
+
+template <typename XT, int EPI, int K, int NTW>
+__global__ void __launch_bounds__(kStreamThreads, 2) linear_stream_kernel(LinArgs p) {
+  constexpr int TR = kStreamRows;
+  constexpr int SKR = frag_stride<K>();
+  constexpr int KT = K / 32;
+  constexpr int TPR = kStreamThreads / TR;        // staging threads per row
+  constexpr int EPT = K / TPR;                    // elements per staging thread
+  constexpr int VX = Vec<XT>::N;
+  constexpr int NV = EPT / VX;                    // 16-byte loads per staging thread
+  using XV = typename XStage<XT>::T;
+  __shared__ __attribute__((aligned(16))) bf16 Xs[2][TR * SKR];
+  __shared__ int32_t s_cp[kStreamMaxSamples + 1], s_len[kStreamMaxSamples], s_pad[kStreamMaxSamples];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, g = lane >> 4;
+  const int wc = p.wc, wr_n = 8 / wc, wcol = wave % wc, wrow = wave / wc;
+  const int nt16 = (p.N + 15) >> 4;
+  const XT* x = static_cast<const XT*>(p.x);
+  const bool padded_tail = p.y_tail && p.tail_mode != kTailChannelMajor;
+  const bool transposed = p.tail_mode == kTailPairPaddedT;
+  int tile = blockIdx.x;
+  if (tile >= p.ntiles) return;
+
+  // ---- staging: thread owns EPT consecutive k of one row of the tile -----
+  const int srow = tid / TPR, spart = tid % TPR;
+  XV xr[NV];
+  auto load_x = [&](int t) {
+    const int m = t * TR + srow;
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+      xr[v] = m < p.rows ? *reinterpret_cast<const XV*>(x + (int64_t)m * p.ldx + spart * EPT + v * VX)
+                         : XStage<XT>::zero();
+  };
+  // residual of the wave's own output fragments, prefetched with the rows
+  uint2 rq_next[4][NTW], rq[4][NTW];
+  auto load_res = [&](int t) {
+    if constexpr (EPI == NT_EPI_RESIDUAL) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int j = 0; j < NTW; ++j) {
+          const int m = t * TR + u * 16 + l16, n = (wcol + wc * j) * 16 + 4 * g;
+          rq_next[u][j] = (u % wr_n == wrow && m < p.rows && n + 4 <= p.n_main)
+                              ? *reinterpret_cast<const uint2*>(p.res + (int64_t)m * p.ld_res + n)
+                              : make_uint2(0u, 0u);
+        }
+    }
+  };
+  load_x(tile);
+  load_res(tile);
+
+  // ---- resident weights and bias of the wave's column tiles ---------------
+  bf16x8 wf[NTW][KT];
+  float bv[NTW][4];
+#pragma unroll
+  for (int j = 0; j < NTW; ++j) {
+    const int ct = wcol + wc * j, n = ct * 16 + l16;
+#pragma unroll
+    for (int kk = 0; kk < KT; ++kk) {
+      if (ct < nt16 && n < p.N) wf[j][kk] = *reinterpret_cast<const bf16x8*>(p.w + (int64_t)n * K + kk * 32 + g * 8);
+      else wf[j][kk] = bf16x8{};
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int nb = ct * 16 + 4 * g + i;
+      bv[j][i] = (p.bias && nb < p.N) ? p.bias[nb] : 0.f;
+    }
+  }
+  if (padded_tail) {
+    for (int j = tid; j <= p.batch; j += kStreamThreads) s_cp[j] = p.cu_pairs[j];
+    for (int j = tid; j < p.batch; j += kStreamThreads) {
+      s_len[j] = p.cu_seqlens[j + 1] - p.cu_seqlens[j];
+      s_pad[j] = p.cu_pad[j];
+    }
+  }
+
+  for (int it = 0; tile < p.ntiles; ++it) {
+    const int next = tile + (int)gridDim.x;
+    bf16* xs = Xs[it & 1];
+    // ---- LayerNorm of the staged rows into this tile's LDS buffer ---------
+    {
+      float v[EPT];
+#pragma unroll
+      for (int vv = 0; vv < NV; ++vv) XStage<XT>::unpack(xr[vv], v + vv * VX);
+      const bool valid = tile * TR + srow < p.rows;
+      if (p.gamma) {
+        float s = 0.f;
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) s += v[e];
+        const float mean = group_sum<TPR>(s) / (float)K;
+        float q = 0.f;
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) { const float d = v[e] - mean; q += d * d; }
+        const float rstd = valid ? rsqrtf(group_sum<TPR>(q) / (float)K + p.eps) : 0.f;
+#pragma unroll
+        for (int e = 0; e < EPT; e += 4) {
+          const float4 ga = *reinterpret_cast<const float4*>(p.gamma + spart * EPT + e);
+          const float4 be = p.beta ? *reinterpret_cast<const float4*>(p.beta + spart * EPT + e)
+                                   : make_float4(0.f, 0.f, 0.f, 0.f);
+          v[e] = valid ? (v[e] - mean) * rstd * ga.x + be.x : 0.f;
+          v[e + 1] = valid ? (v[e + 1] - mean) * rstd * ga.y + be.y : 0.f;
+          v[e + 2] = valid ? (v[e + 2] - mean) * rstd * ga.z + be.z : 0.f;
+          v[e + 3] = valid ? (v[e + 3] - mean) * rstd * ga.w + be.w : 0.f;
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < EPT; e += 8) {
+        bf16x8 o;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) o[j] = (bf16)v[e + j];
+        *reinterpret_cast<bf16x8*>(&xs[srow * SKR + spart * EPT + e]) = o;
+      }
+    }
+    if constexpr (EPI == NT_EPI_RESIDUAL) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int j = 0; j < NTW; ++j) rq[u][j] = rq_next[u][j];
+    }
+    if (next < p.ntiles) {
+      load_x(next);
+      load_res(next);
+    }
+    __syncthreads();
+
+    // ---- the wave's subtiles: resident weights x staged rows ---------------
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (u % wr_n != wrow) continue;
+      bf16x8 xf[KT];
+#pragma unroll
+      for (int kk = 0; kk < KT; ++kk) xf[kk] = *reinterpret_cast<const bf16x8*>(&xs[(u * 16 + l16) * SKR + kk * 32 + g * 8]);
+      f32x4 acc[NTW];
+#pragma unroll
+      for (int j = 0; j < NTW; ++j) {
+        acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (wcol + wc * j < nt16) {
+#pragma unroll
+          for (int kk = 0; kk < KT; ++kk) acc[j] = mfma16(wf[j][kk], xf[kk], acc[j]);
+        }
+      }
+      const int m = tile * TR + u * 16 + l16;
+      if (m >= p.rows) continue;
+      int32_t tpos = m;
+      if (padded_tail) tpos = padded_pos_lds(s_cp, s_len, s_pad, p.batch, m, transposed);
+#pragma unroll
+      for (int j = 0; j < NTW; ++j) {
+        const int n = (wcol + wc * j) * 16 + 4 * g;
+        if (n >= p.N) continue;
+        float r[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          r[i] = acc[j][i] + bv[j][i];
+          if constexpr (EPI == NT_EPI_GELU) r[i] = gelu_erf(r[i]);
+        }
+        if (n + 4 <= p.n_main) {
+          if constexpr (EPI == NT_EPI_RESIDUAL) {
+            r[0] += __uint_as_float(rq[u][j].x << 16); r[1] += __uint_as_float(rq[u][j].x & 0xffff0000u);
+            r[2] += __uint_as_float(rq[u][j].y << 16); r[3] += __uint_as_float(rq[u][j].y & 0xffff0000u);
+          }
+          bf16x4 o;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) o[i] = (bf16)r[i];
+          *reinterpret_cast<bf16x4*>(p.y + (int64_t)m * p.ldy + n) = o;
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int nn = n + i;
+            if (nn >= p.N) break;
+            if (nn < p.n_main) {
+              float val = r[i];
+              if constexpr (EPI == NT_EPI_RESIDUAL) val += (float)p.res[(int64_t)m * p.ld_res + nn];
+              p.y[(int64_t)m * p.ldy + nn] = (bf16)val;
+            } else {
+              p.y_tail[(int64_t)(nn - p.n_main) * p.ld_tail + tpos] = (bf16)r[i];
+            }
+          }
+        }
+      }
+    }
+    tile = next;
+  }
+}
+
 // ---------------------------------------------------------------- SwiGLU
 // Pre-normalised SwiGLU transition (Eq. running-block, second line):
 //   y = res + (silu(LN(x) Wg^T + bg) * (LN(x) Wu^T + bu)) Wd^T + bd.
@@ -776,6 +996,35 @@ __global__ void __launch_bounds__(256) linear_f32_kernel(F32Args p) {
   }
 }
 
+// Compute units of the current device (cached per device).
+int compute_units() {
+  static int cache[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cache[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cache[dev] = n;
+  }
+  return cache[dev];
+}
+
+// One resident workgroup per slot: grid = min(tiles, resident workgroups per
+// CU x CUs); every workgroup walks tiles blockIdx.x + j * gridDim.x.
+template <typename XT, int EPI, int K, int NTW>
+void launch_stream(const LinArgs& p, hipStream_t s) {
+  static int per_cu = 0;
+  if (per_cu == 0) {
+    int nb = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, linear_stream_kernel<XT, EPI, K, NTW>, kStreamThreads, 0) !=
+            hipSuccess || nb < 1)
+      nb = 1;
+    per_cu = nb;
+  }
+  const int grid = std::min(p.ntiles, per_cu * compute_units());
+  linear_stream_kernel<XT, EPI, K, NTW><<<dim3((unsigned)grid), dim3(kStreamThreads), 0, s>>>(p);
+}
+
 }  // namespace
 
 hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
@@ -836,6 +1085,33 @@ hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
   p.mblocks = (rows + BM - 1) / BM;
   p.nblocks = (a.c_out + BN - 1) / BN;
   const bool xf = a.x_dtype == NT_F32;
+
+  const bool padded = p.y_tail && p.tail_mode != kTailChannelMajor;
+  if ((a.c_in == 64 || a.c_in == 128) && a.c_out <= 512 &&
+      (!padded || (plan.layout && plan.layout->batch <= kStreamMaxSamples))) {
+    if (padded) { p.cu_pairs = plan.layout->d_cu_pairs; p.batch = plan.layout->batch; }
+    const int nt16 = (a.c_out + 15) / 16;
+    const int ntw = nt16 <= 16 ? 2 : 4;
+    int wc = 2;
+    while (wc < 8 && wc * ntw < nt16) wc *= 2;
+    p.wc = wc;
+    p.ntiles = (rows + kStreamRows - 1) / kStreamRows;
+#define NT_ST(XT, EPI, KK, W) launch_stream<XT, EPI, KK, W>(p, s)
+#define NT_ST_W(XT, EPI, KK) do { if (ntw == 2) NT_ST(XT, EPI, KK, 2); else NT_ST(XT, EPI, KK, 4); } while (0)
+#define NT_ST_K(XT, EPI) do { if (a.c_in == 64) NT_ST_W(XT, EPI, 64); else NT_ST_W(XT, EPI, 128); } while (0)
+#define NT_ST_X(EPI) do { if (xf) NT_ST_K(float, EPI); else NT_ST_K(bf16, EPI); } while (0)
+    switch (a.epilogue) {
+      case NT_EPI_NONE: NT_ST_X(NT_EPI_NONE); break;
+      case NT_EPI_RESIDUAL: NT_ST_X(NT_EPI_RESIDUAL); break;
+      case NT_EPI_GELU: NT_ST_X(NT_EPI_GELU); break;
+      default: return hipErrorInvalidValue;
+    }
+#undef NT_ST_X
+#undef NT_ST_K
+#undef NT_ST_W
+#undef NT_ST
+    return hipGetLastError();
+  }
   if (a.c_in == 64 || a.c_in == 128 || a.c_in == 256) {
     const dim3 g1((unsigned)p.mblocks), b1(256);
 #define NT_RES(XT, EPI, KK) linear_res_kernel<XT, EPI, KK><<<g1, b1, 0, s>>>(p)

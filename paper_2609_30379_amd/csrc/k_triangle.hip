@@ -4,17 +4,25 @@
 //
 // Operands arrive pair-padded channel-major (rows start 16-byte aligned), so
 // every matrix-core fragment is one 16-byte load.  A workgroup owns a 32x32
-// cell tile of one sample and 32 channels (8 per wave); each lane finishes
-// holding 8 consecutive channels of one cell for every accumulator slot,
-// which makes the z update a 16-byte read-modify-write.
+// cell tile of one sample and a block of 16 channels (4 per wave).  Workgroup
+// ids interleave the channel blocks of each tile, so with 8 blocks (C = 128)
+// XCD x (ids = x mod 8) always works on channel block x: it walks the tile
+// list sample by sample and keeps the current sample's 16 channel planes
+// (2 x 16 x N^2 x 2 bytes, about 3 MB at N = 216) in its own L2, where the
+// operand re-reads of neighbouring tiles hit.  The next k-step's fragments
+// are loaded while the current one is on the matrix cores; with 64
+// accumulator registers per lane two waves fit on each SIMD.
 #include "nt_device.h"
 #include "nt_internal.h"
 
 namespace nt {
 namespace {
 
+constexpr int kTriCB = 16;    // channels per workgroup
+constexpr int kTriCW = 4;     // channels per wave
+
 struct TriArgs {
-  int C, ncb;
+  int C, nblk;
   const bf16* a;
   const bf16* b;
   int64_t ld_ab;
@@ -26,6 +34,8 @@ struct TriArgs {
   const int32_t* cu_pad;
 };
 
+// Fragment of rows row..row+15 (lane row = l16) and k..k+7 of one plane;
+// rows past the sample and k past N read as zero.
 __device__ __forceinline__ bf16x8 load_frag(const bf16* plane, int row, int k, int n, int n8, bool tail) {
   if (row >= n || k >= n) return bf16x8{};
   bf16x8 f = *reinterpret_cast<const bf16x8*>(plane + (int64_t)row * n8 + k);
@@ -37,12 +47,9 @@ __device__ __forceinline__ bf16x8 load_frag(const bf16* plane, int row, int k, i
   return f;
 }
 
-__global__ void __launch_bounds__(256) triangle_mfma_kernel(TriArgs p) {
-  // XCD-aware order: consecutive channel blocks of one tile run on one XCD.
+__global__ void __launch_bounds__(256, 2) triangle_mfma_kernel(TriArgs p) {
   const int id = blockIdx.x;
-  const int xcd = id % kXcds, kq = id / kXcds;
-  const int item = (kq / p.ncb) * kXcds + xcd;
-  const int cb = kq % p.ncb;
+  const int item = id / p.nblk, cb = id % p.nblk;
   const int i = p.work[4 * item];
   if (i < 0) return;
   const int xt = p.work[4 * item + 1], yt = p.work[4 * item + 2];
@@ -52,49 +59,65 @@ __global__ void __launch_bounds__(256) triangle_mfma_kernel(TriArgs p) {
   const int x0 = xt * kTriTile, y0 = yt * kTriTile;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, g = lane >> 4;
-  const int c0 = cb * 32 + wave * 8;
+  const int c0 = cb * kTriCB + wave * kTriCW;
 
-  f32x4 acc[8][2][2];
+  const bf16* ap[kTriCW];
+  const bf16* bp[kTriCW];
 #pragma unroll
-  for (int ch = 0; ch < 8; ++ch)
+  for (int ch = 0; ch < kTriCW; ++ch) {
+    ap[ch] = p.a + (int64_t)(c0 + ch) * p.ld_ab + P;
+    bp[ch] = p.b + (int64_t)(c0 + ch) * p.ld_ab + P;
+  }
+  f32x4 acc[kTriCW][2][2];
+#pragma unroll
+  for (int ch = 0; ch < kTriCW; ++ch)
 #pragma unroll
     for (int xs = 0; xs < 2; ++xs)
 #pragma unroll
       for (int ys = 0; ys < 2; ++ys) acc[ch][xs][ys] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int k0 = 0; k0 < n; k0 += 32) {
+  bf16x8 fa[kTriCW][2], fb[kTriCW][2];
+  auto load_step = [&](int k0, bf16x8 (&ra)[kTriCW][2], bf16x8 (&rb)[kTriCW][2]) {
     const int k = k0 + 8 * g;
     const bool tail = k0 + 32 > n;
 #pragma unroll
-    for (int ch = 0; ch < 8; ++ch) {
-      const bf16* ap = p.a + (int64_t)(c0 + ch) * p.ld_ab + P;
-      const bf16* bp = p.b + (int64_t)(c0 + ch) * p.ld_ab + P;
-      const bf16x8 a0 = load_frag(ap, x0 + l16, k, n, n8, tail);
-      const bf16x8 a1 = load_frag(ap, x0 + 16 + l16, k, n, n8, tail);
-      const bf16x8 b0 = load_frag(bp, y0 + l16, k, n, n8, tail);
-      const bf16x8 b1 = load_frag(bp, y0 + 16 + l16, k, n, n8, tail);
-      acc[ch][0][0] = mfma16(a0, b0, acc[ch][0][0]);
-      acc[ch][0][1] = mfma16(a0, b1, acc[ch][0][1]);
-      acc[ch][1][0] = mfma16(a1, b0, acc[ch][1][0]);
-      acc[ch][1][1] = mfma16(a1, b1, acc[ch][1][1]);
-    }
+    for (int ch = 0; ch < kTriCW; ++ch)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        ra[ch][h] = load_frag(ap[ch], x0 + 16 * h + l16, k, n, n8, tail);
+        rb[ch][h] = load_frag(bp[ch], y0 + 16 * h + l16, k, n, n8, tail);
+      }
+  };
+  load_step(0, fa, fb);
+  for (int k0 = 0; k0 < n; k0 += 32) {
+    bf16x8 na[kTriCW][2], nb[kTriCW][2];
+    load_step(k0 + 32, na, nb);              // all-zero without a load past the last step
+#pragma unroll
+    for (int ch = 0; ch < kTriCW; ++ch)
+#pragma unroll
+      for (int xs = 0; xs < 2; ++xs)
+#pragma unroll
+        for (int ys = 0; ys < 2; ++ys) acc[ch][xs][ys] = mfma16(fa[ch][xs], fb[ch][ys], acc[ch][xs][ys]);
+#pragma unroll
+    for (int ch = 0; ch < kTriCW; ++ch)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) { fa[ch][h] = na[ch][h]; fb[ch][h] = nb[ch][h]; }
   }
 
-  // acc[ch][xs][ys][i] = T_{c0+ch}[x0 + 16xs + 4g + i][y0 + 16ys + l16]
+  // acc[ch][xs][ys][r] = T_{c0+ch}[x0 + 16xs + 4g + r][y0 + 16ys + l16]
 #pragma unroll
   for (int xs = 0; xs < 2; ++xs)
 #pragma unroll
     for (int ys = 0; ys < 2; ++ys)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int x = x0 + 16 * xs + 4 * g + i, y = y0 + 16 * ys + l16;
+      for (int r = 0; r < 4; ++r) {
+        const int x = x0 + 16 * xs + 4 * g + r, y = y0 + 16 * ys + l16;
         if (x >= n || y >= n) continue;
-        bf16* zp = p.z + (cu + (int64_t)x * n + y) * p.ld_z + c0;
-        Vec<bf16> zz;
-        zz.load(zp);
+        bf16x4* zp = reinterpret_cast<bf16x4*>(p.z + (cu + (int64_t)x * n + y) * p.ld_z + c0);
+        bf16x4 zz = *zp;
 #pragma unroll
-        for (int ch = 0; ch < 8; ++ch) zz.v[ch] += acc[ch][xs][ys][i];
-        zz.store(zp);
+        for (int ch = 0; ch < kTriCW; ++ch) zz[ch] = (bf16)((float)zz[ch] + acc[ch][xs][ys][r]);
+        *zp = zz;
       }
 }
 
@@ -146,10 +169,10 @@ hipError_t launch_triangle(const nt_layout& L, int C, const void* a, const void*
     triangle_f32_kernel<<<dim3((unsigned)items), dim3(256), 0, s>>>(t);
     return hipGetLastError();
   }
-  const int ncb = C / 32;
-  TriArgs t{C, ncb, (const bf16*)a, (const bf16*)b, ld_ab, (bf16*)z, ld_z, L.d_tri_work, L.d_cu_seqlens,
+  const int nblk = C / kTriCB;
+  TriArgs t{C, nblk, (const bf16*)a, (const bf16*)b, ld_ab, (bf16*)z, ld_z, L.d_tri_work, L.d_cu_seqlens,
             L.d_cu_pairs, L.d_cu_pad};
-  triangle_mfma_kernel<<<dim3((unsigned)(items * ncb)), dim3(256), 0, s>>>(t);
+  triangle_mfma_kernel<<<dim3((unsigned)(items * nblk)), dim3(256), 0, s>>>(t);
   return hipGetLastError();
 }
 

@@ -157,21 +157,27 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L) {
     }
     L->pattn_work = xcd_order<4>(items, cost);
   }
-  // triangle: one item per (sample, 32x32 output tile), cost = valid x * valid y * N
+  // triangle: one item per (sample, 32x32 output tile), largest samples first.
+  // The channel blocks, not the tiles, are spread over the XCDs (the launch
+  // interleaves every tile's channel blocks), so each XCD walks the whole list
+  // for its own channels and holds one sample's channel planes in its L2 at a
+  // time; the list is padded to a multiple of 8 with idle items.
   {
-    std::vector<std::array<int32_t, 4>> items;
-    std::vector<double> cost;
-    for (int32_t i = 0; i < batch; ++i) {
+    std::vector<int32_t> order(batch);
+    std::iota(order.begin(), order.end(), 0);
+    std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) { return lengths[a] > lengths[b]; });
+    L->tri_work.clear();
+    for (int32_t i : order) {
       const int32_t n = lengths[i], nt = (n + kTriTile - 1) / kTriTile;
       for (int32_t xt = 0; xt < nt; ++xt)
         for (int32_t yt = 0; yt < nt; ++yt) {
-          items.push_back({i, xt, yt, 0});
-          const double vx = std::min(kTriTile, n - xt * kTriTile);
-          const double vy = std::min(kTriTile, n - yt * kTriTile);
-          cost.push_back(vx * vy * n);
+          L->tri_work.push_back(i);
+          L->tri_work.push_back(xt);
+          L->tri_work.push_back(yt);
+          L->tri_work.push_back(0);
         }
     }
-    L->tri_work = xcd_order<4>(items, cost);
+    while ((L->tri_work.size() / 4) % kXcds) L->tri_work.insert(L->tri_work.end(), {-1, -1, -1, -1});
   }
   // 1-D attention: one item per (sample, block of kSeqQBlock queries), cost = queries * N_i
   {
