@@ -12,12 +12,18 @@
  * Packed layouts used by the calls below (all row-major, elements not bytes):
  *   singles      [sum_i N_i, C]        row eta_i + a         (eta = cu_seqlens)
  *   square pairs [sum_i N_i^2, C]      row o_i + a N_i + b   (Eq. coordinate)
- *   pair-padded channel-major operands of the triangle update: channel c of
- *                cell (i,a,b) at c*ld + P_i + a n8_i + b, where n8_i = N_i
- *                rounded up to a multiple of 8 and P_i = sum_{j<i} N_j n8_j
- *                (every operand row starts 16-byte aligned; entries b >= N_i
- *                are padding and never read as data); the transposed variant
- *                stores cell (i,a,b) at c*ld + P_i + b n8_i + a
+ *   pair-tiled channel-major operands of the triangle update: channel c of
+ *                sample i is an N_i x N_i plane (row r, column k) stored from
+ *                c*ld + P_i, cut into 16 x 32 tiles (row tiles outer, tile
+ *                (r/16, k/32) at ((r/16) nkt_i + k/32) * 512 with
+ *                nkt_i = ceil(N_i/32)), element (r,k) inside its tile at
+ *                ((k%32)/8 * 16 + r%16) * 8 + k%8 -- the lane order of a
+ *                matrix-core fragment, so a wave reads 1 KB contiguously.
+ *                A plane spans n16_i n32_i elements (N_i rounded up to 16 and
+ *                to 32) and P_i = sum_{j<i} n16_j n32_j; entries outside the
+ *                N_i x N_i matrix are padding and never read as data.  Plain
+ *                variant: cell (i,a,b) is element (r,k) = (a,b); transposed
+ *                variant: (r,k) = (b,a)
  *   head-major pair bias: [H][sum_i N_i^2], head h of cell at h*ld + cell
  * Row strides ("ld_*") are in elements and let callers address column slices
  * of a wider buffer (e.g. u and v inside one [sum N, 2C] projection).
@@ -74,8 +80,8 @@ typedef enum { NT_LEVEL_SINGLES = 0, NT_LEVEL_PAIRS = 1 } nt_level;
 /* Layout of the columns that nt_layernorm_linear routes to y_tail. */
 typedef enum {
   NT_TAIL_CHANNEL_MAJOR = 0,   /* column j of row r at j*ld_tail + r               */
-  NT_TAIL_PAIR_PADDED = 1,     /* pair-padded channel-major (needs a pair layout)  */
-  NT_TAIL_PAIR_PADDED_T = 2    /* transposed pair-padded channel-major             */
+  NT_TAIL_PAIR_TILED = 1,      /* pair-tiled channel-major (needs a pair layout)   */
+  NT_TAIL_PAIR_TILED_T = 2     /* transposed pair-tiled channel-major              */
 } nt_tail_layout;
 
 enum { NT_LAYOUT_HOST_ONLY = 1u };           /* nt_from_*: no device mirrors */
@@ -90,7 +96,7 @@ typedef enum {
   NT_ARR_ATTN_WORK = 5,        /* pair-row work map (sample, row) pairs, XCD-ordered */
   NT_ARR_TRI_WORK = 6,         /* triangle tile map (sample, x-tile, y-tile, 0) quads */
   NT_ARR_SEQ_WORK = 7,         /* 1-D attention map (sample, query block) pairs */
-  NT_ARR_CU_PAD = 8            /* P_i offsets of pair-padded operands, [B+1]    */
+  NT_ARR_CU_PAD = 8            /* P_i offsets of pair-tiled operands, [B+1]     */
 } nt_array;
 
 typedef struct {
@@ -99,7 +105,7 @@ typedef struct {
   int64_t sum_n;               /* sum_i N_i    (rows of a single tensor)         */
   int64_t sum_n2;              /* sum_i N_i^2  (rows of a square pair tensor)    */
   int64_t sum_n3;              /* sum_i N_i^3  (work of the pair contractions)   */
-  int64_t sum_pad;             /* sum_i N_i n8_i (channel stride of pair-padded operands) */
+  int64_t sum_pad;             /* sum_i n16_i n32_i (channel extent of pair-tiled operands) */
   const int32_t* d_cu_seqlens; /* device mirrors (NULL for host-only layouts)   */
   const int32_t* d_cu_pairs;
   const int32_t* d_row_splits2;
@@ -202,7 +208,7 @@ typedef struct {
 /* Errors: NT_ERR_INVALID_ARG, NT_ERR_LAYOUT_MISMATCH (residual_layout differs
  * from layout, or rows differ from the layout's count), NT_ERR_UNSUPPORTED
  * (bf16 SwiGLU unless x is bf16, K == N in {64, 128, 256} and F % 32 == 0;
- * f32 SwiGLU with K > 1024 or F > 4096; n_tail with SwiGLU; a pair-padded
+ * f32 SwiGLU with K > 1024 or F > 4096; n_tail with SwiGLU; a pair-tiled
  * tail without a pair layout).  ln_gamma/ln_beta must be 16-byte aligned.    */
 nt_status nt_layernorm_linear(const nt_linear_args* args, void* stream);
 
@@ -237,10 +243,10 @@ nt_status nt_pair_row_attention(const nt_layout* layout, int32_t axis,
  * Pairformer; reading: no gates, no output projection), accumulated into z:
  *   direction 0 (outgoing)  z[cell(x,y),c] += sum_k a_c[x,k] b_c[y,k]
  *   direction 1 (incoming)  z[cell(x,y),c] += sum_k a_c[k,x] b_c[k,y]
- * a, b are pair-padded channel-major with channel stride ld_ab (>= sum_pad):
- * for direction 0 in the plain variant (a_c[x,k] at c*ld_ab + P_i + x n8_i + k),
- * for direction 1 in the transposed variant (a_c[k,x] at c*ld_ab + P_i + x n8_i + k),
- * which is what nt_layernorm_linear writes with NT_TAIL_PAIR_PADDED(_T); the
+ * a, b are pair-tiled channel-major with channel stride ld_ab (>= sum_pad):
+ * for direction 0 in the plain variant (a_c[x,k] is plane element (x,k)),
+ * for direction 1 in the transposed variant (a_c[k,x] is plane element (x,k)),
+ * which is what nt_layernorm_linear writes with NT_TAIL_PAIR_TILED(_T); the
  * incoming update is then the outgoing contraction of the transposes.  z is the
  * channel-last pair state [sum N^2, C] with row stride ld_z.  One ragged grouped
  * GEMM over all samples and channels; fp32 accumulation, z rounded once.

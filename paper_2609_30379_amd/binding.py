@@ -20,7 +20,7 @@ NT_OK, NT_ERR_INVALID_ARG, NT_ERR_LAYOUT_MISMATCH, NT_ERR_OVERFLOW, NT_ERR_UNSUP
 NT_F32, NT_BF16 = 0, 1
 EPILOGUES = {"none": 0, "residual": 1, "swiglu_residual": 2, "gelu": 3}
 LEVELS = {"singles": 0, "pairs": 1}
-TAILS = {"channel_major": 0, "pair_padded": 1, "pair_padded_t": 2}
+TAILS = {"channel_major": 0, "pair_tiled": 1, "pair_tiled_t": 2}
 ARRAYS = {"lengths": 0, "cu_seqlens": 1, "cu_pairs": 2, "row_splits2": 3, "row_sample": 4,
           "attn_work": 5, "tri_work": 6, "seq_work": 7, "cu_pad": 8}
 NT_LAYOUT_HOST_ONLY = 1
@@ -209,7 +209,7 @@ def nt_pair_row_attention(layout: NestedLayout, axis: int, heads: int, head_dim:
 
 
 def nt_triangle_mul(layout: NestedLayout, direction: int, a, b, z):
-    """a, b: pair-padded channel-major operands [C, >= sum_pad] (rows = channels)."""
+    """a, b: pair-tiled channel-major operands [C, >= sum_pad] (rows = channels)."""
     pz, ldz = _mat(z, "z")
     _check(load().nt_triangle_mul(layout.handle, int(direction), int(z.size(1)), _ptr(a), _ptr(b),
                                   int(a.stride(0)), pz, ldz, _dtype(z), _stream()))

@@ -138,7 +138,7 @@ def pair_block(layout: B.NestedLayout, s, W: dict, dims: dict, order, ws: PairWo
             with _op("tri_proj"):
                 B.nt_layernorm_linear(z, W[step + ".w"], W[step + ".b"], None,
                                       ln=(W[step + ".ln_g"], W[step + ".ln_b"]), n_tail=2 * C, y_tail=ws.ab,
-                                      tail_layout="pair_padded" if step == "tri_out" else "pair_padded_t",
+                                      tail_layout="pair_tiled" if step == "tri_out" else "pair_tiled_t",
                                       layout=layout, level="pairs", c_out=2 * C)
             with _op("triangle_" + step[4:]):
                 B.nt_triangle_mul(layout, 0 if step == "tri_out" else 1, ws.ab[:C], ws.ab[C:], z)

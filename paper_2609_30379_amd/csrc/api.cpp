@@ -39,8 +39,7 @@ nt_status upload(nt_layout* L, hipStream_t s) {
       {&L->cu_pairs, &L->d_cu_pairs},     {&L->cu_pad, &L->d_cu_pad},
       {&L->row_splits2, &L->d_row_splits2}, {&L->row_sample, &L->d_row_sample},
       {&L->attn_work, &L->d_attn_work},   {&L->tri_work, &L->d_tri_work},
-      {&L->seq_work, &L->d_seq_work},     {&L->prow_base, &L->d_prow_base},
-      {&L->prow_tbase, &L->d_prow_tbase}, {&L->prow_n8, &L->d_prow_n8},
+      {&L->seq_work, &L->d_seq_work},
       {&L->blk_prow, &L->d_blk_prow},     {&L->pattn_work, &L->d_pattn_work},
   };
   size_t total = 0;
@@ -224,12 +223,12 @@ nt_status nt_layernorm_linear(const nt_linear_args* a, void* stream) {
   const int vx = vec_elems(a->x_dtype), vy = vec_elems(a->dtype);
   if (a->ldx < a->c_in || a->ldx % vx) return nt::fail(NT_ERR_INVALID_ARG, "ldx must be >= c_in and a multiple of the vector width");
   if (a->n_tail < 0 || a->n_tail > a->c_out) return nt::fail(NT_ERR_INVALID_ARG, "n_tail out of range");
-  if (a->tail_layout < NT_TAIL_CHANNEL_MAJOR || a->tail_layout > NT_TAIL_PAIR_PADDED_T)
+  if (a->tail_layout < NT_TAIL_CHANNEL_MAJOR || a->tail_layout > NT_TAIL_PAIR_TILED_T)
     return nt::fail(NT_ERR_INVALID_ARG, "bad tail_layout");
   const int n_main = a->c_out - a->n_tail;
   if (a->layout) {
     if (!a->layout->has_device && a->n_tail && a->tail_layout != NT_TAIL_CHANNEL_MAJOR)
-      return nt::fail(NT_ERR_INVALID_ARG, "pair-padded tails need a layout with device mirrors");
+      return nt::fail(NT_ERR_INVALID_ARG, "pair-tiled tails need a layout with device mirrors");
     const int64_t expect = a->level == NT_LEVEL_PAIRS ? a->layout->sum_n2 : a->layout->sum_n;
     if (a->level != NT_LEVEL_PAIRS && a->level != NT_LEVEL_SINGLES) return nt::fail(NT_ERR_INVALID_ARG, "bad level");
     if (expect != a->rows) return nt::fail(NT_ERR_LAYOUT_MISMATCH, "rows differ from the layout's row count");
@@ -238,7 +237,7 @@ nt_status nt_layernorm_linear(const nt_linear_args* a, void* stream) {
     return nt::fail(NT_ERR_LAYOUT_MISMATCH, "residual has a different logical partition than x");
   if (a->n_tail && a->tail_layout != NT_TAIL_CHANNEL_MAJOR &&
       (!a->layout || a->level != NT_LEVEL_PAIRS))
-    return nt::fail(NT_ERR_UNSUPPORTED, "pair-padded tail output needs a pair-level layout");
+    return nt::fail(NT_ERR_UNSUPPORTED, "pair-tiled tail output needs a pair-level layout");
   if (swiglu) {
     if (a->dtype == NT_BF16 && (a->c_in != a->c_out || (a->c_in != 64 && a->c_in != 128 && a->c_in != 256) ||
                                 a->hidden <= 0 || a->hidden % 32 || a->x_dtype != NT_BF16))
@@ -266,6 +265,8 @@ nt_status nt_layernorm_linear(const nt_linear_args* a, void* stream) {
   if (a->n_tail > 0) {
     const int64_t need = a->tail_layout == NT_TAIL_CHANNEL_MAJOR ? a->rows : a->layout->sum_pad;
     if (a->ld_tail < need) return nt::fail(NT_ERR_INVALID_ARG, "ld_tail is smaller than the tail's row extent");
+    if (a->tail_layout != NT_TAIL_CHANNEL_MAJOR && a->ld_tail % 8)
+      return nt::fail(NT_ERR_INVALID_ARG, "pair-tiled tails need ld_tail % 8 == 0");
   }
   nt::LinearPlan p{a, a->tail_layout, a->layout};
   return check_hip(nt::launch_linear(p, static_cast<hipStream_t>(stream)), "nt_layernorm_linear launch");

@@ -39,18 +39,22 @@ struct LinArgs {
   const int32_t* cu_pad;
   int sum_n;
   int mblocks, nblocks;
-  const int32_t* prow_base;   // pair-row tables of the pair-padded tail layouts
-  const int32_t* prow_tbase;
-  const int32_t* prow_n8;
-  const int32_t* blk_prow;
-  const int32_t* cu_pairs;    // sample tables of the streaming kernel's pair-padded tails
+  const int32_t* blk_prow;    // first pair row of every kLinRows-cell block
+  const int32_t* cu_pairs;    // sample tables of the streaming kernel's pair-tiled tails
   int batch;
   int wc, ntiles;             // streaming kernel: waves along the columns, 64-row tiles
 };
 
-// Position of packed pair row m (cell (i, x, k)) in a pair-padded channel-major
-// block: P_i + x n8_i + k, or P_i + k n8_i + x when transposed.
-__device__ __forceinline__ int64_t pair_padded_pos(const LinArgs& p, int m) {
+// Position of the pair cell (a, b) of sample i in its pair-tiled operand plane:
+// row a, column b, or row b, column a for the transposed (incoming) operand.
+__device__ __forceinline__ int32_t tiled_cell_pos(int32_t P, int n, int a, int b, bool transposed) {
+  const int nkt = (n + 31) >> 5;
+  return P + (transposed ? tiled_offset(b, a, nkt) : tiled_offset(a, b, nkt));
+}
+
+// Pair-tiled position of packed pair row m (cell (i, a, b)): pair row by
+// binary search over the level-2 row splits.
+__device__ __forceinline__ int32_t pair_tiled_pos(const LinArgs& p, int m) {
   int lo = 0, hi = p.sum_n - 1;               // largest eta with row_splits2[eta] <= m
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
@@ -58,10 +62,7 @@ __device__ __forceinline__ int64_t pair_padded_pos(const LinArgs& p, int m) {
   }
   const int i = p.row_sample[lo];
   const int n = p.cu_seqlens[i + 1] - p.cu_seqlens[i];
-  const int n8 = (n + 7) & ~7;
-  const int x = lo - p.cu_seqlens[i];
-  const int k = m - p.row_splits2[lo];
-  return (int64_t)p.cu_pad[i] + (p.tail_mode == kTailPairPadded ? (int64_t)x * n8 + k : (int64_t)k * n8 + x);
+  return tiled_cell_pos(p.cu_pad[i], n, lo - p.cu_seqlens[i], m - p.row_splits2[lo], p.tail_mode == kTailPairTiledT);
 }
 
 __device__ __forceinline__ float gelu_erf(float v) { return 0.5f * v * (1.f + erff(v * 0.70710678118654752f)); }
@@ -248,7 +249,7 @@ __global__ void __launch_bounds__(256) linear_mfma_kernel(LinArgs p) {
     const int m = m0 + wm_off + b * 16 + l16;
     if (m >= p.rows) continue;
     int64_t tpos = m;
-    if (p.y_tail && p.tail_mode != kTailChannelMajor && n0 + BN > p.n_main) tpos = pair_padded_pos(p, m);
+    if (p.y_tail && p.tail_mode != kTailChannelMajor && n0 + BN > p.n_main) tpos = pair_tiled_pos(p, m);
 #pragma unroll
     for (int a = 0; a < 4; ++a) {
       const int n = n0 + wn_off + a * 16 + g * 4;
@@ -293,7 +294,7 @@ __global__ void __launch_bounds__(256) linear_mfma_kernel(LinArgs p) {
 // sit in LDS after a single global round trip, LayerNorm statistics come from
 // registers (two threads per row), and the next weight block is prefetched
 // into registers while the current one runs on the matrix cores.  Rows of a
-// pair-level input are cells; their pair-padded tail offsets come from the
+// pair-level input are cells; their pair-tiled tail offsets come from the
 // per-pair-row tables (first pair row of the tile from blk_prow, the tile's
 // row splits cached in LDS).
 // LDS row stride (elements) for 16-byte fragment reads of a K-wide bf16 tile:
@@ -342,9 +343,9 @@ __global__ void __launch_bounds__(256) linear_res_kernel(LinArgs p) {
     }
   };
   load_w(0);
-  const bool padded_tail = p.y_tail && p.tail_mode != kTailChannelMajor;
+  const bool tiled_tail = p.y_tail && p.tail_mode != kTailChannelMajor;
   int eta0 = 0;
-  if (padded_tail) {
+  if (tiled_tail) {
     eta0 = p.blk_prow[mb];
     for (int j = tid; j <= BM; j += 256) rs[j] = p.row_splits2[min(eta0 + j, p.sum_n)];
   }
@@ -402,21 +403,22 @@ __global__ void __launch_bounds__(256) linear_res_kernel(LinArgs p) {
   store_w();
   __syncthreads();
 
-  // pair-padded offsets of the lane's four rows
+  // pair-tiled offsets of the lane's four rows
   const int wn_off = (wave >> 1) * 64, wm_off = (wave & 1) * 64;
   int32_t tpos[4];
 #pragma unroll
   for (int b = 0; b < 4; ++b) {
     const int m = m0 + wm_off + b * 16 + l16;
     tpos[b] = m;
-    if (padded_tail && m < p.rows) {
+    if (tiled_tail && m < p.rows) {
       int lo = 0, hi = min(BM, p.sum_n - eta0) - 1;
       while (lo < hi) {
         const int mid = (lo + hi + 1) >> 1;
         if (rs[mid] <= m) lo = mid; else hi = mid - 1;
       }
-      const int eta = eta0 + lo, kk = m - rs[lo];
-      tpos[b] = p.tail_mode == kTailPairPadded ? p.prow_base[eta] + kk : p.prow_tbase[eta] + kk * p.prow_n8[eta];
+      const int eta = eta0 + lo, i = p.row_sample[eta];
+      tpos[b] = tiled_cell_pos(p.cu_pad[i], p.cu_seqlens[i + 1] - p.cu_seqlens[i], eta - p.cu_seqlens[i], m - rs[lo],
+                               p.tail_mode == kTailPairTiledT);
     }
   }
 
@@ -505,23 +507,23 @@ __global__ void __launch_bounds__(256) linear_res_kernel(LinArgs p) {
 // column tiles wcol + wc*t and 16-row subtiles u with u % (8/wc) == wrow.
 constexpr int kStreamRows = 64;
 constexpr int kStreamThreads = 512;
-constexpr int kStreamMaxSamples = 1024;   // sample tables cached in LDS for pair-padded tails
+constexpr int kStreamMaxSamples = 1024;   // sample tables cached in LDS for pair-tiled tails
 
-// Pair-padded position of packed pair cell m (Eq. coordinate inverted with the
+// Pair-tiled position of packed pair cell m (Eq. coordinate inverted with the
 // sample tables): sample i by binary search over the pair offsets, then
 // (a, b) = divmod(m - o_i, N_i).
-__device__ __forceinline__ int32_t padded_pos_lds(const int32_t* cp, const int32_t* len, const int32_t* pad,
-                                                  int batch, int m, bool transposed) {
+__device__ __forceinline__ int32_t tiled_pos_lds(const int32_t* cp, const int32_t* len, const int32_t* pad,
+                                                 int batch, int m, bool transposed) {
   int lo = 0, hi = batch - 1;
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
     if (cp[mid] <= m) lo = mid; else hi = mid - 1;
   }
-  const int n = len[lo], local = m - cp[lo], n8 = (n + 7) & ~7;
+  const int n = len[lo], local = m - cp[lo];
   int a = (int)((float)local / (float)n);
   int b = local - a * n;
   if (b < 0) { --a; b += n; } else if (b >= n) { ++a; b -= n; }
-  return pad[lo] + (transposed ? b * n8 + a : a * n8 + b);
+  return tiled_cell_pos(pad[lo], n, a, b, transposed);
 }
 
 template <typename XT, int EPI, int K, int NTW>
@@ -542,8 +544,8 @@ __global__ void __launch_bounds__(kStreamThreads, 2) linear_stream_kernel(LinArg
   const int wc = p.wc, wr_n = 8 / wc, wcol = wave % wc, wrow = wave / wc;
   const int nt16 = (p.N + 15) >> 4;
   const XT* x = static_cast<const XT*>(p.x);
-  const bool padded_tail = p.y_tail && p.tail_mode != kTailChannelMajor;
-  const bool transposed = p.tail_mode == kTailPairPaddedT;
+  const bool tiled_tail = p.y_tail && p.tail_mode != kTailChannelMajor;
+  const bool transposed = p.tail_mode == kTailPairTiledT;
   int tile = blockIdx.x;
   if (tile >= p.ntiles) return;
 
@@ -592,7 +594,7 @@ __global__ void __launch_bounds__(kStreamThreads, 2) linear_stream_kernel(LinArg
       bv[j][i] = (p.bias && nb < p.N) ? p.bias[nb] : 0.f;
     }
   }
-  if (padded_tail) {
+  if (tiled_tail) {
     for (int j = tid; j <= p.batch; j += kStreamThreads) s_cp[j] = p.cu_pairs[j];
     for (int j = tid; j < p.batch; j += kStreamThreads) {
       s_len[j] = p.cu_seqlens[j + 1] - p.cu_seqlens[j];
@@ -668,7 +670,7 @@ __global__ void __launch_bounds__(kStreamThreads, 2) linear_stream_kernel(LinArg
       const int m = tile * TR + u * 16 + l16;
       if (m >= p.rows) continue;
       int32_t tpos = m;
-      if (padded_tail) tpos = padded_pos_lds(s_cp, s_len, s_pad, p.batch, m, transposed);
+      if (tiled_tail) tpos = tiled_pos_lds(s_cp, s_len, s_pad, p.batch, m, transposed);
 #pragma unroll
       for (int j = 0; j < NTW; ++j) {
         const int n = (wcol + wc * j) * 16 + 4 * g;
@@ -704,6 +706,157 @@ __global__ void __launch_bounds__(kStreamThreads, 2) linear_stream_kernel(LinArg
         }
       }
     }
+    tile = next;
+  }
+}
+
+// ---------------------------------------------------------------- tiled output
+// Projection whose every output column goes to a pair-tiled plane (the
+// triangle operands).  A workgroup tile is one 128-element chunk of the
+// planes: rows r = 0..15 and k = 8*gk .. 8*gk+7 of fragment tile (rt, kt) of
+// one sample, i.e. 128 cells gathered from 16 pair rows (8 consecutive cells
+// each; transposed: 8 pair rows, 16 cells each).  Tile rows are ordered
+// kk*16 + r, so the wave's 16-row subtile kk holds k-offset kk for all 16 r
+// and after the 8 subtiles each lane holds the 8 consecutive k of its row r
+// for every channel it owns: one 16-byte store per channel, and the 16 lanes
+// of a channel write 256 contiguous bytes.  Chunk t of the planes is tile t,
+// so tiles run over [0, sum_pad/128) and padding cells get bias-only values.
+constexpr int kTiledRows = 128;
+
+template <int K, int NTW>
+__global__ void __launch_bounds__(kStreamThreads, 1) linear_tiled_kernel(LinArgs p) {
+  constexpr int TR = kTiledRows;
+  constexpr int SKR = frag_stride<K>();
+  constexpr int KT = K / 32;
+  constexpr int TPR = kStreamThreads / TR;        // 4 staging threads per row
+  constexpr int EPT = K / TPR;
+  constexpr int NV = EPT / 8;
+  __shared__ __attribute__((aligned(16))) bf16 Xs[2][TR * SKR];
+  __shared__ int32_t s_pad[kStreamMaxSamples + 1], s_cp[kStreamMaxSamples], s_len[kStreamMaxSamples];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, g = lane >> 4;
+  const int nt16 = (p.N + 15) >> 4;
+  const bf16* x = static_cast<const bf16*>(p.x);
+  const bool transposed = p.tail_mode == kTailPairTiledT;
+  int tile = blockIdx.x;
+  if (tile >= p.ntiles) return;
+  for (int j = tid; j <= p.batch; j += kStreamThreads) s_pad[j] = p.cu_pad[j];
+  for (int j = tid; j < p.batch; j += kStreamThreads) {
+    s_cp[j] = p.cu_pairs[j];
+    s_len[j] = p.cu_seqlens[j + 1] - p.cu_seqlens[j];
+  }
+  __syncthreads();
+
+  // packed row of tile row `row` of tile t, or -1 for a padding cell
+  auto cell_row = [&](int t, int row) -> int {
+    const int e = t * TR;
+    int lo = 0, hi = p.batch - 1;                 // sample whose plane holds chunk t
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (s_pad[mid] <= e) lo = mid; else hi = mid - 1;
+    }
+    const int n = s_len[lo], nkt = (n + 31) >> 5;
+    const int tl = (e - s_pad[lo]) / TR;          // chunk index inside the plane
+    const int gk = tl & 3, kt = (tl >> 2) % nkt, rt = (tl >> 2) / nkt;
+    const int rr = 16 * rt + (row & 15), kk = 32 * kt + 8 * gk + (row >> 4);
+    const int a = transposed ? kk : rr, b = transposed ? rr : kk;
+    return (a < n && b < n) ? s_cp[lo] + a * n + b : -1;
+  };
+
+  const int srow = tid / TPR, spart = tid % TPR;
+  uint4 xr[NV];
+  auto load_x = [&](int t) {
+    const int m = cell_row(t, srow);
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+      xr[v] = m >= 0 ? *reinterpret_cast<const uint4*>(x + (int64_t)m * p.ldx + spart * EPT + v * 8)
+                     : make_uint4(0u, 0u, 0u, 0u);
+  };
+  load_x(tile);
+
+  bf16x8 wf[NTW][KT];
+  float bv[NTW][4];
+#pragma unroll
+  for (int j = 0; j < NTW; ++j) {
+    const int ct = wave + 8 * j, n = ct * 16 + l16;
+#pragma unroll
+    for (int kk = 0; kk < KT; ++kk) {
+      if (ct < nt16 && n < p.N) wf[j][kk] = *reinterpret_cast<const bf16x8*>(p.w + (int64_t)n * K + kk * 32 + g * 8);
+      else wf[j][kk] = bf16x8{};
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int nb = ct * 16 + 4 * g + i;
+      bv[j][i] = (p.bias && nb < p.N) ? p.bias[nb] : 0.f;
+    }
+  }
+
+  for (int it = 0; tile < p.ntiles; ++it) {
+    const int next = tile + (int)gridDim.x;
+    bf16* xs = Xs[it & 1];
+    {
+      float v[EPT];
+#pragma unroll
+      for (int vv = 0; vv < NV; ++vv) XStage<bf16>::unpack(xr[vv], v + vv * 8);
+      if (p.gamma) {                              // padding cells (zero rows) normalise to beta
+        float s = 0.f;
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) s += v[e];
+        const float mean = group_sum<TPR>(s) / (float)K;
+        float q = 0.f;
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) { const float d = v[e] - mean; q += d * d; }
+        const float rstd = rsqrtf(group_sum<TPR>(q) / (float)K + p.eps);
+#pragma unroll
+        for (int e = 0; e < EPT; e += 4) {
+          const float4 ga = *reinterpret_cast<const float4*>(p.gamma + spart * EPT + e);
+          const float4 be = p.beta ? *reinterpret_cast<const float4*>(p.beta + spart * EPT + e)
+                                   : make_float4(0.f, 0.f, 0.f, 0.f);
+          v[e] = (v[e] - mean) * rstd * ga.x + be.x;
+          v[e + 1] = (v[e + 1] - mean) * rstd * ga.y + be.y;
+          v[e + 2] = (v[e + 2] - mean) * rstd * ga.z + be.z;
+          v[e + 3] = (v[e + 3] - mean) * rstd * ga.w + be.w;
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < EPT; e += 8) {
+        bf16x8 o;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) o[j] = (bf16)v[e + j];
+        *reinterpret_cast<bf16x8*>(&xs[srow * SKR + spart * EPT + e]) = o;
+      }
+    }
+    if (next < p.ntiles) load_x(next);
+    __syncthreads();
+
+    // 8 subtiles (k-offsets); lane (r = l16, g) collects k-offsets 0..7 of
+    // channels 4g..4g+3 of each owned column tile
+    bf16x8 hold[NTW][4];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      bf16x8 xf[KT];
+#pragma unroll
+      for (int kk = 0; kk < KT; ++kk) xf[kk] = *reinterpret_cast<const bf16x8*>(&xs[(u * 16 + l16) * SKR + kk * 32 + g * 8]);
+#pragma unroll
+      for (int j = 0; j < NTW; ++j) {
+        f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (wave + 8 * j < nt16) {
+#pragma unroll
+          for (int kk = 0; kk < KT; ++kk) acc = mfma16(wf[j][kk], xf[kk], acc);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) hold[j][i][u] = (bf16)(acc[i] + bv[j][i]);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < NTW; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int c = (wave + 8 * j) * 16 + 4 * g + i;
+        if (c < p.N)
+          *reinterpret_cast<bf16x8*>(p.y_tail + (int64_t)c * p.ld_tail + (int64_t)tile * TR + 8 * l16) = hold[j][i];
+      }
     tile = next;
   }
 }
@@ -931,7 +1084,7 @@ struct F32Args {
   int64_t ldy;
   float* y_tail;
   int64_t ld_tail;
-  LinArgs pair;         // only the pair-padded tail fields are used
+  LinArgs pair;         // only the pair-tiled tail fields are used
 };
 
 __global__ void __launch_bounds__(256) linear_f32_kernel(F32Args p) {
@@ -990,7 +1143,7 @@ __global__ void __launch_bounds__(256) linear_f32_kernel(F32Args p) {
       if (p.epi == NT_EPI_RESIDUAL) s += p.res[(int64_t)m * p.ld_res + n];
       p.y[(int64_t)m * p.ldy + n] = s;
     } else {
-      const int64_t pos = p.pair.tail_mode == kTailChannelMajor ? (int64_t)m : pair_padded_pos(p.pair, m);
+      const int64_t pos = p.pair.tail_mode == kTailChannelMajor ? (int64_t)m : pair_tiled_pos(p.pair, m);
       p.y_tail[(int64_t)(n - p.n_main) * p.ld_tail + pos] = s;
     }
   }
@@ -1025,6 +1178,20 @@ void launch_stream(const LinArgs& p, hipStream_t s) {
   linear_stream_kernel<XT, EPI, K, NTW><<<dim3((unsigned)grid), dim3(kStreamThreads), 0, s>>>(p);
 }
 
+template <int K>
+void launch_tiled(const LinArgs& p, hipStream_t s) {
+  static int per_cu = 0;
+  if (per_cu == 0) {
+    int nb = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, linear_tiled_kernel<K, 2>, kStreamThreads, 0) !=
+            hipSuccess || nb < 1)
+      nb = 1;
+    per_cu = nb;
+  }
+  const int grid = std::min(p.ntiles, per_cu * compute_units());
+  if (grid > 0) linear_tiled_kernel<K, 2><<<dim3((unsigned)grid), dim3(kStreamThreads), 0, s>>>(p);
+}
+
 }  // namespace
 
 hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
@@ -1042,8 +1209,7 @@ hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
     p.row_splits2 = plan.layout->d_row_splits2; p.row_sample = plan.layout->d_row_sample;
     p.cu_seqlens = plan.layout->d_cu_seqlens; p.cu_pad = plan.layout->d_cu_pad;
     p.sum_n = (int)plan.layout->sum_n;
-    p.prow_base = plan.layout->d_prow_base; p.prow_tbase = plan.layout->d_prow_tbase;
-    p.prow_n8 = plan.layout->d_prow_n8; p.blk_prow = plan.layout->d_blk_prow;
+    p.blk_prow = plan.layout->d_blk_prow;
   }
   if (a.n_tail == 0) p.y_tail = nullptr;
 
@@ -1086,10 +1252,19 @@ hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
   p.nblocks = (a.c_out + BN - 1) / BN;
   const bool xf = a.x_dtype == NT_F32;
 
-  const bool padded = p.y_tail && p.tail_mode != kTailChannelMajor;
+  const bool tiled = p.y_tail && p.tail_mode != kTailChannelMajor;
+  if (tiled && p.n_main == 0 && !xf && a.epilogue == NT_EPI_NONE && (a.c_in == 64 || a.c_in == 128) &&
+      a.c_out <= 256 && plan.layout && plan.layout->batch <= kStreamMaxSamples) {
+    p.cu_pairs = plan.layout->d_cu_pairs;
+    p.batch = plan.layout->batch;
+    p.ntiles = (int)(plan.layout->sum_pad / kTiledRows);
+    if (a.c_in == 64) launch_tiled<64>(p, s);
+    else launch_tiled<128>(p, s);
+    return hipGetLastError();
+  }
   if ((a.c_in == 64 || a.c_in == 128) && a.c_out <= 512 &&
-      (!padded || (plan.layout && plan.layout->batch <= kStreamMaxSamples))) {
-    if (padded) { p.cu_pairs = plan.layout->d_cu_pairs; p.batch = plan.layout->batch; }
+      (!tiled || (plan.layout && plan.layout->batch <= kStreamMaxSamples))) {
+    if (tiled) { p.cu_pairs = plan.layout->d_cu_pairs; p.batch = plan.layout->batch; }
     const int nt16 = (a.c_out + 15) / 16;
     const int ntw = nt16 <= 16 ? 2 : 4;
     int wc = 2;

@@ -2,16 +2,17 @@
 // for every sample i and channel c, T_c = A_c B_c^T with A_c, B_c the
 // sample's N_i x N_i channel planes, then z[cell(x,y), c] += T_c[x, y].
 //
-// Operands arrive pair-padded channel-major (rows start 16-byte aligned), so
-// every matrix-core fragment is one 16-byte load.  A workgroup owns a 32x32
-// cell tile of one sample and a block of 16 channels (4 per wave).  Workgroup
-// ids interleave the channel blocks of each tile, so with 8 blocks (C = 128)
-// XCD x (ids = x mod 8) always works on channel block x: it walks the tile
-// list sample by sample and keeps the current sample's 16 channel planes
-// (2 x 16 x N^2 x 2 bytes, about 3 MB at N = 216) in its own L2, where the
-// operand re-reads of neighbouring tiles hit.  The next k-step's fragments
-// are loaded while the current one is on the matrix cores; with 64
-// accumulator registers per lane two waves fit on each SIMD.
+// Operands arrive pair-tiled (every 16 x 32 fragment stored in lane order),
+// so each matrix-core fragment is one contiguous 1 KB wave load.  A workgroup
+// owns a 32x32 cell tile of one sample and a block of 16 channels (4 per
+// wave).  Workgroup ids interleave the channel blocks of each tile, so with 8
+// blocks (C = 128) XCD x (ids = x mod 8) always works on channel block x: it
+// walks the tile list sample by sample and keeps the current sample's 16
+// channel planes (about 3 MB at N = 216) in its own L2, where the operand
+// re-reads of neighbouring tiles hit.  The next k-step's fragments load while
+// the current one is on the matrix cores.  The finished tile goes through LDS
+// so that z is updated in 32-byte pieces (16 channels of one cell) instead of
+// the 8-byte pieces a single wave holds.
 #include "nt_device.h"
 #include "nt_internal.h"
 
@@ -20,6 +21,7 @@ namespace {
 
 constexpr int kTriCB = 16;    // channels per workgroup
 constexpr int kTriCW = 4;     // channels per wave
+constexpr int kTriSC = 20;    // LDS floats per staged cell (16 channels + 4: conflict-free 16-byte writes)
 
 struct TriArgs {
   int C, nblk;
@@ -34,39 +36,30 @@ struct TriArgs {
   const int32_t* cu_pad;
 };
 
-// Fragment of rows row..row+15 (lane row = l16) and k..k+7 of one plane;
-// rows past the sample and k past N read as zero.
-__device__ __forceinline__ bf16x8 load_frag(const bf16* plane, int row, int k, int n, int n8, bool tail) {
-  if (row >= n || k >= n) return bf16x8{};
-  bf16x8 f = *reinterpret_cast<const bf16x8*>(plane + (int64_t)row * n8 + k);
-  if (tail) {
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-      if (k + j >= n) f[j] = (bf16)0.f;
-  }
-  return f;
-}
-
 __global__ void __launch_bounds__(256, 2) triangle_mfma_kernel(TriArgs p) {
+  __shared__ __attribute__((aligned(16))) float stage[kTriTile * kTriTile * kTriSC];
   const int id = blockIdx.x;
   const int item = id / p.nblk, cb = id % p.nblk;
   const int i = p.work[4 * item];
   if (i < 0) return;
   const int xt = p.work[4 * item + 1], yt = p.work[4 * item + 2];
   const int n = p.cu_seqlens[i + 1] - p.cu_seqlens[i];
-  const int n8 = (n + 7) & ~7;
+  const int nkt = (n + 31) >> 5;
   const int64_t P = p.cu_pad[i], cu = p.cu_pairs[i];
   const int x0 = xt * kTriTile, y0 = yt * kTriTile;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, g = lane >> 4;
   const int c0 = cb * kTriCB + wave * kTriCW;
 
+  // row tiles of the output tile that hold rows of the sample (uniform)
+  const bool xv[2] = {x0 < n, x0 + 16 < n};
+  const bool yv[2] = {y0 < n, y0 + 16 < n};
   const bf16* ap[kTriCW];
   const bf16* bp[kTriCW];
 #pragma unroll
   for (int ch = 0; ch < kTriCW; ++ch) {
-    ap[ch] = p.a + (int64_t)(c0 + ch) * p.ld_ab + P;
-    bp[ch] = p.b + (int64_t)(c0 + ch) * p.ld_ab + P;
+    ap[ch] = p.a + (int64_t)(c0 + ch) * p.ld_ab + P + lane * 8;
+    bp[ch] = p.b + (int64_t)(c0 + ch) * p.ld_ab + P + lane * 8;
   }
   f32x4 acc[kTriCW][2][2];
 #pragma unroll
@@ -76,22 +69,36 @@ __global__ void __launch_bounds__(256, 2) triangle_mfma_kernel(TriArgs p) {
 #pragma unroll
       for (int ys = 0; ys < 2; ++ys) acc[ch][xs][ys] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // Fragments of k-step kt: tile (row tile, kt) of each channel plane.  Row
+  // tiles past the sample read as zero without a load; k past N is zeroed in
+  // the last step (rows past N inside a row tile only reach discarded cells).
   bf16x8 fa[kTriCW][2], fb[kTriCW][2];
-  auto load_step = [&](int k0, bf16x8 (&ra)[kTriCW][2], bf16x8 (&rb)[kTriCW][2]) {
-    const int k = k0 + 8 * g;
-    const bool tail = k0 + 32 > n;
+  auto load_step = [&](int kt, bf16x8 (&ra)[kTriCW][2], bf16x8 (&rb)[kTriCW][2]) {
+    const bool any = kt < nkt;
+    const int kbase = kt * 32 + 8 * g;
 #pragma unroll
     for (int ch = 0; ch < kTriCW; ++ch)
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
-        ra[ch][h] = load_frag(ap[ch], x0 + 16 * h + l16, k, n, n8, tail);
-        rb[ch][h] = load_frag(bp[ch], y0 + 16 * h + l16, k, n, n8, tail);
+        const int64_t ta = ((int64_t)((x0 >> 4) + h) * nkt + kt) << 9;
+        const int64_t tb = ((int64_t)((y0 >> 4) + h) * nkt + kt) << 9;
+        ra[ch][h] = (any && xv[h]) ? *reinterpret_cast<const bf16x8*>(ap[ch] + ta) : bf16x8{};
+        rb[ch][h] = (any && yv[h]) ? *reinterpret_cast<const bf16x8*>(bp[ch] + tb) : bf16x8{};
       }
+    if (any && kbase + 8 > n) {
+#pragma unroll
+      for (int ch = 0; ch < kTriCW; ++ch)
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            if (kbase + j >= n) { ra[ch][h][j] = (bf16)0.f; rb[ch][h][j] = (bf16)0.f; }
+    }
   };
   load_step(0, fa, fb);
-  for (int k0 = 0; k0 < n; k0 += 32) {
+  for (int kt = 0; kt < nkt; ++kt) {
     bf16x8 na[kTriCW][2], nb[kTriCW][2];
-    load_step(k0 + 32, na, nb);              // all-zero without a load past the last step
+    load_step(kt + 1, na, nb);              // all-zero without a load past the last step
 #pragma unroll
     for (int ch = 0; ch < kTriCW; ++ch)
 #pragma unroll
@@ -104,21 +111,34 @@ __global__ void __launch_bounds__(256, 2) triangle_mfma_kernel(TriArgs p) {
       for (int h = 0; h < 2; ++h) { fa[ch][h] = na[ch][h]; fb[ch][h] = nb[ch][h]; }
   }
 
-  // acc[ch][xs][ys][r] = T_{c0+ch}[x0 + 16xs + 4g + r][y0 + 16ys + l16]
+  // acc[ch][xs][ys][r] = T_{c0+ch}[x0 + 16xs + 4g + r][y0 + 16ys + l16]; stage
+  // the tile as [cell][16 channels] fp32
 #pragma unroll
   for (int xs = 0; xs < 2; ++xs)
 #pragma unroll
     for (int ys = 0; ys < 2; ++ys)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int x = x0 + 16 * xs + 4 * g + r, y = y0 + 16 * ys + l16;
-        if (x >= n || y >= n) continue;
-        bf16x4* zp = reinterpret_cast<bf16x4*>(p.z + (cu + (int64_t)x * n + y) * p.ld_z + c0);
-        bf16x4 zz = *zp;
-#pragma unroll
-        for (int ch = 0; ch < kTriCW; ++ch) zz[ch] = (bf16)((float)zz[ch] + acc[ch][xs][ys][r]);
-        *zp = zz;
+        const int cell = (16 * xs + 4 * g + r) * kTriTile + 16 * ys + l16;
+        *reinterpret_cast<float4*>(&stage[cell * kTriSC + wave * kTriCW]) =
+            make_float4(acc[0][xs][ys][r], acc[1][xs][ys][r], acc[2][xs][ys][r], acc[3][xs][ys][r]);
       }
+  __syncthreads();
+  // z += T: two threads per cell, 8 channels (16 bytes) each
+#pragma unroll
+  for (int it = 0; it < kTriTile * kTriTile * 2 / 256; ++it) {
+    const int u = it * 256 + tid, cell = u >> 1, half = u & 1;
+    const int x = x0 + cell / kTriTile, y = y0 + cell % kTriTile;
+    if (x >= n || y >= n) continue;
+    const float4 t0 = *reinterpret_cast<const float4*>(&stage[cell * kTriSC + half * 8]);
+    const float4 t1 = *reinterpret_cast<const float4*>(&stage[cell * kTriSC + half * 8 + 4]);
+    bf16* zp = p.z + (cu + (int64_t)x * n + y) * p.ld_z + cb * kTriCB + half * 8;
+    Vec<bf16> zz;
+    zz.load(zp);
+    zz.v[0] += t0.x; zz.v[1] += t0.y; zz.v[2] += t0.z; zz.v[3] += t0.w;
+    zz.v[4] += t1.x; zz.v[5] += t1.y; zz.v[6] += t1.z; zz.v[7] += t1.w;
+    zz.store(zp);
+  }
 }
 
 // ---------------------------------------------------------------- fp32 path
@@ -142,17 +162,17 @@ __global__ void __launch_bounds__(256) triangle_f32_kernel(TriF32Args p) {
   if (i < 0) return;
   const int xt = p.work[4 * item + 1], yt = p.work[4 * item + 2];
   const int n = p.cu_seqlens[i + 1] - p.cu_seqlens[i];
-  const int n8 = (n + 7) & ~7;
+  const int nkt = (n + 31) >> 5;
   const int64_t P = p.cu_pad[i], cu = p.cu_pairs[i];
   const int total = kTriTile * kTriTile * p.C;
   for (int e = threadIdx.x; e < total; e += 256) {
     const int c = e % p.C, cell = e / p.C;
     const int x = xt * kTriTile + cell / kTriTile, y = yt * kTriTile + cell % kTriTile;
     if (x >= n || y >= n) continue;
-    const float* ar = p.a + (int64_t)c * p.ld_ab + P + (int64_t)x * n8;
-    const float* br = p.b + (int64_t)c * p.ld_ab + P + (int64_t)y * n8;
+    const float* ap = p.a + (int64_t)c * p.ld_ab + P;
+    const float* bp = p.b + (int64_t)c * p.ld_ab + P;
     float s = 0.f;
-    for (int k = 0; k < n; ++k) s = fmaf(ar[k], br[k], s);
+    for (int k = 0; k < n; ++k) s = fmaf(ap[tiled_offset(x, k, nkt)], bp[tiled_offset(y, k, nkt)], s);
     p.z[(cu + (int64_t)x * n + y) * p.ld_z + c] += s;
   }
 }

@@ -79,7 +79,7 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L) {
     sn += n;
     sn2 += n * n;
     sn3 += n * n * n;
-    spad += n * ((n + 7) / 8 * 8);
+    spad += ((n + 15) / 16 * 16) * ((n + 31) / 32 * 32);
     if (sn > INT32_MAX || sn2 > INT32_MAX || spad > INT32_MAX)
       return fail(NT_ERR_OVERFLOW, "packed pair extent exceeds int32 at sample " + std::to_string(i));
     L->cu_seqlens[i + 1] = (int32_t)sn;
@@ -106,20 +106,8 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L) {
   }
   L->row_splits2[sn] = (int32_t)sn2;
 
-  // pair-padded operand addressing per pair row, and the first pair row of
-  // every kLinRows-cell block of the pair tensor (projection row tiles)
-  L->prow_base.assign(sn, 0);
-  L->prow_tbase.assign(sn, 0);
-  L->prow_n8.assign(sn, 0);
-  for (int32_t i = 0; i < batch; ++i) {
-    const int32_t n = lengths[i], n8 = (n + 7) / 8 * 8;
-    for (int32_t a = 0; a < n; ++a) {
-      const int64_t eta = (int64_t)L->cu_seqlens[i] + a;
-      L->prow_base[eta] = L->cu_pad[i] + a * n8;
-      L->prow_tbase[eta] = L->cu_pad[i] + a;
-      L->prow_n8[eta] = n8;
-    }
-  }
+  // first pair row of every kLinRows-cell block of the pair tensor (row tiles
+  // of the projections that write pair-tiled outputs)
   const int64_t nblk = (sn2 + kLinRows - 1) / kLinRows;
   L->blk_prow.assign(nblk, 0);
   for (int64_t b = 0, eta = 0; b < nblk; ++b) {

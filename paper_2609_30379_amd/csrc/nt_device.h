@@ -22,6 +22,17 @@ __device__ __forceinline__ f32x4 mfma16(const bf16x8& a, const bf16x8& b, const 
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+// ---- pair-tiled operand layout -----------------------------------------------
+// One channel plane of sample i (an N x N matrix, rows r, columns k) is cut
+// into 16 x 32 tiles, row tiles outer, each tile stored in the lane order of a
+// matrix-core fragment: element (r, k) of a tile sits at ((k/8)*16 + r%16)*8
+// + k%8, so lane l of a wave reads the 8 consecutive k of tile row l%16 and
+// k-group l/16 as one 16-byte piece and the whole wave reads 1 KB contiguously.
+// Planes occupy round_up(N,16) x round_up(N,32) elements; nkt = round_up(N,32)/32.
+__host__ __device__ __forceinline__ int32_t tiled_offset(int32_t r, int32_t k, int32_t nkt) {
+  return (((r >> 4) * nkt + (k >> 5)) << 9) + ((((k & 31) >> 3) << 4) + (r & 15)) * 8 + (k & 7);
+}
+
 // ---- 16-byte vectors of a storage type, converted to/from fp32 ------------
 template <typename T> struct Vec;
 

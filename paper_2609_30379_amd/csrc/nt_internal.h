@@ -32,21 +32,18 @@ struct nt_layout {
   int32_t batch = 0;
   int32_t max_len = 0;
   int64_t sum_n = 0, sum_n2 = 0, sum_n3 = 0;
-  int64_t sum_pad = 0;             // sum_i N_i * round_up(N_i, 8)
+  int64_t sum_pad = 0;             // sum_i round_up(N_i,16) * round_up(N_i,32): pair-tiled plane extent
 
   std::vector<int32_t> lengths;      // [B]
   std::vector<int32_t> cu_seqlens;   // [B+1]
   std::vector<int32_t> cu_pairs;     // [B+1]
-  std::vector<int32_t> cu_pad;       // [B+1] offsets of the padded channel-major operand blocks
+  std::vector<int32_t> cu_pad;       // [B+1] offsets P_i of the pair-tiled operand planes
   std::vector<int32_t> row_splits2;  // [sum N + 1]
   std::vector<int32_t> row_sample;   // [sum N]
   std::vector<int32_t> attn_work;    // pairs (sample, row); count multiple of 8; (-1,-1) = idle
   std::vector<int32_t> tri_work;     // quads (sample, xt, yt, 0); count multiple of 8
   std::vector<int32_t> seq_work;     // pairs (sample, query block); count multiple of 8
   std::vector<int32_t> pattn_work;   // quads (sample, query block, row group, 0); count multiple of 8
-  std::vector<int32_t> prow_base;    // [sum N] P_i + a n8_i: padded offset of pair row (i, a)
-  std::vector<int32_t> prow_tbase;   // [sum N] P_i + a: transposed padded offset of row (i, a)
-  std::vector<int32_t> prow_n8;      // [sum N] n8_i
   std::vector<int32_t> blk_prow;     // [ceil(sum N^2 / kLinRows)] pair row holding cell kLinRows*b
 
   bool has_device = false;
@@ -62,9 +59,6 @@ struct nt_layout {
   const int32_t* d_tri_work = nullptr;
   const int32_t* d_seq_work = nullptr;
   const int32_t* d_pattn_work = nullptr;
-  const int32_t* d_prow_base = nullptr;
-  const int32_t* d_prow_tbase = nullptr;
-  const int32_t* d_prow_n8 = nullptr;
   const int32_t* d_blk_prow = nullptr;
 
   int64_t attn_items() const { return (int64_t)attn_work.size() / 2; }
@@ -89,12 +83,12 @@ hipError_t launch_segment_reduce(const nt_layout& L, nt_level level, int op, int
                                  float* y, int64_t ld_y, hipStream_t s);
 
 // Tail output modes of the projection (columns routed to y_tail).
-enum TailMode { kTailChannelMajor = 0, kTailPairPadded = 1, kTailPairPaddedT = 2 };
+enum TailMode { kTailChannelMajor = 0, kTailPairTiled = 1, kTailPairTiledT = 2 };
 
 struct LinearPlan {
   const nt_linear_args* a;
   int tail_mode;
-  const nt_layout* layout;   // for pair-padded tail modes
+  const nt_layout* layout;   // for pair-tiled tail modes
 };
 hipError_t launch_linear(const LinearPlan& p, hipStream_t s);
 

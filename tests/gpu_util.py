@@ -52,40 +52,45 @@ def check(got: np.ndarray, ref: np.ndarray, dtype: str, what: str = "", equal_na
     return err
 
 
-def pair_padded(x: np.ndarray, lengths, transposed: bool = False, ld: int | None = None,
-                fill: float = 0.0) -> np.ndarray:
-    """Channel-major pair-padded operand layout of a [sum N^2, C] pair tensor:
-    channel c of cell (i,a,b) at c*ld + P_i + a*n8 + b (or b*n8 + a); padding
-    entries hold `fill` (NaN checks that a kernel never reads them as data)."""
+def _tiled_plane_index(n: int, transposed: bool) -> np.ndarray:
+    """Offsets inside one pair-tiled plane of every cell (a, b), a-major: plane
+    element (r, k) of a 16 x 32 tile grid (row tiles outer, ceil(n/32) tiles
+    per row), stored in fragment lane order ((k%32)//8 * 16 + r%16) * 8 + k%8;
+    the plain variant puts cell (a, b) at (r, k) = (a, b), the transposed one
+    at (b, a)."""
+    a, b = np.meshgrid(np.arange(n), np.arange(n), indexing="ij")
+    r, k = (b, a) if transposed else (a, b)
+    nkt = -(-n // 32)
+    return (((r // 16) * nkt + k // 32) * 512 + ((k % 32) // 8 * 16 + r % 16) * 8 + k % 8).reshape(-1)
+
+
+def tiled_offsets(lengths) -> np.ndarray:
+    sizes = [(-(-int(n) // 16) * 16) * (-(-int(n) // 32) * 32) for n in lengths]
+    return np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+
+
+def pair_tiled(x: np.ndarray, lengths, transposed: bool = False, ld: int | None = None,
+               fill: float = 0.0) -> np.ndarray:
+    """Channel-major pair-tiled operand layout of a [sum N^2, C] pair tensor;
+    padding entries hold `fill` (NaN checks that a kernel never reads them as
+    data)."""
     C = x.shape[1]
-    n8 = [(int(n) + 7) // 8 * 8 for n in lengths]
-    P = np.concatenate([[0], np.cumsum([int(n) * m for n, m in zip(lengths, n8)])]).astype(np.int64)
+    P = tiled_offsets(lengths)
     ld = int(P[-1]) if ld is None else ld
     ld = max(8, (ld + 7) // 8 * 8)
     out = np.full((C, ld), fill, np.float64)
     off = 0
     for i, n in enumerate(lengths):
         n = int(n)
-        blk = x[off:off + n * n].reshape(n, n, C)
-        if transposed:
-            blk = blk.transpose(1, 0, 2)
-        pad = np.full((n, n8[i], C), fill)
-        pad[:, :n] = blk
-        out[:, P[i]:P[i] + n * n8[i]] = pad.reshape(n * n8[i], C).T
+        idx = P[i] + _tiled_plane_index(n, transposed)
+        out[:, idx] = x[off:off + n * n].T
         off += n * n
     return out
 
 
-def unpad_pair(y: np.ndarray, lengths, transposed: bool = False) -> np.ndarray:
-    """Inverse of pair_padded: [C, ld] -> [sum N^2, C] (padding dropped)."""
+def untile_pair(y: np.ndarray, lengths, transposed: bool = False) -> np.ndarray:
+    """Inverse of pair_tiled: [C, ld] -> [sum N^2, C] (padding dropped)."""
     C = y.shape[0]
-    n8 = [(int(n) + 7) // 8 * 8 for n in lengths]
-    rows, P = [], 0
-    for i, n in enumerate(lengths):
-        n = int(n)
-        blk = y[:, P:P + n * n8[i]].T.reshape(n, n8[i], C)[:, :n]
-        if transposed:
-            blk = blk.transpose(1, 0, 2)
-        rows.append(blk.reshape(n * n, C))
-        P += n * n8[i]
+    P = tiled_offsets(lengths)
+    rows = [y[:, P[i] + _tiled_plane_index(int(n), transposed)].T for i, n in enumerate(lengths)]
     return np.concatenate(rows) if rows else np.zeros((0, C))

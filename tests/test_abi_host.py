@@ -40,8 +40,8 @@ def test_host_layout_matches_oracle(L):
     assert lay.host_array("cu_seqlens").tolist() == OL.single_offsets(L).tolist()
     assert lay.host_array("cu_pairs").tolist() == OL.pair_offsets(L).tolist()
     assert lay.host_array("row_splits2").tolist() == OL.pair_row_splits(L)[1].tolist()
-    n8 = [(n + 7) // 8 * 8 for n in L]
-    assert lay.host_array("cu_pad").tolist() == OL.offsets([n * m for n, m in zip(L, n8)]).tolist()
+    plane = [(-(-n // 16) * 16) * (-(-n // 32) * 32) for n in L]     # pair-tiled plane extents
+    assert lay.host_array("cu_pad").tolist() == OL.offsets(plane).tolist()
     rs = lay.host_array("row_sample")
     assert rs.tolist() == [i for i, n in enumerate(L) for _ in range(n)]
     assert (lay.sum_n, lay.sum_n2, lay.sum_n3) == (sum(L), sum(n * n for n in L), sum(n ** 3 for n in L))
@@ -154,3 +154,24 @@ def test_op_argument_errors_need_no_device(lib):
     dev = B.NestedLayout([2, 3], host_only=True)
     assert lib.nt_pair_row_attention(dev.handle, 0, 4, 32, None, None, None, 384, None, 0, 1.0, None, 128,
                                      B.NT_BF16, None) == B.NT_ERR_INVALID_ARG    # host-only layout
+
+
+@pytest.mark.parametrize("n", [1, 15, 16, 17, 33, 216])
+def test_pair_tiled_plane_is_a_fragment_order_bijection(n):
+    """The pair-tiled plane of an N x N matrix places every cell once inside the
+    round_up(N,16) x round_up(N,32) extent, and the 8 consecutive k of (row r,
+    k-group g) of a 16 x 32 tile form the 16-byte piece of lane g*16 + r%16."""
+    from tests.gpu_util import _tiled_plane_index, pair_tiled, untile_pair
+    idx = _tiled_plane_index(n, False)
+    ext = (-(-n // 16) * 16) * (-(-n // 32) * 32)
+    assert len(set(idx.tolist())) == n * n and idx.min() >= 0 and idx.max() < ext
+    a, b = np.divmod(np.arange(n * n), n)
+    tile_base = ((a // 16) * (-(-n // 32)) + b // 32) * 512
+    lane = ((b % 32) // 8) * 16 + a % 16
+    assert np.array_equal(idx, tile_base + lane * 8 + b % 8)
+    t = _tiled_plane_index(n, True)
+    assert np.array_equal(t.reshape(n, n).T, idx.reshape(n, n))
+    x = np.random.default_rng(n).standard_normal((n * n + 9, 3))
+    L = [n, 3]
+    for tr in (False, True):
+        assert np.array_equal(untile_pair(pair_tiled(x, L, tr, fill=np.nan), L, tr), x)

@@ -6,7 +6,7 @@ import pytest
 
 from oracle import ops as O
 from paper_2609_30379_amd import synth
-from tests.gpu_util import check, dev, host, pair_padded, unpad_pair
+from tests.gpu_util import check, dev, host, pair_tiled, untile_pair
 
 pytestmark = pytest.mark.gpu
 
@@ -134,7 +134,7 @@ def test_layernorm_linear(B, R, K, N, ln, epi, xdt, dtype, n_tail):
 
 @pytest.mark.parametrize("transposed", [False, True])
 @pytest.mark.parametrize("dtype,C", [("bf16", 64), ("f32", 16)])
-def test_layernorm_linear_pair_padded_tail(B, transposed, dtype, C):
+def test_layernorm_linear_pair_tiled_tail(B, transposed, dtype, C):
     import torch
     L = LENGTHS["ragged"]
     lay = _layout(B, L)
@@ -147,10 +147,10 @@ def test_layernorm_linear_pair_padded_tail(B, transposed, dtype, C):
     ld = (lay.sum_pad + 7) // 8 * 8
     yt = torch.full((2 * C, ld), float("nan"), dtype=td, device="cuda")
     B.nt_layernorm_linear(dev(x, dtype), dev(w, dtype), dev(b, "f32"), None, ln=(dev(g, "f32"), dev(be, "f32")),
-                          n_tail=2 * C, y_tail=yt, tail_layout="pair_padded_t" if transposed else "pair_padded",
+                          n_tail=2 * C, y_tail=yt, tail_layout="pair_tiled_t" if transposed else "pair_tiled",
                           layout=lay, level="pairs", c_out=2 * C)
     ref = O.layernorm_linear(x, w, b, ln=(g, be))
-    check(unpad_pair(host(yt), L, transposed), ref, dtype, "pair-padded tail")
+    check(untile_pair(host(yt), L, transposed), ref, dtype, "pair-tiled tail")
 
 
 @pytest.mark.parametrize("R,K,F,dtype", [(1000, 128, 512, "bf16"), (333, 64, 256, "bf16"), (65, 256, 96, "bf16"),
@@ -239,8 +239,8 @@ def test_triangle(B, direction, dtype, C, lname):
     z0 = _n(28, "z0", (R, C), 0.5, dtype)
     tr = direction == 1
     ld = (lay.sum_pad + 7) // 8 * 8
-    ap = dev(pair_padded(a, L, tr, ld, fill=np.nan), dtype)
-    bp = dev(pair_padded(b, L, tr, ld, fill=np.nan), dtype)
+    ap = dev(pair_tiled(a, L, tr, ld, fill=np.nan), dtype)
+    bp = dev(pair_tiled(b, L, tr, ld, fill=np.nan), dtype)
     z = dev(z0, dtype)
     B.nt_triangle_mul(lay, direction, ap, bp, z)
     ref = z0 + O.triangle_mul(a, b, L, "outgoing" if direction == 0 else "incoming")
