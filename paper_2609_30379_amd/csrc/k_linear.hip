@@ -1062,6 +1062,236 @@ __global__ void __launch_bounds__(256) swiglu_kernel(SwiArgs p) {
   }
 }
 
+// ---------------------------------------------------------------- transition
+// Persistent pre-normalised SwiGLU transition for K = N in {64, 128}: eight
+// waves share a pass of 256 rows (32 per wave, held as matrix-core B
+// fragments in registers), and the hidden width is walked in chunks of 32.
+// A chunk's weights (gate and up rows, and the matching 32 columns of the
+// down projection) are staged in LDS as fragment images -- 64 lanes x 16
+// bytes in the order the matrix cores consume them -- so every LDS read is
+// one conflict-free 1 KB wave read.  Chunk weights are loaded two chunks
+// ahead into registers and written to the other of two LDS buffers, one
+// barrier per chunk; the chunk sequence simply cycles, so the pipeline runs
+// on across passes.  The gated hidden goes from the first product's
+// accumulators straight into the second product (same lane layout).
+constexpr int kTrThreads = 512;
+constexpr int kTrMT = 2;                          // 16-row subtiles per wave
+constexpr int kTrRows = 8 * 16 * kTrMT;           // rows per pass
+
+template <int K>
+constexpr int tr_chunk_frags() { return 4 * (K / 32) + K / 16; }   // gate + up + down images
+
+template <int K>
+constexpr size_t tr_smem_bytes(int F) {
+  return sizeof(bf16) * ((size_t)kTrRows * frag_stride<K>() + 2 * (size_t)tr_chunk_frags<K>() * 512) +
+         sizeof(float) * (2 * (size_t)F + K + 2 * (size_t)K);
+}
+
+template <int K>
+__global__ void __launch_bounds__(kTrThreads, 1) transition_kernel(SwiArgs p) {
+  constexpr int N = K, KT = K / 32, NT = N / 16;
+  constexpr int SKX = frag_stride<K>();
+  constexpr int CF = tr_chunk_frags<K>();
+  constexpr int GU_PIECES = 64 * K / 8, PIECES = GU_PIECES + N * 4;
+  constexpr int PPT = (PIECES + kTrThreads - 1) / kTrThreads;
+  extern __shared__ __attribute__((aligned(16))) bf16 smem[];
+  bf16* Xn = smem;                                    // [kTrRows][SKX]
+  bf16* Wb0 = Xn + kTrRows * SKX;                     // chunk fragment images, two buffers
+  bf16* Wb1 = Wb0 + CF * 512;
+  float* s_b = reinterpret_cast<float*>(Wb1 + CF * 512);   // [2F] gate/up bias
+  float* s_b2 = s_b + 2 * p.F;                             // [N] down bias
+  float* s_g = s_b2 + N;                                   // [K] LayerNorm gamma, then beta
+  float* s_be = s_g + K;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, g = lane >> 4;
+  const int nch = p.F / 32;
+  const int nrb = (p.rows + kTrRows - 1) / kTrRows;
+  if ((int)blockIdx.x >= nrb) return;
+  for (int j = tid; j < 2 * p.F; j += kTrThreads) s_b[j] = p.bias ? p.bias[j] : 0.f;
+  for (int j = tid; j < N; j += kTrThreads) s_b2[j] = p.bias2 ? p.bias2[j] : 0.f;
+  for (int j = tid; j < K; j += kTrThreads) {
+    s_g[j] = p.gamma ? p.gamma[j] : 1.f;
+    s_be[j] = p.beta ? p.beta[j] : 0.f;
+  }
+
+  // ---- chunk weight staging: piece q of chunk f (16 global bytes each) -----
+  uint4 R0[PPT], R1[PPT];
+  auto load_chunk = [&](int f, uint4 (&R)[PPT]) {
+    const int f0 = f * 32;
+#pragma unroll
+    for (int j = 0; j < PPT; ++j) {
+      const int q = tid + kTrThreads * j;
+      if (q < GU_PIECES) {
+        const int r = q / (K / 8), kc = q % (K / 8);
+        const int wrow = r < 32 ? f0 + r : p.F + f0 + (r - 32);
+        R[j] = *reinterpret_cast<const uint4*>(p.w + (int64_t)wrow * K + kc * 8);
+      } else if (q < PIECES) {
+        const int q2 = q - GU_PIECES, n = q2 >> 2, pc = q2 & 3;
+        R[j] = *reinterpret_cast<const uint4*>(p.w2 + (int64_t)n * p.F + f0 + pc * 8);
+      }
+    }
+  };
+  auto store_chunk = [&](bf16* W, const uint4 (&R)[PPT]) {
+#pragma unroll
+    for (int j = 0; j < PPT; ++j) {
+      const int q = tid + kTrThreads * j;
+      if (q < GU_PIECES) {
+        const int r = q / (K / 8), kc = q % (K / 8);
+        const int which = r >> 5, rr = r & 31;                 // gate / up, row in chunk
+        const int frag = (which * 2 + (rr >> 4)) * KT + (kc >> 2);
+        const int ln = (kc & 3) * 16 + (rr & 15);
+        *reinterpret_cast<uint4*>(&W[frag * 512 + ln * 8]) = R[j];
+      } else if (q < PIECES) {
+        // down weights W2[n][f0 + 8pc + 4hf + t]: hidden h goes to k-group
+        // (h%16)/4, slot 4*(h/16) + h%4 of fragment n/16 (the order in which
+        // the gated hidden leaves the first product)
+        const int q2 = q - GU_PIECES, n = q2 >> 2, pc = q2 & 3;
+        const int frag = 4 * KT + (n >> 4), slot = (pc >> 1) * 4;
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          const int gg = 2 * (pc & 1) + hf;
+          const uint2 v = hf ? make_uint2(R[j].z, R[j].w) : make_uint2(R[j].x, R[j].y);
+          *reinterpret_cast<uint2*>(&W[frag * 512 + (gg * 16 + (n & 15)) * 8 + slot]) = v;
+        }
+      }
+    }
+  };
+
+  // prologue: chunk 0 staged, chunk 1 in registers
+  load_chunk(0, R0);
+  store_chunk(Wb0, R0);
+  load_chunk(1 % nch, R1);
+
+  bf16x8 xf[kTrMT][KT];
+  f32x4 accY[NT][kTrMT];
+  int q = 0;                                          // global chunk step
+  for (int rb = blockIdx.x; rb < nrb; rb += gridDim.x) {
+    // ---- LayerNorm of the pass's rows into Xn, then fragments into registers
+    __syncthreads();                                  // Xn free, staging and tables visible
+    {
+      const int r = tid >> 1, hh = tid & 1, m = rb * kTrRows + r;
+      constexpr int HALF = K / 2, NV = HALF / 8;
+      uint4 raw[NV];
+#pragma unroll
+      for (int v = 0; v < NV; ++v)
+        raw[v] = m < p.rows ? *reinterpret_cast<const uint4*>(p.x + (int64_t)m * p.ldx + hh * HALF + v * 8)
+                            : make_uint4(0u, 0u, 0u, 0u);
+      float s = 0.f;
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        float t[8];
+        XStage<bf16>::unpack(raw[v], t);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s += t[e];
+      }
+      const float mean = (s + __shfl_xor(s, 1, 64)) / (float)K;
+      float qv = 0.f;
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        float t[8];
+        XStage<bf16>::unpack(raw[v], t);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) { const float d = t[e] - mean; qv += d * d; }
+      }
+      const float rstd = rsqrtf((qv + __shfl_xor(qv, 1, 64)) / (float)K + p.eps);
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        float t[8];
+        XStage<bf16>::unpack(raw[v], t);
+        bf16x8 o;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int k = hh * HALF + v * 8 + e;
+          o[e] = (bf16)(m < p.rows ? (t[e] - mean) * rstd * s_g[k] + s_be[k] : 0.f);
+        }
+        *reinterpret_cast<bf16x8*>(&Xn[r * SKX + hh * HALF + v * 8]) = o;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int mt = 0; mt < kTrMT; ++mt)
+#pragma unroll
+      for (int kk = 0; kk < KT; ++kk)
+        xf[mt][kk] = *reinterpret_cast<const bf16x8*>(&Xn[(wave * 16 * kTrMT + mt * 16 + l16) * SKX + kk * 32 + g * 8]);
+#pragma unroll
+    for (int a = 0; a < NT; ++a)
+#pragma unroll
+      for (int mt = 0; mt < kTrMT; ++mt) accY[a][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // ---- hidden chunks ----------------------------------------------------
+    auto step = [&](uint4 (&RA)[PPT], uint4 (&RB)[PPT], const bf16* W, bf16* Wn, int f) {
+      load_chunk((f + 2) % nch, RA);                 // two chunks ahead (cyclic)
+      const int f0 = f * 32;
+      f32x4 accG[2][kTrMT], accU[2][kTrMT];
+#pragma unroll
+      for (int ft = 0; ft < 2; ++ft)
+#pragma unroll
+        for (int mt = 0; mt < kTrMT; ++mt) { accG[ft][mt] = f32x4{0.f, 0.f, 0.f, 0.f}; accU[ft][mt] = accG[ft][mt]; }
+#pragma unroll
+      for (int kk = 0; kk < KT; ++kk)
+#pragma unroll
+        for (int ft = 0; ft < 2; ++ft) {
+          const bf16x8 ag = *reinterpret_cast<const bf16x8*>(&W[(ft * KT + kk) * 512 + lane * 8]);
+          const bf16x8 au = *reinterpret_cast<const bf16x8*>(&W[((2 + ft) * KT + kk) * 512 + lane * 8]);
+#pragma unroll
+          for (int mt = 0; mt < kTrMT; ++mt) {
+            accG[ft][mt] = mfma16(ag, xf[mt][kk], accG[ft][mt]);
+            accU[ft][mt] = mfma16(au, xf[mt][kk], accU[ft][mt]);
+          }
+        }
+      // gated hidden in the B-operand layout of the second product: slot
+      // 4*ft + i holds hidden f0 + 16 ft + 4g + i
+      const float4 bg0 = *reinterpret_cast<const float4*>(&s_b[f0 + 4 * g]);
+      const float4 bg1 = *reinterpret_cast<const float4*>(&s_b[f0 + 16 + 4 * g]);
+      const float4 bu0 = *reinterpret_cast<const float4*>(&s_b[p.F + f0 + 4 * g]);
+      const float4 bu1 = *reinterpret_cast<const float4*>(&s_b[p.F + f0 + 16 + 4 * g]);
+      const float bgv[8] = {bg0.x, bg0.y, bg0.z, bg0.w, bg1.x, bg1.y, bg1.z, bg1.w};
+      const float buv[8] = {bu0.x, bu0.y, bu0.z, bu0.w, bu1.x, bu1.y, bu1.z, bu1.w};
+      bf16x8 hv[kTrMT];
+#pragma unroll
+      for (int mt = 0; mt < kTrMT; ++mt)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float gv = accG[j >> 2][mt][j & 3] + bgv[j];
+          const float uv = accU[j >> 2][mt][j & 3] + buv[j];
+          hv[mt][j] = (bf16)(gv * __builtin_amdgcn_rcpf(1.f + __expf(-gv)) * uv);
+        }
+#pragma unroll
+      for (int a = 0; a < NT; ++a) {
+        const bf16x8 ad = *reinterpret_cast<const bf16x8*>(&W[(4 * KT + a) * 512 + lane * 8]);
+#pragma unroll
+        for (int mt = 0; mt < kTrMT; ++mt) accY[a][mt] = mfma16(ad, hv[mt], accY[a][mt]);
+      }
+      store_chunk(Wn, RB);                           // chunk f + 1 into the other buffer
+      __syncthreads();
+    };
+    for (int c = 0; c < nch; ++c, ++q) {
+      if (q & 1) step(R1, R0, Wb1, Wb0, c);
+      else step(R0, R1, Wb0, Wb1, c);
+    }
+
+    // ---- epilogue: residual + bias, lane owns channels n..n+3 of row m ----
+#pragma unroll
+    for (int mt = 0; mt < kTrMT; ++mt) {
+      const int m = rb * kTrRows + wave * 16 * kTrMT + mt * 16 + l16;
+      if (m >= p.rows) continue;
+#pragma unroll
+      for (int a = 0; a < NT; ++a) {
+        const int n = a * 16 + 4 * g;
+        const uint2 rr = *reinterpret_cast<const uint2*>(p.res + (int64_t)m * p.ld_res + n);
+        const float4 b2 = *reinterpret_cast<const float4*>(&s_b2[n]);
+        bf16x4 o;
+        o[0] = (bf16)(accY[a][mt][0] + b2.x + __uint_as_float(rr.x << 16));
+        o[1] = (bf16)(accY[a][mt][1] + b2.y + __uint_as_float(rr.x & 0xffff0000u));
+        o[2] = (bf16)(accY[a][mt][2] + b2.z + __uint_as_float(rr.y << 16));
+        o[3] = (bf16)(accY[a][mt][3] + b2.w + __uint_as_float(rr.y & 0xffff0000u));
+        *reinterpret_cast<bf16x4*>(p.y + (int64_t)m * p.ldy + n) = o;
+      }
+    }
+  }
+}
+
 // ---------------------------------------------------------------- fp32 path
 // Plain fp32 FMA path (used by the fp32 workloads): RB rows per workgroup, one
 // wave normalises each row into LDS, then threads compute output channels.
@@ -1234,6 +1464,20 @@ hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
     w.res = a.residual ? (const bf16*)a.residual : (const bf16*)a.x;
     w.ld_res = a.residual ? a.ld_residual : a.ldx;
     w.y = (bf16*)a.y; w.ldy = a.ldy;
+    const size_t tr_smem = a.c_in == 64 ? tr_smem_bytes<64>(a.hidden) : tr_smem_bytes<128>(a.hidden);
+    if ((a.c_in == 64 || a.c_in == 128) && a.c_out == a.c_in && tr_smem <= 160 * 1024) {
+      const int nrb = (rows + kTrRows - 1) / kTrRows;
+      const int grid = std::min(nrb, compute_units());
+      const size_t smem = tr_smem;
+      if (a.c_in == 64) {
+        hipFuncSetAttribute((const void*)transition_kernel<64>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+        transition_kernel<64><<<dim3((unsigned)grid), dim3(kTrThreads), smem, s>>>(w);
+      } else {
+        hipFuncSetAttribute((const void*)transition_kernel<128>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+        transition_kernel<128><<<dim3((unsigned)grid), dim3(kTrThreads), smem, s>>>(w);
+      }
+      return hipGetLastError();
+    }
     constexpr int MT = 2;
     const int rw = 4 * MT * 16;
     const int sk = a.c_in + ((16 - a.c_in % 128) + 128) % 128;
