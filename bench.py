@@ -28,6 +28,50 @@ BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 matrix cores, TFLOP/s
 F32_PEAK_TFLOPS = 157.3        # fp32 vector
 
 
+# Measured HBM traffic per launch of each op's kernel on the default workload:
+# rocprofv3 --pmc FETCH_SIZE and --pmc WRITE_SIZE passes (KiB per dispatch),
+# tagged with a hash of the kernel's source file (plus the shared device
+# header) at the time the counters were taken.  A plain 256 MiB device copy
+# reads 131,083 KiB on FETCH_SIZE and 262,144 KiB on WRITE_SIZE, so bytes =
+# 2.0 x FETCH_SIZE + 1.0 x WRITE_SIZE.  When the source hash no longer
+# matches, the kernel has changed since the counters and traffic is null.
+FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
+COUNTER_WORKLOAD = "pair_b8_n208_224_bf16"
+COUNTERS = {  # op: (kernel source, source hash, FETCH_SIZE KiB, WRITE_SIZE KiB)
+    "attention_row": ("k_attention.hip", "5bcd92cc29a69522", 389791, 91895),
+    "transition": ("k_linear.hip", "86ed532cdb860f2e", 71840, 95170),
+    "triangle_out": ("k_triangle.hip", "8f868c65030d3dee", 317664, 90996),
+    "attn_proj": ("k_linear.hip", "86ed532cdb860f2e", 46039, 276189),
+    "tri_proj": ("k_linear.hip", "86ed532cdb860f2e", 45825, 197120),
+    "ln_linear": ("k_linear.hip", "86ed532cdb860f2e", 45724, 90996),
+    "attn_out_residual": ("k_linear.hip", "86ed532cdb860f2e", 91233, 90996),
+    "single_proj": ("k_linear.hip", "86ed532cdb860f2e", 1574, 853),
+    "pair_broadcast": ("k_segment.hip", "2fdde8205d37aa49", 1999, 90996),
+    "segment_mean": ("k_segment.hip", "2fdde8205d37aa49", 45570, 853),
+    "single_update": ("k_linear.hip", "86ed532cdb860f2e", 1645, 1928),
+}
+
+
+def source_hash(fname: str) -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in (fname, "nt_device.h"):
+        with open(os.path.join(ROOT, "paper_2609_30379_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(op: str, workload: str):
+    """HBM bytes per launch from the committed counters, or None when they do
+    not apply (another workload, or the kernel source changed since)."""
+    if workload != COUNTER_WORKLOAD or op not in COUNTERS:
+        return None
+    src, tag, fetch_kib, write_kib = COUNTERS[op]
+    if source_hash(src) != tag:
+        return None
+    return int((FETCH_SCALE * fetch_kib + WRITE_SCALE * write_kib) * 1024)
+
+
 def op_costs(w, L):
     """Algorithmic HBM bytes and flops per launch of every op of one block
     (bf16 storage = 2 bytes; every tensor read or written once)."""
@@ -68,9 +112,10 @@ def roofline_for(name, bytes_, flops, us, dtype):
             "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None}
 
 
-def cpu_baseline(w, run, budget_s: float = 30.0):
+def cpu_baseline(w, run, min_s: float = 10.0):
     """The CPU oracle timed on this host: one pass of the same pair block over
-    one sample of the workload (the smallest), pair positions per second."""
+    samples of the batch taken smallest first, one at a time, until at least
+    min_s seconds of work (about 10-15 s); pair positions per second."""
     import numpy as np
     from oracle import blocks as OB
     try:
@@ -78,21 +123,26 @@ def cpu_baseline(w, run, budget_s: float = 30.0):
         threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     except Exception:
         threads = 1
-    i = int(np.argmin(run.lengths))
-    n = run.lengths[i]
-    eta = int(np.sum(run.lengths[:i]))
     dims = dict(c_z=w.c_z, heads=w.heads, head_dim=w.head_dim)
-    s = run.s_init[eta:eta + n]
-    t0 = time.perf_counter()
-    z = None
-    for b in range(w.blocks):
-        steps = w.steps if b == 0 else tuple(t for t in w.steps if t != "lin")
-        s, z, _ = OB.pair_block(s, [n], run.params[b], dims, steps, z=z, dtype=w.dtype)
-    dt = time.perf_counter() - t0
-    return {"value": round(n * n * w.blocks / dt, 1), "unit": "pair positions/s", "cores": int(threads),
+    eta = np.concatenate([[0], np.cumsum(run.lengths)])
+    done, positions, dt = [], 0, 0.0
+    for i in np.argsort(run.lengths, kind="stable"):
+        n = int(run.lengths[i])
+        s = run.s_init[eta[i]:eta[i] + n]
+        t0 = time.perf_counter()
+        z = None
+        for b in range(w.blocks):
+            steps = w.steps if b == 0 else tuple(t for t in w.steps if t != "lin")
+            s, z, _ = OB.pair_block(s, [n], run.params[b], dims, steps, z=z, dtype=w.dtype)
+        dt += time.perf_counter() - t0
+        done.append(f"{int(i)} (N={n})")
+        positions += n * n * w.blocks
+        if dt >= min_s:
+            break
+    return {"value": round(positions / dt, 1), "unit": "pair positions/s", "cores": int(threads),
             "kind": "oracle",
-            "sample": f"sample {i} of the batch (N={n}, {n * n} pair positions), one pass of the block "
-                      f"({w.blocks} block(s)) in float64 NumPy, {dt:.1f} s; host has {os.cpu_count()} CPUs"}
+            "sample": f"samples {', '.join(done)} of the batch ({positions} pair positions), one pass of the block "
+                      f"({w.blocks} block(s)) each in float64 NumPy, {dt:.1f} s; host has {os.cpu_count()} CPUs"}
 
 
 def main():
@@ -157,12 +207,15 @@ def main():
     dominant = max(total_us, key=total_us.get)
     n_launch, us_launch = per_op[dominant]
     rl = roofline_for(dominant, costs[dominant][0], costs[dominant][1], us_launch, w.dtype)
+    rl["traffic"] = measured_traffic(dominant, w.name)
+    rl["algorithmic_bytes"] = costs[dominant][0]
     rl["us_per_launch"] = round(us_launch, 2)
     kernels = {}
     for k, (n, us) in per_op.items():
         r = roofline_for(k, costs[k][0], costs[k][1], us, w.dtype)
         kernels[k] = {"us": round(us, 2), "launches_per_step": n // args.steps, "bound": r["bound"],
-                      "frac": r["frac"]}
+                      "frac": r["frac"], "algorithmic_bytes": costs[k][0],
+                      "traffic": measured_traffic(k, w.name)}
 
     out = {
         "metric": METRIC, "value": round(w.blocks * R / (ms * 1e-3), 1), "unit": "pair positions/s",
@@ -179,7 +232,9 @@ def main():
         out["cpu_baseline"] = cpu_baseline(w, run)
     if args.kernels:
         for k, v in sorted(kernels.items(), key=lambda kv: -kv[1]["us"] * kv[1]["launches_per_step"]):
-            print(f"{k:20s} {v['us']:9.2f} us x{v['launches_per_step']}  {v['bound']} frac {v['frac']:.3f}",
+            tr = v["traffic"]
+            ratio = f"  traffic/alg {tr / v['algorithmic_bytes']:.2f}" if tr else ""
+            print(f"{k:20s} {v['us']:9.2f} us x{v['launches_per_step']}  {v['bound']} frac {v['frac']:.3f}{ratio}",
                   file=sys.stderr)
     print(json.dumps(out), flush=True)
 
