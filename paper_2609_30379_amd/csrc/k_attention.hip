@@ -205,6 +205,7 @@ struct PairAttnArgs {
   const int32_t* cu_seqlens;
   const int32_t* cu_pairs;
   int vstride, bstride;  // LDS strides (elements) of V^T and of the bias tile
+  float inv_scale;       // 1 / softmax scale (short-row kernel's bias staging)
 };
 
 template <int D, int NMAX>
@@ -399,6 +400,209 @@ __global__ void __launch_bounds__(256) attention_pair_kernel(PairAttnArgs p) {
   }
 }
 
+// ---------------------------------------------------------------- pair attention, short rows
+// Pair attention for head_dim 32 and N_i <= kAttn2MaxLen, organised so that
+// the exponentials are nearly the only vector work.  A workgroup of 8 waves
+// takes (sample, block of 128 queries, group of 16 pair rows, head):
+//   * the bias slice of its query block is staged once in LDS, divided by the
+//     softmax scale (one bf16 rounding), and becomes the initial value of the
+//     score accumulators, so the matrix cores produce bias/scale + q.k and the
+//     softmax needs no separate scale or bias step;
+//   * keys and values of a row are staged as fragment images (64 lanes x 16
+//     bytes, read as one contiguous 1 KB per wave), double-buffered, the next
+//     row loading into registers while the current row runs: one barrier per
+//     row;
+//   * the softmax denominator comes from one more matrix-core product with a
+//     ones operand, on the same bf16 probabilities as the numerator.
+// Scores are kept transposed (S^T = K Q^T), so a lane holds 16 keys of one
+// query per 64-key chunk and the running max is mostly lane-local.
+template <int NMAX>
+__global__ void __launch_bounds__(512, 1) attention_pair2_kernel(PairAttnArgs p) {
+  constexpr int D = 32;
+  extern __shared__ __attribute__((aligned(16))) bf16 lds[];
+  const int4 w4 = reinterpret_cast<const int4*>(p.work)[blockIdx.x];
+  const int i = w4.x;
+  if (i < 0) return;
+  const int jb = w4.y, rg = w4.z;
+  const int h = blockIdx.y;
+  const int n = p.cu_seqlens[i + 1] - p.cu_seqlens[i];
+  const int npad = (n + 63) & ~63;
+  const int64_t cu = p.cu_pairs[i];
+  const int64_t sr = p.axis == 0 ? n : 1, st = p.axis == 0 ? 1 : n;   // cell(r, t) = cu + r*sr + t*st
+  bf16* Bs = lds;                                          // [kAttnQB2][bstride]
+  bf16* Kb0 = Bs + (size_t)kAttnQB2 * p.bstride;           // key images: tile of 16 keys -> 512 elements
+  bf16* Kb1 = Kb0 + NMAX * D;
+  bf16* Vb0 = Kb1 + NMAX * D;                              // value images: (32 keys, 16 dims) -> 512 elements
+  bf16* Vb1 = Vb0 + NMAX * D;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, g = lane >> 4;
+  const int j0 = jb * kAttnQB2;
+
+  // ---- bias slice / scale: Bs[q][k] = bias(j0 + q, k) / scale, 0 past N --
+  {
+    const bf16* bh = p.bias ? p.bias + (int64_t)h * p.ld_bias + cu : nullptr;
+    const float inv_scale = p.inv_scale;
+    if (p.axis == 0) {
+      for (int e = tid; e < kAttnQB2 * (npad / 8); e += 512) {
+        const int q = e / (npad / 8), k0 = (e % (npad / 8)) * 8, j = j0 + q;
+        bf16x4 o0, o1;                            // rows are 8-byte aligned (stride 4 mod 8 elements)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          o0[u] = (bf16)((bh && j < n && k0 + u < n) ? (float)bh[(int64_t)j * n + k0 + u] * inv_scale : 0.f);
+          o1[u] = (bf16)((bh && j < n && k0 + 4 + u < n) ? (float)bh[(int64_t)j * n + k0 + 4 + u] * inv_scale : 0.f);
+        }
+        *reinterpret_cast<bf16x4*>(&Bs[q * p.bstride + k0]) = o0;
+        *reinterpret_cast<bf16x4*>(&Bs[q * p.bstride + k0 + 4]) = o1;
+      }
+    } else {
+      for (int e = tid; e < kAttnQB2 * npad; e += 512) {
+        const int q = e % kAttnQB2, k = e / kAttnQB2, j = j0 + q;
+        Bs[q * p.bstride + k] = (bf16)((bh && j < n && k < n) ? (float)bh[(int64_t)k * n + j] * inv_scale : 0.f);
+      }
+    }
+  }
+
+  // ---- per-row staging into fragment images --------------------------------
+  // keys: piece c = (key, dim group of 8); values: item c = (key pair, dim group)
+  constexpr int KP = (NMAX * 4 + 511) / 512;               // key pieces per thread
+  uint4 kr[KP], va[1], vb[1];
+  auto load_kv = [&](int r) {
+#pragma unroll
+    for (int j = 0; j < KP; ++j) {
+      const int c = tid + 512 * j, key = c >> 2, dg = c & 3;
+      const int64_t row = cu + (int64_t)r * sr + (int64_t)key * st;
+      kr[j] = key < n ? *reinterpret_cast<const uint4*>(p.k + row * p.ld_qkv + h * D + dg * 8) : make_uint4(0, 0, 0, 0);
+    }
+    {
+      const int kp = tid >> 2, dg = tid & 3, k0 = 2 * kp;
+      const int64_t row0 = cu + (int64_t)r * sr + (int64_t)k0 * st;
+      va[0] = (k0 < n && k0 < NMAX) ? *reinterpret_cast<const uint4*>(p.v + row0 * p.ld_qkv + h * D + dg * 8) : make_uint4(0, 0, 0, 0);
+      vb[0] = (k0 + 1 < n && k0 < NMAX) ? *reinterpret_cast<const uint4*>(p.v + (row0 + st) * p.ld_qkv + h * D + dg * 8)
+                                        : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto store_kv = [&](bf16* Kb, bf16* Vb) {
+#pragma unroll
+    for (int j = 0; j < KP; ++j) {
+      const int c = tid + 512 * j, key = c >> 2, dg = c & 3;
+      if (key < npad) *reinterpret_cast<uint4*>(&Kb[(key >> 4) * 512 + (dg * 16 + (key & 15)) * 8]) = kr[j];
+    }
+    const int kp = tid >> 2, dg = tid & 3, k0 = 2 * kp;
+    if (k0 < npad) {
+      // key k0 (even) and k0+1 share a lane: slot (kin/16)*4 + kin%4 of k-group (kin%16)/4
+      const int kin = k0 & 31, kgrp = (kin & 15) >> 2, slot = (kin >> 4) * 4 + (kin & 3);
+      const uint32_t a[4] = {va[0].x, va[0].y, va[0].z, va[0].w};
+      const uint32_t b[4] = {vb[0].x, vb[0].y, vb[0].z, vb[0].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          const int d = dg * 8 + 2 * e + hf;
+          const uint32_t pair = hf ? ((a[e] >> 16) | (b[e] & 0xffff0000u)) : ((a[e] & 0xffffu) | (b[e] << 16));
+          bf16* img = Vb + ((k0 >> 5) * 2 + (d >> 4)) * 512;
+          *reinterpret_cast<uint32_t*>(&img[(kgrp * 16 + (d & 15)) * 8 + slot]) = pair;
+        }
+      }
+    }
+  };
+
+  const int jw = j0 + 16 * wave + l16;          // this lane's query
+  const bool wave_has_queries = j0 + 16 * wave < n;
+  const bool qvalid = jw < n;
+  const int r0 = rg * kAttnRG2, r1 = min(n, r0 + kAttnRG2);
+  load_kv(r0);
+  bf16x8 qf = qvalid ? *reinterpret_cast<const bf16x8*>(p.q + (cu + (int64_t)r0 * sr + (int64_t)jw * st) * p.ld_qkv + h * D + g * 8)
+                     : bf16x8{};
+  store_kv(Kb0, Vb0);
+  __syncthreads();
+
+  bf16x8 ones;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) ones[e] = (bf16)1.f;
+  const float c = p.scale_log2;                 // scale * log2(e)
+  const bf16* brow = &Bs[(16 * wave + l16) * p.bstride];
+  for (int r = r0; r < r1; ++r) {
+    const bool odd = (r - r0) & 1;
+    const bf16* Kb = odd ? Kb1 : Kb0;
+    const bf16* Vb = odd ? Vb1 : Vb0;
+    const bool more = r + 1 < r1;
+    bf16x8 qn = qf;
+    if (more) {
+      load_kv(r + 1);
+      if (qvalid) qn = *reinterpret_cast<const bf16x8*>(p.q + (cu + (int64_t)(r + 1) * sr + (int64_t)jw * st) * p.ld_qkv + h * D + g * 8);
+    }
+    if (wave_has_queries) {
+      float m_s = -INFINITY;                      // running max of bias/scale + q.k
+      f32x4 O[3];                                 // dims 0-15, 16-31, row sum
+#pragma unroll
+      for (int t = 0; t < 3; ++t) O[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+      auto chunk = [&](int kc, bool tail) {
+        f32x4 sacc[4];
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt) {
+          const uint2 bb = *reinterpret_cast<const uint2*>(brow + kc + kt * 16 + 4 * g);
+          sacc[kt] = f32x4{__uint_as_float(bb.x << 16), __uint_as_float(bb.x & 0xffff0000u),
+                           __uint_as_float(bb.y << 16), __uint_as_float(bb.y & 0xffff0000u)};
+          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Kb[((kc >> 4) + kt) * 512 + lane * 8]);
+          sacc[kt] = mfma16(kf, qf, sacc[kt]);
+        }
+        if (tail) {
+#pragma unroll
+          for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+            for (int ii = 0; ii < 4; ++ii)
+              if (kc + kt * 16 + 4 * g + ii >= n) sacc[kt][ii] = -INFINITY;
+        }
+        float mloc = fmaxf(fmaxf(sacc[0][0], sacc[0][1]), fmaxf(sacc[0][2], sacc[0][3]));
+#pragma unroll
+        for (int kt = 1; kt < 4; ++kt)
+          mloc = fmaxf(mloc, fmaxf(fmaxf(sacc[kt][0], sacc[kt][1]), fmaxf(sacc[kt][2], sacc[kt][3])));
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+        const float m_new = fmaxf(m_s, mloc);
+        const float alpha = __builtin_amdgcn_exp2f((m_s - m_new) * c);
+        m_s = m_new;
+#pragma unroll
+        for (int t = 0; t < 3; ++t) O[t] *= alpha;
+        const float nm = -m_new * c;
+        bf16x8 pf[2];
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+          for (int ii = 0; ii < 4; ++ii)
+            pf[kt >> 1][(kt & 1) * 4 + ii] = (bf16)__builtin_amdgcn_exp2f(fmaf(sacc[kt][ii], c, nm));
+#pragma unroll
+        for (int pp = 0; pp < 2; ++pp) {
+          const int kb = (kc >> 5) + pp;
+#pragma unroll
+          for (int dt = 0; dt < 2; ++dt) {
+            const bf16x8 vf = *reinterpret_cast<const bf16x8*>(&Vb[(kb * 2 + dt) * 512 + lane * 8]);
+            O[dt] = mfma16(vf, pf[pp], O[dt]);
+          }
+          O[2] = mfma16(ones, pf[pp], O[2]);
+        }
+      };
+      const int full = n & ~63;
+      for (int kc = 0; kc < full; kc += 64) chunk(kc, false);
+      if (full < n) chunk(full, true);
+      if (qvalid) {
+        const float inv = 1.f / O[2][0];
+        bf16* orow = p.o + (cu + (int64_t)r * sr + (int64_t)jw * st) * p.ld_o + h * D;
+#pragma unroll
+        for (int dt = 0; dt < 2; ++dt) {
+          bf16x4 ov;
+#pragma unroll
+          for (int ii = 0; ii < 4; ++ii) ov[ii] = (bf16)(O[dt][ii] * inv);
+          *reinterpret_cast<bf16x4*>(orow + dt * 16 + 4 * g) = ov;
+        }
+      }
+    }
+    if (more) store_kv(odd ? Kb0 : Kb1, odd ? Vb0 : Vb1);
+    __syncthreads();
+    qf = qn;
+  }
+}
+
 // ---------------------------------------------------------------- fp32 path
 struct AttnF32Args {
   int axis, H;
@@ -476,11 +680,24 @@ hipError_t launch_attention(const nt_layout& L, int axis, int H, int D, const vo
     return hipGetLastError();
   }
   const int npad = (L.max_len + 63) & ~63;
+  if (D == 32 && axis != 2 && L.max_len <= kAttn2MaxLen) {
+    if (L.pattn2_items() == 0) return hipSuccess;
+    // bias rows: 8-byte fragment reads are conflict-free with a row stride of 2 (mod 4) dwords
+    const int bstride = kAttn2MaxLen + 4;
+    PairAttnArgs a{axis, (const bf16*)q, (const bf16*)k, (const bf16*)v, ld_qkv, (const bf16*)bias, ld_bias,
+                   scale * kLog2e, (bf16*)o, ld_o, L.d_pattn2_work, L.d_cu_seqlens, L.d_cu_pairs, 0, bstride,
+                   1.f / scale};
+    const size_t smem = sizeof(bf16) * ((size_t)kAttnQB2 * bstride + 4 * (size_t)kAttn2MaxLen * 32);
+    const dim3 grid((unsigned)L.pattn2_items(), (unsigned)H);
+    hipFuncSetAttribute((const void*)attention_pair2_kernel<kAttn2MaxLen>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    attention_pair2_kernel<kAttn2MaxLen><<<grid, dim3(512), smem, s>>>(a);
+    return hipGetLastError();
+  }
   if (D == 32 && axis != 2 && L.max_len <= kAttnFastMaxLen) {
     // 8-byte fragment reads are conflict-free with a row stride of 2 (mod 4) dwords
     const int stride = (npad + 127) / 128 * 128 + 4;
     PairAttnArgs a{axis, (const bf16*)q, (const bf16*)k, (const bf16*)v, ld_qkv, (const bf16*)bias, ld_bias,
-                   scale * kLog2e, (bf16*)o, ld_o, L.d_pattn_work, L.d_cu_seqlens, L.d_cu_pairs, stride, stride};
+                   scale * kLog2e, (bf16*)o, ld_o, L.d_pattn_work, L.d_cu_seqlens, L.d_cu_pairs, stride, stride, 0.f};
     const size_t smem = sizeof(bf16) * ((size_t)npad * (32 + 8) + (size_t)32 * stride + (size_t)kAttnQB * stride);
     if (L.pattn_items() == 0) return hipSuccess;
     const dim3 grid((unsigned)L.pattn_items(), (unsigned)H);

@@ -128,23 +128,25 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L) {
       }
     L->attn_work = xcd_order<2>(items, cost);
   }
-  // pair attention, bias-resident form: one item per (sample, block of kAttnQB
-  // queries, group of kAttnRG pair rows); the query blocks of one row group are
+  // pair attention, bias-resident form: one item per (sample, block of QB
+  // queries, group of RG pair rows); the query blocks of one row group are
   // generated next to each other so they run back to back on one XCD and share
   // the rows' keys and values in its L2
-  {
+  auto pair_attn_items = [&](int32_t QB, int32_t RG) {
     std::vector<std::array<int32_t, 4>> items;
     std::vector<double> cost;
     for (int32_t i = 0; i < batch; ++i) {
       const int32_t n = lengths[i];
-      for (int32_t rg = 0; rg * kAttnRG < n; ++rg)
-        for (int32_t jb = 0; jb * kAttnQB < n; ++jb) {
+      for (int32_t rg = 0; rg * RG < n; ++rg)
+        for (int32_t jb = 0; jb * QB < n; ++jb) {
           items.push_back({i, jb, rg, 0});
-          cost.push_back((double)std::min(kAttnRG, n - rg * kAttnRG) * std::min(kAttnQB, n - jb * kAttnQB) * n);
+          cost.push_back((double)std::min(RG, n - rg * RG) * std::min(QB, n - jb * QB) * n);
         }
     }
-    L->pattn_work = xcd_order<4>(items, cost);
-  }
+    return xcd_order<4>(items, cost);
+  };
+  L->pattn_work = pair_attn_items(kAttnQB, kAttnRG);
+  L->pattn2_work = pair_attn_items(kAttnQB2, kAttnRG2);
   // triangle: one item per (sample, 32x32 output tile), largest samples first.
   // The channel blocks, not the tiles, are spread over the XCDs (the launch
   // interleaves every tile's channel blocks), so each XCD walks the whole list
