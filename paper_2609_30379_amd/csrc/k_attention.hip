@@ -9,6 +9,8 @@
 //                     so the running max/sum of a query live in one lane column
 //   O^T += V^T P^T    P is taken from the S^T registers as the B operand
 //                     (keys {4g..4g+3} of two 16-key tiles), no shuffles.
+#include <algorithm>
+
 #include "nt_device.h"
 #include "nt_internal.h"
 
@@ -206,6 +208,7 @@ struct PairAttnArgs {
   const int32_t* cu_pairs;
   int vstride, bstride;  // LDS strides (elements) of V^T and of the bias tile
   float inv_scale;       // 1 / softmax scale (short-row kernel's bias staging)
+  int H;                 // heads (short-row kernel: heads interleaved in the grid)
 };
 
 template <int D, int NMAX>
@@ -402,37 +405,44 @@ __global__ void __launch_bounds__(256) attention_pair_kernel(PairAttnArgs p) {
 
 // ---------------------------------------------------------------- pair attention, short rows
 // Pair attention for head_dim 32 and N_i <= kAttn2MaxLen, organised so that
-// the exponentials are nearly the only vector work.  A workgroup of 8 waves
-// takes (sample, block of 128 queries, group of 16 pair rows, head):
-//   * the bias slice of its query block is staged once in LDS, divided by the
-//     softmax scale (one bf16 rounding), and becomes the initial value of the
-//     score accumulators, so the matrix cores produce bias/scale + q.k and the
-//     softmax needs no separate scale or bias step;
+// the exponentials are nearly the only vector work and two workgroups share
+// each CU.  A workgroup of 8 waves takes (sample, block of 128 queries, group
+// of 16 pair rows, head):
+//   * the bias of (query, key) does not depend on the pair row, so each lane
+//     keeps the bias of its query for its 4-key groups of every key tile in
+//     registers for the whole group of rows -- staged once through LDS and
+//     divided by the softmax scale (one bf16 rounding) -- and it seeds the
+//     score accumulators: the matrix cores produce bias/scale + q.k directly;
 //   * keys and values of a row are staged as fragment images (64 lanes x 16
-//     bytes, read as one contiguous 1 KB per wave), double-buffered, the next
-//     row loading into registers while the current row runs: one barrier per
-//     row;
+//     bytes, read as one contiguous 1 KB per wave) in two buffers that alias
+//     the bias staging area, the next row loading into registers while the
+//     current row runs: one barrier per row, 64 KB of LDS;
 //   * the softmax denominator comes from one more matrix-core product with a
 //     ones operand, on the same bf16 probabilities as the numerator.
 // Scores are kept transposed (S^T = K Q^T), so a lane holds 16 keys of one
 // query per 64-key chunk and the running max is mostly lane-local.
 template <int NMAX>
-__global__ void __launch_bounds__(512, 1) attention_pair2_kernel(PairAttnArgs p) {
+__global__ void __launch_bounds__(512, 4) attention_pair2_kernel(PairAttnArgs p) {
   constexpr int D = 32;
+  constexpr int KT16 = NMAX / 16;               // key tiles
   extern __shared__ __attribute__((aligned(16))) bf16 lds[];
-  const int4 w4 = reinterpret_cast<const int4*>(p.work)[blockIdx.x];
+  // Work position pos runs on XCD pos % 8; the H heads of one position are
+  // launched as consecutive workgroups of that XCD (ids 8 (H k + h) + x), so
+  // they read the same q|k|v cache lines at about the same time.
+  const int x = blockIdx.x % kXcds, t = blockIdx.x / kXcds;
+  const int h = t % p.H, pos = (t / p.H) * kXcds + x;
+  const int4 w4 = reinterpret_cast<const int4*>(p.work)[pos];
   const int i = w4.x;
   if (i < 0) return;
   const int jb = w4.y, rg = w4.z;
-  const int h = blockIdx.y;
   const int n = p.cu_seqlens[i + 1] - p.cu_seqlens[i];
   const int npad = (n + 63) & ~63;
   const int64_t cu = p.cu_pairs[i];
   const int64_t sr = p.axis == 0 ? n : 1, st = p.axis == 0 ? 1 : n;   // cell(r, t) = cu + r*sr + t*st
-  bf16* Bs = lds;                                          // [kAttnQB2][bstride]
-  bf16* Kb0 = Bs + (size_t)kAttnQB2 * p.bstride;           // key images: tile of 16 keys -> 512 elements
+  bf16* Bs = lds;                                          // [kAttnQB2][bstride], start-up only
+  bf16* Kb0 = lds;                                         // key images: tile of 16 keys -> 512 elements
   bf16* Kb1 = Kb0 + NMAX * D;
-  bf16* Vb0 = Kb1 + NMAX * D;                              // value images: (32 keys, 16 dims) -> 512 elements
+  bf16* Vb0 = Kb1 + NMAX * D;                              // values, row-major [key][D]
   bf16* Vb1 = Vb0 + NMAX * D;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, g = lane >> 4;
@@ -462,65 +472,61 @@ __global__ void __launch_bounds__(512, 1) attention_pair2_kernel(PairAttnArgs p)
     }
   }
 
-  // ---- per-row staging into fragment images --------------------------------
-  // keys: piece c = (key, dim group of 8); values: item c = (key pair, dim group)
-  constexpr int KP = (NMAX * 4 + 511) / 512;               // key pieces per thread
-  uint4 kr[KP], va[1], vb[1];
-  auto load_kv = [&](int r) {
+  // ---- per-row staging: straight global -> LDS copies ---------------------
+  // Each wave copies its key tiles (wave, wave + 8, ...; 16 keys each) with
+  // global_load_lds, lane l's 16 bytes landing at byte 16 l of the tile:
+  //   keys as fragment images: lane l = (key l%16, dims 8 (l/16) ..),
+  //   values row-major [key][32]: lane l = (key l/4, dims 8 (l%4) ..).
+  // Every tile below the 64-key padded length is written (the last chunk
+  // reads up to there): keys past N repeat key N-1, so the padding holds
+  // finite values whose probabilities are masked to zero.
+  auto dma_kv = [&](int r, bf16* Kb, bf16* Vr) {
 #pragma unroll
-    for (int j = 0; j < KP; ++j) {
-      const int c = tid + 512 * j, key = c >> 2, dg = c & 3;
-      const int64_t row = cu + (int64_t)r * sr + (int64_t)key * st;
-      kr[j] = key < n ? *reinterpret_cast<const uint4*>(p.k + row * p.ld_qkv + h * D + dg * 8) : make_uint4(0, 0, 0, 0);
-    }
-    {
-      const int kp = tid >> 2, dg = tid & 3, k0 = 2 * kp;
-      const int64_t row0 = cu + (int64_t)r * sr + (int64_t)k0 * st;
-      va[0] = (k0 < n && k0 < NMAX) ? *reinterpret_cast<const uint4*>(p.v + row0 * p.ld_qkv + h * D + dg * 8) : make_uint4(0, 0, 0, 0);
-      vb[0] = (k0 + 1 < n && k0 < NMAX) ? *reinterpret_cast<const uint4*>(p.v + (row0 + st) * p.ld_qkv + h * D + dg * 8)
-                                        : make_uint4(0, 0, 0, 0);
+    for (int kt = wave; kt < KT16; kt += 8) {
+      if (kt * 16 >= npad) break;
+      const int key_k = min(kt * 16 + l16, n - 1), key_v = min(kt * 16 + (lane >> 2), n - 1);
+      const bf16* sk = p.k + (cu + (int64_t)r * sr + (int64_t)key_k * st) * p.ld_qkv + h * D + g * 8;
+      const bf16* sv = p.v + (cu + (int64_t)r * sr + (int64_t)key_v * st) * p.ld_qkv + h * D + (lane & 3) * 8;
+      __builtin_amdgcn_global_load_lds((const void*)sk, (__attribute__((address_space(3))) void*)(Kb + kt * 512), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((const void*)sv, (__attribute__((address_space(3))) void*)(Vr + kt * 512), 16, 0, 0);
     }
   };
-  auto store_kv = [&](bf16* Kb, bf16* Vb) {
-#pragma unroll
-    for (int j = 0; j < KP; ++j) {
-      const int c = tid + 512 * j, key = c >> 2, dg = c & 3;
-      if (key < npad) *reinterpret_cast<uint4*>(&Kb[(key >> 4) * 512 + (dg * 16 + (key & 15)) * 8]) = kr[j];
-    }
-    const int kp = tid >> 2, dg = tid & 3, k0 = 2 * kp;
-    if (k0 < npad) {
-      // key k0 (even) and k0+1 share a lane: slot (kin/16)*4 + kin%4 of k-group (kin%16)/4
-      const int kin = k0 & 31, kgrp = (kin & 15) >> 2, slot = (kin >> 4) * 4 + (kin & 3);
-      const uint32_t a[4] = {va[0].x, va[0].y, va[0].z, va[0].w};
-      const uint32_t b[4] = {vb[0].x, vb[0].y, vb[0].z, vb[0].w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-          const int d = dg * 8 + 2 * e + hf;
-          const uint32_t pair = hf ? ((a[e] >> 16) | (b[e] & 0xffff0000u)) : ((a[e] & 0xffffu) | (b[e] << 16));
-          bf16* img = Vb + ((k0 >> 5) * 2 + (d >> 4)) * 512;
-          *reinterpret_cast<uint32_t*>(&img[(kgrp * 16 + (d & 15)) * 8 + slot]) = pair;
-        }
-      }
-    }
+  // Value fragment for O^T += V^T P^T: lane (dim 16 dt + l16, k-group g)
+  // needs keys 32 kb + {4g..4g+3, 16+4g..16+4g+3}.  ds_read_b64_tr_b16 hands
+  // lane 4q+m of each 16-lane group element m of the 8-byte pieces addressed
+  // by lanes q, q+4, q+8, q+12; pointing lane i at key base + i/4, dims
+  // 16 dt + 4 (i%4) therefore delivers 4 consecutive keys of dim l16.
+  auto v_frag = [&](const bf16* Vr, int kb, int dt) -> bf16x8 {
+    typedef short s4 __attribute__((ext_vector_type(4)));
+    const int kk = kb * 32 + 4 * g + (l16 >> 2), dd = dt * 16 + 4 * (l16 & 3);
+    const s4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4*)(Vr + kk * D + dd));
+    const s4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4*)(Vr + (kk + 16) * D + dd));
+    const bf16x4 a = __builtin_bit_cast(bf16x4, lo), b = __builtin_bit_cast(bf16x4, hi);
+    return bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
   };
 
   const int jw = j0 + 16 * wave + l16;          // this lane's query
   const bool wave_has_queries = j0 + 16 * wave < n;
   const bool qvalid = jw < n;
   const int r0 = rg * kAttnRG2, r1 = min(n, r0 + kAttnRG2);
-  load_kv(r0);
   bf16x8 qf = qvalid ? *reinterpret_cast<const bf16x8*>(p.q + (cu + (int64_t)r0 * sr + (int64_t)jw * st) * p.ld_qkv + h * D + g * 8)
                      : bf16x8{};
-  store_kv(Kb0, Vb0);
+  __syncthreads();                              // bias slice staged
+  // lane's bias: query 16*wave + l16, keys 16*kt + 4g .. +3 of every key tile
+  uint2 bias_r[KT16];
+#pragma unroll
+  for (int kt = 0; kt < KT16; ++kt)
+    bias_r[kt] = kt * 16 < npad ? *reinterpret_cast<const uint2*>(&Bs[(16 * wave + l16) * p.bstride + kt * 16 + 4 * g])
+                                : make_uint2(0u, 0u);
+  __syncthreads();                              // staging area free for keys and values
+  dma_kv(r0, Kb0, Vb0);
+  __builtin_amdgcn_s_waitcnt(0);                // this wave's copies have landed
   __syncthreads();
 
   bf16x8 ones;
 #pragma unroll
   for (int e = 0; e < 8; ++e) ones[e] = (bf16)1.f;
   const float c = p.scale_log2;                 // scale * log2(e)
-  const bf16* brow = &Bs[(16 * wave + l16) * p.bstride];
   for (int r = r0; r < r1; ++r) {
     const bool odd = (r - r0) & 1;
     const bf16* Kb = odd ? Kb1 : Kb0;
@@ -528,22 +534,32 @@ __global__ void __launch_bounds__(512, 1) attention_pair2_kernel(PairAttnArgs p)
     const bool more = r + 1 < r1;
     bf16x8 qn = qf;
     if (more) {
-      load_kv(r + 1);
+      dma_kv(r + 1, odd ? Kb0 : Kb1, odd ? Vb0 : Vb1);
       if (qvalid) qn = *reinterpret_cast<const bf16x8*>(p.q + (cu + (int64_t)(r + 1) * sr + (int64_t)jw * st) * p.ld_qkv + h * D + g * 8);
     }
+    // keep the bias packed: converting it once outside the row loop would
+    // double its registers
+#pragma unroll
+    for (int kt = 0; kt < KT16; ++kt) asm volatile("" : "+v"(bias_r[kt].x), "+v"(bias_r[kt].y));
     if (wave_has_queries) {
       float m_s = -INFINITY;                      // running max of bias/scale + q.k
       f32x4 O[3];                                 // dims 0-15, 16-31, row sum
 #pragma unroll
-      for (int t = 0; t < 3; ++t) O[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-      auto chunk = [&](int kc, bool tail) {
+      for (int u = 0; u < 3; ++u) O[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ci = 0; ci < NMAX / 64; ++ci) {
+        const int kc = ci * 64;
+        if (kc >= n) break;
+        const bool tail = kc + 64 > n;
+        const int ntile = (tail && n - kc <= 32) ? 2 : 4;   // a short tail takes half a chunk
         f32x4 sacc[4];
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt) {
-          const uint2 bb = *reinterpret_cast<const uint2*>(brow + kc + kt * 16 + 4 * g);
+          if (kt >= ntile) break;
+          const uint2 bb = bias_r[ci * 4 + kt];
           sacc[kt] = f32x4{__uint_as_float(bb.x << 16), __uint_as_float(bb.x & 0xffff0000u),
                            __uint_as_float(bb.y << 16), __uint_as_float(bb.y & 0xffff0000u)};
-          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Kb[((kc >> 4) + kt) * 512 + lane * 8]);
+          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Kb[(ci * 4 + kt) * 512 + lane * 8]);
           sacc[kt] = mfma16(kf, qf, sacc[kt]);
         }
         if (tail) {
@@ -551,40 +567,39 @@ __global__ void __launch_bounds__(512, 1) attention_pair2_kernel(PairAttnArgs p)
           for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
             for (int ii = 0; ii < 4; ++ii)
-              if (kc + kt * 16 + 4 * g + ii >= n) sacc[kt][ii] = -INFINITY;
+              if (kt >= ntile || kc + kt * 16 + 4 * g + ii >= n) sacc[kt][ii] = -INFINITY;
         }
         float mloc = fmaxf(fmaxf(sacc[0][0], sacc[0][1]), fmaxf(sacc[0][2], sacc[0][3]));
 #pragma unroll
-        for (int kt = 1; kt < 4; ++kt)
+        for (int kt = 1; kt < 4; ++kt) {
+          if (kt >= ntile) break;
           mloc = fmaxf(mloc, fmaxf(fmaxf(sacc[kt][0], sacc[kt][1]), fmaxf(sacc[kt][2], sacc[kt][3])));
+        }
         mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
         mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
         const float m_new = fmaxf(m_s, mloc);
         const float alpha = __builtin_amdgcn_exp2f((m_s - m_new) * c);
         m_s = m_new;
 #pragma unroll
-        for (int t = 0; t < 3; ++t) O[t] *= alpha;
+        for (int u = 0; u < 3; ++u) O[u] *= alpha;
         const float nm = -m_new * c;
         bf16x8 pf[2];
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
+        for (int kt = 0; kt < 4; ++kt) {
+          if (kt >= ntile) break;
 #pragma unroll
           for (int ii = 0; ii < 4; ++ii)
             pf[kt >> 1][(kt & 1) * 4 + ii] = (bf16)__builtin_amdgcn_exp2f(fmaf(sacc[kt][ii], c, nm));
+        }
 #pragma unroll
         for (int pp = 0; pp < 2; ++pp) {
-          const int kb = (kc >> 5) + pp;
+          if (2 * pp >= ntile) break;
+          const int kb = ci * 2 + pp;
 #pragma unroll
-          for (int dt = 0; dt < 2; ++dt) {
-            const bf16x8 vf = *reinterpret_cast<const bf16x8*>(&Vb[(kb * 2 + dt) * 512 + lane * 8]);
-            O[dt] = mfma16(vf, pf[pp], O[dt]);
-          }
+          for (int dt = 0; dt < 2; ++dt) O[dt] = mfma16(v_frag(Vb, kb, dt), pf[pp], O[dt]);
           O[2] = mfma16(ones, pf[pp], O[2]);
         }
-      };
-      const int full = n & ~63;
-      for (int kc = 0; kc < full; kc += 64) chunk(kc, false);
-      if (full < n) chunk(full, true);
+      }
       if (qvalid) {
         const float inv = 1.f / O[2][0];
         bf16* orow = p.o + (cu + (int64_t)r * sr + (int64_t)jw * st) * p.ld_o + h * D;
@@ -597,7 +612,7 @@ __global__ void __launch_bounds__(512, 1) attention_pair2_kernel(PairAttnArgs p)
         }
       }
     }
-    if (more) store_kv(odd ? Kb0 : Kb1, odd ? Vb0 : Vb1);
+    __builtin_amdgcn_s_waitcnt(0);              // copies for the next row have landed
     __syncthreads();
     qf = qn;
   }
@@ -686,9 +701,9 @@ hipError_t launch_attention(const nt_layout& L, int axis, int H, int D, const vo
     const int bstride = kAttn2MaxLen + 4;
     PairAttnArgs a{axis, (const bf16*)q, (const bf16*)k, (const bf16*)v, ld_qkv, (const bf16*)bias, ld_bias,
                    scale * kLog2e, (bf16*)o, ld_o, L.d_pattn2_work, L.d_cu_seqlens, L.d_cu_pairs, 0, bstride,
-                   1.f / scale};
-    const size_t smem = sizeof(bf16) * ((size_t)kAttnQB2 * bstride + 4 * (size_t)kAttn2MaxLen * 32);
-    const dim3 grid((unsigned)L.pattn2_items(), (unsigned)H);
+                   1.f / scale, H};
+    const size_t smem = sizeof(bf16) * std::max((size_t)kAttnQB2 * bstride, 4 * (size_t)kAttn2MaxLen * 32);
+    const dim3 grid((unsigned)(L.pattn2_items() * H));
     hipFuncSetAttribute((const void*)attention_pair2_kernel<kAttn2MaxLen>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     attention_pair2_kernel<kAttn2MaxLen><<<grid, dim3(512), smem, s>>>(a);
     return hipGetLastError();
@@ -697,7 +712,7 @@ hipError_t launch_attention(const nt_layout& L, int axis, int H, int D, const vo
     // 8-byte fragment reads are conflict-free with a row stride of 2 (mod 4) dwords
     const int stride = (npad + 127) / 128 * 128 + 4;
     PairAttnArgs a{axis, (const bf16*)q, (const bf16*)k, (const bf16*)v, ld_qkv, (const bf16*)bias, ld_bias,
-                   scale * kLog2e, (bf16*)o, ld_o, L.d_pattn_work, L.d_cu_seqlens, L.d_cu_pairs, stride, stride, 0.f};
+                   scale * kLog2e, (bf16*)o, ld_o, L.d_pattn_work, L.d_cu_seqlens, L.d_cu_pairs, stride, stride, 0.f, H};
     const size_t smem = sizeof(bf16) * ((size_t)npad * (32 + 8) + (size_t)32 * stride + (size_t)kAttnQB * stride);
     if (L.pattn_items() == 0) return hipSuccess;
     const dim3 grid((unsigned)L.pattn_items(), (unsigned)H);

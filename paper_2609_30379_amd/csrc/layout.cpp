@@ -19,7 +19,7 @@ namespace {
 // the summed cost per XCD is balanced.  Idle positions are filled with -1.
 template <int W>
 std::vector<int32_t> xcd_order(const std::vector<std::array<int32_t, W>>& items,
-                               const std::vector<double>& cost) {
+                               const std::vector<double>& cost, bool largest_first = true) {
   const size_t n = items.size();
   std::vector<size_t> idx(n);
   std::iota(idx.begin(), idx.end(), 0);
@@ -48,7 +48,7 @@ std::vector<int32_t> xcd_order(const std::vector<std::array<int32_t, W>>& items,
   }
   size_t depth = 0;
   for (auto& v : q) {
-    std::stable_sort(v.begin(), v.end(), [&](size_t a, size_t b) { return cost[a] > cost[b]; });
+    if (largest_first) std::stable_sort(v.begin(), v.end(), [&](size_t a, size_t b) { return cost[a] > cost[b]; });
     depth = std::max(depth, v.size());
   }
   std::vector<int32_t> out(depth * kXcds * W, -1);
@@ -132,7 +132,7 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L) {
   // queries, group of RG pair rows); the query blocks of one row group are
   // generated next to each other so they run back to back on one XCD and share
   // the rows' keys and values in its L2
-  auto pair_attn_items = [&](int32_t QB, int32_t RG) {
+  auto pair_attn_items = [&](int32_t QB, int32_t RG, bool largest_first) {
     std::vector<std::array<int32_t, 4>> items;
     std::vector<double> cost;
     for (int32_t i = 0; i < batch; ++i) {
@@ -143,10 +143,12 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L) {
           cost.push_back((double)std::min(RG, n - rg * RG) * std::min(QB, n - jb * QB) * n);
         }
     }
-    return xcd_order<4>(items, cost);
+    return xcd_order<4>(items, cost, largest_first);
   };
-  L->pattn_work = pair_attn_items(kAttnQB, kAttnRG);
-  L->pattn2_work = pair_attn_items(kAttnQB2, kAttnRG2);
+  L->pattn_work = pair_attn_items(kAttnQB, kAttnRG, true);
+  // the short-row kernel keeps generation order inside each XCD's queue, so
+  // the query blocks of a row group stay adjacent and share keys and values
+  L->pattn2_work = pair_attn_items(kAttnQB2, kAttnRG2, false);
   // triangle: one item per (sample, 32x32 output tile), largest samples first.
   // The channel blocks, not the tiles, are spread over the XCDs (the launch
   // interleaves every tile's channel blocks), so each XCD walks the whole list

@@ -207,10 +207,14 @@ def test_pair_attention(B, axis, dtype, H, D, lset):
     td = torch.bfloat16 if dtype == "bf16" else torch.float32
     o = torch.full((R, H * D), float("nan"), dtype=td, device="cuda")
     c = H * D
-    B.nt_pair_row_attention(lay, axis, H, D, qd[:, :c], qd[:, c:2 * c], qd[:, 2 * c:], o,
-                            bias=dev(_head_major(bias), dtype))
+    bd = dev(_head_major(bias), dtype)
+    B.nt_pair_row_attention(lay, axis, H, D, qd[:, :c], qd[:, c:2 * c], qd[:, 2 * c:], o, bias=bd)
+    first = host(o)
+    # a second call over whatever the first left in LDS must give the same bits
+    B.nt_pair_row_attention(lay, axis, H, D, qd[:, :c], qd[:, c:2 * c], qd[:, 2 * c:], o, bias=bd)
+    assert np.array_equal(host(o), first, equal_nan=True), "pair attention is not deterministic"
     ref = O.pair_row_attention(qkv[:, :c], qkv[:, c:2 * c], qkv[:, 2 * c:], bias, L, H, D, axis=axis)
-    check(host(o), ref, dtype, f"pair attention axis {axis} {dtype}")
+    check(first, ref, dtype, f"pair attention axis {axis} {dtype}")
 
 
 @pytest.mark.parametrize("dtype,H,D,L", [("bf16", 3, 64, [1, 5, 64, 65, 130, 512, 0, 200]),
