@@ -491,18 +491,31 @@ __global__ void __launch_bounds__(512, 4) attention_pair2_kernel(PairAttnArgs p)
       __builtin_amdgcn_global_load_lds((const void*)sv, (__attribute__((address_space(3))) void*)(Vr + kt * 512), 16, 0, 0);
     }
   };
-  // Value fragment for O^T += V^T P^T: lane (dim 16 dt + l16, k-group g)
+  // Value fragments for O^T += V^T P^T: lane (dim 16 dt + l16, k-group g)
   // needs keys 32 kb + {4g..4g+3, 16+4g..16+4g+3}.  ds_read_b64_tr_b16 hands
   // lane 4q+m of each 16-lane group element m of the 8-byte pieces addressed
   // by lanes q, q+4, q+8, q+12; pointing lane i at key base + i/4, dims
-  // 16 dt + 4 (i%4) therefore delivers 4 consecutive keys of dim l16.
-  auto v_frag = [&](const bf16* Vr, int kb, int dt) -> bf16x8 {
-    typedef short s4 __attribute__((ext_vector_type(4)));
-    const int kk = kb * 32 + 4 * g + (l16 >> 2), dd = dt * 16 + 4 * (l16 & 3);
-    const s4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4*)(Vr + kk * D + dd));
-    const s4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4*)(Vr + (kk + 16) * D + dd));
-    const bf16x4 a = __builtin_bit_cast(bf16x4, lo), b = __builtin_bit_cast(bf16x4, hi);
-    return bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  // 16 dt + 4 (i%4) therefore delivers 4 consecutive keys of dim l16.  The
+  // four reads of a key block are issued together from inline assembly with
+  // their own wait: the compiler cannot tell them apart from the copies into
+  // the other buffer and would otherwise wait for those first.  The row-end
+  // wait and barrier make the buffer being read complete.
+  auto v_frags = [&](const bf16* Vr, int kb, bf16x8& f0, bf16x8& f1) {
+    const int kk = kb * 32 + 4 * g + (l16 >> 2), dd = 4 * (l16 & 3);
+    const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) bf16*)(Vr + kk * D + dd);
+    uint2 lo0, hi0, lo1, hi1;                     // dims 0-15 (keys +0, +16), dims 16-31
+    asm volatile(
+        "ds_read_b64_tr_b16 %0, %4\n"
+        "ds_read_b64_tr_b16 %1, %4 offset:1024\n"
+        "ds_read_b64_tr_b16 %2, %4 offset:32\n"
+        "ds_read_b64_tr_b16 %3, %4 offset:1056\n"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(lo0), "=&v"(hi0), "=&v"(lo1), "=&v"(hi1)
+        : "v"(a)
+        : "memory");
+    const uint32_t w0[4] = {lo0.x, lo0.y, hi0.x, hi0.y}, w1[4] = {lo1.x, lo1.y, hi1.x, hi1.y};
+    f0 = __builtin_bit_cast(bf16x8, w0);
+    f1 = __builtin_bit_cast(bf16x8, w1);
   };
 
   const int jw = j0 + 16 * wave + l16;          // this lane's query
@@ -595,8 +608,10 @@ __global__ void __launch_bounds__(512, 4) attention_pair2_kernel(PairAttnArgs p)
         for (int pp = 0; pp < 2; ++pp) {
           if (2 * pp >= ntile) break;
           const int kb = ci * 2 + pp;
-#pragma unroll
-          for (int dt = 0; dt < 2; ++dt) O[dt] = mfma16(v_frag(Vb, kb, dt), pf[pp], O[dt]);
+          bf16x8 vf0, vf1;
+          v_frags(Vb, kb, vf0, vf1);
+          O[0] = mfma16(vf0, pf[pp], O[0]);
+          O[1] = mfma16(vf1, pf[pp], O[1]);
           O[2] = mfma16(ones, pf[pp], O[2]);
         }
       }
