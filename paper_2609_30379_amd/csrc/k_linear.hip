@@ -1066,41 +1066,46 @@ __global__ void __launch_bounds__(256) swiglu_kernel(SwiArgs p) {
 // Persistent pre-normalised SwiGLU transition for K = N in {64, 128}: eight
 // waves share a pass of 256 rows (32 per wave, held as matrix-core B
 // fragments in registers), and the hidden width is walked in chunks of 32.
-// A chunk's weights (gate and up rows, and the matching 32 columns of the
-// down projection) are staged in LDS as fragment images -- 64 lanes x 16
-// bytes in the order the matrix cores consume them -- so every LDS read is
-// one conflict-free 1 KB wave read.  Chunk weights are loaded two chunks
-// ahead into registers and written to the other of two LDS buffers, one
-// barrier per chunk; the chunk sequence simply cycles, so the pipeline runs
-// on across passes.  The gated hidden goes from the first product's
-// accumulators straight into the second product (same lane layout).
+//   * LayerNorm runs in registers: the four lanes l16 + 16 g of a row hold
+//     its K values between them, so statistics are two shuffles away.
+//   * A chunk's weights -- gate and up rows, and the matching 32 columns of
+//     the down projection -- are copied straight from global memory into LDS
+//     as fragment images (global_load_lds: lane l's 16 bytes land at byte
+//     16 l, exactly the order the matrix cores consume), three buffers deep,
+//     so the copies of the next two chunks run under the current one and
+//     every LDS read is one conflict-free 1 KB wave read.
+//   * Hidden units are permuted inside a chunk: row r of the gate/up
+//     fragment ft is hidden unit 8 (r/4) + 4 ft + r%4, so a lane of k-group
+//     g ends up holding hidden units 8g .. 8g+7 of its row -- the B operand
+//     of the down projection, whose fragment then reads 16 contiguous bytes
+//     of each down-projection row.  The gated hidden never leaves registers.
 constexpr int kTrThreads = 512;
 constexpr int kTrMT = 2;                          // 16-row subtiles per wave
 constexpr int kTrRows = 8 * 16 * kTrMT;           // rows per pass
+constexpr int kTrBufs = 3;                        // chunk buffers in LDS
+constexpr int kTrMaxHidden = 2048;                // largest hidden width (bias table size)
 
 template <int K>
 constexpr int tr_chunk_frags() { return 4 * (K / 32) + K / 16; }   // gate + up + down images
 
 template <int K>
-constexpr size_t tr_smem_bytes(int F) {
-  return sizeof(bf16) * ((size_t)kTrRows * frag_stride<K>() + 2 * (size_t)tr_chunk_frags<K>() * 512) +
-         sizeof(float) * (2 * (size_t)F + K + 2 * (size_t)K);
+constexpr size_t tr_smem_bytes() {
+  return sizeof(bf16) * (size_t)kTrBufs * tr_chunk_frags<K>() * 512;
 }
 
 template <int K>
 __global__ void __launch_bounds__(kTrThreads, 1) transition_kernel(SwiArgs p) {
   constexpr int N = K, KT = K / 32, NT = N / 16;
-  constexpr int SKX = frag_stride<K>();
   constexpr int CF = tr_chunk_frags<K>();
-  constexpr int GU_PIECES = 64 * K / 8, PIECES = GU_PIECES + N * 4;
-  constexpr int PPT = (PIECES + kTrThreads - 1) / kTrThreads;
+  constexpr int DMA_PER_WAVE = CF / 8;            // images each wave copies per chunk (exact for K = 128)
   extern __shared__ __attribute__((aligned(16))) bf16 smem[];
-  bf16* Xn = smem;                                    // [kTrRows][SKX]
-  bf16* Wb0 = Xn + kTrRows * SKX;                     // chunk fragment images, two buffers
-  bf16* Wb1 = Wb0 + CF * 512;
-  float* s_b = reinterpret_cast<float*>(Wb1 + CF * 512);   // [2F] gate/up bias
-  float* s_b2 = s_b + 2 * p.F;                             // [N] down bias
-  float* s_g = s_b2 + N;                                   // [K] LayerNorm gamma, then beta
+  // The tables live in their own LDS object, which lets the compiler see
+  // that reading them does not depend on the weight copies in flight.
+  __shared__ __attribute__((aligned(16))) float s_tab[2 * kTrMaxHidden + 3 * K];
+  bf16* Wb = smem;                                    // kTrBufs x CF fragment images
+  float* s_b = s_tab;                                 // [2F] gate/up bias
+  float* s_b2 = s_b + 2 * p.F;                        // [N] down bias
+  float* s_g = s_b2 + N;                              // [K] LayerNorm gamma, then beta
   float* s_be = s_g + K;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -1115,114 +1120,97 @@ __global__ void __launch_bounds__(kTrThreads, 1) transition_kernel(SwiArgs p) {
     s_be[j] = p.beta ? p.beta[j] : 0.f;
   }
 
-  // ---- chunk weight staging: piece q of chunk f (16 global bytes each) -----
-  uint4 R0[PPT], R1[PPT];
-  auto load_chunk = [&](int f, uint4 (&R)[PPT]) {
+  // ---- chunk copies: image im of chunk f into buffer buf --------------------
+  auto dma_chunk = [&](int f, int buf) {
     const int f0 = f * 32;
+    bf16* W = Wb + buf * CF * 512;
 #pragma unroll
-    for (int j = 0; j < PPT; ++j) {
-      const int q = tid + kTrThreads * j;
-      if (q < GU_PIECES) {
-        const int r = q / (K / 8), kc = q % (K / 8);
-        const int wrow = r < 32 ? f0 + r : p.F + f0 + (r - 32);
-        R[j] = *reinterpret_cast<const uint4*>(p.w + (int64_t)wrow * K + kc * 8);
-      } else if (q < PIECES) {
-        const int q2 = q - GU_PIECES, n = q2 >> 2, pc = q2 & 3;
-        R[j] = *reinterpret_cast<const uint4*>(p.w2 + (int64_t)n * p.F + f0 + pc * 8);
+    for (int im = wave; im < CF; im += 8) {
+      const bf16* src;
+      if (im < 4 * KT) {                          // gate (im < 2 KT) or up image (ft, kk)
+        const int which = im / (2 * KT), ft = (im / KT) & 1, kk = im % KT;
+        const int hid = f0 + 8 * (l16 >> 2) + 4 * ft + (l16 & 3);
+        src = p.w + (int64_t)(which * p.F + hid) * K + kk * 32 + g * 8;
+      } else {                                    // down image a: rows 16a + l16, hidden 8g ..
+        const int a = im - 4 * KT;
+        src = p.w2 + (int64_t)(a * 16 + l16) * p.F + f0 + g * 8;
       }
-    }
-  };
-  auto store_chunk = [&](bf16* W, const uint4 (&R)[PPT]) {
-#pragma unroll
-    for (int j = 0; j < PPT; ++j) {
-      const int q = tid + kTrThreads * j;
-      if (q < GU_PIECES) {
-        const int r = q / (K / 8), kc = q % (K / 8);
-        const int which = r >> 5, rr = r & 31;                 // gate / up, row in chunk
-        const int frag = (which * 2 + (rr >> 4)) * KT + (kc >> 2);
-        const int ln = (kc & 3) * 16 + (rr & 15);
-        *reinterpret_cast<uint4*>(&W[frag * 512 + ln * 8]) = R[j];
-      } else if (q < PIECES) {
-        // down weights W2[n][f0 + 8pc + 4hf + t]: hidden h goes to k-group
-        // (h%16)/4, slot 4*(h/16) + h%4 of fragment n/16 (the order in which
-        // the gated hidden leaves the first product)
-        const int q2 = q - GU_PIECES, n = q2 >> 2, pc = q2 & 3;
-        const int frag = 4 * KT + (n >> 4), slot = (pc >> 1) * 4;
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-          const int gg = 2 * (pc & 1) + hf;
-          const uint2 v = hf ? make_uint2(R[j].z, R[j].w) : make_uint2(R[j].x, R[j].y);
-          *reinterpret_cast<uint2*>(&W[frag * 512 + (gg * 16 + (n & 15)) * 8 + slot]) = v;
-        }
-      }
+      __builtin_amdgcn_global_load_lds((const void*)src, (__attribute__((address_space(3))) void*)(W + im * 512), 16, 0, 0);
     }
   };
 
-  // prologue: chunk 0 staged, chunk 1 in registers
-  load_chunk(0, R0);
-  store_chunk(Wb0, R0);
-  load_chunk(1 % nch, R1);
+  __syncthreads();                                    // tables visible
+  dma_chunk(0, 0);
+  dma_chunk(1 % nch, 1);
 
   bf16x8 xf[kTrMT][KT];
   f32x4 accY[NT][kTrMT];
   int q = 0;                                          // global chunk step
   for (int rb = blockIdx.x; rb < nrb; rb += gridDim.x) {
-    // ---- LayerNorm of the pass's rows into Xn, then fragments into registers
-    __syncthreads();                                  // Xn free, staging and tables visible
+    // ---- LayerNorm of the pass's rows, straight into B fragments ----------
     {
-      const int r = tid >> 1, hh = tid & 1, m = rb * kTrRows + r;
-      constexpr int HALF = K / 2, NV = HALF / 8;
-      uint4 raw[NV];
+      uint4 raw[kTrMT][KT];
 #pragma unroll
-      for (int v = 0; v < NV; ++v)
-        raw[v] = m < p.rows ? *reinterpret_cast<const uint4*>(p.x + (int64_t)m * p.ldx + hh * HALF + v * 8)
-                            : make_uint4(0u, 0u, 0u, 0u);
-      float s = 0.f;
+      for (int mt = 0; mt < kTrMT; ++mt) {
+        const int m = rb * kTrRows + wave * 16 * kTrMT + mt * 16 + l16;
 #pragma unroll
-      for (int v = 0; v < NV; ++v) {
-        float t[8];
-        XStage<bf16>::unpack(raw[v], t);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) s += t[e];
+        for (int kk = 0; kk < KT; ++kk)
+          raw[mt][kk] = m < p.rows ? *reinterpret_cast<const uint4*>(p.x + (int64_t)m * p.ldx + kk * 32 + g * 8)
+                                   : make_uint4(0u, 0u, 0u, 0u);
       }
-      const float mean = (s + __shfl_xor(s, 1, 64)) / (float)K;
-      float qv = 0.f;
 #pragma unroll
-      for (int v = 0; v < NV; ++v) {
-        float t[8];
-        XStage<bf16>::unpack(raw[v], t);
+      for (int mt = 0; mt < kTrMT; ++mt) {
+        const int m = rb * kTrRows + wave * 16 * kTrMT + mt * 16 + l16;
+        float s = 0.f;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) { const float d = t[e] - mean; qv += d * d; }
-      }
-      const float rstd = rsqrtf((qv + __shfl_xor(qv, 1, 64)) / (float)K + p.eps);
+        for (int kk = 0; kk < KT; ++kk) {
+          float t[8];
+          XStage<bf16>::unpack(raw[mt][kk], t);
 #pragma unroll
-      for (int v = 0; v < NV; ++v) {
-        float t[8];
-        XStage<bf16>::unpack(raw[v], t);
-        bf16x8 o;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int k = hh * HALF + v * 8 + e;
-          o[e] = (bf16)(m < p.rows ? (t[e] - mean) * rstd * s_g[k] + s_be[k] : 0.f);
+          for (int e = 0; e < 8; ++e) s += t[e];
         }
-        *reinterpret_cast<bf16x8*>(&Xn[r * SKX + hh * HALF + v * 8]) = o;
+        s += __shfl_xor(s, 16, 64);
+        s += __shfl_xor(s, 32, 64);
+        const float mean = s / (float)K;
+        float qv = 0.f;
+#pragma unroll
+        for (int kk = 0; kk < KT; ++kk) {
+          float t[8];
+          XStage<bf16>::unpack(raw[mt][kk], t);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) { const float d = t[e] - mean; qv += d * d; }
+        }
+        qv += __shfl_xor(qv, 16, 64);
+        qv += __shfl_xor(qv, 32, 64);
+        const float rstd = rsqrtf(qv / (float)K + p.eps);
+#pragma unroll
+        for (int kk = 0; kk < KT; ++kk) {
+          float t[8];
+          XStage<bf16>::unpack(raw[mt][kk], t);
+          const int k0 = kk * 32 + g * 8;
+          const float4 g0 = *reinterpret_cast<const float4*>(&s_g[k0]), g1 = *reinterpret_cast<const float4*>(&s_g[k0 + 4]);
+          const float4 b0 = *reinterpret_cast<const float4*>(&s_be[k0]), b1 = *reinterpret_cast<const float4*>(&s_be[k0 + 4]);
+          const float gg[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+          const float bb[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+#pragma unroll
+          for (int e = 0; e < 8; ++e) xf[mt][kk][e] = (bf16)(m < p.rows ? (t[e] - mean) * rstd * gg[e] + bb[e] : 0.f);
+        }
       }
     }
-    __syncthreads();
-#pragma unroll
-    for (int mt = 0; mt < kTrMT; ++mt)
-#pragma unroll
-      for (int kk = 0; kk < KT; ++kk)
-        xf[mt][kk] = *reinterpret_cast<const bf16x8*>(&Xn[(wave * 16 * kTrMT + mt * 16 + l16) * SKX + kk * 32 + g * 8]);
 #pragma unroll
     for (int a = 0; a < NT; ++a)
 #pragma unroll
       for (int mt = 0; mt < kTrMT; ++mt) accY[a][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // the pass's first chunk has landed in every wave (on later passes this
+    // repeats the previous step's wait)
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
 
     // ---- hidden chunks ----------------------------------------------------
-    auto step = [&](uint4 (&RA)[PPT], uint4 (&RB)[PPT], const bf16* W, bf16* Wn, int f) {
-      load_chunk((f + 2) % nch, RA);                 // two chunks ahead (cyclic)
-      const int f0 = f * 32;
+    for (int c = 0; c < nch; ++c, ++q) {
+      dma_chunk((c + 2) % nch, (q + 2) % kTrBufs);   // two chunks ahead, cycling into the next pass
+      const bf16* W = Wb + (q % kTrBufs) * CF * 512;
+      const int f0 = c * 32;
       f32x4 accG[2][kTrMT], accU[2][kTrMT];
 #pragma unroll
       for (int ft = 0; ft < 2; ++ft)
@@ -1240,12 +1228,23 @@ __global__ void __launch_bounds__(kTrThreads, 1) transition_kernel(SwiArgs p) {
             accU[ft][mt] = mfma16(au, xf[mt][kk], accU[ft][mt]);
           }
         }
-      // gated hidden in the B-operand layout of the second product: slot
-      // 4*ft + i holds hidden f0 + 16 ft + 4g + i
-      const float4 bg0 = *reinterpret_cast<const float4*>(&s_b[f0 + 4 * g]);
-      const float4 bg1 = *reinterpret_cast<const float4*>(&s_b[f0 + 16 + 4 * g]);
-      const float4 bu0 = *reinterpret_cast<const float4*>(&s_b[p.F + f0 + 4 * g]);
-      const float4 bu1 = *reinterpret_cast<const float4*>(&s_b[p.F + f0 + 16 + 4 * g]);
+      // slot j = 4 ft + i of lane group g holds hidden f0 + 8g + j.  The four
+      // bias reads come from inline assembly with their own wait: the
+      // compiler would otherwise wait for the weight copies in flight first.
+      float4 bg0, bg1, bu0, bu1;
+      {
+        const uint32_t ag = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) float*)(&s_b[f0 + 8 * g]);
+        const uint32_t au = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) float*)(&s_b[p.F + f0 + 8 * g]);
+        asm volatile(
+            "ds_read_b128 %0, %4\n"
+            "ds_read_b128 %1, %4 offset:16\n"
+            "ds_read_b128 %2, %5\n"
+            "ds_read_b128 %3, %5 offset:16\n"
+            "s_waitcnt lgkmcnt(0)"
+            : "=&v"(bg0), "=&v"(bg1), "=&v"(bu0), "=&v"(bu1)
+            : "v"(ag), "v"(au)
+            : "memory");
+      }
       const float bgv[8] = {bg0.x, bg0.y, bg0.z, bg0.w, bg1.x, bg1.y, bg1.z, bg1.w};
       const float buv[8] = {bu0.x, bu0.y, bu0.z, bu0.w, bu1.x, bu1.y, bu1.z, bu1.w};
       bf16x8 hv[kTrMT];
@@ -1263,12 +1262,12 @@ __global__ void __launch_bounds__(kTrThreads, 1) transition_kernel(SwiArgs p) {
 #pragma unroll
         for (int mt = 0; mt < kTrMT; ++mt) accY[a][mt] = mfma16(ad, hv[mt], accY[a][mt]);
       }
-      store_chunk(Wn, RB);                           // chunk f + 1 into the other buffer
+      // the next chunk's images (issued a step ago) must have landed in
+      // every wave before any wave reads them; this chunk's buffer is then
+      // free for the copy issued at the next step
+      if (K == 128 && c + 1 < nch) __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8) | DMA_PER_WAVE);  // vmcnt(3)
+      else __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
-    };
-    for (int c = 0; c < nch; ++c, ++q) {
-      if (q & 1) step(R1, R0, Wb1, Wb0, c);
-      else step(R0, R1, Wb0, Wb1, c);
     }
 
     // ---- epilogue: residual + bias, lane owns channels n..n+3 of row m ----
@@ -1290,6 +1289,7 @@ __global__ void __launch_bounds__(kTrThreads, 1) transition_kernel(SwiArgs p) {
       }
     }
   }
+  __builtin_amdgcn_s_waitcnt(0);                      // no copy outstanding at exit
 }
 
 // ---------------------------------------------------------------- fp32 path
@@ -1464,8 +1464,8 @@ hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
     w.res = a.residual ? (const bf16*)a.residual : (const bf16*)a.x;
     w.ld_res = a.residual ? a.ld_residual : a.ldx;
     w.y = (bf16*)a.y; w.ldy = a.ldy;
-    const size_t tr_smem = a.c_in == 64 ? tr_smem_bytes<64>(a.hidden) : tr_smem_bytes<128>(a.hidden);
-    if ((a.c_in == 64 || a.c_in == 128) && a.c_out == a.c_in && tr_smem <= 160 * 1024) {
+    const size_t tr_smem = a.c_in == 64 ? tr_smem_bytes<64>() : tr_smem_bytes<128>();
+    if ((a.c_in == 64 || a.c_in == 128) && a.c_out == a.c_in && a.hidden <= kTrMaxHidden) {
       const int nrb = (rows + kTrRows - 1) / kTrRows;
       const int grid = std::min(nrb, compute_units());
       const size_t smem = tr_smem;
