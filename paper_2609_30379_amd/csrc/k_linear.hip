@@ -43,6 +43,7 @@ struct LinArgs {
   const int32_t* cu_pairs;    // sample tables of the streaming kernel's pair-tiled tails
   int batch;
   int wc, ntiles;             // streaming kernel: waves along the columns, 64-row tiles
+  int stage_out;              // streaming kernel: write the output tile back through LDS
 };
 
 // Position of the pair cell (a, b) of sample i in its pair-tiled operand plane:
@@ -498,13 +499,17 @@ __global__ void __launch_bounds__(256) linear_res_kernel(LinArgs p) {
 // ---------------------------------------------------------------- streaming
 // Persistent projection for K in {64, 128} and up to 512 output columns (the
 // pair path).  The product is HBM-bound, so the kernel is organised around
-// keeping loads in flight: every workgroup stays resident and walks 64-row
-// tiles; the weights of each wave's output columns live in registers for the
-// whole launch; while one tile is on the matrix cores the next tile's rows
-// (and its residual) are already loading into registers, and the normalised
-// tiles alternate between two LDS buffers, so one barrier per tile suffices.
-// The eight waves split a tile as (row groups) x (column groups): a wave owns
-// column tiles wcol + wc*t and 16-row subtiles u with u % (8/wc) == wrow.
+// keeping loads in flight and stores coalesced: every workgroup stays
+// resident and walks 64-row tiles; the weights of each wave's output columns
+// live in registers for the whole launch; while one tile is on the matrix
+// cores the next tile's rows are already loading into registers, and the
+// normalised tiles alternate between two LDS buffers.  The eight waves split
+// a tile as (row groups) x (column groups): a wave owns column tiles
+// wcol + wc*t and 16-row subtiles u with u % (8/wc) == wrow.
+// The finished tile (bias, activation; fp32 when a residual follows) is
+// staged in LDS and written back row-contiguously, 16 bytes per lane, with
+// the residual read the same way: a lane's own fragment would otherwise
+// scatter every store over 16 rows.
 constexpr int kStreamRows = 64;
 constexpr int kStreamThreads = 512;
 constexpr int kStreamMaxSamples = 1024;   // sample tables cached in LDS for pair-tiled tails
@@ -526,6 +531,9 @@ __device__ __forceinline__ int32_t tiled_pos_lds(const int32_t* cp, const int32_
   return tiled_cell_pos(pad[lo], n, a, b, transposed);
 }
 
+// LDS row stride (elements) of the staged output tile.
+__host__ __device__ constexpr int stage_stride(int n_main, bool f32) { return n_main + (f32 ? 4 : 8); }
+
 template <typename XT, int EPI, int K, int NTW>
 __global__ void __launch_bounds__(kStreamThreads, 2) linear_stream_kernel(LinArgs p) {
   constexpr int TR = kStreamRows;
@@ -535,9 +543,14 @@ __global__ void __launch_bounds__(kStreamThreads, 2) linear_stream_kernel(LinArg
   constexpr int EPT = K / TPR;                    // elements per staging thread
   constexpr int VX = Vec<XT>::N;
   constexpr int NV = EPT / VX;                    // 16-byte loads per staging thread
+  constexpr bool RES = EPI == NT_EPI_RESIDUAL;
+  constexpr int OCH = RES ? 4 : 2 * NTW;          // output 16-byte chunks per thread per tile, at most
   using XV = typename XStage<XT>::T;
   __shared__ __attribute__((aligned(16))) bf16 Xs[2][TR * SKR];
   __shared__ int32_t s_cp[kStreamMaxSamples + 1], s_len[kStreamMaxSamples], s_pad[kStreamMaxSamples];
+  __shared__ __attribute__((aligned(16))) float s_bias[32 * 16];          // bias of all output columns
+  __shared__ __attribute__((aligned(16))) float s_gamma[K], s_beta[K];     // LayerNorm affine
+  extern __shared__ __attribute__((aligned(16))) unsigned char ys_raw[];   // staged output tile
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, g = lane >> 4;
@@ -546,40 +559,53 @@ __global__ void __launch_bounds__(kStreamThreads, 2) linear_stream_kernel(LinArg
   const XT* x = static_cast<const XT*>(p.x);
   const bool tiled_tail = p.y_tail && p.tail_mode != kTailChannelMajor;
   const bool transposed = p.tail_mode == kTailPairTiledT;
-  int tile = blockIdx.x;
-  if (tile >= p.ntiles) return;
+  const bool stage = p.stage_out;                 // n_main % 8 == 0, 16-byte aligned rows
+  const int NS = stage_stride(p.n_main, RES);
+  const int c8n = p.n_main / 8;                   // 16-byte chunks per output row
+  const int G = (int)gridDim.x;
+  if ((int)blockIdx.x >= p.ntiles) return;
+  auto ysf = [&](int) { return reinterpret_cast<float*>(ys_raw); };
+  auto ysb = [&](int) { return reinterpret_cast<bf16*>(ys_raw); };
+  auto tile_of = [&](int i) { return (int)blockIdx.x + i * G; };
 
-  // ---- staging: thread owns EPT consecutive k of one row of the tile -----
+  // ---- input rows: a ring of PF register slots, loads issued PF tiles ahead
+  constexpr int PF = NTW == 2 ? 3 : 1;
   const int srow = tid / TPR, spart = tid % TPR;
-  XV xr[NV];
-  auto load_x = [&](int t) {
-    const int m = t * TR + srow;
+  const XT* xthread = x + (int64_t)srow * p.ldx + spart * EPT;   // row srow of tile 0
+  const int64_t xtile = (int64_t)TR * p.ldx;
+  XV xr[PF][NV];
+  auto load_x = [&](int t, XV (&dst)[NV]) {
+    const bool ok = t < p.ntiles && t * TR + srow < p.rows;
+    const XT* src = xthread + t * xtile;
 #pragma unroll
-    for (int v = 0; v < NV; ++v)
-      xr[v] = m < p.rows ? *reinterpret_cast<const XV*>(x + (int64_t)m * p.ldx + spart * EPT + v * VX)
-                         : XStage<XT>::zero();
+    for (int v = 0; v < NV; ++v) dst[v] = ok ? *reinterpret_cast<const XV*>(src + v * VX) : XStage<XT>::zero();
   };
-  // residual of the wave's own output fragments, prefetched with the rows
-  uint2 rq_next[4][NTW], rq[4][NTW];
+  // write-back chunks of this thread: (row, 8 columns), fixed for every tile
+  int wb_row[OCH], wb_col[OCH];
+#pragma unroll
+  for (int c = 0; c < OCH; ++c) {
+    const int ch = tid + kStreamThreads * c;
+    wb_row[c] = (stage && ch < TR * c8n) ? ch / c8n : TR;       // TR: no chunk
+    wb_col[c] = (stage && ch < TR * c8n) ? (ch % c8n) * 8 : 0;
+  }
+  // residual chunks of the staged write-back, loaded a tile ahead of it
+  uint4 rres[RES ? OCH : 1];
   auto load_res = [&](int t) {
-    if constexpr (EPI == NT_EPI_RESIDUAL) {
+    if constexpr (RES) {
+      const bf16* rtile = p.res + (int64_t)t * TR * p.ld_res;
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int j = 0; j < NTW; ++j) {
-          const int m = t * TR + u * 16 + l16, n = (wcol + wc * j) * 16 + 4 * g;
-          rq_next[u][j] = (u % wr_n == wrow && m < p.rows && n + 4 <= p.n_main)
-                              ? *reinterpret_cast<const uint2*>(p.res + (int64_t)m * p.ld_res + n)
-                              : make_uint2(0u, 0u);
-        }
+      for (int c = 0; c < OCH; ++c) {
+        const bool ok = stage && t < p.ntiles && wb_row[c] < TR && t * TR + wb_row[c] < p.rows;
+        rres[c] = ok ? *reinterpret_cast<const uint4*>(rtile + wb_row[c] * p.ld_res + wb_col[c]) : make_uint4(0u, 0u, 0u, 0u);
+      }
     }
   };
-  load_x(tile);
-  load_res(tile);
+#pragma unroll
+  for (int d = 0; d < PF; ++d) load_x(tile_of(d), xr[d]);
+  load_res(tile_of(0));
 
-  // ---- resident weights and bias of the wave's column tiles ---------------
+  // ---- resident weights of the wave's column tiles; bias and affine in LDS
   bf16x8 wf[NTW][KT];
-  float bv[NTW][4];
 #pragma unroll
   for (int j = 0; j < NTW; ++j) {
     const int ct = wcol + wc * j, n = ct * 16 + l16;
@@ -588,11 +614,11 @@ __global__ void __launch_bounds__(kStreamThreads, 2) linear_stream_kernel(LinArg
       if (ct < nt16 && n < p.N) wf[j][kk] = *reinterpret_cast<const bf16x8*>(p.w + (int64_t)n * K + kk * 32 + g * 8);
       else wf[j][kk] = bf16x8{};
     }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int nb = ct * 16 + 4 * g + i;
-      bv[j][i] = (p.bias && nb < p.N) ? p.bias[nb] : 0.f;
-    }
+  }
+  for (int j = tid; j < 32 * 16; j += kStreamThreads) s_bias[j] = (p.bias && j < p.N) ? p.bias[j] : 0.f;
+  for (int j = tid; j < K; j += kStreamThreads) {
+    s_gamma[j] = p.gamma ? p.gamma[j] : 1.f;
+    s_beta[j] = p.beta ? p.beta[j] : 0.f;
   }
   if (tiled_tail) {
     for (int j = tid; j <= p.batch; j += kStreamThreads) s_cp[j] = p.cu_pairs[j];
@@ -601,57 +627,49 @@ __global__ void __launch_bounds__(kStreamThreads, 2) linear_stream_kernel(LinArg
       s_pad[j] = p.cu_pad[j];
     }
   }
+  __syncthreads();                                // tables visible before the first tile
 
-  for (int it = 0; tile < p.ntiles; ++it) {
-    const int next = tile + (int)gridDim.x;
-    bf16* xs = Xs[it & 1];
-    // ---- LayerNorm of the staged rows into this tile's LDS buffer ---------
-    {
-      float v[EPT];
+  // ---- stage 1: LayerNorm of tile i's rows into Xs[i & 1] ------------------
+  auto ln_stage = [&](int i, XV (&cur)[NV]) {
+    const int tile = tile_of(i);
+    bf16* xs = Xs[i & 1];
+    float v[EPT];
 #pragma unroll
-      for (int vv = 0; vv < NV; ++vv) XStage<XT>::unpack(xr[vv], v + vv * VX);
-      const bool valid = tile * TR + srow < p.rows;
-      if (p.gamma) {
-        float s = 0.f;
+    for (int vv = 0; vv < NV; ++vv) XStage<XT>::unpack(cur[vv], v + vv * VX);
+    const bool valid = tile * TR + srow < p.rows;
+    if (p.gamma) {
+      float s = 0.f;
 #pragma unroll
-        for (int e = 0; e < EPT; ++e) s += v[e];
-        const float mean = group_sum<TPR>(s) / (float)K;
-        float q = 0.f;
+      for (int e = 0; e < EPT; ++e) s += v[e];
+      const float mean = group_sum<TPR>(s) / (float)K;
+      float q = 0.f;
 #pragma unroll
-        for (int e = 0; e < EPT; ++e) { const float d = v[e] - mean; q += d * d; }
-        const float rstd = valid ? rsqrtf(group_sum<TPR>(q) / (float)K + p.eps) : 0.f;
+      for (int e = 0; e < EPT; ++e) { const float d = v[e] - mean; q += d * d; }
+      const float rstd = valid ? rsqrtf(group_sum<TPR>(q) / (float)K + p.eps) : 0.f;
 #pragma unroll
-        for (int e = 0; e < EPT; e += 4) {
-          const float4 ga = *reinterpret_cast<const float4*>(p.gamma + spart * EPT + e);
-          const float4 be = p.beta ? *reinterpret_cast<const float4*>(p.beta + spart * EPT + e)
-                                   : make_float4(0.f, 0.f, 0.f, 0.f);
-          v[e] = valid ? (v[e] - mean) * rstd * ga.x + be.x : 0.f;
-          v[e + 1] = valid ? (v[e + 1] - mean) * rstd * ga.y + be.y : 0.f;
-          v[e + 2] = valid ? (v[e + 2] - mean) * rstd * ga.z + be.z : 0.f;
-          v[e + 3] = valid ? (v[e + 3] - mean) * rstd * ga.w + be.w : 0.f;
-        }
-      }
-#pragma unroll
-      for (int e = 0; e < EPT; e += 8) {
-        bf16x8 o;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) o[j] = (bf16)v[e + j];
-        *reinterpret_cast<bf16x8*>(&xs[srow * SKR + spart * EPT + e]) = o;
+      for (int e = 0; e < EPT; e += 4) {
+        const float4 ga = *reinterpret_cast<const float4*>(&s_gamma[spart * EPT + e]);
+        const float4 be = *reinterpret_cast<const float4*>(&s_beta[spart * EPT + e]);
+        v[e] = valid ? (v[e] - mean) * rstd * ga.x + be.x : 0.f;
+        v[e + 1] = valid ? (v[e + 1] - mean) * rstd * ga.y + be.y : 0.f;
+        v[e + 2] = valid ? (v[e + 2] - mean) * rstd * ga.z + be.z : 0.f;
+        v[e + 3] = valid ? (v[e + 3] - mean) * rstd * ga.w + be.w : 0.f;
       }
     }
-    if constexpr (EPI == NT_EPI_RESIDUAL) {
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+    for (int e = 0; e < EPT; e += 8) {
+      bf16x8 o;
 #pragma unroll
-        for (int j = 0; j < NTW; ++j) rq[u][j] = rq_next[u][j];
+      for (int j = 0; j < 8; ++j) o[j] = (bf16)v[e + j];
+      *reinterpret_cast<bf16x8*>(&xs[srow * SKR + spart * EPT + e]) = o;
     }
-    if (next < p.ntiles) {
-      load_x(next);
-      load_res(next);
-    }
-    __syncthreads();
+    load_x(tile_of(i + PF), cur);                 // the slot is free again
+  };
 
-    // ---- the wave's subtiles: resident weights x staged rows ---------------
+  // ---- stage 2: the wave's subtiles of tile i into Ys[i & 1] ---------------
+  auto compute_stage = [&](int i) {
+    const int tile = tile_of(i);
+    const bf16* xs = Xs[i & 1];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       if (u % wr_n != wrow) continue;
@@ -667,7 +685,7 @@ __global__ void __launch_bounds__(kStreamThreads, 2) linear_stream_kernel(LinArg
           for (int kk = 0; kk < KT; ++kk) acc[j] = mfma16(wf[j][kk], xf[kk], acc[j]);
         }
       }
-      const int m = tile * TR + u * 16 + l16;
+      const int rl = u * 16 + l16, m = tile * TR + rl;
       if (m >= p.rows) continue;
       int32_t tpos = m;
       if (tiled_tail) tpos = tiled_pos_lds(s_cp, s_len, s_pad, p.batch, m, transposed);
@@ -675,38 +693,91 @@ __global__ void __launch_bounds__(kStreamThreads, 2) linear_stream_kernel(LinArg
       for (int j = 0; j < NTW; ++j) {
         const int n = (wcol + wc * j) * 16 + 4 * g;
         if (n >= p.N) continue;
-        float r[4];
+        const float4 bq = *reinterpret_cast<const float4*>(&s_bias[n]);
+        float r[4] = {acc[j][0] + bq.x, acc[j][1] + bq.y, acc[j][2] + bq.z, acc[j][3] + bq.w};
+        if constexpr (EPI == NT_EPI_GELU) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          r[i] = acc[j][i] + bv[j][i];
-          if constexpr (EPI == NT_EPI_GELU) r[i] = gelu_erf(r[i]);
+          for (int ii = 0; ii < 4; ++ii) r[ii] = gelu_erf(r[ii]);
         }
-        if (n + 4 <= p.n_main) {
-          if constexpr (EPI == NT_EPI_RESIDUAL) {
-            r[0] += __uint_as_float(rq[u][j].x << 16); r[1] += __uint_as_float(rq[u][j].x & 0xffff0000u);
-            r[2] += __uint_as_float(rq[u][j].y << 16); r[3] += __uint_as_float(rq[u][j].y & 0xffff0000u);
+        if (stage && n + 4 <= p.n_main) {
+          if constexpr (RES) *reinterpret_cast<float4*>(&ysf(i & 1)[rl * NS + n]) = make_float4(r[0], r[1], r[2], r[3]);
+          else {
+            bf16x4 o;
+#pragma unroll
+            for (int ii = 0; ii < 4; ++ii) o[ii] = (bf16)r[ii];
+            *reinterpret_cast<bf16x4*>(&ysb(i & 1)[rl * NS + n]) = o;
+          }
+        } else if (n + 4 <= p.n_main) {
+          if constexpr (RES) {
+            const uint2 q2 = *reinterpret_cast<const uint2*>(p.res + (int64_t)m * p.ld_res + n);
+            r[0] += __uint_as_float(q2.x << 16); r[1] += __uint_as_float(q2.x & 0xffff0000u);
+            r[2] += __uint_as_float(q2.y << 16); r[3] += __uint_as_float(q2.y & 0xffff0000u);
           }
           bf16x4 o;
 #pragma unroll
-          for (int i = 0; i < 4; ++i) o[i] = (bf16)r[i];
+          for (int ii = 0; ii < 4; ++ii) o[ii] = (bf16)r[ii];
           *reinterpret_cast<bf16x4*>(p.y + (int64_t)m * p.ldy + n) = o;
         } else {
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int nn = n + i;
+          for (int ii = 0; ii < 4; ++ii) {
+            const int nn = n + ii;
             if (nn >= p.N) break;
             if (nn < p.n_main) {
-              float val = r[i];
-              if constexpr (EPI == NT_EPI_RESIDUAL) val += (float)p.res[(int64_t)m * p.ld_res + nn];
+              float val = r[ii];
+              if constexpr (RES) val += (float)p.res[(int64_t)m * p.ld_res + nn];
               p.y[(int64_t)m * p.ldy + nn] = (bf16)val;
             } else {
-              p.y_tail[(int64_t)(nn - p.n_main) * p.ld_tail + tpos] = (bf16)r[i];
+              p.y_tail[(int64_t)(nn - p.n_main) * p.ld_tail + tpos] = (bf16)r[ii];
             }
           }
         }
       }
     }
-    tile = next;
+  };
+
+  // ---- stage 3: staged write-back of tile i, 16 contiguous bytes per lane --
+  auto wb_stage = [&](int i) {
+    const int tile = tile_of(i);
+    bf16* ytile = p.y + (int64_t)tile * TR * p.ldy;
+#pragma unroll
+    for (int c = 0; c < OCH; ++c) {
+      const int row = wb_row[c], col = wb_col[c];
+      if (row >= TR || tile * TR + row >= p.rows) continue;
+      bf16x8 o;
+      if constexpr (RES) {
+        const float* ys = ysf(i & 1);
+        const float4 a0 = *reinterpret_cast<const float4*>(&ys[row * NS + col]);
+        const float4 a1 = *reinterpret_cast<const float4*>(&ys[row * NS + col + 4]);
+        const float av[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+        float rv[8];
+        XStage<bf16>::unpack(rres[c], rv);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] = (bf16)(av[e] + rv[e]);
+      } else {
+        o = *reinterpret_cast<const bf16x8*>(&ysb(i & 1)[row * NS + col]);
+      }
+      *reinterpret_cast<bf16x8*>(ytile + row * p.ldy + col) = o;
+    }
+    load_res(tile_of(i + 1));
+  };
+
+  // ---- per tile: normalise (and prefetch) | barrier | matrix cores into the
+  // staged tile | barrier | coalesced write-back
+  int n_my = 0;
+  while (tile_of(n_my) < p.ntiles) ++n_my;
+  auto body = [&](int i, XV (&cur)[NV]) {
+    ln_stage(i, cur);
+    __syncthreads();
+    compute_stage(i);
+    if (stage) {
+      __syncthreads();
+      wb_stage(i);
+    }
+  };
+  for (int i = 0; i < n_my;) {
+    body(i++, xr[0]);
+    if constexpr (PF > 1) { if (i < n_my) body(i++, xr[1]); }
+    if constexpr (PF > 2) { if (i < n_my) body(i++, xr[2]); }
   }
 }
 
@@ -733,6 +804,7 @@ __global__ void __launch_bounds__(kStreamThreads, 1) linear_tiled_kernel(LinArgs
   constexpr int NV = EPT / 8;
   __shared__ __attribute__((aligned(16))) bf16 Xs[2][TR * SKR];
   __shared__ int32_t s_pad[kStreamMaxSamples + 1], s_cp[kStreamMaxSamples], s_len[kStreamMaxSamples];
+  __shared__ __attribute__((aligned(16))) float s_gamma[K], s_beta[K];     // LayerNorm affine
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, g = lane >> 4;
@@ -745,6 +817,10 @@ __global__ void __launch_bounds__(kStreamThreads, 1) linear_tiled_kernel(LinArgs
   for (int j = tid; j < p.batch; j += kStreamThreads) {
     s_cp[j] = p.cu_pairs[j];
     s_len[j] = p.cu_seqlens[j + 1] - p.cu_seqlens[j];
+  }
+  for (int j = tid; j < K; j += kStreamThreads) {
+    s_gamma[j] = p.gamma ? p.gamma[j] : 1.f;
+    s_beta[j] = p.beta ? p.beta[j] : 0.f;
   }
   __syncthreads();
 
@@ -810,9 +886,8 @@ __global__ void __launch_bounds__(kStreamThreads, 1) linear_tiled_kernel(LinArgs
         const float rstd = rsqrtf(group_sum<TPR>(q) / (float)K + p.eps);
 #pragma unroll
         for (int e = 0; e < EPT; e += 4) {
-          const float4 ga = *reinterpret_cast<const float4*>(p.gamma + spart * EPT + e);
-          const float4 be = p.beta ? *reinterpret_cast<const float4*>(p.beta + spart * EPT + e)
-                                   : make_float4(0.f, 0.f, 0.f, 0.f);
+          const float4 ga = *reinterpret_cast<const float4*>(&s_gamma[spart * EPT + e]);
+          const float4 be = *reinterpret_cast<const float4*>(&s_beta[spart * EPT + e]);
           v[e] = (v[e] - mean) * rstd * ga.x + be.x;
           v[e + 1] = (v[e + 1] - mean) * rstd * ga.y + be.y;
           v[e + 2] = (v[e + 2] - mean) * rstd * ga.z + be.z;
@@ -1396,16 +1471,15 @@ int compute_units() {
 // CU x CUs); every workgroup walks tiles blockIdx.x + j * gridDim.x.
 template <typename XT, int EPI, int K, int NTW>
 void launch_stream(const LinArgs& p, hipStream_t s) {
-  static int per_cu = 0;
-  if (per_cu == 0) {
-    int nb = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, linear_stream_kernel<XT, EPI, K, NTW>, kStreamThreads, 0) !=
-            hipSuccess || nb < 1)
-      nb = 1;
-    per_cu = nb;
-  }
-  const int grid = std::min(p.ntiles, per_cu * compute_units());
-  linear_stream_kernel<XT, EPI, K, NTW><<<dim3((unsigned)grid), dim3(kStreamThreads), 0, s>>>(p);
+  const size_t smem = p.stage_out ? (size_t)kStreamRows * stage_stride(p.n_main, EPI == NT_EPI_RESIDUAL) *
+                                        (EPI == NT_EPI_RESIDUAL ? 4 : 2)
+                                  : 0;
+  auto kern = linear_stream_kernel<XT, EPI, K, NTW>;
+  (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+  int nb = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kern, kStreamThreads, smem) != hipSuccess || nb < 1) nb = 1;
+  const int grid = std::min(p.ntiles, nb * compute_units());
+  kern<<<dim3((unsigned)grid), dim3(kStreamThreads), smem, s>>>(p);
 }
 
 template <int K>
@@ -1515,6 +1589,11 @@ hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
     while (wc < 8 && wc * ntw < nt16) wc *= 2;
     p.wc = wc;
     p.ntiles = (rows + kStreamRows - 1) / kStreamRows;
+    // staged write-back: whole 16-byte chunks per row, within the LDS budget
+    const bool res = a.epilogue == NT_EPI_RESIDUAL;
+    const size_t stage_bytes = (size_t)kStreamRows * stage_stride(p.n_main, res) * (res ? 4 : 2);
+    p.stage_out = p.n_main > 0 && p.n_main % 8 == 0 && p.ldy % 8 == 0 && (!res || a.ld_residual % 8 == 0) &&
+                  p.n_main <= (res ? 256 : 32 * ntw * 8) && stage_bytes <= 108 * 1024;
 #define NT_ST(XT, EPI, KK, W) launch_stream<XT, EPI, KK, W>(p, s)
 #define NT_ST_W(XT, EPI, KK) do { if (ntw == 2) NT_ST(XT, EPI, KK, 2); else NT_ST(XT, EPI, KK, 4); } while (0)
 #define NT_ST_K(XT, EPI) do { if (a.c_in == 64) NT_ST_W(XT, EPI, 64); else NT_ST_W(XT, EPI, 128); } while (0)
