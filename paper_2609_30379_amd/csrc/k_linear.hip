@@ -15,6 +15,7 @@ namespace nt {
 namespace {
 
 constexpr int BM = 128, BN = 128, BK = 32;
+constexpr int kSmallRows = 8192;    // row counts taken by the one-wave-per-block kernel
 constexpr int SK = BK + 8;          // LDS row stride (bf16): 80 bytes, keeps b128 reads spread
 
 struct LinArgs {
@@ -492,6 +493,83 @@ __global__ void __launch_bounds__(256) linear_res_kernel(LinArgs p) {
       __syncthreads();
       store_w();
       __syncthreads();
+    }
+  }
+}
+
+// ---------------------------------------------------------------- small row counts
+// Projections over few rows (the single track: one row per token) are pure
+// latency: a handful of large tiles would each walk the whole K loop alone.
+// Here one wave owns a 16-row x 64-column output block, so hundreds of waves
+// run at once, and the next k-step's fragments load while the current step is
+// on the matrix cores.  No LayerNorm and no tail columns (those take the
+// other paths).
+template <typename XT, int EPI>
+__global__ void __launch_bounds__(64) linear_small_kernel(LinArgs p) {
+  const int lane = threadIdx.x, l16 = lane & 15, g = lane >> 4;
+  const int m0 = blockIdx.x * 16, n0 = blockIdx.y * 64;
+  const XT* x = static_cast<const XT*>(p.x);
+  const int m = m0 + l16;
+  const bool mrow = m < p.rows;
+  auto load_step = [&](int k0, bf16x8 (&wa)[4], bf16x8& xb) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int n = n0 + t * 16 + l16;
+      wa[t] = n < p.N ? *reinterpret_cast<const bf16x8*>(p.w + (int64_t)n * p.K + k0 + g * 8) : bf16x8{};
+    }
+    if constexpr (Vec<XT>::N == 8) {
+      xb = mrow ? *reinterpret_cast<const bf16x8*>(x + (int64_t)m * p.ldx + k0 + g * 8) : bf16x8{};
+    } else {
+      float4 a = make_float4(0.f, 0.f, 0.f, 0.f), b = a;
+      if (mrow) {
+        a = *reinterpret_cast<const float4*>(x + (int64_t)m * p.ldx + k0 + g * 8);
+        b = *reinterpret_cast<const float4*>(x + (int64_t)m * p.ldx + k0 + g * 8 + 4);
+      }
+      xb = bf16x8{(bf16)a.x, (bf16)a.y, (bf16)a.z, (bf16)a.w, (bf16)b.x, (bf16)b.y, (bf16)b.z, (bf16)b.w};
+    }
+  };
+  f32x4 acc[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  bf16x8 wa[4], xb, wn[4], xn;
+  load_step(0, wa, xb);
+  for (int k0 = 0; k0 < p.K; k0 += 32) {
+    if (k0 + 32 < p.K) load_step(k0 + 32, wn, xn);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc[t] = mfma16(wa[t], xb, acc[t]);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) wa[t] = wn[t];
+    xb = xn;
+  }
+  if (!mrow) return;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int n = n0 + t * 16 + 4 * g;            // lane owns channels n..n+3 of row m
+    if (n >= p.N) continue;
+    float r[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      r[i] = acc[t][i] + ((p.bias && n + i < p.N) ? p.bias[n + i] : 0.f);
+      if constexpr (EPI == NT_EPI_GELU) r[i] = gelu_erf(r[i]);
+    }
+    if (n + 4 <= p.N) {
+      if constexpr (EPI == NT_EPI_RESIDUAL) {
+        const uint2 q2 = *reinterpret_cast<const uint2*>(p.res + (int64_t)m * p.ld_res + n);
+        r[0] += __uint_as_float(q2.x << 16); r[1] += __uint_as_float(q2.x & 0xffff0000u);
+        r[2] += __uint_as_float(q2.y << 16); r[3] += __uint_as_float(q2.y & 0xffff0000u);
+      }
+      bf16x4 o;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) o[i] = (bf16)r[i];
+      *reinterpret_cast<bf16x4*>(p.y + (int64_t)m * p.ldy + n) = o;
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (n + i >= p.N) break;
+        float v = r[i];
+        if constexpr (EPI == NT_EPI_RESIDUAL) v += (float)p.res[(int64_t)m * p.ld_res + n + i];
+        p.y[(int64_t)m * p.ldy + n + i] = (bf16)v;
+      }
     }
   }
 }
@@ -1571,6 +1649,20 @@ hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
   const bool xf = a.x_dtype == NT_F32;
 
   const bool tiled = p.y_tail && p.tail_mode != kTailChannelMajor;
+  if (!a.ln_gamma && a.n_tail == 0 && a.c_in % 32 == 0 && rows <= kSmallRows) {
+    const dim3 g1((unsigned)((rows + 15) / 16), (unsigned)((a.c_out + 63) / 64)), b1(64);
+#define NT_SM(XT, EPI) linear_small_kernel<XT, EPI><<<g1, b1, 0, s>>>(p)
+#define NT_SM_X(EPI) do { if (xf) NT_SM(float, EPI); else NT_SM(bf16, EPI); } while (0)
+    switch (a.epilogue) {
+      case NT_EPI_NONE: NT_SM_X(NT_EPI_NONE); break;
+      case NT_EPI_RESIDUAL: NT_SM_X(NT_EPI_RESIDUAL); break;
+      case NT_EPI_GELU: NT_SM_X(NT_EPI_GELU); break;
+      default: return hipErrorInvalidValue;
+    }
+#undef NT_SM_X
+#undef NT_SM
+    return hipGetLastError();
+  }
   if (tiled && p.n_main == 0 && !xf && a.epilogue == NT_EPI_NONE && (a.c_in == 64 || a.c_in == 128) &&
       a.c_out <= 256 && plan.layout && plan.layout->batch <= kStreamMaxSamples) {
     p.cu_pairs = plan.layout->d_cu_pairs;
