@@ -434,7 +434,7 @@ __global__ void __launch_bounds__(512, 4) attention_pair2_kernel(PairAttnArgs p)
   const int4 w4 = reinterpret_cast<const int4*>(p.work)[pos];
   const int i = w4.x;
   if (i < 0) return;
-  const int jb = w4.y, rg = w4.z;
+  const int qt0 = w4.y, rg = w4.z, nqt = w4.w;       // first 16-query tile, row group, tile count
   const int n = p.cu_seqlens[i + 1] - p.cu_seqlens[i];
   const int npad = (n + 63) & ~63;
   const int64_t cu = p.cu_pairs[i];
@@ -446,7 +446,7 @@ __global__ void __launch_bounds__(512, 4) attention_pair2_kernel(PairAttnArgs p)
   bf16* Vb1 = Vb0 + NMAX * D;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, g = lane >> 4;
-  const int j0 = jb * kAttnQB2;
+  const int j0 = qt0 * 16;
 
   // ---- bias slice / scale: Bs[q][k] = bias(j0 + q, k) / scale, 0 past N --
   {
@@ -484,9 +484,14 @@ __global__ void __launch_bounds__(512, 4) attention_pair2_kernel(PairAttnArgs p)
 #pragma unroll
     for (int kt = wave; kt < KT16; kt += 8) {
       if (kt * 16 >= npad) break;
-      const int key_k = min(kt * 16 + l16, n - 1), key_v = min(kt * 16 + (lane >> 2), n - 1);
+      // values: the 16-byte chunk at column c of key row kv holds dim group
+      // c ^ ((kv >> 2) & 3), so the four key groups of a transpose read fall
+      // on different banks
+      const int kv = kt * 16 + (lane >> 2);
+      const int key_k = min(kt * 16 + l16, n - 1), key_v = min(kv, n - 1);
+      const int dgv = (lane & 3) ^ ((kv >> 2) & 3);
       const bf16* sk = p.k + (cu + (int64_t)r * sr + (int64_t)key_k * st) * p.ld_qkv + h * D + g * 8;
-      const bf16* sv = p.v + (cu + (int64_t)r * sr + (int64_t)key_v * st) * p.ld_qkv + h * D + (lane & 3) * 8;
+      const bf16* sv = p.v + (cu + (int64_t)r * sr + (int64_t)key_v * st) * p.ld_qkv + h * D + dgv * 8;
       __builtin_amdgcn_global_load_lds((const void*)sk, (__attribute__((address_space(3))) void*)(Kb + kt * 512), 16, 0, 0);
       __builtin_amdgcn_global_load_lds((const void*)sv, (__attribute__((address_space(3))) void*)(Vr + kt * 512), 16, 0, 0);
     }
@@ -501,17 +506,21 @@ __global__ void __launch_bounds__(512, 4) attention_pair2_kernel(PairAttnArgs p)
   // the other buffer and would otherwise wait for those first.  The row-end
   // wait and barrier make the buffer being read complete.
   auto v_frags = [&](const bf16* Vr, int kb, bf16x8& f0, bf16x8& f1) {
-    const int kk = kb * 32 + 4 * g + (l16 >> 2), dd = 4 * (l16 & 3);
-    const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) bf16*)(Vr + kk * D + dd);
+    // key kk and kk + 16 share (kk >> 2) & 3 = g, hence the same swizzle
+    const int kk = kb * 32 + 4 * g + (l16 >> 2), q = l16 & 3;
+    const int off0 = ((q >> 1) ^ g) * 8 + (q & 1) * 4;         // dims 4q .. 4q+3 (dim group q/2)
+    const int off1 = (((q >> 1) + 2) ^ g) * 8 + (q & 1) * 4;   // dims 16 + 4q ..
+    const uint32_t a0 = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) bf16*)(Vr + kk * D + off0);
+    const uint32_t a1 = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) bf16*)(Vr + kk * D + off1);
     uint2 lo0, hi0, lo1, hi1;                     // dims 0-15 (keys +0, +16), dims 16-31
     asm volatile(
         "ds_read_b64_tr_b16 %0, %4\n"
         "ds_read_b64_tr_b16 %1, %4 offset:1024\n"
-        "ds_read_b64_tr_b16 %2, %4 offset:32\n"
-        "ds_read_b64_tr_b16 %3, %4 offset:1056\n"
+        "ds_read_b64_tr_b16 %2, %5\n"
+        "ds_read_b64_tr_b16 %3, %5 offset:1024\n"
         "s_waitcnt lgkmcnt(0)"
         : "=&v"(lo0), "=&v"(hi0), "=&v"(lo1), "=&v"(hi1)
-        : "v"(a)
+        : "v"(a0), "v"(a1)
         : "memory");
     const uint32_t w0[4] = {lo0.x, lo0.y, hi0.x, hi0.y}, w1[4] = {lo1.x, lo1.y, hi1.x, hi1.y};
     f0 = __builtin_bit_cast(bf16x8, w0);
@@ -519,7 +528,7 @@ __global__ void __launch_bounds__(512, 4) attention_pair2_kernel(PairAttnArgs p)
   };
 
   const int jw = j0 + 16 * wave + l16;          // this lane's query
-  const bool wave_has_queries = j0 + 16 * wave < n;
+  const bool wave_has_queries = wave < nqt && j0 + 16 * wave < n;
   const bool qvalid = jw < n;
   const int r0 = rg * kAttnRG2, r1 = min(n, r0 + kAttnRG2);
   bf16x8 qf = qvalid ? *reinterpret_cast<const bf16x8*>(p.q + (cu + (int64_t)r0 * sr + (int64_t)jw * st) * p.ld_qkv + h * D + g * 8)
@@ -590,12 +599,17 @@ __global__ void __launch_bounds__(512, 4) attention_pair2_kernel(PairAttnArgs p)
         }
         mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
         mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-        const float m_new = fmaxf(m_s, mloc);
-        const float alpha = __builtin_amdgcn_exp2f((m_s - m_new) * c);
-        m_s = m_new;
+        // the reference max moves only when some query's max grew by more
+        // than 8 (log2 units): probabilities then stay below 2^8, and most
+        // chunks skip rescaling the accumulators
+        if (__any((mloc - m_s) * c > 8.f)) {
+          const float m_new = fmaxf(m_s, mloc);
+          const float alpha = __builtin_amdgcn_exp2f((m_s - m_new) * c);
+          m_s = m_new;
 #pragma unroll
-        for (int u = 0; u < 3; ++u) O[u] *= alpha;
-        const float nm = -m_new * c;
+          for (int u = 0; u < 3; ++u) O[u] *= alpha;
+        }
+        const float nm = -m_s * c;
         bf16x8 pf[2];
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt) {
