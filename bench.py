@@ -98,6 +98,23 @@ def op_costs(w, L):
     return c
 
 
+def token_op_costs(w, L):
+    """Algorithmic HBM bytes and flops per launch of the token-path ops (one
+    pre-LN encoder layer on packed tokens and the per-sample mean pool)."""
+    T = sum(L)
+    S2 = sum(n * n for n in L)
+    c, F = w.c_s, w.hidden
+    e = 2 if w.dtype == "bf16" else 4
+    return {
+        "qkv_proj": (T * (c + 3 * c) * e, 2 * T * c * 3 * c),
+        "attention_1d": (T * 4 * c * e, 4 * c * S2),
+        "out_proj_residual": (T * 3 * c * e, 2 * T * c * c),
+        "ffn_up_gelu": (T * (c + F) * e, 2 * T * c * F),
+        "ffn_down_residual": (T * (F + 2 * c) * e, 2 * T * F * c),
+        "sample_mean": (T * c * e + len(L) * c * 4, T * c),
+    }
+
+
 def roofline_for(name, bytes_, flops, us, dtype):
     """Bound = whichever of HBM time and matrix-core time is longer."""
     peak_f = BF16_PEAK_TFLOPS if dtype == "bf16" else F32_PEAK_TFLOPS
@@ -110,6 +127,32 @@ def roofline_for(name, bytes_, flops, us, dtype):
     ach = bytes_ / (us * 1e-6) / 1e9
     return {"kernel": name, "bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None}
+
+
+def cpu_baseline_tokens(w, run, min_s: float = 10.0):
+    """The CPU oracle on the token path: one encoder layer over samples taken
+    smallest first until at least min_s seconds of work; tokens per second."""
+    import numpy as np
+    from oracle import blocks as OB
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    eta = np.concatenate([[0], np.cumsum(run.lengths)])
+    done, tokens, dt = [], 0, 0.0
+    for i in np.argsort(run.lengths, kind="stable"):
+        n = int(run.lengths[i])
+        t0 = time.perf_counter()
+        OB.encoder_layer(run.x_init[eta[i]:eta[i] + n], [n], run.params, w.heads, w.head_dim, dtype=w.dtype)
+        dt += time.perf_counter() - t0
+        done.append(f"{int(i)} (N={n})")
+        tokens += n
+        if dt >= min_s:
+            break
+    return {"value": round(tokens / dt, 1), "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"samples {', '.join(done[:8])}{' ...' if len(done) > 8 else ''} of the batch ({tokens} tokens), "
+                      f"one encoder layer each in float64 NumPy, {dt:.1f} s; host has {os.cpu_count()} CPUs"}
 
 
 def cpu_baseline(w, run, min_s: float = 10.0):
@@ -150,7 +193,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="pair_b8_n208_224_bf16")
+    ap.add_argument("--workload", default="pair_b8_n208_224_bf16",
+                    help="default: the B=8 near-uniform pair block; the other workloads are parity cases, "
+                         "timed here on request")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernels", action="store_true", help="also print the per-op breakdown to stderr")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -174,10 +219,9 @@ def main():
     from paper_2609_30379_amd import binding, blocks, synth
     binding.load()
     w = synth.WORKLOADS[args.workload]
-    if w.kind != "pair":
-        raise SystemExit("bench.py times the pair workloads")
     torch.cuda.set_device(0)
-    run = blocks.PairRun(w)
+    tokens = w.kind != "pair"
+    run = blocks.TokenRun(w) if tokens else blocks.PairRun(w)
     L = run.lengths
     R = sum(n * n for n in L)
 
@@ -202,7 +246,7 @@ def main():
     ms_dev = ev0.elapsed_time(ev1) / args.steps
     per_op = tm.summary()                            # {op: (launches, mean us)}
 
-    costs = op_costs(w, L)
+    costs = token_op_costs(w, L) if tokens else op_costs(w, L)
     total_us = {k: n * us / args.steps for k, (n, us) in per_op.items()}
     dominant = max(total_us, key=total_us.get)
     n_launch, us_launch = per_op[dominant]
@@ -217,19 +261,26 @@ def main():
                       "frac": r["frac"], "algorithmic_bytes": costs[k][0],
                       "traffic": measured_traffic(k, w.name)}
 
+    if tokens:
+        metric, value, unit = "packed tokens/sec per encoder layer (1 MI355X)", sum(L) / (ms * 1e-3), "tokens/s"
+        config = {"workload": w.name, "batch": w.batch, "lengths": L, "sum_n": sum(L), "sum_n2": R,
+                  "c": w.c_s, "heads": w.heads, "head_dim": w.head_dim, "hidden": w.hidden}
+    else:
+        metric, value, unit = METRIC, w.blocks * R / (ms * 1e-3), "pair positions/s"
+        config = {"workload": w.name, "batch": w.batch, "lengths": L, "sum_n": sum(L), "sum_n2": R,
+                  "c_s": w.c_s, "c_z": w.c_z, "heads": w.heads, "head_dim": w.head_dim, "hidden": w.hidden,
+                  "blocks": w.blocks, "steps_per_block": list(w.steps)}
     out = {
-        "metric": METRIC, "value": round(w.blocks * R / (ms * 1e-3), 1), "unit": "pair positions/s",
+        "metric": metric, "value": round(value, 1), "unit": unit,
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
         "device_ms_per_step": round(ms_dev, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
-        "config": {"workload": w.name, "batch": w.batch, "lengths": L, "sum_n": sum(L), "sum_n2": R,
-                   "c_s": w.c_s, "c_z": w.c_z, "heads": w.heads, "head_dim": w.head_dim, "hidden": w.hidden,
-                   "blocks": w.blocks, "steps_per_block": list(w.steps)},
+        "config": config,
         "roofline": rl,
         "kernels": kernels,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, run)
+        out["cpu_baseline"] = cpu_baseline_tokens(w, run) if tokens else cpu_baseline(w, run)
     if args.kernels:
         for k, v in sorted(kernels.items(), key=lambda kv: -kv[1]["us"] * kv[1]["launches_per_step"]):
             tr = v["traffic"]

@@ -40,8 +40,8 @@ nt_status upload(nt_layout* L, hipStream_t s) {
       {&L->row_splits2, &L->d_row_splits2}, {&L->row_sample, &L->d_row_sample},
       {&L->attn_work, &L->d_attn_work},   {&L->tri_work, &L->d_tri_work},
       {&L->seq_work, &L->d_seq_work},
-      {&L->blk_prow, &L->d_blk_prow},     {&L->pattn_work, &L->d_pattn_work},
-      {&L->pattn2_work, &L->d_pattn2_work},
+      {&L->blk_prow, &L->d_blk_prow},
+      {&L->pattn_work, &L->d_pattn_work},
   };
   size_t total = 0;
   for (auto& p : parts) total += (p.v->size() * sizeof(int32_t) + 255) / 256 * 256;

@@ -182,16 +182,7 @@ __global__ void __launch_bounds__(256) attention_mfma_kernel(AttnArgs p) {
   }
 }
 
-// ---------------------------------------------------------------- pair attention, bias-resident
-// Pair attention for head_dim 32 and N_i <= kAttnFastMaxLen.  The bias of a
-// query j against key k does not depend on the pair row, so a workgroup takes
-// (sample, block of kAttnQB queries, group of kAttnRG rows, head): the bias
-// slice of its query block is staged in LDS once and reused by every row of
-// the group, and the next row's keys, values and queries are prefetched into
-// registers while the current row runs, so no global load sits on the
-// softmax's critical path.  Values are staged transposed with 4-byte writes
-// (two keys per lane); LDS strides put the 16 rows of every fragment read on
-// distinct bank groups.
+// ---------------------------------------------------------------- pair attention arguments
 struct PairAttnArgs {
   int axis;
   const bf16* q;
@@ -203,226 +194,35 @@ struct PairAttnArgs {
   float scale_log2;
   bf16* o;
   int64_t ld_o;
-  const int32_t* work;   // quads (sample, query block, row group, 0)
+  const int32_t* work;   // quads (sample, first 16-query tile, row group, tile count)
   const int32_t* cu_seqlens;
   const int32_t* cu_pairs;
-  int vstride, bstride;  // LDS strides (elements) of V^T and of the bias tile
-  float inv_scale;       // 1 / softmax scale (short-row kernel's bias staging)
-  int H;                 // heads (short-row kernel: heads interleaved in the grid)
+  int bstride;           // LDS stride (elements) of the staged bias slice
+  float inv_scale;       // 1 / softmax scale
+  int H;                 // heads (interleaved in the grid)
 };
 
-template <int D, int NMAX>
-__global__ void __launch_bounds__(256) attention_pair_kernel(PairAttnArgs p) {
-  extern __shared__ __attribute__((aligned(16))) bf16 lds[];
-  constexpr int KS = D + 8;
-  constexpr int DV = D / 8;
-  constexpr int MAXIT = (NMAX / 2) * DV / 256;               // staging items per thread
-  const int4 w4 = reinterpret_cast<const int4*>(p.work)[blockIdx.x];
-  const int i = w4.x;
-  if (i < 0) return;
-  const int jb = w4.y, rg = w4.z;
-  const int h = blockIdx.y;
-  const int n = p.cu_seqlens[i + 1] - p.cu_seqlens[i];
-  const int npad = (n + 63) & ~63;
-  const int npairs = npad / 2;
-  const int64_t cu = p.cu_pairs[i];
-  const int64_t sr = p.axis == 0 ? n : 1, st = p.axis == 0 ? 1 : n;   // cell(r, t) = cu + r*sr + t*st
-  bf16* Ks = lds;                                // [npad][KS]
-  bf16* Vt = lds + (size_t)npad * KS;            // [D][vstride]
-  bf16* Bs = Vt + (size_t)D * p.vstride;         // [kAttnQB][bstride]
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int l16 = lane & 15, g = lane >> 4;
-  const int j0 = jb * kAttnQB;
-
-  // ---- bias slice of the query block: Bs[q][k] = bias(j0 + q, k) ---------
-  // 16 loads in flight per thread before the first store
-  const bf16* bh = p.bias ? p.bias + (int64_t)h * p.ld_bias + cu : nullptr;
-  if (p.axis == 0) {
-    for (int q0 = 0; q0 < kAttnQB; q0 += 16)
-      for (int kk = tid; kk < npad; kk += 256) {
-        bf16 bv[16];
-#pragma unroll
-        for (int u = 0; u < 16; ++u) {
-          const int j = j0 + q0 + u;
-          bv[u] = (bh && j < n && kk < n) ? bh[(int64_t)j * n + kk] : (bf16)0.f;
-        }
-#pragma unroll
-        for (int u = 0; u < 16; ++u) Bs[(q0 + u) * p.bstride + kk] = bv[u];
-      }
-  } else {
-    const int j = j0 + lane;
-    for (int k0 = 4 * wave; k0 < npad; k0 += 64) {
-      bf16 bv[16];
-#pragma unroll
-      for (int u = 0; u < 16; ++u) {
-        const int kk = k0 + (u >> 2) * 16 + (u & 3);
-        bv[u] = (bh && j < n && kk < n) ? bh[(int64_t)kk * n + j] : (bf16)0.f;
-      }
-#pragma unroll
-      for (int u = 0; u < 16; ++u) Bs[lane * p.bstride + k0 + (u >> 2) * 16 + (u & 3)] = bv[u];
-    }
-  }
-
-  // ---- per-row staging: keys row-major, values transposed (2 keys per item)
-  const int nitems = npairs * DV;
-  uint4 kr[MAXIT][2], vr[MAXIT][2];
-  auto load_kv = [&](int r) {
-#pragma unroll
-    for (int it = 0; it < MAXIT; ++it) {
-      const int c = tid + 256 * it;
-      const int kp = c % npairs, dc = (c / npairs) * 8;
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int key = 2 * kp + u;
-        const bool valid = c < nitems && key < n;
-        const int64_t row = cu + (int64_t)r * sr + (int64_t)key * st;
-        kr[it][u] = valid ? *reinterpret_cast<const uint4*>(p.k + row * p.ld_qkv + h * D + dc) : make_uint4(0, 0, 0, 0);
-        vr[it][u] = valid ? *reinterpret_cast<const uint4*>(p.v + row * p.ld_qkv + h * D + dc) : make_uint4(0, 0, 0, 0);
-      }
-    }
-  };
-  auto store_kv = [&]() {
-#pragma unroll
-    for (int it = 0; it < MAXIT; ++it) {
-      const int c = tid + 256 * it;
-      if (c >= nitems) continue;
-      const int kp = c % npairs, dc = (c / npairs) * 8;
-      *reinterpret_cast<uint4*>(&Ks[(2 * kp) * KS + dc]) = kr[it][0];
-      *reinterpret_cast<uint4*>(&Ks[(2 * kp + 1) * KS + dc]) = kr[it][1];
-      const uint32_t a[4] = {vr[it][0].x, vr[it][0].y, vr[it][0].z, vr[it][0].w};
-      const uint32_t b[4] = {vr[it][1].x, vr[it][1].y, vr[it][1].z, vr[it][1].w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        // d = dc + 2e: (key 2kp, key 2kp+1) low halves; d = dc + 2e + 1: high halves
-        *reinterpret_cast<uint32_t*>(&Vt[(dc + 2 * e) * p.vstride + 2 * kp]) = (a[e] & 0xffffu) | (b[e] << 16);
-        *reinterpret_cast<uint32_t*>(&Vt[(dc + 2 * e + 1) * p.vstride + 2 * kp]) = (a[e] >> 16) | (b[e] & 0xffff0000u);
-      }
-    }
-  };
-
-  const int jw = j0 + 16 * wave + l16;          // this lane's query
-  const bool wave_has_queries = j0 + 16 * wave < n;
-  const bool qvalid = jw < n;
-  const int r0 = rg * kAttnRG, r1 = min(n, r0 + kAttnRG);
-  load_kv(r0);
-  bf16x8 qf[D / 32], qn[D / 32];
-#pragma unroll
-  for (int dd = 0; dd < D / 32; ++dd)
-    qf[dd] = qvalid ? *reinterpret_cast<const bf16x8*>(p.q + (cu + (int64_t)r0 * sr + (int64_t)jw * st) * p.ld_qkv + h * D + dd * 32 + g * 8)
-                    : bf16x8{};
-  store_kv();
-  __syncthreads();
-
-  for (int r = r0; r < r1; ++r) {
-    const int rn = r + 1 < r1 ? r + 1 : r;      // the last iteration reloads its own row (unused)
-    load_kv(rn);
-#pragma unroll
-    for (int dd = 0; dd < D / 32; ++dd)
-      qn[dd] = qvalid ? *reinterpret_cast<const bf16x8*>(p.q + (cu + (int64_t)rn * sr + (int64_t)jw * st) * p.ld_qkv + h * D + dd * 32 + g * 8)
-                      : bf16x8{};
-    if (wave_has_queries) {
-      float m_run = -INFINITY, l_run = 0.f;
-      f32x4 O[D / 16];
-#pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) O[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      const bf16* brow = &Bs[(16 * wave + l16) * p.bstride];
-      for (int kc = 0; kc < npad; kc += 64) {
-        f32x4 sacc[4];
-#pragma unroll
-        for (int kt = 0; kt < 4; ++kt) {
-          sacc[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int dd = 0; dd < D / 32; ++dd) {
-            const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Ks[(kc + kt * 16 + l16) * KS + dd * 32 + g * 8]);
-            sacc[kt] = mfma16(kf, qf[dd], sacc[kt]);
-          }
-        }
-        float x[4][4];
-        float mloc = -INFINITY;
-        const bool tail = kc + 64 > n;                       // only the last chunk holds padded keys
-#pragma unroll
-        for (int kt = 0; kt < 4; ++kt) {
-          const bf16x4 bb = *reinterpret_cast<const bf16x4*>(brow + kc + kt * 16 + 4 * g);
-#pragma unroll
-          for (int ii = 0; ii < 4; ++ii) {
-            float t = fmaf(sacc[kt][ii], p.scale_log2, (float)bb[ii] * kLog2e);
-            if (tail && kc + kt * 16 + 4 * g + ii >= n) t = -INFINITY;
-            x[kt][ii] = t;
-            mloc = fmaxf(mloc, t);
-          }
-        }
-        mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
-        mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-        const float m_new = fmaxf(m_run, mloc);
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-        m_run = m_new;
-        l_run *= alpha;
-#pragma unroll
-        for (int dt = 0; dt < D / 16; ++dt) O[dt] *= alpha;
-        bf16x8 pf[2];
-#pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-          for (int ii = 0; ii < 4; ++ii) {
-            const float e = __builtin_amdgcn_exp2f(x[kt][ii] - m_new);
-            l_run += e;
-            pf[kt >> 1][(kt & 1) * 4 + ii] = (bf16)e;
-          }
-#pragma unroll
-        for (int dt = 0; dt < D / 16; ++dt)
-#pragma unroll
-          for (int pp = 0; pp < 2; ++pp) {
-            const bf16* vrow = &Vt[(dt * 16 + l16) * p.vstride + kc + pp * 32 + 4 * g];
-            const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow);
-            const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 16);
-            const bf16x8 vf = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-            O[dt] = mfma16(vf, pf[pp], O[dt]);
-          }
-      }
-      l_run += __shfl_xor(l_run, 16, 64);
-      l_run += __shfl_xor(l_run, 32, 64);
-      if (qvalid) {
-        const float inv = 1.f / l_run;
-        bf16* orow = p.o + (cu + (int64_t)r * sr + (int64_t)jw * st) * p.ld_o + h * D;
-#pragma unroll
-        for (int dt = 0; dt < D / 16; ++dt) {
-          bf16x4 ov;
-#pragma unroll
-          for (int ii = 0; ii < 4; ++ii) ov[ii] = (bf16)(O[dt][ii] * inv);
-          *reinterpret_cast<bf16x4*>(orow + dt * 16 + 4 * g) = ov;
-        }
-      }
-    }
-    __syncthreads();
-    if (r + 1 < r1) {
-      store_kv();
-#pragma unroll
-      for (int dd = 0; dd < D / 32; ++dd) qf[dd] = qn[dd];
-    }
-    __syncthreads();
-  }
-}
-
-// ---------------------------------------------------------------- pair attention, short rows
-// Pair attention for head_dim 32 and N_i <= kAttn2MaxLen, organised so that
-// the exponentials are nearly the only vector work and two workgroups share
-// each CU.  A workgroup of 8 waves takes (sample, block of 128 queries, group
-// of 16 pair rows, head):
+// ---------------------------------------------------------------- pair attention, head_dim 32
+// Pair attention for head_dim 32 and N_i <= kAttnLongLen, organised so that
+// the exponentials are nearly the only vector work.  A workgroup of 8 waves
+// takes (sample, block of up to 128 queries, group of 16 pair rows, head):
 //   * the bias of (query, key) does not depend on the pair row, so each lane
 //     keeps the bias of its query for its 4-key groups of every key tile in
 //     registers for the whole group of rows -- staged once through LDS and
 //     divided by the softmax scale (one bf16 rounding) -- and it seeds the
 //     score accumulators: the matrix cores produce bias/scale + q.k directly;
-//   * keys and values of a row are staged as fragment images (64 lanes x 16
-//     bytes, read as one contiguous 1 KB per wave) in two buffers that alias
-//     the bias staging area, the next row loading into registers while the
-//     current row runs: one barrier per row, 64 KB of LDS;
+//   * keys and values of a row are copied straight into LDS (keys as fragment
+//     images: 64 lanes x 16 bytes, read as one contiguous 1 KB per wave) in
+//     two buffers that alias the bias staging area, the next row's copies in
+//     flight while the current row runs: one barrier per row;
 //   * the softmax denominator comes from one more matrix-core product with a
 //     ones operand, on the same bf16 probabilities as the numerator.
 // Scores are kept transposed (S^T = K Q^T), so a lane holds 16 keys of one
 // query per 64-key chunk and the running max is mostly lane-local.
+// Two instances: N <= 256 (64 KB of LDS, two workgroups per CU) and N <= 512
+// (128 KB, one workgroup per CU, twice the bias registers).
 template <int NMAX>
-__global__ void __launch_bounds__(512, 4) attention_pair2_kernel(PairAttnArgs p) {
+__global__ void __launch_bounds__(512, NMAX <= 256 ? 4 : 2) attention_pair_kernel(PairAttnArgs p) {
   constexpr int D = 32;
   constexpr int KT16 = NMAX / 16;               // key tiles
   extern __shared__ __attribute__((aligned(16))) bf16 lds[];
@@ -439,7 +239,7 @@ __global__ void __launch_bounds__(512, 4) attention_pair2_kernel(PairAttnArgs p)
   const int npad = (n + 63) & ~63;
   const int64_t cu = p.cu_pairs[i];
   const int64_t sr = p.axis == 0 ? n : 1, st = p.axis == 0 ? 1 : n;   // cell(r, t) = cu + r*sr + t*st
-  bf16* Bs = lds;                                          // [kAttnQB2][bstride], start-up only
+  bf16* Bs = lds;                                          // [kAttnQB][bstride], start-up only
   bf16* Kb0 = lds;                                         // key images: tile of 16 keys -> 512 elements
   bf16* Kb1 = Kb0 + NMAX * D;
   bf16* Vb0 = Kb1 + NMAX * D;                              // values, row-major [key][D]
@@ -453,7 +253,7 @@ __global__ void __launch_bounds__(512, 4) attention_pair2_kernel(PairAttnArgs p)
     const bf16* bh = p.bias ? p.bias + (int64_t)h * p.ld_bias + cu : nullptr;
     const float inv_scale = p.inv_scale;
     if (p.axis == 0) {
-      for (int e = tid; e < kAttnQB2 * (npad / 8); e += 512) {
+      for (int e = tid; e < kAttnQB * (npad / 8); e += 512) {
         const int q = e / (npad / 8), k0 = (e % (npad / 8)) * 8, j = j0 + q;
         bf16x4 o0, o1;                            // rows are 8-byte aligned (stride 4 mod 8 elements)
 #pragma unroll
@@ -465,8 +265,8 @@ __global__ void __launch_bounds__(512, 4) attention_pair2_kernel(PairAttnArgs p)
         *reinterpret_cast<bf16x4*>(&Bs[q * p.bstride + k0 + 4]) = o1;
       }
     } else {
-      for (int e = tid; e < kAttnQB2 * npad; e += 512) {
-        const int q = e % kAttnQB2, k = e / kAttnQB2, j = j0 + q;
+      for (int e = tid; e < kAttnQB * npad; e += 512) {
+        const int q = e % kAttnQB, k = e / kAttnQB, j = j0 + q;
         Bs[q * p.bstride + k] = (bf16)((bh && j < n && k < n) ? (float)bh[(int64_t)k * n + j] * inv_scale : 0.f);
       }
     }
@@ -530,7 +330,7 @@ __global__ void __launch_bounds__(512, 4) attention_pair2_kernel(PairAttnArgs p)
   const int jw = j0 + 16 * wave + l16;          // this lane's query
   const bool wave_has_queries = wave < nqt && j0 + 16 * wave < n;
   const bool qvalid = jw < n;
-  const int r0 = rg * kAttnRG2, r1 = min(n, r0 + kAttnRG2);
+  const int r0 = rg * kAttnRG, r1 = min(n, r0 + kAttnRG);
   bf16x8 qf = qvalid ? *reinterpret_cast<const bf16x8*>(p.q + (cu + (int64_t)r0 * sr + (int64_t)jw * st) * p.ld_qkv + h * D + g * 8)
                      : bf16x8{};
   __syncthreads();                              // bias slice staged
@@ -724,34 +524,23 @@ hipError_t launch_attention(const nt_layout& L, int axis, int H, int D, const vo
     return hipGetLastError();
   }
   const int npad = (L.max_len + 63) & ~63;
-  if (D == 32 && axis != 2 && L.max_len <= kAttn2MaxLen) {
-    if (L.pattn2_items() == 0) return hipSuccess;
-    // bias rows: 8-byte fragment reads are conflict-free with a row stride of 2 (mod 4) dwords
-    const int bstride = kAttn2MaxLen + 4;
-    PairAttnArgs a{axis, (const bf16*)q, (const bf16*)k, (const bf16*)v, ld_qkv, (const bf16*)bias, ld_bias,
-                   scale * kLog2e, (bf16*)o, ld_o, L.d_pattn2_work, L.d_cu_seqlens, L.d_cu_pairs, 0, bstride,
-                   1.f / scale, H};
-    const size_t smem = sizeof(bf16) * std::max((size_t)kAttnQB2 * bstride, 4 * (size_t)kAttn2MaxLen * 32);
-    const dim3 grid((unsigned)(L.pattn2_items() * H));
-    hipFuncSetAttribute((const void*)attention_pair2_kernel<kAttn2MaxLen>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-    attention_pair2_kernel<kAttn2MaxLen><<<grid, dim3(512), smem, s>>>(a);
-    return hipGetLastError();
-  }
-  if (D == 32 && axis != 2 && L.max_len <= kAttnFastMaxLen) {
-    // 8-byte fragment reads are conflict-free with a row stride of 2 (mod 4) dwords
-    const int stride = (npad + 127) / 128 * 128 + 4;
-    PairAttnArgs a{axis, (const bf16*)q, (const bf16*)k, (const bf16*)v, ld_qkv, (const bf16*)bias, ld_bias,
-                   scale * kLog2e, (bf16*)o, ld_o, L.d_pattn_work, L.d_cu_seqlens, L.d_cu_pairs, stride, stride, 0.f, H};
-    const size_t smem = sizeof(bf16) * ((size_t)npad * (32 + 8) + (size_t)32 * stride + (size_t)kAttnQB * stride);
+  if (D == 32 && axis != 2 && L.max_len <= kAttnLongLen) {
     if (L.pattn_items() == 0) return hipSuccess;
-    const dim3 grid((unsigned)L.pattn_items(), (unsigned)H);
-    if (npad <= 256) {
-      hipFuncSetAttribute((const void*)attention_pair_kernel<32, 256>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-      attention_pair_kernel<32, 256><<<grid, dim3(256), smem, s>>>(a);
-    } else {
-      hipFuncSetAttribute((const void*)attention_pair_kernel<32, kAttnFastMaxLen>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-      attention_pair_kernel<32, kAttnFastMaxLen><<<grid, dim3(256), smem, s>>>(a);
-    }
+    const int nmax = L.max_len <= kAttnShortLen ? kAttnShortLen : kAttnLongLen;
+    // bias rows: 8-byte fragment reads are conflict-free with a row stride of 2 (mod 4) dwords
+    const int bstride = nmax + 4;
+    PairAttnArgs a{axis, (const bf16*)q, (const bf16*)k, (const bf16*)v, ld_qkv, (const bf16*)bias, ld_bias,
+                   scale * kLog2e, (bf16*)o, ld_o, L.d_pattn_work, L.d_cu_seqlens, L.d_cu_pairs, bstride,
+                   1.f / scale, H};
+    const size_t smem = sizeof(bf16) * std::max((size_t)kAttnQB * bstride, 4 * (size_t)nmax * 32);
+    const dim3 grid((unsigned)(L.pattn_items() * H));
+    const void* fn = nmax == kAttnShortLen ? (const void*)attention_pair_kernel<kAttnShortLen>
+                                          : (const void*)attention_pair_kernel<kAttnLongLen>;
+    hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    if (nmax == kAttnShortLen)
+      attention_pair_kernel<kAttnShortLen><<<grid, dim3(512), smem, s>>>(a);
+    else
+      attention_pair_kernel<kAttnLongLen><<<grid, dim3(512), smem, s>>>(a);
     return hipGetLastError();
   }
   const int vstride = (npad + 127) / 128 * 128 + 4;

@@ -128,25 +128,7 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L) {
       }
     L->attn_work = xcd_order<2>(items, cost);
   }
-  // pair attention, bias-resident form: one item per (sample, block of QB
-  // queries, group of RG pair rows); the query blocks of one row group are
-  // generated next to each other so they run back to back on one XCD and share
-  // the rows' keys and values in its L2
-  auto pair_attn_items = [&](int32_t QB, int32_t RG, bool largest_first) {
-    std::vector<std::array<int32_t, 4>> items;
-    std::vector<double> cost;
-    for (int32_t i = 0; i < batch; ++i) {
-      const int32_t n = lengths[i];
-      for (int32_t rg = 0; rg * RG < n; ++rg)
-        for (int32_t jb = 0; jb * QB < n; ++jb) {
-          items.push_back({i, jb, rg, 0});
-          cost.push_back((double)std::min(RG, n - rg * RG) * std::min(QB, n - jb * QB) * n);
-        }
-    }
-    return xcd_order<4>(items, cost, largest_first);
-  };
-  L->pattn_work = pair_attn_items(kAttnQB, kAttnRG, true);
-  // Short-row kernel: a sample's 16-query tiles are split evenly over
+  // pair attention: a sample's 16-query tiles are split evenly over
   // ceil(tiles / 8) blocks (items: sample, first tile, row group, tile count),
   // so no block leaves most of its 8 waves idle; generation order is kept in
   // each XCD's queue so the blocks of a row group stay adjacent and share keys
@@ -156,15 +138,15 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L) {
     std::vector<double> cost;
     for (int32_t i = 0; i < batch; ++i) {
       const int32_t n = lengths[i], tiles = (n + 15) / 16;
-      const int32_t blocks = (tiles + kAttnQB2 / 16 - 1) / (kAttnQB2 / 16);
-      for (int32_t rg = 0; rg * kAttnRG2 < n; ++rg)
+      const int32_t blocks = (tiles + kAttnQB / 16 - 1) / (kAttnQB / 16);
+      for (int32_t rg = 0; rg * kAttnRG < n; ++rg)
         for (int32_t b = 0; b < blocks; ++b) {
           const int32_t t0 = b * tiles / blocks, t1 = (b + 1) * tiles / blocks;
           items.push_back({i, t0, rg, t1 - t0});
-          cost.push_back((double)std::min(kAttnRG2, n - rg * kAttnRG2) * std::min(16 * (t1 - t0), n - 16 * t0) * n);
+          cost.push_back((double)std::min(kAttnRG, n - rg * kAttnRG) * std::min(16 * (t1 - t0), n - 16 * t0) * n);
         }
     }
-    L->pattn2_work = xcd_order<4>(items, cost, false);
+    L->pattn_work = xcd_order<4>(items, cost, false);
   }
   // triangle: one item per (sample, 32x32 output tile), largest samples first.
   // The channel blocks, not the tiles, are spread over the XCDs (the launch

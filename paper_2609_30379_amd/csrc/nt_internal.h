@@ -16,12 +16,10 @@ constexpr int kXcds = 8;          // MI355X: 8 XCDs, workgroups dispatched round
 constexpr int kTriTile = 32;      // triangle output tile: 32 x 32 cells
 constexpr int kSeqQBlock = 64;    // 1-D attention: queries per workgroup
 constexpr int kLinRows = 128;     // rows per projection workgroup (pair-row table granularity)
-constexpr int kAttnQB = 64;       // pair attention: queries per workgroup
-constexpr int kAttnRG = 16;       // pair attention: pair rows per workgroup
-constexpr int kAttnFastMaxLen = 512;  // pair attention with the bias tile resident in LDS
-constexpr int kAttnQB2 = 128;     // pair attention, short rows: queries per workgroup (8 waves x 16)
-constexpr int kAttnRG2 = 16;      // pair attention, short rows: pair rows per workgroup
-constexpr int kAttn2MaxLen = 256; // longest sample of the short-row pair attention
+constexpr int kAttnQB = 128;      // pair attention (head_dim 32): queries per workgroup (8 waves x 16)
+constexpr int kAttnRG = 16;       // pair attention (head_dim 32): pair rows per workgroup
+constexpr int kAttnShortLen = 256;  // its instance with two workgroups per CU: longest sample
+constexpr int kAttnLongLen = 512;   // its instance with one workgroup per CU: longest sample
 
 // Attention limits imposed by staging a whole key segment in LDS.
 constexpr int kAttnMaxLenD32 = 1024;
@@ -46,8 +44,7 @@ struct nt_layout {
   std::vector<int32_t> attn_work;    // pairs (sample, row); count multiple of 8; (-1,-1) = idle
   std::vector<int32_t> tri_work;     // quads (sample, xt, yt, 0); count multiple of 8
   std::vector<int32_t> seq_work;     // pairs (sample, query block); count multiple of 8
-  std::vector<int32_t> pattn_work;   // quads (sample, query block, row group, 0); count multiple of 8
-  std::vector<int32_t> pattn2_work;  // the same with kAttnQB2-query blocks and kAttnRG2-row groups
+  std::vector<int32_t> pattn_work;  // quads (sample, first 16-query tile, row group, tile count)
   std::vector<int32_t> blk_prow;     // [ceil(sum N^2 / kLinRows)] pair row holding cell kLinRows*b
 
   bool has_device = false;
@@ -63,14 +60,12 @@ struct nt_layout {
   const int32_t* d_tri_work = nullptr;
   const int32_t* d_seq_work = nullptr;
   const int32_t* d_pattn_work = nullptr;
-  const int32_t* d_pattn2_work = nullptr;
   const int32_t* d_blk_prow = nullptr;
 
   int64_t attn_items() const { return (int64_t)attn_work.size() / 2; }
   int64_t tri_items() const { return (int64_t)tri_work.size() / 4; }
   int64_t seq_items() const { return (int64_t)seq_work.size() / 2; }
   int64_t pattn_items() const { return (int64_t)pattn_work.size() / 4; }
-  int64_t pattn2_items() const { return (int64_t)pattn2_work.size() / 4; }
 };
 
 namespace nt {
