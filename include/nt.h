@@ -32,6 +32,8 @@
  * calls never allocate, free or retain them.  An nt_layout and its device
  * mirrors are owned by the library from nt_from_* until nt_layout_destroy;
  * the caller must not destroy a layout while work that uses it is queued.
+ * One op allocates: nt_pair_row_attention keeps a workspace in the layout
+ * (see there).
  *
  * Streams: every op enqueues asynchronously on the caller's HIP stream
  * (NULL = the default stream) and returns without synchronising.  Only
@@ -230,8 +232,16 @@ nt_status nt_layernorm_linear(const nt_linear_args* args, void* stream);
  *   bias     head-major [H][ld_bias] or NULL (axes 0/1).
  *   scale    softmax scale (e.g. 1/sqrt(d)).
  *   o        [rows, H*d] row stride ld_o.
+ * Workspace: with a bias, bf16, d = 32 and every N_i <= 512 the call first
+ * writes bias/scale (rounded to bf16) in the per-lane order of the attention
+ * kernel into a workspace owned by the layout, H * T * 512 bytes with
+ * T = sum_i ceil(N_i/16) * ceil(N_i/64) * 4.  The first such call allocates it
+ * (hipMalloc; a later call with more heads regrows it), nt_layout_destroy
+ * frees it.  Such calls on one layout must therefore be ordered (one stream,
+ * or synchronised), not concurrent.
  * Errors: NT_ERR_INVALID_ARG, NT_ERR_UNSUPPORTED (d, or N_i beyond the
- * on-chip limit: 1024 for d=32, 512 for d=64).                               */
+ * on-chip limit: 1024 for d=32, 512 for d=64), NT_ERR_HIP (also when the
+ * workspace cannot be allocated).                                            */
 nt_status nt_pair_row_attention(const nt_layout* layout, int32_t axis,
                                 int32_t heads, int32_t head_dim,
                                 const void* q, const void* k, const void* v, int64_t ld_qkv,

@@ -41,7 +41,7 @@ nt_status upload(nt_layout* L, hipStream_t s) {
       {&L->attn_work, &L->d_attn_work},   {&L->tri_work, &L->d_tri_work},
       {&L->seq_work, &L->d_seq_work},
       {&L->blk_prow, &L->d_blk_prow},
-      {&L->pattn_work, &L->d_pattn_work},
+      {&L->pattn_work, &L->d_pattn_work}, {&L->bias_tiles, &L->d_bias_tiles},
   };
   size_t total = 0;
   for (auto& p : parts) total += (p.v->size() * sizeof(int32_t) + 255) / 256 * 256;
@@ -123,6 +123,9 @@ nt_status nt_layout_destroy(nt_layout* L) {
   nt_status st = NT_OK;
   if (L->d_base) {
     if (hipFree(L->d_base) != hipSuccess) st = nt::fail(NT_ERR_HIP, "hipFree of layout mirrors failed");
+  }
+  if (L->d_attn_ws) {
+    if (hipFree(L->d_attn_ws) != hipSuccess) st = nt::fail(NT_ERR_HIP, "hipFree of the attention workspace failed");
   }
   delete L;
   return st;

@@ -10,6 +10,7 @@
 //   O^T += V^T P^T    P is taken from the S^T registers as the B operand
 //                     (keys {4g..4g+3} of two 16-key tiles), no shuffles.
 #include <algorithm>
+#include <type_traits>
 
 #include "nt_device.h"
 #include "nt_internal.h"
@@ -197,10 +198,56 @@ struct PairAttnArgs {
   const int32_t* work;   // quads (sample, first 16-query tile, row group, tile count)
   const int32_t* cu_seqlens;
   const int32_t* cu_pairs;
-  int bstride;           // LDS stride (elements) of the staged bias slice
-  float inv_scale;       // 1 / softmax scale
   int H;                 // heads (interleaved in the grid)
+  const uint2* bias_img; // bias image (see bias_image_kernel) or NULL for no bias
+  int64_t img_head;      // uint2 entries per head of the image
+  const int32_t* bias_tiles;
 };
+
+// Pair bias image: for head h, sample i, 16-query tile qt and 16-key tile kt
+// (kt < round_up(N_i,64)/16), lane l = l16 + 16 g of tile
+// ((h * T + bias_tiles[i] + qt * KT_i + kt) holds the four values
+// bias(j, k) / scale, j = 16 qt + l16, k = 16 kt + 4 g .. +3, each rounded to
+// bf16, 0 past N -- exactly the register image the attention lanes keep.
+// bias(j, k) is bias[h][cell(j, k)] for axis 0 and bias[h][cell(k, j)] for
+// axis 1.  One wave per tile, the sample found by bisection.
+struct BiasImgArgs {
+  int axis, batch;
+  const bf16* bias;
+  int64_t ld_bias;
+  float inv_scale;
+  uint2* img;
+  int64_t tiles;          // tiles per head
+  const int32_t* bias_tiles;
+  const int32_t* cu_seqlens;
+  const int32_t* cu_pairs;
+};
+
+__global__ void __launch_bounds__(256) bias_image_kernel(BiasImgArgs p) {
+  const int64_t tile = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (tile >= p.tiles) return;
+  const int h = blockIdx.y, lane = threadIdx.x & 63, l16 = lane & 15, g = lane >> 4;
+  int lo = 0, hi = p.batch - 1;                 // sample: largest i with bias_tiles[i] <= tile
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (p.bias_tiles[mid] <= tile) lo = mid; else hi = mid - 1;
+  }
+  const int i = lo;
+  const int n = p.cu_seqlens[i + 1] - p.cu_seqlens[i];
+  const int kti = ((n + 63) >> 6) * 4;
+  const int t = (int)(tile - p.bias_tiles[i]);
+  const int j = (t / kti) * 16 + l16, k0 = (t % kti) * 16 + 4 * g;
+  const bf16* bh = p.bias + (int64_t)h * p.ld_bias + p.cu_pairs[i];
+  bf16x4 o;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int k = k0 + e;
+    float b = 0.f;
+    if (j < n && k < n) b = (float)bh[p.axis == 0 ? (int64_t)j * n + k : (int64_t)k * n + j] * p.inv_scale;
+    o[e] = (bf16)b;
+  }
+  *reinterpret_cast<bf16x4*>(&p.img[(int64_t)h * p.tiles * 64 + tile * 64 + lane]) = o;
+}
 
 // ---------------------------------------------------------------- pair attention, head_dim 32
 // Pair attention for head_dim 32 and N_i <= kAttnLongLen, organised so that
@@ -239,7 +286,6 @@ __global__ void __launch_bounds__(512, NMAX <= 256 ? 4 : 2) attention_pair_kerne
   const int npad = (n + 63) & ~63;
   const int64_t cu = p.cu_pairs[i];
   const int64_t sr = p.axis == 0 ? n : 1, st = p.axis == 0 ? 1 : n;   // cell(r, t) = cu + r*sr + t*st
-  bf16* Bs = lds;                                          // [kAttnQB][bstride], start-up only
   bf16* Kb0 = lds;                                         // key images: tile of 16 keys -> 512 elements
   bf16* Kb1 = Kb0 + NMAX * D;
   bf16* Vb0 = Kb1 + NMAX * D;                              // values, row-major [key][D]
@@ -247,30 +293,6 @@ __global__ void __launch_bounds__(512, NMAX <= 256 ? 4 : 2) attention_pair_kerne
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, g = lane >> 4;
   const int j0 = qt0 * 16;
-
-  // ---- bias slice / scale: Bs[q][k] = bias(j0 + q, k) / scale, 0 past N --
-  {
-    const bf16* bh = p.bias ? p.bias + (int64_t)h * p.ld_bias + cu : nullptr;
-    const float inv_scale = p.inv_scale;
-    if (p.axis == 0) {
-      for (int e = tid; e < kAttnQB * (npad / 8); e += 512) {
-        const int q = e / (npad / 8), k0 = (e % (npad / 8)) * 8, j = j0 + q;
-        bf16x4 o0, o1;                            // rows are 8-byte aligned (stride 4 mod 8 elements)
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          o0[u] = (bf16)((bh && j < n && k0 + u < n) ? (float)bh[(int64_t)j * n + k0 + u] * inv_scale : 0.f);
-          o1[u] = (bf16)((bh && j < n && k0 + 4 + u < n) ? (float)bh[(int64_t)j * n + k0 + 4 + u] * inv_scale : 0.f);
-        }
-        *reinterpret_cast<bf16x4*>(&Bs[q * p.bstride + k0]) = o0;
-        *reinterpret_cast<bf16x4*>(&Bs[q * p.bstride + k0 + 4]) = o1;
-      }
-    } else {
-      for (int e = tid; e < kAttnQB * npad; e += 512) {
-        const int q = e % kAttnQB, k = e / kAttnQB, j = j0 + q;
-        Bs[q * p.bstride + k] = (bf16)((bh && j < n && k < n) ? (float)bh[(int64_t)k * n + j] * inv_scale : 0.f);
-      }
-    }
-  }
 
   // ---- per-row staging: straight global -> LDS copies ---------------------
   // Each wave copies its key tiles (wave, wave + 8, ...; 16 keys each) with
@@ -301,30 +323,70 @@ __global__ void __launch_bounds__(512, NMAX <= 256 ? 4 : 2) attention_pair_kerne
   // lane 4q+m of each 16-lane group element m of the 8-byte pieces addressed
   // by lanes q, q+4, q+8, q+12; pointing lane i at key base + i/4, dims
   // 16 dt + 4 (i%4) therefore delivers 4 consecutive keys of dim l16.  The
-  // four reads of a key block are issued together from inline assembly with
-  // their own wait: the compiler cannot tell them apart from the copies into
-  // the other buffer and would otherwise wait for those first.  The row-end
-  // wait and barrier make the buffer being read complete.
-  auto v_frags = [&](const bf16* Vr, int kb, bf16x8& f0, bf16x8& f1) {
-    // key kk and kk + 16 share (kk >> 2) & 3 = g, hence the same swizzle
-    const int kk = kb * 32 + 4 * g + (l16 >> 2), q = l16 & 3;
-    const int off0 = ((q >> 1) ^ g) * 8 + (q & 1) * 4;         // dims 4q .. 4q+3 (dim group q/2)
-    const int off1 = (((q >> 1) + 2) ^ g) * 8 + (q & 1) * 4;   // dims 16 + 4q ..
-    const uint32_t a0 = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) bf16*)(Vr + kk * D + off0);
-    const uint32_t a1 = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) bf16*)(Vr + kk * D + off1);
-    uint2 lo0, hi0, lo1, hi1;                     // dims 0-15 (keys +0, +16), dims 16-31
+  // reads of one or two key blocks are issued together from inline assembly
+  // with their own wait: the compiler cannot tell them apart from the copies
+  // into the other buffer and would otherwise wait for those first.  The
+  // row-end wait and barrier make the buffer being read complete.  Key
+  // blocks are 2 KB apart and keys kk, kk + 16 share (kk >> 2) & 3 = g, so
+  // every read of a lane uses the same swizzled column.
+  int v_a0, v_a1;                                 // LDS byte offsets within a value buffer, key block 0
+  {
+    const int kk = 4 * g + (l16 >> 2), q = l16 & 3;
+    v_a0 = (kk * D + ((q >> 1) ^ g) * 8 + (q & 1) * 4) * 2;         // dims 4q .. 4q+3 (dim group q/2)
+    v_a1 = (kk * D + (((q >> 1) + 2) ^ g) * 8 + (q & 1) * 4) * 2;   // dims 16 + 4q ..
+  }
+  auto lds_addr = [](const bf16* ptr) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) bf16*)ptr;
+  };
+  auto pack = [](uint2 lo, uint2 hi) {
+    const uint32_t w[4] = {lo.x, lo.y, hi.x, hi.y};
+    return __builtin_bit_cast(bf16x8, w);
+  };
+  // one key block: f[0] dims 0-15, f[1] dims 16-31
+  auto v_frags1 = [&](const bf16* Vr, int kb, bf16x8 (&f)[2]) {
+    const uint32_t a0 = lds_addr(Vr + kb * 32 * D) + v_a0, a1 = lds_addr(Vr + kb * 32 * D) + v_a1;
+    uint2 r[4];
     asm volatile(
         "ds_read_b64_tr_b16 %0, %4\n"
         "ds_read_b64_tr_b16 %1, %4 offset:1024\n"
         "ds_read_b64_tr_b16 %2, %5\n"
         "ds_read_b64_tr_b16 %3, %5 offset:1024\n"
         "s_waitcnt lgkmcnt(0)"
-        : "=&v"(lo0), "=&v"(hi0), "=&v"(lo1), "=&v"(hi1)
+        : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3])
         : "v"(a0), "v"(a1)
         : "memory");
-    const uint32_t w0[4] = {lo0.x, lo0.y, hi0.x, hi0.y}, w1[4] = {lo1.x, lo1.y, hi1.x, hi1.y};
-    f0 = __builtin_bit_cast(bf16x8, w0);
-    f1 = __builtin_bit_cast(bf16x8, w1);
+    f[0] = pack(r[0], r[1]);
+    f[1] = pack(r[2], r[3]);
+  };
+  // two key blocks kb, kb + 1: f[0..1] as above for kb, f[2..3] for kb + 1
+  auto v_frags2 = [&](const bf16* Vr, int kb, bf16x8 (&f)[4]) {
+    const uint32_t a0 = lds_addr(Vr + kb * 32 * D) + v_a0, a1 = lds_addr(Vr + kb * 32 * D) + v_a1;
+    uint2 r[8];
+    asm volatile(
+        "ds_read_b64_tr_b16 %0, %8\n"
+        "ds_read_b64_tr_b16 %1, %8 offset:1024\n"
+        "ds_read_b64_tr_b16 %2, %9\n"
+        "ds_read_b64_tr_b16 %3, %9 offset:1024\n"
+        "ds_read_b64_tr_b16 %4, %8 offset:2048\n"
+        "ds_read_b64_tr_b16 %5, %8 offset:3072\n"
+        "ds_read_b64_tr_b16 %6, %9 offset:2048\n"
+        "ds_read_b64_tr_b16 %7, %9 offset:3072\n"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]), "=&v"(r[6]), "=&v"(r[7])
+        : "v"(a0), "v"(a1)
+        : "memory");
+    f[0] = pack(r[0], r[1]);
+    f[1] = pack(r[2], r[3]);
+    f[2] = pack(r[4], r[5]);
+    f[3] = pack(r[6], r[7]);
+  };
+  // maximum over the four lanes l16 + 16 g holding one query: the swaps pair
+  // lane l with l ^ 16, then with l ^ 32, and leave both values in place
+  auto query_max = [](float v) {
+    const auto s16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = fmaxf(__uint_as_float(s16[0]), __uint_as_float(s16[1]));
+    const auto s32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(s32[0]), __uint_as_float(s32[1]));
   };
 
   const int jw = j0 + 16 * wave + l16;          // this lane's query
@@ -333,14 +395,17 @@ __global__ void __launch_bounds__(512, NMAX <= 256 ? 4 : 2) attention_pair_kerne
   const int r0 = rg * kAttnRG, r1 = min(n, r0 + kAttnRG);
   bf16x8 qf = qvalid ? *reinterpret_cast<const bf16x8*>(p.q + (cu + (int64_t)r0 * sr + (int64_t)jw * st) * p.ld_qkv + h * D + g * 8)
                      : bf16x8{};
-  __syncthreads();                              // bias slice staged
-  // lane's bias: query 16*wave + l16, keys 16*kt + 4g .. +3 of every key tile
+  // lane's bias: query 16*wave + l16, keys 16*kt + 4g .. +3 of every key
+  // tile, read from the bias image (one contiguous 512 bytes per wave and tile)
   uint2 bias_r[KT16];
+  {
+    const int kti = npad / 16;
+    const uint2* img = p.bias_img && wave_has_queries
+                           ? p.bias_img + h * p.img_head + ((int64_t)p.bias_tiles[i] + (int64_t)(qt0 + wave) * kti) * 64 + lane
+                           : nullptr;
 #pragma unroll
-  for (int kt = 0; kt < KT16; ++kt)
-    bias_r[kt] = kt * 16 < npad ? *reinterpret_cast<const uint2*>(&Bs[(16 * wave + l16) * p.bstride + kt * 16 + 4 * g])
-                                : make_uint2(0u, 0u);
-  __syncthreads();                              // staging area free for keys and values
+    for (int kt = 0; kt < KT16; ++kt) bias_r[kt] = img && kt < kti ? img[kt * 64] : make_uint2(0u, 0u);
+  }
   dma_kv(r0, Kb0, Vb0);
   __builtin_amdgcn_s_waitcnt(0);                // this wave's copies have landed
   __syncthreads();
@@ -368,40 +433,41 @@ __global__ void __launch_bounds__(512, NMAX <= 256 ? 4 : 2) attention_pair_kerne
       f32x4 O[3];                                 // dims 0-15, 16-31, row sum
 #pragma unroll
       for (int u = 0; u < 3; ++u) O[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+      // Keys in super-chunks of 128 (8 key tiles), the last one cut to the
+      // 2, 4 or 6 tiles that hold keys: all score products of a super-chunk
+      // are issued together, one maximum per query, then the exponentials
+      // and the value products.  Tiles read stay below the staged length.
+      auto super_chunk = [&](auto sc_c, auto nt_c) {
+        constexpr int SC = decltype(sc_c)::value, NT = decltype(nt_c)::value;
+        constexpr int T0 = SC * 8;                // first key tile
+        const int kc = SC * 128;
+        f32x4 S[NT];
 #pragma unroll
-      for (int ci = 0; ci < NMAX / 64; ++ci) {
-        const int kc = ci * 64;
-        if (kc >= n) break;
-        const bool tail = kc + 64 > n;
-        const int ntile = (tail && n - kc <= 32) ? 2 : 4;   // a short tail takes half a chunk
-        f32x4 sacc[4];
-#pragma unroll
-        for (int kt = 0; kt < 4; ++kt) {
-          if (kt >= ntile) break;
-          const uint2 bb = bias_r[ci * 4 + kt];
-          sacc[kt] = f32x4{__uint_as_float(bb.x << 16), __uint_as_float(bb.x & 0xffff0000u),
-                           __uint_as_float(bb.y << 16), __uint_as_float(bb.y & 0xffff0000u)};
-          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Kb[(ci * 4 + kt) * 512 + lane * 8]);
-          sacc[kt] = mfma16(kf, qf, sacc[kt]);
+        for (int kt = 0; kt < NT; ++kt) {
+          const uint2 bb = bias_r[T0 + kt];
+          S[kt] = f32x4{__uint_as_float(bb.x << 16), __uint_as_float(bb.x & 0xffff0000u),
+                        __uint_as_float(bb.y << 16), __uint_as_float(bb.y & 0xffff0000u)};
+          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Kb[(T0 + kt) * 512 + lane * 8]);
+          S[kt] = mfma16(kf, qf, S[kt]);
+          // at most four key fragments in flight (registers)
+          if (kt % 4 == 3) __builtin_amdgcn_sched_barrier(0);
         }
-        if (tail) {
+        if (kc + NT * 16 > n) {                   // keys past N
 #pragma unroll
-          for (int kt = 0; kt < 4; ++kt)
+          for (int kt = 0; kt < NT; ++kt)
 #pragma unroll
             for (int ii = 0; ii < 4; ++ii)
-              if (kt >= ntile || kc + kt * 16 + 4 * g + ii >= n) sacc[kt][ii] = -INFINITY;
+              if (kc + kt * 16 + 4 * g + ii >= n) S[kt][ii] = -INFINITY;
         }
-        float mloc = fmaxf(fmaxf(sacc[0][0], sacc[0][1]), fmaxf(sacc[0][2], sacc[0][3]));
+        float mloc = S[0][0];
 #pragma unroll
-        for (int kt = 1; kt < 4; ++kt) {
-          if (kt >= ntile) break;
-          mloc = fmaxf(mloc, fmaxf(fmaxf(sacc[kt][0], sacc[kt][1]), fmaxf(sacc[kt][2], sacc[kt][3])));
-        }
-        mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
-        mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+        for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+          for (int ii = 0; ii < 4; ++ii) mloc = fmaxf(mloc, S[kt][ii]);
+        mloc = query_max(mloc);
         // the reference max moves only when some query's max grew by more
         // than 8 (log2 units): probabilities then stay below 2^8, and most
-        // chunks skip rescaling the accumulators
+        // super-chunks skip rescaling the accumulators
         if (__any((mloc - m_s) * c > 8.f)) {
           const float m_new = fmaxf(m_s, mloc);
           const float alpha = __builtin_amdgcn_exp2f((m_s - m_new) * c);
@@ -410,24 +476,47 @@ __global__ void __launch_bounds__(512, NMAX <= 256 ? 4 : 2) attention_pair_kerne
           for (int u = 0; u < 3; ++u) O[u] *= alpha;
         }
         const float nm = -m_s * c;
-        bf16x8 pf[2];
+        bf16x8 P[NT / 2];
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt) {
-          if (kt >= ntile) break;
+        for (int kt = 0; kt < NT; ++kt)
 #pragma unroll
           for (int ii = 0; ii < 4; ++ii)
-            pf[kt >> 1][(kt & 1) * 4 + ii] = (bf16)__builtin_amdgcn_exp2f(fmaf(sacc[kt][ii], c, nm));
-        }
+            P[kt >> 1][(kt & 1) * 4 + ii] = (bf16)__builtin_amdgcn_exp2f(fmaf(S[kt][ii], c, nm));
 #pragma unroll
-        for (int pp = 0; pp < 2; ++pp) {
-          if (2 * pp >= ntile) break;
-          const int kb = ci * 2 + pp;
-          bf16x8 vf0, vf1;
-          v_frags(Vb, kb, vf0, vf1);
-          O[0] = mfma16(vf0, pf[pp], O[0]);
-          O[1] = mfma16(vf1, pf[pp], O[1]);
-          O[2] = mfma16(ones, pf[pp], O[2]);
+        for (int pp = 0; pp + 1 < NT / 2; pp += 2) {
+          bf16x8 vf[4];
+          v_frags2(Vb, SC * 4 + pp, vf);
+          O[0] = mfma16(vf[0], P[pp], O[0]);
+          O[1] = mfma16(vf[1], P[pp], O[1]);
+          O[2] = mfma16(ones, P[pp], O[2]);
+          O[0] = mfma16(vf[2], P[pp + 1], O[0]);
+          O[1] = mfma16(vf[3], P[pp + 1], O[1]);
+          O[2] = mfma16(ones, P[pp + 1], O[2]);
         }
+        if constexpr ((NT / 2) % 2 == 1) {
+          bf16x8 vf[2];
+          v_frags1(Vb, SC * 4 + NT / 2 - 1, vf);
+          O[0] = mfma16(vf[0], P[NT / 2 - 1], O[0]);
+          O[1] = mfma16(vf[1], P[NT / 2 - 1], O[1]);
+          O[2] = mfma16(ones, P[NT / 2 - 1], O[2]);
+        }
+      };
+      // keys left at super-chunk SC: more than 96 take all 8 tiles (the
+      // staged length, a multiple of 64, then reaches 128 past kc)
+      auto run_sc = [&](auto sc_c) {
+        constexpr int SC = decltype(sc_c)::value;
+        const int rem = n - SC * 128;
+        if (rem <= 0) return;
+        if (rem > 96) super_chunk(sc_c, std::integral_constant<int, 8>{});
+        else if (rem > 64) super_chunk(sc_c, std::integral_constant<int, 6>{});
+        else if (rem > 32) super_chunk(sc_c, std::integral_constant<int, 4>{});
+        else super_chunk(sc_c, std::integral_constant<int, 2>{});
+      };
+      run_sc(std::integral_constant<int, 0>{});
+      run_sc(std::integral_constant<int, 1>{});
+      if constexpr (NMAX > 256) {
+        run_sc(std::integral_constant<int, 2>{});
+        run_sc(std::integral_constant<int, 3>{});
       }
       if (qvalid) {
         const float inv = 1.f / O[2][0];
@@ -527,12 +616,34 @@ hipError_t launch_attention(const nt_layout& L, int axis, int H, int D, const vo
   if (D == 32 && axis != 2 && L.max_len <= kAttnLongLen) {
     if (L.pattn_items() == 0) return hipSuccess;
     const int nmax = L.max_len <= kAttnShortLen ? kAttnShortLen : kAttnLongLen;
-    // bias rows: 8-byte fragment reads are conflict-free with a row stride of 2 (mod 4) dwords
-    const int bstride = nmax + 4;
+    const int64_t tiles = L.bias_tiles_total();
+    const uint2* img = nullptr;
+    if (bias && tiles > 0) {
+      // the layout's workspace holds the bias image (allocated on first use)
+      const size_t need = (size_t)H * (size_t)tiles * 512;
+      if (L.attn_ws_bytes < need) {
+        if (L.d_attn_ws) {
+          const hipError_t e = hipFree(L.d_attn_ws);
+          L.d_attn_ws = nullptr;
+          L.attn_ws_bytes = 0;
+          if (e != hipSuccess) return e;
+        }
+        const hipError_t e = hipMalloc(&L.d_attn_ws, need);
+        if (e != hipSuccess) {
+          L.d_attn_ws = nullptr;
+          return e;
+        }
+        L.attn_ws_bytes = need;
+      }
+      BiasImgArgs b{axis, L.batch, (const bf16*)bias, ld_bias, 1.f / scale, (uint2*)L.d_attn_ws, tiles,
+                    L.d_bias_tiles, L.d_cu_seqlens, L.d_cu_pairs};
+      bias_image_kernel<<<dim3((unsigned)((tiles + 3) / 4), (unsigned)H), dim3(256), 0, s>>>(b);
+      img = (const uint2*)L.d_attn_ws;
+    }
     PairAttnArgs a{axis, (const bf16*)q, (const bf16*)k, (const bf16*)v, ld_qkv, (const bf16*)bias, ld_bias,
-                   scale * kLog2e, (bf16*)o, ld_o, L.d_pattn_work, L.d_cu_seqlens, L.d_cu_pairs, bstride,
-                   1.f / scale, H};
-    const size_t smem = sizeof(bf16) * std::max((size_t)kAttnQB * bstride, 4 * (size_t)nmax * 32);
+                   scale * kLog2e, (bf16*)o, ld_o, L.d_pattn_work, L.d_cu_seqlens, L.d_cu_pairs, H,
+                   img, tiles * 64, L.d_bias_tiles};
+    const size_t smem = sizeof(bf16) * 4 * (size_t)nmax * 32;
     const dim3 grid((unsigned)(L.pattn_items() * H));
     const void* fn = nmax == kAttnShortLen ? (const void*)attention_pair_kernel<kAttnShortLen>
                                           : (const void*)attention_pair_kernel<kAttnLongLen>;

@@ -1224,9 +1224,10 @@ __global__ void __launch_bounds__(256) swiglu_kernel(SwiArgs p) {
 //   * A chunk's weights -- gate and up rows, and the matching 32 columns of
 //     the down projection -- are copied straight from global memory into LDS
 //     as fragment images (global_load_lds: lane l's 16 bytes land at byte
-//     16 l, exactly the order the matrix cores consume), three buffers deep,
-//     so the copies of the next two chunks run under the current one and
-//     every LDS read is one conflict-free 1 KB wave read.
+//     16 l, exactly the order the matrix cores consume), four buffers deep:
+//     a step reads two chunks (see the pipelined loop below) while the copies
+//     of the next two are in flight, and every LDS read is one
+//     conflict-free 1 KB wave read.
 //   * Hidden units are permuted inside a chunk: row r of the gate/up
 //     fragment ft is hidden unit 8 (r/4) + 4 ft + r%4, so a lane of k-group
 //     g ends up holding hidden units 8g .. 8g+7 of its row -- the B operand
@@ -1235,7 +1236,7 @@ __global__ void __launch_bounds__(256) swiglu_kernel(SwiArgs p) {
 constexpr int kTrThreads = 512;
 constexpr int kTrMT = 2;                          // 16-row subtiles per wave
 constexpr int kTrRows = 8 * 16 * kTrMT;           // rows per pass
-constexpr int kTrBufs = 3;                        // chunk buffers in LDS
+constexpr int kTrBufs = 4;                        // chunk buffers in LDS
 constexpr int kTrMaxHidden = 2048;                // largest hidden width (bias table size)
 
 template <int K>
@@ -1261,7 +1262,7 @@ __global__ void __launch_bounds__(kTrThreads, 1) transition_kernel(SwiArgs p) {
   float* s_g = s_b2 + N;                              // [K] LayerNorm gamma, then beta
   float* s_be = s_g + K;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l16 = lane & 15, g = lane >> 4;
   const int nch = p.F / 32;
   const int nrb = (p.rows + kTrRows - 1) / kTrRows;
@@ -1295,6 +1296,7 @@ __global__ void __launch_bounds__(kTrThreads, 1) transition_kernel(SwiArgs p) {
   __syncthreads();                                    // tables visible
   dma_chunk(0, 0);
   dma_chunk(1 % nch, 1);
+  dma_chunk(2 % nch, 2);
 
   bf16x8 xf[kTrMT][KT];
   f32x4 accY[NT][kTrMT];
@@ -1360,64 +1362,117 @@ __global__ void __launch_bounds__(kTrThreads, 1) transition_kernel(SwiArgs p) {
     __syncthreads();
 
     // ---- hidden chunks ----------------------------------------------------
-    for (int c = 0; c < nch; ++c, ++q) {
-      dma_chunk((c + 2) % nch, (q + 2) % kTrBufs);   // two chunks ahead, cycling into the next pass
-      const bf16* W = Wb + (q % kTrBufs) * CF * 512;
-      const int f0 = c * 32;
-      f32x4 accG[2][kTrMT], accU[2][kTrMT];
+    // Chunk c lives in ring slot q % kTrBufs; its copies are issued three
+    // chunks ahead.  The loop is software-pipelined: step c issues the gate
+    // and up products of chunk c + 1 first, then gates chunk c and runs its
+    // down projection, so the matrix cores work on the next chunk while the
+    // vector units evaluate SiLU.  At the last chunk of a pass the products
+    // "of chunk c + 1" use the next pass's first weights with this pass's
+    // rows and are discarded (keeping the step free of branches).
+    // gate and up biases of the chunk at hidden offset f0: slot j = 4 ft + i
+    // of lane group g is hidden unit f0 + 8g + j.  The reads come from inline
+    // assembly with their own wait: the compiler would otherwise wait for the
+    // weight copies in flight first.
+    auto read_bias = [&](int f0, float (&bg)[8], float (&bu)[8]) {
+      float4 bg0, bg1, bu0, bu1;
+      const uint32_t ag = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) float*)(&s_b[f0 + 8 * g]);
+      const uint32_t au = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) float*)(&s_b[p.F + f0 + 8 * g]);
+      asm volatile(
+          "ds_read_b128 %0, %4\n"
+          "ds_read_b128 %1, %4 offset:16\n"
+          "ds_read_b128 %2, %5\n"
+          "ds_read_b128 %3, %5 offset:16\n"
+          "s_waitcnt lgkmcnt(0)"
+          : "=&v"(bg0), "=&v"(bg1), "=&v"(bu0), "=&v"(bu1)
+          : "v"(ag), "v"(au)
+          : "memory");
+      bg[0] = bg0.x; bg[1] = bg0.y; bg[2] = bg0.z; bg[3] = bg0.w; bg[4] = bg1.x; bg[5] = bg1.y; bg[6] = bg1.z; bg[7] = bg1.w;
+      bu[0] = bu0.x; bu[1] = bu0.y; bu[2] = bu0.z; bu[3] = bu0.w; bu[4] = bu1.x; bu[5] = bu1.y; bu[6] = bu1.z; bu[7] = bu1.w;
+    };
+    // gate and up products of one chunk, accumulators seeded with the biases
+    auto seed = [&](const float (&bg)[8], const float (&bu)[8], f32x4 (&aG)[2][kTrMT], f32x4 (&aU)[2][kTrMT]) {
 #pragma unroll
       for (int ft = 0; ft < 2; ++ft)
 #pragma unroll
-        for (int mt = 0; mt < kTrMT; ++mt) { accG[ft][mt] = f32x4{0.f, 0.f, 0.f, 0.f}; accU[ft][mt] = accG[ft][mt]; }
-#pragma unroll
-      for (int kk = 0; kk < KT; ++kk)
-#pragma unroll
-        for (int ft = 0; ft < 2; ++ft) {
-          const bf16x8 ag = *reinterpret_cast<const bf16x8*>(&W[(ft * KT + kk) * 512 + lane * 8]);
-          const bf16x8 au = *reinterpret_cast<const bf16x8*>(&W[((2 + ft) * KT + kk) * 512 + lane * 8]);
-#pragma unroll
-          for (int mt = 0; mt < kTrMT; ++mt) {
-            accG[ft][mt] = mfma16(ag, xf[mt][kk], accG[ft][mt]);
-            accU[ft][mt] = mfma16(au, xf[mt][kk], accU[ft][mt]);
-          }
+        for (int mt = 0; mt < kTrMT; ++mt) {
+          aG[ft][mt] = f32x4{bg[4 * ft], bg[4 * ft + 1], bg[4 * ft + 2], bg[4 * ft + 3]};
+          aU[ft][mt] = f32x4{bu[4 * ft], bu[4 * ft + 1], bu[4 * ft + 2], bu[4 * ft + 3]};
         }
-      // slot j = 4 ft + i of lane group g holds hidden f0 + 8g + j.  The four
-      // bias reads come from inline assembly with their own wait: the
-      // compiler would otherwise wait for the weight copies in flight first.
-      float4 bg0, bg1, bu0, bu1;
-      {
-        const uint32_t ag = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) float*)(&s_b[f0 + 8 * g]);
-        const uint32_t au = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) float*)(&s_b[p.F + f0 + 8 * g]);
-        asm volatile(
-            "ds_read_b128 %0, %4\n"
-            "ds_read_b128 %1, %4 offset:16\n"
-            "ds_read_b128 %2, %5\n"
-            "ds_read_b128 %3, %5 offset:16\n"
-            "s_waitcnt lgkmcnt(0)"
-            : "=&v"(bg0), "=&v"(bg1), "=&v"(bu0), "=&v"(bu1)
-            : "v"(ag), "v"(au)
-            : "memory");
+    };
+    // gate/up fragments of product step st = 2 kk + ft
+    auto gu_frags = [&](const bf16* W, int st, bf16x8& ag, bf16x8& au) {
+      const int kk = st >> 1, ft = st & 1;
+      ag = *reinterpret_cast<const bf16x8*>(&W[(ft * KT + kk) * 512 + lane * 8]);
+      au = *reinterpret_cast<const bf16x8*>(&W[((2 + ft) * KT + kk) * 512 + lane * 8]);
+    };
+    auto gu_step = [&](int st, const bf16x8& ag, const bf16x8& au, f32x4 (&aG)[2][kTrMT], f32x4 (&aU)[2][kTrMT]) {
+      const int kk = st >> 1, ft = st & 1;
+#pragma unroll
+      for (int mt = 0; mt < kTrMT; ++mt) {
+        aG[ft][mt] = mfma16(ag, xf[mt][kk], aG[ft][mt]);
+        aU[ft][mt] = mfma16(au, xf[mt][kk], aU[ft][mt]);
       }
-      const float bgv[8] = {bg0.x, bg0.y, bg0.z, bg0.w, bg1.x, bg1.y, bg1.z, bg1.w};
-      const float buv[8] = {bu0.x, bu0.y, bu0.z, bu0.w, bu1.x, bu1.y, bu1.z, bu1.w};
+    };
+    f32x4 accG[2][kTrMT], accU[2][kTrMT];
+    {
+      float bg[8], bu[8];
+      read_bias(0, bg, bu);
+      seed(bg, bu, accG, accU);
+      const bf16* W0 = Wb + (q % kTrBufs) * CF * 512;
+#pragma unroll
+      for (int st = 0; st < 2 * KT; ++st) {
+        bf16x8 ag, au;
+        gu_frags(W0, st, ag, au);
+        gu_step(st, ag, au, accG, accU);
+      }
+    }
+    constexpr int NSTEP = 2 * KT;                       // gate/up product steps per chunk
+    constexpr int EPS = 8 * kTrMT / NSTEP;              // gated values per step
+    static_assert(EPS * NSTEP == 8 * kTrMT, "gating must split evenly over the product steps");
+    for (int c = 0; c < nch; ++c, ++q) {
+      dma_chunk((c + 3) % nch, (q + 3) % kTrBufs);   // three chunks ahead, cycling into the next pass
+      const bf16* W = Wb + (q % kTrBufs) * CF * 512;
+      const bf16* Wn = Wb + ((q + 1) % kTrBufs) * CF * 512;
+      float bg[8], bu[8];
+      read_bias(((c + 1) % nch) * 32, bg, bu);
+      f32x4 nG[2][kTrMT], nU[2][kTrMT];
+      seed(bg, bu, nG, nU);
+      // Step st: the products of chunk c + 1 for step st (fragments read one
+      // step ahead), then EPS gated values of chunk c -- so SiLU runs on the
+      // vector units while the products occupy the matrix cores.  The
+      // scheduling barriers keep that order.  Gated value e = 8 mt + j (slot
+      // j = 4 ft + i of lane group g: hidden unit 32 c + 8g + j).
       bf16x8 hv[kTrMT];
+      bf16x8 ag, au;
+      gu_frags(Wn, 0, ag, au);
 #pragma unroll
-      for (int mt = 0; mt < kTrMT; ++mt)
+      for (int st = 0; st < NSTEP; ++st) {
+        bf16x8 agn, aun;
+        if (st + 1 < NSTEP) gu_frags(Wn, st + 1, agn, aun);
+        gu_step(st, ag, au, nG, nU);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const float gv = accG[j >> 2][mt][j & 3] + bgv[j];
-          const float uv = accU[j >> 2][mt][j & 3] + buv[j];
+        for (int u = 0; u < EPS; ++u) {
+          const int e = st * EPS + u, mt = e >> 3, j = e & 7;
+          const float gv = accG[j >> 2][mt][j & 3];
+          const float uv = accU[j >> 2][mt][j & 3];
           hv[mt][j] = (bf16)(gv * __builtin_amdgcn_rcpf(1.f + __expf(-gv)) * uv);
         }
+        if (st + 1 < NSTEP) { ag = agn; au = aun; }
+        __builtin_amdgcn_sched_barrier(0);
+      }
 #pragma unroll
       for (int a = 0; a < NT; ++a) {
         const bf16x8 ad = *reinterpret_cast<const bf16x8*>(&W[(4 * KT + a) * 512 + lane * 8]);
 #pragma unroll
         for (int mt = 0; mt < kTrMT; ++mt) accY[a][mt] = mfma16(ad, hv[mt], accY[a][mt]);
       }
-      // the next chunk's images (issued a step ago) must have landed in
-      // every wave before any wave reads them; this chunk's buffer is then
-      // free for the copy issued at the next step
+#pragma unroll
+      for (int ft = 0; ft < 2; ++ft)
+#pragma unroll
+        for (int mt = 0; mt < kTrMT; ++mt) { accG[ft][mt] = nG[ft][mt]; accU[ft][mt] = nU[ft][mt]; }
+      // chunk c + 2 (copied a step ago) must have landed in every wave
+      // before the next step reads it as "chunk c + 1"; after the barrier
+      // this chunk's slot is free for the copy issued at the next step
       if (K == 128 && c + 1 < nch) __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8) | DMA_PER_WAVE);  // vmcnt(3)
       else __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();

@@ -148,6 +148,15 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L) {
     }
     L->pattn_work = xcd_order<4>(items, cost, false);
   }
+  // pair attention bias image: per sample, one 512-byte tile per (16-query
+  // tile, 16-key tile) up to the 64-key padded length
+  L->bias_tiles.assign(batch + 1, 0);
+  for (int32_t i = 0; i < batch; ++i) {
+    const int64_t n = lengths[i];
+    const int64_t t = L->bias_tiles[i] + (n + 15) / 16 * ((n + 63) / 64 * 4);
+    if (t > INT32_MAX) return fail(NT_ERR_OVERFLOW, "bias image extent exceeds int32 at sample " + std::to_string(i));
+    L->bias_tiles[i + 1] = (int32_t)t;
+  }
   // triangle: one item per (sample, 32x32 output tile), largest samples first.
   // The channel blocks, not the tiles, are spread over the XCDs (the launch
   // interleaves every tile's channel blocks), so each XCD walks the whole list
