@@ -3,25 +3,27 @@
 // sample's N_i x N_i channel planes, then z[cell(x,y), c] += T_c[x, y].
 //
 // Operands arrive pair-tiled (every 16 x 32 fragment stored in lane order),
-// so each matrix-core fragment is one contiguous 1 KB wave load.  A workgroup
-// owns a 32x32 cell tile of one sample and a block of 16 channels (4 per
-// wave).  Workgroup ids interleave the channel blocks of each tile, so with 8
-// blocks (C = 128) XCD x (ids = x mod 8) always works on channel block x: it
-// walks the tile list sample by sample and keeps the current sample's 16
-// channel planes (about 3 MB at N = 216) in its own L2, where the operand
-// re-reads of neighbouring tiles hit.  The next k-step's fragments load while
-// the current one is on the matrix cores.  The finished tile goes through LDS
-// so that z is updated in 32-byte pieces (16 channels of one cell) instead of
-// the 8-byte pieces a single wave holds.
+// so each matrix-core fragment is one contiguous 1 KB wave load.  The kernel
+// is bound by the vector-memory path that carries those loads, so a wave
+// keeps a whole 64 x 64 cell tile of one channel in registers: each k-step
+// loads 4 + 4 fragments for 16 products (half a load per product).  A
+// workgroup of 16 waves owns the tile for a block of 16 channels, and the
+// finished tile goes through LDS in four bands of 16 rows so that z is
+// updated in 32-byte pieces (16 channels of a cell).  The four channel blocks
+// that share one 128-byte line of z (64 channels) run back to back on the
+// same XCD, so each z line is fetched into one L2 once instead of into four;
+// this outweighs keeping a sample's operand planes in one L2 (re-reads of
+// neighbouring tiles then come from the memory-side cache).
 #include "nt_device.h"
 #include "nt_internal.h"
 
 namespace nt {
 namespace {
 
-constexpr int kTriCB = 16;    // channels per workgroup
-constexpr int kTriCW = 4;     // channels per wave
-constexpr int kTriSC = 20;    // LDS floats per staged cell (16 channels + 4: conflict-free 16-byte writes)
+constexpr int kTriCB = 16;         // channels per workgroup (one per wave)
+constexpr int kTriThreads = 64 * kTriCB;
+constexpr int kTriSC = 20;         // LDS floats per staged cell (16 channels + 4)
+constexpr int kTriRS = kTriTile + 1;  // staged cells per band row: the 4 lane groups of a write hit different banks
 
 struct TriArgs {
   int C, nblk;
@@ -34,12 +36,18 @@ struct TriArgs {
   const int32_t* cu_seqlens;
   const int32_t* cu_pairs;
   const int32_t* cu_pad;
+  int items, groups;     // tiles, and line groups of four channel blocks
 };
 
-__global__ void __launch_bounds__(256, 2) triangle_mfma_kernel(TriArgs p) {
-  __shared__ __attribute__((aligned(16))) float stage[kTriTile * kTriTile * kTriSC];
+__global__ void __launch_bounds__(kTriThreads, 1) triangle_mfma_kernel(TriArgs p) {
+  __shared__ __attribute__((aligned(16))) float stage[16 * kTriRS * kTriSC];
+  // Workgroup id = 8 (4 k + j) + x runs on XCD x: its k-th (tile, line group)
+  // pair q = 8 k + x, channel block j of that group.
   const int id = blockIdx.x;
-  const int item = id / p.nblk, cb = id % p.nblk;
+  const int xcd = id % kXcds, k = id / kXcds;
+  const int q = (k >> 2) * kXcds + xcd;
+  const int item = q / p.groups, cb = (q % p.groups) * 4 + (k & 3);
+  if (item >= p.items || cb >= p.nblk) return;
   const int i = p.work[4 * item];
   if (i < 0) return;
   const int xt = p.work[4 * item + 1], yt = p.work[4 * item + 2];
@@ -47,97 +55,76 @@ __global__ void __launch_bounds__(256, 2) triangle_mfma_kernel(TriArgs p) {
   const int nkt = (n + 31) >> 5;
   const int64_t P = p.cu_pad[i], cu = p.cu_pairs[i];
   const int x0 = xt * kTriTile, y0 = yt * kTriTile;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l16 = lane & 15, g = lane >> 4;
-  const int c0 = cb * kTriCB + wave * kTriCW;
+  const int c = cb * kTriCB + wave;
 
   // row tiles of the output tile that hold rows of the sample (uniform)
-  const bool xv[2] = {x0 < n, x0 + 16 < n};
-  const bool yv[2] = {y0 < n, y0 + 16 < n};
-  const bf16* ap[kTriCW];
-  const bf16* bp[kTriCW];
+  bool xv[4], yv[4];
 #pragma unroll
-  for (int ch = 0; ch < kTriCW; ++ch) {
-    ap[ch] = p.a + (int64_t)(c0 + ch) * p.ld_ab + P + lane * 8;
-    bp[ch] = p.b + (int64_t)(c0 + ch) * p.ld_ab + P + lane * 8;
-  }
-  f32x4 acc[kTriCW][2][2];
+  for (int s = 0; s < 4; ++s) { xv[s] = x0 + 16 * s < n; yv[s] = y0 + 16 * s < n; }
+  const bf16* ap = p.a + (int64_t)c * p.ld_ab + P + lane * 8;
+  const bf16* bp = p.b + (int64_t)c * p.ld_ab + P + lane * 8;
+  f32x4 acc[4][4];
 #pragma unroll
-  for (int ch = 0; ch < kTriCW; ++ch)
+  for (int xs = 0; xs < 4; ++xs)
 #pragma unroll
-    for (int xs = 0; xs < 2; ++xs)
-#pragma unroll
-      for (int ys = 0; ys < 2; ++ys) acc[ch][xs][ys] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int ys = 0; ys < 4; ++ys) acc[xs][ys] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // Fragments of k-step kt: tile (row tile, kt) of each channel plane.  Row
-  // tiles past the sample read as zero without a load; k past N is zeroed in
-  // the last step (rows past N inside a row tile only reach discarded cells).
-  bf16x8 fa[kTriCW][2], fb[kTriCW][2];
-  auto load_step = [&](int kt, bf16x8 (&ra)[kTriCW][2], bf16x8 (&rb)[kTriCW][2]) {
-    const bool any = kt < nkt;
-    const int kbase = kt * 32 + 8 * g;
-#pragma unroll
-    for (int ch = 0; ch < kTriCW; ++ch)
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int64_t ta = ((int64_t)((x0 >> 4) + h) * nkt + kt) << 9;
-        const int64_t tb = ((int64_t)((y0 >> 4) + h) * nkt + kt) << 9;
-        ra[ch][h] = (any && xv[h]) ? *reinterpret_cast<const bf16x8*>(ap[ch] + ta) : bf16x8{};
-        rb[ch][h] = (any && yv[h]) ? *reinterpret_cast<const bf16x8*>(bp[ch] + tb) : bf16x8{};
-      }
-    if (any && kbase + 8 > n) {
-#pragma unroll
-      for (int ch = 0; ch < kTriCW; ++ch)
-#pragma unroll
-        for (int h = 0; h < 2; ++h)
-#pragma unroll
-          for (int j = 0; j < 8; ++j)
-            if (kbase + j >= n) { ra[ch][h][j] = (bf16)0.f; rb[ch][h][j] = (bf16)0.f; }
-    }
-  };
-  load_step(0, fa, fb);
+  // k-step kt: fragment (row tile, kt) of each plane.  Row tiles past the
+  // sample read as zero without a load; k past N is zeroed in the last step
+  // (rows past N inside a row tile only reach discarded cells).
   for (int kt = 0; kt < nkt; ++kt) {
-    bf16x8 na[kTriCW][2], nb[kTriCW][2];
-    load_step(kt + 1, na, nb);              // all-zero without a load past the last step
+    bf16x8 fa[4], fb[4];
 #pragma unroll
-    for (int ch = 0; ch < kTriCW; ++ch)
+    for (int s = 0; s < 4; ++s) {
+      const int64_t ta = ((int64_t)((x0 >> 4) + s) * nkt + kt) << 9;
+      const int64_t tb = ((int64_t)((y0 >> 4) + s) * nkt + kt) << 9;
+      fa[s] = xv[s] ? *reinterpret_cast<const bf16x8*>(ap + ta) : bf16x8{};
+      fb[s] = yv[s] ? *reinterpret_cast<const bf16x8*>(bp + tb) : bf16x8{};
+    }
+    const int kbase = kt * 32 + 8 * g;
+    if (kbase + 8 > n) {
 #pragma unroll
-      for (int xs = 0; xs < 2; ++xs)
+      for (int s = 0; s < 4; ++s)
 #pragma unroll
-        for (int ys = 0; ys < 2; ++ys) acc[ch][xs][ys] = mfma16(fa[ch][xs], fb[ch][ys], acc[ch][xs][ys]);
+        for (int j = 0; j < 8; ++j)
+          if (kbase + j >= n) { fa[s][j] = (bf16)0.f; fb[s][j] = (bf16)0.f; }
+    }
 #pragma unroll
-    for (int ch = 0; ch < kTriCW; ++ch)
+    for (int xs = 0; xs < 4; ++xs)
 #pragma unroll
-      for (int h = 0; h < 2; ++h) { fa[ch][h] = na[ch][h]; fb[ch][h] = nb[ch][h]; }
+      for (int ys = 0; ys < 4; ++ys) acc[xs][ys] = mfma16(fa[xs], fb[ys], acc[xs][ys]);
   }
 
-  // acc[ch][xs][ys][r] = T_{c0+ch}[x0 + 16xs + 4g + r][y0 + 16ys + l16]; stage
-  // the tile as [cell][16 channels] fp32
+  // acc[xs][ys][r] = T_c[x0 + 16xs + 4g + r][y0 + 16ys + l16].  Band xs:
+  // stage its 16 x 64 cells as [cell][16 channels] fp32, then two threads
+  // per cell add 8 channels (16 bytes) each into z.
 #pragma unroll
-  for (int xs = 0; xs < 2; ++xs)
+  for (int xs = 0; xs < 4; ++xs) {
+    if (!xv[xs]) break;                               // uniform
 #pragma unroll
-    for (int ys = 0; ys < 2; ++ys)
+    for (int ys = 0; ys < 4; ++ys)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int cell = (16 * xs + 4 * g + r) * kTriTile + 16 * ys + l16;
-        *reinterpret_cast<float4*>(&stage[cell * kTriSC + wave * kTriCW]) =
-            make_float4(acc[0][xs][ys][r], acc[1][xs][ys][r], acc[2][xs][ys][r], acc[3][xs][ys][r]);
-      }
-  __syncthreads();
-  // z += T: two threads per cell, 8 channels (16 bytes) each
+      for (int r = 0; r < 4; ++r) stage[((4 * g + r) * kTriRS + 16 * ys + l16) * kTriSC + wave] = acc[xs][ys][r];
+    __syncthreads();
 #pragma unroll
-  for (int it = 0; it < kTriTile * kTriTile * 2 / 256; ++it) {
-    const int u = it * 256 + tid, cell = u >> 1, half = u & 1;
-    const int x = x0 + cell / kTriTile, y = y0 + cell % kTriTile;
-    if (x >= n || y >= n) continue;
-    const float4 t0 = *reinterpret_cast<const float4*>(&stage[cell * kTriSC + half * 8]);
-    const float4 t1 = *reinterpret_cast<const float4*>(&stage[cell * kTriSC + half * 8 + 4]);
-    bf16* zp = p.z + (cu + (int64_t)x * n + y) * p.ld_z + cb * kTriCB + half * 8;
-    Vec<bf16> zz;
-    zz.load(zp);
-    zz.v[0] += t0.x; zz.v[1] += t0.y; zz.v[2] += t0.z; zz.v[3] += t0.w;
-    zz.v[4] += t1.x; zz.v[5] += t1.y; zz.v[6] += t1.z; zz.v[7] += t1.w;
-    zz.store(zp);
+    for (int it = 0; it < 16 * kTriTile * 2 / kTriThreads; ++it) {
+      const int u = it * kTriThreads + tid, cell = u >> 1, half = u & 1;
+      const int row = cell / kTriTile, col = cell % kTriTile;
+      const int x = x0 + 16 * xs + row, y = y0 + col;
+      if (x >= n || y >= n) continue;
+      const float* st = &stage[(row * kTriRS + col) * kTriSC + half * 8];
+      const float4 t0 = *reinterpret_cast<const float4*>(st);
+      const float4 t1 = *reinterpret_cast<const float4*>(st + 4);
+      bf16* zp = p.z + (cu + (int64_t)x * n + y) * p.ld_z + cb * kTriCB + half * 8;
+      Vec<bf16> zz;
+      zz.load(zp);
+      zz.v[0] += t0.x; zz.v[1] += t0.y; zz.v[2] += t0.z; zz.v[3] += t0.w;
+      zz.v[4] += t1.x; zz.v[5] += t1.y; zz.v[6] += t1.z; zz.v[7] += t1.w;
+      zz.store(zp);
+    }
+    __syncthreads();
   }
 }
 
@@ -189,10 +176,11 @@ hipError_t launch_triangle(const nt_layout& L, int C, const void* a, const void*
     triangle_f32_kernel<<<dim3((unsigned)items), dim3(256), 0, s>>>(t);
     return hipGetLastError();
   }
-  const int nblk = C / kTriCB;
+  const int nblk = C / kTriCB, groups = (nblk + 3) / 4;
   TriArgs t{C, nblk, (const bf16*)a, (const bf16*)b, ld_ab, (bf16*)z, ld_z, L.d_tri_work, L.d_cu_seqlens,
-            L.d_cu_pairs, L.d_cu_pad};
-  triangle_mfma_kernel<<<dim3((unsigned)(items * nblk)), dim3(256), 0, s>>>(t);
+            L.d_cu_pairs, L.d_cu_pad, (int)items, groups};
+  const int64_t pairs = (items * groups + kXcds - 1) / kXcds * kXcds;   // (tile, line group) pairs, padded
+  triangle_mfma_kernel<<<dim3((unsigned)(pairs * 4)), dim3(kTriThreads), 0, s>>>(t);
   return hipGetLastError();
 }
 

@@ -157,11 +157,9 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L) {
     if (t > INT32_MAX) return fail(NT_ERR_OVERFLOW, "bias image extent exceeds int32 at sample " + std::to_string(i));
     L->bias_tiles[i + 1] = (int32_t)t;
   }
-  // triangle: one item per (sample, 32x32 output tile), largest samples first.
-  // The channel blocks, not the tiles, are spread over the XCDs (the launch
-  // interleaves every tile's channel blocks), so each XCD walks the whole list
-  // for its own channels and holds one sample's channel planes in its L2 at a
-  // time; the list is padded to a multiple of 8 with idle items.
+  // triangle: one item per (sample, 64x64 output tile), largest samples first
+  // (the launch spreads (tile, group of channel blocks) pairs over the XCDs);
+  // the list is padded to a multiple of 8 with idle items.
   {
     std::vector<int32_t> order(batch);
     std::iota(order.begin(), order.end(), 0);

@@ -13,7 +13,7 @@
 namespace nt {
 
 constexpr int kXcds = 8;          // MI355X: 8 XCDs, workgroups dispatched round-robin
-constexpr int kTriTile = 32;      // triangle output tile: 32 x 32 cells
+constexpr int kTriTile = 64;      // triangle output tile: 64 x 64 cells
 constexpr int kSeqQBlock = 64;    // 1-D attention: queries per workgroup
 constexpr int kLinRows = 128;     // rows per projection workgroup (pair-row table granularity)
 constexpr int kAttnQB = 128;      // pair attention (head_dim 32): queries per workgroup (8 waves x 16)

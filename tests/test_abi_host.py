@@ -67,7 +67,7 @@ def test_work_maps_cover_each_item_once(L):
     tri = lay.host_array("tri_work").reshape(-1, 4)
     assert len(tri) % 8 == 0
     got = sorted(map(tuple, tri[tri[:, 0] >= 0, :3].tolist()))
-    T = 32
+    T = 64
     assert got == sorted((i, x, y) for i, n in enumerate(L) for x in range(-(-n // T)) for y in range(-(-n // T)))
     seq = lay.host_array("seq_work").reshape(-1, 2)
     got = sorted(map(tuple, seq[seq[:, 0] >= 0].tolist()))
