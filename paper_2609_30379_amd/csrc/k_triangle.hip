@@ -99,7 +99,25 @@ __global__ void __launch_bounds__(kTriThreads, 1) triangle_mfma_kernel(TriArgs p
 
   // acc[xs][ys][r] = T_c[x0 + 16xs + 4g + r][y0 + 16ys + l16].  Band xs:
   // stage its 16 x 64 cells as [cell][16 channels] fp32, then two threads
-  // per cell add 8 channels (16 bytes) each into z.
+  // per cell add 8 channels (16 bytes) each into z.  The z values of the next
+  // band are loaded while the current band is staged and written.
+  constexpr int kIt = 16 * kTriTile * 2 / kTriThreads;     // (cell, half) items per thread and band
+  auto z_ptr = [&](int xs, int it, bool& ok) {
+    const int u = it * kTriThreads + tid, cell = u >> 1, half = u & 1;
+    const int x = x0 + 16 * xs + cell / kTriTile, y = y0 + cell % kTriTile;
+    ok = x < n && y < n;
+    return p.z + (cu + (int64_t)x * n + y) * p.ld_z + cb * kTriCB + half * 8;
+  };
+  uint4 zr[kIt];
+  auto z_load = [&](int xs) {
+#pragma unroll
+    for (int it = 0; it < kIt; ++it) {
+      bool ok;
+      const bf16* zp = z_ptr(xs, it, ok);
+      zr[it] = ok ? *reinterpret_cast<const uint4*>(zp) : make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
+  z_load(0);
 #pragma unroll
   for (int xs = 0; xs < 4; ++xs) {
     if (!xv[xs]) break;                               // uniform
@@ -108,21 +126,33 @@ __global__ void __launch_bounds__(kTriThreads, 1) triangle_mfma_kernel(TriArgs p
 #pragma unroll
       for (int r = 0; r < 4; ++r) stage[((4 * g + r) * kTriRS + 16 * ys + l16) * kTriSC + wave] = acc[xs][ys][r];
     __syncthreads();
+    uint4 cur[kIt];
 #pragma unroll
-    for (int it = 0; it < 16 * kTriTile * 2 / kTriThreads; ++it) {
+    for (int it = 0; it < kIt; ++it) cur[it] = zr[it];
+    if (xs + 1 < 4 && xv[xs + 1]) z_load(xs + 1);
+#pragma unroll
+    for (int it = 0; it < kIt; ++it) {
       const int u = it * kTriThreads + tid, cell = u >> 1, half = u & 1;
       const int row = cell / kTriTile, col = cell % kTriTile;
-      const int x = x0 + 16 * xs + row, y = y0 + col;
-      if (x >= n || y >= n) continue;
+      bool ok;
+      bf16* zp = z_ptr(xs, it, ok);
+      if (!ok) continue;
       const float* st = &stage[(row * kTriRS + col) * kTriSC + half * 8];
       const float4 t0 = *reinterpret_cast<const float4*>(st);
       const float4 t1 = *reinterpret_cast<const float4*>(st + 4);
-      bf16* zp = p.z + (cu + (int64_t)x * n + y) * p.ld_z + cb * kTriCB + half * 8;
-      Vec<bf16> zz;
-      zz.load(zp);
-      zz.v[0] += t0.x; zz.v[1] += t0.y; zz.v[2] += t0.z; zz.v[3] += t0.w;
-      zz.v[4] += t1.x; zz.v[5] += t1.y; zz.v[6] += t1.z; zz.v[7] += t1.w;
-      zz.store(zp);
+      const uint32_t w4[4] = {cur[it].x, cur[it].y, cur[it].z, cur[it].w};
+      float v[8];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        v[2 * j] = __uint_as_float(w4[j] << 16);
+        v[2 * j + 1] = __uint_as_float(w4[j] & 0xffff0000u);
+      }
+      v[0] += t0.x; v[1] += t0.y; v[2] += t0.z; v[3] += t0.w;
+      v[4] += t1.x; v[5] += t1.y; v[6] += t1.z; v[7] += t1.w;
+      bf16x8 o;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = (bf16)v[e];
+      *reinterpret_cast<bf16x8*>(zp) = o;
     }
     __syncthreads();
   }
