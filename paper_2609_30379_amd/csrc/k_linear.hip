@@ -859,6 +859,215 @@ __global__ void __launch_bounds__(kStreamThreads, 2) linear_stream_kernel(LinArg
   }
 }
 
+// ---------------------------------------------------------------- wave-streamed
+// Projection for bf16 rows, K in {64, 128}, a row-major main output and an
+// optional channel-major tail, with no workgroup barrier after set-up: the
+// weights of all output columns sit in LDS as matrix-core fragment images
+// (copied once per workgroup), and every wave streams its own 16-row tiles
+// -- rows loaded straight into B-fragment order three tiles ahead,
+// LayerNorm in registers (a row's K values are spread over the four lanes
+// l16 + 16 g, two lane swaps per statistic), the products over groups of 8
+// column tiles, and a write-back through a wave-private LDS stage so that
+// global stores are row-contiguous 16-byte pieces.  Waves of one CU thus
+// never wait for each other; per tile a wave reads the weights from LDS once
+// per 16 rows.
+constexpr int kWaveThreads = 512;
+constexpr int kWavePF = 3;                        // tiles in flight per wave
+constexpr int kWaveGroup = 8;                     // column tiles per product group (128 columns)
+
+template <int EPI> constexpr int wave_stage_stride() { return EPI == NT_EPI_RESIDUAL ? 132 : 144; }
+template <int EPI> constexpr int wave_stage_bytes() {
+  return 16 * wave_stage_stride<EPI>() * (EPI == NT_EPI_RESIDUAL ? 4 : 2);
+}
+template <int K, int EPI> size_t wave_smem_bytes(int nt16) {
+  return (size_t)nt16 * (K / 32) * 1024 + (size_t)nt16 * 16 * 4 + 2 * (size_t)K * 4 +
+         (size_t)(kWaveThreads / 64) * wave_stage_bytes<EPI>();
+}
+
+template <int EPI, int K>
+__global__ void __launch_bounds__(kWaveThreads, 1) linear_wave_kernel(LinArgs p) {
+  constexpr int KT = K / 32;
+  constexpr bool RES = EPI == NT_EPI_RESIDUAL;
+  constexpr int SS = wave_stage_stride<EPI>();
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
+  const int nt16 = (p.N + 15) >> 4;
+  bf16* Wimg = reinterpret_cast<bf16*>(smem_raw);                         // [nt16][KT] fragment images
+  float* s_bias = reinterpret_cast<float*>(smem_raw + (size_t)nt16 * KT * 1024);
+  float* s_gamma = s_bias + nt16 * 16;
+  float* s_beta = s_gamma + K;
+  unsigned char* stage_base = reinterpret_cast<unsigned char*>(s_beta + K);
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l16 = lane & 15, g = lane >> 4;
+  const bf16* x = static_cast<const bf16*>(p.x);
+
+  // ---- set-up: weight images (rows past N repeat row N-1; their channels
+  // are never stored), bias, LayerNorm affine
+  for (int im = wave; im < nt16 * KT; im += kWaveThreads / 64) {
+    const int ct = im / KT, kk = im % KT;
+    const int n = min(ct * 16 + l16, p.N - 1);
+    const bf16* src = p.w + (int64_t)n * K + kk * 32 + g * 8;
+    __builtin_amdgcn_global_load_lds((const void*)src, (__attribute__((address_space(3))) void*)(Wimg + im * 512), 16, 0, 0);
+  }
+  for (int j = tid; j < nt16 * 16; j += kWaveThreads) s_bias[j] = (p.bias && j < p.N) ? p.bias[j] : 0.f;
+  for (int j = tid; j < K; j += kWaveThreads) {
+    s_gamma[j] = p.gamma ? p.gamma[j] : 1.f;
+    s_beta[j] = p.beta ? p.beta[j] : 0.f;
+  }
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+
+  const int ntile = (p.rows + 15) >> 4;
+  const int wid = (int)blockIdx.x * (kWaveThreads / 64) + wave;
+  const int nw = (int)gridDim.x * (kWaveThreads / 64);
+  unsigned char* stage = stage_base + (size_t)wave * wave_stage_bytes<EPI>();
+  const int c8n = p.n_main / 8;                   // 16-byte chunks per output row
+
+  // rows of tile t in B-fragment order: lane (l16, g) holds row 16t + l16,
+  // k = 32 kk + 8 g .. +7; residual rows in write-back order (4 chunks a lane)
+  auto load_tile = [&](int t, uint4 (&xr)[KT], uint4 (&rr)[4]) {
+    const int m = t * 16 + l16;
+    const bool ok = t < ntile && m < p.rows;
+#pragma unroll
+    for (int kk = 0; kk < KT; ++kk)
+      xr[kk] = ok ? *reinterpret_cast<const uint4*>(x + (int64_t)m * p.ldx + kk * 32 + g * 8) : make_uint4(0u, 0u, 0u, 0u);
+    if constexpr (RES) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int row = q * 4 + (lane >> 4), cc = lane & 15, mm = t * 16 + row;
+        rr[q] = (t < ntile && mm < p.rows && cc < c8n) ? *reinterpret_cast<const uint4*>(p.res + (int64_t)mm * p.ld_res + cc * 8)
+                                                      : make_uint4(0u, 0u, 0u, 0u);
+      }
+    }
+  };
+
+  auto process = [&](int t, const uint4 (&xr)[KT], const uint4 (&rr)[4]) {
+    const int m = t * 16 + l16;
+    // ---- LayerNorm (or plain conversion) into B fragments
+    bf16x8 xb[KT];
+    if (p.gamma) {
+      float v[KT][8];
+#pragma unroll
+      for (int kk = 0; kk < KT; ++kk) XStage<bf16>::unpack(xr[kk], v[kk]);
+      float s = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < KT; ++kk)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s += v[kk][e];
+      s += __shfl_xor(s, 16, 64);
+      s += __shfl_xor(s, 32, 64);
+      const float mean = s / (float)K;
+      float q = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < KT; ++kk)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) { const float d = v[kk][e] - mean; q += d * d; }
+      q += __shfl_xor(q, 16, 64);
+      q += __shfl_xor(q, 32, 64);
+      const float rstd = rsqrtf(q / (float)K + p.eps);
+#pragma unroll
+      for (int kk = 0; kk < KT; ++kk) {
+        const int k0 = kk * 32 + g * 8;
+        const float4 g0 = *reinterpret_cast<const float4*>(&s_gamma[k0]), g1 = *reinterpret_cast<const float4*>(&s_gamma[k0 + 4]);
+        const float4 b0 = *reinterpret_cast<const float4*>(&s_beta[k0]), b1 = *reinterpret_cast<const float4*>(&s_beta[k0 + 4]);
+        const float gg[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+        const float bb[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) xb[kk][e] = (bf16)(m < p.rows ? (v[kk][e] - mean) * rstd * gg[e] + bb[e] : 0.f);
+      }
+    } else {
+#pragma unroll
+      for (int kk = 0; kk < KT; ++kk) xb[kk] = __builtin_bit_cast(bf16x8, xr[kk]);
+    }
+    // ---- main columns, group by group of 8 column tiles
+    const int nmt = (p.n_main + 15) >> 4;
+    for (int cg = 0; cg * kWaveGroup < nmt; ++cg) {
+      f32x4 acc[kWaveGroup];
+#pragma unroll
+      for (int j = 0; j < kWaveGroup; ++j) {
+        const int ct = cg * kWaveGroup + j;
+        if (ct >= nmt) break;
+        acc[j] = *reinterpret_cast<const f32x4*>(&s_bias[ct * 16 + 4 * g]);
+#pragma unroll
+        for (int kk = 0; kk < KT; ++kk)
+          acc[j] = mfma16(*reinterpret_cast<const bf16x8*>(&Wimg[(ct * KT + kk) * 512 + lane * 8]), xb[kk], acc[j]);
+        if (j & 1) __builtin_amdgcn_sched_barrier(0);   // two column tiles of weight fragments in flight
+      }
+      // acc[j][i]: channel 16 ct + 4g + i of row m, staged
+#pragma unroll
+      for (int j = 0; j < kWaveGroup; ++j) {
+        const int ct = cg * kWaveGroup + j;
+        if (ct >= nmt) break;
+        const int n = ct * 16 + 4 * g;
+        if (n >= p.n_main) continue;              // n_main % 8 == 0: all four are main channels
+        float r[4] = {acc[j][0], acc[j][1], acc[j][2], acc[j][3]};
+        if constexpr (EPI == NT_EPI_GELU) {
+#pragma unroll
+          for (int ii = 0; ii < 4; ++ii) r[ii] = gelu_erf(r[ii]);
+        }
+        if constexpr (RES) *reinterpret_cast<float4*>(stage + (size_t)(l16 * SS + j * 16 + 4 * g) * 4) = make_float4(r[0], r[1], r[2], r[3]);
+        else {
+          bf16x4 o;
+#pragma unroll
+          for (int ii = 0; ii < 4; ++ii) o[ii] = (bf16)r[ii];
+          *reinterpret_cast<bf16x4*>(stage + (size_t)(l16 * SS + j * 16 + 4 * g) * 2) = o;
+        }
+      }
+      // write-back of the group's main columns: lane L, pass q -> row
+      // 4q + L/16, 8 columns from 8 (L % 16); four rows per store instruction
+      const int cc = lane & 15, col = cg * 128 + cc * 8;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int row = q * 4 + (lane >> 4), mm = t * 16 + row;
+        if (col >= p.n_main || mm >= p.rows) continue;
+        bf16x8 o;
+        if constexpr (RES) {
+          const float* sf = reinterpret_cast<const float*>(stage) + row * SS + cc * 8;
+          const float4 a0 = *reinterpret_cast<const float4*>(sf), a1 = *reinterpret_cast<const float4*>(sf + 4);
+          const float av[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+          float rv[8];
+          XStage<bf16>::unpack(rr[q], rv);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] = (bf16)(av[e] + rv[e]);
+        } else {
+          o = *reinterpret_cast<const bf16x8*>(stage + (size_t)(row * SS + cc * 8) * 2);
+        }
+        *reinterpret_cast<bf16x8*>(p.y + (int64_t)mm * p.ldy + col) = o;
+      }
+    }
+    // ---- tail columns (channel-major planes), column tile by column tile
+    if (p.y_tail) {
+      for (int ct = p.n_main >> 4; ct < nt16; ++ct) {
+        f32x4 acc = *reinterpret_cast<const f32x4*>(&s_bias[ct * 16 + 4 * g]);
+#pragma unroll
+        for (int kk = 0; kk < KT; ++kk)
+          acc = mfma16(*reinterpret_cast<const bf16x8*>(&Wimg[(ct * KT + kk) * 512 + lane * 8]), xb[kk], acc);
+        if (m >= p.rows) continue;
+#pragma unroll
+        for (int ii = 0; ii < 4; ++ii) {
+          const int nn = ct * 16 + 4 * g + ii;
+          float r = acc[ii];
+          if constexpr (EPI == NT_EPI_GELU) r = gelu_erf(r);
+          if (nn >= p.n_main && nn < p.N) p.y_tail[(int64_t)(nn - p.n_main) * p.ld_tail + m] = (bf16)r;
+        }
+      }
+    }
+  };
+
+  uint4 xr[kWavePF][KT], rr[kWavePF][4];
+#pragma unroll
+  for (int d = 0; d < kWavePF; ++d) load_tile(wid + d * nw, xr[d], rr[d]);
+  for (int i = 0; wid + i * nw < ntile;) {
+#pragma unroll
+    for (int d = 0; d < kWavePF; ++d) {
+      const int t = wid + i * nw;
+      if (t >= ntile) break;
+      process(t, xr[d], rr[d]);
+      load_tile(wid + (i + kWavePF) * nw, xr[d], rr[d]);
+      ++i;
+    }
+  }
+}
+
 // ---------------------------------------------------------------- tiled output
 // Projection whose every output column goes to a pair-tiled plane (the
 // triangle operands).  A workgroup tile is one 128-element chunk of the
@@ -1615,6 +1824,17 @@ void launch_stream(const LinArgs& p, hipStream_t s) {
   kern<<<dim3((unsigned)grid), dim3(kStreamThreads), smem, s>>>(p);
 }
 
+template <int EPI, int K>
+void launch_wave(const LinArgs& p, hipStream_t s) {
+  const int nt16 = (p.N + 15) / 16;
+  const size_t smem = wave_smem_bytes<K, EPI>(nt16);
+  auto kern = linear_wave_kernel<EPI, K>;
+  (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+  const int ntile = (p.rows + 15) / 16;
+  const int grid = std::min((ntile + kWaveThreads / 64 - 1) / (kWaveThreads / 64), compute_units());
+  kern<<<dim3((unsigned)grid), dim3(kWaveThreads), smem, s>>>(p);
+}
+
 template <int K>
 void launch_tiled(const LinArgs& p, hipStream_t s) {
   static int per_cu = 0;
@@ -1726,6 +1946,24 @@ hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
     if (a.c_in == 64) launch_tiled<64>(p, s);
     else launch_tiled<128>(p, s);
     return hipGetLastError();
+  }
+  {
+    // wave-streamed kernel: bf16 rows, a row-major main output (whole 16-byte
+    // chunks) and at most a channel-major tail, weights within the LDS budget
+    const bool res = a.epilogue == NT_EPI_RESIDUAL;
+    const int nt16 = (a.c_out + 15) / 16;
+    const size_t smem = a.c_in == 64 ? (res ? wave_smem_bytes<64, NT_EPI_RESIDUAL>(nt16) : wave_smem_bytes<64, NT_EPI_NONE>(nt16))
+                                     : (res ? wave_smem_bytes<128, NT_EPI_RESIDUAL>(nt16) : wave_smem_bytes<128, NT_EPI_NONE>(nt16));
+    if (!xf && !tiled && (a.c_in == 64 || a.c_in == 128) && p.n_main % 8 == 0 && a.ldx % 8 == 0 &&
+        p.ldy % 8 == 0 && (!res || (p.n_main <= 128 && a.ld_residual % 8 == 0)) && smem <= 150 * 1024 &&
+        (a.epilogue == NT_EPI_NONE || a.epilogue == NT_EPI_GELU || res)) {
+#define NT_WV(EPI) do { if (a.c_in == 64) launch_wave<EPI, 64>(p, s); else launch_wave<EPI, 128>(p, s); } while (0)
+      if (res) NT_WV(NT_EPI_RESIDUAL);
+      else if (a.epilogue == NT_EPI_GELU) NT_WV(NT_EPI_GELU);
+      else NT_WV(NT_EPI_NONE);
+#undef NT_WV
+      return hipGetLastError();
+    }
   }
   if ((a.c_in == 64 || a.c_in == 128) && a.c_out <= 512 &&
       (!tiled || (plan.layout && plan.layout->batch <= kStreamMaxSamples))) {
