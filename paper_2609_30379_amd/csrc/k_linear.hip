@@ -945,6 +945,16 @@ __global__ void __launch_bounds__(kWaveThreads, 1) linear_wave_kernel(LinArgs p)
     // ---- LayerNorm (or plain conversion) into B fragments
     bf16x8 xb[KT];
     if (p.gamma) {
+      // affine first: its LDS reads overlap the statistics
+      float4 ga[KT][2], be[KT][2];
+#pragma unroll
+      for (int kk = 0; kk < KT; ++kk) {
+        const int k0 = kk * 32 + g * 8;
+        ga[kk][0] = *reinterpret_cast<const float4*>(&s_gamma[k0]);
+        ga[kk][1] = *reinterpret_cast<const float4*>(&s_gamma[k0 + 4]);
+        be[kk][0] = *reinterpret_cast<const float4*>(&s_beta[k0]);
+        be[kk][1] = *reinterpret_cast<const float4*>(&s_beta[k0 + 4]);
+      }
       float v[KT][8];
 #pragma unroll
       for (int kk = 0; kk < KT; ++kk) XStage<bf16>::unpack(xr[kk], v[kk]);
@@ -953,24 +963,17 @@ __global__ void __launch_bounds__(kWaveThreads, 1) linear_wave_kernel(LinArgs p)
       for (int kk = 0; kk < KT; ++kk)
 #pragma unroll
         for (int e = 0; e < 8; ++e) s += v[kk][e];
-      s += __shfl_xor(s, 16, 64);
-      s += __shfl_xor(s, 32, 64);
-      const float mean = s / (float)K;
+      const float mean = sum_over_kgroups(s) / (float)K;
       float q = 0.f;
 #pragma unroll
       for (int kk = 0; kk < KT; ++kk)
 #pragma unroll
         for (int e = 0; e < 8; ++e) { const float d = v[kk][e] - mean; q += d * d; }
-      q += __shfl_xor(q, 16, 64);
-      q += __shfl_xor(q, 32, 64);
-      const float rstd = rsqrtf(q / (float)K + p.eps);
+      const float rstd = rsqrtf(sum_over_kgroups(q) / (float)K + p.eps);
 #pragma unroll
       for (int kk = 0; kk < KT; ++kk) {
-        const int k0 = kk * 32 + g * 8;
-        const float4 g0 = *reinterpret_cast<const float4*>(&s_gamma[k0]), g1 = *reinterpret_cast<const float4*>(&s_gamma[k0 + 4]);
-        const float4 b0 = *reinterpret_cast<const float4*>(&s_beta[k0]), b1 = *reinterpret_cast<const float4*>(&s_beta[k0 + 4]);
-        const float gg[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
-        const float bb[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+        const float gg[8] = {ga[kk][0].x, ga[kk][0].y, ga[kk][0].z, ga[kk][0].w, ga[kk][1].x, ga[kk][1].y, ga[kk][1].z, ga[kk][1].w};
+        const float bb[8] = {be[kk][0].x, be[kk][0].y, be[kk][0].z, be[kk][0].w, be[kk][1].x, be[kk][1].y, be[kk][1].z, be[kk][1].w};
 #pragma unroll
         for (int e = 0; e < 8; ++e) xb[kk][e] = (bf16)(m < p.rows ? (v[kk][e] - mean) * rstd * gg[e] + bb[e] : 0.f);
       }
@@ -1533,9 +1536,7 @@ __global__ void __launch_bounds__(kTrThreads, 1) transition_kernel(SwiArgs p) {
 #pragma unroll
           for (int e = 0; e < 8; ++e) s += t[e];
         }
-        s += __shfl_xor(s, 16, 64);
-        s += __shfl_xor(s, 32, 64);
-        const float mean = s / (float)K;
+        const float mean = sum_over_kgroups(s) / (float)K;
         float qv = 0.f;
 #pragma unroll
         for (int kk = 0; kk < KT; ++kk) {
@@ -1544,9 +1545,7 @@ __global__ void __launch_bounds__(kTrThreads, 1) transition_kernel(SwiArgs p) {
 #pragma unroll
           for (int e = 0; e < 8; ++e) { const float d = t[e] - mean; qv += d * d; }
         }
-        qv += __shfl_xor(qv, 16, 64);
-        qv += __shfl_xor(qv, 32, 64);
-        const float rstd = rsqrtf(qv / (float)K + p.eps);
+        const float rstd = rsqrtf(sum_over_kgroups(qv) / (float)K + p.eps);
 #pragma unroll
         for (int kk = 0; kk < KT; ++kk) {
           float t[8];
