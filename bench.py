@@ -38,17 +38,17 @@ F32_PEAK_TFLOPS = 157.3        # fp32 vector
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 COUNTER_WORKLOAD = "pair_b8_n208_224_bf16"
 COUNTERS = {  # op: (kernel source, source hash, FETCH_SIZE KiB, WRITE_SIZE KiB)
-    "attention_row": ("k_attention.hip", "5bcd92cc29a69522", 389791, 91895),
-    "transition": ("k_linear.hip", "86ed532cdb860f2e", 71840, 95170),
-    "triangle_out": ("k_triangle.hip", "8f868c65030d3dee", 317664, 90996),
-    "attn_proj": ("k_linear.hip", "86ed532cdb860f2e", 46039, 276189),
-    "tri_proj": ("k_linear.hip", "86ed532cdb860f2e", 45825, 197120),
-    "ln_linear": ("k_linear.hip", "86ed532cdb860f2e", 45724, 90996),
-    "attn_out_residual": ("k_linear.hip", "86ed532cdb860f2e", 91233, 90996),
-    "single_proj": ("k_linear.hip", "86ed532cdb860f2e", 1574, 853),
-    "pair_broadcast": ("k_segment.hip", "2fdde8205d37aa49", 1999, 90996),
-    "segment_mean": ("k_segment.hip", "2fdde8205d37aa49", 45570, 853),
-    "single_update": ("k_linear.hip", "86ed532cdb860f2e", 1645, 1928),
+    "attention_row": ("k_attention.hip", "85e05222acec14a1", 175893, 96233),
+    "transition": ("k_linear.hip", "937763db3aad8bda", 72770, 94314),
+    "triangle_out": ("k_triangle.hip", "7a4aa0ad16c08dba", 305493, 91403),
+    "attn_proj": ("k_linear.hip", "937763db3aad8bda", 46043, 276211),
+    "tri_proj": ("k_linear.hip", "937763db3aad8bda", 45830, 197120),
+    "ln_linear": ("k_linear.hip", "937763db3aad8bda", 45775, 90997),
+    "attn_out_residual": ("k_linear.hip", "937763db3aad8bda", 91301, 90996),
+    "single_proj": ("k_linear.hip", "937763db3aad8bda", 3368, 853),
+    "pair_broadcast": ("k_segment.hip", "a2aacf3085c626e1", 1999, 90996),
+    "segment_mean": ("k_segment.hip", "a2aacf3085c626e1", 45570, 853),
+    "single_update": ("k_linear.hip", "937763db3aad8bda", 3632, 1280),
 }
 
 
