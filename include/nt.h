@@ -32,8 +32,9 @@
  * calls never allocate, free or retain them.  An nt_layout and its device
  * mirrors are owned by the library from nt_from_* until nt_layout_destroy;
  * the caller must not destroy a layout while work that uses it is queued.
- * One op allocates: nt_pair_row_attention keeps a workspace in the layout
- * (see there).
+ * Two ops allocate scratch of their own: nt_pair_row_attention keeps a
+ * workspace in the layout and nt_layernorm_linear (large K with a LayerNorm)
+ * one per device (see there).
  *
  * Streams: every op enqueues asynchronously on the caller's HIP stream
  * (NULL = the default stream) and returns without synchronising.  Only
@@ -207,11 +208,19 @@ typedef struct {
   const nt_layout* residual_layout;  /* optional: must be compatible with layout */
 } nt_linear_args;
 
-/* Errors: NT_ERR_INVALID_ARG, NT_ERR_LAYOUT_MISMATCH (residual_layout differs
+/* Workspace: a bf16 call with a LayerNorm, bf16 x, K >= 384 (K % 32 == 0,
+ * K <= 4096), N % 8 == 0 and no tail first writes LN(x) (rounded to bf16, as
+ * the product consumes it) into a per-device workspace owned by the library,
+ * R * K * 2 bytes, allocated by the first such call and regrown (after a
+ * device synchronisation) when a later call needs more; it lives until the
+ * process ends.  Such calls on one device must therefore be ordered (one
+ * stream, or synchronised), not concurrent.
+ * Errors: NT_ERR_INVALID_ARG, NT_ERR_LAYOUT_MISMATCH (residual_layout differs
  * from layout, or rows differ from the layout's count), NT_ERR_UNSUPPORTED
  * (bf16 SwiGLU unless x is bf16, K == N in {64, 128, 256} and F % 32 == 0;
  * f32 SwiGLU with K > 1024 or F > 4096; n_tail with SwiGLU; a pair-tiled
- * tail without a pair layout).  ln_gamma/ln_beta must be 16-byte aligned.    */
+ * tail without a pair layout), NT_ERR_HIP (also when the workspace cannot be
+ * allocated).  ln_gamma/ln_beta must be 16-byte aligned.                     */
 nt_status nt_layernorm_linear(const nt_linear_args* args, void* stream);
 
 /* ---------------------------------------------------------------- attention

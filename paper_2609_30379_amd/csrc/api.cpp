@@ -2,6 +2,7 @@
 // lifetime, and dispatch to the kernel launchers.  No entry point throws,
 // aborts or synchronises the device.
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 
@@ -88,6 +89,34 @@ namespace nt {
 nt_status fail(nt_status s, const std::string& msg) {
   g_last_error = msg;
   return s;
+}
+
+hipError_t device_workspace(size_t bytes, void** ptr) {
+  static std::mutex mu;
+  static void* buf[64] = {nullptr};
+  static size_t size[64] = {0};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (size[dev] < bytes) {
+    if (buf[dev]) {
+      // work queued earlier may still read the old buffer
+      if ((e = hipDeviceSynchronize()) != hipSuccess) return e;
+      if ((e = hipFree(buf[dev])) != hipSuccess) return e;
+      buf[dev] = nullptr;
+      size[dev] = 0;
+    }
+    const size_t grown = bytes + bytes / 4;
+    if ((e = hipMalloc(&buf[dev], grown)) != hipSuccess) {
+      buf[dev] = nullptr;
+      return e;
+    }
+    size[dev] = grown;
+  }
+  *ptr = buf[dev];
+  return hipSuccess;
 }
 }  // namespace nt
 

@@ -1994,6 +1994,17 @@ hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
 #undef NT_ST
     return hipGetLastError();
   }
+  if (!xf && !p.y_tail && a.c_in >= 384 && a.c_in % 32 == 0 && a.c_out % 8 == 0 && a.ldx % 8 == 0 &&
+      p.ldy % 8 == 0 && (a.epilogue != NT_EPI_RESIDUAL || a.ld_residual % 8 == 0) &&
+      (a.epilogue == NT_EPI_NONE || a.epilogue == NT_EPI_GELU || a.epilogue == NT_EPI_RESIDUAL) &&
+      gemm_fits(a.c_in) && a.c_in <= 4096) {
+    GemmArgs g{};
+    g.rows = rows; g.K = a.c_in; g.N = a.c_out;
+    g.x = (const bf16*)a.x; g.ldx = a.ldx; g.gamma = a.ln_gamma; g.beta = a.ln_beta; g.eps = a.ln_eps;
+    g.w = (const bf16*)a.w; g.bias = a.bias; g.res = (const bf16*)a.residual; g.ld_res = a.ld_residual;
+    g.y = (bf16*)a.y; g.ldy = a.ldy; g.epi = a.epilogue;
+    return launch_gemm(g, s);
+  }
   if (a.c_in == 64 || a.c_in == 128 || a.c_in == 256) {
     const dim3 g1((unsigned)p.mblocks), b1(256);
 #define NT_RES(XT, EPI, KK) linear_res_kernel<XT, EPI, KK><<<g1, b1, 0, s>>>(p)

@@ -77,6 +77,33 @@ struct nt_layout {
 
 namespace nt {
 
+// Large-K bf16 projection (k_gemm.hip): y = epi(LN?(x) W^T + b) for row-major
+// x [rows, K], w [N, K], y [rows, N]; K % 32 == 0, N % 8 == 0, 16-byte rows.
+struct GemmArgs {
+  int rows, K, N;
+  const __bf16* x;
+  int64_t ldx;
+  const float* gamma;    // LayerNorm of x when non-NULL
+  const float* beta;
+  float eps;
+  const __bf16* w;
+  const float* bias;
+  const __bf16* res;     // epi == NT_EPI_RESIDUAL
+  int64_t ld_res;
+  __bf16* y;
+  int64_t ldy;
+  int epi;               // NT_EPI_NONE, NT_EPI_GELU or NT_EPI_RESIDUAL
+  int ntm, ntn;          // tiles (set by the launcher)
+};
+bool gemm_fits(int K);
+// With gamma set, the rows are first normalised into the device workspace.
+hipError_t launch_gemm(GemmArgs p, hipStream_t s);
+
+// Per-device scratch owned by the library (api.cpp): at least `bytes`, grown
+// on demand (growing synchronises the device); calls that use it on one
+// device must be ordered.
+hipError_t device_workspace(size_t bytes, void** ptr);
+
 // Sets the thread-local error message and returns the status.
 nt_status fail(nt_status s, const std::string& msg);
 

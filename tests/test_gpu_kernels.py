@@ -101,6 +101,8 @@ LIN_CASES = [
     (600, 768, 2304, True, "none", "bf16", "bf16", 0),
     (600, 768, 3072, True, "gelu", "bf16", "bf16", 0),
     (600, 3072, 768, False, "residual", "bf16", "bf16", 0),
+    (200, 416, 136, True, "gelu", "bf16", "bf16", 0),        # large-K path: 13 k-steps, part of a channel tile
+    (257, 1024, 520, False, "residual", "bf16", "bf16", 0),  # large-K path: one row past a row tile
     (300, 128, 384, False, "residual", "f32", "bf16", 0),
     (129, 136, 40, True, "residual", "bf16", "bf16", 0),
     (100, 16, 50, True, "none", "f32", "f32", 2),
