@@ -249,6 +249,82 @@ __global__ void __launch_bounds__(256) bias_image_kernel(BiasImgArgs p) {
   *reinterpret_cast<bf16x4*>(&p.img[(int64_t)h * p.tiles * 64 + tile * 64 + lane]) = o;
 }
 
+// ---------------------------------------------------------------- shared pieces
+// Value rows of 32 dims (64 bytes) staged row-major, the 16-byte piece at
+// column c of key row kv holding dim group c ^ ((kv >> 2) & 3) (so the four
+// key groups of a transposed read fall on different banks).  Fragments for
+// O^T += V^T P^T: lane (dim 16 dt + l16, k-group g) needs keys 32 kb +
+// {4g..4g+3, 16+4g..16+4g+3}.  ds_read_b64_tr_b16 hands lane 4q+m of each
+// 16-lane group element m of the 8-byte pieces addressed by lanes q, q+4,
+// q+8, q+12; pointing lane i at key base + i/4, dims 16 dt + 4 (i%4)
+// therefore delivers 4 consecutive keys of dim l16.  Key blocks are 2 KB
+// apart and keys kk, kk + 16 share (kk >> 2) & 3 = g, so every read of a lane
+// uses the same swizzled column.  The reads of one or two key blocks are
+// issued together from inline assembly with their own wait: the compiler
+// cannot tell them apart from global->LDS copies in flight into other
+// buffers and would otherwise wait for those first.
+struct VtLane {
+  uint32_t a0, a1;       // byte offsets in a value buffer, key block 0: dims 4q.., 16 + 4q..
+};
+__device__ __forceinline__ VtLane vt_lane(int l16, int g) {
+  const int kk = 4 * g + (l16 >> 2), q = l16 & 3;
+  return VtLane{(uint32_t)((kk * 32 + ((q >> 1) ^ g) * 8 + (q & 1) * 4) * 2),
+                (uint32_t)((kk * 32 + (((q >> 1) + 2) ^ g) * 8 + (q & 1) * 4) * 2)};
+}
+__device__ __forceinline__ uint32_t lds_addr(const bf16* ptr) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) bf16*)ptr;
+}
+__device__ __forceinline__ bf16x8 pack_u2(uint2 lo, uint2 hi) {
+  const uint32_t w[4] = {lo.x, lo.y, hi.x, hi.y};
+  return __builtin_bit_cast(bf16x8, w);
+}
+// one key block: f[0] dims 0-15, f[1] dims 16-31
+__device__ __forceinline__ void vt_frags1(const bf16* Vr, int kb, const VtLane& vl, bf16x8 (&f)[2]) {
+  const uint32_t base = lds_addr(Vr + kb * 32 * 32), a0 = base + vl.a0, a1 = base + vl.a1;
+  uint2 r[4];
+  asm volatile(
+      "ds_read_b64_tr_b16 %0, %4\n"
+      "ds_read_b64_tr_b16 %1, %4 offset:1024\n"
+      "ds_read_b64_tr_b16 %2, %5\n"
+      "ds_read_b64_tr_b16 %3, %5 offset:1024\n"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3])
+      : "v"(a0), "v"(a1)
+      : "memory");
+  f[0] = pack_u2(r[0], r[1]);
+  f[1] = pack_u2(r[2], r[3]);
+}
+// two key blocks kb, kb + 1: f[0..1] as above for kb, f[2..3] for kb + 1
+__device__ __forceinline__ void vt_frags2(const bf16* Vr, int kb, const VtLane& vl, bf16x8 (&f)[4]) {
+  const uint32_t base = lds_addr(Vr + kb * 32 * 32), a0 = base + vl.a0, a1 = base + vl.a1;
+  uint2 r[8];
+  asm volatile(
+      "ds_read_b64_tr_b16 %0, %8\n"
+      "ds_read_b64_tr_b16 %1, %8 offset:1024\n"
+      "ds_read_b64_tr_b16 %2, %9\n"
+      "ds_read_b64_tr_b16 %3, %9 offset:1024\n"
+      "ds_read_b64_tr_b16 %4, %8 offset:2048\n"
+      "ds_read_b64_tr_b16 %5, %8 offset:3072\n"
+      "ds_read_b64_tr_b16 %6, %9 offset:2048\n"
+      "ds_read_b64_tr_b16 %7, %9 offset:3072\n"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]), "=&v"(r[6]), "=&v"(r[7])
+      : "v"(a0), "v"(a1)
+      : "memory");
+  f[0] = pack_u2(r[0], r[1]);
+  f[1] = pack_u2(r[2], r[3]);
+  f[2] = pack_u2(r[4], r[5]);
+  f[3] = pack_u2(r[6], r[7]);
+}
+// maximum over the four lanes l16 + 16 g holding one query: the swaps pair
+// lane l with l ^ 16, then with l ^ 32, and leave both values in place
+__device__ __forceinline__ float query_max(float v) {
+  const auto s16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(s16[0]), __uint_as_float(s16[1]));
+  const auto s32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(s32[0]), __uint_as_float(s32[1]));
+}
+
 // ---------------------------------------------------------------- pair attention, head_dim 32
 // Pair attention for head_dim 32 and N_i <= kAttnLongLen, organised so that
 // the exponentials are nearly the only vector work.  A workgroup of 8 waves
@@ -318,76 +394,9 @@ __global__ void __launch_bounds__(512, NMAX <= 256 ? 4 : 2) attention_pair_kerne
       __builtin_amdgcn_global_load_lds((const void*)sv, (__attribute__((address_space(3))) void*)(Vr + kt * 512), 16, 0, 0);
     }
   };
-  // Value fragments for O^T += V^T P^T: lane (dim 16 dt + l16, k-group g)
-  // needs keys 32 kb + {4g..4g+3, 16+4g..16+4g+3}.  ds_read_b64_tr_b16 hands
-  // lane 4q+m of each 16-lane group element m of the 8-byte pieces addressed
-  // by lanes q, q+4, q+8, q+12; pointing lane i at key base + i/4, dims
-  // 16 dt + 4 (i%4) therefore delivers 4 consecutive keys of dim l16.  The
-  // reads of one or two key blocks are issued together from inline assembly
-  // with their own wait: the compiler cannot tell them apart from the copies
-  // into the other buffer and would otherwise wait for those first.  The
-  // row-end wait and barrier make the buffer being read complete.  Key
-  // blocks are 2 KB apart and keys kk, kk + 16 share (kk >> 2) & 3 = g, so
-  // every read of a lane uses the same swizzled column.
-  int v_a0, v_a1;                                 // LDS byte offsets within a value buffer, key block 0
-  {
-    const int kk = 4 * g + (l16 >> 2), q = l16 & 3;
-    v_a0 = (kk * D + ((q >> 1) ^ g) * 8 + (q & 1) * 4) * 2;         // dims 4q .. 4q+3 (dim group q/2)
-    v_a1 = (kk * D + (((q >> 1) + 2) ^ g) * 8 + (q & 1) * 4) * 2;   // dims 16 + 4q ..
-  }
-  auto lds_addr = [](const bf16* ptr) {
-    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) bf16*)ptr;
-  };
-  auto pack = [](uint2 lo, uint2 hi) {
-    const uint32_t w[4] = {lo.x, lo.y, hi.x, hi.y};
-    return __builtin_bit_cast(bf16x8, w);
-  };
-  // one key block: f[0] dims 0-15, f[1] dims 16-31
-  auto v_frags1 = [&](const bf16* Vr, int kb, bf16x8 (&f)[2]) {
-    const uint32_t a0 = lds_addr(Vr + kb * 32 * D) + v_a0, a1 = lds_addr(Vr + kb * 32 * D) + v_a1;
-    uint2 r[4];
-    asm volatile(
-        "ds_read_b64_tr_b16 %0, %4\n"
-        "ds_read_b64_tr_b16 %1, %4 offset:1024\n"
-        "ds_read_b64_tr_b16 %2, %5\n"
-        "ds_read_b64_tr_b16 %3, %5 offset:1024\n"
-        "s_waitcnt lgkmcnt(0)"
-        : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3])
-        : "v"(a0), "v"(a1)
-        : "memory");
-    f[0] = pack(r[0], r[1]);
-    f[1] = pack(r[2], r[3]);
-  };
-  // two key blocks kb, kb + 1: f[0..1] as above for kb, f[2..3] for kb + 1
-  auto v_frags2 = [&](const bf16* Vr, int kb, bf16x8 (&f)[4]) {
-    const uint32_t a0 = lds_addr(Vr + kb * 32 * D) + v_a0, a1 = lds_addr(Vr + kb * 32 * D) + v_a1;
-    uint2 r[8];
-    asm volatile(
-        "ds_read_b64_tr_b16 %0, %8\n"
-        "ds_read_b64_tr_b16 %1, %8 offset:1024\n"
-        "ds_read_b64_tr_b16 %2, %9\n"
-        "ds_read_b64_tr_b16 %3, %9 offset:1024\n"
-        "ds_read_b64_tr_b16 %4, %8 offset:2048\n"
-        "ds_read_b64_tr_b16 %5, %8 offset:3072\n"
-        "ds_read_b64_tr_b16 %6, %9 offset:2048\n"
-        "ds_read_b64_tr_b16 %7, %9 offset:3072\n"
-        "s_waitcnt lgkmcnt(0)"
-        : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]), "=&v"(r[6]), "=&v"(r[7])
-        : "v"(a0), "v"(a1)
-        : "memory");
-    f[0] = pack(r[0], r[1]);
-    f[1] = pack(r[2], r[3]);
-    f[2] = pack(r[4], r[5]);
-    f[3] = pack(r[6], r[7]);
-  };
-  // maximum over the four lanes l16 + 16 g holding one query: the swaps pair
-  // lane l with l ^ 16, then with l ^ 32, and leave both values in place
-  auto query_max = [](float v) {
-    const auto s16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-    v = fmaxf(__uint_as_float(s16[0]), __uint_as_float(s16[1]));
-    const auto s32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-    return fmaxf(__uint_as_float(s32[0]), __uint_as_float(s32[1]));
-  };
+  const VtLane vl = vt_lane(l16, g);
+  auto v_frags1 = [&](const bf16* Vr, int kb, bf16x8 (&f)[2]) { vt_frags1(Vr, kb, vl, f); };
+  auto v_frags2 = [&](const bf16* Vr, int kb, bf16x8 (&f)[4]) { vt_frags2(Vr, kb, vl, f); };
 
   const int jw = j0 + 16 * wave + l16;          // this lane's query
   const bool wave_has_queries = wave < nqt && j0 + 16 * wave < n;
@@ -536,6 +545,180 @@ __global__ void __launch_bounds__(512, NMAX <= 256 ? 4 : 2) attention_pair_kerne
   }
 }
 
+// ---------------------------------------------------------------- 1-D attention, head_dim 64
+// Variable-length self-attention over each sample's tokens (Sec. 3.3
+// "Attention through packed blocks"), head_dim 64, N_i <= kAttnLongLen.  A
+// workgroup of 8 waves takes (sample, block of up to 128 queries, head): all
+// keys and values of the sample are copied global -> LDS once (64-dim rows as
+// two 32-dim halves: keys as fragment images, values row-major with the
+// swizzle of the value reads), then each wave runs its 16 queries over 128-key
+// super-chunks -- score products of both halves, one maximum per query, the
+// exponentials and the value products -- with the lazily rescaled running
+// maximum of the pair kernel.  Keys past N repeat key N-1 in LDS and get
+// probability zero.
+struct SeqAttnArgs {
+  const bf16* q;
+  const bf16* k;
+  const bf16* v;
+  int64_t ld_qkv;
+  float scale_log2;
+  bf16* o;
+  int64_t ld_o;
+  const int32_t* work;   // quads (sample, first 16-query tile, 0, tile count)
+  const int32_t* cu_seqlens;
+  int H;
+};
+
+template <int NMAX>
+__global__ void __launch_bounds__(512, NMAX <= 256 ? 4 : 2) attention_seq_kernel(SeqAttnArgs p) {
+  constexpr int D = 64;
+  constexpr int KT16 = NMAX / 16;
+  extern __shared__ __attribute__((aligned(16))) bf16 lds[];
+  const int x = blockIdx.x % kXcds, t = blockIdx.x / kXcds;
+  const int h = t % p.H, pos = (t / p.H) * kXcds + x;
+  const int4 w4 = reinterpret_cast<const int4*>(p.work)[pos];
+  const int i = w4.x;
+  if (i < 0) return;
+  const int qt0 = w4.y, nqt = w4.w;
+  const int64_t base = p.cu_seqlens[i];
+  const int n = p.cu_seqlens[i + 1] - (int)base;
+  const int npad = (n + 63) & ~63;
+  bf16* Kh0 = lds;                                // key images, dims 0-31: tile of 16 keys -> 512 elements
+  bf16* Kh1 = Kh0 + NMAX * 32;                    // dims 32-63
+  bf16* Vh0 = Kh1 + NMAX * 32;                    // values, row-major [key][32], dims 0-31
+  bf16* Vh1 = Vh0 + NMAX * 32;                    // dims 32-63
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l16 = lane & 15, g = lane >> 4;
+
+  // ---- stage keys and values of the whole sample (tiles below npad)
+  for (int kt = wave; kt < KT16; kt += 8) {
+    if (kt * 16 >= npad) break;
+    const int key_k = min(kt * 16 + l16, n - 1);
+    const int kv = kt * 16 + (lane >> 2), key_v = min(kv, n - 1);
+    const int dgv = (lane & 3) ^ ((kv >> 2) & 3);
+    const bf16* sk = p.k + (base + key_k) * p.ld_qkv + h * D + g * 8;
+    const bf16* sv = p.v + (base + key_v) * p.ld_qkv + h * D + dgv * 8;
+    __builtin_amdgcn_global_load_lds((const void*)sk, (__attribute__((address_space(3))) void*)(Kh0 + kt * 512), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds((const void*)(sk + 32), (__attribute__((address_space(3))) void*)(Kh1 + kt * 512), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds((const void*)sv, (__attribute__((address_space(3))) void*)(Vh0 + kt * 512), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds((const void*)(sv + 32), (__attribute__((address_space(3))) void*)(Vh1 + kt * 512), 16, 0, 0);
+  }
+  const int j0 = qt0 * 16;
+  const int jw = j0 + 16 * wave + l16;            // this lane's query
+  const bool wave_has_queries = wave < nqt && j0 + 16 * wave < n;
+  const bool qvalid = jw < n;
+  bf16x8 qf0 = bf16x8{}, qf1 = bf16x8{};
+  if (qvalid) {
+    const bf16* qr = p.q + (base + jw) * p.ld_qkv + h * D + g * 8;
+    qf0 = *reinterpret_cast<const bf16x8*>(qr);
+    qf1 = *reinterpret_cast<const bf16x8*>(qr + 32);
+  }
+  __builtin_amdgcn_s_waitcnt(0);                  // this wave's copies have landed
+  __syncthreads();
+  if (!wave_has_queries) return;
+
+  const VtLane vl = vt_lane(l16, g);
+  bf16x8 ones;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) ones[e] = (bf16)1.f;
+  const float c = p.scale_log2;
+  float m_s = -INFINITY;
+  f32x4 O[5];                                     // dims 0-15, 16-31, 32-47, 48-63, row sum
+#pragma unroll
+  for (int u = 0; u < 5; ++u) O[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto super_chunk = [&](auto sc_c, auto nt_c) {
+    constexpr int SC = decltype(sc_c)::value, NT = decltype(nt_c)::value;
+    constexpr int T0 = SC * 8;
+    const int kc = SC * 128;
+    f32x4 S[NT];
+#pragma unroll
+    for (int kt = 0; kt < NT; ++kt) {
+      const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(&Kh0[(T0 + kt) * 512 + lane * 8]);
+      const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(&Kh1[(T0 + kt) * 512 + lane * 8]);
+      S[kt] = mfma16(k0, qf0, f32x4{0.f, 0.f, 0.f, 0.f});
+      S[kt] = mfma16(k1, qf1, S[kt]);
+      if (kt % 4 == 3) __builtin_amdgcn_sched_barrier(0);   // bounded key fragments in flight
+    }
+    if (kc + NT * 16 > n) {
+#pragma unroll
+      for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+        for (int ii = 0; ii < 4; ++ii)
+          if (kc + kt * 16 + 4 * g + ii >= n) S[kt][ii] = -INFINITY;
+    }
+    float mloc = S[0][0];
+#pragma unroll
+    for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) mloc = fmaxf(mloc, S[kt][ii]);
+    mloc = query_max(mloc);
+    if (__any((mloc - m_s) * c > 8.f)) {
+      const float m_new = fmaxf(m_s, mloc);
+      const float alpha = __builtin_amdgcn_exp2f((m_s - m_new) * c);
+      m_s = m_new;
+#pragma unroll
+      for (int u = 0; u < 5; ++u) O[u] *= alpha;
+    }
+    const float nm = -m_s * c;
+    bf16x8 P[NT / 2];
+#pragma unroll
+    for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii)
+        P[kt >> 1][(kt & 1) * 4 + ii] = (bf16)__builtin_amdgcn_exp2f(fmaf(S[kt][ii], c, nm));
+#pragma unroll
+    for (int pp = 0; pp + 1 < NT / 2; pp += 2) {
+      bf16x8 va[4], vb[4];
+      vt_frags2(Vh0, SC * 4 + pp, vl, va);
+      vt_frags2(Vh1, SC * 4 + pp, vl, vb);
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        O[0] = mfma16(va[2 * u], P[pp + u], O[0]);
+        O[1] = mfma16(va[2 * u + 1], P[pp + u], O[1]);
+        O[2] = mfma16(vb[2 * u], P[pp + u], O[2]);
+        O[3] = mfma16(vb[2 * u + 1], P[pp + u], O[3]);
+        O[4] = mfma16(ones, P[pp + u], O[4]);
+      }
+    }
+    if constexpr ((NT / 2) % 2 == 1) {
+      bf16x8 va[2], vb[2];
+      vt_frags1(Vh0, SC * 4 + NT / 2 - 1, vl, va);
+      vt_frags1(Vh1, SC * 4 + NT / 2 - 1, vl, vb);
+      O[0] = mfma16(va[0], P[NT / 2 - 1], O[0]);
+      O[1] = mfma16(va[1], P[NT / 2 - 1], O[1]);
+      O[2] = mfma16(vb[0], P[NT / 2 - 1], O[2]);
+      O[3] = mfma16(vb[1], P[NT / 2 - 1], O[3]);
+      O[4] = mfma16(ones, P[NT / 2 - 1], O[4]);
+    }
+  };
+  auto run_sc = [&](auto sc_c) {
+    constexpr int SC = decltype(sc_c)::value;
+    const int rem = n - SC * 128;
+    if (rem <= 0) return;
+    if (rem > 96) super_chunk(sc_c, std::integral_constant<int, 8>{});
+    else if (rem > 64) super_chunk(sc_c, std::integral_constant<int, 6>{});
+    else if (rem > 32) super_chunk(sc_c, std::integral_constant<int, 4>{});
+    else super_chunk(sc_c, std::integral_constant<int, 2>{});
+  };
+  run_sc(std::integral_constant<int, 0>{});
+  run_sc(std::integral_constant<int, 1>{});
+  if constexpr (NMAX > 256) {
+    run_sc(std::integral_constant<int, 2>{});
+    run_sc(std::integral_constant<int, 3>{});
+  }
+  if (qvalid) {
+    const float inv = 1.f / O[4][0];
+    bf16* orow = p.o + (base + jw) * p.ld_o + h * D;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+      bf16x4 ov;
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) ov[ii] = (bf16)(O[dt][ii] * inv);
+      *reinterpret_cast<bf16x4*>(orow + dt * 16 + 4 * g) = ov;
+    }
+  }
+}
+
 // ---------------------------------------------------------------- fp32 path
 struct AttnF32Args {
   int axis, H;
@@ -613,6 +796,22 @@ hipError_t launch_attention(const nt_layout& L, int axis, int H, int D, const vo
     return hipGetLastError();
   }
   const int npad = (L.max_len + 63) & ~63;
+  if (D == 64 && axis == 2 && L.max_len <= kAttnLongLen) {
+    if (L.sattn_items() == 0) return hipSuccess;
+    const int nmax = L.max_len <= kAttnShortLen ? kAttnShortLen : kAttnLongLen;
+    SeqAttnArgs a{(const bf16*)q, (const bf16*)k, (const bf16*)v, ld_qkv, scale * kLog2e, (bf16*)o, ld_o,
+                  L.d_sattn_work, L.d_cu_seqlens, H};
+    const size_t smem = sizeof(bf16) * 4 * (size_t)nmax * 32;
+    const dim3 grid((unsigned)(L.sattn_items() * H));
+    const void* fn = nmax == kAttnShortLen ? (const void*)attention_seq_kernel<kAttnShortLen>
+                                          : (const void*)attention_seq_kernel<kAttnLongLen>;
+    hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    if (nmax == kAttnShortLen)
+      attention_seq_kernel<kAttnShortLen><<<grid, dim3(512), smem, s>>>(a);
+    else
+      attention_seq_kernel<kAttnLongLen><<<grid, dim3(512), smem, s>>>(a);
+    return hipGetLastError();
+  }
   if (D == 32 && axis != 2 && L.max_len <= kAttnLongLen) {
     if (L.pattn_items() == 0) return hipSuccess;
     const int nmax = L.max_len <= kAttnShortLen ? kAttnShortLen : kAttnLongLen;

@@ -148,6 +148,22 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L) {
     }
     L->pattn_work = xcd_order<4>(items, cost, false);
   }
+  // 1-D attention: the same even split of a sample's 16-query tiles over
+  // blocks of at most kAttnQB queries, one item per block
+  {
+    std::vector<std::array<int32_t, 4>> items;
+    std::vector<double> cost;
+    for (int32_t i = 0; i < batch; ++i) {
+      const int32_t n = lengths[i], tiles = (n + 15) / 16;
+      const int32_t blocks = (tiles + kAttnQB / 16 - 1) / (kAttnQB / 16);
+      for (int32_t b = 0; b < blocks; ++b) {
+        const int32_t t0 = b * tiles / blocks, t1 = (b + 1) * tiles / blocks;
+        items.push_back({i, t0, 0, t1 - t0});
+        cost.push_back((double)std::min(16 * (t1 - t0), n - 16 * t0) * n);
+      }
+    }
+    L->sattn_work = xcd_order<4>(items, cost, true);
+  }
   // pair attention bias image: per sample, one 512-byte tile per (16-query
   // tile, 16-key tile) up to the 64-key padded length
   L->bias_tiles.assign(batch + 1, 0);

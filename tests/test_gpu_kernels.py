@@ -222,6 +222,7 @@ def test_pair_attention(B, axis, dtype, H, D, lset):
 
 
 @pytest.mark.parametrize("dtype,H,D,L", [("bf16", 3, 64, [1, 5, 64, 65, 130, 512, 0, 200]),
+                                         ("bf16", 2, 64, [256, 17, 1, 100, 33, 0]),
                                          ("bf16", 2, 32, [33, 1, 97]),
                                          ("f32", 2, 8, [15, 12, 10, 7, 0, 1])])
 def test_attention_1d(B, dtype, H, D, L):
