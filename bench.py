@@ -197,6 +197,7 @@ def main():
                     help="default: the B=8 near-uniform pair block; the other workloads are parity cases, "
                          "timed here on request")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true", help="time replays of the step captured into a HIP graph")
     ap.add_argument("--kernels", action="store_true", help="also print the per-op breakdown to stderr")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device-to-device copy (scale reference for HBM counters)")
@@ -225,26 +226,59 @@ def main():
     L = run.lengths
     R = sum(n * n for n in L)
 
-    for _ in range(args.warmup):
-        run.step()
+    for _ in range(max(1, args.warmup)):
+        ref = [t.clone() for t in run.step() if t is not None]
     torch.cuda.synchronize()
 
-    # timed region: per-op events on the launch stream, wall clock around it
-    tm = blocks.OpTimer()
-    blocks.timer = tm
+    # With --graph the step is captured once into a HIP graph and replayed in
+    # the timed region, after checking that a replay reproduces the eager step
+    # bit for bit (otherwise, and by default, eager steps are timed).
+    graph = None
+    if args.graph:
+        try:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                outs = [t for t in run.step() if t is not None]
+            g.replay()
+            torch.cuda.synchronize()
+            if all(torch.equal(a, b) for a, b in zip(ref, outs)):
+                graph = g
+            else:
+                print("bench.py: graph replay differs from the eager step; timing eager steps", file=sys.stderr)
+        except Exception as e:                       # capture unsupported: time eager steps
+            print(f"bench.py: graph capture failed ({e}); timing eager steps", file=sys.stderr)
+        torch.cuda.synchronize()
+
+    # timed region: wall clock and events on the launch stream around it (no
+    # per-op events inside: recording them adds gaps between the kernels)
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     ev0.record()
     for _ in range(args.steps):
-        run.step()
+        if graph is not None:
+            graph.replay()
+        else:
+            run.step()
     ev1.record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    blocks.timer = None
     ms = (t1 - t0) * 1e3 / args.steps
     ms_dev = ev0.elapsed_time(ev1) / args.steps
+
+    # per-op attribution: eager steps with an event pair around every op on
+    # the launch stream (a captured graph cannot carry timing events)
+    tm = blocks.OpTimer()
+    blocks.timer = tm
+    torch.cuda.synchronize()
+    te0 = time.perf_counter()
+    for _ in range(args.steps):
+        run.step()
+    torch.cuda.synchronize()
+    te1 = time.perf_counter()
+    blocks.timer = None
     per_op = tm.summary()                            # {op: (launches, mean us)}
+    ms_eager = (te1 - te0) * 1e3 / args.steps
 
     costs = token_op_costs(w, L) if tokens else op_costs(w, L)
     total_us = {k: n * us / args.steps for k, (n, us) in per_op.items()}
@@ -273,7 +307,8 @@ def main():
     out = {
         "metric": metric, "value": round(value, 1), "unit": unit,
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
-        "device_ms_per_step": round(ms_dev, 4),
+        "device_ms_per_step": round(ms_dev, 4), "graph": graph is not None,
+        "eager_ms_per_step_with_op_events": round(ms_eager, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
         "config": config,
         "roofline": rl,
