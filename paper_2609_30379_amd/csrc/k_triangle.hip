@@ -41,6 +41,7 @@ struct TriArgs {
 
 __global__ void __launch_bounds__(kTriThreads, 1) triangle_mfma_kernel(TriArgs p) {
   __shared__ __attribute__((aligned(16))) float stage[16 * kTriRS * kTriSC];
+  __shared__ __attribute__((aligned(16))) bf16 zbuf[2][16 * kTriTile * kTriCB];   // z of two bands, [row][col][16]
   // Workgroup id = 8 (4 k + j) + x runs on XCD x: its k-th (tile, line group)
   // pair q = 8 k + x, channel block j of that group.
   const int id = blockIdx.x;
@@ -58,6 +59,25 @@ __global__ void __launch_bounds__(kTriThreads, 1) triangle_mfma_kernel(TriArgs p
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l16 = lane & 15, g = lane >> 4;
   const int c = cb * kTriCB + wave;
+
+  // z of band xs (16 rows x 64 cells x 16 channels) copied global -> LDS into
+  // zbuf[slot] as [row][cell][16]: copy instruction u of the band covers row
+  // u / 2, cells 32 (u % 2) .. +31, two lanes per cell.  Cells past N read the
+  // sample's last cell (never written back).  Bands 0 and 1 are copied before
+  // the contraction, band xs + 2 while band xs is written.
+  auto z_copy = [&](int xs, int slot) {
+#pragma unroll
+    for (int v = 0; v < 2; ++v) {
+      const int u = wave + kTriCB * v;                // 0 .. 31
+      const int r = u >> 1, cell = (u & 1) * 32 + (lane >> 1), half = lane & 1;
+      const int x = min(x0 + 16 * xs + r, n - 1), y = min(y0 + cell, n - 1);
+      const bf16* src = p.z + (cu + (int64_t)x * n + y) * p.ld_z + cb * kTriCB + half * 8;
+      bf16* dst = &zbuf[slot][(r * kTriTile + (u & 1) * 32) * kTriCB];
+      __builtin_amdgcn_global_load_lds((const void*)src, (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+    }
+  };
+  z_copy(0, 0);
+  if (x0 + 16 < n) z_copy(1, 1);
 
   // row tiles of the output tile that hold rows of the sample (uniform)
   bool xv[4], yv[4];
@@ -99,25 +119,7 @@ __global__ void __launch_bounds__(kTriThreads, 1) triangle_mfma_kernel(TriArgs p
 
   // acc[xs][ys][r] = T_c[x0 + 16xs + 4g + r][y0 + 16ys + l16].  Band xs:
   // stage its 16 x 64 cells as [cell][16 channels] fp32, then two threads
-  // per cell add 8 channels (16 bytes) each into z.  The z values of the next
-  // band are loaded while the current band is staged and written.
-  constexpr int kIt = 16 * kTriTile * 2 / kTriThreads;     // (cell, half) items per thread and band
-  auto z_ptr = [&](int xs, int it, bool& ok) {
-    const int u = it * kTriThreads + tid, cell = u >> 1, half = u & 1;
-    const int x = x0 + 16 * xs + cell / kTriTile, y = y0 + cell % kTriTile;
-    ok = x < n && y < n;
-    return p.z + (cu + (int64_t)x * n + y) * p.ld_z + cb * kTriCB + half * 8;
-  };
-  uint4 zr[kIt];
-  auto z_load = [&](int xs) {
-#pragma unroll
-    for (int it = 0; it < kIt; ++it) {
-      bool ok;
-      const bf16* zp = z_ptr(xs, it, ok);
-      zr[it] = ok ? *reinterpret_cast<const uint4*>(zp) : make_uint4(0u, 0u, 0u, 0u);
-    }
-  };
-  z_load(0);
+  // per cell add 8 channels (16 bytes) to the band's z copy and store them.
 #pragma unroll
   for (int xs = 0; xs < 4; ++xs) {
     if (!xv[xs]) break;                               // uniform
@@ -125,22 +127,19 @@ __global__ void __launch_bounds__(kTriThreads, 1) triangle_mfma_kernel(TriArgs p
     for (int ys = 0; ys < 4; ++ys)
 #pragma unroll
       for (int r = 0; r < 4; ++r) stage[((4 * g + r) * kTriRS + 16 * ys + l16) * kTriSC + wave] = acc[xs][ys][r];
+    __builtin_amdgcn_s_waitcnt(0);                    // this wave's z copies (and earlier stores) are done
     __syncthreads();
-    uint4 cur[kIt];
 #pragma unroll
-    for (int it = 0; it < kIt; ++it) cur[it] = zr[it];
-    if (xs + 1 < 4 && xv[xs + 1]) z_load(xs + 1);
-#pragma unroll
-    for (int it = 0; it < kIt; ++it) {
+    for (int it = 0; it < 16 * kTriTile * 2 / kTriThreads; ++it) {
       const int u = it * kTriThreads + tid, cell = u >> 1, half = u & 1;
       const int row = cell / kTriTile, col = cell % kTriTile;
-      bool ok;
-      bf16* zp = z_ptr(xs, it, ok);
-      if (!ok) continue;
+      const int x = x0 + 16 * xs + row, y = y0 + col;
+      if (x >= n || y >= n) continue;
       const float* st = &stage[(row * kTriRS + col) * kTriSC + half * 8];
       const float4 t0 = *reinterpret_cast<const float4*>(st);
       const float4 t1 = *reinterpret_cast<const float4*>(st + 4);
-      const uint32_t w4[4] = {cur[it].x, cur[it].y, cur[it].z, cur[it].w};
+      const uint4 zq = *reinterpret_cast<const uint4*>(&zbuf[xs & 1][(row * kTriTile + col) * kTriCB + half * 8]);
+      const uint32_t w4[4] = {zq.x, zq.y, zq.z, zq.w};
       float v[8];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
@@ -152,9 +151,10 @@ __global__ void __launch_bounds__(kTriThreads, 1) triangle_mfma_kernel(TriArgs p
       bf16x8 o;
 #pragma unroll
       for (int e = 0; e < 8; ++e) o[e] = (bf16)v[e];
-      *reinterpret_cast<bf16x8*>(zp) = o;
+      *reinterpret_cast<bf16x8*>(p.z + (cu + (int64_t)x * n + y) * p.ld_z + cb * kTriCB + half * 8) = o;
     }
-    __syncthreads();
+    __syncthreads();                                  // stage and this band's z copy are free
+    if (xs + 2 < 4 && xv[xs + 2]) z_copy(xs + 2, xs & 1);
   }
 }
 
