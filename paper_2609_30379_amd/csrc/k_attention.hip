@@ -327,8 +327,8 @@ __device__ __forceinline__ float query_max(float v) {
 
 // ---------------------------------------------------------------- pair attention, head_dim 32
 // Pair attention for head_dim 32 and N_i <= kAttnLongLen, organised so that
-// the exponentials are nearly the only vector work.  A workgroup of 8 waves
-// takes (sample, block of up to 128 queries, group of 16 pair rows, head):
+// the exponentials are nearly the only vector work.  A workgroup of NW waves
+// takes (sample, block of up to 16 NW queries, group of 16 pair rows, head):
 //   * the bias of (query, key) does not depend on the pair row, so each lane
 //     keeps the bias of its query for its 4-key groups of every key tile in
 //     registers for the whole group of rows -- staged once through LDS and
@@ -342,10 +342,12 @@ __device__ __forceinline__ float query_max(float v) {
 //     ones operand, on the same bf16 probabilities as the numerator.
 // Scores are kept transposed (S^T = K Q^T), so a lane holds 16 keys of one
 // query per 64-key chunk and the running max is mostly lane-local.
-// Two instances: N <= 256 (64 KB of LDS, two workgroups per CU) and N <= 512
-// (128 KB, one workgroup per CU, twice the bias registers).
-template <int NMAX>
-__global__ void __launch_bounds__(512, NMAX <= 256 ? 4 : 2) attention_pair_kernel(PairAttnArgs p) {
+// Two instances: N <= 256 with 16 waves (all queries of a row group in one
+// workgroup, so a row's keys and values are copied once per CU; 64 KB of LDS,
+// four waves per SIMD) and N <= 512 with 8 waves (128 KB, twice the bias
+// registers, two waves per SIMD).
+template <int NMAX, int NW>
+__global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_kernel(PairAttnArgs p) {
   constexpr int D = 32;
   constexpr int KT16 = NMAX / 16;               // key tiles
   extern __shared__ __attribute__((aligned(16))) bf16 lds[];
@@ -371,7 +373,7 @@ __global__ void __launch_bounds__(512, NMAX <= 256 ? 4 : 2) attention_pair_kerne
   const int j0 = qt0 * 16;
 
   // ---- per-row staging: straight global -> LDS copies ---------------------
-  // Each wave copies its key tiles (wave, wave + 8, ...; 16 keys each) with
+  // Each wave copies its key tiles (wave, wave + NW, ...; 16 keys each) with
   // global_load_lds, lane l's 16 bytes landing at byte 16 l of the tile:
   //   keys as fragment images: lane l = (key l%16, dims 8 (l/16) ..),
   //   values row-major [key][32]: lane l = (key l/4, dims 8 (l%4) ..).
@@ -380,7 +382,7 @@ __global__ void __launch_bounds__(512, NMAX <= 256 ? 4 : 2) attention_pair_kerne
   // finite values whose probabilities are masked to zero.
   auto dma_kv = [&](int r, bf16* Kb, bf16* Vr) {
 #pragma unroll
-    for (int kt = wave; kt < KT16; kt += 8) {
+    for (int kt = wave; kt < KT16; kt += NW) {
       if (kt * 16 >= npad) break;
       // values: the 16-byte chunk at column c of key row kv holds dim group
       // c ^ ((kv >> 2) & 3), so the four key groups of a transpose read fall
@@ -844,13 +846,16 @@ hipError_t launch_attention(const nt_layout& L, int axis, int H, int D, const vo
                    img, tiles * 64, L.d_bias_tiles};
     const size_t smem = sizeof(bf16) * 4 * (size_t)nmax * 32;
     const dim3 grid((unsigned)(L.pattn_items() * H));
-    const void* fn = nmax == kAttnShortLen ? (const void*)attention_pair_kernel<kAttnShortLen>
-                                          : (const void*)attention_pair_kernel<kAttnLongLen>;
-    hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-    if (nmax == kAttnShortLen)
-      attention_pair_kernel<kAttnShortLen><<<grid, dim3(512), smem, s>>>(a);
-    else
-      attention_pair_kernel<kAttnLongLen><<<grid, dim3(512), smem, s>>>(a);
+    if (nmax == kAttnShortLen) {
+      // one workgroup of 16 waves covers all queries of a row group
+      a.work = L.d_pattn16_work;
+      const dim3 grid16((unsigned)(L.pattn16_items() * H));
+      hipFuncSetAttribute((const void*)attention_pair_kernel<kAttnShortLen, 16>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+      attention_pair_kernel<kAttnShortLen, 16><<<grid16, dim3(1024), smem, s>>>(a);
+    } else {
+      hipFuncSetAttribute((const void*)attention_pair_kernel<kAttnLongLen, 8>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+      attention_pair_kernel<kAttnLongLen, 8><<<grid, dim3(512), smem, s>>>(a);
+    }
     return hipGetLastError();
   }
   const int vstride = (npad + 127) / 128 * 128 + 4;

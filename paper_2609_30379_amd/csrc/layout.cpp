@@ -129,16 +129,17 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L) {
     L->attn_work = xcd_order<2>(items, cost);
   }
   // pair attention: a sample's 16-query tiles are split evenly over
-  // ceil(tiles / 8) blocks (items: sample, first tile, row group, tile count),
-  // so no block leaves most of its 8 waves idle; generation order is kept in
-  // each XCD's queue so the blocks of a row group stay adjacent and share keys
-  // and values.
-  {
+  // ceil(tiles / W) blocks of at most W tiles (items: sample, first tile, row
+  // group, tile count), so no block leaves most of its waves idle; generation
+  // order is kept in each XCD's queue so the blocks of a row group stay
+  // adjacent and share keys and values.  W = 8 (the N <= 512 instance) and
+  // W = 16 (the 16-wave N <= 256 instance).
+  auto pair_attn_items = [&](int32_t W) {
     std::vector<std::array<int32_t, 4>> items;
     std::vector<double> cost;
     for (int32_t i = 0; i < batch; ++i) {
       const int32_t n = lengths[i], tiles = (n + 15) / 16;
-      const int32_t blocks = (tiles + kAttnQB / 16 - 1) / (kAttnQB / 16);
+      const int32_t blocks = (tiles + W - 1) / W;
       for (int32_t rg = 0; rg * kAttnRG < n; ++rg)
         for (int32_t b = 0; b < blocks; ++b) {
           const int32_t t0 = b * tiles / blocks, t1 = (b + 1) * tiles / blocks;
@@ -146,8 +147,10 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L) {
           cost.push_back((double)std::min(kAttnRG, n - rg * kAttnRG) * std::min(16 * (t1 - t0), n - 16 * t0) * n);
         }
     }
-    L->pattn_work = xcd_order<4>(items, cost, false);
-  }
+    return xcd_order<4>(items, cost, false);
+  };
+  L->pattn_work = pair_attn_items(kAttnQB / 16);
+  L->pattn16_work = pair_attn_items(16);
   // 1-D attention: the same even split of a sample's 16-query tiles over
   // blocks of at most kAttnQB queries, one item per block
   {
