@@ -1428,28 +1428,31 @@ __global__ void __launch_bounds__(256) swiglu_kernel(SwiArgs p) {
 }
 
 // ---------------------------------------------------------------- transition
-// Persistent pre-normalised SwiGLU transition for K = N in {64, 128}: eight
-// waves share a pass of 256 rows (32 per wave, held as matrix-core B
+// Persistent pre-normalised SwiGLU transition for K = N in {64, 128}: four
+// waves share a pass of 128 rows (32 per wave, held as matrix-core B
 // fragments in registers), and the hidden width is walked in chunks of 32.
+// Two such workgroups share a CU, each with its own weight ring, so one keeps
+// the CU busy while the other waits at its per-chunk barrier.
 //   * LayerNorm runs in registers: the four lanes l16 + 16 g of a row hold
-//     its K values between them, so statistics are two shuffles away.
+//     its K values between them, so statistics are two lane swaps away.
 //   * A chunk's weights -- gate and up rows, and the matching 32 columns of
 //     the down projection -- are copied straight from global memory into LDS
 //     as fragment images (global_load_lds: lane l's 16 bytes land at byte
-//     16 l, exactly the order the matrix cores consume), four buffers deep:
-//     a step reads two chunks (see the pipelined loop below) while the copies
-//     of the next two are in flight, and every LDS read is one
-//     conflict-free 1 KB wave read.
+//     16 l, exactly the order the matrix cores consume), three buffers deep:
+//     a step reads two chunks (see the pipelined loop below) while the copy
+//     of the next one is in flight, and every LDS read is one conflict-free
+//     1 KB wave read.
 //   * Hidden units are permuted inside a chunk: row r of the gate/up
 //     fragment ft is hidden unit 8 (r/4) + 4 ft + r%4, so a lane of k-group
 //     g ends up holding hidden units 8g .. 8g+7 of its row -- the B operand
 //     of the down projection, whose fragment then reads 16 contiguous bytes
 //     of each down-projection row.  The gated hidden never leaves registers.
-constexpr int kTrThreads = 512;
+constexpr int kTrThreads = 256;                   // 4 waves; two workgroups share a CU
 constexpr int kTrMT = 2;                          // 16-row subtiles per wave
-constexpr int kTrRows = 8 * 16 * kTrMT;           // rows per pass
-constexpr int kTrBufs = 4;                        // chunk buffers in LDS
-constexpr int kTrMaxHidden = 2048;                // largest hidden width (bias table size)
+constexpr int kTrWaves = kTrThreads / 64;
+constexpr int kTrRows = kTrWaves * 16 * kTrMT;    // rows per pass
+constexpr int kTrBufs = 3;                        // chunk buffers in LDS
+constexpr int kTrMaxHidden = 768;                 // largest hidden width (bias table size; two workgroups fit LDS)
 
 template <int K>
 constexpr int tr_chunk_frags() { return 4 * (K / 32) + K / 16; }   // gate + up + down images
@@ -1460,10 +1463,9 @@ constexpr size_t tr_smem_bytes() {
 }
 
 template <int K>
-__global__ void __launch_bounds__(kTrThreads, 1) transition_kernel(SwiArgs p) {
+__global__ void __launch_bounds__(kTrThreads, 2) transition_kernel(SwiArgs p) {
   constexpr int N = K, KT = K / 32, NT = N / 16;
   constexpr int CF = tr_chunk_frags<K>();
-  constexpr int DMA_PER_WAVE = CF / 8;            // images each wave copies per chunk (exact for K = 128)
   extern __shared__ __attribute__((aligned(16))) bf16 smem[];
   // The tables live in their own LDS object, which lets the compiler see
   // that reading them does not depend on the weight copies in flight.
@@ -1491,7 +1493,7 @@ __global__ void __launch_bounds__(kTrThreads, 1) transition_kernel(SwiArgs p) {
     const int f0 = f * 32;
     bf16* W = Wb + buf * CF * 512;
 #pragma unroll
-    for (int im = wave; im < CF; im += 8) {
+    for (int im = wave; im < CF; im += kTrWaves) {
       const bf16* src;
       if (im < 4 * KT) {                          // gate (im < 2 KT) or up image (ft, kk)
         const int which = im / (2 * KT), ft = (im / KT) & 1, kk = im % KT;
@@ -1508,7 +1510,6 @@ __global__ void __launch_bounds__(kTrThreads, 1) transition_kernel(SwiArgs p) {
   __syncthreads();                                    // tables visible
   dma_chunk(0, 0);
   dma_chunk(1 % nch, 1);
-  dma_chunk(2 % nch, 2);
 
   bf16x8 xf[kTrMT][KT];
   f32x4 accY[NT][kTrMT];
@@ -1570,7 +1571,7 @@ __global__ void __launch_bounds__(kTrThreads, 1) transition_kernel(SwiArgs p) {
     __syncthreads();
 
     // ---- hidden chunks ----------------------------------------------------
-    // Chunk c lives in ring slot q % kTrBufs; its copies are issued three
+    // Chunk c lives in ring slot q % kTrBufs; its copies are issued two
     // chunks ahead.  The loop is software-pipelined: step c issues the gate
     // and up products of chunk c + 1 first, then gates chunk c and runs its
     // down projection, so the matrix cores work on the next chunk while the
@@ -1638,7 +1639,7 @@ __global__ void __launch_bounds__(kTrThreads, 1) transition_kernel(SwiArgs p) {
     constexpr int EPS = 8 * kTrMT / NSTEP;              // gated values per step
     static_assert(EPS * NSTEP == 8 * kTrMT, "gating must split evenly over the product steps");
     for (int c = 0; c < nch; ++c, ++q) {
-      dma_chunk((c + 3) % nch, (q + 3) % kTrBufs);   // three chunks ahead, cycling into the next pass
+      dma_chunk((c + 2) % nch, (q + 2) % kTrBufs);   // two chunks ahead, cycling into the next pass
       const bf16* W = Wb + (q % kTrBufs) * CF * 512;
       const bf16* Wn = Wb + ((q + 1) % kTrBufs) * CF * 512;
       float bg[8], bu[8];
@@ -1678,11 +1679,10 @@ __global__ void __launch_bounds__(kTrThreads, 1) transition_kernel(SwiArgs p) {
       for (int ft = 0; ft < 2; ++ft)
 #pragma unroll
         for (int mt = 0; mt < kTrMT; ++mt) { accG[ft][mt] = nG[ft][mt]; accU[ft][mt] = nU[ft][mt]; }
-      // chunk c + 2 (copied a step ago) must have landed in every wave
+      // chunk c + 2 (copied at this step) must have landed in every wave
       // before the next step reads it as "chunk c + 1"; after the barrier
       // this chunk's slot is free for the copy issued at the next step
-      if (K == 128 && c + 1 < nch) __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8) | DMA_PER_WAVE);  // vmcnt(3)
-      else __builtin_amdgcn_s_waitcnt(0);
+      __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
     }
 
@@ -1893,7 +1893,7 @@ hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
     const size_t tr_smem = a.c_in == 64 ? tr_smem_bytes<64>() : tr_smem_bytes<128>();
     if ((a.c_in == 64 || a.c_in == 128) && a.c_out == a.c_in && a.hidden <= kTrMaxHidden) {
       const int nrb = (rows + kTrRows - 1) / kTrRows;
-      const int grid = std::min(nrb, compute_units());
+      const int grid = std::min(nrb, 2 * compute_units());
       const size_t smem = tr_smem;
       if (a.c_in == 64) {
         hipFuncSetAttribute((const void*)transition_kernel<64>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
