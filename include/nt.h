@@ -33,8 +33,8 @@
  * mirrors are owned by the library from nt_from_* until nt_layout_destroy;
  * the caller must not destroy a layout while work that uses it is queued.
  * Two ops allocate scratch of their own: nt_pair_row_attention keeps a
- * workspace in the layout and nt_layernorm_linear (large K with a LayerNorm)
- * one per device (see there).
+ * workspace in the layout and nt_layernorm_linear (large K with a LayerNorm,
+ * and the SwiGLU transition) one per device (see there).
  *
  * Streams: every op enqueues asynchronously on the caller's HIP stream
  * (NULL = the default stream) and returns without synchronising.  Only
@@ -208,13 +208,15 @@ typedef struct {
   const nt_layout* residual_layout;  /* optional: must be compatible with layout */
 } nt_linear_args;
 
-/* Workspace: a bf16 call with a LayerNorm, bf16 x, K >= 384 (K % 32 == 0,
- * K <= 4096), N % 8 == 0 and no tail first writes LN(x) (rounded to bf16, as
- * the product consumes it) into a per-device workspace owned by the library,
- * R * K * 2 bytes, allocated by the first such call and regrown (after a
- * device synchronisation) when a later call needs more; it lives until the
- * process ends.  Such calls on one device must therefore be ordered (one
- * stream, or synchronised), not concurrent.
+/* Workspace: two kinds of bf16 call use a per-device workspace owned by the
+ * library: one with a LayerNorm, bf16 x, K >= 384 (K % 32 == 0, K <= 4096),
+ * N % 8 == 0 and no tail first writes LN(x) (rounded to bf16, as the product
+ * consumes it) there, R * K * 2 bytes; a SwiGLU transition with K in {64, 128}
+ * and F <= 768 first copies its weights there in the order its kernel
+ * consumes them, 3 * F * K * 2 bytes.  The workspace is allocated by the first
+ * such call and regrown (after a device synchronisation) when a later call
+ * needs more; it lives until the process ends.  Such calls on one device must
+ * therefore be ordered (one stream, or synchronised), not concurrent.
  * Errors: NT_ERR_INVALID_ARG, NT_ERR_LAYOUT_MISMATCH (residual_layout differs
  * from layout, or rows differ from the layout's count), NT_ERR_UNSUPPORTED
  * (bf16 SwiGLU unless x is bf16, K == N in {64, 128, 256} and F % 32 == 0;

@@ -1249,6 +1249,7 @@ struct SwiArgs {
   int64_t ld_res;
   bf16* y;
   int64_t ldy;
+  const bf16* wimg;    // transition: weights in chunk/fragment-image order, or NULL
 };
 
 template <int MT, int K, int N>
@@ -1462,6 +1463,34 @@ constexpr size_t tr_smem_bytes() {
   return sizeof(bf16) * (size_t)kTrBufs * tr_chunk_frags<K>() * 512;
 }
 
+// Weights of the transition in the order its chunks are consumed: for hidden
+// chunk f (32 units) the CF fragment images, each 64 lanes x 8 elements.
+//   gate/up image (which, ft, kk), lane (l16, g): row which*F + hid with
+//     hid = 32 f + 8 (l16 / 4) + 4 ft + l16 % 4, columns 32 kk + 8 g .. +7
+//     (hidden units permuted so a lane's gated values are 8 contiguous units);
+//   down image a, lane (l16, g): row 16 a + l16 of W2, columns 32 f + 8 g ..
+// One thread per 16-byte lane piece.
+template <int K>
+__global__ void __launch_bounds__(256) transition_image_kernel(const bf16* w, const bf16* w2, int F, bf16* img) {
+  constexpr int KT = K / 32;
+  constexpr int CF = tr_chunk_frags<K>();
+  const int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;  // piece index
+  const int64_t total = (int64_t)(F / 32) * CF * 64;
+  if (u >= total) return;
+  const int lane = (int)(u % 64), im = (int)((u / 64) % CF), f = (int)(u / (64 * CF));
+  const int l16 = lane & 15, g = lane >> 4;
+  const bf16* src;
+  if (im < 4 * KT) {
+    const int which = im / (2 * KT), ft = (im / KT) & 1, kk = im % KT;
+    const int hid = f * 32 + 8 * (l16 >> 2) + 4 * ft + (l16 & 3);
+    src = w + (int64_t)(which * F + hid) * K + kk * 32 + g * 8;
+  } else {
+    const int a = im - 4 * KT;
+    src = w2 + (int64_t)(a * 16 + l16) * F + f * 32 + g * 8;
+  }
+  *reinterpret_cast<uint4*>(img + u * 8) = *reinterpret_cast<const uint4*>(src);
+}
+
 template <int K>
 __global__ void __launch_bounds__(kTrThreads, 2) transition_kernel(SwiArgs p) {
   constexpr int N = K, KT = K / 32, NT = N / 16;
@@ -1489,22 +1518,14 @@ __global__ void __launch_bounds__(kTrThreads, 2) transition_kernel(SwiArgs p) {
   }
 
   // ---- chunk copies: image im of chunk f into buffer buf --------------------
+  // The weight image holds chunk f's CF fragment images contiguously
+  // (transition_image_kernel), so every copy reads 1 KB in one piece.
   auto dma_chunk = [&](int f, int buf) {
-    const int f0 = f * 32;
     bf16* W = Wb + buf * CF * 512;
+    const bf16* img = p.wimg + (int64_t)f * CF * 512 + lane * 8;
 #pragma unroll
-    for (int im = wave; im < CF; im += kTrWaves) {
-      const bf16* src;
-      if (im < 4 * KT) {                          // gate (im < 2 KT) or up image (ft, kk)
-        const int which = im / (2 * KT), ft = (im / KT) & 1, kk = im % KT;
-        const int hid = f0 + 8 * (l16 >> 2) + 4 * ft + (l16 & 3);
-        src = p.w + (int64_t)(which * p.F + hid) * K + kk * 32 + g * 8;
-      } else {                                    // down image a: rows 16a + l16, hidden 8g ..
-        const int a = im - 4 * KT;
-        src = p.w2 + (int64_t)(a * 16 + l16) * p.F + f0 + g * 8;
-      }
-      __builtin_amdgcn_global_load_lds((const void*)src, (__attribute__((address_space(3))) void*)(W + im * 512), 16, 0, 0);
-    }
+    for (int im = wave; im < CF; im += kTrWaves)
+      __builtin_amdgcn_global_load_lds((const void*)(img + im * 512), (__attribute__((address_space(3))) void*)(W + im * 512), 16, 0, 0);
   };
 
   __syncthreads();                                    // tables visible
@@ -1895,6 +1916,17 @@ hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
       const int nrb = (rows + kTrRows - 1) / kTrRows;
       const int grid = std::min(nrb, 2 * compute_units());
       const size_t smem = tr_smem;
+      // weights in consumption order, in the device workspace
+      const int nch = a.hidden / 32;
+      const size_t img_elems = (size_t)nch * (a.c_in == 64 ? tr_chunk_frags<64>() : tr_chunk_frags<128>()) * 512;
+      void* ws = nullptr;
+      hipError_t e = device_workspace(img_elems * sizeof(bf16), &ws);
+      if (e != hipSuccess) return e;
+      w.wimg = static_cast<const bf16*>(ws);
+      const unsigned ig = (unsigned)((img_elems / 8 + 255) / 256);
+      if (a.c_in == 64) transition_image_kernel<64><<<dim3(ig), dim3(256), 0, s>>>(w.w, w.w2, a.hidden, (bf16*)ws);
+      else transition_image_kernel<128><<<dim3(ig), dim3(256), 0, s>>>(w.w, w.w2, a.hidden, (bf16*)ws);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
       if (a.c_in == 64) {
         hipFuncSetAttribute((const void*)transition_kernel<64>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
         transition_kernel<64><<<dim3((unsigned)grid), dim3(kTrThreads), smem, s>>>(w);
