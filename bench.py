@@ -32,23 +32,23 @@ F32_PEAK_TFLOPS = 157.3        # fp32 vector
 # rocprofv3 --pmc FETCH_SIZE and --pmc WRITE_SIZE passes (KiB per dispatch),
 # tagged with a hash of the kernel's source file (plus the shared device
 # header) at the time the counters were taken.  A plain 256 MiB device copy
-# reads 131,083 KiB on FETCH_SIZE and 262,144 KiB on WRITE_SIZE, so bytes =
+# reads 131,087 KiB on FETCH_SIZE and 262,144 KiB on WRITE_SIZE, so bytes =
 # 2.0 x FETCH_SIZE + 1.0 x WRITE_SIZE.  When the source hash no longer
 # matches, the kernel has changed since the counters and traffic is null.
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 COUNTER_WORKLOAD = "pair_b8_n208_224_bf16"
 COUNTERS = {  # op: (kernel source, source hash, FETCH_SIZE KiB, WRITE_SIZE KiB)
-    "attention_row": ("k_attention.hip", "85e05222acec14a1", 175893, 96233),
-    "transition": ("k_linear.hip", "937763db3aad8bda", 72770, 94314),
-    "triangle_out": ("k_triangle.hip", "7a4aa0ad16c08dba", 305493, 91403),
-    "attn_proj": ("k_linear.hip", "937763db3aad8bda", 46043, 276211),
-    "tri_proj": ("k_linear.hip", "937763db3aad8bda", 45830, 197120),
-    "ln_linear": ("k_linear.hip", "937763db3aad8bda", 45775, 90997),
-    "attn_out_residual": ("k_linear.hip", "937763db3aad8bda", 91301, 90996),
-    "single_proj": ("k_linear.hip", "937763db3aad8bda", 3368, 853),
-    "pair_broadcast": ("k_segment.hip", "a2aacf3085c626e1", 1999, 90996),
+    "attention_row": ("k_attention.hip", "7de75a2977e897f8", 142570, 90997),
+    "transition": ("k_linear.hip", "5da75a59fb862322", 50634, 90997),
+    "triangle_out": ("k_triangle.hip", "3a2d7b8ae374561a", 301099, 92083),
+    "attn_proj": ("k_linear.hip", "5da75a59fb862322", 46041, 276220),
+    "tri_proj": ("k_linear.hip", "5da75a59fb862322", 45829, 197120),
+    "ln_linear": ("k_linear.hip", "5da75a59fb862322", 45777, 90996),
+    "attn_out_residual": ("k_linear.hip", "5da75a59fb862322", 91273, 90996),
+    "single_proj": ("k_linear.hip", "5da75a59fb862322", 3368, 853),
+    "pair_broadcast": ("k_segment.hip", "a2aacf3085c626e1", 1998, 90996),
     "segment_mean": ("k_segment.hip", "a2aacf3085c626e1", 45570, 853),
-    "single_update": ("k_linear.hip", "937763db3aad8bda", 3632, 1280),
+    "single_update": ("k_linear.hip", "5da75a59fb862322", 3632, 1280),
 }
 
 
