@@ -39,7 +39,7 @@ FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 COUNTER_WORKLOAD = "pair_b8_n208_224_bf16"
 COUNTERS = {  # op: (kernel source, source hash, FETCH_SIZE KiB, WRITE_SIZE KiB)
     "attention_row": ("k_attention.hip", "7de75a2977e897f8", 142570, 90997),
-    "transition": ("k_linear.hip", "5da75a59fb862322", 50634, 90997),
+    "transition": ("k_transition.hip", "unmeasured", 0, 0),
     "triangle_out": ("k_triangle.hip", "3a2d7b8ae374561a", 301099, 92083),
     "attn_proj": ("k_linear.hip", "5da75a59fb862322", 46041, 276220),
     "tri_proj": ("k_linear.hip", "5da75a59fb862322", 45829, 197120),

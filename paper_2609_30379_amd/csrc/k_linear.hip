@@ -1249,7 +1249,6 @@ struct SwiArgs {
   int64_t ld_res;
   bf16* y;
   int64_t ldy;
-  const bf16* wimg;    // transition: weights in chunk/fragment-image order, or NULL
 };
 
 template <int MT, int K, int N>
@@ -1428,307 +1427,6 @@ __global__ void __launch_bounds__(256) swiglu_kernel(SwiArgs p) {
   }
 }
 
-// ---------------------------------------------------------------- transition
-// Persistent pre-normalised SwiGLU transition for K = N in {64, 128}: four
-// waves share a pass of 128 rows (32 per wave, held as matrix-core B
-// fragments in registers), and the hidden width is walked in chunks of 32.
-// Two such workgroups share a CU, each with its own weight ring, so one keeps
-// the CU busy while the other waits at its per-chunk barrier.
-//   * LayerNorm runs in registers: the four lanes l16 + 16 g of a row hold
-//     its K values between them, so statistics are two lane swaps away.
-//   * A chunk's weights -- gate and up rows, and the matching 32 columns of
-//     the down projection -- are copied straight from global memory into LDS
-//     as fragment images (global_load_lds: lane l's 16 bytes land at byte
-//     16 l, exactly the order the matrix cores consume), three buffers deep:
-//     a step reads two chunks (see the pipelined loop below) while the copy
-//     of the next one is in flight, and every LDS read is one conflict-free
-//     1 KB wave read.
-//   * Hidden units are permuted inside a chunk: row r of the gate/up
-//     fragment ft is hidden unit 8 (r/4) + 4 ft + r%4, so a lane of k-group
-//     g ends up holding hidden units 8g .. 8g+7 of its row -- the B operand
-//     of the down projection, whose fragment then reads 16 contiguous bytes
-//     of each down-projection row.  The gated hidden never leaves registers.
-constexpr int kTrThreads = 256;                   // 4 waves; two workgroups share a CU
-constexpr int kTrMT = 2;                          // 16-row subtiles per wave
-constexpr int kTrWaves = kTrThreads / 64;
-constexpr int kTrRows = kTrWaves * 16 * kTrMT;    // rows per pass
-constexpr int kTrBufs = 3;                        // chunk buffers in LDS
-constexpr int kTrMaxHidden = 768;                 // largest hidden width (bias table size; two workgroups fit LDS)
-
-template <int K>
-constexpr int tr_chunk_frags() { return 4 * (K / 32) + K / 16; }   // gate + up + down images
-
-template <int K>
-constexpr size_t tr_smem_bytes() {
-  return sizeof(bf16) * (size_t)kTrBufs * tr_chunk_frags<K>() * 512;
-}
-
-// Weights of the transition in the order its chunks are consumed: for hidden
-// chunk f (32 units) the CF fragment images, each 64 lanes x 8 elements.
-//   gate/up image (which, ft, kk), lane (l16, g): row which*F + hid with
-//     hid = 32 f + 8 (l16 / 4) + 4 ft + l16 % 4, columns 32 kk + 8 g .. +7
-//     (hidden units permuted so a lane's gated values are 8 contiguous units);
-//   down image a, lane (l16, g): row 16 a + l16 of W2, columns 32 f + 8 g ..
-// One thread per 16-byte lane piece.
-template <int K>
-__global__ void __launch_bounds__(256) transition_image_kernel(const bf16* w, const bf16* w2, int F, bf16* img) {
-  constexpr int KT = K / 32;
-  constexpr int CF = tr_chunk_frags<K>();
-  const int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;  // piece index
-  const int64_t total = (int64_t)(F / 32) * CF * 64;
-  if (u >= total) return;
-  const int lane = (int)(u % 64), im = (int)((u / 64) % CF), f = (int)(u / (64 * CF));
-  const int l16 = lane & 15, g = lane >> 4;
-  const bf16* src;
-  if (im < 4 * KT) {
-    const int which = im / (2 * KT), ft = (im / KT) & 1, kk = im % KT;
-    const int hid = f * 32 + 8 * (l16 >> 2) + 4 * ft + (l16 & 3);
-    src = w + (int64_t)(which * F + hid) * K + kk * 32 + g * 8;
-  } else {
-    const int a = im - 4 * KT;
-    src = w2 + (int64_t)(a * 16 + l16) * F + f * 32 + g * 8;
-  }
-  *reinterpret_cast<uint4*>(img + u * 8) = *reinterpret_cast<const uint4*>(src);
-}
-
-template <int K>
-__global__ void __launch_bounds__(kTrThreads, 2) transition_kernel(SwiArgs p) {
-  constexpr int N = K, KT = K / 32, NT = N / 16;
-  constexpr int CF = tr_chunk_frags<K>();
-  extern __shared__ __attribute__((aligned(16))) bf16 smem[];
-  // The tables live in their own LDS object, which lets the compiler see
-  // that reading them does not depend on the weight copies in flight.
-  __shared__ __attribute__((aligned(16))) float s_tab[2 * kTrMaxHidden + 3 * K];
-  bf16* Wb = smem;                                    // kTrBufs x CF fragment images
-  float* s_b = s_tab;                                 // [2F] gate/up bias
-  float* s_b2 = s_b + 2 * p.F;                        // [N] down bias
-  float* s_g = s_b2 + N;                              // [K] LayerNorm gamma, then beta
-  float* s_be = s_g + K;
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int l16 = lane & 15, g = lane >> 4;
-  const int nch = p.F / 32;
-  const int nrb = (p.rows + kTrRows - 1) / kTrRows;
-  if ((int)blockIdx.x >= nrb) return;
-  for (int j = tid; j < 2 * p.F; j += kTrThreads) s_b[j] = p.bias ? p.bias[j] : 0.f;
-  for (int j = tid; j < N; j += kTrThreads) s_b2[j] = p.bias2 ? p.bias2[j] : 0.f;
-  for (int j = tid; j < K; j += kTrThreads) {
-    s_g[j] = p.gamma ? p.gamma[j] : 1.f;
-    s_be[j] = p.beta ? p.beta[j] : 0.f;
-  }
-
-  // ---- chunk copies: image im of chunk f into buffer buf --------------------
-  // The weight image holds chunk f's CF fragment images contiguously
-  // (transition_image_kernel), so every copy reads 1 KB in one piece.
-  auto dma_chunk = [&](int f, int buf) {
-    bf16* W = Wb + buf * CF * 512;
-    const bf16* img = p.wimg + (int64_t)f * CF * 512 + lane * 8;
-#pragma unroll
-    for (int im = wave; im < CF; im += kTrWaves)
-      __builtin_amdgcn_global_load_lds((const void*)(img + im * 512), (__attribute__((address_space(3))) void*)(W + im * 512), 16, 0, 0);
-  };
-
-  __syncthreads();                                    // tables visible
-  dma_chunk(0, 0);
-  dma_chunk(1 % nch, 1);
-
-  bf16x8 xf[kTrMT][KT];
-  f32x4 accY[NT][kTrMT];
-  int q = 0;                                          // global chunk step
-  for (int rb = blockIdx.x; rb < nrb; rb += gridDim.x) {
-    // ---- LayerNorm of the pass's rows, straight into B fragments ----------
-    {
-      uint4 raw[kTrMT][KT];
-#pragma unroll
-      for (int mt = 0; mt < kTrMT; ++mt) {
-        const int m = rb * kTrRows + wave * 16 * kTrMT + mt * 16 + l16;
-#pragma unroll
-        for (int kk = 0; kk < KT; ++kk)
-          raw[mt][kk] = m < p.rows ? *reinterpret_cast<const uint4*>(p.x + (int64_t)m * p.ldx + kk * 32 + g * 8)
-                                   : make_uint4(0u, 0u, 0u, 0u);
-      }
-#pragma unroll
-      for (int mt = 0; mt < kTrMT; ++mt) {
-        const int m = rb * kTrRows + wave * 16 * kTrMT + mt * 16 + l16;
-        float s = 0.f;
-#pragma unroll
-        for (int kk = 0; kk < KT; ++kk) {
-          float t[8];
-          XStage<bf16>::unpack(raw[mt][kk], t);
-#pragma unroll
-          for (int e = 0; e < 8; ++e) s += t[e];
-        }
-        const float mean = sum_over_kgroups(s) / (float)K;
-        float qv = 0.f;
-#pragma unroll
-        for (int kk = 0; kk < KT; ++kk) {
-          float t[8];
-          XStage<bf16>::unpack(raw[mt][kk], t);
-#pragma unroll
-          for (int e = 0; e < 8; ++e) { const float d = t[e] - mean; qv += d * d; }
-        }
-        const float rstd = rsqrtf(sum_over_kgroups(qv) / (float)K + p.eps);
-#pragma unroll
-        for (int kk = 0; kk < KT; ++kk) {
-          float t[8];
-          XStage<bf16>::unpack(raw[mt][kk], t);
-          const int k0 = kk * 32 + g * 8;
-          const float4 g0 = *reinterpret_cast<const float4*>(&s_g[k0]), g1 = *reinterpret_cast<const float4*>(&s_g[k0 + 4]);
-          const float4 b0 = *reinterpret_cast<const float4*>(&s_be[k0]), b1 = *reinterpret_cast<const float4*>(&s_be[k0 + 4]);
-          const float gg[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
-          const float bb[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
-#pragma unroll
-          for (int e = 0; e < 8; ++e) xf[mt][kk][e] = (bf16)(m < p.rows ? (t[e] - mean) * rstd * gg[e] + bb[e] : 0.f);
-        }
-      }
-    }
-#pragma unroll
-    for (int a = 0; a < NT; ++a)
-#pragma unroll
-      for (int mt = 0; mt < kTrMT; ++mt) accY[a][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    // the pass's first chunk has landed in every wave (on later passes this
-    // repeats the previous step's wait)
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-
-    // ---- hidden chunks ----------------------------------------------------
-    // Chunk c lives in ring slot q % kTrBufs; its copies are issued two
-    // chunks ahead.  The loop is software-pipelined: step c issues the gate
-    // and up products of chunk c + 1 first, then gates chunk c and runs its
-    // down projection, so the matrix cores work on the next chunk while the
-    // vector units evaluate SiLU.  At the last chunk of a pass the products
-    // "of chunk c + 1" use the next pass's first weights with this pass's
-    // rows and are discarded (keeping the step free of branches).
-    // gate and up biases of the chunk at hidden offset f0: slot j = 4 ft + i
-    // of lane group g is hidden unit f0 + 8g + j.  The reads come from inline
-    // assembly with their own wait: the compiler would otherwise wait for the
-    // weight copies in flight first.
-    auto read_bias = [&](int f0, float (&bg)[8], float (&bu)[8]) {
-      float4 bg0, bg1, bu0, bu1;
-      const uint32_t ag = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) float*)(&s_b[f0 + 8 * g]);
-      const uint32_t au = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) float*)(&s_b[p.F + f0 + 8 * g]);
-      asm volatile(
-          "ds_read_b128 %0, %4\n"
-          "ds_read_b128 %1, %4 offset:16\n"
-          "ds_read_b128 %2, %5\n"
-          "ds_read_b128 %3, %5 offset:16\n"
-          "s_waitcnt lgkmcnt(0)"
-          : "=&v"(bg0), "=&v"(bg1), "=&v"(bu0), "=&v"(bu1)
-          : "v"(ag), "v"(au)
-          : "memory");
-      bg[0] = bg0.x; bg[1] = bg0.y; bg[2] = bg0.z; bg[3] = bg0.w; bg[4] = bg1.x; bg[5] = bg1.y; bg[6] = bg1.z; bg[7] = bg1.w;
-      bu[0] = bu0.x; bu[1] = bu0.y; bu[2] = bu0.z; bu[3] = bu0.w; bu[4] = bu1.x; bu[5] = bu1.y; bu[6] = bu1.z; bu[7] = bu1.w;
-    };
-    // gate and up products of one chunk, accumulators seeded with the biases
-    auto seed = [&](const float (&bg)[8], const float (&bu)[8], f32x4 (&aG)[2][kTrMT], f32x4 (&aU)[2][kTrMT]) {
-#pragma unroll
-      for (int ft = 0; ft < 2; ++ft)
-#pragma unroll
-        for (int mt = 0; mt < kTrMT; ++mt) {
-          aG[ft][mt] = f32x4{bg[4 * ft], bg[4 * ft + 1], bg[4 * ft + 2], bg[4 * ft + 3]};
-          aU[ft][mt] = f32x4{bu[4 * ft], bu[4 * ft + 1], bu[4 * ft + 2], bu[4 * ft + 3]};
-        }
-    };
-    // gate/up fragments of product step st = 2 kk + ft
-    auto gu_frags = [&](const bf16* W, int st, bf16x8& ag, bf16x8& au) {
-      const int kk = st >> 1, ft = st & 1;
-      ag = *reinterpret_cast<const bf16x8*>(&W[(ft * KT + kk) * 512 + lane * 8]);
-      au = *reinterpret_cast<const bf16x8*>(&W[((2 + ft) * KT + kk) * 512 + lane * 8]);
-    };
-    auto gu_step = [&](int st, const bf16x8& ag, const bf16x8& au, f32x4 (&aG)[2][kTrMT], f32x4 (&aU)[2][kTrMT]) {
-      const int kk = st >> 1, ft = st & 1;
-#pragma unroll
-      for (int mt = 0; mt < kTrMT; ++mt) {
-        aG[ft][mt] = mfma16(ag, xf[mt][kk], aG[ft][mt]);
-        aU[ft][mt] = mfma16(au, xf[mt][kk], aU[ft][mt]);
-      }
-    };
-    f32x4 accG[2][kTrMT], accU[2][kTrMT];
-    {
-      float bg[8], bu[8];
-      read_bias(0, bg, bu);
-      seed(bg, bu, accG, accU);
-      const bf16* W0 = Wb + (q % kTrBufs) * CF * 512;
-#pragma unroll
-      for (int st = 0; st < 2 * KT; ++st) {
-        bf16x8 ag, au;
-        gu_frags(W0, st, ag, au);
-        gu_step(st, ag, au, accG, accU);
-      }
-    }
-    constexpr int NSTEP = 2 * KT;                       // gate/up product steps per chunk
-    constexpr int EPS = 8 * kTrMT / NSTEP;              // gated values per step
-    static_assert(EPS * NSTEP == 8 * kTrMT, "gating must split evenly over the product steps");
-    for (int c = 0; c < nch; ++c, ++q) {
-      dma_chunk((c + 2) % nch, (q + 2) % kTrBufs);   // two chunks ahead, cycling into the next pass
-      const bf16* W = Wb + (q % kTrBufs) * CF * 512;
-      const bf16* Wn = Wb + ((q + 1) % kTrBufs) * CF * 512;
-      float bg[8], bu[8];
-      read_bias(((c + 1) % nch) * 32, bg, bu);
-      f32x4 nG[2][kTrMT], nU[2][kTrMT];
-      seed(bg, bu, nG, nU);
-      // Step st: the products of chunk c + 1 for step st (fragments read one
-      // step ahead), then EPS gated values of chunk c -- so SiLU runs on the
-      // vector units while the products occupy the matrix cores.  The
-      // scheduling barriers keep that order.  Gated value e = 8 mt + j (slot
-      // j = 4 ft + i of lane group g: hidden unit 32 c + 8g + j).
-      bf16x8 hv[kTrMT];
-      bf16x8 ag, au;
-      gu_frags(Wn, 0, ag, au);
-#pragma unroll
-      for (int st = 0; st < NSTEP; ++st) {
-        bf16x8 agn, aun;
-        if (st + 1 < NSTEP) gu_frags(Wn, st + 1, agn, aun);
-        gu_step(st, ag, au, nG, nU);
-#pragma unroll
-        for (int u = 0; u < EPS; ++u) {
-          const int e = st * EPS + u, mt = e >> 3, j = e & 7;
-          const float gv = accG[j >> 2][mt][j & 3];
-          const float uv = accU[j >> 2][mt][j & 3];
-          hv[mt][j] = (bf16)(gv * __builtin_amdgcn_rcpf(1.f + __expf(-gv)) * uv);
-        }
-        if (st + 1 < NSTEP) { ag = agn; au = aun; }
-        __builtin_amdgcn_sched_barrier(0);
-      }
-#pragma unroll
-      for (int a = 0; a < NT; ++a) {
-        const bf16x8 ad = *reinterpret_cast<const bf16x8*>(&W[(4 * KT + a) * 512 + lane * 8]);
-#pragma unroll
-        for (int mt = 0; mt < kTrMT; ++mt) accY[a][mt] = mfma16(ad, hv[mt], accY[a][mt]);
-      }
-#pragma unroll
-      for (int ft = 0; ft < 2; ++ft)
-#pragma unroll
-        for (int mt = 0; mt < kTrMT; ++mt) { accG[ft][mt] = nG[ft][mt]; accU[ft][mt] = nU[ft][mt]; }
-      // chunk c + 2 (copied at this step) must have landed in every wave
-      // before the next step reads it as "chunk c + 1"; after the barrier
-      // this chunk's slot is free for the copy issued at the next step
-      __builtin_amdgcn_s_waitcnt(0);
-      __syncthreads();
-    }
-
-    // ---- epilogue: residual + bias, lane owns channels n..n+3 of row m ----
-#pragma unroll
-    for (int mt = 0; mt < kTrMT; ++mt) {
-      const int m = rb * kTrRows + wave * 16 * kTrMT + mt * 16 + l16;
-      if (m >= p.rows) continue;
-#pragma unroll
-      for (int a = 0; a < NT; ++a) {
-        const int n = a * 16 + 4 * g;
-        const uint2 rr = *reinterpret_cast<const uint2*>(p.res + (int64_t)m * p.ld_res + n);
-        const float4 b2 = *reinterpret_cast<const float4*>(&s_b2[n]);
-        bf16x4 o;
-        o[0] = (bf16)(accY[a][mt][0] + b2.x + __uint_as_float(rr.x << 16));
-        o[1] = (bf16)(accY[a][mt][1] + b2.y + __uint_as_float(rr.x & 0xffff0000u));
-        o[2] = (bf16)(accY[a][mt][2] + b2.z + __uint_as_float(rr.y << 16));
-        o[3] = (bf16)(accY[a][mt][3] + b2.w + __uint_as_float(rr.y & 0xffff0000u));
-        *reinterpret_cast<bf16x4*>(p.y + (int64_t)m * p.ldy + n) = o;
-      }
-    }
-  }
-  __builtin_amdgcn_s_waitcnt(0);                      // no copy outstanding at exit
-}
-
 // ---------------------------------------------------------------- fp32 path
 // Plain fp32 FMA path (used by the fp32 workloads): RB rows per workgroup, one
 // wave normalises each row into LDS, then threads compute output channels.
@@ -1816,18 +1514,6 @@ __global__ void __launch_bounds__(256) linear_f32_kernel(F32Args p) {
   }
 }
 
-// Compute units of the current device (cached per device).
-int compute_units() {
-  static int cache[64] = {0};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cache[dev] == 0) {
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-    cache[dev] = n;
-  }
-  return cache[dev];
-}
 
 // One resident workgroup per slot: grid = min(tiles, resident workgroups per
 // CU x CUs); every workgroup walks tiles blockIdx.x + j * gridDim.x.
@@ -1871,6 +1557,19 @@ void launch_tiled(const LinArgs& p, hipStream_t s) {
 
 }  // namespace
 
+// Compute units of the current device (cached per device).
+int compute_units() {
+  static int cache[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cache[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cache[dev] = n;
+  }
+  return cache[dev];
+}
+
 hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
   const nt_linear_args& a = *plan.a;
   const int rows = (int)a.rows;
@@ -1911,30 +1610,16 @@ hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
     w.res = a.residual ? (const bf16*)a.residual : (const bf16*)a.x;
     w.ld_res = a.residual ? a.ld_residual : a.ldx;
     w.y = (bf16*)a.y; w.ldy = a.ldy;
-    const size_t tr_smem = a.c_in == 64 ? tr_smem_bytes<64>() : tr_smem_bytes<128>();
-    if ((a.c_in == 64 || a.c_in == 128) && a.c_out == a.c_in && a.hidden <= kTrMaxHidden) {
-      const int nrb = (rows + kTrRows - 1) / kTrRows;
-      const int grid = std::min(nrb, 2 * compute_units());
-      const size_t smem = tr_smem;
-      // weights in consumption order, in the device workspace
-      const int nch = a.hidden / 32;
-      const size_t img_elems = (size_t)nch * (a.c_in == 64 ? tr_chunk_frags<64>() : tr_chunk_frags<128>()) * 512;
+    if (transition_supported(a.c_in, a.c_out, a.hidden) && w.res == w.x && w.ld_res == w.ldx) {
+      TransArgs t{};
+      t.rows = rows; t.K = a.c_in; t.F = a.hidden;
+      t.x = w.x; t.ldx = w.ldx; t.gamma = w.gamma; t.beta = w.beta; t.eps = w.eps;
+      t.w = w.w; t.bias = w.bias; t.w2 = w.w2; t.bias2 = w.bias2;
+      t.y = w.y; t.ldy = w.ldy;
       void* ws = nullptr;
-      hipError_t e = device_workspace(img_elems * sizeof(bf16), &ws);
+      const hipError_t e = device_workspace(transition_image_bytes(a.c_in, a.hidden), &ws);
       if (e != hipSuccess) return e;
-      w.wimg = static_cast<const bf16*>(ws);
-      const unsigned ig = (unsigned)((img_elems / 8 + 255) / 256);
-      if (a.c_in == 64) transition_image_kernel<64><<<dim3(ig), dim3(256), 0, s>>>(w.w, w.w2, a.hidden, (bf16*)ws);
-      else transition_image_kernel<128><<<dim3(ig), dim3(256), 0, s>>>(w.w, w.w2, a.hidden, (bf16*)ws);
-      if ((e = hipGetLastError()) != hipSuccess) return e;
-      if (a.c_in == 64) {
-        hipFuncSetAttribute((const void*)transition_kernel<64>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-        transition_kernel<64><<<dim3((unsigned)grid), dim3(kTrThreads), smem, s>>>(w);
-      } else {
-        hipFuncSetAttribute((const void*)transition_kernel<128>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-        transition_kernel<128><<<dim3((unsigned)grid), dim3(kTrThreads), smem, s>>>(w);
-      }
-      return hipGetLastError();
+      return launch_transition(t, ws, s);
     }
     constexpr int MT = 2;
     const int rw = 4 * MT * 16;

@@ -105,6 +105,33 @@ bool gemm_fits(int K);
 // With gamma set, the rows are first normalised into the device workspace.
 hipError_t launch_gemm(GemmArgs p, hipStream_t s);
 
+// SwiGLU transition with residual (k_transition.hip):
+//   y = x + (silu(LN(x) W_g^T + b_g) * (LN(x) W_u^T + b_u)) W_d^T + b_d
+// for x, y [rows, K] bf16, w [2F, K] (gate rows, then up rows), w2 [K, F].
+constexpr int kTransitionMaxHidden = 768;
+struct TransArgs {
+  int rows, K, F;
+  const __bf16* x;
+  int64_t ldx;
+  const float* gamma;    // LayerNorm affine (NULL: 1 / 0)
+  const float* beta;
+  float eps;
+  const __bf16* w;
+  const float* bias;     // [2F] or NULL
+  const __bf16* w2;
+  const float* bias2;    // [K] or NULL
+  __bf16* y;             // may alias x
+  int64_t ldy;
+  const __bf16* wimg;    // set by the launcher: weights in consumption order
+};
+// The residual must be x itself (same rows and stride).
+bool transition_supported(int K, int N, int F);
+size_t transition_image_bytes(int K, int F);
+// wimg_workspace: transition_image_bytes(K, F) bytes of device memory that the
+// launch rewrites (weights in consumption order); calls sharing it must be ordered.
+hipError_t launch_transition(TransArgs p, void* wimg_workspace, hipStream_t s);
+int compute_units();
+
 // Per-device scratch owned by the library (api.cpp): at least `bytes`, grown
 // on demand (growing synchronises the device); calls that use it on one
 // device must be ordered.

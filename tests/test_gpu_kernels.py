@@ -156,7 +156,11 @@ def test_layernorm_linear_pair_tiled_tail(B, transposed, dtype, C):
 
 
 @pytest.mark.parametrize("R,K,F,dtype", [(1000, 128, 512, "bf16"), (333, 64, 256, "bf16"), (65, 256, 96, "bf16"),
-                                         (100, 16, 64, "f32")])
+                                         (100, 16, 64, "f32"),
+                                         # several 256-row passes per workgroup, ragged last pass
+                                         (140001, 128, 512, "bf16"),
+                                         # two hidden chunks; hidden width not a multiple of 64
+                                         (1000, 128, 64, "bf16"), (500, 128, 96, "bf16"), (777, 64, 128, "bf16")])
 def test_swiglu_transition(B, R, K, F, dtype):
     import torch
     x = _n(16, "x", (R, K), 0.5, dtype)
