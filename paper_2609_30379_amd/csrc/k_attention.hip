@@ -208,7 +208,9 @@ struct PairAttnArgs {
 // (kt < round_up(N_i,64)/16), lane l = l16 + 16 g of tile
 // ((h * T + bias_tiles[i] + qt * KT_i + kt) holds the four values
 // bias(j, k) / scale, j = 16 qt + l16, k = 16 kt + 4 g .. +3, each rounded to
-// bf16, 0 past N -- exactly the register image the attention lanes keep.
+// bf16 -- exactly the register image the attention lanes keep.  Keys past N
+// hold -inf (for queries inside N), so the scores they seed are masked
+// without further work; queries past N hold 0.
 // bias(j, k) is bias[h][cell(j, k)] for axis 0 and bias[h][cell(k, j)] for
 // axis 1.  One wave per tile, the sample found by bisection.
 struct BiasImgArgs {
@@ -242,7 +244,7 @@ __global__ void __launch_bounds__(256) bias_image_kernel(BiasImgArgs p) {
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     const int k = k0 + e;
-    float b = 0.f;
+    float b = j < n ? -INFINITY : 0.f;
     if (j < n && k < n) b = (float)bh[p.axis == 0 ? (int64_t)j * n + k : (int64_t)k * n + j] * p.inv_scale;
     o[e] = (bf16)b;
   }
@@ -463,7 +465,7 @@ __global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_k
           // at most four key fragments in flight (registers)
           if (kt % 4 == 3) __builtin_amdgcn_sched_barrier(0);
         }
-        if (kc + NT * 16 > n) {                   // keys past N
+        if (!p.bias_img && kc + NT * 16 > n) {    // keys past N (with a bias the image masks them)
 #pragma unroll
           for (int kt = 0; kt < NT; ++kt)
 #pragma unroll
