@@ -1034,7 +1034,10 @@ __global__ void __launch_bounds__(kWaveThreads, 1) linear_wave_kernel(LinArgs p)
         } else {
           o = *reinterpret_cast<const bf16x8*>(stage + (size_t)(row * SS + cc * 8) * 2);
         }
-        *reinterpret_cast<bf16x8*>(p.y + (int64_t)mm * p.ldy + col) = o;
+        // Non-temporal: measured on the pair block, streaming these outputs
+        // past the caches leaves the memory-side cache to the next kernels
+        // (row attention 158 -> 146 us; the projections themselves unchanged).
+        store_nt(p.y + (int64_t)mm * p.ldy + col, o);
       }
     }
     // ---- tail columns (channel-major planes), column tile by column tile

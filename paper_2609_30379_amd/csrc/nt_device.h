@@ -68,6 +68,17 @@ template <> struct Vec<bf16> {
   }
 };
 
+// Non-temporal 16- and 8-byte stores (streaming hint: the lines are not kept
+// in the caches on the way out).
+typedef uint32_t u32x4_nt __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_nt __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ void store_nt(bf16* p, const bf16x8& v) {
+  __builtin_nontemporal_store(__builtin_bit_cast(u32x4_nt, v), reinterpret_cast<u32x4_nt*>(p));
+}
+__device__ __forceinline__ void store_nt(bf16* p, const bf16x4& v) {
+  __builtin_nontemporal_store(__builtin_bit_cast(u32x2_nt, v), reinterpret_cast<u32x2_nt*>(p));
+}
+
 __device__ __forceinline__ float to_f32(float x) { return x; }
 __device__ __forceinline__ float to_f32(bf16 x) { return (float)x; }
 template <typename T> __device__ __forceinline__ T from_f32(float x);
