@@ -2,7 +2,8 @@
 """Benchmark of the packed pair-state hot path on one MI355X.
 
 One step = one pass of the whole pair block over the batch: single
-projections, pair broadcast, LayerNorm+Linear, row attention with pair bias
+projections, pair broadcast and LayerNorm+Linear (one fused launch: the
+broadcast rows are built as the projection reads them), row attention with pair bias
 (projection, attention, output projection + residual), triangle update
 (projection + contraction), SwiGLU transition, and the column mean back to the
 single track.  Default workload: B=8 near-uniform lengths 208..224, C_s=384,
@@ -84,6 +85,7 @@ def op_costs(w, L):
         "single_proj": (S * (Cs + 2 * C) * e, 2 * S * Cs * 2 * C),
         "pair_broadcast": (R * C * e + 2 * S * C * e, R * C),
         "ln_linear": (R * 2 * C * e, 2 * R * C * C),
+        "bcast_ln_linear": (2 * S * C * e + R * C * e, R * C + 2 * R * C * C),
         "attn_proj": (R * (C + 3 * C + H) * e, 2 * R * C * (3 * C + H)),
         "attention_row": (R * (4 * H * d + H) * e, 4 * H * d * N3),
         "attention_col": (R * (4 * H * d + H) * e, 4 * H * d * N3),

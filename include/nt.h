@@ -206,6 +206,19 @@ typedef struct {
   const nt_layout* layout;     /* optional: rows must equal the layout's row count */
   nt_level level;              /*   at this level                               */
   const nt_layout* residual_layout;  /* optional: must be compatible with layout */
+  /* Broadcast rows (x NULL, bcast_u and bcast_v set): the rows are the pair
+   * broadcast of u and v over `layout` (level NT_LEVEL_PAIRS):
+   *     x[o_i + a N_i + b] = u[eta_i + a] + v[eta_i + b]
+   * summed in fp32 and rounded to bf16 -- exactly what nt_pair_broadcast
+   * stores -- so LN(broadcast) W^T + b is computed without writing or reading
+   * the broadcast pair tensor (Eq. running-block, first two lines, fused).
+   * bf16 only, c_in in {64, 128}, c_out <= 512 (multiple of 8), epilogue
+   * NONE or GELU, no tail, no residual; u, v: [sum N, c_in] with row strides
+   * ld_bcast_u, ld_bcast_v (multiples of 8; may alias).                    */
+  const void* bcast_u;
+  int64_t ld_bcast_u;
+  const void* bcast_v;
+  int64_t ld_bcast_v;
 } nt_linear_args;
 
 /* Workspace: two kinds of bf16 call use a per-device workspace owned by the

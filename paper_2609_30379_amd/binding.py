@@ -47,7 +47,8 @@ class LinearArgs(C.Structure):
                 ("residual", C.c_void_p), ("ld_residual", C.c_int64),
                 ("y", C.c_void_p), ("ldy", C.c_int64),
                 ("n_tail", C.c_int32), ("y_tail", C.c_void_p), ("ld_tail", C.c_int64), ("tail_layout", C.c_int),
-                ("layout", C.c_void_p), ("level", C.c_int), ("residual_layout", C.c_void_p)]
+                ("layout", C.c_void_p), ("level", C.c_int), ("residual_layout", C.c_void_p),
+                ("bcast_u", C.c_void_p), ("ld_bcast_u", C.c_int64), ("bcast_v", C.c_void_p), ("ld_bcast_v", C.c_int64)]
 
 
 _lib = None
@@ -170,12 +171,24 @@ def nt_pair_broadcast(layout: NestedLayout, u, v, z, accumulate: bool = False):
 def nt_layernorm_linear(x, w, bias, y, ln=None, eps: float = 1e-5, epilogue: str = "none", w2=None, bias2=None,
                         hidden: int = 0, residual=None, n_tail: int = 0, y_tail=None,
                         tail_layout: str = "channel_major", layout: NestedLayout | None = None,
-                        level: str = "pairs", residual_layout: NestedLayout | None = None, c_out: int | None = None):
+                        level: str = "pairs", residual_layout: NestedLayout | None = None, c_out: int | None = None,
+                        bcast=None):
+    """bcast=(u, v) with x=None: the rows are the pair broadcast u[eta_i+a] + v[eta_i+b] over `layout`."""
     a = LinearArgs()
-    px, ldx = _mat(x, "x")
-    a.rows, a.c_in = int(x.size(0)), int(x.size(1))
+    if bcast is not None:
+        if x is not None or layout is None:
+            raise ValueError("broadcast rows need x=None and a layout")
+        u, v = bcast
+        a.bcast_u, a.ld_bcast_u = _mat(u, "u")
+        a.bcast_v, a.ld_bcast_v = _mat(v, "v")
+        a.rows, a.c_in = int(layout.sum_n2), int(u.size(1))
+        a.x, a.ldx, a.x_dtype = None, 0, _dtype(u)
+    else:
+        px, ldx = _mat(x, "x")
+        a.rows, a.c_in = int(x.size(0)), int(x.size(1))
+        a.x, a.ldx, a.x_dtype = px, ldx, _dtype(x)
     a.c_out = int(c_out if c_out is not None else (w2.size(0) if epilogue == "swiglu_residual" else w.size(0)))
-    a.dtype, a.x, a.ldx, a.x_dtype = _dtype(w), px, ldx, _dtype(x)
+    a.dtype = _dtype(w)
     if ln is not None:
         a.ln_gamma, a.ln_beta = _ptr(ln[0]), _ptr(ln[1])
     a.ln_eps = eps

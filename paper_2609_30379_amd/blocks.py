@@ -103,12 +103,33 @@ class PairWorkspace:
         self.cur = 0
 
 
+fuse_broadcast = True             # the pair block fuses broadcast -> LayerNorm+Linear when it can
+
+
+def fuse_bcast(ws: PairWorkspace, C: int) -> bool:
+    return fuse_broadcast and ws.td == torch.bfloat16 and C in (64, 128)
+
+
 def pair_block(layout: B.NestedLayout, s, W: dict, dims: dict, order, ws: PairWorkspace, z=None):
     """Runs one pair block.  s ([sum N, C_s]) is updated in place by the
     "single" step; returns the pair state tensor (a workspace buffer, or z)."""
     C, H, d = dims["c_z"], dims["heads"], dims["head_dim"]
-    for step in order:
-        if step == "bcast":
+    order = list(order)
+    k = 0
+    while k < len(order):
+        step = order[k]
+        k += 1
+        if step == "bcast" and z is None and k < len(order) and order[k] == "lin" and fuse_bcast(ws, C):
+            # broadcast feeding the LayerNorm+Linear directly: the broadcast
+            # pair tensor is never written (its rows are built as they are read)
+            with _op("single_proj"):
+                B.nt_layernorm_linear(s, W["uv.w"], W["uv.b"], ws.uv, layout=layout, level="singles")
+            z = ws.z[ws.cur]
+            with _op("bcast_ln_linear"):
+                B.nt_layernorm_linear(None, W["lin.w"], W["lin.b"], z, ln=(W["lin.ln_g"], W["lin.ln_b"]),
+                                      layout=layout, level="pairs", bcast=(ws.uv[:, :C], ws.uv[:, C:]))
+            k += 1
+        elif step == "bcast":
             with _op("single_proj"):
                 B.nt_layernorm_linear(s, W["uv.w"], W["uv.b"], ws.uv, layout=layout, level="singles")
             acc = z is not None

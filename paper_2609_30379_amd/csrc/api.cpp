@@ -44,6 +44,7 @@ nt_status upload(nt_layout* L, hipStream_t s) {
       {&L->blk_prow, &L->d_blk_prow},
       {&L->pattn_work, &L->d_pattn_work}, {&L->bias_tiles, &L->d_bias_tiles},
       {&L->sattn_work, &L->d_sattn_work}, {&L->pattn16_work, &L->d_pattn16_work},
+      {&L->bc_tiles, &L->d_bc_tiles},
   };
   size_t total = 0;
   for (auto& p : parts) total += (p.v->size() * sizeof(int32_t) + 255) / 256 * 256;
@@ -255,7 +256,22 @@ nt_status nt_layernorm_linear(const nt_linear_args* a, void* stream) {
   if (a->ln_gamma && !(a->ln_eps >= 0.f)) return nt::fail(NT_ERR_INVALID_ARG, "ln_eps must be >= 0");
   const bool swiglu = a->epilogue == NT_EPI_SWIGLU_RESIDUAL;
   const int vx = vec_elems(a->x_dtype), vy = vec_elems(a->dtype);
-  if (a->ldx < a->c_in || a->ldx % vx) return nt::fail(NT_ERR_INVALID_ARG, "ldx must be >= c_in and a multiple of the vector width");
+  const bool bcast = a->bcast_u || a->bcast_v;
+  if (bcast) {
+    if (!a->bcast_u || !a->bcast_v) return nt::fail(NT_ERR_INVALID_ARG, "broadcast rows need both bcast_u and bcast_v");
+    if (a->x) return nt::fail(NT_ERR_INVALID_ARG, "x must be NULL with broadcast rows");
+    if (!a->layout || a->level != NT_LEVEL_PAIRS) return nt::fail(NT_ERR_INVALID_ARG, "broadcast rows need a pair-level layout");
+    if (!a->layout->has_device) return nt::fail(NT_ERR_INVALID_ARG, "broadcast rows need a layout with device mirrors");
+    if (a->dtype != NT_BF16 || a->x_dtype != NT_BF16 || (a->c_in != 64 && a->c_in != 128) || a->c_out > 512 ||
+        a->c_out % 8 || (a->epilogue != NT_EPI_NONE && a->epilogue != NT_EPI_GELU) || a->n_tail || a->residual)
+      return nt::fail(NT_ERR_UNSUPPORTED, "broadcast rows: bf16, c_in in {64, 128}, c_out <= 512 (multiple of 8), "
+                                          "epilogue none or gelu, no tail, no residual");
+    if (a->ld_bcast_u < a->c_in || a->ld_bcast_u % 8 || a->ld_bcast_v < a->c_in || a->ld_bcast_v % 8)
+      return nt::fail(NT_ERR_INVALID_ARG, "ld_bcast_u/v must be >= c_in and multiples of 8");
+    if (!aligned16(a->bcast_u) || !aligned16(a->bcast_v)) return nt::fail(NT_ERR_INVALID_ARG, "pointers must be 16-byte aligned");
+  } else if (a->ldx < a->c_in || a->ldx % vx) {
+    return nt::fail(NT_ERR_INVALID_ARG, "ldx must be >= c_in and a multiple of the vector width");
+  }
   if (a->n_tail < 0 || a->n_tail > a->c_out) return nt::fail(NT_ERR_INVALID_ARG, "n_tail out of range");
   if (a->tail_layout < NT_TAIL_CHANNEL_MAJOR || a->tail_layout > NT_TAIL_PAIR_TILED_T)
     return nt::fail(NT_ERR_INVALID_ARG, "bad tail_layout");
@@ -286,12 +302,12 @@ nt_status nt_layernorm_linear(const nt_linear_args* a, void* stream) {
   if (a->dtype == NT_F32 && !swiglu && a->c_in > 4096) return nt::fail(NT_ERR_UNSUPPORTED, "f32 path needs c_in <= 4096");
   if (a->epilogue == NT_EPI_RESIDUAL && !a->residual) return nt::fail(NT_ERR_INVALID_ARG, "residual epilogue needs residual");
   if (a->rows == 0) return NT_OK;
-  if (!a->x || !a->w) return nt::fail(NT_ERR_INVALID_ARG, "x and w must be non-NULL");
+  if ((!a->x && !bcast) || !a->w) return nt::fail(NT_ERR_INVALID_ARG, "x and w must be non-NULL");
   if (n_main > 0 && !a->y) return nt::fail(NT_ERR_INVALID_ARG, "y is NULL");
   if (a->n_tail > 0 && !a->y_tail) return nt::fail(NT_ERR_INVALID_ARG, "y_tail is NULL");
   if ((a->ln_gamma && !aligned16(a->ln_gamma)) || (a->ln_beta && !aligned16(a->ln_beta)))
     return nt::fail(NT_ERR_INVALID_ARG, "ln_gamma and ln_beta must be 16-byte aligned");
-  if (!aligned16(a->x) || !aligned16(a->w) || (a->y && !aligned16(a->y)) || (a->residual && !aligned16(a->residual)) ||
+  if ((a->x && !aligned16(a->x)) || !aligned16(a->w) || (a->y && !aligned16(a->y)) || (a->residual && !aligned16(a->residual)) ||
       (a->w2 && !aligned16(a->w2)) || (a->y_tail && !aligned16(a->y_tail)))
     return nt::fail(NT_ERR_INVALID_ARG, "pointers must be 16-byte aligned");
   if (n_main > 0 && (a->ldy < n_main || a->ldy % vy)) return nt::fail(NT_ERR_INVALID_ARG, "ldy must be >= the main width and a multiple of the vector width");

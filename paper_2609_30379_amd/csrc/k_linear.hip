@@ -45,6 +45,11 @@ struct LinArgs {
   int batch;
   int wc, ntiles;             // streaming kernel: waves along the columns, 64-row tiles
   int stage_out;              // streaming kernel: write the output tile back through LDS
+  // pair-broadcast rows (wave kernel): row cell(i, a, b) is u[eta_i + a] + v[eta_i + b]
+  const bf16* bc_u;
+  const bf16* bc_v;
+  int64_t ld_bc_u, ld_bc_v;
+  const int4* bc_tiles;       // per 16-cell tile: pair row, column, N_i, eta_i of its first cell
 };
 
 // Position of the pair cell (a, b) of sample i in its pair-tiled operand plane:
@@ -884,8 +889,14 @@ template <int K, int EPI> size_t wave_smem_bytes(int nt16) {
          (size_t)(kWaveThreads / 64) * wave_stage_bytes<EPI>();
 }
 
-template <int EPI, int K>
+// With BC the rows are not read from x: row m = cell(i, a, b) of a pair layout
+// is the pair broadcast u[eta_i + a] + v[eta_i + b] (fp32 sum rounded to bf16,
+// exactly what the broadcast op stores), built as the tile is loaded.  Each
+// wave then takes a contiguous range of tiles and walks its lanes' cells
+// forward from the layout's per-tile table (no search per tile).
+template <int EPI, int K, bool BC>
 __global__ void __launch_bounds__(kWaveThreads, 1) linear_wave_kernel(LinArgs p) {
+  static_assert(!BC || EPI != NT_EPI_RESIDUAL, "the broadcast rows use the residual buffers");
   constexpr int KT = K / 32;
   constexpr bool RES = EPI == NT_EPI_RESIDUAL;
   constexpr int SS = wave_stage_stride<EPI>();
@@ -922,9 +933,50 @@ __global__ void __launch_bounds__(kWaveThreads, 1) linear_wave_kernel(LinArgs p)
   unsigned char* stage = stage_base + (size_t)wave * wave_stage_bytes<EPI>();
   const int c8n = p.n_main / 8;                   // 16-byte chunks per output row
 
+  // broadcast cursor of this lane: cell (pair row c_pr = eta_i + a, column
+  // c_b) of sample i with N_i = c_n and eta_i = c_vb; it only moves forward
+  int c_pr = 0, c_b = 0, c_n = 1, c_vb = 0, c_m = 0;
+  auto bc_wrap = [&]() {
+    while (c_b >= c_n) {
+      c_b -= c_n;
+      ++c_pr;
+      if (c_pr == c_vb + c_n) {                 // first pair row of the next sample
+        const int i = p.row_sample[c_pr];
+        c_vb = p.cu_seqlens[i];
+        c_n = p.cu_seqlens[i + 1] - c_vb;
+      }
+    }
+  };
+  auto bc_start = [&](int t) {
+    const int4 rec = p.bc_tiles[t];
+    c_m = min(t * 16 + l16, p.rows - 1);
+    c_pr = rec.x; c_b = rec.y + (c_m - t * 16); c_n = rec.z; c_vb = rec.w;
+    bc_wrap();
+  };
+  auto bc_next = [&]() {                        // to the same lane's cell 16 rows on
+    if (c_m + 16 < p.rows) {
+      c_m += 16;
+      c_b += 16;
+      bc_wrap();
+    }
+  };
+
   // rows of tile t in B-fragment order: lane (l16, g) holds row 16t + l16,
-  // k = 32 kk + 8 g .. +7; residual rows in write-back order (4 chunks a lane)
+  // k = 32 kk + 8 g .. +7; residual rows in write-back order (4 chunks a lane);
+  // broadcast sources: u in xr, v in rr (the cursor is at tile t)
   auto load_tile = [&](int t, uint4 (&xr)[KT], uint4 (&rr)[4]) {
+    if constexpr (BC) {
+      static_assert(KT <= 4, "v rows fit the residual buffers");
+      const bf16* su = p.bc_u + (int64_t)c_pr * p.ld_bc_u + g * 8;
+      const bf16* sv = p.bc_v + (int64_t)(c_vb + c_b) * p.ld_bc_v + g * 8;
+#pragma unroll
+      for (int kk = 0; kk < KT; ++kk) {
+        xr[kk] = *reinterpret_cast<const uint4*>(su + kk * 32);
+        rr[kk] = *reinterpret_cast<const uint4*>(sv + kk * 32);
+      }
+      bc_next();
+      return;
+    }
     const int m = t * 16 + l16;
     const bool ok = t < ntile && m < p.rows;
 #pragma unroll
@@ -940,8 +992,24 @@ __global__ void __launch_bounds__(kWaveThreads, 1) linear_wave_kernel(LinArgs p)
     }
   };
 
-  auto process = [&](int t, const uint4 (&xr)[KT], const uint4 (&rr)[4]) {
+  auto process = [&](int t, const uint4 (&xr_in)[KT], const uint4 (&rr)[4]) {
     const int m = t * 16 + l16;
+    uint4 xr[KT];
+#pragma unroll
+    for (int kk = 0; kk < KT; ++kk) xr[kk] = xr_in[kk];
+    if constexpr (BC) {
+      // the broadcast cell, rounded to bf16 as the broadcast op stores it
+#pragma unroll
+      for (int kk = 0; kk < KT; ++kk) {
+        float a[8], b[8];
+        XStage<bf16>::unpack(xr_in[kk], a);
+        XStage<bf16>::unpack(rr[kk], b);
+        bf16x8 o;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] = (bf16)(a[e] + b[e]);
+        xr[kk] = __builtin_bit_cast(uint4, o);
+      }
+    }
     // ---- LayerNorm (or plain conversion) into B fragments
     bf16x8 xb[KT];
     if (p.gamma) {
@@ -1059,16 +1127,22 @@ __global__ void __launch_bounds__(kWaveThreads, 1) linear_wave_kernel(LinArgs p)
     }
   };
 
+  // tiles: strided over the waves, or with BC a contiguous range per wave
+  const int t0 = BC ? (int)((int64_t)ntile * wid / nw) : wid;
+  const int t1 = BC ? (int)((int64_t)ntile * (wid + 1) / nw) : ntile;
+  const int ts = BC ? 1 : nw;
+  if (BC && t0 >= t1) return;
+  if constexpr (BC) bc_start(t0);
   uint4 xr[kWavePF][KT], rr[kWavePF][4];
 #pragma unroll
-  for (int d = 0; d < kWavePF; ++d) load_tile(wid + d * nw, xr[d], rr[d]);
-  for (int i = 0; wid + i * nw < ntile;) {
+  for (int d = 0; d < kWavePF; ++d) load_tile(t0 + d * ts, xr[d], rr[d]);
+  for (int i = 0; t0 + i * ts < t1;) {
 #pragma unroll
     for (int d = 0; d < kWavePF; ++d) {
-      const int t = wid + i * nw;
-      if (t >= ntile) break;
+      const int t = t0 + i * ts;
+      if (t >= t1) break;
       process(t, xr[d], rr[d]);
-      load_tile(wid + (i + kWavePF) * nw, xr[d], rr[d]);
+      load_tile(t0 + (i + kWavePF) * ts, xr[d], rr[d]);
       ++i;
     }
   }
@@ -1533,11 +1607,11 @@ void launch_stream(const LinArgs& p, hipStream_t s) {
   kern<<<dim3((unsigned)grid), dim3(kStreamThreads), smem, s>>>(p);
 }
 
-template <int EPI, int K>
+template <int EPI, int K, bool BC = false>
 void launch_wave(const LinArgs& p, hipStream_t s) {
   const int nt16 = (p.N + 15) / 16;
   const size_t smem = wave_smem_bytes<K, EPI>(nt16);
-  auto kern = linear_wave_kernel<EPI, K>;
+  auto kern = linear_wave_kernel<EPI, K, BC>;
   (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
   const int ntile = (p.rows + 15) / 16;
   const int grid = std::min((ntile + kWaveThreads / 64 - 1) / (kWaveThreads / 64), compute_units());
@@ -1591,6 +1665,22 @@ hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
     p.blk_prow = plan.layout->d_blk_prow;
   }
   if (a.n_tail == 0) p.y_tail = nullptr;
+
+  if (a.bcast_u) {
+    // pair-broadcast rows: the wave-streamed kernel builds them from u and v
+    const int nt16 = (a.c_out + 15) / 16;
+    const size_t smem = a.c_in == 64 ? wave_smem_bytes<64, NT_EPI_NONE>(nt16) : wave_smem_bytes<128, NT_EPI_NONE>(nt16);
+    if (smem > 150 * 1024) return hipErrorInvalidValue;
+    p.bc_u = (const bf16*)a.bcast_u; p.bc_v = (const bf16*)a.bcast_v;
+    p.ld_bc_u = a.ld_bcast_u; p.ld_bc_v = a.ld_bcast_v;
+    p.bc_tiles = reinterpret_cast<const int4*>(plan.layout->d_bc_tiles);
+    p.ldx = a.c_in;
+#define NT_WB(EPI) do { if (a.c_in == 64) launch_wave<EPI, 64, true>(p, s); else launch_wave<EPI, 128, true>(p, s); } while (0)
+    if (a.epilogue == NT_EPI_GELU) NT_WB(NT_EPI_GELU);
+    else NT_WB(NT_EPI_NONE);
+#undef NT_WB
+    return hipGetLastError();
+  }
 
   if (a.dtype == NT_F32) {
     F32Args f{};

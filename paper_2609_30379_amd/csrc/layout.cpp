@@ -116,6 +116,23 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L) {
     L->blk_prow[b] = (int32_t)eta;
   }
 
+  // broadcast sources of the projections: for every 16-cell tile, the pair
+  // row and column of its first cell and that sample's N_i and first single
+  // row (a lane finds its own cell from there, see linear_wave_kernel)
+  {
+    const int64_t nt16 = (sn2 + 15) / 16;
+    L->bc_tiles.assign(nt16 * 4, 0);
+    for (int64_t t = 0, eta = 0; t < nt16; ++t) {
+      const int64_t m = t * 16;
+      while (eta + 1 < sn && L->row_splits2[eta + 1] <= m) ++eta;
+      const int32_t i = L->row_sample[eta];
+      L->bc_tiles[4 * t] = (int32_t)eta;
+      L->bc_tiles[4 * t + 1] = (int32_t)(m - L->row_splits2[eta]);
+      L->bc_tiles[4 * t + 2] = lengths[i];
+      L->bc_tiles[4 * t + 3] = L->cu_seqlens[i];
+    }
+  }
+
   // pair-row attention: one item per (sample, pair row), cost N_i^2
   {
     std::vector<std::array<int32_t, 2>> items;

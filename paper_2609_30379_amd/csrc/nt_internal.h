@@ -49,6 +49,8 @@ struct nt_layout {
   std::vector<int32_t> pattn16_work;  // the same with blocks of up to 256 queries (16 waves)
   std::vector<int32_t> sattn_work;   // 1-D attention: quads (sample, first 16-query tile, 0, tile count)
   std::vector<int32_t> blk_prow;     // [ceil(sum N^2 / kLinRows)] pair row holding cell kLinRows*b
+  std::vector<int32_t> bc_tiles;     // quads per 16-cell tile t: pair row eta of cell 16t, its column
+                                     // b = 16t - row_splits2[eta], N_i and cu_seqlens[i] of its sample
 
   bool has_device = false;
   int device = -1;
@@ -67,6 +69,7 @@ struct nt_layout {
   const int32_t* d_bias_tiles = nullptr;
   const int32_t* d_sattn_work = nullptr;
   const int32_t* d_pattn16_work = nullptr;
+  const int32_t* d_bc_tiles = nullptr;
   // pair attention workspace (the bias image), allocated by the first call
   // that needs it and grown on demand; freed with the layout
   mutable void* d_attn_ws = nullptr;

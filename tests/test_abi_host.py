@@ -146,6 +146,12 @@ def test_op_argument_errors_need_no_device(lib):
         (dict(rows=24, layout=host.handle, level=1), B.NT_ERR_LAYOUT_MISMATCH),
         (dict(dtype=B.NT_F32, x_dtype=B.NT_BF16), B.NT_ERR_INVALID_ARG),
         (dict(ldy=4), B.NT_ERR_INVALID_ARG),
+        # broadcast rows: both sources, x NULL, a pair layout with device mirrors
+        (dict(bcast_u=C.c_void_p(0x7000), ld_bcast_u=16), B.NT_ERR_INVALID_ARG),
+        (dict(bcast_u=C.c_void_p(0x7000), bcast_v=C.c_void_p(0x8000), ld_bcast_u=16, ld_bcast_v=16),
+         B.NT_ERR_INVALID_ARG),                                          # x set
+        (dict(x=None, bcast_u=C.c_void_p(0x7000), bcast_v=C.c_void_p(0x8000), ld_bcast_u=16, ld_bcast_v=16,
+              rows=25, layout=host.handle, level=1), B.NT_ERR_INVALID_ARG),   # host-only layout
     ]
     for kw, want in cases:
         a = _linear_args(**kw)

@@ -85,3 +85,20 @@ def test_token_workload():
                                       round_last=False)
         check(xg[eta[i]:eta[i + 1]], xr, "bf16", f"token layer x sample {i}")
         check(pg[i:i + 1], pr, "bf16", f"token pooled sample {i}")
+
+
+def test_pair_block_fused_broadcast_matches_two_calls():
+    """The block's broadcast -> LayerNorm+Linear runs fused (broadcast rows built
+    as they are read); the two-call path must give the same bits."""
+    from paper_2609_30379_amd import blocks
+    from paper_2609_30379_amd.blocks import PairRun
+    base = synth.WORKLOADS["pair_b8_n208_224_bf16"]
+    L = [120, 90, 33, 1, 0, 7, 17, 16]
+    run = PairRun(base, lengths=L)
+    s1, z1 = (host(t) for t in run.step())
+    blocks.fuse_broadcast = False
+    try:
+        s2, z2 = (host(t) for t in run.step())
+    finally:
+        blocks.fuse_broadcast = True
+    assert np.array_equal(z1, z2) and np.array_equal(s1, s2)

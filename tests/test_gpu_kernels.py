@@ -134,6 +134,38 @@ def test_layernorm_linear(B, R, K, N, ln, epi, xdt, dtype, n_tail):
         check(host(yt)[:, :R].T, ref[:, N - n_tail:], dtype, "linear tail")
 
 
+@pytest.mark.parametrize("lname,C,N,epi", [("ragged", 128, 128, "none"), ("tiny", 64, 64, "none"),
+                                           ("ragged", 64, 96, "gelu"), ("one", 128, 128, "none"),
+                                           ("small_mix", 128, 256, "none"), ("wide", 128, 128, "none")])
+def test_layernorm_linear_broadcast_rows(B, lname, C, N, epi):
+    """LN+Linear over the pair broadcast of u and v, built as the rows are read:
+    equals the broadcast (stored in bf16) followed by LN+Linear, and the
+    plain two-call path bit for bit."""
+    import torch
+    L = {"small_mix": [1, 2, 3, 17, 0, 5, 16, 15, 33], "wide": [230, 7, 300, 1, 64]}.get(lname) or LENGTHS[lname]
+    lay = _layout(B, L)
+    S, R = sum(L), sum(n * n for n in L)
+    uv = _n(31, "uv", (S, 2 * C), 0.6, "bf16")
+    w = _n(32, "w", (N, C), 0.5 / np.sqrt(C), "bf16")
+    b = _n(33, "b", (N,), 0.1, "f32")
+    g, be = _n(34, "g", (C,), 0.1, "f32") + 1, _n(35, "be", (C,), 0.1, "f32")
+    uvd = dev(uv, "bf16")
+    wd, bd, lnd = dev(w, "bf16"), dev(b, "f32"), (dev(g, "f32"), dev(be, "f32"))
+    y = torch.full((R, N), float("nan"), dtype=torch.bfloat16, device="cuda")
+    B.nt_layernorm_linear(None, wd, bd, y, ln=lnd, epilogue=epi, layout=lay, level="pairs",
+                          bcast=(uvd[:, :C], uvd[:, C:]))
+    from oracle.numerics import round_bf16
+    zb = round_bf16(O.pair_broadcast(uv[:, :C], uv[:, C:], L))
+    ref = O.layernorm_linear(zb, w, b, ln=(g, be), epilogue=epi)
+    check(host(y), ref, "bf16", f"broadcast rows {lname} C={C} N={N} {epi}")
+    z = torch.empty((R, C), dtype=torch.bfloat16, device="cuda")
+    B.nt_pair_broadcast(lay, uvd[:, :C], uvd[:, C:], z)
+    y2 = torch.full((R, N), float("nan"), dtype=torch.bfloat16, device="cuda")
+    B.nt_layernorm_linear(z, wd, bd, y2, ln=lnd, epilogue=epi, layout=lay, level="pairs")
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2), "broadcast rows differ from broadcast + LN+Linear"
+
+
 @pytest.mark.parametrize("transposed", [False, True])
 @pytest.mark.parametrize("dtype,C", [("bf16", 64), ("f32", 16)])
 def test_layernorm_linear_pair_tiled_tail(B, transposed, dtype, C):
