@@ -505,17 +505,25 @@ __global__ void __launch_bounds__(256) linear_res_kernel(LinArgs p) {
 // ---------------------------------------------------------------- small row counts
 // Projections over few rows (the single track: one row per token) are pure
 // latency: a handful of large tiles would each walk the whole K loop alone.
-// Here one wave owns a 16-row x 64-column output block, so hundreds of waves
-// run at once, and the next k-step's fragments load while the current step is
-// on the matrix cores.  No LayerNorm and no tail columns (those take the
-// other paths).
+// Here a workgroup of four waves owns a 16-row x 64-column output block and
+// splits K between its waves (wave w takes k-steps w, w + 4, ...): each wave
+// issues the loads of all its k-steps at once, so the block costs about one
+// memory round trip instead of one per k-step; the partial products meet in
+// LDS and wave w finishes column tile w.  No LayerNorm and no tail columns
+// (those take the other paths).
+constexpr int kSmallWaves = 4;
+constexpr int kSmallSteps = 4;       // k-steps per wave loaded at once (K <= 512 in one round)
+
 template <typename XT, int EPI>
-__global__ void __launch_bounds__(64) linear_small_kernel(LinArgs p) {
-  const int lane = threadIdx.x, l16 = lane & 15, g = lane >> 4;
+__global__ void __launch_bounds__(64 * kSmallWaves) linear_small_kernel(LinArgs p) {
+  __shared__ f32x4 part[kSmallWaves][4][64];
+  const int lane = threadIdx.x & 63, l16 = lane & 15, g = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
   const int m0 = blockIdx.x * 16, n0 = blockIdx.y * 64;
   const XT* x = static_cast<const XT*>(p.x);
   const int m = m0 + l16;
   const bool mrow = m < p.rows;
+  const int nks = p.K / 32;
   auto load_step = [&](int k0, bf16x8 (&wa)[4], bf16x8& xb) {
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
@@ -536,45 +544,51 @@ __global__ void __launch_bounds__(64) linear_small_kernel(LinArgs p) {
   f32x4 acc[4];
 #pragma unroll
   for (int t = 0; t < 4; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-  bf16x8 wa[4], xb, wn[4], xn;
-  load_step(0, wa, xb);
-  for (int k0 = 0; k0 < p.K; k0 += 32) {
-    if (k0 + 32 < p.K) load_step(k0 + 32, wn, xn);
+  for (int s0 = wave; s0 < nks; s0 += kSmallWaves * kSmallSteps) {
+    bf16x8 wa[kSmallSteps][4], xb[kSmallSteps];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) acc[t] = mfma16(wa[t], xb, acc[t]);
+    for (int j = 0; j < kSmallSteps; ++j)
+      if (s0 + kSmallWaves * j < nks) load_step((s0 + kSmallWaves * j) * 32, wa[j], xb[j]);
 #pragma unroll
-    for (int t = 0; t < 4; ++t) wa[t] = wn[t];
-    xb = xn;
+    for (int j = 0; j < kSmallSteps; ++j)
+      if (s0 + kSmallWaves * j < nks) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t) acc[t] = mfma16(wa[j][t], xb[j], acc[t]);
+      }
   }
-  if (!mrow) return;
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    const int n = n0 + t * 16 + 4 * g;            // lane owns channels n..n+3 of row m
-    if (n >= p.N) continue;
-    float r[4];
+  for (int t = 0; t < 4; ++t) part[wave][t][lane] = acc[t];
+  __syncthreads();
+  // column tile t = wave: the four partial products in wave order
+  f32x4 r4 = part[0][wave][lane];
+#pragma unroll
+  for (int w = 1; w < kSmallWaves; ++w) r4 += part[w][wave][lane];
+  if (!mrow) return;
+  const int n = n0 + wave * 16 + 4 * g;            // lane owns channels n..n+3 of row m
+  if (n >= p.N) return;
+  float r[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    r[i] = r4[i] + ((p.bias && n + i < p.N) ? p.bias[n + i] : 0.f);
+    if constexpr (EPI == NT_EPI_GELU) r[i] = gelu_erf(r[i]);
+  }
+  if (n + 4 <= p.N) {
+    if constexpr (EPI == NT_EPI_RESIDUAL) {
+      const uint2 q2 = *reinterpret_cast<const uint2*>(p.res + (int64_t)m * p.ld_res + n);
+      r[0] += __uint_as_float(q2.x << 16); r[1] += __uint_as_float(q2.x & 0xffff0000u);
+      r[2] += __uint_as_float(q2.y << 16); r[3] += __uint_as_float(q2.y & 0xffff0000u);
+    }
+    bf16x4 o;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) o[i] = (bf16)r[i];
+    *reinterpret_cast<bf16x4*>(p.y + (int64_t)m * p.ldy + n) = o;
+  } else {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      r[i] = acc[t][i] + ((p.bias && n + i < p.N) ? p.bias[n + i] : 0.f);
-      if constexpr (EPI == NT_EPI_GELU) r[i] = gelu_erf(r[i]);
-    }
-    if (n + 4 <= p.N) {
-      if constexpr (EPI == NT_EPI_RESIDUAL) {
-        const uint2 q2 = *reinterpret_cast<const uint2*>(p.res + (int64_t)m * p.ld_res + n);
-        r[0] += __uint_as_float(q2.x << 16); r[1] += __uint_as_float(q2.x & 0xffff0000u);
-        r[2] += __uint_as_float(q2.y << 16); r[3] += __uint_as_float(q2.y & 0xffff0000u);
-      }
-      bf16x4 o;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) o[i] = (bf16)r[i];
-      *reinterpret_cast<bf16x4*>(p.y + (int64_t)m * p.ldy + n) = o;
-    } else {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        if (n + i >= p.N) break;
-        float v = r[i];
-        if constexpr (EPI == NT_EPI_RESIDUAL) v += (float)p.res[(int64_t)m * p.ld_res + n + i];
-        p.y[(int64_t)m * p.ldy + n + i] = (bf16)v;
-      }
+      if (n + i >= p.N) break;
+      float v = r[i];
+      if constexpr (EPI == NT_EPI_RESIDUAL) v += (float)p.res[(int64_t)m * p.ld_res + n + i];
+      p.y[(int64_t)m * p.ldy + n + i] = (bf16)v;
     }
   }
 }
@@ -1734,7 +1748,7 @@ hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
 
   const bool tiled = p.y_tail && p.tail_mode != kTailChannelMajor;
   if (!a.ln_gamma && a.n_tail == 0 && a.c_in % 32 == 0 && rows <= kSmallRows) {
-    const dim3 g1((unsigned)((rows + 15) / 16), (unsigned)((a.c_out + 63) / 64)), b1(64);
+    const dim3 g1((unsigned)((rows + 15) / 16), (unsigned)((a.c_out + 63) / 64)), b1(64 * kSmallWaves);
 #define NT_SM(XT, EPI) linear_small_kernel<XT, EPI><<<g1, b1, 0, s>>>(p)
 #define NT_SM_X(EPI) do { if (xf) NT_SM(float, EPI); else NT_SM(bf16, EPI); } while (0)
     switch (a.epilogue) {
