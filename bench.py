@@ -39,17 +39,16 @@ F32_PEAK_TFLOPS = 157.3        # fp32 vector
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 COUNTER_WORKLOAD = "pair_b8_n208_224_bf16"
 COUNTERS = {  # op: (kernel source, source hash, FETCH_SIZE KiB, WRITE_SIZE KiB)
-    "attention_row": ("k_attention.hip", "7de75a2977e897f8", 142570, 90997),
-    "transition": ("k_transition.hip", "unmeasured", 0, 0),
-    "triangle_out": ("k_triangle.hip", "3a2d7b8ae374561a", 301099, 92083),
-    "attn_proj": ("k_linear.hip", "5da75a59fb862322", 46041, 276220),
-    "tri_proj": ("k_linear.hip", "5da75a59fb862322", 45829, 197120),
-    "ln_linear": ("k_linear.hip", "5da75a59fb862322", 45777, 90996),
-    "attn_out_residual": ("k_linear.hip", "5da75a59fb862322", 91273, 90996),
-    "single_proj": ("k_linear.hip", "5da75a59fb862322", 3368, 853),
-    "pair_broadcast": ("k_segment.hip", "a2aacf3085c626e1", 1998, 90996),
-    "segment_mean": ("k_segment.hip", "a2aacf3085c626e1", 45570, 853),
-    "single_update": ("k_linear.hip", "5da75a59fb862322", 3632, 1280),
+    "attention_row": ("k_attention.hip", "f426dccbd46dbcc7", 142573, 90997),
+    "transition": ("k_transition.hip", "e2f701d5925d7f6e", 53103, 90996),
+    "triangle_out": ("k_triangle.hip", "199724cf5276c94e", 304096, 91523),
+    "attn_proj": ("k_linear.hip", "33ddea92dec844b9", 46035, 276012),
+    "tri_proj": ("k_linear.hip", "33ddea92dec844b9", 45826, 197120),
+    "bcast_ln_linear": ("k_linear.hip", "33ddea92dec844b9", 2401, 90997),
+    "attn_out_residual": ("k_linear.hip", "33ddea92dec844b9", 91287, 90997),
+    "single_proj": ("k_linear.hip", "33ddea92dec844b9", 3366, 853),
+    "segment_mean": ("k_segment.hip", "c95eabc6d4c62896", 45570, 853),
+    "single_update": ("k_linear.hip", "33ddea92dec844b9", 3628, 1280),
 }
 
 
