@@ -97,7 +97,7 @@ typedef enum {
   NT_ARR_ROW_SPLITS2 = 3,      /* level-2 pair row splits, [1 + sum N_i]        */
   NT_ARR_ROW_SAMPLE = 4,       /* sample id of every single row, [sum N_i]      */
   NT_ARR_ATTN_WORK = 5,        /* pair-row work map (sample, row) pairs, XCD-ordered */
-  NT_ARR_TRI_WORK = 6,         /* triangle tile map (sample, x-tile, y-tile, 0) quads */
+  NT_ARR_TRI_WORK = 6,         /* triangle tile map (sample, x-tile, y-tile, first tile of the sample) quads */
   NT_ARR_SEQ_WORK = 7,         /* 1-D attention map (sample, query block) pairs */
   NT_ARR_CU_PAD = 8            /* P_i offsets of pair-tiled operands, [B+1]     */
 } nt_array;

@@ -43,7 +43,7 @@ nt_status upload(nt_layout* L, hipStream_t s) {
       {&L->seq_work, &L->d_seq_work},
       {&L->blk_prow, &L->d_blk_prow},
       {&L->pattn_work, &L->d_pattn_work}, {&L->bias_tiles, &L->d_bias_tiles},
-      {&L->sattn_work, &L->d_sattn_work}, {&L->pattn16_work, &L->d_pattn16_work},
+      {&L->sattn_work, &L->d_sattn_work},
       {&L->bc_tiles, &L->d_bc_tiles},
   };
   size_t total = 0;

@@ -202,6 +202,8 @@ struct PairAttnArgs {
   const uint2* bias_img; // bias image (see bias_image_kernel) or NULL for no bias
   int64_t img_head;      // uint2 entries per head of the image
   const int32_t* bias_tiles;
+  int batch;             // samples (persistent instance: rows are found from cu_seqlens)
+  int64_t total_rows;    // sum of N_i (persistent instance)
 };
 
 // Pair bias image: for head h, sample i, 16-query tile qt and 16-key tile kt
@@ -330,49 +332,86 @@ __device__ __forceinline__ float query_max(float v) {
 // ---------------------------------------------------------------- pair attention, head_dim 32
 // Pair attention for head_dim 32 and N_i <= kAttnLongLen, organised so that
 // the exponentials are nearly the only vector work.  A workgroup of NW waves
-// takes (sample, block of up to 16 NW queries, group of 16 pair rows, head):
+// runs a stretch of pair rows of one head, a block of up to 16 NW queries:
 //   * the bias of (query, key) does not depend on the pair row, so each lane
 //     keeps the bias of its query for its 4-key groups of every key tile in
-//     registers for the whole group of rows -- staged once through LDS and
-//     divided by the softmax scale (one bf16 rounding) -- and it seeds the
-//     score accumulators: the matrix cores produce bias/scale + q.k directly;
+//     registers while the rows belong to one sample -- read from the bias
+//     image, already divided by the softmax scale (one bf16 rounding) -- and
+//     it seeds the score accumulators: the matrix cores produce
+//     bias/scale + q.k directly;
 //   * keys and values of a row are copied straight into LDS (keys as fragment
 //     images: 64 lanes x 16 bytes, read as one contiguous 1 KB per wave) in
-//     two buffers that alias the bias staging area, the next row's copies in
-//     flight while the current row runs: one barrier per row;
+//     two buffers, the next row's copies in flight while the current row
+//     runs: one barrier per row;
 //   * the softmax denominator comes from one more matrix-core product with a
 //     ones operand, on the same bf16 probabilities as the numerator.
 // Scores are kept transposed (S^T = K Q^T), so a lane holds 16 keys of one
 // query per 64-key chunk and the running max is mostly lane-local.
-// Two instances: N <= 256 with 16 waves (all queries of a row group in one
-// workgroup, so a row's keys and values are copied once per CU; 64 KB of LDS,
-// four waves per SIMD) and N <= 512 with 8 waves (128 KB, twice the bias
-// registers, two waves per SIMD).
-template <int NMAX, int NW>
+// Two instances: N <= 256, persistent, with 16 waves (all queries of a row in
+// one workgroup, so a row's keys and values are copied once per CU; 64 KB of
+// LDS, four waves per SIMD, one workgroup per CU with an equal share of the
+// rows) and N <= 512 from a work list of (sample, query block, group of 16
+// rows) items with 8 waves (128 KB, twice the bias registers, two waves per
+// SIMD).
+template <int NMAX, int NW, bool PERSIST>
 __global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_kernel(PairAttnArgs p) {
   constexpr int D = 32;
   constexpr int KT16 = NMAX / 16;               // key tiles
+  static_assert(!PERSIST || NW * 16 >= NMAX, "the persistent instance covers all queries of a row");
   extern __shared__ __attribute__((aligned(16))) bf16 lds[];
-  // Work position pos runs on XCD pos % 8; the H heads of one position are
-  // launched as consecutive workgroups of that XCD (ids 8 (H k + h) + x), so
-  // they read the same q|k|v cache lines at about the same time.
-  const int x = blockIdx.x % kXcds, t = blockIdx.x / kXcds;
-  const int h = t % p.H, pos = (t / p.H) * kXcds + x;
-  const int4 w4 = reinterpret_cast<const int4*>(p.work)[pos];
-  const int i = w4.x;
-  if (i < 0) return;
-  const int qt0 = w4.y, rg = w4.z, nqt = w4.w;       // first 16-query tile, row group, tile count
-  const int n = p.cu_seqlens[i + 1] - p.cu_seqlens[i];
-  const int npad = (n + 63) & ~63;
-  const int64_t cu = p.cu_pairs[i];
-  const int64_t sr = p.axis == 0 ? n : 1, st = p.axis == 0 ? 1 : n;   // cell(r, t) = cu + r*sr + t*st
   bf16* Kb0 = lds;                                         // key images: tile of 16 keys -> 512 elements
   bf16* Kb1 = Kb0 + NMAX * D;
   bf16* Vb0 = Kb1 + NMAX * D;                              // values, row-major [key][D]
   bf16* Vb1 = Vb0 + NMAX * D;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l16 = lane & 15, g = lane >> 4;
+
+  // ---- rows of this workgroup: packed rows [row, row_end) of one head, a
+  // query block starting at tile qt0.
+  //   * work-list instance: workgroup 8 (H k + h) + x runs on XCD x and takes
+  //     work position pos = 8 k + x, head h: the H heads of a position are
+  //     consecutive workgroups of one XCD, so they read the same q|k|v cache
+  //     lines at about the same time; rows of one sample only.
+  //   * persistent instance (one workgroup per CU): XCD x takes the x-th
+  //     eighth of all packed rows, and its workgroups split that range among
+  //     the heads, workgroup k taking head k % H and the (k / H)-th of the
+  //     equal slices of that head, so every CU gets the same number of rows
+  //     (crossing sample boundaries) and the heads of a row still run on one
+  //     XCD together.
+  int h, i, qt0, nqt_w = 0;
+  int64_t row, row_end;
+  if constexpr (PERSIST) {
+    const int x = blockIdx.x % kXcds, k = blockIdx.x / kXcds, per = (int)(gridDim.x / kXcds);
+    h = k % p.H;
+    const int m = k / p.H, M = (per - h + p.H - 1) / p.H;
+    const int64_t xa = p.total_rows * x / kXcds, xb = p.total_rows * (x + 1) / kXcds;
+    row = xa + (xb - xa) * m / M;
+    row_end = xa + (xb - xa) * (m + 1) / M;
+    if (row >= row_end) return;
+    int lo = 0, hi = p.batch;                   // cu_seqlens[lo] <= row < cu_seqlens[hi]
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (p.cu_seqlens[mid] <= row) lo = mid;
+      else hi = mid;
+    }
+    i = __builtin_amdgcn_readfirstlane(lo);
+    qt0 = 0;
+  } else {
+    const int x = blockIdx.x % kXcds, t = blockIdx.x / kXcds;
+    h = t % p.H;
+    const int pos = (t / p.H) * kXcds + x;
+    const int4 w4 = reinterpret_cast<const int4*>(p.work)[pos];
+    i = w4.x;
+    if (i < 0) return;
+    qt0 = w4.y;
+    const int nn = p.cu_seqlens[i + 1] - p.cu_seqlens[i];
+    const int r0 = w4.z * kAttnRG;
+    row = p.cu_seqlens[i] + r0;
+    row_end = p.cu_seqlens[i] + min(nn, r0 + kAttnRG);
+    nqt_w = w4.w;
+  }
   const int j0 = qt0 * 16;
+  const int jw = j0 + 16 * wave + l16;          // this lane's query
 
   // ---- per-row staging: straight global -> LDS copies ---------------------
   // Each wave copies its key tiles (wave, wave + NW, ...; 16 keys each) with
@@ -382,44 +421,60 @@ __global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_k
   // Every tile below the 64-key padded length is written (the last chunk
   // reads up to there): keys past N repeat key N-1, so the padding holds
   // finite values whose probabilities are masked to zero.
-  auto dma_kv = [&](int r, bf16* Kb, bf16* Vr) {
+  auto dma_kv = [&](int sn, int64_t scu, int r, bf16* Kb, bf16* Vr) {
+    const int snpad = (sn + 63) & ~63;
+    const int64_t ssr = p.axis == 0 ? sn : 1, sst = p.axis == 0 ? 1 : sn;
 #pragma unroll
     for (int kt = wave; kt < KT16; kt += NW) {
-      if (kt * 16 >= npad) break;
+      if (kt * 16 >= snpad) break;
       // values: the 16-byte chunk at column c of key row kv holds dim group
       // c ^ ((kv >> 2) & 3), so the four key groups of a transpose read fall
       // on different banks
       const int kv = kt * 16 + (lane >> 2);
-      const int key_k = min(kt * 16 + l16, n - 1), key_v = min(kv, n - 1);
+      const int key_k = min(kt * 16 + l16, sn - 1), key_v = min(kv, sn - 1);
       const int dgv = (lane & 3) ^ ((kv >> 2) & 3);
-      const bf16* sk = p.k + (cu + (int64_t)r * sr + (int64_t)key_k * st) * p.ld_qkv + h * D + g * 8;
-      const bf16* sv = p.v + (cu + (int64_t)r * sr + (int64_t)key_v * st) * p.ld_qkv + h * D + dgv * 8;
+      const bf16* sk = p.k + (scu + (int64_t)r * ssr + (int64_t)key_k * sst) * p.ld_qkv + h * D + g * 8;
+      const bf16* sv = p.v + (scu + (int64_t)r * ssr + (int64_t)key_v * sst) * p.ld_qkv + h * D + dgv * 8;
       __builtin_amdgcn_global_load_lds((const void*)sk, (__attribute__((address_space(3))) void*)(Kb + kt * 512), 16, 0, 0);
       __builtin_amdgcn_global_load_lds((const void*)sv, (__attribute__((address_space(3))) void*)(Vr + kt * 512), 16, 0, 0);
     }
+  };
+  // query fragment of this lane for row r of a sample with sn elements at
+  // pair offset scu (zero past N)
+  auto load_q = [&](int sn, int64_t scu, int r) -> bf16x8 {
+    if (jw >= sn) return bf16x8{};
+    const int64_t ssr = p.axis == 0 ? sn : 1, sst = p.axis == 0 ? 1 : sn;
+    return *reinterpret_cast<const bf16x8*>(p.q + (scu + (int64_t)r * ssr + (int64_t)jw * sst) * p.ld_qkv + h * D + g * 8);
   };
   const VtLane vl = vt_lane(l16, g);
   auto v_frags1 = [&](const bf16* Vr, int kb, bf16x8 (&f)[2]) { vt_frags1(Vr, kb, vl, f); };
   auto v_frags2 = [&](const bf16* Vr, int kb, bf16x8 (&f)[4]) { vt_frags2(Vr, kb, vl, f); };
 
-  const int jw = j0 + 16 * wave + l16;          // this lane's query
-  const bool wave_has_queries = wave < nqt && j0 + 16 * wave < n;
-  const bool qvalid = jw < n;
-  const int r0 = rg * kAttnRG, r1 = min(n, r0 + kAttnRG);
-  bf16x8 qf = qvalid ? *reinterpret_cast<const bf16x8*>(p.q + (cu + (int64_t)r0 * sr + (int64_t)jw * st) * p.ld_qkv + h * D + g * 8)
-                     : bf16x8{};
+  // ---- per-sample state ------------------------------------------------------
+  int n = 0;
+  int64_t cu = 0, sr = 0, st = 0;               // cell(r, t) = cu + r*sr + t*st
+  bool wave_has_queries = false, qvalid = false;
   // lane's bias: query 16*wave + l16, keys 16*kt + 4g .. +3 of every key
   // tile, read from the bias image (one contiguous 512 bytes per wave and tile)
   uint2 bias_r[KT16];
-  {
-    const int kti = npad / 16;
+  auto set_sample = [&](int si, int sn, int64_t scu) {
+    n = sn;
+    cu = scu;
+    sr = p.axis == 0 ? n : 1;
+    st = p.axis == 0 ? 1 : n;
+    wave_has_queries = wave < (PERSIST ? (n + 15) / 16 : nqt_w) && j0 + 16 * wave < n;
+    qvalid = jw < n;
+    const int kti = ((n + 63) & ~63) / 16;
     const uint2* img = p.bias_img && wave_has_queries
-                           ? p.bias_img + h * p.img_head + ((int64_t)p.bias_tiles[i] + (int64_t)(qt0 + wave) * kti) * 64 + lane
+                           ? p.bias_img + h * p.img_head + ((int64_t)p.bias_tiles[si] + (int64_t)(qt0 + wave) * kti) * 64 + lane
                            : nullptr;
 #pragma unroll
     for (int kt = 0; kt < KT16; ++kt) bias_r[kt] = img && kt < kti ? img[kt * 64] : make_uint2(0u, 0u);
-  }
-  dma_kv(r0, Kb0, Vb0);
+  };
+  set_sample(i, __builtin_amdgcn_readfirstlane(p.cu_seqlens[i + 1] - p.cu_seqlens[i]), p.cu_pairs[i]);
+  int r = __builtin_amdgcn_readfirstlane((int)(row - p.cu_seqlens[i]));
+  bf16x8 qf = load_q(n, cu, r);
+  dma_kv(n, cu, r, Kb0, Vb0);
   __builtin_amdgcn_s_waitcnt(0);                // this wave's copies have landed
   __syncthreads();
 
@@ -427,15 +482,32 @@ __global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_k
 #pragma unroll
   for (int e = 0; e < 8; ++e) ones[e] = (bf16)1.f;
   const float c = p.scale_log2;                 // scale * log2(e)
-  for (int r = r0; r < r1; ++r) {
-    const bool odd = (r - r0) & 1;
+  bool odd = false;
+  for (; row < row_end; ++row) {
     const bf16* Kb = odd ? Kb1 : Kb0;
     const bf16* Vb = odd ? Vb1 : Vb0;
-    const bool more = r + 1 < r1;
+    const bool more = row + 1 < row_end;
+    // the next row: same sample, or the first row of the next non-empty one
+    // (sample extents are read only when the sample changes: a global load
+    // here would make the wave wait for every copy and store in flight)
+    int i2 = i, r2 = r + 1, n2 = n;
+    int64_t cu2 = cu;
+    if (more && r2 >= n) {
+      i2 = i + 1;
+      while (p.cu_seqlens[i2 + 1] <= row + 1) ++i2;
+      r2 = 0;
+      n2 = p.cu_seqlens[i2 + 1] - p.cu_seqlens[i2];
+      cu2 = p.cu_pairs[i2];
+    }
+    i2 = __builtin_amdgcn_readfirstlane(i2);
+    r2 = __builtin_amdgcn_readfirstlane(r2);
+    n2 = __builtin_amdgcn_readfirstlane(n2);
+    cu2 = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(cu2 >> 32)) << 32) |
+                    (uint32_t)__builtin_amdgcn_readfirstlane((int)cu2));
     bf16x8 qn = qf;
     if (more) {
-      dma_kv(r + 1, odd ? Kb0 : Kb1, odd ? Vb0 : Vb1);
-      if (qvalid) qn = *reinterpret_cast<const bf16x8*>(p.q + (cu + (int64_t)(r + 1) * sr + (int64_t)jw * st) * p.ld_qkv + h * D + g * 8);
+      dma_kv(n2, cu2, r2, odd ? Kb0 : Kb1, odd ? Vb0 : Vb1);
+      qn = load_q(n2, cu2, r2);
     }
     // keep the bias packed: converting it once outside the row loop would
     // double its registers
@@ -545,7 +617,16 @@ __global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_k
     }
     __builtin_amdgcn_s_waitcnt(0);              // copies for the next row have landed
     __syncthreads();
+    if (i2 != i) {                              // bias of the next sample
+      set_sample(i2, n2, cu2);
+      // landed before the back edge, so the loop head has no load pending
+      // and waits for none of the next row's copies
+      __builtin_amdgcn_s_waitcnt(0);
+    }
+    i = i2;
+    r = r2;
     qf = qn;
+    odd = !odd;
   }
 }
 
@@ -845,18 +926,20 @@ hipError_t launch_attention(const nt_layout& L, int axis, int H, int D, const vo
     }
     PairAttnArgs a{axis, (const bf16*)q, (const bf16*)k, (const bf16*)v, ld_qkv, (const bf16*)bias, ld_bias,
                    scale * kLog2e, (bf16*)o, ld_o, L.d_pattn_work, L.d_cu_seqlens, L.d_cu_pairs, H,
-                   img, tiles * 64, L.d_bias_tiles};
+                   img, tiles * 64, L.d_bias_tiles, L.batch, L.sum_n};
     const size_t smem = sizeof(bf16) * 4 * (size_t)nmax * 32;
     const dim3 grid((unsigned)(L.pattn_items() * H));
     if (nmax == kAttnShortLen) {
-      // one workgroup of 16 waves covers all queries of a row group
-      a.work = L.d_pattn16_work;
-      const dim3 grid16((unsigned)(L.pattn16_items() * H));
-      hipFuncSetAttribute((const void*)attention_pair_kernel<kAttnShortLen, 16>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-      attention_pair_kernel<kAttnShortLen, 16><<<grid16, dim3(1024), smem, s>>>(a);
+      // persistent: one workgroup of 16 waves per CU (all queries of a row);
+      // per XCD a multiple of H workgroups, at least H, so every head gets an
+      // equal share of each XCD's rows
+      const int per_xcd = std::max(H, compute_units() / kXcds / H * H);
+      const dim3 gridp((unsigned)(per_xcd * kXcds));
+      hipFuncSetAttribute((const void*)attention_pair_kernel<kAttnShortLen, 16, true>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+      attention_pair_kernel<kAttnShortLen, 16, true><<<gridp, dim3(1024), smem, s>>>(a);
     } else {
-      hipFuncSetAttribute((const void*)attention_pair_kernel<kAttnLongLen, 8>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-      attention_pair_kernel<kAttnLongLen, 8><<<grid, dim3(512), smem, s>>>(a);
+      hipFuncSetAttribute((const void*)attention_pair_kernel<kAttnLongLen, 8, false>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+      attention_pair_kernel<kAttnLongLen, 8, false><<<grid, dim3(512), smem, s>>>(a);
     }
     return hipGetLastError();
   }

@@ -42,17 +42,26 @@ struct TriArgs {
 __global__ void __launch_bounds__(kTriThreads, 1) triangle_mfma_kernel(TriArgs p) {
   __shared__ __attribute__((aligned(16))) float stage[16 * kTriRS * kTriSC];
   __shared__ __attribute__((aligned(16))) bf16 zbuf[2][16 * kTriTile * kTriCB];   // z of two bands, [row][col][16]
-  // Workgroup id = 8 (4 k + j) + x runs on XCD x: its k-th (tile, line group)
-  // pair q = 8 k + x, channel block j of that group.
+  // Workgroup id runs on XCD id % 8, which takes the contiguous range
+  // [x W / 8, (x + 1) W / 8) of the sequence u = 4 v + j, where v runs over
+  // (sample, line group, tile) with the sample's tiles innermost and j is the
+  // channel block inside the line group.  The 32 workgroups an XCD holds at
+  // once then cover 8 tiles x 4 channel blocks of one sample and line group:
+  // an operand row block is fetched into that L2 for all tiles that use it,
+  // and each z line by the four blocks that share it.
   const int id = blockIdx.x;
-  const int xcd = id % kXcds, k = id / kXcds;
-  const int q = (k >> 2) * kXcds + xcd;
-  const int item = q / p.groups, cb = (q % p.groups) * 4 + (k & 3);
-  if (item >= p.items || cb >= p.nblk) return;
-  const int i = p.work[4 * item];
+  const int u = (id % kXcds) * (int)(gridDim.x / kXcds) + id / kXcds;
+  const int v = u >> 2;
+  const int e = v / p.groups;                         // an item of the same sample
+  if (e >= p.items) return;
+  const int i = p.work[4 * e];
   if (i < 0) return;
-  const int xt = p.work[4 * item + 1], yt = p.work[4 * item + 2];
   const int n = p.cu_seqlens[i + 1] - p.cu_seqlens[i];
+  const int first = p.work[4 * e + 3], ntile = (n + kTriTile - 1) / kTriTile;
+  const int r = v - p.groups * first;                 // in [0, groups * ntile^2)
+  const int item = first + r % (ntile * ntile), cb = (r / (ntile * ntile)) * 4 + (u & 3);
+  if (cb >= p.nblk) return;
+  const int xt = p.work[4 * item + 1], yt = p.work[4 * item + 2];
   const int nkt = (n + 31) >> 5;
   const int64_t P = p.cu_pad[i], cu = p.cu_pairs[i];
   const int x0 = xt * kTriTile, y0 = yt * kTriTile;
@@ -209,8 +218,8 @@ hipError_t launch_triangle(const nt_layout& L, int C, const void* a, const void*
   const int nblk = C / kTriCB, groups = (nblk + 3) / 4;
   TriArgs t{C, nblk, (const bf16*)a, (const bf16*)b, ld_ab, (bf16*)z, ld_z, L.d_tri_work, L.d_cu_seqlens,
             L.d_cu_pairs, L.d_cu_pad, (int)items, groups};
-  const int64_t pairs = (items * groups + kXcds - 1) / kXcds * kXcds;   // (tile, line group) pairs, padded
-  triangle_mfma_kernel<<<dim3((unsigned)(pairs * 4)), dim3(kTriThreads), 0, s>>>(t);
+  // items is a multiple of 8, so the grid splits evenly over the XCDs
+  triangle_mfma_kernel<<<dim3((unsigned)(items * groups * 4)), dim3(kTriThreads), 0, s>>>(t);
   return hipGetLastError();
 }
 

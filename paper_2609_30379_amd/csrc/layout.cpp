@@ -149,8 +149,9 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L) {
   // ceil(tiles / W) blocks of at most W tiles (items: sample, first tile, row
   // group, tile count), so no block leaves most of its waves idle; generation
   // order is kept in each XCD's queue so the blocks of a row group stay
-  // adjacent and share keys and values.  W = 8 (the N <= 512 instance) and
-  // W = 16 (the 16-wave N <= 256 instance).
+  // adjacent and share keys and values.  W = 8, for the N <= 512 instance
+  // (the N <= 256 instance needs no list: its workgroups find their rows
+  // from the prefix sums).
   auto pair_attn_items = [&](int32_t W) {
     std::vector<std::array<int32_t, 4>> items;
     std::vector<double> cost;
@@ -167,7 +168,6 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L) {
     return xcd_order<4>(items, cost, false);
   };
   L->pattn_work = pair_attn_items(kAttnQB / 16);
-  L->pattn16_work = pair_attn_items(16);
   // 1-D attention: the same even split of a sample's 16-query tiles over
   // blocks of at most kAttnQB queries, one item per block
   {
@@ -193,9 +193,11 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L) {
     if (t > INT32_MAX) return fail(NT_ERR_OVERFLOW, "bias image extent exceeds int32 at sample " + std::to_string(i));
     L->bias_tiles[i + 1] = (int32_t)t;
   }
-  // triangle: one item per (sample, 64x64 output tile), largest samples first
-  // (the launch spreads (tile, group of channel blocks) pairs over the XCDs);
-  // the list is padded to a multiple of 8 with idle items.
+  // triangle: one item per (sample, 64x64 output tile), largest samples first,
+  // a sample's tiles contiguous and each carrying the index of the sample's
+  // first item (the launch walks (sample, channel line group, tile) in this
+  // order, one contiguous stretch per XCD); the list is padded to a multiple
+  // of 8 with idle items.
   {
     std::vector<int32_t> order(batch);
     std::iota(order.begin(), order.end(), 0);
@@ -203,12 +205,13 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L) {
     L->tri_work.clear();
     for (int32_t i : order) {
       const int32_t n = lengths[i], nt = (n + kTriTile - 1) / kTriTile;
+      const int32_t first = (int32_t)(L->tri_work.size() / 4);
       for (int32_t xt = 0; xt < nt; ++xt)
         for (int32_t yt = 0; yt < nt; ++yt) {
           L->tri_work.push_back(i);
           L->tri_work.push_back(xt);
           L->tri_work.push_back(yt);
-          L->tri_work.push_back(0);
+          L->tri_work.push_back(first);
         }
     }
     while ((L->tri_work.size() / 4) % kXcds) L->tri_work.insert(L->tri_work.end(), {-1, -1, -1, -1});

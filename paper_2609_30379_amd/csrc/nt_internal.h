@@ -46,7 +46,6 @@ struct nt_layout {
   std::vector<int32_t> seq_work;     // pairs (sample, query block); count multiple of 8
   std::vector<int32_t> pattn_work;  // quads (sample, first 16-query tile, row group, tile count)
   std::vector<int32_t> bias_tiles;   // [B+1] prefix of ceil(N_i/16) * round_up(N_i,64)/16: bias image tiles
-  std::vector<int32_t> pattn16_work;  // the same with blocks of up to 256 queries (16 waves)
   std::vector<int32_t> sattn_work;   // 1-D attention: quads (sample, first 16-query tile, 0, tile count)
   std::vector<int32_t> blk_prow;     // [ceil(sum N^2 / kLinRows)] pair row holding cell kLinRows*b
   std::vector<int32_t> bc_tiles;     // quads per 16-cell tile t: pair row eta of cell 16t, its column
@@ -68,7 +67,6 @@ struct nt_layout {
   const int32_t* d_blk_prow = nullptr;
   const int32_t* d_bias_tiles = nullptr;
   const int32_t* d_sattn_work = nullptr;
-  const int32_t* d_pattn16_work = nullptr;
   const int32_t* d_bc_tiles = nullptr;
   // pair attention workspace (the bias image), allocated by the first call
   // that needs it and grown on demand; freed with the layout
@@ -79,7 +77,6 @@ struct nt_layout {
   int64_t tri_items() const { return (int64_t)tri_work.size() / 4; }
   int64_t seq_items() const { return (int64_t)seq_work.size() / 2; }
   int64_t pattn_items() const { return (int64_t)pattn_work.size() / 4; }
-  int64_t pattn16_items() const { return (int64_t)pattn16_work.size() / 4; }
   int64_t sattn_items() const { return (int64_t)sattn_work.size() / 4; }
   int64_t bias_tiles_total() const { return bias_tiles.empty() ? 0 : bias_tiles.back(); }
 };

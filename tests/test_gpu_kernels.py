@@ -224,18 +224,22 @@ def _head_major(bias_cells):
 
 @pytest.mark.parametrize("axis", [0, 1])
 @pytest.mark.parametrize("dtype,H,D,lset", [("bf16", 4, 32, "att"), ("bf16", 2, 64, "att"), ("f32", 2, 8, "tiny"),
+                                            ("bf16", 3, 32, "att"), ("bf16", 4, 32, "few"),
                                             ("bf16", 2, 32, "long"), ("bf16", 2, 32, "edge256"),
                                             ("bf16", 2, 32, "mid"), ("bf16", 2, 32, "mid512")])
 def test_pair_attention(B, axis, dtype, H, D, lset):
     import torch
-    # head_dim 32: samples up to 256 take the short-row kernel with two
-    # workgroups per CU ("att"; "edge256": the longest sample, whole key chunks
-    # only, one full query block), up to 512 its one-workgroup-per-CU instance
-    # ("mid": a short tail chunk; "mid512": the longest sample, a sample just
-    # past 256 and one of length 1); "long" (a sample above 512) and head_dim
-    # 64 take the per-row path
+    # head_dim 32: samples up to 256 take the persistent short-row kernel, one
+    # workgroup per CU with an equal share of all rows, crossing sample
+    # boundaries ("att", also with 3 heads, which do not divide the
+    # workgroups of an XCD; "few": fewer rows than workgroups, an empty
+    # sample; "edge256": the longest sample, whole key chunks only, one full
+    # query block), up to 512 its work-list instance ("mid": a short tail
+    # chunk; "mid512": the longest sample, a sample just past 256 and one of
+    # length 1); "long" (a sample above 512) and head_dim 64 take the per-row
+    # path
     L = {"att": ATT_LENGTHS, "tiny": LENGTHS["tiny"], "long": [530, 7, 64], "edge256": [256, 128, 2, 192, 65],
-         "mid": [300, 64, 3], "mid512": [512, 257, 1, 100]}[lset]
+         "mid": [300, 64, 3], "mid512": [512, 257, 1, 100], "few": [3, 0, 2]}[lset]
     lay = _layout(B, L)
     R = sum(n * n for n in L)
     qkv = _n(23, "qkv", (R, 3 * H * D), 1.0, dtype)
