@@ -44,7 +44,7 @@ nt_status upload(nt_layout* L, hipStream_t s) {
       {&L->blk_prow, &L->d_blk_prow},
       {&L->pattn_work, &L->d_pattn_work}, {&L->bias_tiles, &L->d_bias_tiles},
       {&L->sattn_work, &L->d_sattn_work},
-      {&L->bc_tiles, &L->d_bc_tiles},
+      {&L->bc_cu_tiles, &L->d_bc_cu_tiles},
   };
   size_t total = 0;
   for (auto& p : parts) total += (p.v->size() * sizeof(int32_t) + 255) / 256 * 256;

@@ -49,7 +49,8 @@ struct LinArgs {
   const bf16* bc_u;
   const bf16* bc_v;
   int64_t ld_bc_u, ld_bc_v;
-  const int4* bc_tiles;       // per 16-cell tile: pair row, column, N_i, eta_i of its first cell
+  const int32_t* bc_cu_tiles; // per sample: broadcast tiles (16 cells of one pair row) before it
+  int bc_ntiles;              // all broadcast tiles
 };
 
 // Position of the pair cell (a, b) of sample i in its pair-tiled operand plane:
@@ -883,7 +884,7 @@ __global__ void __launch_bounds__(kStreamThreads, 2) linear_stream_kernel(LinArg
 // optional channel-major tail, with no workgroup barrier after set-up: the
 // weights of all output columns sit in LDS as matrix-core fragment images
 // (copied once per workgroup), and every wave streams its own 16-row tiles
-// -- rows loaded straight into B-fragment order three tiles ahead,
+// -- rows loaded straight into B-fragment order one tile ahead,
 // LayerNorm in registers (a row's K values are spread over the four lanes
 // l16 + 16 g, two lane swaps per statistic), the products over groups of 8
 // column tiles, and a write-back through a wave-private LDS stage so that
@@ -891,8 +892,13 @@ __global__ void __launch_bounds__(kStreamThreads, 2) linear_stream_kernel(LinArg
 // never wait for each other; per tile a wave reads the weights from LDS once
 // per 16 rows.
 constexpr int kWaveThreads = 512;
-constexpr int kWavePF = 3;                        // tiles in flight per wave
 constexpr int kWaveGroup = 8;                     // column tiles per product group (128 columns)
+// Outputs of one column group (G = 1) and the tail tiles are written without
+// a loop of run-time trip count: such a loop that stores makes the compiler
+// wait for every load in flight (the next tile's rows) before entering it.
+// Wider outputs (G > 1) keep the group loop and that wait.
+constexpr int kWaveMaxGroups = 4;                 // main columns up to 512
+constexpr int kWaveMaxTail = 2;                   // channel-major tail up to 32 channels
 
 template <int EPI> constexpr int wave_stage_stride() { return EPI == NT_EPI_RESIDUAL ? 132 : 144; }
 template <int EPI> constexpr int wave_stage_bytes() {
@@ -905,10 +911,14 @@ template <int K, int EPI> size_t wave_smem_bytes(int nt16) {
 
 // With BC the rows are not read from x: row m = cell(i, a, b) of a pair layout
 // is the pair broadcast u[eta_i + a] + v[eta_i + b] (fp32 sum rounded to bf16,
-// exactly what the broadcast op stores), built as the tile is loaded.  Each
-// wave then takes a contiguous range of tiles and walks its lanes' cells
-// forward from the layout's per-tile table (no search per tile).
-template <int EPI, int K, bool BC>
+// exactly what the broadcast op stores), built as the tile is loaded.  A tile
+// is then 16 cells of one pair row (the last of a row masked), so u is one
+// row per tile and v rows follow the lane; each wave takes a contiguous range
+// of tiles and walks it with wave-uniform (sample, pair row, column tile)
+// counters.  (A per-lane cursor that wraps across pair rows makes the
+// compiler copy the prefetched rows out of their load registers, which waits
+// for the loads and defeats the prefetch.)
+template <int EPI, int K, bool BC, int G>
 __global__ void __launch_bounds__(kWaveThreads, 1) linear_wave_kernel(LinArgs p) {
   static_assert(!BC || EPI != NT_EPI_RESIDUAL, "the broadcast rows use the residual buffers");
   constexpr int KT = K / 32;
@@ -947,67 +957,82 @@ __global__ void __launch_bounds__(kWaveThreads, 1) linear_wave_kernel(LinArgs p)
   unsigned char* stage = stage_base + (size_t)wave * wave_stage_bytes<EPI>();
   const int c8n = p.n_main / 8;                   // 16-byte chunks per output row
 
-  // broadcast cursor of this lane: cell (pair row c_pr = eta_i + a, column
-  // c_b) of sample i with N_i = c_n and eta_i = c_vb; it only moves forward
-  int c_pr = 0, c_b = 0, c_n = 1, c_vb = 0, c_m = 0;
-  auto bc_wrap = [&]() {
-    while (c_b >= c_n) {
-      c_b -= c_n;
-      ++c_pr;
-      if (c_pr == c_vb + c_n) {                 // first pair row of the next sample
-        const int i = p.row_sample[c_pr];
-        c_vb = p.cu_seqlens[i];
-        c_n = p.cu_seqlens[i + 1] - c_vb;
-      }
-    }
+  // broadcast walk (uniform across the wave): sample w_i with N_i = w_n,
+  // first single row w_vb and first pair cell w_cup; pair row w_a, column
+  // tile w_ct.  Sample tables are read only when the walk enters a sample.
+  int w_i = 0, w_n = 1, w_vb = 0, w_cup = 0, w_a = 0, w_ct = 0;
+  auto bc_sample = [&](int i) {
+    w_i = i;
+    w_vb = __builtin_amdgcn_readfirstlane(p.cu_seqlens[i]);
+    w_n = __builtin_amdgcn_readfirstlane(p.cu_seqlens[i + 1]) - w_vb;
+    w_cup = __builtin_amdgcn_readfirstlane(p.cu_pairs[i]);
   };
   auto bc_start = [&](int t) {
-    const int4 rec = p.bc_tiles[t];
-    c_m = min(t * 16 + l16, p.rows - 1);
-    c_pr = rec.x; c_b = rec.y + (c_m - t * 16); c_n = rec.z; c_vb = rec.w;
-    bc_wrap();
+    int lo = 0, hi = p.batch;                   // bc_cu_tiles[lo] <= t < bc_cu_tiles[hi]
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (p.bc_cu_tiles[mid] <= t) lo = mid;
+      else hi = mid;
+    }
+    lo = __builtin_amdgcn_readfirstlane(lo);
+    bc_sample(lo);
+    const int loc = t - __builtin_amdgcn_readfirstlane(p.bc_cu_tiles[lo]), ctn = (w_n + 15) >> 4;
+    w_a = loc / ctn;
+    w_ct = loc - w_a * ctn;
   };
-  auto bc_next = [&]() {                        // to the same lane's cell 16 rows on
-    if (c_m + 16 < p.rows) {
-      c_m += 16;
-      c_b += 16;
-      bc_wrap();
+  auto bc_advance = [&]() {                     // to the next tile (stays on the last one at the end)
+    if (++w_ct * 16 >= w_n) {
+      w_ct = 0;
+      if (++w_a == w_n) {
+        w_a = 0;
+        int i = w_i + 1;
+        while (i < p.batch && p.cu_seqlens[i + 1] == p.cu_seqlens[i]) ++i;
+        if (i < p.batch) bc_sample(__builtin_amdgcn_readfirstlane(i));
+        else { w_a = w_n - 1; w_ct = (w_n - 1) >> 4; }
+      }
     }
   };
 
   // rows of tile t in B-fragment order: lane (l16, g) holds row 16t + l16,
   // k = 32 kk + 8 g .. +7; residual rows in write-back order (4 chunks a lane);
-  // broadcast sources: u in xr, v in rr (the cursor is at tile t)
-  auto load_tile = [&](int t, uint4 (&xr)[KT], uint4 (&rr)[4]) {
+  // broadcast sources: u in xr, v in rr (the walk is at the tile).  m0 and nv:
+  // the tile's first output row and its rows
+  auto load_tile = [&](int t, uint4 (&xr)[KT], uint4 (&rr)[4], int64_t& m0, int& nv) {
     if constexpr (BC) {
       static_assert(KT <= 4, "v rows fit the residual buffers");
-      const bf16* su = p.bc_u + (int64_t)c_pr * p.ld_bc_u + g * 8;
-      const bf16* sv = p.bc_v + (int64_t)(c_vb + c_b) * p.ld_bc_v + g * 8;
+      const bf16* su = p.bc_u + (int64_t)(w_vb + w_a) * p.ld_bc_u + g * 8;
+      const bf16* sv = p.bc_v + (int64_t)(w_vb + min(w_ct * 16 + l16, w_n - 1)) * p.ld_bc_v + g * 8;
 #pragma unroll
       for (int kk = 0; kk < KT; ++kk) {
         xr[kk] = *reinterpret_cast<const uint4*>(su + kk * 32);
         rr[kk] = *reinterpret_cast<const uint4*>(sv + kk * 32);
       }
-      bc_next();
+      m0 = (int64_t)w_cup + (int64_t)w_a * w_n + w_ct * 16;
+      nv = min(16, w_n - w_ct * 16);
+      bc_advance();
       return;
     }
-    const int m = t * 16 + l16;
-    const bool ok = t < ntile && m < p.rows;
+    m0 = (int64_t)t * 16;
+    nv = min(16, p.rows - t * 16);
+    // unconditional loads from rows clamped to the last one (rows past the
+    // end are masked by the LayerNorm or never stored): a load under a lane
+    // predicate would write zeros into registers that may still be awaiting
+    // an earlier load, and the compiler then waits for every load in flight
+    const int m = min(t * 16 + l16, p.rows - 1);
 #pragma unroll
-    for (int kk = 0; kk < KT; ++kk)
-      xr[kk] = ok ? *reinterpret_cast<const uint4*>(x + (int64_t)m * p.ldx + kk * 32 + g * 8) : make_uint4(0u, 0u, 0u, 0u);
+    for (int kk = 0; kk < KT; ++kk) xr[kk] = *reinterpret_cast<const uint4*>(x + (int64_t)m * p.ldx + kk * 32 + g * 8);
     if constexpr (RES) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const int row = q * 4 + (lane >> 4), cc = lane & 15, mm = t * 16 + row;
-        rr[q] = (t < ntile && mm < p.rows && cc < c8n) ? *reinterpret_cast<const uint4*>(p.res + (int64_t)mm * p.ld_res + cc * 8)
-                                                      : make_uint4(0u, 0u, 0u, 0u);
+        const int row = q * 4 + (lane >> 4), cc = max(min(lane & 15, c8n - 1), 0), mm = min(t * 16 + row, p.rows - 1);
+        rr[q] = *reinterpret_cast<const uint4*>(p.res + (int64_t)mm * p.ld_res + cc * 8);
       }
     }
   };
 
-  auto process = [&](int t, const uint4 (&xr_in)[KT], const uint4 (&rr)[4]) {
-    const int m = t * 16 + l16;
+  auto process = [&](int64_t m0, int nv, const uint4 (&xr_in)[KT], const uint4 (&rr)[4]) {
+    const int64_t m = m0 + l16;
+    const bool mv = l16 < nv;
     uint4 xr[KT];
 #pragma unroll
     for (int kk = 0; kk < KT; ++kk) xr[kk] = xr_in[kk];
@@ -1057,7 +1082,7 @@ __global__ void __launch_bounds__(kWaveThreads, 1) linear_wave_kernel(LinArgs p)
         const float gg[8] = {ga[kk][0].x, ga[kk][0].y, ga[kk][0].z, ga[kk][0].w, ga[kk][1].x, ga[kk][1].y, ga[kk][1].z, ga[kk][1].w};
         const float bb[8] = {be[kk][0].x, be[kk][0].y, be[kk][0].z, be[kk][0].w, be[kk][1].x, be[kk][1].y, be[kk][1].z, be[kk][1].w};
 #pragma unroll
-        for (int e = 0; e < 8; ++e) xb[kk][e] = (bf16)(m < p.rows ? (v[kk][e] - mean) * rstd * gg[e] + bb[e] : 0.f);
+        for (int e = 0; e < 8; ++e) xb[kk][e] = (bf16)(mv ? (v[kk][e] - mean) * rstd * gg[e] + bb[e] : 0.f);
       }
     } else {
 #pragma unroll
@@ -1065,7 +1090,7 @@ __global__ void __launch_bounds__(kWaveThreads, 1) linear_wave_kernel(LinArgs p)
     }
     // ---- main columns, group by group of 8 column tiles
     const int nmt = (p.n_main + 15) >> 4;
-    for (int cg = 0; cg * kWaveGroup < nmt; ++cg) {
+    auto group = [&](int cg) __attribute__((always_inline)) {
       f32x4 acc[kWaveGroup];
 #pragma unroll
       for (int j = 0; j < kWaveGroup; ++j) {
@@ -1102,8 +1127,9 @@ __global__ void __launch_bounds__(kWaveThreads, 1) linear_wave_kernel(LinArgs p)
       const int cc = lane & 15, col = cg * 128 + cc * 8;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const int row = q * 4 + (lane >> 4), mm = t * 16 + row;
-        if (col >= p.n_main || mm >= p.rows) continue;
+        const int row = q * 4 + (lane >> 4);
+        const int64_t mm = m0 + row;
+        if (col >= p.n_main || row >= nv) continue;
         bf16x8 o;
         if constexpr (RES) {
           const float* sf = reinterpret_cast<const float*>(stage) + row * SS + cc * 8;
@@ -1119,17 +1145,23 @@ __global__ void __launch_bounds__(kWaveThreads, 1) linear_wave_kernel(LinArgs p)
         // Non-temporal: measured on the pair block, streaming these outputs
         // past the caches leaves the memory-side cache to the next kernels
         // (row attention 158 -> 146 us; the projections themselves unchanged).
-        store_nt(p.y + (int64_t)mm * p.ldy + col, o);
+        store_nt(p.y + mm * p.ldy + col, o);
       }
-    }
+    };
+    if constexpr (G == 1) group(0);
+    else
+      for (int cg = 0; cg * kWaveGroup < nmt; ++cg) group(cg);
     // ---- tail columns (channel-major planes), column tile by column tile
     if (p.y_tail) {
-      for (int ct = p.n_main >> 4; ct < nt16; ++ct) {
+#pragma unroll
+      for (int jt = 0; jt < kWaveMaxTail; ++jt) {
+        const int ct = (p.n_main >> 4) + jt;
+        if (ct >= nt16) break;
         f32x4 acc = *reinterpret_cast<const f32x4*>(&s_bias[ct * 16 + 4 * g]);
 #pragma unroll
         for (int kk = 0; kk < KT; ++kk)
           acc = mfma16(*reinterpret_cast<const bf16x8*>(&Wimg[(ct * KT + kk) * 512 + lane * 8]), xb[kk], acc);
-        if (m >= p.rows) continue;
+        if (!mv) continue;
 #pragma unroll
         for (int ii = 0; ii < 4; ++ii) {
           const int nn = ct * 16 + 4 * g + ii;
@@ -1142,23 +1174,28 @@ __global__ void __launch_bounds__(kWaveThreads, 1) linear_wave_kernel(LinArgs p)
   };
 
   // tiles: strided over the waves, or with BC a contiguous range per wave
-  const int t0 = BC ? (int)((int64_t)ntile * wid / nw) : wid;
-  const int t1 = BC ? (int)((int64_t)ntile * (wid + 1) / nw) : ntile;
+  const int nT = BC ? p.bc_ntiles : ntile;
+  const int t0 = BC ? (int)((int64_t)nT * wid / nw) : wid;
+  const int t1 = BC ? (int)((int64_t)nT * (wid + 1) / nw) : ntile;
   const int ts = BC ? 1 : nw;
-  if (BC && t0 >= t1) return;
+  if (t0 >= t1) return;                         // (no barrier follows)
   if constexpr (BC) bc_start(t0);
-  uint4 xr[kWavePF][KT], rr[kWavePF][4];
-#pragma unroll
-  for (int d = 0; d < kWavePF; ++d) load_tile(t0 + d * ts, xr[d], rr[d]);
-  for (int i = 0; t0 + i * ts < t1;) {
-#pragma unroll
-    for (int d = 0; d < kWavePF; ++d) {
-      const int t = t0 + i * ts;
-      if (t >= t1) break;
-      process(t, xr[d], rr[d]);
-      load_tile(t0 + (i + kWavePF) * ts, xr[d], rr[d]);
-      ++i;
-    }
+  // Two register slots, each step issuing the next tile's loads before it
+  // processes the current one: the compiler's wait counts treat loads
+  // carried around a loop as just issued, so a tile consumed in the step
+  // after its loads would wait for everything in flight; loads issued in the
+  // same step before the first use stay outstanding.  Past the end the
+  // loads repeat valid rows and are never used.
+  uint4 xa[KT], ra[4], xb[KT], rb[4];
+  int64_t ma, mb;
+  int na, nb;
+  load_tile(t0, xa, ra, ma, na);
+  for (int t = t0; t < t1; t += 2 * ts) {
+    load_tile(t + ts, xb, rb, mb, nb);
+    process(ma, na, xa, ra);
+    if (t + ts >= t1) break;
+    load_tile(t + 2 * ts, xa, ra, ma, na);
+    process(mb, nb, xb, rb);
   }
 }
 
@@ -1621,15 +1658,22 @@ void launch_stream(const LinArgs& p, hipStream_t s) {
   kern<<<dim3((unsigned)grid), dim3(kStreamThreads), smem, s>>>(p);
 }
 
-template <int EPI, int K, bool BC = false>
-void launch_wave(const LinArgs& p, hipStream_t s) {
+template <int EPI, int K, bool BC, int G>
+void launch_wave_g(const LinArgs& p, hipStream_t s) {
   const int nt16 = (p.N + 15) / 16;
   const size_t smem = wave_smem_bytes<K, EPI>(nt16);
-  auto kern = linear_wave_kernel<EPI, K, BC>;
+  auto kern = linear_wave_kernel<EPI, K, BC, G>;
   (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
   const int ntile = (p.rows + 15) / 16;
   const int grid = std::min((ntile + kWaveThreads / 64 - 1) / (kWaveThreads / 64), compute_units());
   kern<<<dim3((unsigned)grid), dim3(kWaveThreads), smem, s>>>(p);
+}
+
+// instance by main column groups: one (up to 128 columns) or up to four
+template <int EPI, int K, bool BC = false>
+void launch_wave(const LinArgs& p, hipStream_t s) {
+  if (p.n_main <= 16 * kWaveGroup) launch_wave_g<EPI, K, BC, 1>(p, s);
+  else if constexpr (EPI != NT_EPI_RESIDUAL) launch_wave_g<EPI, K, BC, kWaveMaxGroups>(p, s);
 }
 
 template <int K>
@@ -1687,7 +1731,11 @@ hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
     if (smem > 150 * 1024) return hipErrorInvalidValue;
     p.bc_u = (const bf16*)a.bcast_u; p.bc_v = (const bf16*)a.bcast_v;
     p.ld_bc_u = a.ld_bcast_u; p.ld_bc_v = a.ld_bcast_v;
-    p.bc_tiles = reinterpret_cast<const int4*>(plan.layout->d_bc_tiles);
+    p.bc_cu_tiles = plan.layout->d_bc_cu_tiles;
+    p.bc_ntiles = plan.layout->bc_cu_tiles.back();
+    p.cu_seqlens = plan.layout->d_cu_seqlens;
+    p.cu_pairs = plan.layout->d_cu_pairs;
+    p.batch = plan.layout->batch;
     p.ldx = a.c_in;
 #define NT_WB(EPI) do { if (a.c_in == 64) launch_wave<EPI, 64, true>(p, s); else launch_wave<EPI, 128, true>(p, s); } while (0)
     if (a.epilogue == NT_EPI_GELU) NT_WB(NT_EPI_GELU);
@@ -1777,8 +1825,11 @@ hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
     const int nt16 = (a.c_out + 15) / 16;
     const size_t smem = a.c_in == 64 ? (res ? wave_smem_bytes<64, NT_EPI_RESIDUAL>(nt16) : wave_smem_bytes<64, NT_EPI_NONE>(nt16))
                                      : (res ? wave_smem_bytes<128, NT_EPI_RESIDUAL>(nt16) : wave_smem_bytes<128, NT_EPI_NONE>(nt16));
+    const int main_groups = (p.n_main + 16 * kWaveGroup - 1) / (16 * kWaveGroup);
+    const int tail_tiles = nt16 - p.n_main / 16;
     if (!xf && !tiled && (a.c_in == 64 || a.c_in == 128) && p.n_main % 8 == 0 && a.ldx % 8 == 0 &&
         p.ldy % 8 == 0 && (!res || (p.n_main <= 128 && a.ld_residual % 8 == 0)) && smem <= 150 * 1024 &&
+        main_groups <= kWaveMaxGroups && tail_tiles <= kWaveMaxTail &&
         (a.epilogue == NT_EPI_NONE || a.epilogue == NT_EPI_GELU || res)) {
 #define NT_WV(EPI) do { if (a.c_in == 64) launch_wave<EPI, 64>(p, s); else launch_wave<EPI, 128>(p, s); } while (0)
       if (res) NT_WV(NT_EPI_RESIDUAL);

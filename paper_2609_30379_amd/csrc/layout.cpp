@@ -116,20 +116,16 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L) {
     L->blk_prow[b] = (int32_t)eta;
   }
 
-  // broadcast sources of the projections: for every 16-cell tile, the pair
-  // row and column of its first cell and that sample's N_i and first single
-  // row (a lane finds its own cell from there, see linear_wave_kernel)
+  // broadcast sources of the projections: the rows are walked as tiles of
+  // 16 cells of one pair row (ceil(N_i / 16) per pair row, the last one
+  // masked); bc_cu_tiles[i] counts the tiles of the samples before i
   {
-    const int64_t nt16 = (sn2 + 15) / 16;
-    L->bc_tiles.assign(nt16 * 4, 0);
-    for (int64_t t = 0, eta = 0; t < nt16; ++t) {
-      const int64_t m = t * 16;
-      while (eta + 1 < sn && L->row_splits2[eta + 1] <= m) ++eta;
-      const int32_t i = L->row_sample[eta];
-      L->bc_tiles[4 * t] = (int32_t)eta;
-      L->bc_tiles[4 * t + 1] = (int32_t)(m - L->row_splits2[eta]);
-      L->bc_tiles[4 * t + 2] = lengths[i];
-      L->bc_tiles[4 * t + 3] = L->cu_seqlens[i];
+    L->bc_cu_tiles.assign(batch + 1, 0);
+    int64_t t = 0;
+    for (int32_t i = 0; i < batch; ++i) {
+      t += (int64_t)lengths[i] * ((lengths[i] + 15) / 16);
+      if (t > INT32_MAX) return fail(NT_ERR_OVERFLOW, "broadcast tile count exceeds int32 at sample " + std::to_string(i));
+      L->bc_cu_tiles[i + 1] = (int32_t)t;
     }
   }
 

@@ -48,8 +48,7 @@ struct nt_layout {
   std::vector<int32_t> bias_tiles;   // [B+1] prefix of ceil(N_i/16) * round_up(N_i,64)/16: bias image tiles
   std::vector<int32_t> sattn_work;   // 1-D attention: quads (sample, first 16-query tile, 0, tile count)
   std::vector<int32_t> blk_prow;     // [ceil(sum N^2 / kLinRows)] pair row holding cell kLinRows*b
-  std::vector<int32_t> bc_tiles;     // quads per 16-cell tile t: pair row eta of cell 16t, its column
-                                     // b = 16t - row_splits2[eta], N_i and cu_seqlens[i] of its sample
+  std::vector<int32_t> bc_cu_tiles;  // [B+1] prefix of N_i * ceil(N_i/16): broadcast tiles (16 cells of one pair row)
 
   bool has_device = false;
   int device = -1;
@@ -67,7 +66,7 @@ struct nt_layout {
   const int32_t* d_blk_prow = nullptr;
   const int32_t* d_bias_tiles = nullptr;
   const int32_t* d_sattn_work = nullptr;
-  const int32_t* d_bc_tiles = nullptr;
+  const int32_t* d_bc_cu_tiles = nullptr;
   // pair attention workspace (the bias image), allocated by the first call
   // that needs it and grown on demand; freed with the layout
   mutable void* d_attn_ws = nullptr;
