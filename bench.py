@@ -39,16 +39,16 @@ F32_PEAK_TFLOPS = 157.3        # fp32 vector
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 COUNTER_WORKLOAD = "pair_b8_n208_224_bf16"
 COUNTERS = {  # op: (kernel source, source hash, FETCH_SIZE KiB, WRITE_SIZE KiB)
-    "attention_row": ("k_attention.hip", "f426dccbd46dbcc7", 142573, 90997),
-    "transition": ("k_transition.hip", "e2f701d5925d7f6e", 53103, 90996),
-    "triangle_out": ("k_triangle.hip", "199724cf5276c94e", 304096, 91523),
-    "attn_proj": ("k_linear.hip", "33ddea92dec844b9", 46035, 276012),
-    "tri_proj": ("k_linear.hip", "33ddea92dec844b9", 45826, 197120),
-    "bcast_ln_linear": ("k_linear.hip", "33ddea92dec844b9", 2401, 90997),
-    "attn_out_residual": ("k_linear.hip", "33ddea92dec844b9", 91287, 90997),
-    "single_proj": ("k_linear.hip", "33ddea92dec844b9", 3366, 853),
+    "attention_row": ("k_attention.hip", "c7ed897a1dd532b7", 141456, 90997),
+    "transition": ("k_transition.hip", "e2f701d5925d7f6e", 53031, 90998),
+    "triangle_out": ("k_triangle.hip", "e32c93982e48a7b7", 229416, 96571),
+    "attn_proj": ("k_linear.hip", "4e89098be581aed2", 45996, 276033),
+    "tri_proj": ("k_linear.hip", "4e89098be581aed2", 45830, 197120),
+    "bcast_ln_linear": ("k_linear.hip", "4e89098be581aed2", 2218, 90996),
+    "attn_out_residual": ("k_linear.hip", "4e89098be581aed2", 91222, 90998),
+    "single_proj": ("k_linear.hip", "4e89098be581aed2", 3360, 853),
     "segment_mean": ("k_segment.hip", "c95eabc6d4c62896", 45570, 853),
-    "single_update": ("k_linear.hip", "33ddea92dec844b9", 3628, 1280),
+    "single_update": ("k_linear.hip", "4e89098be581aed2", 3624, 1280),
 }
 
 
