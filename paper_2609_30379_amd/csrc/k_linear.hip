@@ -1259,15 +1259,16 @@ __global__ void __launch_bounds__(kStreamThreads, 1) linear_tiled_kernel(LinArgs
   };
 
   const int srow = tid / TPR, spart = tid % TPR;
-  uint4 xr[NV];
-  auto load_x = [&](int t) {
+  // a tile row's input: padding cells load row 0 and are zeroed when staged
+  // (a load under a lane predicate would zero registers that may await an
+  // earlier load, and the compiler then waits for every load in flight)
+  auto load_x = [&](int t, uint4 (&xr)[NV], bool& valid) {
     const int m = cell_row(t, srow);
+    valid = m >= 0;
+    const int64_t mm = valid ? m : 0;
 #pragma unroll
-    for (int v = 0; v < NV; ++v)
-      xr[v] = m >= 0 ? *reinterpret_cast<const uint4*>(x + (int64_t)m * p.ldx + spart * EPT + v * 8)
-                     : make_uint4(0u, 0u, 0u, 0u);
+    for (int v = 0; v < NV; ++v) xr[v] = *reinterpret_cast<const uint4*>(x + mm * p.ldx + spart * EPT + v * 8);
   };
-  load_x(tile);
 
   bf16x8 wf[NTW][KT];
   float bv[NTW][4];
@@ -1286,13 +1287,26 @@ __global__ void __launch_bounds__(kStreamThreads, 1) linear_tiled_kernel(LinArgs
     }
   }
 
-  for (int it = 0; tile < p.ntiles; ++it) {
+  // Each step issues the next tile's loads before it stages the current
+  // one (two register sets): loads carried around a loop are treated by the
+  // compiler as just issued, so consuming them first would wait for
+  // everything in flight.  The barrier after staging waits for the LDS writes
+  // only (__syncthreads would also wait for the loads just issued).
+  uint4 xa[NV], xb[NV];
+  bool va, vb;
+  load_x(tile, xa, va);
+  auto step = [&](int it, uint4 (&cur)[NV], bool vcur, uint4 (&nxt)[NV], bool& vnxt) __attribute__((always_inline)) {
     const int next = tile + (int)gridDim.x;
+    load_x(next < p.ntiles ? next : tile, nxt, vnxt);   // unconditional: see above (unused past the end)
     bf16* xs = Xs[it & 1];
     {
       float v[EPT];
 #pragma unroll
-      for (int vv = 0; vv < NV; ++vv) XStage<bf16>::unpack(xr[vv], v + vv * 8);
+      for (int vv = 0; vv < NV; ++vv) XStage<bf16>::unpack(cur[vv], v + vv * 8);
+      if (!vcur) {
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) v[e] = 0.f;
+      }
       if (p.gamma) {                              // padding cells (zero rows) normalise to beta
         float s = 0.f;
 #pragma unroll
@@ -1320,8 +1334,8 @@ __global__ void __launch_bounds__(kStreamThreads, 1) linear_tiled_kernel(LinArgs
         *reinterpret_cast<bf16x8*>(&xs[srow * SKR + spart * EPT + e]) = o;
       }
     }
-    if (next < p.ntiles) load_x(next);
-    __syncthreads();
+    __builtin_amdgcn_s_waitcnt(0xC07F);          // lgkmcnt(0): this thread's LDS writes done
+    __builtin_amdgcn_s_barrier();
 
     // 8 subtiles (k-offsets); lane (r = l16, g) collects k-offsets 0..7 of
     // channels 4g..4g+3 of each owned column tile
@@ -1351,6 +1365,11 @@ __global__ void __launch_bounds__(kStreamThreads, 1) linear_tiled_kernel(LinArgs
           *reinterpret_cast<bf16x8*>(p.y_tail + (int64_t)c * p.ld_tail + (int64_t)tile * TR + 8 * l16) = hold[j][i];
       }
     tile = next;
+  };
+  for (int it = 0; tile < p.ntiles; it += 2) {
+    step(it, xa, va, xb, vb);
+    if (tile >= p.ntiles) break;
+    step(it + 1, xb, vb, xa, va);
   }
 }
 
