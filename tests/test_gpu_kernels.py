@@ -97,6 +97,9 @@ LIN_CASES = [
     # rows, K, N, ln, epilogue, x dtype, dtype, n_tail
     (1000, 128, 128, True, "none", "bf16", "bf16", 0),
     (777, 128, 388, True, "none", "bf16", "bf16", 4),
+    (500, 128, 176, True, "none", "bf16", "bf16", 48),      # tail of 3 column tiles: not the wave kernel
+    (333, 64, 512, True, "gelu", "bf16", "bf16", 0),        # wave kernel, four column groups
+    (95, 128, 128, True, "residual", "bf16", "bf16", 0),    # wave kernel, residual, last tile of 15 rows
     (300, 384, 256, False, "none", "bf16", "bf16", 0),
     (600, 768, 2304, True, "none", "bf16", "bf16", 0),
     (600, 768, 3072, True, "gelu", "bf16", "bf16", 0),
