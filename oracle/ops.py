@@ -127,6 +127,32 @@ def pair_row_attention(q, k, v, bias, lengths, heads, head_dim, axis=0, scale=No
     return layout.pack(outs, (H * d,))
 
 
+def single_attention_pair_bias(q, k, v, bias, lengths, heads, head_dim, scale=None):
+    """Attention over each sample's single rows with a bias read from its pair
+    state (the Pairformer's single attention with pair bias, which Sec. 4.3
+    cites for its pair application): for sample i, query t and key k,
+      o[t] = sum_k softmax_k(scale * q[t].k[k] + bias[cell(i,t,k)]) v[k],
+    with q, k, v, o token-major [sum N, H*d] and bias [sum N^2, H].  This is
+    the row-attention step with one row per sample, in the single index
+    space.  Parity: a reading of a cited method; pinned by zero queries, one
+    dominant bias entry, masked padded attention and brute force."""
+    H, d = int(heads), int(head_dim)
+    scale = 1.0 / np.sqrt(d) if scale is None else float(scale)
+    Qs, Ks, Vs = (_single_elements(t, lengths) for t in (q, k, v))
+    Bs = _pair_elements(bias, lengths)
+    outs = []
+    for Q, K, V, Bm in zip(Qs, Ks, Vs, Bs):
+        N = Q.shape[0]
+        Q, K, V = (t.reshape(N, H, d) for t in (Q, K, V))
+        O = np.zeros_like(Q)
+        for h in range(H):
+            if N:
+                s = scale * (Q[:, h, :] @ K[:, h, :].T) + Bm[:, :, h]
+                O[:, h, :] = softmax(s, axis=-1) @ V[:, h, :]
+        outs.append(O.reshape(N, H * d))
+    return layout.pack(outs, (H * d,))
+
+
 def attention_1d(q, k, v, lengths, heads, head_dim, scale=None):
     """Variable-length self-attention on packed token-major [T, H*d] buffers with
     cumulative lengths (Sec. 3.3 "Attention through packed blocks"): queries

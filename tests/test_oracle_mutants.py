@@ -41,6 +41,18 @@ def _mut_attention_no_scale(q, k, v, bias, lengths, heads, head_dim, axis=0, sca
     return _orig["pair_row_attention"](q, k, v, bias, lengths, heads, head_dim, axis, 1.0)
 
 
+def _mut_single_attention_bias_transposed(q, k, v, bias, lengths, heads, head_dim, scale=None):
+    bias = np.array(bias, np.float64)
+    for off, n in zip(layout.pair_offsets(lengths), lengths):
+        blk = bias[off:off + n * n].reshape(n, n, -1)
+        bias[off:off + n * n] = blk.transpose(1, 0, 2).reshape(n * n, -1)
+    return _orig["single_attention_pair_bias"](q, k, v, bias, lengths, heads, head_dim, scale)
+
+
+def _mut_single_attention_no_bias(q, k, v, bias, lengths, heads, head_dim, scale=None):
+    return _orig["single_attention_pair_bias"](q, k, v, np.zeros_like(np.asarray(bias, np.float64)), lengths, heads, head_dim, scale)
+
+
 def _mut_triangle_transposed(a, b, lengths, direction="outgoing"):
     return _orig["triangle_mul"](b, a, lengths, direction)
 
@@ -65,7 +77,8 @@ def _mut_pair_offsets(lengths):
     return layout.offsets([int(n) * int(n) + (1 if i == 0 else 0) for i, n in enumerate(lengths)])
 
 
-_orig = {k: getattr(ops, k) for k in ("pair_broadcast", "pair_row_attention", "triangle_mul", "segment_reduce")}
+_orig = {k: getattr(ops, k) for k in ("pair_broadcast", "pair_row_attention", "triangle_mul", "segment_reduce",
+                                        "single_attention_pair_bias")}
 
 MUTANTS = [
     ("broadcast_swapped", ops, "pair_broadcast", _mut_broadcast_swapped,
@@ -76,6 +89,10 @@ MUTANTS = [
      [(T_ops.test_attention_brute_force, ()), (T_ops.test_attention_dominant_bias_selects_value, ())]),
     ("attention_no_scale", ops, "pair_row_attention", _mut_attention_no_scale,
      [(T_ops.test_attention_brute_force, ())]),
+    ("single_attention_bias_transposed", ops, "single_attention_pair_bias", _mut_single_attention_bias_transposed,
+     [(T_ops.test_single_attention_brute_force, ()), (T_ops.test_single_attention_dominant_bias_selects_value, ())]),
+    ("single_attention_no_bias", ops, "single_attention_pair_bias", _mut_single_attention_no_bias,
+     [(T_ops.test_single_attention_brute_force, ())]),
     ("triangle_operands_swapped", ops, "triangle_mul", _mut_triangle_transposed,
      [(T_ops.test_triangle_masked_padded_and_brute_force, ())]),
     ("triangle_direction", ops, "triangle_mul", _mut_triangle_direction,

@@ -289,6 +289,69 @@ def test_attention_1d_matches_masked_padded_sdpa(torch_cpu):
     np.testing.assert_allclose(o, np.concatenate([ref[i, :n] for i, n in enumerate(L)]), rtol=1e-12, atol=1e-12)
 
 
+# ------------------------------------------------- single attention, pair bias
+def _single_attn_inputs(L, H, d):
+    T, R = sum(L), sum(n * n for n in L)
+    return _rand(T, H * d), _rand(T, H * d), _rand(T, H * d), _rand(R, H)
+
+
+def test_single_attention_zero_queries_average_values():
+    L, H, d = [3, 0, 5], 2, 4
+    q, k, v, _ = _single_attn_inputs(L, H, d)
+    o = ops.single_attention_pair_bias(np.zeros_like(q), k, v, np.zeros((sum(n * n for n in L), H)), L, H, d)
+    for s, e in zip(layout.single_offsets(L)[:-1], layout.single_offsets(L)[1:]):
+        if e > s:
+            np.testing.assert_allclose(o[s:e], np.repeat(v[s:e].mean(0, keepdims=True), e - s, axis=0), rtol=1e-12, atol=1e-12)
+
+
+def test_single_attention_dominant_bias_selects_value():
+    L, H, d = [4, 2, 3], 2, 3
+    q, k, v, _ = _single_attn_inputs(L, H, d)
+    bias = np.zeros((sum(n * n for n in L), H))
+    pick = {}
+    for n, po, so in zip(L, layout.pair_offsets(L), layout.single_offsets(L)):
+        for t in range(n):
+            for h in range(H):
+                kk = (t + 1 + h) % n
+                bias[po + t * n + kk, h] = 1e4          # bias[t, kk] dominates query t
+                pick[(so, t, h)] = kk
+    o = ops.single_attention_pair_bias(q, k, v, bias, L, H, d)
+    for (so, t, h), kk in pick.items():
+        np.testing.assert_allclose(o[so + t, h * d:(h + 1) * d], v[so + kk, h * d:(h + 1) * d], rtol=1e-9, atol=1e-9)
+
+
+def test_single_attention_equals_masked_padded_sdpa(torch_cpu):
+    L, H, d = [5, 1, 3], 3, 4
+    q, k, v, b = _single_attn_inputs(L, H, d)
+    o = ops.single_attention_pair_bias(q, k, v, b, L, H, d)
+    B, N = len(L), max(L)
+    so = layout.single_offsets(L)
+    pad = lambda x: np.stack([np.pad(x[s:e], ((0, N - (e - s)), (0, 0))) for s, e in zip(so[:-1], so[1:])])  # noqa: E731
+    t = lambda x: torch.from_numpy(pad(x).reshape(B, N, H, d)).transpose(1, 2)  # noqa: E731
+    bp, _ = _pad_pairs(b, L)                                           # [B, N, N, H]
+    keymask = np.array([[kk < n for kk in range(N)] for n in L])
+    add = np.where(keymask[:, None, None, :], bp.transpose(0, 3, 1, 2), -np.inf)
+    add = np.where(keymask[:, None, :, None], add, 0.0)
+    ref = torch.nn.functional.scaled_dot_product_attention(t(q), t(k), t(v), attn_mask=torch.from_numpy(add))
+    ref = ref.transpose(1, 2).reshape(B, N, H * d).numpy()
+    np.testing.assert_allclose(o, np.concatenate([ref[i, :n] for i, n in enumerate(L)]), rtol=1e-11, atol=1e-11)
+
+
+def test_single_attention_brute_force():
+    L, H, d = [3, 2], 2, 2
+    q, k, v, b = _single_attn_inputs(L, H, d)
+    o = ops.single_attention_pair_bias(q, k, v, b, L, H, d, scale=0.7)
+    for n, po, so in zip(L, layout.pair_offsets(L), layout.single_offsets(L)):
+        for t in range(n):
+            for h in range(H):
+                sl = slice(h * d, (h + 1) * d)
+                logits = [0.7 * sum(q[so + t, sl] * k[so + kk, sl]) + b[po + t * n + kk, h] for kk in range(n)]
+                mx = max(logits)
+                w = [np.exp(x - mx) for x in logits]
+                acc = sum(w[kk] * v[so + kk, sl] for kk in range(n)) / sum(w)
+                np.testing.assert_allclose(o[so + t, sl], acc, rtol=1e-12, atol=1e-12)
+
+
 # ---------------------------------------------------------------- triangle
 def test_triangle_ones_gives_row_sums():
     L, C = [4, 2, 3], 3
