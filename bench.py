@@ -189,6 +189,62 @@ def cpu_baseline(w, run, min_s: float = 10.0):
                       f"({w.blocks} block(s)) each in float64 NumPy, {dt:.1f} s; host has {os.cpu_count()} CPUs"}
 
 
+def bench_single_attention(args, w):
+    """Single attention with pair bias (axis 3) alone, on the workload's
+    lengths with C_s / 32 heads of 32: q, k, v, o token-major, the bias from
+    the pair state.  value = query-key scores per second (H * sum N^2 / t)."""
+    import torch
+    from paper_2609_30379_amd import binding, synth
+    L = [int(n) for n in synth.lengths_for(w)]
+    H, d = w.c_s // 32, 32
+    T, R = sum(L), sum(n * n for n in L)
+    lay = binding.NestedLayout(L)
+    qkv = torch.from_numpy(synth.normal(w.seed, "single_attn_qkv", (T, 3 * H * d), dtype="bf16")).to("cuda", torch.bfloat16)
+    bias = torch.from_numpy(synth.normal(w.seed, "single_attn_bias", (H, R), dtype="bf16")).to("cuda", torch.bfloat16)
+    o = torch.empty((T, H * d), dtype=torch.bfloat16, device="cuda")
+    c = H * d
+    call = lambda: binding.nt_pair_row_attention(lay, 3, H, d, qkv[:, :c], qkv[:, c:2 * c], qkv[:, 2 * c:], o,  # noqa: E731
+                                                 bias=bias)
+    for _ in range(max(1, args.warmup)):
+        call()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        call()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    us = ev0.elapsed_time(ev1) * 1e3 / args.steps
+    nbytes = (4 * T * c + H * R) * 2
+    flops = 4 * H * d * R
+    line = {"metric": "query-key scores/sec, single attention with pair bias (1 MI355X)",
+            "value": round(H * R / (ms * 1e-3), 1), "unit": "scores/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": w.name + "_single_attention", "lengths": L, "heads": H, "head_dim": d},
+            "roofline": {"bound": "hbm", "achieved": round(nbytes / (us * 1e-6) / 1e9, 2), "peak": HBM_PEAK_GBS,
+                         "unit": "GB/s", "frac": round(nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                         "traffic": None, "algorithmic_bytes": nbytes, "us_per_launch": round(us, 2),
+                         "mfma_frac": round(flops / (us * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 4)}}
+    if not args.no_cpu_baseline:
+        # the oracle on the smallest sample, scaled to scores per second
+        from oracle import ops as oracle_ops
+        n = min(L)
+        q1 = qkv[:n].float().cpu().numpy()
+        b1 = bias[:, :n * n].float().cpu().numpy().T
+        t0, reps = time.perf_counter(), 0
+        while time.perf_counter() - t0 < 1.0:
+            oracle_ops.single_attention_pair_bias(q1[:, :c], q1[:, c:2 * c], q1[:, 2 * c:], b1, [n], H, d)
+            reps += 1
+        dt = (time.perf_counter() - t0) / reps
+        line["cpu_baseline"] = {"value": round(H * n * n / dt, 1), "unit": "scores/s", "cores": torch.get_num_threads(),
+                                "kind": "oracle", "sample": f"one sample of N={n}, {reps} runs"}
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -200,6 +256,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--graph", action="store_true", help="time replays of the step captured into a HIP graph")
     ap.add_argument("--kernels", action="store_true", help="also print the per-op breakdown to stderr")
+    ap.add_argument("--op", choices=["single_attention"], default=None,
+                    help="time one widened op alone instead of the pair block (its own JSON line)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device-to-device copy (scale reference for HBM counters)")
     args = ap.parse_args()
@@ -222,6 +280,9 @@ def main():
     binding.load()
     w = synth.WORKLOADS[args.workload]
     torch.cuda.set_device(0)
+    if args.op == "single_attention":
+        bench_single_attention(args, w)
+        return
     tokens = w.kind != "pair"
     run = blocks.TokenRun(w) if tokens else blocks.PairRun(w)
     L = run.lengths

@@ -248,12 +248,17 @@ nt_status nt_layernorm_linear(const nt_linear_args* args, void* stream);
  *           transpose (q, k, v and the bias read at cell(b,a) for (a,b)).
  *   axis 2  1-D variable-length self-attention over the tokens of each sample
  *           (Sec. 3.3 "Attention through packed blocks"); bias must be NULL.
+ *   axis 3  single attention with pair bias (the Pairformer's, cited in
+ *           Sec. 4.3): over the tokens of each sample, query t, key k,
+ *             o[t,h] = sum_k softmax_k(scale q[t,h].k[k,h] + bias[h][cell(t,k)]) v[k,h]
+ *           with q, k, v, o token-major (rows = sum N) and the bias read from
+ *           the pair state; bf16, d = 32, N_i <= 512 (else NT_ERR_UNSUPPORTED).
  * cell(a,b) = o_i + a N_i + b.  Pair attention follows the Pairformer's
  * triangle attention cited in Sec. 4.3 (reading: no gating, no mask).
  *   heads, head_dim  H and d; d in {8 (f32 only), 32, 64}; H*d <= ld_qkv.
  *   q, k, v  [rows, H*d] with common row stride ld_qkv (may be slices of one
- *            buffer); rows = sum N^2 (axes 0/1) or sum N (axis 2).
- *   bias     head-major [H][ld_bias] or NULL (axes 0/1).
+ *            buffer); rows = sum N^2 (axes 0/1) or sum N (axes 2/3).
+ *   bias     head-major [H][ld_bias] (ld_bias >= sum N^2) or NULL (axes 0/1/3).
  *   scale    softmax scale (e.g. 1/sqrt(d)).
  *   o        [rows, H*d] row stride ld_o.
  * Workspace: with a bias, bf16, d = 32 and every N_i <= 512 the call first

@@ -328,7 +328,10 @@ nt_status nt_pair_row_attention(const nt_layout* L, int32_t axis, int32_t H, int
                                 void* stream) {
   g_last_error.clear();
   if (nt_status st = need_device(L)) return st;
-  if (axis < 0 || axis > 2) return nt::fail(NT_ERR_INVALID_ARG, "axis must be 0, 1 or 2");
+  if (axis < 0 || axis > 3) return nt::fail(NT_ERR_INVALID_ARG, "axis must be 0, 1, 2 or 3");
+  if (axis == 3 && (dtype != NT_BF16 || D != 32 || L->max_len > nt::kAttnLongLen))
+    return nt::fail(NT_ERR_UNSUPPORTED, "single attention with pair bias supports bf16, head_dim 32, N_i <= " +
+                                            std::to_string(nt::kAttnLongLen));
   if (!valid_dtype(dtype)) return nt::fail(NT_ERR_INVALID_ARG, "bad dtype");
   if (H <= 0 || D <= 0) return nt::fail(NT_ERR_INVALID_ARG, "heads and head_dim must be > 0");
   if (dtype == NT_BF16 && D != 32 && D != 64) return nt::fail(NT_ERR_UNSUPPORTED, "bf16 attention supports head_dim 32 or 64");
@@ -339,8 +342,8 @@ nt_status nt_pair_row_attention(const nt_layout* L, int32_t axis, int32_t H, int
     return nt::fail(NT_ERR_INVALID_ARG, "row strides must hold H*head_dim and be multiples of the vector width");
   const int lim = dtype == NT_F32 ? 4096 : (D == 32 ? nt::kAttnMaxLenD32 : nt::kAttnMaxLenD64);
   if (L->max_len > lim) return nt::fail(NT_ERR_UNSUPPORTED, "a sample is longer than the attention limit " + std::to_string(lim));
-  const int64_t rows = axis == 2 ? L->sum_n : L->sum_n2;
-  if (bias && ld_bias < rows) return nt::fail(NT_ERR_INVALID_ARG, "ld_bias must be >= the pair row count");
+  const int64_t rows = axis >= 2 ? L->sum_n : L->sum_n2;
+  if (bias && ld_bias < L->sum_n2) return nt::fail(NT_ERR_INVALID_ARG, "ld_bias must be >= the pair row count");
   if (rows == 0) return NT_OK;
   if (!q || !k || !v || !o) return nt::fail(NT_ERR_INVALID_ARG, "q, k, v and o must be non-NULL");
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || (bias && (reinterpret_cast<uintptr_t>(bias) & 3u)))

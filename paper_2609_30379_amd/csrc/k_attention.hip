@@ -247,7 +247,7 @@ __global__ void __launch_bounds__(256) bias_image_kernel(BiasImgArgs p) {
   for (int e = 0; e < 4; ++e) {
     const int k = k0 + e;
     float b = j < n ? -INFINITY : 0.f;
-    if (j < n && k < n) b = (float)bh[p.axis == 0 ? (int64_t)j * n + k : (int64_t)k * n + j] * p.inv_scale;
+    if (j < n && k < n) b = (float)bh[p.axis != 1 ? (int64_t)j * n + k : (int64_t)k * n + j] * p.inv_scale;
     o[e] = (bf16)b;
   }
   *reinterpret_cast<bf16x4*>(&p.img[(int64_t)h * p.tiles * 64 + tile * 64 + lane]) = o;
@@ -407,7 +407,7 @@ __global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_k
     const int nn = p.cu_seqlens[i + 1] - p.cu_seqlens[i];
     const int r0 = w4.z * kAttnRG;
     row = p.cu_seqlens[i] + r0;
-    row_end = p.cu_seqlens[i] + min(nn, r0 + kAttnRG);
+    row_end = p.axis == 3 ? row + 1 : p.cu_seqlens[i] + min(nn, r0 + kAttnRG);   // axis 3: one row per sample
     nqt_w = w4.w;
   }
   const int j0 = qt0 * 16;
@@ -423,7 +423,7 @@ __global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_k
   // finite values whose probabilities are masked to zero.
   auto dma_kv = [&](int sn, int64_t scu, int r, bf16* Kb, bf16* Vr) {
     const int snpad = (sn + 63) & ~63;
-    const int64_t ssr = p.axis == 0 ? sn : 1, sst = p.axis == 0 ? 1 : sn;
+    const int64_t ssr = p.axis == 0 ? sn : (p.axis == 1 ? 1 : 0), sst = p.axis == 1 ? sn : 1;
 #pragma unroll
     for (int kt = wave; kt < KT16; kt += NW) {
       if (kt * 16 >= snpad) break;
@@ -443,7 +443,7 @@ __global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_k
   // pair offset scu (zero past N)
   auto load_q = [&](int sn, int64_t scu, int r) -> bf16x8 {
     if (jw >= sn) return bf16x8{};
-    const int64_t ssr = p.axis == 0 ? sn : 1, sst = p.axis == 0 ? 1 : sn;
+    const int64_t ssr = p.axis == 0 ? sn : (p.axis == 1 ? 1 : 0), sst = p.axis == 1 ? sn : 1;
     return *reinterpret_cast<const bf16x8*>(p.q + (scu + (int64_t)r * ssr + (int64_t)jw * sst) * p.ld_qkv + h * D + g * 8);
   };
   const VtLane vl = vt_lane(l16, g);
@@ -460,8 +460,8 @@ __global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_k
   auto set_sample = [&](int si, int sn, int64_t scu) {
     n = sn;
     cu = scu;
-    sr = p.axis == 0 ? n : 1;
-    st = p.axis == 0 ? 1 : n;
+    sr = p.axis == 0 ? n : (p.axis == 1 ? 1 : 0);
+    st = p.axis == 1 ? n : 1;
     wave_has_queries = wave < (PERSIST ? (n + 15) / 16 : nqt_w) && j0 + 16 * wave < n;
     qvalid = jw < n;
     const int kti = ((n + 63) & ~63) / 16;
@@ -471,7 +471,9 @@ __global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_k
 #pragma unroll
     for (int kt = 0; kt < KT16; ++kt) bias_r[kt] = img && kt < kti ? img[kt * 64] : make_uint2(0u, 0u);
   };
-  set_sample(i, __builtin_amdgcn_readfirstlane(p.cu_seqlens[i + 1] - p.cu_seqlens[i]), p.cu_pairs[i]);
+  // first cell of the sample: pair offset, or for axis 3 its first token
+  set_sample(i, __builtin_amdgcn_readfirstlane(p.cu_seqlens[i + 1] - p.cu_seqlens[i]),
+             p.axis == 3 ? p.cu_seqlens[i] : p.cu_pairs[i]);
   int r = __builtin_amdgcn_readfirstlane((int)(row - p.cu_seqlens[i]));
   bf16x8 qf = load_q(n, cu, r);
   dma_kv(n, cu, r, Kb0, Vb0);
@@ -497,7 +499,7 @@ __global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_k
       while (p.cu_seqlens[i2 + 1] <= row + 1) ++i2;
       r2 = 0;
       n2 = p.cu_seqlens[i2 + 1] - p.cu_seqlens[i2];
-      cu2 = p.cu_pairs[i2];
+      cu2 = p.axis == 3 ? p.cu_seqlens[i2] : p.cu_pairs[i2];
     }
     i2 = __builtin_amdgcn_readfirstlane(i2);
     r2 = __builtin_amdgcn_readfirstlane(r2);
@@ -929,7 +931,15 @@ hipError_t launch_attention(const nt_layout& L, int axis, int H, int D, const vo
                    img, tiles * 64, L.d_bias_tiles, L.batch, L.sum_n};
     const size_t smem = sizeof(bf16) * 4 * (size_t)nmax * 32;
     const dim3 grid((unsigned)(L.pattn_items() * H));
-    if (nmax == kAttnShortLen) {
+    if (axis == 3) {
+      // single attention with pair bias: one row per sample, the 8-wave
+      // instance over the 1-D attention's (sample, 128-query block) items
+      if (L.sattn_items() == 0) return hipSuccess;
+      a.work = L.d_sattn_work;
+      const size_t smem3 = sizeof(bf16) * 4 * (size_t)kAttnLongLen * 32;
+      hipFuncSetAttribute((const void*)attention_pair_kernel<kAttnLongLen, 8, false>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem3);
+      attention_pair_kernel<kAttnLongLen, 8, false><<<dim3((unsigned)(L.sattn_items() * H)), dim3(512), smem3, s>>>(a);
+    } else if (nmax == kAttnShortLen) {
       // persistent: one workgroup of 16 waves per CU (all queries of a row);
       // per XCD a multiple of H workgroups, at least H, so every head gets an
       // equal share of each XCD's rows

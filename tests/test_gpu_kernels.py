@@ -264,6 +264,31 @@ def test_pair_attention(B, axis, dtype, H, D, lset):
     check(first, ref, dtype, f"pair attention axis {axis} {dtype}")
 
 
+@pytest.mark.parametrize("H,lset", [(4, "att"), (12, "att"), (12, "mid512"), (4, "one")])
+def test_single_attention_pair_bias(B, H, lset):
+    """Axis 3: attention over each sample's tokens with the bias read from the
+    pair state (bf16, d = 32), against the oracle; plus its argument errors."""
+    import torch
+    D = 32
+    L = {"att": ATT_LENGTHS, "mid512": [512, 257, 1, 100], "one": [1, 1, 2]}[lset]
+    lay = _layout(B, L)
+    T, R = sum(L), sum(n * n for n in L)
+    qkv = synth.snap_bf16(_n(41, "qkv1", (T, 3 * H * D), 1.0, "bf16"))
+    bias = _n(42, "bias1", (R, H), 1.0, "bf16")
+    c = H * D
+    qd = dev(qkv, "bf16")
+    o = torch.full((T, c), float("nan"), dtype=torch.bfloat16, device="cuda")
+    B.nt_pair_row_attention(lay, 3, H, D, qd[:, :c], qd[:, c:2 * c], qd[:, 2 * c:], o, bias=dev(_head_major(bias), "bf16"))
+    ref = O.single_attention_pair_bias(qkv[:, :c], qkv[:, c:2 * c], qkv[:, 2 * c:], bias, L, H, D)
+    check(host(o), ref, "bf16", f"single attention with pair bias H={H} {lset}")
+    with pytest.raises(B.NtError):              # f32 is not supported on axis 3
+        of = torch.zeros((T, c), dtype=torch.float32, device="cuda")
+        qf = torch.zeros((T, 3 * c), dtype=torch.float32, device="cuda")
+        B.nt_pair_row_attention(lay, 3, H, D, qf[:, :c], qf[:, c:2 * c], qf[:, 2 * c:], of)
+    with pytest.raises(B.NtError):
+        B.nt_pair_row_attention(lay, 4, H, D, qd[:, :c], qd[:, c:2 * c], qd[:, 2 * c:], o)
+
+
 @pytest.mark.parametrize("dtype,H,D,L", [("bf16", 3, 64, [1, 5, 64, 65, 130, 512, 0, 200]),
                                          ("bf16", 2, 64, [256, 17, 1, 100, 33, 0]),
                                          ("bf16", 2, 32, [33, 1, 97]),
