@@ -39,13 +39,13 @@ F32_PEAK_TFLOPS = 157.3        # fp32 vector
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 COUNTER_WORKLOAD = "pair_b8_n208_224_bf16"
 COUNTERS = {  # op: (kernel source, source hash, FETCH_SIZE KiB, WRITE_SIZE KiB)
-    "attention_row": ("k_attention.hip", "c7ed897a1dd532b7", 141456, 90997),
-    "transition": ("k_transition.hip", "e2f701d5925d7f6e", 53100, 91002),
-    "triangle_out": ("k_triangle.hip", "e32c93982e48a7b7", 235849, 93926),
-    "attn_proj": ("k_linear.hip", "d85e0184919ac8cf", 46004, 276031),
-    "tri_proj": ("k_linear.hip", "d85e0184919ac8cf", 46215, 197120),
-    "bcast_ln_linear": ("k_linear.hip", "d85e0184919ac8cf", 2218, 90997),
-    "attn_out_residual": ("k_linear.hip", "d85e0184919ac8cf", 91221, 91002),
+    "attention_row": ("k_attention.hip", "edb107d47362cde5", 141466, 90996),
+    "transition": ("k_transition.hip", "e2f701d5925d7f6e", 53091, 91003),
+    "triangle_out": ("k_triangle.hip", "e32c93982e48a7b7", 231648, 94069),
+    "attn_proj": ("k_linear.hip", "d85e0184919ac8cf", 46004, 276032),
+    "tri_proj": ("k_linear.hip", "d85e0184919ac8cf", 46263, 197120),
+    "bcast_ln_linear": ("k_linear.hip", "d85e0184919ac8cf", 2218, 90996),
+    "attn_out_residual": ("k_linear.hip", "d85e0184919ac8cf", 91221, 91004),
     "single_proj": ("k_linear.hip", "d85e0184919ac8cf", 3360, 853),
     "segment_mean": ("k_segment.hip", "c95eabc6d4c62896", 45570, 853),
     "single_update": ("k_linear.hip", "d85e0184919ac8cf", 3624, 1280),
