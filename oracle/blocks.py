@@ -6,6 +6,11 @@ projection output and every pair/single state.  Those points are rounded here
 (numerics.store); all arithmetic between them is float64.  For the fp32
 workloads nothing is rounded.
 
+Each kernel-sized piece of a block is its own function (`ref_*`), returning
+its output unrounded; the block composes them and rounds every output that a
+later piece consumes.  The per-kernel parity tests call the same functions on
+the GPU's own stored inputs.
+
 TEST INFRASTRUCTURE ONLY (see the package docstring).
 """
 from __future__ import annotations
@@ -21,13 +26,69 @@ def _ln_linear(x, w, b, ln, st):
     return linear(st(layernorm(x, *ln)), w, b)
 
 
-def _swiglu(x, p, st):
-    """x + SwiGLU(LN(x)) with bf16 storage of LN(x) and of the gated hidden
-    (Eq. running-block, second line)."""
-    gu = _ln_linear(x, p["trans.w"], p["trans.b"], (p["trans.ln_g"], p["trans.ln_b"]), st)
+def _ln(p, key):
+    return (p[key + ".ln_g"], p[key + ".ln_b"])
+
+
+# ------------------------------------------------------------ kernel pieces
+# Every function takes stored (already rounded) inputs and returns its output
+# unrounded; `st` is the storage rounding of values inside the piece (the
+# normalised features, the gated SwiGLU hidden).
+
+def ref_single_proj(s, p):
+    """[u|v] = s W_uv^T + b_uv (Eq. running-block, first line: u_theta, v_theta)."""
+    return linear(s, p["uv.w"], p["uv.b"])
+
+
+def ref_broadcast(uv, C, lengths, z=None):
+    """z (+)= u_a + v_b over every sample's pair cells (Eq. running-block, first line)."""
+    return ops.pair_broadcast(uv[:, :C], uv[:, C:], lengths, z_in=z)
+
+
+def ref_ln_linear(z, p, key, st):
+    """LN(z) W^T + b with LN(z) stored (Sec. 3.3)."""
+    return _ln_linear(z, p[key + ".w"], p[key + ".b"], _ln(p, key), st)
+
+
+def ref_bcast_ln_linear(uv, C, lengths, p, key, st):
+    """The broadcast, stored, then LN+Linear (the pair construction followed
+    by the block's configuration step)."""
+    return ref_ln_linear(st(ref_broadcast(uv, C, lengths)), p, key, st)
+
+
+def ref_attention(qkv, beta, lengths, C, H, d, axis):
+    """Row (axis 0) or column (axis 1) attention with pair bias on stored q|k|v
+    ([R, 3C]) and bias ([R, H])."""
+    return ops.pair_row_attention(qkv[:, :C], qkv[:, C:2 * C], qkv[:, 2 * C:3 * C], beta, lengths, H, d, axis=axis)
+
+
+def ref_attn_out(o, z, p, key):
+    """z + o W_o^T + b_o."""
+    return z + linear(o, p[key + ".wo"], p[key + ".bo"])
+
+
+def ref_triangle(ab, z, C, lengths, direction):
+    """z + triangle(a, b), direction "outgoing" or "incoming"."""
+    return z + ops.triangle_mul(ab[:, :C], ab[:, C:], lengths, direction)
+
+
+def ref_transition(z, p, st):
+    """z + SwiGLU(LN(z)) with LN(z) and the gated hidden stored (Eq.
+    running-block, second line)."""
+    gu = _ln_linear(z, p["trans.w"], p["trans.b"], _ln(p, "trans"), st)
     F = gu.shape[1] // 2
     h = st(silu(gu[:, :F]) * gu[:, F:])
-    return x + linear(h, p["trans.w2"], p["trans.b2"])
+    return z + linear(h, p["trans.w2"], p["trans.b2"])
+
+
+def ref_column_mean(z, lengths):
+    """(1/N_i) sum_b z[a, b] (Eq. running-block, third line; Eq. pair-reduction)."""
+    return ops.segment_reduce(z, lengths, "pair_cols", "mean")
+
+
+def ref_single_update(m, s, p, st):
+    """s + m W_s^T + b_s with the column mean m stored (g_theta)."""
+    return s + linear(st(m), p["single.w"], p["single.b"])
 
 
 PAIR_ORDER_BLOCK = ("bcast", "lin", "att_row", "tri_out", "trans", "single")
@@ -62,31 +123,26 @@ def pair_block(s, lengths, p, dims, order, z=None, dtype="bf16", round_last=True
         last = k == len(order) - 1
         st = keep if (round_last or not last) else (lambda t: np.asarray(t, np.float64))
         if step == "bcast":
-            uv = keep(linear(s, p["uv.w"], p["uv.b"]))
+            uv = keep(ref_single_proj(s, p))
             trace["uv"] = uv
-            z = st(ops.pair_broadcast(uv[:, :C], uv[:, C:], lengths, z_in=z))
+            z = st(ref_broadcast(uv, C, lengths, z))
         elif step == "lin":
-            z = st(_ln_linear(z, p["lin.w"], p["lin.b"], (p["lin.ln_g"], p["lin.ln_b"]), keep))
+            z = st(ref_ln_linear(z, p, "lin", keep))
         elif step in ("att_row", "att_col"):
-            key = step
-            proj = _ln_linear(z, p[key + ".w"], p[key + ".b"], (p[key + ".ln_g"], p[key + ".ln_b"]), keep)
-            q, kk, v = keep(proj[:, :C]), keep(proj[:, C:2 * C]), keep(proj[:, 2 * C:3 * C])
-            beta = keep(proj[:, 3 * C:3 * C + H])
-            o = keep(ops.pair_row_attention(q, kk, v, beta, lengths, H, d,
-                                            axis=0 if step == "att_row" else 1))
+            proj = keep(ref_ln_linear(z, p, step, keep))
+            qkv, beta = proj[:, :3 * C], proj[:, 3 * C:3 * C + H]
+            o = keep(ref_attention(qkv, beta, lengths, C, H, d, 0 if step == "att_row" else 1))
             trace[step + ".o"] = o
-            z = st(z + linear(o, p[key + ".wo"], p[key + ".bo"]))
+            z = st(ref_attn_out(o, z, p, step))
         elif step in ("tri_out", "tri_in"):
-            ab = keep(_ln_linear(z, p[step + ".w"], p[step + ".b"], (p[step + ".ln_g"], p[step + ".ln_b"]), keep))
-            t = ops.triangle_mul(ab[:, :C], ab[:, C:], lengths,
-                                 "outgoing" if step == "tri_out" else "incoming")
-            z = st(z + t)
+            ab = keep(ref_ln_linear(z, p, step, keep))
+            z = st(ref_triangle(ab, z, C, lengths, "outgoing" if step == "tri_out" else "incoming"))
         elif step == "trans":
-            z = st(_swiglu(z, p, keep))
+            z = st(ref_transition(z, p, keep))
         elif step == "single":
-            m = ops.segment_reduce(z, lengths, "pair_cols", "mean")
+            m = ref_column_mean(z, lengths)
             trace["col_mean"] = m
-            s = st(s + linear(keep(m), p["single.w"], p["single.b"]))
+            s = st(ref_single_update(m, s, p, keep))
         else:
             raise ValueError(f"unknown step {step!r}")
         trace[step] = z

@@ -132,14 +132,15 @@ def single_attention_pair_bias(q, k, v, bias, lengths, heads, head_dim, scale=No
     state (the Pairformer's single attention with pair bias, which Sec. 4.3
     cites for its pair application): for sample i, query t and key k,
       o[t] = sum_k softmax_k(scale * q[t].k[k] + bias[cell(i,t,k)]) v[k],
-    with q, k, v, o token-major [sum N, H*d] and bias [sum N^2, H].  This is
+    with q, k, v, o token-major [sum N, H*d] and bias [sum N^2, H] (None: no
+    bias, which is plain per-sample self-attention).  This is
     the row-attention step with one row per sample, in the single index
     space.  Parity: a reading of a cited method; pinned by zero queries, one
     dominant bias entry, masked padded attention and brute force."""
     H, d = int(heads), int(head_dim)
     scale = 1.0 / np.sqrt(d) if scale is None else float(scale)
     Qs, Ks, Vs = (_single_elements(t, lengths) for t in (q, k, v))
-    Bs = _pair_elements(bias, lengths)
+    Bs = _pair_elements(bias, lengths) if bias is not None else [None] * len(lengths)
     outs = []
     for Q, K, V, Bm in zip(Qs, Ks, Vs, Bs):
         N = Q.shape[0]
@@ -147,7 +148,9 @@ def single_attention_pair_bias(q, k, v, bias, lengths, heads, head_dim, scale=No
         O = np.zeros_like(Q)
         for h in range(H):
             if N:
-                s = scale * (Q[:, h, :] @ K[:, h, :].T) + Bm[:, :, h]
+                s = scale * (Q[:, h, :] @ K[:, h, :].T)
+                if Bm is not None:
+                    s = s + Bm[:, :, h]
                 O[:, h, :] = softmax(s, axis=-1) @ V[:, h, :]
         outs.append(O.reshape(N, H * d))
     return layout.pack(outs, (H * d,))
@@ -184,15 +187,19 @@ def triangle_mul(a, b, lengths, direction="outgoing"):
     Parity: reading; pinned by b = 1 (row sums), a = b (symmetry), incoming =
     outgoing of transposes, equal lengths = dense einsum and brute force."""
     As, Bs = _pair_elements(a, lengths), _pair_elements(b, lengths)
+    if direction not in ("outgoing", "incoming"):
+        raise ValueError(direction)
     outs = []
     for A, Bm in zip(As, Bs):
+        # one N x N matrix product per channel c: A_c B_c^T (outgoing) or
+        # A_c^T B_c (incoming), on channel-first copies of the planes
+        Ac = np.ascontiguousarray(np.moveaxis(A, 2, 0))
+        Bc = np.ascontiguousarray(np.moveaxis(Bm, 2, 0))
         if direction == "outgoing":
-            T = np.einsum("xkc,ykc->xyc", A, Bm)
-        elif direction == "incoming":
-            T = np.einsum("kxc,kyc->xyc", A, Bm)
+            Tc = Ac @ np.swapaxes(Bc, 1, 2)
         else:
-            raise ValueError(direction)
-        outs.append(T)
+            Tc = np.swapaxes(Ac, 1, 2) @ Bc
+        outs.append(np.moveaxis(Tc, 0, 2))
     C = _f64(a).shape[1]
     return layout.pack(outs, (C,))
 

@@ -337,6 +337,24 @@ def test_single_attention_equals_masked_padded_sdpa(torch_cpu):
     np.testing.assert_allclose(o, np.concatenate([ref[i, :n] for i, n in enumerate(L)]), rtol=1e-11, atol=1e-11)
 
 
+def test_single_attention_without_bias_is_masked_padded_sdpa(torch_cpu):
+    """bias=None: plain per-sample self-attention, i.e. padded SDPA with the
+    padded keys masked (no pair term)."""
+    L, H, d = [4, 1, 6, 0], 2, 3
+    q, k, v, _ = _single_attn_inputs(L, H, d)
+    o = ops.single_attention_pair_bias(q, k, v, None, L, H, d)
+    B, N = len(L), max(L)
+    so = layout.single_offsets(L)
+    pad = lambda x: np.stack([np.pad(x[s:e], ((0, N - (e - s)), (0, 0))) for s, e in zip(so[:-1], so[1:])])  # noqa: E731
+    t = lambda x: torch.from_numpy(pad(x).reshape(B, N, H, d)).transpose(1, 2)  # noqa: E731
+    keymask = np.array([[kk < n for kk in range(N)] for n in L])
+    add = np.where(keymask[:, None, None, :], 0.0, -np.inf)
+    add = np.where(keymask[:, None, :, None], add, 0.0)
+    ref = torch.nn.functional.scaled_dot_product_attention(t(q), t(k), t(v), attn_mask=torch.from_numpy(add))
+    ref = ref.transpose(1, 2).reshape(B, N, H * d).numpy()
+    np.testing.assert_allclose(o, np.concatenate([ref[i, :n] for i, n in enumerate(L)]), rtol=1e-11, atol=1e-11)
+
+
 def test_single_attention_brute_force():
     L, H, d = [3, 2], 2, 2
     q, k, v, b = _single_attn_inputs(L, H, d)
