@@ -203,8 +203,9 @@ def bench_single_attention(args, w):
     bias = torch.from_numpy(synth.normal(w.seed, "single_attn_bias", (H, R), dtype="bf16")).to("cuda", torch.bfloat16)
     o = torch.empty((T, H * d), dtype=torch.bfloat16, device="cuda")
     c = H * d
+    ws = binding.workspace_tensor(binding.attention_workspace_bytes(lay, 3, H, d, "bf16", True))
     call = lambda: binding.nt_pair_row_attention(lay, 3, H, d, qkv[:, :c], qkv[:, c:2 * c], qkv[:, 2 * c:], o,  # noqa: E731
-                                                 bias=bias)
+                                                 bias=bias, bias_layout="heads", workspace=ws)
     for _ in range(max(1, args.warmup)):
         call()
     torch.cuda.synchronize()

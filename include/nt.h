@@ -24,21 +24,28 @@
  *                N_i x N_i matrix are padding and never read as data.  Plain
  *                variant: cell (i,a,b) is element (r,k) = (a,b); transposed
  *                variant: (r,k) = (b,a)
- *   head-major pair bias: [H][sum_i N_i^2], head h of cell at h*ld + cell
+ *   pair bias    [sum_i N_i^2, H] with a row stride (cell-major, heads
+ *                last), or any other (cell stride, head stride) pair, e.g.
+ *                head-major [H][ld] = (1, ld)
  * Row strides ("ld_*") are in elements and let callers address column slices
  * of a wider buffer (e.g. u and v inside one [sum N, 2C] projection).
  *
  * Ownership: every value buffer is a device pointer owned by the caller; op
- * calls never allocate, free or retain them.  An nt_layout and its device
+ * calls never allocate, free or retain memory.  An nt_layout and its device
  * mirrors are owned by the library from nt_from_* until nt_layout_destroy;
  * the caller must not destroy a layout while work that uses it is queued.
- * Two ops allocate scratch of their own: nt_pair_row_attention keeps a
- * workspace in the layout and nt_layernorm_linear (large K with a LayerNorm,
- * and the SwiGLU transition) one per device (see there).
+ * Workspaces: an op that needs scratch device memory (a bias image, packed
+ * operands re-tiled, normalised rows, weights in consumption order) takes it
+ * as a caller-provided (workspace, workspace_bytes) pair whose minimum size
+ * the matching *_workspace query returns; 0 means the call needs none.  A
+ * call that needs a workspace and is given none, or too little, returns
+ * NT_ERR_INVALID_ARG without enqueuing anything.  The workspace is scratch for
+ * the duration of the call's device work: calls that share one must be
+ * stream-ordered.
  *
  * Streams: every op enqueues asynchronously on the caller's HIP stream
  * (NULL = the default stream) and returns without synchronising.  Only
- * nt_from_* copies host->device (stream-ordered).
+ * nt_from_* copies host->device (stream-ordered) and nt_layout_destroy frees.
  *
  * Errors: every call returns an nt_status; nothing aborts or throws across the
  * ABI.  All argument checks run on the host before any launch; on an error no
@@ -79,6 +86,13 @@ typedef enum {
 } nt_epilogue;
 
 typedef enum { NT_LEVEL_SINGLES = 0, NT_LEVEL_PAIRS = 1 } nt_level;
+
+/* Operand layout of the triangle update (nt_triangle_mul). */
+typedef enum {
+  NT_TRI_PACKED = 0,           /* a, b: packed pair tensors [sum N^2, C], row stride ld_ab */
+  NT_TRI_PAIR_TILED = 1,       /* a, b: pair-tiled channel-major planes, channel stride ld_ab */
+  NT_TRI_PAIR_TILED_T = 2      /* the transposed pair-tiled variant                        */
+} nt_tri_operands;
 
 /* Layout of the columns that nt_layernorm_linear routes to y_tail. */
 typedef enum {
@@ -219,24 +233,32 @@ typedef struct {
   int64_t ld_bcast_u;
   const void* bcast_v;
   int64_t ld_bcast_v;
+  /* Caller-provided scratch (see nt_layernorm_linear_workspace); NULL / 0
+   * when the call needs none.                                              */
+  void* workspace;
+  uint64_t workspace_bytes;
 } nt_linear_args;
 
-/* Workspace: two kinds of bf16 call use a per-device workspace owned by the
- * library: one with a LayerNorm, bf16 x, K >= 384 (K % 32 == 0, K <= 4096),
- * N % 8 == 0 and no tail first writes LN(x) (rounded to bf16, as the product
- * consumes it) there, R * K * 2 bytes; a SwiGLU transition with K in {64, 128}
- * and F <= 768 first copies its weights there in the order its kernel
- * consumes them, 3 * F * K * 2 bytes.  The workspace is allocated by the first
- * such call and regrown (after a device synchronisation) when a later call
- * needs more; it lives until the process ends.  Such calls on one device must
- * therefore be ordered (one stream, or synchronised), not concurrent.
- * Errors: NT_ERR_INVALID_ARG, NT_ERR_LAYOUT_MISMATCH (residual_layout differs
+/* Workspace (args->workspace, args->workspace_bytes): two kinds of bf16 call
+ * need one.  A call with a LayerNorm, bf16 x, K >= 384 (K % 32 == 0,
+ * K <= 4096), N % 8 == 0 and no tail first writes LN(x) there (rounded to
+ * bf16, as the product consumes it): R * K * 2 bytes.  A SwiGLU transition
+ * with K in {64, 128} and F <= 768 first copies its weights there in the
+ * order its kernel consumes them: 3 * F * K * 2 bytes.  Every other call needs
+ * none.  nt_layernorm_linear_workspace returns the size for a given argument
+ * set (it reads only sizes, dtypes and flags, never the pointers).
+ * Errors: NT_ERR_INVALID_ARG (also a missing or too small workspace),
+ * NT_ERR_LAYOUT_MISMATCH (residual_layout differs
  * from layout, or rows differ from the layout's count), NT_ERR_UNSUPPORTED
  * (bf16 SwiGLU unless x is bf16, K == N in {64, 128, 256} and F % 32 == 0;
  * f32 SwiGLU with K > 1024 or F > 4096; n_tail with SwiGLU; a pair-tiled
  * tail without a pair layout), NT_ERR_HIP (also when the workspace cannot be
  * allocated).  ln_gamma/ln_beta must be 16-byte aligned.                     */
 nt_status nt_layernorm_linear(const nt_linear_args* args, void* stream);
+
+/* Minimum workspace of nt_layernorm_linear(args) in bytes (0: none).
+ * Errors: NT_ERR_INVALID_ARG (NULL).                                        */
+nt_status nt_layernorm_linear_workspace(const nt_linear_args* args, uint64_t* bytes);
 
 /* ---------------------------------------------------------------- attention
  * Segmented softmax attention, one launch over the whole batch.
@@ -255,44 +277,68 @@ nt_status nt_layernorm_linear(const nt_linear_args* args, void* stream);
  *           the pair state; bf16, d = 32, N_i <= 512 (else NT_ERR_UNSUPPORTED).
  * cell(a,b) = o_i + a N_i + b.  Pair attention follows the Pairformer's
  * triangle attention cited in Sec. 4.3 (reading: no gating, no mask).
- *   heads, head_dim  H and d; d in {8 (f32 only), 32, 64}; H*d <= ld_qkv.
+ *   heads, head_dim  H and d; d in {8, 16 (f32 only), 32, 64}; H*d <= ld_qkv.
  *   q, k, v  [rows, H*d] with common row stride ld_qkv (may be slices of one
  *            buffer); rows = sum N^2 (axes 0/1) or sum N (axes 2/3).
- *   bias     head-major [H][ld_bias] (ld_bias >= sum N^2) or NULL (axes 0/1/3).
+ *   bias     NULL (axes 0/1/3), or the pair bias: head h of cell c at
+ *            bias[c * ld_bias + h * ld_bias_head], i.e. [sum N^2, H] with row
+ *            stride ld_bias (>= H) and ld_bias_head = 1; the head-major form
+ *            [H][ld] is ld_bias = 1, ld_bias_head = ld (>= sum N^2).  Strides
+ *            are positive and in elements.
  *   scale    softmax scale (e.g. 1/sqrt(d)).
  *   o        [rows, H*d] row stride ld_o.
  * Workspace: with a bias, bf16, d = 32 and every N_i <= 512 the call first
  * writes bias/scale (rounded to bf16) in the per-lane order of the attention
- * kernel into a workspace owned by the layout, H * T * 512 bytes with
- * T = sum_i ceil(N_i/16) * ceil(N_i/64) * 4.  The first such call allocates it
- * (hipMalloc; a later call with more heads regrows it), nt_layout_destroy
- * frees it.  Such calls on one layout must therefore be ordered (one stream,
- * or synchronised), not concurrent.
- * Errors: NT_ERR_INVALID_ARG, NT_ERR_UNSUPPORTED (d, or N_i beyond the
- * on-chip limit: 1024 for d=32, 512 for d=64), NT_ERR_HIP (also when the
- * workspace cannot be allocated).                                            */
+ * kernel into the workspace: H * T * 512 bytes with
+ * T = sum_i ceil(N_i/16) * ceil(N_i/64) * 4 (nt_pair_row_attention_workspace).
+ * Errors: NT_ERR_INVALID_ARG (also a missing or too small workspace),
+ * NT_ERR_UNSUPPORTED (d, or N_i beyond the on-chip limit: 1024 for d=32,
+ * 512 for d=64), NT_ERR_HIP.                                                 */
 nt_status nt_pair_row_attention(const nt_layout* layout, int32_t axis,
                                 int32_t heads, int32_t head_dim,
                                 const void* q, const void* k, const void* v, int64_t ld_qkv,
-                                const void* bias, int64_t ld_bias, float scale,
-                                void* o, int64_t ld_o, nt_dtype dtype, void* stream);
+                                const void* bias, int64_t ld_bias, int64_t ld_bias_head, float scale,
+                                void* o, int64_t ld_o, nt_dtype dtype,
+                                void* workspace, uint64_t workspace_bytes, void* stream);
+
+/* Minimum workspace of nt_pair_row_attention for these arguments, in bytes
+ * (0: none); has_bias is 0 or 1.
+ * Errors: NT_ERR_INVALID_ARG.                                               */
+nt_status nt_pair_row_attention_workspace(const nt_layout* layout, int32_t axis, int32_t heads,
+                                          int32_t head_dim, nt_dtype dtype, int32_t has_bias,
+                                          uint64_t* bytes);
 
 /* ---------------------------------------------------------------- triangle
  * Triangle multiplicative update, channelwise (Sec. 4.3, after the AlphaFold 3
  * Pairformer; reading: no gates, no output projection), accumulated into z:
- *   direction 0 (outgoing)  z[cell(x,y),c] += sum_k a_c[x,k] b_c[y,k]
- *   direction 1 (incoming)  z[cell(x,y),c] += sum_k a_c[k,x] b_c[k,y]
- * a, b are pair-tiled channel-major with channel stride ld_ab (>= sum_pad):
- * for direction 0 in the plain variant (a_c[x,k] is plane element (x,k)),
- * for direction 1 in the transposed variant (a_c[k,x] is plane element (x,k)),
- * which is what nt_layernorm_linear writes with NT_TAIL_PAIR_TILED(_T); the
- * incoming update is then the outgoing contraction of the transposes.  z is the
- * channel-last pair state [sum N^2, C] with row stride ld_z.  One ragged grouped
- * GEMM over all samples and channels; fp32 accumulation, z rounded once.
- * Errors: NT_ERR_INVALID_ARG (C not a multiple of 32 for bf16).              */
+ *   direction 0 (outgoing)  z[cell(x,y),c] += sum_k a[cell(x,k),c] b[cell(y,k),c]
+ *   direction 1 (incoming)  z[cell(x,y),c] += sum_k a[cell(k,x),c] b[cell(k,y),c]
+ * One ragged grouped GEMM over all samples and channels (per sample and
+ * channel an N_i x N_i x N_i product); fp32 accumulation, z rounded once.
+ *   operands  NT_TRI_PACKED: a, b are packed pair tensors [sum N^2, C] (the
+ *             paper's layout, Eq. packing) with row stride ld_ab (>= C); the
+ *             call re-tiles them into the workspace, 2 * C * round_up(sum_pad,
+ *             8) elements (nt_triangle_mul_workspace), in the variant the
+ *             direction needs.
+ *             NT_TRI_PAIR_TILED / NT_TRI_PAIR_TILED_T: a, b are already
+ *             pair-tiled channel-major planes with channel stride ld_ab
+ *             (>= sum_pad, multiple of 8), as nt_layernorm_linear writes them
+ *             with NT_TAIL_PAIR_TILED(_T); the plain variant serves direction
+ *             0 and the transposed one direction 1 (the incoming update is the
+ *             outgoing contraction of the transposes); a variant that does
+ *             not match the direction is rejected.  No workspace.
+ *   z         channel-last pair state [sum N^2, C] with row stride ld_z.
+ * Errors: NT_ERR_INVALID_ARG (C not a multiple of 32 for bf16 or of 4 for f32,
+ * operand variant and direction disagree, missing or too small workspace).   */
 nt_status nt_triangle_mul(const nt_layout* layout, int32_t direction, int32_t C,
-                          const void* a, const void* b, int64_t ld_ab,
-                          void* z, int64_t ld_z, nt_dtype dtype, void* stream);
+                          const void* a, const void* b, int64_t ld_ab, nt_tri_operands operands,
+                          void* z, int64_t ld_z, nt_dtype dtype,
+                          void* workspace, uint64_t workspace_bytes, void* stream);
+
+/* Minimum workspace of nt_triangle_mul in bytes (0: none).
+ * Errors: NT_ERR_INVALID_ARG.                                               */
+nt_status nt_triangle_mul_workspace(const nt_layout* layout, int32_t C, nt_tri_operands operands,
+                                    nt_dtype dtype, uint64_t* bytes);
 
 /* ---------------------------------------------------------------- reduce
  * Reductions that consume a ragged axis, with fp32 accumulation and fp32

@@ -21,6 +21,7 @@ NT_F32, NT_BF16 = 0, 1
 EPILOGUES = {"none": 0, "residual": 1, "swiglu_residual": 2, "gelu": 3}
 LEVELS = {"singles": 0, "pairs": 1}
 TAILS = {"channel_major": 0, "pair_tiled": 1, "pair_tiled_t": 2}
+TRI_OPERANDS = {"packed": 0, "pair_tiled": 1, "pair_tiled_t": 2}
 ARRAYS = {"lengths": 0, "cu_seqlens": 1, "cu_pairs": 2, "row_splits2": 3, "row_sample": 4,
           "attn_work": 5, "tri_work": 6, "seq_work": 7, "cu_pad": 8}
 NT_LAYOUT_HOST_ONLY = 1
@@ -48,7 +49,8 @@ class LinearArgs(C.Structure):
                 ("y", C.c_void_p), ("ldy", C.c_int64),
                 ("n_tail", C.c_int32), ("y_tail", C.c_void_p), ("ld_tail", C.c_int64), ("tail_layout", C.c_int),
                 ("layout", C.c_void_p), ("level", C.c_int), ("residual_layout", C.c_void_p),
-                ("bcast_u", C.c_void_p), ("ld_bcast_u", C.c_int64), ("bcast_v", C.c_void_p), ("ld_bcast_v", C.c_int64)]
+                ("bcast_u", C.c_void_p), ("ld_bcast_u", C.c_int64), ("bcast_v", C.c_void_p), ("ld_bcast_v", C.c_int64),
+                ("workspace", C.c_void_p), ("workspace_bytes", C.c_uint64)]
 
 
 _lib = None
@@ -62,7 +64,7 @@ def load(path: str = LIB_PATH):
     if not os.path.exists(path):
         raise ImportError(f"{path} is missing: build it with `python -m paper_2609_30379_amd.build`")
     lib = C.CDLL(path)
-    vp, i32, i64, f32 = C.c_void_p, C.c_int32, C.c_int64, C.c_float
+    vp, i32, i64, u64, f32 = C.c_void_p, C.c_int32, C.c_int64, C.c_uint64, C.c_float
     sig = {
         "nt_from_lengths": [vp, i32, C.c_uint32, vp, C.POINTER(vp)],
         "nt_from_offsets": [vp, i32, C.c_uint32, vp, C.POINTER(vp)],
@@ -72,8 +74,11 @@ def load(path: str = LIB_PATH):
         "nt_layouts_compatible": [vp, vp],
         "nt_pair_broadcast": [vp, i32, vp, i64, vp, i64, vp, i64, i32, C.c_int, vp],
         "nt_layernorm_linear": [C.POINTER(LinearArgs), vp],
-        "nt_pair_row_attention": [vp, i32, i32, i32, vp, vp, vp, i64, vp, i64, f32, vp, i64, C.c_int, vp],
-        "nt_triangle_mul": [vp, i32, i32, vp, vp, i64, vp, i64, C.c_int, vp],
+        "nt_layernorm_linear_workspace": [C.POINTER(LinearArgs), C.POINTER(u64)],
+        "nt_pair_row_attention": [vp, i32, i32, i32, vp, vp, vp, i64, vp, i64, i64, f32, vp, i64, C.c_int, vp, u64, vp],
+        "nt_pair_row_attention_workspace": [vp, i32, i32, i32, C.c_int, i32, C.POINTER(u64)],
+        "nt_triangle_mul": [vp, i32, i32, vp, vp, i64, C.c_int, vp, i64, C.c_int, vp, u64, vp],
+        "nt_triangle_mul_workspace": [vp, i32, C.c_int, C.c_int, C.POINTER(u64)],
         "nt_segment_reduce": [vp, C.c_int, i32, i32, vp, i64, C.c_int, vp, i64, vp],
         "nt_last_error": [],
         "nt_version": [],
@@ -118,6 +123,20 @@ def _mat(t, name):
 
 def _ptr(t):
     return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def workspace_tensor(nbytes: int, device="cuda"):
+    """A device buffer of at least nbytes (16-byte aligned) for an op's
+    workspace argument, or None when the op needs none."""
+    import torch
+    if nbytes <= 0:
+        return None
+    words = (int(nbytes) + 15) // 16 * 2          # whole 16-byte units, as 8-byte words (16-byte aligned)
+    return torch.empty((words,), dtype=torch.int64, device=device).view(torch.uint8)[:int(nbytes)]
+
+
+def _ws(ws):
+    return (C.c_void_p(ws.data_ptr()), int(ws.numel() * ws.element_size())) if ws is not None else (None, 0)
 
 
 class NestedLayout:
@@ -172,8 +191,9 @@ def nt_layernorm_linear(x, w, bias, y, ln=None, eps: float = 1e-5, epilogue: str
                         hidden: int = 0, residual=None, n_tail: int = 0, y_tail=None,
                         tail_layout: str = "channel_major", layout: NestedLayout | None = None,
                         level: str = "pairs", residual_layout: NestedLayout | None = None, c_out: int | None = None,
-                        bcast=None):
-    """bcast=(u, v) with x=None: the rows are the pair broadcast u[eta_i+a] + v[eta_i+b] over `layout`."""
+                        bcast=None, workspace=None):
+    """bcast=(u, v) with x=None: the rows are the pair broadcast u[eta_i+a] + v[eta_i+b] over `layout`.
+    workspace: a device buffer from workspace_tensor(), or None to allocate one of the queried size."""
     a = LinearArgs()
     if bcast is not None:
         if x is not None or layout is None:
@@ -202,30 +222,103 @@ def nt_layernorm_linear(x, w, bias, y, ln=None, eps: float = 1e-5, epilogue: str
     a.layout = layout.handle if layout is not None else None
     a.level = LEVELS[level]
     a.residual_layout = residual_layout.handle if residual_layout is not None else None
+    if workspace is None:
+        workspace = workspace_tensor(_linear_ws_bytes(a))
+    a.workspace, a.workspace_bytes = _ws(workspace)
     _check(load().nt_layernorm_linear(C.byref(a), _stream()))
     return y
 
 
+def _linear_ws_bytes(a) -> int:
+    n = C.c_uint64()
+    _check(load().nt_layernorm_linear_workspace(C.byref(a), C.byref(n)))
+    return int(n.value)
+
+
+def layernorm_linear_workspace_bytes(x_rows: int, c_in: int, c_out: int, dtype: str = "bf16", ln: bool = True,
+                                     epilogue: str = "none", hidden: int = 0, residual_is_x: bool = True,
+                                     n_tail: int = 0) -> int:
+    """Workspace bytes of an nt_layernorm_linear call with these sizes and flags
+    (row-major operands with their natural strides)."""
+    a = LinearArgs()
+    a.rows, a.c_in, a.c_out = int(x_rows), int(c_in), int(c_out)
+    a.dtype = a.x_dtype = NT_BF16 if dtype == "bf16" else NT_F32
+    a.ldx, a.ldy = int(c_in), int(c_out - n_tail)
+    a.ld_residual = int(c_out - n_tail)
+    a.ln_gamma = C.c_void_p(16) if ln else None
+    a.epilogue, a.hidden, a.n_tail = EPILOGUES[epilogue], int(hidden), int(n_tail)
+    if epilogue == "swiglu_residual" and not residual_is_x:
+        a.residual = C.c_void_p(32)
+    return _linear_ws_bytes(a)
+
+
+def attention_workspace_bytes(layout: NestedLayout, axis: int, heads: int, head_dim: int, dtype: str = "bf16",
+                              has_bias: bool = True) -> int:
+    n = C.c_uint64()
+    _check(load().nt_pair_row_attention_workspace(layout.handle, int(axis), int(heads), int(head_dim),
+                                                  NT_BF16 if dtype == "bf16" else NT_F32, int(bool(has_bias)),
+                                                  C.byref(n)))
+    return int(n.value)
+
+
 def nt_pair_row_attention(layout: NestedLayout, axis: int, heads: int, head_dim: int, q, k, v, o,
-                          bias=None, scale: float | None = None):
+                          bias=None, scale: float | None = None, bias_layout: str = "cells", workspace=None):
+    """bias: [sum N^2, H] with a row stride (bias_layout "cells"), or head-major
+    [H, >= sum N^2] (bias_layout "heads")."""
     pq, ld = _mat(q, "q")
     pk, ldk = _mat(k, "k")
     pv, ldv = _mat(v, "v")
     if not (ld == ldk == ldv):
         raise ValueError("q, k and v must share one row stride")
     po, ldo = _mat(o, "o")
-    pb, ldb = (_ptr(bias), int(bias.stride(0))) if bias is not None else (None, 0)
+    if bias is None:
+        pb, ldb, ldbh = None, 0, 0
+    elif bias_layout == "cells":
+        if bias.dim() != 2 or bias.stride(1) != 1:
+            raise ValueError("bias must be [sum N^2, H] with unit head stride")
+        pb, ldb, ldbh = _ptr(bias), int(bias.stride(0)), 1
+    elif bias_layout == "heads":
+        if bias.dim() != 2 or bias.stride(1) != 1:
+            raise ValueError("head-major bias must be [H, ld] with contiguous rows")
+        pb, ldb, ldbh = _ptr(bias), 1, int(bias.stride(0))
+    else:
+        raise ValueError(bias_layout)
     scale = 1.0 / float(np.sqrt(head_dim)) if scale is None else float(scale)
+    dt = _dtype(q)
+    if workspace is None:
+        workspace = workspace_tensor(attention_workspace_bytes(layout, axis, heads, head_dim,
+                                                               "bf16" if dt == NT_BF16 else "f32", bias is not None))
+    pw, nw = _ws(workspace)
     _check(load().nt_pair_row_attention(layout.handle, int(axis), int(heads), int(head_dim), pq, pk, pv, ld,
-                                        pb, ldb, scale, po, ldo, _dtype(q), _stream()))
+                                        pb, ldb, ldbh, scale, po, ldo, dt, pw, nw, _stream()))
     return o
 
 
-def nt_triangle_mul(layout: NestedLayout, direction: int, a, b, z):
-    """a, b: pair-tiled channel-major operands [C, >= sum_pad] (rows = channels)."""
+def triangle_workspace_bytes(layout: NestedLayout, C_: int, operands: str = "packed", dtype: str = "bf16") -> int:
+    n = C.c_uint64()
+    _check(load().nt_triangle_mul_workspace(layout.handle, int(C_), TRI_OPERANDS[operands],
+                                            NT_BF16 if dtype == "bf16" else NT_F32, C.byref(n)))
+    return int(n.value)
+
+
+def nt_triangle_mul(layout: NestedLayout, direction: int, a, b, z, operands: str = "packed", workspace=None):
+    """operands "packed": a, b are [sum N^2, C] pair tensors (row stride shared);
+    "pair_tiled" / "pair_tiled_t": pair-tiled channel-major planes [C, >= sum_pad]."""
     pz, ldz = _mat(z, "z")
-    _check(load().nt_triangle_mul(layout.handle, int(direction), int(z.size(1)), _ptr(a), _ptr(b),
-                                  int(a.stride(0)), pz, ldz, _dtype(z), _stream()))
+    Cz = int(z.size(1))
+    if operands == "packed":
+        pa, lda = _mat(a, "a")
+        pb, ldb = _mat(b, "b")
+        if lda != ldb:
+            raise ValueError("a and b must share one row stride")
+    else:
+        pa, lda = _ptr(a), int(a.stride(0))
+        pb = _ptr(b)
+    if workspace is None:
+        workspace = workspace_tensor(triangle_workspace_bytes(layout, Cz, operands, "bf16" if _dtype(z) == NT_BF16 else "f32"))
+    pw, nw = _ws(workspace)
+    _check(load().nt_triangle_mul(layout.handle, int(direction), Cz, pa, pb, lda, TRI_OPERANDS[operands], pz, ldz,
+                                  _dtype(z), pw, nw, _stream()))
     return z
 
 

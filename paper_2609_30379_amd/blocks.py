@@ -7,7 +7,8 @@ pair block      the single-pair-single block of Eq. running-block, extended with
 encoder layer   a pre-LayerNorm encoder layer on packed [sum N_i, C] tokens
                 with segmented attention and a per-sample mean pool.
 
-Workspaces are allocated once per (layout, dims); a step allocates nothing.
+Workspaces (activation buffers and the ops' scratch) are allocated once per
+(layout, dims); a step allocates nothing.
 """
 from __future__ import annotations
 
@@ -100,6 +101,12 @@ class PairWorkspace:
         self.o = torch.empty((R, c_z), dtype=td, device=device)
         self.ab = torch.empty((2 * c_z, max(_round8(layout.sum_pad), 8)), dtype=td, device=device)
         self.m = torch.empty((S, c_z), dtype=torch.float32, device=device)
+        # op scratch: the attention bias image (both axes) and the
+        # transition's weight image, used one op at a time on one stream
+        need = max(B.attention_workspace_bytes(layout, ax, heads, c_z // heads, dtype, True) for ax in (0, 1))
+        need = max(need, B.layernorm_linear_workspace_bytes(R, c_z, c_z, dtype, epilogue="swiglu_residual",
+                                                            hidden=4 * c_z))
+        self.scratch = B.workspace_tensor(need, device)
         self.cur = 0
 
 
@@ -110,10 +117,13 @@ def fuse_bcast(ws: PairWorkspace, C: int) -> bool:
     return fuse_broadcast and ws.td == torch.bfloat16 and C in (64, 128)
 
 
-def pair_block(layout: B.NestedLayout, s, W: dict, dims: dict, order, ws: PairWorkspace, z=None):
+def pair_block(layout: B.NestedLayout, s, W: dict, dims: dict, order, ws: PairWorkspace, z=None, tap=None):
     """Runs one pair block.  s ([sum N, C_s]) is updated in place by the
-    "single" step; returns the pair state tensor (a workspace buffer, or z)."""
+    "single" step; returns the pair state tensor (a workspace buffer, or z).
+    tap(op, **outputs), when given, is called after every op with the device
+    tensors that op wrote (the per-kernel parity tests read them)."""
     C, H, d = dims["c_z"], dims["heads"], dims["head_dim"]
+    tap = tap or (lambda op, **t: None)
     order = list(order)
     k = 0
     while k < len(order):
@@ -124,23 +134,28 @@ def pair_block(layout: B.NestedLayout, s, W: dict, dims: dict, order, ws: PairWo
             # pair tensor is never written (its rows are built as they are read)
             with _op("single_proj"):
                 B.nt_layernorm_linear(s, W["uv.w"], W["uv.b"], ws.uv, layout=layout, level="singles")
+            tap("single_proj", uv=ws.uv)
             z = ws.z[ws.cur]
             with _op("bcast_ln_linear"):
                 B.nt_layernorm_linear(None, W["lin.w"], W["lin.b"], z, ln=(W["lin.ln_g"], W["lin.ln_b"]),
                                       layout=layout, level="pairs", bcast=(ws.uv[:, :C], ws.uv[:, C:]))
+            tap("bcast_ln_linear", z=z)
             k += 1
         elif step == "bcast":
             with _op("single_proj"):
                 B.nt_layernorm_linear(s, W["uv.w"], W["uv.b"], ws.uv, layout=layout, level="singles")
+            tap("single_proj", uv=ws.uv)
             acc = z is not None
             z = ws.z[ws.cur] if z is None else z
             with _op("pair_broadcast"):
                 B.nt_pair_broadcast(layout, ws.uv[:, :C], ws.uv[:, C:], z, accumulate=acc)
+            tap("pair_broadcast", z=z)
         elif step == "lin":
             out = ws.z[1 - ws.cur] if z is ws.z[ws.cur] else ws.z[ws.cur]
             with _op("ln_linear"):
                 B.nt_layernorm_linear(z, W["lin.w"], W["lin.b"], out, ln=(W["lin.ln_g"], W["lin.ln_b"]),
                                       layout=layout, level="pairs")
+            tap("lin", z=out)
             if out is ws.z[1 - ws.cur]:
                 ws.cur = 1 - ws.cur
             z = out
@@ -149,31 +164,42 @@ def pair_block(layout: B.NestedLayout, s, W: dict, dims: dict, order, ws: PairWo
                 B.nt_layernorm_linear(z, W[step + ".w"], W[step + ".b"], ws.qkv,
                                       ln=(W[step + ".ln_g"], W[step + ".ln_b"]), n_tail=H, y_tail=ws.bias,
                                       tail_layout="channel_major", layout=layout, level="pairs")
+            tap(step + ".proj", qkv=ws.qkv, bias=ws.bias)
             with _op("attention_" + step[4:]):
                 B.nt_pair_row_attention(layout, 0 if step == "att_row" else 1, H, d, ws.qkv[:, :C],
-                                        ws.qkv[:, C:2 * C], ws.qkv[:, 2 * C:], ws.o, bias=ws.bias)
+                                        ws.qkv[:, C:2 * C], ws.qkv[:, 2 * C:], ws.o, bias=ws.bias, bias_layout="heads",
+                                        workspace=ws.scratch)
+            tap(step + ".attention", o=ws.o)
             with _op("attn_out_residual"):
                 B.nt_layernorm_linear(ws.o, W[step + ".wo"], W[step + ".bo"], z, epilogue="residual", residual=z,
                                       layout=layout, level="pairs", residual_layout=layout)
+            tap(step + ".out", z=z)
         elif step in ("tri_out", "tri_in"):
             with _op("tri_proj"):
                 B.nt_layernorm_linear(z, W[step + ".w"], W[step + ".b"], None,
                                       ln=(W[step + ".ln_g"], W[step + ".ln_b"]), n_tail=2 * C, y_tail=ws.ab,
                                       tail_layout="pair_tiled" if step == "tri_out" else "pair_tiled_t",
                                       layout=layout, level="pairs", c_out=2 * C)
+            tap(step + ".proj", ab=ws.ab)
             with _op("triangle_" + step[4:]):
-                B.nt_triangle_mul(layout, 0 if step == "tri_out" else 1, ws.ab[:C], ws.ab[C:], z)
+                B.nt_triangle_mul(layout, 0 if step == "tri_out" else 1, ws.ab[:C], ws.ab[C:], z,
+                                  operands="pair_tiled" if step == "tri_out" else "pair_tiled_t")
+            tap(step + ".triangle", z=z)
         elif step == "trans":
             with _op("transition"):
                 B.nt_layernorm_linear(z, W["trans.w"], W["trans.b"], z, ln=(W["trans.ln_g"], W["trans.ln_b"]),
                                       epilogue="swiglu_residual", w2=W["trans.w2"], bias2=W["trans.b2"],
-                                      hidden=W["trans.w2"].shape[1], layout=layout, level="pairs")
+                                      hidden=W["trans.w2"].shape[1], layout=layout, level="pairs",
+                                      workspace=ws.scratch)
+            tap("transition", z=z)
         elif step == "single":
             with _op("segment_mean"):
                 B.nt_segment_reduce(layout, "pairs", "mean", z, ws.m)
+            tap("segment_mean", m=ws.m)
             with _op("single_update"):
                 B.nt_layernorm_linear(ws.m, W["single.w"], W["single.b"], s, epilogue="residual", residual=s,
                                       layout=layout, level="singles", residual_layout=layout)
+            tap("single_update", s=s)
         else:
             raise ValueError(f"unknown step {step!r}")
     return z
@@ -187,6 +213,10 @@ class TokenWorkspace:
         self.o = torch.empty((T, c), dtype=td, device=device)
         self.h = torch.empty((T, hidden), dtype=td, device=device)
         self.pooled = torch.empty((layout.batch, c), dtype=torch.float32, device=device)
+        # op scratch: the LayerNorm rows of the large-K products
+        need = max(B.layernorm_linear_workspace_bytes(T, c, 3 * c, dtype, ln=True),
+                   B.layernorm_linear_workspace_bytes(T, c, hidden, dtype, ln=True, epilogue="gelu"))
+        self.scratch = B.workspace_tensor(need, device)
 
 
 def encoder_layer(layout: B.NestedLayout, x, W: dict, heads: int, head_dim: int, ws: TokenWorkspace):
@@ -194,7 +224,7 @@ def encoder_layer(layout: B.NestedLayout, x, W: dict, heads: int, head_dim: int,
     c = heads * head_dim
     with _op("qkv_proj"):
         B.nt_layernorm_linear(x, W["qkv.w"], W["qkv.b"], ws.qkv, ln=(W["ln1_g"], W["ln1_b"]),
-                              layout=layout, level="singles")
+                              layout=layout, level="singles", workspace=ws.scratch)
     with _op("attention_1d"):
         B.nt_pair_row_attention(layout, 2, heads, head_dim, ws.qkv[:, :c], ws.qkv[:, c:2 * c], ws.qkv[:, 2 * c:],
                                 ws.o, scale=1.0 / math.sqrt(head_dim))
@@ -203,7 +233,7 @@ def encoder_layer(layout: B.NestedLayout, x, W: dict, heads: int, head_dim: int,
                               level="singles")
     with _op("ffn_up_gelu"):
         B.nt_layernorm_linear(x, W["ffn1.w"], W["ffn1.b"], ws.h, ln=(W["ln2_g"], W["ln2_b"]), epilogue="gelu",
-                              layout=layout, level="singles")
+                              layout=layout, level="singles", workspace=ws.scratch)
     with _op("ffn_down_residual"):
         B.nt_layernorm_linear(ws.h, W["ffn2.w"], W["ffn2.b"], x, epilogue="residual", residual=x, layout=layout,
                               level="singles")
@@ -231,12 +261,14 @@ class PairRun:
         self.ws = PairWorkspace(self.layout, w.c_s, w.c_z, w.heads, w.dtype, device)
         self.z = None
 
-    def step(self):
+    def step(self, tap=None):
+        """One pass of all blocks; tap(block, op, **outputs) sees every op's outputs."""
         self.s.copy_(self.s0)
         z = None
         for b in range(self.w.blocks):
             steps = self.w.steps if b == 0 else tuple(t for t in self.w.steps if t != "lin")
-            z = pair_block(self.layout, self.s, self.W[b], self.dims, steps, self.ws, z=z)
+            btap = None if tap is None else (lambda op, _b=b, **t: tap(_b, op, **t))
+            z = pair_block(self.layout, self.s, self.W[b], self.dims, steps, self.ws, z=z, tap=btap)
         self.z = z
         return self.s, z
 

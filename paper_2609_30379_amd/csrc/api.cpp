@@ -1,6 +1,7 @@
 // C ABI entry points (include/nt.h): argument validation on the host, layout
-// lifetime, and dispatch to the kernel launchers.  No entry point throws,
-// aborts or synchronises the device.
+// lifetime, and dispatch to the kernel launchers.  No entry point throws or
+// aborts; op calls neither allocate nor synchronise (scratch memory is the
+// caller's workspace, sized by the *_workspace queries).
 #include <cstring>
 #include <mutex>
 #include <new>
@@ -26,6 +27,15 @@ nt_status check_hip(hipError_t e, const char* what) {
 nt_status need_device(const nt_layout* L) {
   if (!L) return nt::fail(NT_ERR_INVALID_ARG, "layout is NULL");
   if (!L->has_device) return nt::fail(NT_ERR_INVALID_ARG, "layout was built host-only; it has no device mirrors");
+  return NT_OK;
+}
+
+nt_status need_workspace(size_t need, const void* ws, uint64_t bytes, const char* query) {
+  if (need == 0) return NT_OK;
+  if (!ws || bytes < need)
+    return nt::fail(NT_ERR_INVALID_ARG, "this call needs a workspace of " + std::to_string(need) + " bytes (" +
+                                            query + "); given " + (ws ? std::to_string(bytes) : std::string("none")));
+  if (!aligned16(ws)) return nt::fail(NT_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
   return NT_OK;
 }
 
@@ -93,33 +103,6 @@ nt_status fail(nt_status s, const std::string& msg) {
   return s;
 }
 
-hipError_t device_workspace(size_t bytes, void** ptr) {
-  static std::mutex mu;
-  static void* buf[64] = {nullptr};
-  static size_t size[64] = {0};
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return e;
-  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
-  std::lock_guard<std::mutex> lock(mu);
-  if (size[dev] < bytes) {
-    if (buf[dev]) {
-      // work queued earlier may still read the old buffer
-      if ((e = hipDeviceSynchronize()) != hipSuccess) return e;
-      if ((e = hipFree(buf[dev])) != hipSuccess) return e;
-      buf[dev] = nullptr;
-      size[dev] = 0;
-    }
-    const size_t grown = bytes + bytes / 4;
-    if ((e = hipMalloc(&buf[dev], grown)) != hipSuccess) {
-      buf[dev] = nullptr;
-      return e;
-    }
-    size[dev] = grown;
-  }
-  *ptr = buf[dev];
-  return hipSuccess;
-}
 }  // namespace nt
 
 extern "C" {
@@ -154,9 +137,6 @@ nt_status nt_layout_destroy(nt_layout* L) {
   nt_status st = NT_OK;
   if (L->d_base) {
     if (hipFree(L->d_base) != hipSuccess) st = nt::fail(NT_ERR_HIP, "hipFree of layout mirrors failed");
-  }
-  if (L->d_attn_ws) {
-    if (hipFree(L->d_attn_ws) != hipSuccess) st = nt::fail(NT_ERR_HIP, "hipFree of the attention workspace failed");
   }
   delete L;
   return st;
@@ -318,16 +298,26 @@ nt_status nt_layernorm_linear(const nt_linear_args* a, void* stream) {
     if (a->tail_layout != NT_TAIL_CHANNEL_MAJOR && a->ld_tail % 8)
       return nt::fail(NT_ERR_INVALID_ARG, "pair-tiled tails need ld_tail % 8 == 0");
   }
+  if (nt_status st = need_workspace(nt::linear_workspace_bytes(*a), a->workspace, a->workspace_bytes,
+                                    "nt_layernorm_linear_workspace"))
+    return st;
   nt::LinearPlan p{a, a->tail_layout, a->layout};
   return check_hip(nt::launch_linear(p, static_cast<hipStream_t>(stream)), "nt_layernorm_linear launch");
 }
 
+nt_status nt_layernorm_linear_workspace(const nt_linear_args* a, uint64_t* bytes) {
+  g_last_error.clear();
+  if (!a || !bytes) return nt::fail(NT_ERR_INVALID_ARG, "NULL argument");
+  *bytes = a->rows > 0 ? (uint64_t)nt::linear_workspace_bytes(*a) : 0;
+  return NT_OK;
+}
+
 nt_status nt_pair_row_attention(const nt_layout* L, int32_t axis, int32_t H, int32_t D, const void* q,
                                 const void* k, const void* v, int64_t ld_qkv, const void* bias,
-                                int64_t ld_bias, float scale, void* o, int64_t ld_o, nt_dtype dtype,
-                                void* stream) {
+                                int64_t ld_bias, int64_t ld_bias_head, float scale, void* o, int64_t ld_o,
+                                nt_dtype dtype, void* workspace, uint64_t workspace_bytes, void* stream) {
   g_last_error.clear();
-  if (nt_status st = need_device(L)) return st;
+  if (!L) return nt::fail(NT_ERR_INVALID_ARG, "layout is NULL");
   if (axis < 0 || axis > 3) return nt::fail(NT_ERR_INVALID_ARG, "axis must be 0, 1, 2 or 3");
   if (axis == 3 && (dtype != NT_BF16 || D != 32 || L->max_len > nt::kAttnLongLen))
     return nt::fail(NT_ERR_UNSUPPORTED, "single attention with pair bias supports bf16, head_dim 32, N_i <= " +
@@ -343,33 +333,76 @@ nt_status nt_pair_row_attention(const nt_layout* L, int32_t axis, int32_t H, int
   const int lim = dtype == NT_F32 ? 4096 : (D == 32 ? nt::kAttnMaxLenD32 : nt::kAttnMaxLenD64);
   if (L->max_len > lim) return nt::fail(NT_ERR_UNSUPPORTED, "a sample is longer than the attention limit " + std::to_string(lim));
   const int64_t rows = axis >= 2 ? L->sum_n : L->sum_n2;
-  if (bias && ld_bias < L->sum_n2) return nt::fail(NT_ERR_INVALID_ARG, "ld_bias must be >= the pair row count");
+  if (bias && (ld_bias <= 0 || ld_bias_head <= 0)) return nt::fail(NT_ERR_INVALID_ARG, "bias strides must be positive");
+  if (nt_status st = need_workspace(nt::attention_workspace_bytes(*L, axis, H, D, dtype, bias != nullptr), workspace,
+                                    workspace_bytes, "nt_pair_row_attention_workspace"))
+    return st;
+  if (nt_status st = need_device(L)) return st;
   if (rows == 0) return NT_OK;
   if (!q || !k || !v || !o) return nt::fail(NT_ERR_INVALID_ARG, "q, k, v and o must be non-NULL");
-  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || (bias && (reinterpret_cast<uintptr_t>(bias) & 3u)))
-    return nt::fail(NT_ERR_INVALID_ARG, "q, k, v, o must be 16-byte aligned, bias 4-byte aligned");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) ||
+      (bias && (reinterpret_cast<uintptr_t>(bias) & (dtype == NT_BF16 ? 1u : 3u))))
+    return nt::fail(NT_ERR_INVALID_ARG, "q, k, v, o must be 16-byte aligned, bias element-aligned");
   if (!(scale == scale)) return nt::fail(NT_ERR_INVALID_ARG, "scale is NaN");
-  return check_hip(nt::launch_attention(*L, axis, H, D, q, k, v, ld_qkv, bias, ld_bias, scale, o, ld_o, dtype,
-                                        static_cast<hipStream_t>(stream)),
+  return check_hip(nt::launch_attention(*L, axis, H, D, q, k, v, ld_qkv, bias, ld_bias, ld_bias_head, scale, o, ld_o,
+                                        dtype, workspace, static_cast<hipStream_t>(stream)),
                    "nt_pair_row_attention launch");
 }
 
-nt_status nt_triangle_mul(const nt_layout* L, int32_t direction, int32_t C, const void* a, const void* b,
-                          int64_t ld_ab, void* z, int64_t ld_z, nt_dtype dtype, void* stream) {
+nt_status nt_pair_row_attention_workspace(const nt_layout* L, int32_t axis, int32_t H, int32_t D, nt_dtype dtype,
+                                          int32_t has_bias, uint64_t* bytes) {
   g_last_error.clear();
-  if (nt_status st = need_device(L)) return st;
+  if (!L || !bytes) return nt::fail(NT_ERR_INVALID_ARG, "NULL argument");
+  if (axis < 0 || axis > 3 || H <= 0 || D <= 0 || !valid_dtype(dtype) || (has_bias != 0 && has_bias != 1))
+    return nt::fail(NT_ERR_INVALID_ARG, "bad axis, heads, head_dim, dtype or has_bias");
+  *bytes = nt::attention_workspace_bytes(*L, axis, H, D, dtype, has_bias != 0);
+  return NT_OK;
+}
+
+nt_status nt_triangle_mul(const nt_layout* L, int32_t direction, int32_t C, const void* a, const void* b,
+                          int64_t ld_ab, nt_tri_operands operands, void* z, int64_t ld_z, nt_dtype dtype,
+                          void* workspace, uint64_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  if (!L) return nt::fail(NT_ERR_INVALID_ARG, "layout is NULL");
   if (direction != 0 && direction != 1) return nt::fail(NT_ERR_INVALID_ARG, "direction must be 0 or 1");
+  if (operands != NT_TRI_PACKED && operands != NT_TRI_PAIR_TILED && operands != NT_TRI_PAIR_TILED_T)
+    return nt::fail(NT_ERR_INVALID_ARG, "bad operand layout");
   if (!valid_dtype(dtype)) return nt::fail(NT_ERR_INVALID_ARG, "bad dtype");
   if (C <= 0) return nt::fail(NT_ERR_INVALID_ARG, "C must be > 0");
   if (dtype == NT_BF16 && C % 32) return nt::fail(NT_ERR_INVALID_ARG, "bf16 triangle needs C % 32 == 0");
   const int ve = vec_elems(dtype);
+  if (dtype == NT_F32 && C % ve) return nt::fail(NT_ERR_INVALID_ARG, "f32 triangle needs C % 4 == 0");
   if (ld_z < C || ld_z % ve) return nt::fail(NT_ERR_INVALID_ARG, "ld_z must be >= C and a multiple of the vector width");
-  if (ld_ab < L->sum_pad || ld_ab % 8) return nt::fail(NT_ERR_INVALID_ARG, "ld_ab must be >= sum_pad and a multiple of 8");
+  if (operands == NT_TRI_PACKED) {
+    if (ld_ab < C || ld_ab % ve) return nt::fail(NT_ERR_INVALID_ARG, "packed operands: ld_ab must be >= C and a multiple of the vector width");
+  } else {
+    if ((operands == NT_TRI_PAIR_TILED) != (direction == 0))
+      return nt::fail(NT_ERR_INVALID_ARG, direction == 0
+                                              ? "the outgoing update needs the plain pair-tiled variant (NT_TRI_PAIR_TILED)"
+                                              : "the incoming update needs the transposed pair-tiled variant (NT_TRI_PAIR_TILED_T)");
+    if (ld_ab < L->sum_pad || ld_ab % 8) return nt::fail(NT_ERR_INVALID_ARG, "pair-tiled operands: ld_ab must be >= sum_pad and a multiple of 8");
+  }
+  if (nt_status st = need_workspace(nt::triangle_workspace_bytes(*L, C, operands, dtype), workspace, workspace_bytes,
+                                    "nt_triangle_mul_workspace"))
+    return st;
+  if (nt_status st = need_device(L)) return st;
   if (L->sum_n2 == 0) return NT_OK;
   if (!a || !b || !z) return nt::fail(NT_ERR_INVALID_ARG, "a, b and z must be non-NULL");
   if (!aligned16(a) || !aligned16(b) || !aligned16(z)) return nt::fail(NT_ERR_INVALID_ARG, "pointers must be 16-byte aligned");
-  return check_hip(nt::launch_triangle(*L, C, a, b, ld_ab, z, ld_z, dtype, static_cast<hipStream_t>(stream)),
+  return check_hip(nt::launch_triangle(*L, direction, C, a, b, ld_ab, operands, z, ld_z, dtype, workspace,
+                                       static_cast<hipStream_t>(stream)),
                    "nt_triangle_mul launch");
+}
+
+nt_status nt_triangle_mul_workspace(const nt_layout* L, int32_t C, nt_tri_operands operands, nt_dtype dtype,
+                                    uint64_t* bytes) {
+  g_last_error.clear();
+  if (!L || !bytes) return nt::fail(NT_ERR_INVALID_ARG, "NULL argument");
+  if (C <= 0 || !valid_dtype(dtype) || (operands != NT_TRI_PACKED && operands != NT_TRI_PAIR_TILED &&
+                                       operands != NT_TRI_PAIR_TILED_T))
+    return nt::fail(NT_ERR_INVALID_ARG, "bad C, dtype or operand layout");
+  *bytes = nt::triangle_workspace_bytes(*L, C, operands, dtype);
+  return NT_OK;
 }
 
 }  // extern "C"

@@ -27,7 +27,7 @@ struct AttnArgs {
   const bf16* v;
   int64_t ld_qkv;
   const bf16* bias;
-  int64_t ld_bias;
+  int64_t ld_bias, ld_bias_head;  // element (cell c, head h) at c * ld_bias + h * ld_bias_head
   float scale_log2;      // softmax scale * log2(e)
   bf16* o;
   int64_t ld_o;
@@ -112,8 +112,9 @@ __global__ void __launch_bounds__(256) attention_mfma_kernel(AttnArgs p) {
 #pragma unroll
     for (int dt = 0; dt < D / 16; ++dt) O[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
     const bf16* brow = nullptr;                // bias row of this query (axis 0)
-    if (p.bias && qvalid) brow = p.bias + (int64_t)h * p.ld_bias + sg.cu + (p.axis == 0 ? (int64_t)qi * n : qi);
-    const int64_t bstep = p.axis == 0 ? 1 : n;
+    if (p.bias && qvalid)
+      brow = p.bias + (int64_t)h * p.ld_bias_head + (sg.cu + (p.axis == 0 ? (int64_t)qi * n : qi)) * p.ld_bias;
+    const int64_t bstep = (p.axis == 0 ? 1 : n) * p.ld_bias;
 
     for (int kc = 0; kc < npad; kc += 64) {
       f32x4 s[4];
@@ -191,7 +192,7 @@ struct PairAttnArgs {
   const bf16* v;
   int64_t ld_qkv;
   const bf16* bias;
-  int64_t ld_bias;
+  int64_t ld_bias, ld_bias_head;
   float scale_log2;
   bf16* o;
   int64_t ld_o;
@@ -213,12 +214,13 @@ struct PairAttnArgs {
 // bf16 -- exactly the register image the attention lanes keep.  Keys past N
 // hold -inf (for queries inside N), so the scores they seed are masked
 // without further work; queries past N hold 0.
-// bias(j, k) is bias[h][cell(j, k)] for axis 0 and bias[h][cell(k, j)] for
-// axis 1.  One wave per tile, the sample found by bisection.
+// bias(j, k) is the head-h bias of cell(j, k) for axis 0 and of cell(k, j)
+// for axis 1, read at cell * ld_bias + h * ld_bias_head.  One wave per tile,
+// the sample found by bisection.
 struct BiasImgArgs {
   int axis, batch;
   const bf16* bias;
-  int64_t ld_bias;
+  int64_t ld_bias, ld_bias_head;
   float inv_scale;
   uint2* img;
   int64_t tiles;          // tiles per head
@@ -241,13 +243,13 @@ __global__ void __launch_bounds__(256) bias_image_kernel(BiasImgArgs p) {
   const int kti = ((n + 63) >> 6) * 4;
   const int t = (int)(tile - p.bias_tiles[i]);
   const int j = (t / kti) * 16 + l16, k0 = (t % kti) * 16 + 4 * g;
-  const bf16* bh = p.bias + (int64_t)h * p.ld_bias + p.cu_pairs[i];
+  const bf16* bh = p.bias + (int64_t)h * p.ld_bias_head + (int64_t)p.cu_pairs[i] * p.ld_bias;
   bf16x4 o;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     const int k = k0 + e;
     float b = j < n ? -INFINITY : 0.f;
-    if (j < n && k < n) b = (float)bh[p.axis != 1 ? (int64_t)j * n + k : (int64_t)k * n + j] * p.inv_scale;
+    if (j < n && k < n) b = (float)bh[(p.axis != 1 ? (int64_t)j * n + k : (int64_t)k * n + j) * p.ld_bias] * p.inv_scale;
     o[e] = (bf16)b;
   }
   *reinterpret_cast<bf16x4*>(&p.img[(int64_t)h * p.tiles * 64 + tile * 64 + lane]) = o;
@@ -814,7 +816,7 @@ struct AttnF32Args {
   const float* v;
   int64_t ld_qkv;
   const float* bias;
-  int64_t ld_bias;
+  int64_t ld_bias, ld_bias_head;
   float scale;
   float* o;
   int64_t ld_o;
@@ -834,14 +836,15 @@ __global__ void __launch_bounds__(256) attention_f32_kernel(AttnF32Args p) {
     float qv[D];
 #pragma unroll
     for (int d = 0; d < D; ++d) qv[d] = p.q[qrow * p.ld_qkv + h * D + d];
-    const float* brow = p.bias ? p.bias + (int64_t)h * p.ld_bias + sg.cu + (p.axis == 0 ? (int64_t)qi * n : qi) : nullptr;
+    const float* brow = p.bias ? p.bias + (int64_t)h * p.ld_bias_head + (sg.cu + (p.axis == 0 ? (int64_t)qi * n : qi)) * p.ld_bias
+                               : nullptr;
     auto logit = [&](int key) {
       const int64_t krow = sg.base + (int64_t)key * sg.step;
       float s = 0.f;
 #pragma unroll
       for (int d = 0; d < D; ++d) s = fmaf(qv[d], p.k[krow * p.ld_qkv + h * D + d], s);
       s *= p.scale;
-      if (brow) s += brow[p.axis == 0 ? (int64_t)key : (int64_t)key * n];
+      if (brow) s += brow[(p.axis == 0 ? (int64_t)key : (int64_t)key * n) * p.ld_bias];
       return s;
     };
     float mx = -INFINITY;
@@ -863,16 +866,22 @@ __global__ void __launch_bounds__(256) attention_f32_kernel(AttnF32Args p) {
 
 }  // namespace
 
+size_t attention_workspace_bytes(const nt_layout& L, int axis, int H, int D, nt_dtype dtype, bool has_bias) {
+  // only the d = 32 pair kernel (N <= 512) reads the bias through an image
+  if (!has_bias || dtype != NT_BF16 || D != 32 || axis == 2 || L.max_len > kAttnLongLen) return 0;
+  return (size_t)H * (size_t)L.bias_tiles_total() * 512;
+}
+
 hipError_t launch_attention(const nt_layout& L, int axis, int H, int D, const void* q, const void* k,
-                            const void* v, int64_t ld_qkv, const void* bias, int64_t ld_bias, float scale,
-                            void* o, int64_t ld_o, nt_dtype dtype, hipStream_t s) {
+                            const void* v, int64_t ld_qkv, const void* bias, int64_t ld_bias, int64_t ld_bias_head,
+                            float scale, void* o, int64_t ld_o, nt_dtype dtype, void* workspace, hipStream_t s) {
   const int32_t* work = axis == 2 ? L.d_seq_work : L.d_attn_work;
   const int64_t items = axis == 2 ? L.seq_items() : L.attn_items();
   if (items == 0) return hipSuccess;
   const dim3 grid((unsigned)items, (unsigned)H), block(256);
   if (dtype == NT_F32) {
     AttnF32Args a{axis, H, (const float*)q, (const float*)k, (const float*)v, ld_qkv, (const float*)bias,
-                  ld_bias, scale, (float*)o, ld_o, work, L.d_cu_seqlens, L.d_cu_pairs};
+                  ld_bias, ld_bias_head, scale, (float*)o, ld_o, work, L.d_cu_seqlens, L.d_cu_pairs};
     switch (D) {
       case 8: attention_f32_kernel<8><<<grid, block, 0, s>>>(a); break;
       case 16: attention_f32_kernel<16><<<grid, block, 0, s>>>(a); break;
@@ -905,29 +914,14 @@ hipError_t launch_attention(const nt_layout& L, int axis, int H, int D, const vo
     const int64_t tiles = L.bias_tiles_total();
     const uint2* img = nullptr;
     if (bias && tiles > 0) {
-      // the layout's workspace holds the bias image (allocated on first use)
-      const size_t need = (size_t)H * (size_t)tiles * 512;
-      if (L.attn_ws_bytes < need) {
-        if (L.d_attn_ws) {
-          const hipError_t e = hipFree(L.d_attn_ws);
-          L.d_attn_ws = nullptr;
-          L.attn_ws_bytes = 0;
-          if (e != hipSuccess) return e;
-        }
-        const hipError_t e = hipMalloc(&L.d_attn_ws, need);
-        if (e != hipSuccess) {
-          L.d_attn_ws = nullptr;
-          return e;
-        }
-        L.attn_ws_bytes = need;
-      }
-      BiasImgArgs b{axis, L.batch, (const bf16*)bias, ld_bias, 1.f / scale, (uint2*)L.d_attn_ws, tiles,
+      // the caller's workspace receives the bias image
+      BiasImgArgs b{axis, L.batch, (const bf16*)bias, ld_bias, ld_bias_head, 1.f / scale, (uint2*)workspace, tiles,
                     L.d_bias_tiles, L.d_cu_seqlens, L.d_cu_pairs};
       bias_image_kernel<<<dim3((unsigned)((tiles + 3) / 4), (unsigned)H), dim3(256), 0, s>>>(b);
-      img = (const uint2*)L.d_attn_ws;
+      img = (const uint2*)workspace;
     }
     PairAttnArgs a{axis, (const bf16*)q, (const bf16*)k, (const bf16*)v, ld_qkv, (const bf16*)bias, ld_bias,
-                   scale * kLog2e, (bf16*)o, ld_o, L.d_pattn_work, L.d_cu_seqlens, L.d_cu_pairs, H,
+                   ld_bias_head, scale * kLog2e, (bf16*)o, ld_o, L.d_pattn_work, L.d_cu_seqlens, L.d_cu_pairs, H,
                    img, tiles * 64, L.d_bias_tiles, L.batch, L.sum_n};
     const size_t smem = sizeof(bf16) * 4 * (size_t)nmax * 32;
     const dim3 grid((unsigned)(L.pattn_items() * H));
@@ -955,7 +949,7 @@ hipError_t launch_attention(const nt_layout& L, int axis, int H, int D, const vo
   }
   const int vstride = (npad + 127) / 128 * 128 + 4;
   AttnArgs a{axis, H, (const bf16*)q, (const bf16*)k, (const bf16*)v, ld_qkv, (const bf16*)bias, ld_bias,
-             scale * kLog2e, (bf16*)o, ld_o, work, L.d_cu_seqlens, L.d_cu_pairs, vstride};
+             ld_bias_head, scale * kLog2e, (bf16*)o, ld_o, work, L.d_cu_seqlens, L.d_cu_pairs, vstride};
   const size_t smem = sizeof(bf16) * ((size_t)npad * (D + 8) + (size_t)D * vstride);
   if (D == 32) {
     if (smem > 65536) hipFuncSetAttribute((const void*)attention_mfma_kernel<32>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);

@@ -216,10 +216,9 @@ bool gemm_fits(int K) { return K % kGBK == 0 && K >= 4 * kGBK && K <= 64 * 8 * 8
 hipError_t launch_gemm(GemmArgs p, hipStream_t s) {
   if (p.rows == 0) return hipSuccess;
   if (p.gamma) {
-    void* ws = nullptr;
-    hipError_t e = device_workspace((size_t)p.rows * p.K * sizeof(bf16), &ws);
-    if (e != hipSuccess) return e;
-    bf16* xn = static_cast<bf16*>(ws);
+    if (!p.ln_ws) return hipErrorInvalidValue;
+    hipError_t e;
+    bf16* xn = p.ln_ws;
     const dim3 grid((unsigned)((p.rows + 3) / 4));
     const int cpl = (p.K / 8 + 63) / 64;          // 16-byte pieces per lane
     if (cpl <= 2) layernorm_rows_kernel<2><<<grid, dim3(256), 0, s>>>(p.x, p.ldx, p.rows, p.K, p.gamma, p.beta, p.eps, xn);

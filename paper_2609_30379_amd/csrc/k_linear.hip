@@ -1724,6 +1724,33 @@ int compute_units() {
   return cache[dev];
 }
 
+namespace {
+
+// The transition kernel serves a bf16 SwiGLU whose residual is x itself.
+bool uses_transition(const nt_linear_args& a) {
+  if (a.dtype != NT_BF16 || a.epilogue != NT_EPI_SWIGLU_RESIDUAL || a.bcast_u) return false;
+  const bool res_is_x = !a.residual || (a.residual == a.x && a.ld_residual == a.ldx);
+  return res_is_x && transition_supported(a.c_in, a.c_out, a.hidden);
+}
+
+// The large-K product: bf16 rows and weights, no tail, whole 16-byte rows.
+bool uses_gemm(const nt_linear_args& a) {
+  if (a.dtype != NT_BF16 || a.bcast_u || a.epilogue == NT_EPI_SWIGLU_RESIDUAL) return false;
+  return a.x_dtype == NT_BF16 && a.n_tail == 0 && a.c_in >= 384 && a.c_in % 32 == 0 && a.c_out % 8 == 0 &&
+         a.ldx % 8 == 0 && a.ldy % 8 == 0 && (a.epilogue != NT_EPI_RESIDUAL || a.ld_residual % 8 == 0) &&
+         (a.epilogue == NT_EPI_NONE || a.epilogue == NT_EPI_GELU || a.epilogue == NT_EPI_RESIDUAL) &&
+         gemm_fits(a.c_in) && a.c_in <= 4096;
+}
+
+}  // namespace
+
+size_t linear_workspace_bytes(const nt_linear_args& a) {
+  if (uses_transition(a)) return transition_image_bytes(a.c_in, a.hidden);
+  if (uses_gemm(a) && a.ln_gamma)     // LN(x) rows written once, then read by the product
+    return (size_t)a.rows * (size_t)a.c_in * sizeof(bf16);
+  return 0;
+}
+
 hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
   const nt_linear_args& a = *plan.a;
   const int rows = (int)a.rows;
@@ -1784,16 +1811,13 @@ hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
     w.res = a.residual ? (const bf16*)a.residual : (const bf16*)a.x;
     w.ld_res = a.residual ? a.ld_residual : a.ldx;
     w.y = (bf16*)a.y; w.ldy = a.ldy;
-    if (transition_supported(a.c_in, a.c_out, a.hidden) && w.res == w.x && w.ld_res == w.ldx) {
+    if (uses_transition(a)) {
       TransArgs t{};
       t.rows = rows; t.K = a.c_in; t.F = a.hidden;
       t.x = w.x; t.ldx = w.ldx; t.gamma = w.gamma; t.beta = w.beta; t.eps = w.eps;
       t.w = w.w; t.bias = w.bias; t.w2 = w.w2; t.bias2 = w.bias2;
       t.y = w.y; t.ldy = w.ldy;
-      void* ws = nullptr;
-      const hipError_t e = device_workspace(transition_image_bytes(a.c_in, a.hidden), &ws);
-      if (e != hipSuccess) return e;
-      return launch_transition(t, ws, s);
+      return launch_transition(t, a.workspace, s);
     }
     constexpr int MT = 2;
     const int rw = 4 * MT * 16;
@@ -1888,13 +1912,11 @@ hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
 #undef NT_ST
     return hipGetLastError();
   }
-  if (!xf && !p.y_tail && a.c_in >= 384 && a.c_in % 32 == 0 && a.c_out % 8 == 0 && a.ldx % 8 == 0 &&
-      p.ldy % 8 == 0 && (a.epilogue != NT_EPI_RESIDUAL || a.ld_residual % 8 == 0) &&
-      (a.epilogue == NT_EPI_NONE || a.epilogue == NT_EPI_GELU || a.epilogue == NT_EPI_RESIDUAL) &&
-      gemm_fits(a.c_in) && a.c_in <= 4096) {
+  if (uses_gemm(a)) {
     GemmArgs g{};
     g.rows = rows; g.K = a.c_in; g.N = a.c_out;
     g.x = (const bf16*)a.x; g.ldx = a.ldx; g.gamma = a.ln_gamma; g.beta = a.ln_beta; g.eps = a.ln_eps;
+    g.ln_ws = (bf16*)a.workspace;
     g.w = (const bf16*)a.w; g.bias = a.bias; g.res = (const bf16*)a.residual; g.ld_res = a.ld_residual;
     g.y = (bf16*)a.y; g.ldy = a.ldy; g.epi = a.epilogue;
     return launch_gemm(g, s);

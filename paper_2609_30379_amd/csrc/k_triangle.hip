@@ -203,12 +203,102 @@ __global__ void __launch_bounds__(256) triangle_f32_kernel(TriF32Args p) {
   }
 }
 
+// ---------------------------------------------------------------- packed operands
+// Re-tiling of a packed pair tensor [sum N^2, C] (row stride ld_src) into
+// pair-tiled channel-major planes (channel stride ld_dst): plane element
+// (r, k) of sample i holds cell (r, k) (plain) or cell (k, r) (transposed);
+// positions outside the N x N matrix hold 0.  One workgroup per 16 x 32 tile
+// (512 positions in fragment order, two per thread); channels are taken 16
+// bytes at a time: each thread loads that piece of its two source cells,
+// parks it in LDS, and the workgroup writes the chunk's channel slices of the
+// tile as contiguous 16-byte pieces.
+template <typename T, bool TRANS>
+__global__ void __launch_bounds__(256) pack_tiled_kernel(const T* __restrict__ src, int64_t ld_src, int C,
+                                                         T* __restrict__ dst, int64_t ld_dst, int batch,
+                                                         const int32_t* __restrict__ cu_seqlens,
+                                                         const int32_t* __restrict__ cu_pairs,
+                                                         const int32_t* __restrict__ cu_pad) {
+  constexpr int V = 16 / sizeof(T);                 // channels per 16-byte piece
+  __shared__ __attribute__((aligned(16))) T park[V * 512];
+  const int64_t tile_pos = (int64_t)blockIdx.x * 512;
+  int lo = 0, hi = batch - 1;                       // sample: largest i with cu_pad[i] <= tile_pos
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (cu_pad[mid] <= tile_pos) lo = mid; else hi = mid - 1;
+  }
+  const int i = lo;
+  const int n = cu_seqlens[i + 1] - cu_seqlens[i];
+  const int nkt = (n + 31) >> 5;
+  const int lt = (int)((tile_pos - cu_pad[i]) >> 9);
+  const int rt = lt / nkt, kt = lt % nkt;
+  const int64_t cu = cu_pairs[i];
+  int64_t row[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int q = threadIdx.x + 256 * h;
+    const int r = rt * 16 + ((q >> 3) & 15), k = kt * 32 + (q >> 7) * 8 + (q & 7);
+    const int a = TRANS ? k : r, b = TRANS ? r : k;
+    row[h] = (r < n && k < n) ? cu + (int64_t)a * n + b : -1;
+  }
+  for (int c0 = 0; c0 < C; c0 += V) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int q = threadIdx.x + 256 * h;
+      uint4 piece = make_uint4(0u, 0u, 0u, 0u);
+      if (row[h] >= 0) piece = *reinterpret_cast<const uint4*>(src + row[h] * ld_src + c0);
+      const T* e = reinterpret_cast<const T*>(&piece);
+#pragma unroll
+      for (int j = 0; j < V; ++j) park[j * 512 + q] = e[j];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int u = threadIdx.x + 256 * h;          // piece u: channel u / (512 / V), positions V * (u % (512 / V))
+      const int ch = u / (512 / V), pos = (u % (512 / V)) * V;
+      if (c0 + ch < C)
+        *reinterpret_cast<uint4*>(dst + (int64_t)(c0 + ch) * ld_dst + tile_pos + pos) =
+            *reinterpret_cast<const uint4*>(&park[ch * 512 + pos]);
+    }
+    __syncthreads();
+  }
+}
+
 }  // namespace
 
-hipError_t launch_triangle(const nt_layout& L, int C, const void* a, const void* b, int64_t ld_ab, void* z,
-                           int64_t ld_z, nt_dtype dtype, hipStream_t s) {
+size_t triangle_workspace_bytes(const nt_layout& L, int C, nt_tri_operands operands, nt_dtype dtype) {
+  if (operands != NT_TRI_PACKED) return 0;
+  const size_t ldp = (size_t)((L.sum_pad + 7) / 8 * 8);
+  return 2 * (size_t)C * ldp * (dtype == NT_BF16 ? 2 : 4);
+}
+
+hipError_t launch_triangle(const nt_layout& L, int direction, int C, const void* a, const void* b, int64_t ld_ab,
+                           nt_tri_operands operands, void* z, int64_t ld_z, nt_dtype dtype, void* workspace,
+                           hipStream_t s) {
   const int64_t items = L.tri_items();
   if (items == 0) return hipSuccess;
+  if (operands == NT_TRI_PACKED) {
+    // re-tile a and b into the workspace in the variant the direction needs
+    const int64_t ldp = (L.sum_pad + 7) / 8 * 8;
+    const size_t es = dtype == NT_BF16 ? 2 : 4;
+    char* wa = static_cast<char*>(workspace);
+    char* wb = wa + (size_t)C * ldp * es;
+    const dim3 grid((unsigned)(L.sum_pad / 512));
+#define NT_PACK(T, TR)                                                                                       \
+    do {                                                                                                     \
+      pack_tiled_kernel<T, TR><<<grid, dim3(256), 0, s>>>((const T*)a, ld_ab, C, (T*)wa, ldp, L.batch,        \
+                                                          L.d_cu_seqlens, L.d_cu_pairs, L.d_cu_pad);           \
+      pack_tiled_kernel<T, TR><<<grid, dim3(256), 0, s>>>((const T*)b, ld_ab, C, (T*)wb, ldp, L.batch,        \
+                                                          L.d_cu_seqlens, L.d_cu_pairs, L.d_cu_pad);           \
+    } while (0)
+    if (dtype == NT_BF16) { if (direction == 0) NT_PACK(bf16, false); else NT_PACK(bf16, true); }
+    else { if (direction == 0) NT_PACK(float, false); else NT_PACK(float, true); }
+#undef NT_PACK
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    a = wa;
+    b = wb;
+    ld_ab = ldp;
+  }
   if (dtype == NT_F32) {
     TriF32Args t{C, (const float*)a, (const float*)b, ld_ab, (float*)z, ld_z, L.d_tri_work, L.d_cu_seqlens,
                  L.d_cu_pairs, L.d_cu_pad};

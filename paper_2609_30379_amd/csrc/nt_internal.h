@@ -67,10 +67,6 @@ struct nt_layout {
   const int32_t* d_bias_tiles = nullptr;
   const int32_t* d_sattn_work = nullptr;
   const int32_t* d_bc_cu_tiles = nullptr;
-  // pair attention workspace (the bias image), allocated by the first call
-  // that needs it and grown on demand; freed with the layout
-  mutable void* d_attn_ws = nullptr;
-  mutable size_t attn_ws_bytes = 0;
 
   int64_t attn_items() const { return (int64_t)attn_work.size() / 2; }
   int64_t tri_items() const { return (int64_t)tri_work.size() / 4; }
@@ -91,6 +87,7 @@ struct GemmArgs {
   const float* gamma;    // LayerNorm of x when non-NULL
   const float* beta;
   float eps;
+  __bf16* ln_ws;         // with gamma: rows * K bf16 of caller workspace for LN(x)
   const __bf16* w;
   const float* bias;
   const __bf16* res;     // epi == NT_EPI_RESIDUAL
@@ -101,7 +98,7 @@ struct GemmArgs {
   int ntm, ntn;          // tiles (set by the launcher)
 };
 bool gemm_fits(int K);
-// With gamma set, the rows are first normalised into the device workspace.
+// With gamma set, the rows are first normalised into p.ln_ws.
 hipError_t launch_gemm(GemmArgs p, hipStream_t s);
 
 // SwiGLU transition with residual (k_transition.hip):
@@ -131,10 +128,6 @@ size_t transition_image_bytes(int K, int F);
 hipError_t launch_transition(TransArgs p, void* wimg_workspace, hipStream_t s);
 int compute_units();
 
-// Per-device scratch owned by the library (api.cpp): at least `bytes`, grown
-// on demand (growing synchronises the device); calls that use it on one
-// device must be ordered.
-hipError_t device_workspace(size_t bytes, void** ptr);
 
 // Sets the thread-local error message and returns the status.
 nt_status fail(nt_status s, const std::string& msg);
@@ -157,16 +150,29 @@ struct LinearPlan {
   int tail_mode;
   const nt_layout* layout;   // for pair-tiled tail modes
 };
+// Workspace bytes the call needs (0: none): LN(x) rows of the large-K product
+// or the transition's weight image.  Mirrors the kernel choice of launch_linear.
+size_t linear_workspace_bytes(const nt_linear_args& a);
+// a.workspace must hold linear_workspace_bytes(a) bytes (checked by the caller).
 hipError_t launch_linear(const LinearPlan& p, hipStream_t s);
 
+// Bias-image bytes of a pair attention call (0: none).
+size_t attention_workspace_bytes(const nt_layout& L, int axis, int H, int D, nt_dtype dtype, bool has_bias);
+// bias element (cell c, head h) at bias[c * ld_bias + h * ld_bias_head];
+// workspace: attention_workspace_bytes(...) bytes.
 hipError_t launch_attention(const nt_layout& L, int axis, int H, int D,
                             const void* q, const void* k, const void* v, int64_t ld_qkv,
-                            const void* bias, int64_t ld_bias, float scale,
-                            void* o, int64_t ld_o, nt_dtype dtype, hipStream_t s);
+                            const void* bias, int64_t ld_bias, int64_t ld_bias_head, float scale,
+                            void* o, int64_t ld_o, nt_dtype dtype, void* workspace, hipStream_t s);
 
-hipError_t launch_triangle(const nt_layout& L, int C, const void* a, const void* b,
-                           int64_t ld_ab, void* z, int64_t ld_z, nt_dtype dtype,
-                           hipStream_t s);
+// Workspace bytes of a triangle call: the re-tiled a and b for packed
+// operands, 0 for pair-tiled ones.
+size_t triangle_workspace_bytes(const nt_layout& L, int C, nt_tri_operands operands, nt_dtype dtype);
+// Pair-tiled operands (plane variant matching the direction) are contracted
+// directly; packed ones are first re-tiled into the workspace.
+hipError_t launch_triangle(const nt_layout& L, int direction, int C, const void* a, const void* b,
+                           int64_t ld_ab, nt_tri_operands operands, void* z, int64_t ld_z, nt_dtype dtype,
+                           void* workspace, hipStream_t s);
 
 // Host-side planner (pure C++; no HIP calls).  Fills every host array of the
 // layout from the lengths, or returns an error status.

@@ -36,3 +36,22 @@ def pytest_collection_modifyitems(config, items):
     for it in items:
         if "gpu" in it.keywords:
             it.add_marker(skip)
+
+
+def pytest_terminal_summary(terminalreporter, exitstatus, config):
+    """Prints every recorded parity comparison with its margin (error / bar)."""
+    try:
+        from tests.gpu_util import PARITY_LOG
+    except Exception:
+        return
+    if not PARITY_LOG:
+        return
+    tr = terminalreporter
+    tr.section(f"parity margins ({len(PARITY_LOG)} comparisons, error / bar)")
+    for what, err, bar, amax in sorted(PARITY_LOG, key=lambda r: -r[1] / r[2]):
+        tr.write_line(f"{err / bar:6.3f}  err {err:.3e}  bar {bar:.0e}  max|ref| {amax:.3g}  {what}")
+    path = os.environ.get("NT_PARITY_LOG")
+    if path:
+        import json
+        with open(path, "w") as f:
+            json.dump([{"case": w, "error": e, "bar": b, "max_abs_ref": a} for w, e, b, a in PARITY_LOG], f, indent=0)

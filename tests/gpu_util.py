@@ -31,6 +31,17 @@ def host(t) -> np.ndarray:
     return t.detach().to(device="cpu", dtype=torch.float64).numpy()
 
 
+# Every comparison is recorded here as (what, error, bar, max |reference|);
+# the test session prints them at its end (tests/conftest.py), so the margin of
+# each case is visible in the log, not only its pass/fail.
+PARITY_LOG: list = []
+
+# bf16 values below this magnitude have a half-ulp of at most 2^-6 < 2e-2, so
+# one rounding of the stored output stays inside the bar; inputs are scaled so
+# every compared bf16 tensor stays below it.
+BF16_MAX_MAGNITUDE = 8.0
+
+
 def check(got: np.ndarray, ref: np.ndarray, dtype: str, what: str = "", equal_nan: bool = False):
     got = np.asarray(got, np.float64)
     ref = np.asarray(ref, np.float64)
@@ -42,13 +53,53 @@ def check(got: np.ndarray, ref: np.ndarray, dtype: str, what: str = "", equal_na
     assert np.all(np.isfinite(got)), f"{what}: non-finite GPU output"
     if got.size == 0:
         return 0.0
+    amax = float(np.max(np.abs(ref)))
     if dtype == "bf16":
         err = float(np.max(np.abs(got - ref)))
+        PARITY_LOG.append((what, err, BF16_MAX_ABS, amax))
         assert err <= BF16_MAX_ABS, f"{what}: max-abs error {err:.4g} > {BF16_MAX_ABS}"
+        assert amax < BF16_MAX_MAGNITUDE, f"{what}: reference magnitude {amax:.3g} beyond the bf16 range of the bar"
     else:
-        denom = float(np.max(np.abs(ref)))
-        err = float(np.max(np.abs(got - ref))) / (denom if denom > 0 else 1.0)
+        err = float(np.max(np.abs(got - ref))) / (amax if amax > 0 else 1.0)
+        PARITY_LOG.append((what, err, F32_NORMWISE, amax))
         assert err <= F32_NORMWISE, f"{what}: normwise relative error {err:.3g} > {F32_NORMWISE}"
+    return err
+
+
+def ulp_bf16(x) -> np.ndarray:
+    """Spacing of bf16 values at |x| (8 significant bits): 2^(floor(log2 |x|) - 7)."""
+    a = np.maximum(np.abs(np.asarray(x, np.float64)), 2.0 ** -126)
+    return np.ldexp(1.0, np.floor(np.log2(a)).astype(np.int64) - 7)
+
+
+# A chain of bf16-stored steps can round one intermediate differently on the
+# two sides (the fp32 and float64 values straddle a rounding boundary); the
+# one-ulp difference then travels down the residual stream and meets the
+# final rounding.  Chained comparisons therefore allow two bf16 ulps of the
+# value where that exceeds the per-kernel bar; each kernel on its own stored
+# inputs is held to the bar itself.
+CHAIN_ULPS = 2.0
+
+
+def check_chained(got: np.ndarray, ref: np.ndarray, what: str = ""):
+    """Chained bf16 comparison: every element within 2e-2, or within two bf16
+    ulps of the larger of the two values where that is wider."""
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    assert got.shape == ref.shape, (what, got.shape, ref.shape)
+    assert np.all(np.isfinite(got)), f"{what}: non-finite GPU output"
+    if got.size == 0:
+        return 0.0
+    d = np.abs(got - ref)
+    bound = np.maximum(BF16_MAX_ABS, CHAIN_ULPS * ulp_bf16(np.maximum(np.abs(got), np.abs(ref))))
+    err = float(np.max(d))
+    ratio = float(np.max(d / bound))
+    amax = float(np.max(np.abs(ref)))
+    PARITY_LOG.append((what + f" [chained; {ratio:.2f} of max(2e-2, 2 ulp)]", err, BF16_MAX_ABS, amax))
+    worst = int(np.argmax(d / bound))
+    assert ratio <= 1.0, (f"{what}: chained error {d.flat[worst]:.4g} at |ref| {abs(ref.flat[worst]):.3g} "
+                          f"exceeds max(2e-2, {CHAIN_ULPS:g} ulp)")
+    assert amax < BF16_MAX_MAGNITUDE, f"{what}: reference magnitude {amax:.3g} beyond the bf16 range of the bar"
     return err
 
 

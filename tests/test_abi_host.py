@@ -135,7 +135,7 @@ def test_op_argument_errors_need_no_device(lib):
     # op calls reject host-only layouts before touching the device
     st = lib.nt_pair_broadcast(host.handle, 8, C.c_void_p(16), 8, C.c_void_p(16), 8, C.c_void_p(16), 8, 0, B.NT_BF16, None)
     assert st == B.NT_ERR_INVALID_ARG and b"host-only" in lib.nt_last_error()
-    st = lib.nt_triangle_mul(host.handle, 0, 32, None, None, 0, None, 32, B.NT_BF16, None)
+    st = lib.nt_triangle_mul(host.handle, 0, 32, None, None, 0, 1, None, 32, B.NT_BF16, None, 0, None)
     assert st == B.NT_ERR_INVALID_ARG
     st = lib.nt_segment_reduce(None, 1, 0, 8, None, 8, B.NT_BF16, None, 8, None)
     assert st == B.NT_ERR_INVALID_ARG
@@ -164,8 +164,68 @@ def test_op_argument_errors_need_no_device(lib):
         assert lib.nt_layernorm_linear(C.byref(a), None) == want, (kw, lib.nt_last_error())
     # attention validation
     dev = B.NestedLayout([2, 3], host_only=True)
-    assert lib.nt_pair_row_attention(dev.handle, 0, 4, 32, None, None, None, 384, None, 0, 1.0, None, 128,
-                                     B.NT_BF16, None) == B.NT_ERR_INVALID_ARG    # host-only layout
+    assert lib.nt_pair_row_attention(dev.handle, 0, 4, 32, None, None, None, 384, None, 0, 0, 1.0, None, 128,
+                                     B.NT_BF16, None, 0, None) == B.NT_ERR_INVALID_ARG    # host-only layout
+
+
+def _q(fn, *args):
+    n = C.c_uint64()
+    assert fn(*args, C.byref(n)) == B.NT_OK
+    return int(n.value)
+
+
+def test_workspace_queries_and_missing_workspace_is_an_error(lib):
+    """Ops take scratch memory only from the caller: the queries return its
+    size from sizes alone, and a call that needs scratch but is given none (or
+    too little) returns NT_ERR_INVALID_ARG instead of allocating."""
+    L = [222, 208, 33, 0, 1]
+    lay = B.NestedLayout(L, host_only=True)
+    tiles = sum(-(-n // 16) * (-(-n // 64) * 4) for n in L)
+    # pair attention, bf16, d = 32, N <= 512, with a bias: the bias image
+    assert _q(lib.nt_pair_row_attention_workspace, lay.handle, 0, 4, 32, B.NT_BF16, 1) == 4 * tiles * 512
+    assert _q(lib.nt_pair_row_attention_workspace, lay.handle, 1, 3, 32, B.NT_BF16, 1) == 3 * tiles * 512
+    assert _q(lib.nt_pair_row_attention_workspace, lay.handle, 0, 4, 32, B.NT_BF16, 0) == 0
+    assert _q(lib.nt_pair_row_attention_workspace, lay.handle, 2, 12, 64, B.NT_BF16, 0) == 0
+    assert _q(lib.nt_pair_row_attention_workspace, lay.handle, 0, 2, 8, B.NT_F32, 1) == 0
+    long = B.NestedLayout([600, 3], host_only=True)           # past 512: the per-row kernel reads the bias directly
+    assert _q(lib.nt_pair_row_attention_workspace, long.handle, 0, 4, 32, B.NT_BF16, 1) == 0
+    # triangle: packed operands are re-tiled into the workspace, tiled ones need none
+    ldp = -(-lay.sum_pad // 8) * 8
+    assert _q(lib.nt_triangle_mul_workspace, lay.handle, 128, 0, B.NT_BF16) == 2 * 128 * ldp * 2
+    assert _q(lib.nt_triangle_mul_workspace, lay.handle, 16, 0, B.NT_F32) == 2 * 16 * ldp * 4
+    assert _q(lib.nt_triangle_mul_workspace, lay.handle, 128, 1, B.NT_BF16) == 0
+    # LayerNorm+Linear: large-K rows with a LayerNorm, and the SwiGLU transition
+    a = _linear_args(rows=600, c_in=768, c_out=2304, ldx=768, ldy=2304, ln_gamma=C.c_void_p(0x9000))
+    assert _q(lib.nt_layernorm_linear_workspace, C.byref(a)) == 600 * 768 * 2
+    a = _linear_args(rows=600, c_in=768, c_out=2304, ldx=768, ldy=2304)           # no LayerNorm: none
+    assert _q(lib.nt_layernorm_linear_workspace, C.byref(a)) == 0
+    a = _linear_args(rows=1000, c_in=128, c_out=128, ldx=128, ldy=128, epilogue=2, hidden=512,
+                     w2=C.c_void_p(0xa000), ln_gamma=C.c_void_p(0x9000))
+    assert _q(lib.nt_layernorm_linear_workspace, C.byref(a)) == 3 * 512 * 128 * 2
+    a = _linear_args(rows=1000, c_in=128, c_out=128, ldx=128, ldy=128, ln_gamma=C.c_void_p(0x9000))
+    assert _q(lib.nt_layernorm_linear_workspace, C.byref(a)) == 0
+    # calls that need scratch and get none, or too little: an error, nothing enqueued
+    a = _linear_args(rows=600, c_in=768, c_out=2304, ldx=768, ldy=2304, ln_gamma=C.c_void_p(0x9000))
+    assert lib.nt_layernorm_linear(C.byref(a), None) == B.NT_ERR_INVALID_ARG
+    assert b"workspace" in lib.nt_last_error()
+    a.workspace, a.workspace_bytes = C.c_void_p(0xb000), 600 * 768 * 2 - 1
+    assert lib.nt_layernorm_linear(C.byref(a), None) == B.NT_ERR_INVALID_ARG
+    assert b"workspace" in lib.nt_last_error()
+    st = lib.nt_pair_row_attention(lay.handle, 0, 4, 32, C.c_void_p(16), C.c_void_p(16), C.c_void_p(16), 384,
+                                   C.c_void_p(16), 1, lay.sum_n2, 0.17, C.c_void_p(16), 128, B.NT_BF16, None, 0, None)
+    assert st == B.NT_ERR_INVALID_ARG and b"workspace" in lib.nt_last_error()
+    st = lib.nt_triangle_mul(lay.handle, 1, 128, C.c_void_p(16), C.c_void_p(16), 256, 0, C.c_void_p(16), 128,
+                             B.NT_BF16, None, 0, None)
+    assert st == B.NT_ERR_INVALID_ARG and b"workspace" in lib.nt_last_error()
+    # with enough workspace the same calls get past the workspace check (and stop
+    # at the host-only layout, still before any device work)
+    st = lib.nt_triangle_mul(lay.handle, 1, 128, C.c_void_p(16), C.c_void_p(16), 256, 0, C.c_void_p(16), 128,
+                             B.NT_BF16, C.c_void_p(0x10000), 2 * 128 * ldp * 2, None)
+    assert st == B.NT_ERR_INVALID_ARG and b"host-only" in lib.nt_last_error()
+    # a pair-tiled variant that does not match the direction
+    st = lib.nt_triangle_mul(lay.handle, 1, 128, C.c_void_p(16), C.c_void_p(16), ldp, 1, C.c_void_p(16), 128,
+                             B.NT_BF16, None, 0, None)
+    assert st == B.NT_ERR_INVALID_ARG and b"transposed" in lib.nt_last_error()
 
 
 @pytest.mark.parametrize("n", [1, 15, 16, 17, 33, 216])
@@ -187,3 +247,10 @@ def test_pair_tiled_plane_is_a_fragment_order_bijection(n):
     L = [n, 3]
     for tr in (False, True):
         assert np.array_equal(untile_pair(pair_tiled(x, L, tr, fill=np.nan), L, tr), x)
+
+
+@pytest.mark.parametrize("n", [1, 15, 16, 17, 401408, 393216 + 3])
+def test_workspace_tensor_holds_the_requested_bytes(n):
+    t = B.workspace_tensor(n, device="cpu")
+    assert t.numel() * t.element_size() == n and t.data_ptr() % 16 == 0
+    assert B.workspace_tensor(0, device="cpu") is None

@@ -101,11 +101,16 @@ LIN_CASES = [
     (333, 64, 512, True, "gelu", "bf16", "bf16", 0),        # wave kernel, four column groups
     (95, 128, 128, True, "residual", "bf16", "bf16", 0),    # wave kernel, residual, last tile of 15 rows
     (300, 384, 256, False, "none", "bf16", "bf16", 0),
-    (600, 768, 2304, True, "none", "bf16", "bf16", 0),
+    (600, 768, 2304, True, "none", "bf16", "bf16", 0),       # large-K path (LayerNorm rows in the workspace)
     (600, 768, 3072, True, "gelu", "bf16", "bf16", 0),
-    (600, 3072, 768, False, "residual", "bf16", "bf16", 0),
+    (600, 3072, 768, False, "residual", "bf16", "bf16", 0),  # no LayerNorm, <= 8192 rows: small-row kernel
+    (8500, 3072, 768, False, "residual", "bf16", "bf16", 0), # no LayerNorm, > 8192 rows: large-K path
     (200, 416, 136, True, "gelu", "bf16", "bf16", 0),        # large-K path: 13 k-steps, part of a channel tile
-    (257, 1024, 520, False, "residual", "bf16", "bf16", 0),  # large-K path: one row past a row tile
+    (257, 1024, 520, True, "residual", "bf16", "bf16", 0),   # large-K path: one row past a row tile
+    (1000, 256, 256, True, "none", "bf16", "bf16", 0),       # K = 256 without SwiGLU: row-tile kernel
+    (9000, 256, 128, False, "gelu", "bf16", "bf16", 0),      # K = 256, no LayerNorm, > 8192 rows: row-tile kernel
+    (700, 128, 600, True, "none", "bf16", "bf16", 0),        # K = 128, > 512 outputs: row-tile kernel
+    (333, 64, 520, True, "residual", "bf16", "bf16", 0),     # K = 64, > 512 outputs with a residual: row-tile kernel
     (300, 128, 384, False, "residual", "f32", "bf16", 0),
     (129, 136, 40, True, "residual", "bf16", "bf16", 0),
     (100, 16, 50, True, "none", "f32", "f32", 2),
@@ -230,7 +235,8 @@ def _head_major(bias_cells):
                                             ("bf16", 3, 32, "att"), ("bf16", 4, 32, "few"),
                                             ("bf16", 2, 32, "long"), ("bf16", 2, 32, "edge256"),
                                             ("bf16", 2, 32, "mid"), ("bf16", 2, 32, "mid512")])
-def test_pair_attention(B, axis, dtype, H, D, lset):
+@pytest.mark.parametrize("bias_layout", ["heads", "cells", None])
+def test_pair_attention(B, axis, dtype, H, D, lset, bias_layout):
     import torch
     # head_dim 32: samples up to 256 take the persistent short-row kernel, one
     # workgroup per CU with an equal share of all rows, crossing sample
@@ -254,18 +260,28 @@ def test_pair_attention(B, axis, dtype, H, D, lset):
     td = torch.bfloat16 if dtype == "bf16" else torch.float32
     o = torch.full((R, H * D), float("nan"), dtype=td, device="cuda")
     c = H * D
-    bd = dev(_head_major(bias), dtype)
-    B.nt_pair_row_attention(lay, axis, H, D, qd[:, :c], qd[:, c:2 * c], qd[:, 2 * c:], o, bias=bd)
+    if bias_layout == "heads":
+        bd = dev(_head_major(bias), dtype)
+    elif bias_layout == "cells":               # [sum N^2, H] as a column slice of a wider buffer (row stride H + 5)
+        wide = np.zeros((R, H + 5))
+        wide[:, 2:2 + H] = bias
+        bd = dev(wide, dtype)[:, 2:2 + H]
+    else:
+        bd, bias = None, None
+    B.nt_pair_row_attention(lay, axis, H, D, qd[:, :c], qd[:, c:2 * c], qd[:, 2 * c:], o, bias=bd,
+                            bias_layout=bias_layout or "cells")
     first = host(o)
     # a second call over whatever the first left in LDS must give the same bits
-    B.nt_pair_row_attention(lay, axis, H, D, qd[:, :c], qd[:, c:2 * c], qd[:, 2 * c:], o, bias=bd)
+    B.nt_pair_row_attention(lay, axis, H, D, qd[:, :c], qd[:, c:2 * c], qd[:, 2 * c:], o, bias=bd,
+                            bias_layout=bias_layout or "cells")
     assert np.array_equal(host(o), first, equal_nan=True), "pair attention is not deterministic"
     ref = O.pair_row_attention(qkv[:, :c], qkv[:, c:2 * c], qkv[:, 2 * c:], bias, L, H, D, axis=axis)
-    check(first, ref, dtype, f"pair attention axis {axis} {dtype}")
+    check(first, ref, dtype, f"pair attention axis {axis} {dtype} {lset} H={H} d={D} bias {bias_layout}")
 
 
 @pytest.mark.parametrize("H,lset", [(4, "att"), (12, "att"), (12, "mid512"), (4, "one")])
-def test_single_attention_pair_bias(B, H, lset):
+@pytest.mark.parametrize("bias_layout", ["heads", "cells", None])
+def test_single_attention_pair_bias(B, H, lset, bias_layout):
     """Axis 3: attention over each sample's tokens with the bias read from the
     pair state (bf16, d = 32), against the oracle; plus its argument errors."""
     import torch
@@ -278,9 +294,20 @@ def test_single_attention_pair_bias(B, H, lset):
     c = H * D
     qd = dev(qkv, "bf16")
     o = torch.full((T, c), float("nan"), dtype=torch.bfloat16, device="cuda")
-    B.nt_pair_row_attention(lay, 3, H, D, qd[:, :c], qd[:, c:2 * c], qd[:, 2 * c:], o, bias=dev(_head_major(bias), "bf16"))
+    if bias_layout == "heads":
+        bd = dev(_head_major(bias), "bf16")
+    elif bias_layout == "cells":
+        bd = dev(bias, "bf16")
+    else:
+        bd, bias = None, None
+    call = lambda: B.nt_pair_row_attention(lay, 3, H, D, qd[:, :c], qd[:, c:2 * c], qd[:, 2 * c:], o, bias=bd,  # noqa: E731
+                                           bias_layout=bias_layout or "cells")
+    call()
+    first = host(o)
+    call()                                       # a second call must give the same bits
+    assert np.array_equal(host(o), first, equal_nan=True), "single attention is not deterministic"
     ref = O.single_attention_pair_bias(qkv[:, :c], qkv[:, c:2 * c], qkv[:, 2 * c:], bias, L, H, D)
-    check(host(o), ref, "bf16", f"single attention with pair bias H={H} {lset}")
+    check(first, ref, "bf16", f"single attention with pair bias H={H} {lset} bias {bias_layout}")
     with pytest.raises(B.NtError):              # f32 is not supported on axis 3
         of = torch.zeros((T, c), dtype=torch.float32, device="cuda")
         qf = torch.zeros((T, 3 * c), dtype=torch.float32, device="cuda")
@@ -311,7 +338,9 @@ def test_attention_1d(B, dtype, H, D, L):
 @pytest.mark.parametrize("direction", [0, 1])
 @pytest.mark.parametrize("dtype,C,lname", [("bf16", 64, "ragged"), ("bf16", 32, "tiny"), ("f32", 16, "tiny"),
                                            ("f32", 16, "ragged")])
-def test_triangle(B, direction, dtype, C, lname):
+def test_triangle_pair_tiled(B, direction, dtype, C, lname):
+    """Operands already pair-tiled (the plain variant for outgoing, the
+    transposed one for incoming), padding filled with NaN."""
     L = LENGTHS[lname]
     lay = _layout(B, L)
     R = sum(n * n for n in L)
@@ -323,6 +352,43 @@ def test_triangle(B, direction, dtype, C, lname):
     ap = dev(pair_tiled(a, L, tr, ld, fill=np.nan), dtype)
     bp = dev(pair_tiled(b, L, tr, ld, fill=np.nan), dtype)
     z = dev(z0, dtype)
-    B.nt_triangle_mul(lay, direction, ap, bp, z)
+    B.nt_triangle_mul(lay, direction, ap, bp, z, operands="pair_tiled_t" if tr else "pair_tiled")
     ref = z0 + O.triangle_mul(a, b, L, "outgoing" if direction == 0 else "incoming")
-    check(host(z), ref, dtype, f"triangle dir {direction} {dtype} {lname}")
+    check(host(z), ref, dtype, f"triangle pair-tiled dir {direction} {dtype} {lname}")
+    # the other variant does not match this direction: rejected before any work
+    with pytest.raises(B.NtError):
+        B.nt_triangle_mul(lay, direction, ap, bp, z, operands="pair_tiled" if tr else "pair_tiled_t")
+
+
+TRI_PACKED = [
+    ("bf16", 64, [5, 0, 1, 37, 64, 3, 70]),
+    ("bf16", 128, [489, 420, 257, 1, 0]),        # the longest pair states of the workloads, full width
+    ("bf16", 128, [222, 208, 33]),
+    ("f32", 16, [15, 12, 10, 7]),
+    ("f32", 12, [5, 0, 1, 37, 3]),
+]
+
+
+@pytest.mark.parametrize("direction", [0, 1])
+@pytest.mark.parametrize("dtype,C,L", TRI_PACKED)
+def test_triangle_packed(B, direction, dtype, C, L):
+    """Operands as packed [sum N^2, C] pair tensors (Eq. packing), the call
+    re-tiling them into its workspace; a and b are column slices of one
+    [sum N^2, 2C] projection, as a producer writes them."""
+    lay = _layout(B, L)
+    R = sum(n * n for n in L)
+    nmax = max(L)
+    ab = _n(29, "ab", (R, 2 * C), float(np.sqrt(0.5 / np.sqrt(nmax))), dtype)    # t = sum_k a b of std ~0.5
+    z0 = _n(30, "z0", (R, C), 0.5, dtype)
+    abd = dev(ab, dtype)
+    z = dev(z0, dtype)
+    B.nt_triangle_mul(lay, direction, abd[:, :C], abd[:, C:], z, operands="packed")
+    direc = "outgoing" if direction == 0 else "incoming"
+    cu = np.concatenate([[0], np.cumsum([n * n for n in L])])
+    got = host(z)
+    for i, n in enumerate(L):                   # per sample: the oracle on one sample at a time
+        if n == 0:
+            continue
+        sl = slice(int(cu[i]), int(cu[i + 1]))
+        ref = z0[sl] + O.triangle_mul(ab[sl, :C], ab[sl, C:], [n], direc)
+        check(got[sl], ref, dtype, f"triangle packed dir {direction} {dtype} C={C} sample N={n}")
