@@ -1,16 +1,22 @@
 #!/usr/bin/env python3
 """Benchmark of the packed pair-state hot path on one MI355X.
 
-One step = one pass of the whole pair block over the batch: single
-projections, pair broadcast and LayerNorm+Linear (one fused launch: the
-broadcast rows are built as the projection reads them), row attention with pair bias
-(projection, attention, output projection + residual), triangle update
-(projection + contraction), SwiGLU transition, and the column mean back to the
-single track.  Default workload: B=8 near-uniform lengths 208..224, C_s=384,
-C_z=128, 4 heads x 32, transition 128->512->128, bf16 with fp32 accumulation.
+One step = one pass of the whole workload over its batch, every op one launch
+over all samples.  Default workload: the four-block Pairformer-style stack
+(B=16, lognormal lengths around 192 clipped to [16, 768], C_s=384, C_z=128,
+4 heads x 32, transition 128->512->128, bf16 with fp32 accumulation); each
+block is pair broadcast, outgoing and incoming triangle updates, row and
+column attention with pair bias, the SwiGLU transition and the column mean
+back to the single track.  value = blocks x sum N^2 / step time (valid pair
+positions per second per pair block).
 
-Prints one JSON line (see the fields below).  --gpus N > 1 is rejected: the
-path runs on one GPU.
+The same JSON line nests the near-uniform (B=8, 208..224) and high-variation
+(B=8, 32..512) single pair blocks and the packed-token encoder layer (tokens
+per second), each timed the same way.  Step times are reported warm (steps
+back to back) and cold (a 512 MB write flushes the memory-side cache before
+each step), as median, p10 and p90.
+
+--gpus N > 1 is rejected: the path runs on one GPU.
 """
 from __future__ import annotations
 
@@ -29,26 +35,34 @@ BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 matrix cores, TFLOP/s
 F32_PEAK_TFLOPS = 157.3        # fp32 vector
 
 
-# Measured HBM traffic per launch of each op's kernel on the default workload:
-# rocprofv3 --pmc FETCH_SIZE and --pmc WRITE_SIZE passes (KiB per dispatch),
-# tagged with a hash of the kernel's source file (plus the shared device
-# header) at the time the counters were taken.  A plain 256 MiB device copy
-# reads 131,087 KiB on FETCH_SIZE and 262,144 KiB on WRITE_SIZE, so bytes =
-# 2.0 x FETCH_SIZE + 1.0 x WRITE_SIZE.  When the source hash no longer
-# matches, the kernel has changed since the counters and traffic is null.
+# Measured HBM traffic per launch of each op's kernels: rocprofv3 --pmc
+# FETCH_SIZE and --pmc WRITE_SIZE passes (KiB per dispatch, summed over the
+# op's kernels), per workload, tagged with a hash of the kernel's source file
+# (plus the shared device header) at the time the counters were taken.  A
+# plain 256 MiB device copy reads 131,087 KiB on FETCH_SIZE and 262,144 KiB on
+# WRITE_SIZE, so bytes = 2.0 x FETCH_SIZE + 1.0 x WRITE_SIZE.  When the source
+# hash no longer matches, the kernel has changed since the counters and
+# traffic is null.
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
-COUNTER_WORKLOAD = "pair_b8_n208_224_bf16"
-COUNTERS = {  # op: (kernel source, source hash, FETCH_SIZE KiB, WRITE_SIZE KiB)
-    "attention_row": ("k_attention.hip", "edb107d47362cde5", 141466, 90996),
-    "transition": ("k_transition.hip", "e2f701d5925d7f6e", 53091, 91003),
-    "triangle_out": ("k_triangle.hip", "e32c93982e48a7b7", 231648, 94069),
-    "attn_proj": ("k_linear.hip", "d85e0184919ac8cf", 46004, 276032),
-    "tri_proj": ("k_linear.hip", "d85e0184919ac8cf", 46263, 197120),
-    "bcast_ln_linear": ("k_linear.hip", "d85e0184919ac8cf", 2218, 90996),
-    "attn_out_residual": ("k_linear.hip", "d85e0184919ac8cf", 91221, 91004),
-    "single_proj": ("k_linear.hip", "d85e0184919ac8cf", 3360, 853),
-    "segment_mean": ("k_segment.hip", "c95eabc6d4c62896", 45570, 853),
-    "single_update": ("k_linear.hip", "d85e0184919ac8cf", 3624, 1280),
+COUNTERS = {  # workload: {op: (kernel source, source hash, FETCH_SIZE KiB, WRITE_SIZE KiB)}
+    "pairformer4_b16_lognormal192_bf16": {
+        "attention_row": ("k_attention.hip", "1c8befb2fe5cd30a", 337377 + 8060, 174369 + 6472),
+        "attention_col": ("k_attention.hip", "1c8befb2fe5cd30a", 337377 + 8060, 174369 + 6472),
+        "triangle_out": ("k_triangle.hip", "d6c9a1770a0bb33e", 686568, 177255),
+        "triangle_in": ("k_triangle.hip", "d6c9a1770a0bb33e", 686568, 177255),
+        "transition": ("k_transition.hip", "e2f701d5925d7f6e", 100348 + 268, 174431 + 384),
+        "attn_proj": ("k_linear.hip", "ab0523789d210285", 87689, 528956),
+        "tri_proj": ("k_linear.hip", "ab0523789d210285", 87863, 386304),
+        "attn_out_residual": ("k_linear.hip", "ab0523789d210285", 174594, 174373),
+        "pair_broadcast": ("k_segment.hip", "c95eabc6d4c62896", 68901, 174369),
+        "segment_mean": ("k_segment.hip", "c95eabc6d4c62896", 87296, 1492),
+        "single_proj": ("k_linear.hip", "ab0523789d210285", 5276, 1492),
+        "single_update": ("k_linear.hip", "ab0523789d210285", 6018, 2237),
+    },
+    "pair_b8_n208_224_bf16": {
+        "transition": ("k_transition.hip", "e2f701d5925d7f6e", 53091, 91003),
+        "segment_mean": ("k_segment.hip", "c95eabc6d4c62896", 45570, 853),
+    },
 }
 
 
@@ -63,10 +77,12 @@ def source_hash(fname: str) -> str:
 
 def measured_traffic(op: str, workload: str):
     """HBM bytes per launch from the committed counters, or None when they do
-    not apply (another workload, or the kernel source changed since)."""
-    if workload != COUNTER_WORKLOAD or op not in COUNTERS:
+    not apply (no counters for this workload and op, or the kernel source
+    changed since they were taken)."""
+    entry = COUNTERS.get(workload, {}).get(op)
+    if entry is None:
         return None
-    src, tag, fetch_kib, write_kib = COUNTERS[op]
+    src, tag, fetch_kib, write_kib = entry
     if source_hash(src) != tag:
         return None
     return int((FETCH_SCALE * fetch_kib + WRITE_SCALE * write_kib) * 1024)
@@ -157,9 +173,11 @@ def cpu_baseline_tokens(w, run, min_s: float = 10.0):
 
 
 def cpu_baseline(w, run, min_s: float = 10.0):
-    """The CPU oracle timed on this host: one pass of the same pair block over
+    """The CPU oracle timed on this host: the whole workload (every block) on
     samples of the batch taken smallest first, one at a time, until at least
-    min_s seconds of work (about 10-15 s); pair positions per second."""
+    min_s seconds of work.  The oracle's time is dominated by the per-sample
+    N^3 contractions, so the time of the whole batch is estimated as the
+    measured time scaled by the batch's sum N^3 over the timed samples'."""
     import numpy as np
     from oracle import blocks as OB
     try:
@@ -169,7 +187,7 @@ def cpu_baseline(w, run, min_s: float = 10.0):
         threads = 1
     dims = dict(c_z=w.c_z, heads=w.heads, head_dim=w.head_dim)
     eta = np.concatenate([[0], np.cumsum(run.lengths)])
-    done, positions, dt = [], 0, 0.0
+    done, n3, dt = [], 0, 0.0
     for i in np.argsort(run.lengths, kind="stable"):
         n = int(run.lengths[i])
         s = run.s_init[eta[i]:eta[i] + n]
@@ -180,13 +198,18 @@ def cpu_baseline(w, run, min_s: float = 10.0):
             s, z, _ = OB.pair_block(s, [n], run.params[b], dims, steps, z=z, dtype=w.dtype)
         dt += time.perf_counter() - t0
         done.append(f"{int(i)} (N={n})")
-        positions += n * n * w.blocks
+        n3 += n ** 3
         if dt >= min_s:
             break
-    return {"value": round(positions / dt, 1), "unit": "pair positions/s", "cores": int(threads),
+    total_n3 = sum(int(n) ** 3 for n in run.lengths)
+    est = dt * total_n3 / n3
+    positions = w.blocks * sum(int(n) ** 2 for n in run.lengths)
+    return {"value": round(positions / est, 1), "unit": "pair positions/s", "cores": int(threads),
             "kind": "oracle",
-            "sample": f"samples {', '.join(done)} of the batch ({positions} pair positions), one pass of the block "
-                      f"({w.blocks} block(s)) each in float64 NumPy, {dt:.1f} s; host has {os.cpu_count()} CPUs"}
+            "sample": f"samples {', '.join(done)} of the batch, every block in float64 NumPy, {dt:.1f} s; "
+                      f"they hold {n3 / total_n3:.1%} of the batch's sum N^3, so the whole batch is estimated at "
+                      f"{est:.1f} s ({positions} pair positions over {w.blocks} block(s)); "
+                      f"host has {os.cpu_count()} CPUs"}
 
 
 def bench_single_attention(args, w):
@@ -246,14 +269,133 @@ def bench_single_attention(args, w):
     print(json.dumps(line), flush=True)
 
 
+def _pct(xs, q):
+    import numpy as np
+    return round(float(np.percentile(np.asarray(xs), q)), 4)
+
+
+def measure(w, steps: int, warmup: int, graph: bool = False, cpu: bool = False):
+    """Times `steps` steps of workload w; returns the result dict."""
+    import torch
+    from paper_2609_30379_amd import blocks
+    tokens = w.kind != "pair"
+    run = blocks.TokenRun(w) if tokens else blocks.PairRun(w)
+    L = run.lengths
+    R, S = sum(n * n for n in L), sum(L)
+    stream = torch.cuda.current_stream()          # the stream every nt_* call launches on
+
+    for _ in range(max(1, warmup)):
+        ref = [t.clone() for t in run.step() if t is not None]
+    torch.cuda.synchronize()
+
+    # With graph=True the step is captured once into a HIP graph and replayed
+    # in the timed region, after checking that a replay reproduces the eager
+    # step bit for bit (otherwise, and by default, eager steps are timed).
+    g = None
+    if graph:
+        try:
+            gg = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gg):
+                outs = [t for t in run.step() if t is not None]
+            gg.replay()
+            torch.cuda.synchronize()
+            if all(torch.equal(a, b) for a, b in zip(ref, outs)):
+                g = gg
+            else:
+                print("bench.py: graph replay differs from the eager step; timing eager steps", file=sys.stderr)
+        except Exception as e:                       # capture unsupported: time eager steps
+            print(f"bench.py: graph capture failed ({e}); timing eager steps", file=sys.stderr)
+        torch.cuda.synchronize()
+    step = g.replay if g is not None else run.step
+
+    # timed region: events at every step boundary on the launch stream (one
+    # event between steps adds no gap inside a step), wall clock around it
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    evs[0].record(stream)
+    for k in range(steps):
+        step()
+        evs[k + 1].record(stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms = (t1 - t0) * 1e3 / steps
+    warm = [evs[k].elapsed_time(evs[k + 1]) for k in range(steps)]
+
+    # cold steps: a 512 MB write evicts the 256 MB memory-side cache before
+    # each step, outside the step's events
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    cold = []
+    for _ in range(max(3, min(steps, 20))):
+        flush.fill_(1)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        step()
+        b.record(stream)
+        torch.cuda.synchronize()
+        cold.append(a.elapsed_time(b))
+    del flush
+
+    # per-op attribution: eager steps with an event pair around every op on
+    # the launch stream (a captured graph cannot carry timing events)
+    tm = blocks.OpTimer()
+    blocks.timer = tm
+    torch.cuda.synchronize()
+    for _ in range(steps):
+        run.step()
+    torch.cuda.synchronize()
+    blocks.timer = None
+    per_op = tm.summary()                            # {op: (launches, mean us)}
+
+    costs = token_op_costs(w, L) if tokens else op_costs(w, L)
+    total_us = {k: n * us / steps for k, (n, us) in per_op.items()}
+    dominant = max(total_us, key=total_us.get)
+    n_launch, us_launch = per_op[dominant]
+    rl = roofline_for(dominant, costs[dominant][0], costs[dominant][1], us_launch, w.dtype)
+    rl["traffic"] = measured_traffic(dominant, w.name)
+    rl["algorithmic_bytes"] = costs[dominant][0]
+    rl["algorithmic_flops"] = costs[dominant][1]
+    rl["us_per_launch"] = round(us_launch, 2)
+    rl["launches_per_step"] = n_launch // steps
+    kernels = {}
+    for k, (n, us) in per_op.items():
+        r = roofline_for(k, costs[k][0], costs[k][1], us, w.dtype)
+        kernels[k] = {"us": round(us, 2), "launches_per_step": n // steps, "bound": r["bound"],
+                      "frac": r["frac"], "algorithmic_bytes": costs[k][0],
+                      "traffic": measured_traffic(k, w.name)}
+    timing = {"warm_ms": {"median": _pct(warm, 50), "p10": _pct(warm, 10), "p90": _pct(warm, 90)},
+              "cold_ms": {"median": _pct(cold, 50), "p10": _pct(cold, 10), "p90": _pct(cold, 90),
+                          "reps": len(cold)},
+              "op_sum_ms": round(sum(total_us.values()) / 1e3, 4)}
+    if tokens:
+        out = {"metric": "packed tokens/sec per encoder layer (1 MI355X)", "value": round(S / (ms * 1e-3), 1),
+               "unit": "tokens/s",
+               "config": {"workload": w.name, "batch": w.batch, "lengths": L, "sum_n": S, "sum_n2": R,
+                          "c": w.c_s, "heads": w.heads, "head_dim": w.head_dim, "hidden": w.hidden}}
+    else:
+        out = {"metric": METRIC, "value": round(w.blocks * R / (ms * 1e-3), 1), "unit": "pair positions/s",
+               "tokens_per_s": round(w.blocks * S / (ms * 1e-3), 1),
+               "config": {"workload": w.name, "batch": w.batch, "lengths": L, "sum_n": S, "sum_n2": R,
+                          "c_s": w.c_s, "c_z": w.c_z, "heads": w.heads, "head_dim": w.head_dim,
+                          "hidden": w.hidden, "blocks": w.blocks, "steps_per_block": list(w.steps)}}
+    out.update({"ms_per_step": round(ms, 4), "graph": g is not None, "timing": timing, "roofline": rl,
+                "kernels": kernels})
+    if cpu:
+        out["cpu_baseline"] = cpu_baseline_tokens(w, run) if tokens else cpu_baseline(w, run)
+    return out
+
+
+NESTED = ("pair_b8_n208_224_bf16", "pair_b8_n32_512_bf16", "tokens_b64_lognormal230_bf16")
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="pair_b8_n208_224_bf16",
-                    help="default: the B=8 near-uniform pair block; the other workloads are parity cases, "
-                         "timed here on request")
+    ap.add_argument("--workload", default="pairformer4_b16_lognormal192_bf16",
+                    help="headline workload (default: the four-block stack, the largest single-GPU workload)")
+    ap.add_argument("--no-nested", action="store_true", help="time only the headline workload")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--graph", action="store_true", help="time replays of the step captured into a HIP graph")
     ap.add_argument("--kernels", action="store_true", help="also print the per-op breakdown to stderr")
@@ -262,6 +404,10 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device-to-device copy (scale reference for HBM counters)")
     args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this path runs on one GPU; --gpus {args.gpus} is not supported "
+              "(samples are independent, see the sharding notes in the design document)", file=sys.stderr)
+        sys.exit(2)
     if args.copy_calibration:
         import torch
         src = torch.ones(64 << 20, dtype=torch.float32, device="cuda")
@@ -271,116 +417,32 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes_per_launch": src.numel() * 4, "launches": args.steps}), flush=True)
         return
-    if args.gpus != 1:
-        print(f"bench.py: this path runs on one GPU; --gpus {args.gpus} is not supported "
-              "(samples are independent, see the sharding notes in the design document)", file=sys.stderr)
-        sys.exit(2)
 
     import torch
-    from paper_2609_30379_amd import binding, blocks, synth
+    from paper_2609_30379_amd import binding, synth
     binding.load()
     w = synth.WORKLOADS[args.workload]
     torch.cuda.set_device(0)
     if args.op == "single_attention":
         bench_single_attention(args, w)
         return
-    tokens = w.kind != "pair"
-    run = blocks.TokenRun(w) if tokens else blocks.PairRun(w)
-    L = run.lengths
-    R = sum(n * n for n in L)
-
-    for _ in range(max(1, args.warmup)):
-        ref = [t.clone() for t in run.step() if t is not None]
-    torch.cuda.synchronize()
-
-    # With --graph the step is captured once into a HIP graph and replayed in
-    # the timed region, after checking that a replay reproduces the eager step
-    # bit for bit (otherwise, and by default, eager steps are timed).
-    graph = None
-    if args.graph:
-        try:
-            g = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g):
-                outs = [t for t in run.step() if t is not None]
-            g.replay()
-            torch.cuda.synchronize()
-            if all(torch.equal(a, b) for a, b in zip(ref, outs)):
-                graph = g
-            else:
-                print("bench.py: graph replay differs from the eager step; timing eager steps", file=sys.stderr)
-        except Exception as e:                       # capture unsupported: time eager steps
-            print(f"bench.py: graph capture failed ({e}); timing eager steps", file=sys.stderr)
-        torch.cuda.synchronize()
-
-    # timed region: wall clock and events on the launch stream around it (no
-    # per-op events inside: recording them adds gaps between the kernels)
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    ev0.record()
-    for _ in range(args.steps):
-        if graph is not None:
-            graph.replay()
-        else:
-            run.step()
-    ev1.record()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms = (t1 - t0) * 1e3 / args.steps
-    ms_dev = ev0.elapsed_time(ev1) / args.steps
-
-    # per-op attribution: eager steps with an event pair around every op on
-    # the launch stream (a captured graph cannot carry timing events)
-    tm = blocks.OpTimer()
-    blocks.timer = tm
-    torch.cuda.synchronize()
-    te0 = time.perf_counter()
-    for _ in range(args.steps):
-        run.step()
-    torch.cuda.synchronize()
-    te1 = time.perf_counter()
-    blocks.timer = None
-    per_op = tm.summary()                            # {op: (launches, mean us)}
-    ms_eager = (te1 - te0) * 1e3 / args.steps
-
-    costs = token_op_costs(w, L) if tokens else op_costs(w, L)
-    total_us = {k: n * us / args.steps for k, (n, us) in per_op.items()}
-    dominant = max(total_us, key=total_us.get)
-    n_launch, us_launch = per_op[dominant]
-    rl = roofline_for(dominant, costs[dominant][0], costs[dominant][1], us_launch, w.dtype)
-    rl["traffic"] = measured_traffic(dominant, w.name)
-    rl["algorithmic_bytes"] = costs[dominant][0]
-    rl["us_per_launch"] = round(us_launch, 2)
-    kernels = {}
-    for k, (n, us) in per_op.items():
-        r = roofline_for(k, costs[k][0], costs[k][1], us, w.dtype)
-        kernels[k] = {"us": round(us, 2), "launches_per_step": n // args.steps, "bound": r["bound"],
-                      "frac": r["frac"], "algorithmic_bytes": costs[k][0],
-                      "traffic": measured_traffic(k, w.name)}
-
-    if tokens:
-        metric, value, unit = "packed tokens/sec per encoder layer (1 MI355X)", sum(L) / (ms * 1e-3), "tokens/s"
-        config = {"workload": w.name, "batch": w.batch, "lengths": L, "sum_n": sum(L), "sum_n2": R,
-                  "c": w.c_s, "heads": w.heads, "head_dim": w.head_dim, "hidden": w.hidden}
-    else:
-        metric, value, unit = METRIC, w.blocks * R / (ms * 1e-3), "pair positions/s"
-        config = {"workload": w.name, "batch": w.batch, "lengths": L, "sum_n": sum(L), "sum_n2": R,
-                  "c_s": w.c_s, "c_z": w.c_z, "heads": w.heads, "head_dim": w.head_dim, "hidden": w.hidden,
-                  "blocks": w.blocks, "steps_per_block": list(w.steps)}
-    out = {
-        "metric": metric, "value": round(value, 1), "unit": unit,
-        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
-        "device_ms_per_step": round(ms_dev, 4), "graph": graph is not None,
-        "eager_ms_per_step_with_op_events": round(ms_eager, 4),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
-        "config": config,
-        "roofline": rl,
-        "kernels": kernels,
-    }
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline_tokens(w, run) if tokens else cpu_baseline(w, run)
+    head = measure(w, args.steps, args.warmup, args.graph, cpu=not args.no_cpu_baseline)
+    out = {"metric": head.pop("metric"), "value": head.pop("value"), "unit": head.pop("unit"),
+           "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": head.pop("ms_per_step"),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+           "config": head.pop("config")}
+    out.update(head)
+    if not args.no_nested:
+        nested = {}
+        for name in NESTED:
+            if name == w.name:
+                continue
+            r = measure(synth.WORKLOADS[name], args.steps, args.warmup, args.graph, cpu=False)
+            r.pop("kernels")
+            nested[name] = r
+        out["other_workloads"] = nested
     if args.kernels:
-        for k, v in sorted(kernels.items(), key=lambda kv: -kv[1]["us"] * kv[1]["launches_per_step"]):
+        for k, v in sorted(out["kernels"].items(), key=lambda kv: -kv[1]["us"] * kv[1]["launches_per_step"]):
             tr = v["traffic"]
             ratio = f"  traffic/alg {tr / v['algorithmic_bytes']:.2f}" if tr else ""
             print(f"{k:20s} {v['us']:9.2f} us x{v['launches_per_step']}  {v['bound']} frac {v['frac']:.3f}{ratio}",
