@@ -301,6 +301,24 @@ nt_status nt_pair_row_attention(const nt_layout* layout, int32_t axis,
                                 void* o, int64_t ld_o, nt_dtype dtype,
                                 void* workspace, uint64_t workspace_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under graph capture,
+ * tight serving loops, harnesses that forbid allocation): the same operation
+ * and arguments as nt_pair_row_attention without a workspace.  The bias image
+ * goes into a scratch array of 16 MiB that the library holds on each device
+ * it runs on until the process ends (resolved once per device on the first
+ * call there); no call allocates or frees.  A call whose bias image would
+ * exceed 16 MiB (H * T * 512 bytes, see above) returns NT_ERR_UNSUPPORTED
+ * before any work.  Every call on one device shares that device's array, so
+ * calls that overlap in time on one device (different streams, or threads
+ * without ordering) race; calls ordered on one stream are safe.
+ * Errors: as nt_pair_row_attention, plus NT_ERR_UNSUPPORTED (scratch too
+ * small) and NT_ERR_HIP (the array's address cannot be resolved).           */
+nt_status nt_pair_row_attention_noalloc(const nt_layout* layout, int32_t axis,
+                                        int32_t heads, int32_t head_dim,
+                                        const void* q, const void* k, const void* v, int64_t ld_qkv,
+                                        const void* bias, int64_t ld_bias, int64_t ld_bias_head, float scale,
+                                        void* o, int64_t ld_o, nt_dtype dtype, void* stream);
+
 /* Minimum workspace of nt_pair_row_attention for these arguments, in bytes
  * (0: none); has_bias is 0 or 1.
  * Errors: NT_ERR_INVALID_ARG.                                               */

@@ -77,6 +77,7 @@ def load(path: str = LIB_PATH):
         "nt_layernorm_linear_workspace": [C.POINTER(LinearArgs), C.POINTER(u64)],
         "nt_pair_row_attention": [vp, i32, i32, i32, vp, vp, vp, i64, vp, i64, i64, f32, vp, i64, C.c_int, vp, u64, vp],
         "nt_pair_row_attention_workspace": [vp, i32, i32, i32, C.c_int, i32, C.POINTER(u64)],
+        "nt_pair_row_attention_noalloc": [vp, i32, i32, i32, vp, vp, vp, i64, vp, i64, i64, f32, vp, i64, C.c_int, vp],
         "nt_triangle_mul": [vp, i32, i32, vp, vp, i64, C.c_int, vp, i64, C.c_int, vp, u64, vp],
         "nt_triangle_mul_workspace": [vp, i32, C.c_int, C.c_int, C.POINTER(u64)],
         "nt_segment_reduce": [vp, C.c_int, i32, i32, vp, i64, C.c_int, vp, i64, vp],
@@ -250,6 +251,28 @@ def layernorm_linear_workspace_bytes(x_rows: int, c_in: int, c_out: int, dtype: 
     if epilogue == "swiglu_residual" and not residual_is_x:
         a.residual = C.c_void_p(32)
     return _linear_ws_bytes(a)
+
+
+def nt_pair_row_attention_noalloc(layout: NestedLayout, axis: int, heads: int, head_dim: int, q, k, v, o,
+                                  bias=None, scale: float | None = None, bias_layout: str = "cells"):
+    """nt_pair_row_attention without a workspace: the library's per-device
+    scratch array holds the bias image (at most 16 MiB)."""
+    pq, ld = _mat(q, "q")
+    pk, ldk = _mat(k, "k")
+    pv, ldv = _mat(v, "v")
+    if not (ld == ldk == ldv):
+        raise ValueError("q, k and v must share one row stride")
+    po, ldo = _mat(o, "o")
+    if bias is None:
+        pb, ldb, ldbh = None, 0, 0
+    elif bias_layout == "cells":
+        pb, ldb, ldbh = _ptr(bias), int(bias.stride(0)), 1
+    else:
+        pb, ldb, ldbh = _ptr(bias), 1, int(bias.stride(0))
+    scale = 1.0 / float(np.sqrt(head_dim)) if scale is None else float(scale)
+    _check(load().nt_pair_row_attention_noalloc(layout.handle, int(axis), int(heads), int(head_dim), pq, pk, pv, ld,
+                                                pb, ldb, ldbh, scale, po, ldo, _dtype(q), _stream()))
+    return o
 
 
 def attention_workspace_bytes(layout: NestedLayout, axis: int, heads: int, head_dim: int, dtype: str = "bf16",

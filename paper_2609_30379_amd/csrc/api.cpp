@@ -349,6 +349,28 @@ nt_status nt_pair_row_attention(const nt_layout* L, int32_t axis, int32_t H, int
                    "nt_pair_row_attention launch");
 }
 
+nt_status nt_pair_row_attention_noalloc(const nt_layout* L, int32_t axis, int32_t H, int32_t D, const void* q,
+                                        const void* k, const void* v, int64_t ld_qkv, const void* bias,
+                                        int64_t ld_bias, int64_t ld_bias_head, float scale, void* o, int64_t ld_o,
+                                        nt_dtype dtype, void* stream) {
+  g_last_error.clear();
+  if (!L) return nt::fail(NT_ERR_INVALID_ARG, "layout is NULL");
+  if (axis < 0 || axis > 3 || H <= 0 || D <= 0 || !valid_dtype(dtype))
+    return nt::fail(NT_ERR_INVALID_ARG, "bad axis, heads, head_dim or dtype");
+  const size_t need = nt::attention_workspace_bytes(*L, axis, H, D, dtype, bias != nullptr);
+  if (need > nt::kNoAllocScratchBytes)
+    return nt::fail(NT_ERR_UNSUPPORTED, "this call needs " + std::to_string(need) + " bytes of scratch; the "
+                                        "allocation-free entry point holds " + std::to_string(nt::kNoAllocScratchBytes) +
+                                        " (use nt_pair_row_attention with a workspace)");
+  void* ws = nullptr;
+  if (need > 0) {
+    if (nt_status st = need_device(L)) return st;
+    if (nt_status st = check_hip(nt::noalloc_scratch(&ws), "scratch address lookup")) return st;
+  }
+  return nt_pair_row_attention(L, axis, H, D, q, k, v, ld_qkv, bias, ld_bias, ld_bias_head, scale, o, ld_o, dtype,
+                               ws, need, stream);
+}
+
 nt_status nt_pair_row_attention_workspace(const nt_layout* L, int32_t axis, int32_t H, int32_t D, nt_dtype dtype,
                                           int32_t has_bias, uint64_t* bytes) {
   g_last_error.clear();

@@ -12,6 +12,8 @@
 #include <algorithm>
 #include <type_traits>
 
+#include <mutex>
+
 #include "nt_device.h"
 #include "nt_internal.h"
 
@@ -865,6 +867,31 @@ __global__ void __launch_bounds__(256) attention_f32_kernel(AttnF32Args p) {
 }
 
 }  // namespace
+
+// ---------------------------------------------------------------- allocation-free scratch
+// Scratch of nt_pair_row_attention_noalloc: one array per device, resolved to
+// its device address once per device on first use.  Host code never passes
+// the array's name to a kernel, only the resolved address.
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+hipError_t noalloc_scratch(void** ptr) {
+  static std::mutex mu;
+  static void* addr[64] = {nullptr};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
+}
 
 size_t attention_workspace_bytes(const nt_layout& L, int axis, int H, int D, nt_dtype dtype, bool has_bias) {
   // only the d = 32 pair kernel (N <= 512) reads the bias through an image

@@ -156,6 +156,13 @@ size_t linear_workspace_bytes(const nt_linear_args& a);
 // a.workspace must hold linear_workspace_bytes(a) bytes (checked by the caller).
 hipError_t launch_linear(const LinearPlan& p, hipStream_t s);
 
+// Allocation-free attention (nt_pair_row_attention_noalloc): its scratch is a
+// file-scope device array of this many bytes, one per device.
+constexpr size_t kNoAllocScratchBytes = size_t(16) << 20;
+// Device address of the calling thread's current device's array (looked up
+// once per device).
+hipError_t noalloc_scratch(void** ptr);
+
 // Bias-image bytes of a pair attention call (0: none).
 size_t attention_workspace_bytes(const nt_layout& L, int axis, int H, int D, nt_dtype dtype, bool has_bias);
 // bias element (cell c, head h) at bias[c * ld_bias + h * ld_bias_head];
