@@ -9,6 +9,8 @@ from oracle import layout
 from tests import test_oracle_ops as T_ops
 from tests import test_oracle_blocks as T_blk
 from tests import test_oracle_layout as T_lay
+from tests import test_oracle_grads as T_grads
+import oracle.grads as grads
 
 
 def _fails(fn, *a, **k):
@@ -77,6 +79,36 @@ def _mut_pair_offsets(lengths):
     return layout.offsets([int(n) * int(n) + (1 if i == 0 else 0) for i, n in enumerate(lengths)])
 
 
+def _mut_triangle_bwd_transposed(a, b, dt, lengths, direction="outgoing"):
+    # uses dT^T where dT belongs (and the reverse)
+    tr = np.concatenate([blk.transpose(1, 0, 2).reshape(-1, blk.shape[2])
+                         for blk in layout.unpack(np.asarray(dt, np.float64), layout.pair_offsets(lengths),
+                                                  [(n, n) for n in lengths])]) if len(dt) else dt
+    return _orig_g["triangle_mul_backward"](a, b, tr, lengths, direction)
+
+
+def _mut_ln_bwd_no_mean(x, gamma, dy, eps=1e-5):
+    x, dy = np.asarray(x, np.float64), np.asarray(dy, np.float64)
+    mu = x.mean(-1, keepdims=True)
+    rstd = 1 / np.sqrt(((x - mu) ** 2).mean(-1, keepdims=True) + eps)
+    xhat = (x - mu) * rstd
+    g = dy * gamma
+    return rstd * (g - xhat * (g * xhat).mean(-1, keepdims=True)), (dy * xhat).sum(0), dy.sum(0)
+
+
+def _mut_attn_bwd_no_bias_grad_sum(q, k, v, bias, do, lengths, heads, head_dim, axis=0, scale=None):
+    dq, dk, dv, db = _orig_g["pair_row_attention_backward"](q, k, v, bias, do, lengths, heads, head_dim, axis, scale)
+    return dq, dk, dv, (None if db is None else db / max(1, max(lengths)))
+
+
+def _mut_broadcast_bwd_swapped(dz, lengths):
+    du, dv = _orig_g["pair_broadcast_backward"](dz, lengths)
+    return dv, du
+
+
+_orig_g = {k: getattr(grads, k) for k in ("triangle_mul_backward", "layernorm_backward",
+                                          "pair_row_attention_backward", "pair_broadcast_backward")}
+
 _orig = {k: getattr(ops, k) for k in ("pair_broadcast", "pair_row_attention", "triangle_mul", "segment_reduce",
                                         "single_attention_pair_bias")}
 
@@ -101,6 +133,14 @@ MUTANTS = [
      [(T_ops.test_pair_column_sum_equation, ())]),
     ("pair_offsets_off_by_one", layout, "pair_offsets", _mut_pair_offsets,
      [(T_lay.test_worked_example_offsets_and_splits, ())]),
+    ("triangle_backward_transposed_cotangent", grads, "triangle_mul_backward", _mut_triangle_bwd_transposed,
+     [(T_grads.test_triangle_backward_finite_differences_and_autograd, ("outgoing", None))]),
+    ("layernorm_backward_without_mean_term", grads, "layernorm_backward", _mut_ln_bwd_no_mean,
+     [(T_grads.test_layernorm_backward_matches_torch_autograd, (None,))]),
+    ("attention_backward_bias_gradient_averaged", grads, "pair_row_attention_backward", _mut_attn_bwd_no_bias_grad_sum,
+     [(T_grads.test_attention_backward_finite_differences, (0, True))]),
+    ("broadcast_backward_swapped", grads, "pair_broadcast_backward", _mut_broadcast_bwd_swapped,
+     [(T_grads.test_broadcast_backward_finite_differences_and_sums, ())]),
 ]
 
 
