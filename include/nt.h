@@ -85,7 +85,11 @@ typedef enum {
   NT_EPI_GELU = 3              /* y = gelu(LN(x) W^T + b), exact erf form            */
 } nt_epilogue;
 
-typedef enum { NT_LEVEL_SINGLES = 0, NT_LEVEL_PAIRS = 1 } nt_level;
+typedef enum {
+  NT_LEVEL_SINGLES = 0,        /* complete reduction within each sample's rows      */
+  NT_LEVEL_PAIRS = 1,          /* over the second pair axis (pair columns b)        */
+  NT_LEVEL_PAIRS_FIRST = 2     /* over the first pair axis (pair rows a)            */
+} nt_level;
 
 /* Operand layout of the triangle update (nt_triangle_mul). */
 typedef enum {
@@ -363,6 +367,9 @@ nt_status nt_triangle_mul_workspace(const nt_layout* layout, int32_t C, nt_tri_o
  * output, one launch, no atomics:
  *   level NT_LEVEL_PAIRS   (pair columns, Eq. pair-reduction)
  *       y[eta_i + a, c] = sum_b x[o_i + a N_i + b, c]     (op 1: / N_i)
+ *   level NT_LEVEL_PAIRS_FIRST (the other pair axis; the broadcast's
+ *       gradient with respect to its column operand)
+ *       y[eta_i + b, c] = sum_a x[o_i + a N_i + b, c]     (op 1: / N_i)
  *   level NT_LEVEL_SINGLES (complete reduction within each element, Appendix A)
  *       y[i, c] = sum_t x[eta_i + t, c]                    (op 1: / N_i;
  *       an empty sample gives 0 for the sum and NaN for the mean)
@@ -372,6 +379,131 @@ nt_status nt_triangle_mul_workspace(const nt_layout* layout, int32_t C, nt_tri_o
 nt_status nt_segment_reduce(const nt_layout* layout, nt_level level, int32_t op, int32_t C,
                             const void* x, int64_t ld_x, nt_dtype x_dtype,
                             float* y, int64_t ld_y, void* stream);
+
+/* ---------------------------------------------------------------- backward
+ * Gradients of the calls above for a training step (forward, loss and
+ * backward through the packed representation, Sec. 3.4 "Gradients across
+ * representations"): every gradient has the packed layout of its value.    */
+
+/* Backward of nt_pair_broadcast (z = u_a + v_b):
+ *   du[eta_i + a, c] (+)= sum_b dz[o_i + a N_i + b, c]
+ *   dv[eta_i + b, c] (+)= sum_a dz[o_i + a N_i + b, c]
+ * dz [sum N^2, C] (dtype, row stride ld_dz); du, dv fp32 [sum N, C] with row
+ * strides ld_du, ld_dv (multiples of 4); accumulate 0 overwrites, 1 adds.
+ * Either of du, dv may be NULL (not computed).  fp32 accumulation, no atomics.
+ * Errors: NT_ERR_INVALID_ARG.                                                */
+nt_status nt_pair_broadcast_backward(const nt_layout* layout, int32_t C, const void* dz, int64_t ld_dz,
+                                     nt_dtype dtype, float* du, int64_t ld_du, float* dv, int64_t ld_dv,
+                                     int32_t accumulate, void* stream);
+
+/* Backward of nt_segment_reduce: every reduced position receives its group's
+ * gradient dy (fp32, the reduce's output layout, row stride ld_dy), divided
+ * by N_i for op 1 (mean):
+ *   NT_LEVEL_PAIRS        dx[o_i + a N_i + b] (+)= dy[eta_i + a] (/ N_i)
+ *   NT_LEVEL_PAIRS_FIRST  dx[o_i + a N_i + b] (+)= dy[eta_i + b] (/ N_i)
+ *   NT_LEVEL_SINGLES      dx[eta_i + t]       (+)= dy[i]        (/ N_i)
+ * dx in dtype with row stride ld_dx; accumulate 0 overwrites, 1 adds.
+ * Errors: NT_ERR_INVALID_ARG.                                                */
+nt_status nt_segment_reduce_backward(const nt_layout* layout, nt_level level, int32_t op, int32_t C,
+                                     const float* dy, int64_t ld_dy, void* dx, int64_t ld_dx, nt_dtype dtype,
+                                     int32_t accumulate, void* stream);
+
+/* Backward of nt_triangle_mul on packed operands (a, b: [sum N^2, C], row
+ * stride ld_ab), for the cotangent dt of the update t (dt: [sum N^2, C], row
+ * stride ld_dt), per sample and channel c:
+ *   direction 0  t = a b^T:   da += dt b,     db += dt^T a
+ *   direction 1  t = a^T b:   da += b dt^T,   db += a dt
+ * (a, b, dt read as each sample's N_i x N_i channel planes).  da and db
+ * (row stride ld_dab; either may be NULL) are accumulated in their dtype,
+ * fp32 sums rounded once per call.  Workspace: the same as the forward on
+ * packed operands (nt_triangle_mul_workspace with NT_TRI_PACKED).
+ * Errors: as nt_triangle_mul.                                                */
+nt_status nt_triangle_mul_backward(const nt_layout* layout, int32_t direction, int32_t C,
+                                   const void* a, const void* b, int64_t ld_ab, const void* dt, int64_t ld_dt,
+                                   void* da, void* db, int64_t ld_dab, nt_dtype dtype,
+                                   void* workspace, uint64_t workspace_bytes, void* stream);
+
+/* Backward of nt_pair_row_attention on axes 0 and 1 (bf16, head_dim 32,
+ * N_i <= 512).  Inputs are the forward's q, k, v (row stride ld_qkv), its
+ * bias (as in the forward, or NULL), the output's gradient dout (ld_dout)
+ * and the softmax scale; the softmax is recomputed.  Per pair row r and head
+ * h, with S = scale q k^T + bias and P = softmax_k(S):
+ *   dS = P (dP - rowsum(P dP)), dP = dout v^T,  dq = scale dS k,  dk = scale dS^T q,
+ *   dv = P^T dout,  dbias = sum over the pair rows r of dS
+ * (axis 1 on each sample's transpose, the bias gradient transposed back).
+ * dq, dk, dv: bf16 [sum N^2, H*d] with row stride ld_dqkv, overwritten;
+ * dbias: fp32, head h of cell c at dbias[c * ld_dbias + h * ld_dbias_head],
+ * overwritten (NULL: not computed).  fp32 arithmetic, no atomics.
+ * Workspace: 8 * H * sum N^2 bytes (the softmax statistics of every query),
+ * nt_pair_row_attention_backward_workspace.
+ * Errors: NT_ERR_INVALID_ARG, NT_ERR_UNSUPPORTED (axis, dtype, head_dim,
+ * N_i > 512).                                                                */
+nt_status nt_pair_row_attention_backward(const nt_layout* layout, int32_t axis, int32_t heads, int32_t head_dim,
+                                         const void* q, const void* k, const void* v, int64_t ld_qkv,
+                                         const void* bias, int64_t ld_bias, int64_t ld_bias_head,
+                                         const void* dout, int64_t ld_dout, float scale,
+                                         void* dq, void* dk, void* dv, int64_t ld_dqkv,
+                                         float* dbias, int64_t ld_dbias, int64_t ld_dbias_head,
+                                         nt_dtype dtype, void* workspace, uint64_t workspace_bytes, void* stream);
+nt_status nt_pair_row_attention_backward_workspace(const nt_layout* layout, int32_t axis, int32_t heads,
+                                                   int32_t head_dim, nt_dtype dtype, uint64_t* bytes);
+
+/* Backward of nt_layernorm_linear (rows of a packed tensor, any level):
+ *   y = epilogue(LN(x) W^T + b)
+ * Given dy = dL/dy it adds the gradients of the weights and writes dx:
+ *   NONE / RESIDUAL   p = LN(x) W^T + b, dp = dy (the residual's gradient is
+ *                     dy itself; the caller adds it where it belongs)
+ *   GELU              dp = dy gelu'(p), p recomputed from x
+ *   SWIGLU_RESIDUAL   [g|u] = LN(x) W^T + b recomputed, h = silu(g) u,
+ *                     dW2 += dy^T h, db2 += sum dy, dh = dy W2,
+ *                     dp = [dh u silu'(g) | dh silu(g)]; with residual_is_x
+ *                     (the forward's residual was x) dx also receives dy
+ *   dW += dp^T LN(x),  db += sum_rows dp,  d(LN x) = dp W, then through the
+ *   LayerNorm: dx = rstd (g - mean(g) - xhat mean(g xhat)), g = d(LN x) gamma,
+ *   dgamma += sum_rows d(LN x) xhat,  dbeta += sum_rows d(LN x).
+ * bf16 weights and dy; products on matrix cores with fp32 accumulation; the
+ * normalised rows and the recomputed hidden are rounded to bf16 as the
+ * forward consumed them.  Weight gradients (dw, db, dgamma, dbeta, dw2, db2:
+ * fp32, contiguous, NULL = not wanted) are accumulated; dx (x_dtype or fp32)
+ * is overwritten unless accumulate_dx.  Partial sums are reduced in a fixed
+ * order: the result is deterministic.                                        */
+typedef struct {
+  int64_t rows;                /* R                                              */
+  int32_t c_in;                /* K (multiple of 8, <= 1024)                      */
+  int32_t c_out;               /* N: width of y (SwiGLU: the residual width)      */
+  const void* x;               /* forward input [R, K], row stride ldx            */
+  int64_t ldx;
+  nt_dtype x_dtype;            /* bf16 or fp32                                   */
+  const float* ln_gamma;       /* [K] or NULL (no LayerNorm)                      */
+  const float* ln_beta;        /* [K] or NULL                                    */
+  float ln_eps;
+  const void* w;               /* bf16 [N_w, K] contiguous, N_w = N or 2F          */
+  const float* bias;           /* [N_w] or NULL (needed to recompute GELU / SwiGLU) */
+  nt_epilogue epilogue;
+  int32_t hidden;              /* F for SwiGLU                                   */
+  const void* w2;              /* SwiGLU: bf16 [N, F] contiguous                  */
+  int32_t residual_is_x;       /* SwiGLU: the residual was x                      */
+  const void* dy;              /* bf16 [R, N], row stride ld_dy                   */
+  int64_t ld_dy;
+  void* dx;                    /* [R, K] in dx_dtype, row stride ld_dx, or NULL    */
+  int64_t ld_dx;
+  nt_dtype dx_dtype;
+  int32_t accumulate_dx;
+  float* dw;                   /* [N_w, K]  */
+  float* db;                   /* [N_w]     */
+  float* dgamma;               /* [K]       */
+  float* dbeta;                /* [K]       */
+  float* dw2;                  /* [N, F]    */
+  float* db2;                  /* [N]       */
+  void* workspace;             /* nt_layernorm_linear_backward_workspace bytes    */
+  uint64_t workspace_bytes;
+} nt_linear_bwd_args;
+
+/* Errors: NT_ERR_INVALID_ARG (also a missing or too small workspace),
+ * NT_ERR_UNSUPPORTED (fp32 weights, K > 1024, no LayerNorm with a bf16 dx
+ * that accumulates), NT_ERR_HIP.                                             */
+nt_status nt_layernorm_linear_backward(const nt_linear_bwd_args* args, void* stream);
+nt_status nt_layernorm_linear_backward_workspace(const nt_linear_bwd_args* args, uint64_t* bytes);
 
 /* Thread-local description of the last error on this thread. */
 const char* nt_last_error(void);

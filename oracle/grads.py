@@ -160,12 +160,15 @@ def layernorm_linear_backward(x, w, b, dy, ln=None, eps=LN_EPS, epilogue="none",
 
 
 # ----------------------------------------------------------------- attention
-def _attention_rows_backward(Q, K, V, Bm, dO, scale):
+def _attention_rows_backward(Q, K, V, Bm, dO, scale, Os=None):
     """One sample, starting-node form (ops._row_attention_sample): Q, K, V, dO
     [N, N, H, d], Bm [N, N, H] or None.  For every pair row r and head h:
       S = scale Q_r K_r^T + B,  P = softmax_k(S),  O_r = P V_r
-      dV_r = P^T dO_r,  dP = dO_r V_r^T,  dS = P * (dP - rowsum(dP * P)),
-      dQ_r = scale dS K_r,  dK_r = scale dS^T Q_r,  dB += dS (summed over r)."""
+      dV_r = P^T dO_r,  dP = dO_r V_r^T,  dS = P * (dP - D),
+      D = rowsum(dP * P) = rowsum(dO_r * O_r),
+      dQ_r = scale dS K_r,  dK_r = scale dS^T Q_r,  dB += dS (summed over r).
+    Os: the forward output as stored ([N, N, H, d]); when given, D is taken
+    from it (rowsum(dO * O)), as a backward that reads the stored output does."""
     N, _, H, d = Q.shape
     dQ, dK, dV = np.zeros_like(Q), np.zeros_like(K), np.zeros_like(V)
     dB = np.zeros((N, N, H))
@@ -178,30 +181,36 @@ def _attention_rows_backward(Q, K, V, Bm, dO, scale):
             g = dO[r, :, h, :]
             dV[r, :, h, :] = P.T @ g
             dP = g @ V[r, :, h, :].T
-            dS = P * (dP - (dP * P).sum(axis=-1, keepdims=True))
+            D = (dP * P).sum(axis=-1, keepdims=True) if Os is None else (g * Os[r, :, h, :]).sum(-1, keepdims=True)
+            dS = P * (dP - D)
             dQ[r, :, h, :] = scale * (dS @ K[r, :, h, :])
             dK[r, :, h, :] = scale * (dS.T @ Q[r, :, h, :])
             dB[:, :, h] += dS
     return dQ, dK, dV, dB
 
 
-def pair_row_attention_backward(q, k, v, bias, do, lengths, heads, head_dim, axis=0, scale=None):
+def pair_row_attention_backward(q, k, v, bias, do, lengths, heads, head_dim, axis=0, scale=None, o=None):
     """Backward of ops.pair_row_attention.  Returns (dq, dk, dv, dbias) in the
     packed layouts of q, k, v ([sum N^2, H*d]) and of the bias ([sum N^2, H];
     None without a bias).  Axis 1 is axis 0 on each sample's transpose, so its
-    gradients are transposed back the same way."""
+    gradients are transposed back the same way.  o: the stored forward output
+    (e.g. rounded to bf16), from which D = rowsum(do * o) is taken; None uses
+    the exact softmax."""
     H, d = int(heads), int(head_dim)
     scale = 1.0 / np.sqrt(d) if scale is None else float(scale)
     Qs, Ks, Vs, Gs = (_pair_elements(t, lengths) for t in (q, k, v, do))
     Bs = _pair_elements(bias, lengths) if bias is not None else [None] * len(lengths)
+    Os = _pair_elements(o, lengths) if o is not None else [None] * len(lengths)
     outs = ([], [], [], [])
-    for Q, K, V, G, Bm in zip(Qs, Ks, Vs, Gs, Bs):
+    for Q, K, V, G, Bm, Om in zip(Qs, Ks, Vs, Gs, Bs, Os):
         N = Q.shape[0]
         Q, K, V, G = (t.reshape(N, N, H, d) for t in (Q, K, V, G))
+        Om = None if Om is None else Om.reshape(N, N, H, d)
         if axis == 1:
             Q, K, V, G = (t.transpose(1, 0, 2, 3) for t in (Q, K, V, G))
+            Om = None if Om is None else Om.transpose(1, 0, 2, 3)
             Bm = None if Bm is None else Bm.transpose(1, 0, 2)
-        dQ, dK, dV, dB = _attention_rows_backward(Q, K, V, Bm, G, scale)
+        dQ, dK, dV, dB = _attention_rows_backward(Q, K, V, Bm, G, scale, Om)
         if axis == 1:
             dQ, dK, dV = (t.transpose(1, 0, 2, 3) for t in (dQ, dK, dV))
             dB = dB.transpose(1, 0, 2)

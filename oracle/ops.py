@@ -210,6 +210,9 @@ def segment_reduce(x, lengths, level="pair_cols", op="sum"):
 
     level "pair_cols": Eq. pair-reduction, V_Y[eta_i + a] = sum_b V_P[o_i + a N_i + b];
         "mean" divides each group by N_i (Eq. running-block, third line).
+    level "pair_rows": the same over the other pair axis,
+        V_Y[eta_i + b] = sum_a V_P[o_i + a N_i + b] (the broadcast's gradient
+        with respect to its column operand).
     level "samples":   complete reduction within each single-axis element,
         y_i = sum_t X_i[t] (Appendix A: sum(dim=0) of [1,2] and [3,4] is [3,7]);
         "mean" divides by N_i.  An empty element sums to 0 and its mean is NaN,
@@ -218,10 +221,10 @@ def segment_reduce(x, lengths, level="pair_cols", op="sum"):
     if op not in ("sum", "mean"):
         raise ValueError(op)
     outs = []
-    if level == "pair_cols":
+    if level in ("pair_cols", "pair_rows"):
         for P in _pair_elements(x, lengths):
             N = P.shape[0]
-            Y = P.sum(axis=1)
+            Y = P.sum(axis=1 if level == "pair_cols" else 0)
             outs.append(Y / N if (op == "mean" and N) else Y)
         C = _f64(x).shape[1]
         return layout.pack(outs, (C,))

@@ -19,7 +19,7 @@ NT_OK, NT_ERR_INVALID_ARG, NT_ERR_LAYOUT_MISMATCH, NT_ERR_OVERFLOW, NT_ERR_UNSUP
     0, -1, -2, -3, -4, -5, -6
 NT_F32, NT_BF16 = 0, 1
 EPILOGUES = {"none": 0, "residual": 1, "swiglu_residual": 2, "gelu": 3}
-LEVELS = {"singles": 0, "pairs": 1}
+LEVELS = {"singles": 0, "pairs": 1, "pairs_first": 2}
 TAILS = {"channel_major": 0, "pair_tiled": 1, "pair_tiled_t": 2}
 TRI_OPERANDS = {"packed": 0, "pair_tiled": 1, "pair_tiled_t": 2}
 ARRAYS = {"lengths": 0, "cu_seqlens": 1, "cu_pairs": 2, "row_splits2": 3, "row_sample": 4,
@@ -37,6 +37,19 @@ class LayoutInfo(C.Structure):
     _fields_ = [("batch", C.c_int32), ("max_len", C.c_int32), ("sum_n", C.c_int64), ("sum_n2", C.c_int64),
                 ("sum_n3", C.c_int64), ("sum_pad", C.c_int64), ("d_cu_seqlens", C.c_void_p),
                 ("d_cu_pairs", C.c_void_p), ("d_row_splits2", C.c_void_p)]
+
+
+class LinearBwdArgs(C.Structure):
+    _fields_ = [("rows", C.c_int64), ("c_in", C.c_int32), ("c_out", C.c_int32),
+                ("x", C.c_void_p), ("ldx", C.c_int64), ("x_dtype", C.c_int),
+                ("ln_gamma", C.c_void_p), ("ln_beta", C.c_void_p), ("ln_eps", C.c_float),
+                ("w", C.c_void_p), ("bias", C.c_void_p), ("epilogue", C.c_int),
+                ("hidden", C.c_int32), ("w2", C.c_void_p), ("residual_is_x", C.c_int32),
+                ("dy", C.c_void_p), ("ld_dy", C.c_int64),
+                ("dx", C.c_void_p), ("ld_dx", C.c_int64), ("dx_dtype", C.c_int), ("accumulate_dx", C.c_int32),
+                ("dw", C.c_void_p), ("db", C.c_void_p), ("dgamma", C.c_void_p), ("dbeta", C.c_void_p),
+                ("dw2", C.c_void_p), ("db2", C.c_void_p),
+                ("workspace", C.c_void_p), ("workspace_bytes", C.c_uint64)]
 
 
 class LinearArgs(C.Structure):
@@ -81,6 +94,14 @@ def load(path: str = LIB_PATH):
         "nt_triangle_mul": [vp, i32, i32, vp, vp, i64, C.c_int, vp, i64, C.c_int, vp, u64, vp],
         "nt_triangle_mul_workspace": [vp, i32, C.c_int, C.c_int, C.POINTER(u64)],
         "nt_segment_reduce": [vp, C.c_int, i32, i32, vp, i64, C.c_int, vp, i64, vp],
+        "nt_pair_broadcast_backward": [vp, i32, vp, i64, C.c_int, vp, i64, vp, i64, i32, vp],
+        "nt_segment_reduce_backward": [vp, C.c_int, i32, i32, vp, i64, vp, i64, C.c_int, i32, vp],
+        "nt_triangle_mul_backward": [vp, i32, i32, vp, vp, i64, vp, i64, vp, vp, i64, C.c_int, vp, u64, vp],
+        "nt_layernorm_linear_backward": [C.POINTER(LinearBwdArgs), vp],
+        "nt_layernorm_linear_backward_workspace": [C.POINTER(LinearBwdArgs), C.POINTER(u64)],
+        "nt_pair_row_attention_backward": [vp, i32, i32, i32, vp, vp, vp, i64, vp, i64, i64, vp, i64, f32,
+                                           vp, vp, vp, i64, vp, i64, i64, C.c_int, vp, u64, vp],
+        "nt_pair_row_attention_backward_workspace": [vp, i32, i32, i32, C.c_int, C.POINTER(u64)],
         "nt_last_error": [],
         "nt_version": [],
     }
@@ -351,6 +372,125 @@ def nt_segment_reduce(layout: NestedLayout, level: str, op: str, x, y):
     _check(load().nt_segment_reduce(layout.handle, LEVELS[level], {"sum": 0, "mean": 1}[op], int(x.size(1)),
                                     px, ldx, _dtype(x), py, ldy, _stream()))
     return y
+
+
+# ---------------------------------------------------------------- backward
+def nt_pair_broadcast_backward(layout: NestedLayout, dz, du=None, dv=None, accumulate: bool = False):
+    """du[eta_i + a] = sum_b dz[a, b], dv[eta_i + b] = sum_a dz[a, b] (fp32 outputs)."""
+    pz, ldz = _mat(dz, "dz")
+    pu, ldu = _mat(du, "du") if du is not None else (None, int(dz.size(1)))
+    pv, ldv = _mat(dv, "dv") if dv is not None else (None, int(dz.size(1)))
+    _check(load().nt_pair_broadcast_backward(layout.handle, int(dz.size(1)), pz, ldz, _dtype(dz), pu, ldu, pv, ldv,
+                                             int(accumulate), _stream()))
+    return du, dv
+
+
+def nt_segment_reduce_backward(layout: NestedLayout, level: str, op: str, dy, dx, accumulate: bool = False):
+    py, ldy = _mat(dy, "dy")
+    px, ldx = _mat(dx, "dx")
+    _check(load().nt_segment_reduce_backward(layout.handle, LEVELS[level], {"sum": 0, "mean": 1}[op], int(dx.size(1)),
+                                             py, ldy, px, ldx, _dtype(dx), int(accumulate), _stream()))
+    return dx
+
+
+def nt_triangle_mul_backward(layout: NestedLayout, direction: int, a, b, dt, da=None, db=None, workspace=None):
+    """Packed operands [sum N^2, C]; da, db accumulate (either may be None)."""
+    pa, lda = _mat(a, "a")
+    pb, ldb = _mat(b, "b")
+    if lda != ldb:
+        raise ValueError("a and b must share one row stride")
+    pt, ldt = _mat(dt, "dt")
+    pda, ldda = _mat(da, "da") if da is not None else (None, 0)
+    pdb, lddb = _mat(db, "db") if db is not None else (None, 0)
+    if da is not None and db is not None and ldda != lddb:
+        raise ValueError("da and db must share one row stride")
+    ld_dab = ldda if da is not None else (lddb if db is not None else int(dt.size(1)))
+    Cz = int(dt.size(1))
+    dt_ = "bf16" if _dtype(dt) == NT_BF16 else "f32"
+    if workspace is None:
+        workspace = workspace_tensor(triangle_workspace_bytes(layout, Cz, "packed", dt_))
+    pw, nw = _ws(workspace)
+    _check(load().nt_triangle_mul_backward(layout.handle, int(direction), Cz, pa, pb, lda, pt, ldt, pda, pdb, ld_dab,
+                                           _dtype(dt), pw, nw, _stream()))
+    return da, db
+
+
+def nt_layernorm_linear_backward(x, w, dy, ln=None, eps: float = 1e-5, bias=None, epilogue: str = "none",
+                                 w2=None, hidden: int = 0, residual_is_x: bool = True, dx=None,
+                                 accumulate_dx: bool = False, dw=None, db=None, dgamma=None, dbeta=None, dw2=None,
+                                 db2=None, workspace=None):
+    """Gradients of y = epilogue(LN(x) W^T + b) given dy; weight gradients (fp32)
+    accumulate, dx is overwritten unless accumulate_dx."""
+    a = LinearBwdArgs()
+    px, ldx = _mat(x, "x")
+    a.rows, a.c_in = int(x.size(0)), int(x.size(1))
+    a.c_out = int(dy.size(1))
+    a.x, a.ldx, a.x_dtype = px, ldx, _dtype(x)
+    if ln is not None:
+        a.ln_gamma, a.ln_beta = _ptr(ln[0]), _ptr(ln[1])
+    a.ln_eps = eps
+    a.w, a.bias, a.epilogue = _ptr(w), _ptr(bias), EPILOGUES[epilogue]
+    a.hidden, a.w2, a.residual_is_x = int(hidden), _ptr(w2), int(bool(residual_is_x))
+    a.dy, a.ld_dy = _mat(dy, "dy")
+    if dx is not None:
+        a.dx, a.ld_dx = _mat(dx, "dx")
+        a.dx_dtype = _dtype(dx)
+    else:
+        a.dx, a.ld_dx, a.dx_dtype = None, a.c_in, NT_BF16
+    a.accumulate_dx = int(bool(accumulate_dx))
+    a.dw, a.db, a.dgamma, a.dbeta = _ptr(dw), _ptr(db), _ptr(dgamma), _ptr(dbeta)
+    a.dw2, a.db2 = _ptr(dw2), _ptr(db2)
+    if workspace is None:
+        n = C.c_uint64()
+        _check(load().nt_layernorm_linear_backward_workspace(C.byref(a), C.byref(n)))
+        workspace = workspace_tensor(int(n.value))
+    a.workspace, a.workspace_bytes = _ws(workspace)
+    _check(load().nt_layernorm_linear_backward(C.byref(a), _stream()))
+    return dx
+
+
+def attention_backward_workspace_bytes(layout: NestedLayout, axis: int, heads: int, head_dim: int,
+                                       dtype: str = "bf16") -> int:
+    n = C.c_uint64()
+    _check(load().nt_pair_row_attention_backward_workspace(layout.handle, int(axis), int(heads), int(head_dim),
+                                                           NT_BF16 if dtype == "bf16" else NT_F32, C.byref(n)))
+    return int(n.value)
+
+
+def nt_pair_row_attention_backward(layout: NestedLayout, axis: int, heads: int, head_dim: int, q, k, v, dout,
+                                   dq, dk, dv, bias=None, dbias=None, scale: float | None = None,
+                                   bias_layout: str = "cells", workspace=None):
+    """dq, dk, dv (bf16, one row stride) overwritten; dbias fp32 [sum N^2, H]
+    (bias_layout "cells") or [H, ld] ("heads"), overwritten."""
+    pq, ld = _mat(q, "q")
+    pk, ldk = _mat(k, "k")
+    pv, ldv = _mat(v, "v")
+    if not (ld == ldk == ldv):
+        raise ValueError("q, k and v must share one row stride")
+    pg, ldg = _mat(dout, "dout")
+    pdq, ldd = _mat(dq, "dq")
+    pdk, ldk2 = _mat(dk, "dk")
+    pdv, ldv2 = _mat(dv, "dv")
+    if not (ldd == ldk2 == ldv2):
+        raise ValueError("dq, dk and dv must share one row stride")
+
+    def strides(t):
+        if t is None:
+            return None, 0, 0
+        if bias_layout == "cells":
+            return _ptr(t), int(t.stride(0)), 1
+        return _ptr(t), 1, int(t.stride(0))
+
+    pb, ldb, ldbh = strides(bias)
+    pdb, lddb, lddbh = strides(dbias)
+    scale = 1.0 / float(np.sqrt(head_dim)) if scale is None else float(scale)
+    if workspace is None:
+        workspace = workspace_tensor(attention_backward_workspace_bytes(layout, axis, heads, head_dim))
+    pw, nw = _ws(workspace)
+    _check(load().nt_pair_row_attention_backward(layout.handle, int(axis), int(heads), int(head_dim), pq, pk, pv, ld,
+                                                 pb, ldb, ldbh, pg, ldg, scale, pdq, pdk, pdv, ldd,
+                                                 pdb, lddb, lddbh, _dtype(q), pw, nw, _stream()))
+    return dq, dk, dv, dbias
 
 
 def version() -> str:

@@ -55,6 +55,7 @@ nt_status upload(nt_layout* L, hipStream_t s) {
       {&L->pattn_work, &L->d_pattn_work}, {&L->bias_tiles, &L->d_bias_tiles},
       {&L->sattn_work, &L->d_sattn_work},
       {&L->bc_cu_tiles, &L->d_bc_cu_tiles},
+      {&L->cu_qblk, &L->d_cu_qblk},
   };
   size_t total = 0;
   for (auto& p : parts) total += (p.v->size() * sizeof(int32_t) + 255) / 256 * 256;
@@ -206,21 +207,73 @@ nt_status nt_segment_reduce(const nt_layout* L, nt_level level, int32_t op, int3
                             int64_t ld_x, nt_dtype x_dtype, float* y, int64_t ld_y, void* stream) {
   g_last_error.clear();
   if (nt_status st = need_device(L)) return st;
-  if (level != NT_LEVEL_SINGLES && level != NT_LEVEL_PAIRS) return nt::fail(NT_ERR_INVALID_ARG, "bad level");
+  if (level != NT_LEVEL_SINGLES && level != NT_LEVEL_PAIRS && level != NT_LEVEL_PAIRS_FIRST)
+    return nt::fail(NT_ERR_INVALID_ARG, "bad level");
   if (op != 0 && op != 1) return nt::fail(NT_ERR_INVALID_ARG, "op must be 0 (sum) or 1 (mean)");
   if (!valid_dtype(x_dtype)) return nt::fail(NT_ERR_INVALID_ARG, "bad dtype");
   if (C <= 0) return nt::fail(NT_ERR_INVALID_ARG, "C must be > 0");
   const int ve = vec_elems(x_dtype);
   if (C % ve || ld_x % ve || ld_x < C) return nt::fail(NT_ERR_INVALID_ARG, "C and ld_x must be multiples of the vector width, ld_x >= C");
   if (ld_y < C || ld_y % 4) return nt::fail(NT_ERR_INVALID_ARG, "ld_y must be >= C and a multiple of 4");
-  const int64_t out_rows = level == NT_LEVEL_PAIRS ? L->sum_n : L->batch;
+  const int64_t out_rows = level != NT_LEVEL_SINGLES ? L->sum_n : L->batch;
   if (out_rows == 0) return NT_OK;
   if (!y) return nt::fail(NT_ERR_INVALID_ARG, "y is NULL");
-  if (!x && (level == NT_LEVEL_PAIRS ? L->sum_n2 : L->sum_n) > 0) return nt::fail(NT_ERR_INVALID_ARG, "x is NULL");
+  if (!x && (level != NT_LEVEL_SINGLES ? L->sum_n2 : L->sum_n) > 0) return nt::fail(NT_ERR_INVALID_ARG, "x is NULL");
   if ((x && !aligned16(x)) || !aligned16(y)) return nt::fail(NT_ERR_INVALID_ARG, "pointers must be 16-byte aligned");
   return check_hip(nt::launch_segment_reduce(*L, level, op, C, x, ld_x, x_dtype, y, ld_y,
                                              static_cast<hipStream_t>(stream)),
                    "nt_segment_reduce launch");
+}
+
+nt_status nt_pair_broadcast_backward(const nt_layout* L, int32_t C, const void* dz, int64_t ld_dz, nt_dtype dtype,
+                                     float* du, int64_t ld_du, float* dv, int64_t ld_dv, int32_t accumulate,
+                                     void* stream) {
+  g_last_error.clear();
+  if (nt_status st = need_device(L)) return st;
+  if (!valid_dtype(dtype)) return nt::fail(NT_ERR_INVALID_ARG, "bad dtype");
+  if (C <= 0 || C % vec_elems(dtype)) return nt::fail(NT_ERR_INVALID_ARG, "C must be > 0 and a multiple of the vector width");
+  if (accumulate != 0 && accumulate != 1) return nt::fail(NT_ERR_INVALID_ARG, "accumulate must be 0 or 1");
+  if (ld_dz < C || ld_dz % vec_elems(dtype)) return nt::fail(NT_ERR_INVALID_ARG, "bad ld_dz");
+  if ((du && (ld_du < C || ld_du % 4)) || (dv && (ld_dv < C || ld_dv % 4)))
+    return nt::fail(NT_ERR_INVALID_ARG, "ld_du / ld_dv must be >= C and multiples of 4");
+  if (L->sum_n == 0 || (!du && !dv)) return NT_OK;
+  if (!dz) return nt::fail(NT_ERR_INVALID_ARG, "dz is NULL");
+  if (!aligned16(dz) || (du && !aligned16(du)) || (dv && !aligned16(dv)))
+    return nt::fail(NT_ERR_INVALID_ARG, "pointers must be 16-byte aligned");
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (du) {
+    if (nt_status st = check_hip(nt::launch_segment_reduce(*L, NT_LEVEL_PAIRS, 0, C, dz, ld_dz, dtype, du, ld_du, s, accumulate),
+                                 "nt_pair_broadcast_backward launch"))
+      return st;
+  }
+  if (dv) {
+    if (nt_status st = check_hip(nt::launch_segment_reduce(*L, NT_LEVEL_PAIRS_FIRST, 0, C, dz, ld_dz, dtype, dv, ld_dv,
+                                                           s, accumulate),
+                                 "nt_pair_broadcast_backward launch"))
+      return st;
+  }
+  return NT_OK;
+}
+
+nt_status nt_segment_reduce_backward(const nt_layout* L, nt_level level, int32_t op, int32_t C, const float* dy,
+                                     int64_t ld_dy, void* dx, int64_t ld_dx, nt_dtype dtype, int32_t accumulate,
+                                     void* stream) {
+  g_last_error.clear();
+  if (nt_status st = need_device(L)) return st;
+  if (level != NT_LEVEL_SINGLES && level != NT_LEVEL_PAIRS && level != NT_LEVEL_PAIRS_FIRST)
+    return nt::fail(NT_ERR_INVALID_ARG, "bad level");
+  if (op != 0 && op != 1) return nt::fail(NT_ERR_INVALID_ARG, "op must be 0 (sum) or 1 (mean)");
+  if (!valid_dtype(dtype)) return nt::fail(NT_ERR_INVALID_ARG, "bad dtype");
+  if (accumulate != 0 && accumulate != 1) return nt::fail(NT_ERR_INVALID_ARG, "accumulate must be 0 or 1");
+  const int ve = vec_elems(dtype);
+  if (C <= 0 || C % ve || ld_dx < C || ld_dx % ve) return nt::fail(NT_ERR_INVALID_ARG, "C and ld_dx must be multiples of the vector width, ld_dx >= C");
+  if (ld_dy < C) return nt::fail(NT_ERR_INVALID_ARG, "ld_dy must be >= C");
+  if (L->sum_n == 0) return NT_OK;
+  if (!dy || !dx) return nt::fail(NT_ERR_INVALID_ARG, "dy and dx must be non-NULL");
+  if (!aligned16(dx) || (reinterpret_cast<uintptr_t>(dy) & 3u)) return nt::fail(NT_ERR_INVALID_ARG, "misaligned pointer");
+  return check_hip(nt::launch_segment_reduce_backward(*L, level, op, C, dy, ld_dy, dx, ld_dx, dtype, accumulate,
+                                                      static_cast<hipStream_t>(stream)),
+                   "nt_segment_reduce_backward launch");
 }
 
 nt_status nt_layernorm_linear(const nt_linear_args* a, void* stream) {
@@ -312,6 +365,44 @@ nt_status nt_layernorm_linear_workspace(const nt_linear_args* a, uint64_t* bytes
   return NT_OK;
 }
 
+nt_status nt_layernorm_linear_backward_workspace(const nt_linear_bwd_args* a, uint64_t* bytes) {
+  g_last_error.clear();
+  if (!a || !bytes) return nt::fail(NT_ERR_INVALID_ARG, "NULL argument");
+  *bytes = a->rows > 0 && a->c_in > 0 && a->c_out > 0 ? (uint64_t)nt::linear_backward_workspace_bytes(*a) : 0;
+  return NT_OK;
+}
+
+nt_status nt_layernorm_linear_backward(const nt_linear_bwd_args* a, void* stream) {
+  g_last_error.clear();
+  if (!a) return nt::fail(NT_ERR_INVALID_ARG, "args is NULL");
+  if (a->rows < 0 || a->c_in <= 0 || a->c_out <= 0) return nt::fail(NT_ERR_INVALID_ARG, "bad sizes");
+  if (a->rows > INT32_MAX) return nt::fail(NT_ERR_OVERFLOW, "rows exceed int32");
+  if (a->c_in % 8 || a->c_in > 1024) return nt::fail(NT_ERR_UNSUPPORTED, "c_in must be a multiple of 8 and <= 1024");
+  if (!valid_dtype(a->x_dtype) || !valid_dtype(a->dx_dtype)) return nt::fail(NT_ERR_INVALID_ARG, "bad dtype");
+  const bool swiglu = a->epilogue == NT_EPI_SWIGLU_RESIDUAL;
+  if (a->epilogue < NT_EPI_NONE || a->epilogue > NT_EPI_GELU) return nt::fail(NT_ERR_INVALID_ARG, "bad epilogue");
+  if (swiglu && (a->hidden <= 0 || !a->w2)) return nt::fail(NT_ERR_INVALID_ARG, "SwiGLU needs hidden > 0 and w2");
+  if (swiglu && a->residual_is_x && (a->c_out != a->c_in || !a->ln_gamma || a->dx_dtype != NT_BF16))
+    return nt::fail(NT_ERR_UNSUPPORTED, "SwiGLU with residual x needs c_out == c_in, a LayerNorm and a bf16 dx");
+  if (!a->ln_gamma && a->dx && a->dx_dtype == NT_BF16 && a->accumulate_dx)
+    return nt::fail(NT_ERR_UNSUPPORTED, "without a LayerNorm a bf16 dx cannot accumulate");
+  if (a->ln_beta && !a->ln_gamma) return nt::fail(NT_ERR_INVALID_ARG, "ln_beta without ln_gamma");
+  if (a->ldx < a->c_in || a->ld_dy < a->c_out || (a->dx && a->ld_dx < a->c_in))
+    return nt::fail(NT_ERR_INVALID_ARG, "row strides too small");
+  if (a->x_dtype == NT_F32 && !a->ln_gamma && a->ldx != a->c_in)
+    return nt::fail(NT_ERR_UNSUPPORTED, "fp32 x without a LayerNorm must be contiguous");
+  if (a->rows == 0) return NT_OK;
+  if (!a->x || !a->w || !a->dy) return nt::fail(NT_ERR_INVALID_ARG, "x, w and dy must be non-NULL");
+  if (!aligned16(a->x) || !aligned16(a->w) || !aligned16(a->dy) || (a->dx && !aligned16(a->dx)) ||
+      (a->w2 && !aligned16(a->w2)))
+    return nt::fail(NT_ERR_INVALID_ARG, "pointers must be 16-byte aligned");
+  if (nt_status st = need_workspace(nt::linear_backward_workspace_bytes(*a), a->workspace, a->workspace_bytes,
+                                    "nt_layernorm_linear_backward_workspace"))
+    return st;
+  return check_hip(nt::launch_linear_backward(*a, a->workspace, static_cast<hipStream_t>(stream)),
+                   "nt_layernorm_linear_backward launch");
+}
+
 nt_status nt_pair_row_attention(const nt_layout* L, int32_t axis, int32_t H, int32_t D, const void* q,
                                 const void* k, const void* v, int64_t ld_qkv, const void* bias,
                                 int64_t ld_bias, int64_t ld_bias_head, float scale, void* o, int64_t ld_o,
@@ -347,6 +438,51 @@ nt_status nt_pair_row_attention(const nt_layout* L, int32_t axis, int32_t H, int
   return check_hip(nt::launch_attention(*L, axis, H, D, q, k, v, ld_qkv, bias, ld_bias, ld_bias_head, scale, o, ld_o,
                                         dtype, workspace, static_cast<hipStream_t>(stream)),
                    "nt_pair_row_attention launch");
+}
+
+nt_status nt_pair_row_attention_backward_workspace(const nt_layout* L, int32_t axis, int32_t H, int32_t D,
+                                                   nt_dtype dtype, uint64_t* bytes) {
+  g_last_error.clear();
+  if (!L || !bytes) return nt::fail(NT_ERR_INVALID_ARG, "NULL argument");
+  if (axis < 0 || axis > 1 || H <= 0 || D <= 0 || !valid_dtype(dtype))
+    return nt::fail(NT_ERR_INVALID_ARG, "bad axis, heads, head_dim or dtype");
+  *bytes = nt::attention_backward_workspace_bytes(*L, H);
+  return NT_OK;
+}
+
+nt_status nt_pair_row_attention_backward(const nt_layout* L, int32_t axis, int32_t H, int32_t D, const void* q,
+                                         const void* k, const void* v, int64_t ld_qkv, const void* bias,
+                                         int64_t ld_bias, int64_t ld_bias_head,
+                                         const void* dout, int64_t ld_dout, float scale, void* dq, void* dk, void* dv,
+                                         int64_t ld_dqkv, float* dbias, int64_t ld_dbias, int64_t ld_dbias_head,
+                                         nt_dtype dtype, void* workspace, uint64_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  if (!L) return nt::fail(NT_ERR_INVALID_ARG, "layout is NULL");
+  if (axis != 0 && axis != 1) return nt::fail(NT_ERR_UNSUPPORTED, "the attention backward covers axes 0 and 1");
+  if (dtype != NT_BF16 || D != 32) return nt::fail(NT_ERR_UNSUPPORTED, "the attention backward needs bf16 and head_dim 32");
+  if (H <= 0) return nt::fail(NT_ERR_INVALID_ARG, "heads must be > 0");
+  if (L->max_len > nt::kAttnLongLen)
+    return nt::fail(NT_ERR_UNSUPPORTED, "the attention backward supports N_i <= " + std::to_string(nt::kAttnLongLen));
+  if ((int64_t)H * D > ld_qkv || ld_qkv % 8 || (int64_t)H * D > ld_dout ||
+      ld_dout % 8 || (int64_t)H * D > ld_dqkv || ld_dqkv % 8)
+    return nt::fail(NT_ERR_INVALID_ARG, "row strides must hold H*head_dim and be multiples of 8");
+  if (bias && (ld_bias <= 0 || ld_bias_head <= 0)) return nt::fail(NT_ERR_INVALID_ARG, "bias strides must be positive");
+  if (dbias && (ld_dbias <= 0 || ld_dbias_head <= 0)) return nt::fail(NT_ERR_INVALID_ARG, "dbias strides must be positive");
+  if (!(scale == scale)) return nt::fail(NT_ERR_INVALID_ARG, "scale is NaN");
+  if (nt_status st = need_workspace(nt::attention_backward_workspace_bytes(*L, H), workspace, workspace_bytes,
+                                    "nt_pair_row_attention_backward_workspace"))
+    return st;
+  if (nt_status st = need_device(L)) return st;
+  if (L->sum_n2 == 0) return NT_OK;
+  if (!q || !k || !v || !dout || !dq || !dk || !dv) return nt::fail(NT_ERR_INVALID_ARG, "NULL tensor");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(dout) || !aligned16(dq) ||
+      !aligned16(dk) || !aligned16(dv) || (bias && (reinterpret_cast<uintptr_t>(bias) & 1u)) ||
+      (dbias && (reinterpret_cast<uintptr_t>(dbias) & 3u)))
+    return nt::fail(NT_ERR_INVALID_ARG, "misaligned pointer");
+  return check_hip(nt::launch_attention_backward(*L, axis, H, q, k, v, ld_qkv, bias, ld_bias, ld_bias_head,
+                                                 dout, ld_dout, scale, dq, dk, dv, ld_dqkv, dbias, ld_dbias,
+                                                 ld_dbias_head, workspace, static_cast<hipStream_t>(stream)),
+                   "nt_pair_row_attention_backward launch");
 }
 
 nt_status nt_pair_row_attention_noalloc(const nt_layout* L, int32_t axis, int32_t H, int32_t D, const void* q,
@@ -414,6 +550,32 @@ nt_status nt_triangle_mul(const nt_layout* L, int32_t direction, int32_t C, cons
   return check_hip(nt::launch_triangle(*L, direction, C, a, b, ld_ab, operands, z, ld_z, dtype, workspace,
                                        static_cast<hipStream_t>(stream)),
                    "nt_triangle_mul launch");
+}
+
+nt_status nt_triangle_mul_backward(const nt_layout* L, int32_t direction, int32_t C, const void* a, const void* b,
+                                   int64_t ld_ab, const void* dt, int64_t ld_dt, void* da, void* db, int64_t ld_dab,
+                                   nt_dtype dtype, void* workspace, uint64_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  if (!L) return nt::fail(NT_ERR_INVALID_ARG, "layout is NULL");
+  if (direction != 0 && direction != 1) return nt::fail(NT_ERR_INVALID_ARG, "direction must be 0 or 1");
+  if (!valid_dtype(dtype)) return nt::fail(NT_ERR_INVALID_ARG, "bad dtype");
+  if (C <= 0) return nt::fail(NT_ERR_INVALID_ARG, "C must be > 0");
+  if (dtype == NT_BF16 && C % 32) return nt::fail(NT_ERR_INVALID_ARG, "bf16 triangle needs C % 32 == 0");
+  const int ve = vec_elems(dtype);
+  if (C % ve) return nt::fail(NT_ERR_INVALID_ARG, "C must be a multiple of the vector width");
+  if (ld_ab < C || ld_ab % ve || ld_dt < C || ld_dt % ve || ld_dab < C || ld_dab % ve)
+    return nt::fail(NT_ERR_INVALID_ARG, "row strides must be >= C and multiples of the vector width");
+  if (nt_status st = need_workspace(nt::triangle_workspace_bytes(*L, C, NT_TRI_PACKED, dtype), workspace,
+                                    workspace_bytes, "nt_triangle_mul_workspace"))
+    return st;
+  if (nt_status st = need_device(L)) return st;
+  if (L->sum_n2 == 0 || (!da && !db)) return NT_OK;
+  if (!dt || (da && !b) || (db && !a)) return nt::fail(NT_ERR_INVALID_ARG, "missing operand");
+  if ((a && !aligned16(a)) || (b && !aligned16(b)) || !aligned16(dt) || (da && !aligned16(da)) || (db && !aligned16(db)))
+    return nt::fail(NT_ERR_INVALID_ARG, "pointers must be 16-byte aligned");
+  return check_hip(nt::launch_triangle_backward(*L, direction, C, a, b, ld_ab, dt, ld_dt, da, db, ld_dab, dtype,
+                                                workspace, static_cast<hipStream_t>(stream)),
+                   "nt_triangle_mul_backward launch");
 }
 
 nt_status nt_triangle_mul_workspace(const nt_layout* L, int32_t C, nt_tri_operands operands, nt_dtype dtype,

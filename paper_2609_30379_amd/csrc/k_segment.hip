@@ -58,26 +58,34 @@ pair_broadcast_kernel(const int32_t* __restrict__ row_sample, const int32_t* __r
 }
 
 // Segment reduction: workgroup (segment, channel block).  Segment = pair row
-// (level pairs: N_i contiguous cells) or sample (level singles: N_i rows).
-// Threads split the segment's rows into 256/CPB groups; groups combine in
-// LDS, so every output is written by exactly one thread (no atomics).
+// (level pairs: the N_i contiguous cells o_i + a N_i + b of pair row a),
+// first-axis group (level pairs-first: the cells o_i + a N_i + b of column b,
+// N_i rows apart) or sample (level singles: N_i rows).  Threads split the
+// segment's rows into 256/CPB groups; groups combine in LDS, so every output
+// is written by exactly one thread (no atomics).
 template <typename T>
 __global__ void __launch_bounds__(256)
-segment_reduce_kernel(int level_pairs, const int32_t* __restrict__ row_sample,
+segment_reduce_kernel(int level, const int32_t* __restrict__ row_sample,
                       const int32_t* __restrict__ cu_seqlens, const int32_t* __restrict__ cu_pairs,
                       int C, const T* __restrict__ x, int64_t ld_x, float* __restrict__ y, int64_t ld_y,
-                      int mean) {
+                      int mean, int accumulate) {
   constexpr int VE = Vec<T>::N;
   constexpr int CPB = 16;                    // vector chunks per workgroup
   constexpr int G = 256 / CPB;               // row groups
   __shared__ float part[G][CPB * VE];
   const int seg = blockIdx.x;
-  int64_t base;
+  int64_t base, step = 1;
   int n;
-  if (level_pairs) {
+  if (level != NT_LEVEL_SINGLES) {
     const int i = row_sample[seg];
     n = cu_seqlens[i + 1] - cu_seqlens[i];
-    base = (int64_t)cu_pairs[i] + (int64_t)(seg - cu_seqlens[i]) * n;
+    const int a = seg - cu_seqlens[i];
+    if (level == NT_LEVEL_PAIRS) {
+      base = (int64_t)cu_pairs[i] + (int64_t)a * n;
+    } else {
+      base = (int64_t)cu_pairs[i] + a;
+      step = n;
+    }
   } else {
     n = cu_seqlens[seg + 1] - cu_seqlens[seg];
     base = cu_seqlens[seg];
@@ -91,7 +99,7 @@ segment_reduce_kernel(int level_pairs, const int32_t* __restrict__ row_sample,
   if (active) {
     for (int r = g; r < n; r += G) {
       Vec<T> t;
-      t.load(x + (base + r) * ld_x + chunk * VE);
+      t.load(x + (base + (int64_t)r * step) * ld_x + chunk * VE);
 #pragma unroll
       for (int j = 0; j < VE; ++j) acc[j] += t.v[j];
     }
@@ -106,11 +114,73 @@ segment_reduce_kernel(int level_pairs, const int32_t* __restrict__ row_sample,
     for (int gg = 0; gg < G; ++gg) s += part[gg][e];
     if (mean) s = n > 0 ? s / (float)n : __builtin_nanf("");
     const int64_t out_row = seg;
+    if (accumulate) s += y[out_row * ld_y + c];
     y[out_row * ld_y + c] = s;
   }
 }
 
+// Backward of a segment reduction: every position of a group receives the
+// group's gradient (divided by N_i for a mean), added to dx or stored.  One
+// workgroup per pair row (levels pairs / pairs-first: the N_i cells of pair
+// row a, from dy[eta_i + a] or dy[eta_i + b]) or per single row (level
+// singles: dx[eta_i + t] from dy[i]).
+template <typename T>
+__global__ void __launch_bounds__(256)
+segment_reduce_backward_kernel(int level, const int32_t* __restrict__ row_sample,
+                               const int32_t* __restrict__ cu_seqlens, const int32_t* __restrict__ cu_pairs,
+                               int C, const float* __restrict__ dy, int64_t ld_dy, T* __restrict__ dx,
+                               int64_t ld_dx, int mean, int accumulate) {
+  constexpr int VE = Vec<T>::N;
+  const int eta = blockIdx.x;
+  const int i = row_sample[eta];
+  const int s0 = cu_seqlens[i];
+  const int n = cu_seqlens[i + 1] - s0;
+  const float scale = mean ? 1.f / (float)n : 1.f;
+  const int cv = C / VE;
+  if (level == NT_LEVEL_SINGLES) {
+    for (int ch = threadIdx.x; ch < cv; ch += 256) {
+      Vec<T> out;
+      T* dst = dx + (int64_t)eta * ld_dx + ch * VE;
+      if (accumulate) out.load(dst);
+#pragma unroll
+      for (int j = 0; j < VE; ++j)
+        out.v[j] = (accumulate ? out.v[j] : 0.f) + dy[(int64_t)i * ld_dy + ch * VE + j] * scale;
+      out.store(dst);
+    }
+    return;
+  }
+  const int a = eta - s0;
+  const int64_t cell0 = (int64_t)cu_pairs[i] + (int64_t)a * n;
+  const int total = n * cv;
+  for (int t = threadIdx.x; t < total; t += 256) {
+    const int b = t / cv, ch = (t - b * cv) * VE;
+    const float* g = dy + (int64_t)(s0 + (level == NT_LEVEL_PAIRS ? a : b)) * ld_dy + ch;
+    T* dst = dx + (cell0 + b) * ld_dx + ch;
+    Vec<T> out;
+    if (accumulate) out.load(dst);
+#pragma unroll
+    for (int j = 0; j < VE; ++j) out.v[j] = (accumulate ? out.v[j] : 0.f) + g[j] * scale;
+    out.store(dst);
+  }
+}
+
 }  // namespace
+
+hipError_t launch_segment_reduce_backward(const nt_layout& L, nt_level level, int op, int C, const float* dy,
+                                          int64_t ld_dy, void* dx, int64_t ld_dx, nt_dtype dtype, int accumulate,
+                                          hipStream_t s) {
+  if (L.sum_n == 0) return hipSuccess;
+  const dim3 grid((unsigned)L.sum_n), block(256);
+  if (dtype == NT_BF16)
+    segment_reduce_backward_kernel<bf16><<<grid, block, 0, s>>>((int)level, L.d_row_sample, L.d_cu_seqlens,
+                                                                L.d_cu_pairs, C, dy, ld_dy, (bf16*)dx, ld_dx, op,
+                                                                accumulate);
+  else
+    segment_reduce_backward_kernel<float><<<grid, block, 0, s>>>((int)level, L.d_row_sample, L.d_cu_seqlens,
+                                                                 L.d_cu_pairs, C, dy, ld_dy, (float*)dx, ld_dx, op,
+                                                                 accumulate);
+  return hipGetLastError();
+}
 
 hipError_t launch_pair_broadcast(const nt_layout& L, int C, const void* u, int64_t ld_u, const void* v,
                                  int64_t ld_v, void* z, int64_t ld_z, int accumulate, nt_dtype dtype,
@@ -129,19 +199,18 @@ hipError_t launch_pair_broadcast(const nt_layout& L, int C, const void* u, int64
 }
 
 hipError_t launch_segment_reduce(const nt_layout& L, nt_level level, int op, int C, const void* x,
-                                 int64_t ld_x, nt_dtype x_dtype, float* y, int64_t ld_y, hipStream_t s) {
-  const int pairs = level == NT_LEVEL_PAIRS;
-  const int64_t segs = pairs ? L.sum_n : L.batch;
+                                 int64_t ld_x, nt_dtype x_dtype, float* y, int64_t ld_y, hipStream_t s, int accumulate) {
+  const int64_t segs = level != NT_LEVEL_SINGLES ? L.sum_n : L.batch;
   if (segs == 0) return hipSuccess;
   const int ve = x_dtype == NT_BF16 ? 8 : 4;
   const int cblocks = (C / ve + 15) / 16;
   const dim3 grid((unsigned)segs, (unsigned)cblocks), block(256);
   if (x_dtype == NT_BF16)
-    segment_reduce_kernel<bf16><<<grid, block, 0, s>>>(pairs, L.d_row_sample, L.d_cu_seqlens, L.d_cu_pairs, C,
-                                                       (const bf16*)x, ld_x, y, ld_y, op);
+    segment_reduce_kernel<bf16><<<grid, block, 0, s>>>((int)level, L.d_row_sample, L.d_cu_seqlens, L.d_cu_pairs, C,
+                                                       (const bf16*)x, ld_x, y, ld_y, op, accumulate);
   else
-    segment_reduce_kernel<float><<<grid, block, 0, s>>>(pairs, L.d_row_sample, L.d_cu_seqlens, L.d_cu_pairs, C,
-                                                        (const float*)x, ld_x, y, ld_y, op);
+    segment_reduce_kernel<float><<<grid, block, 0, s>>>((int)level, L.d_row_sample, L.d_cu_seqlens, L.d_cu_pairs, C,
+                                                        (const float*)x, ld_x, y, ld_y, op, accumulate);
   return hipGetLastError();
 }
 

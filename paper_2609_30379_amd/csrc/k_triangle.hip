@@ -271,34 +271,26 @@ size_t triangle_workspace_bytes(const nt_layout& L, int C, nt_tri_operands opera
   return 2 * (size_t)C * ldp * (dtype == NT_BF16 ? 2 : 4);
 }
 
-hipError_t launch_triangle(const nt_layout& L, int direction, int C, const void* a, const void* b, int64_t ld_ab,
-                           nt_tri_operands operands, void* z, int64_t ld_z, nt_dtype dtype, void* workspace,
-                           hipStream_t s) {
+namespace {
+
+// Re-tiles one packed operand (row stride ld_src) into planes at dst.
+hipError_t pack_planes(const nt_layout& L, const void* src, int64_t ld_src, bool trans, int C, void* dst,
+                       int64_t ldp, nt_dtype dtype, hipStream_t s) {
+  const dim3 grid((unsigned)(L.sum_pad / 512));
+  if (grid.x == 0) return hipSuccess;
+#define NT_PACK(T, TR) pack_tiled_kernel<T, TR><<<grid, dim3(256), 0, s>>>((const T*)src, ld_src, C, (T*)dst, ldp, \
+                                                                        L.batch, L.d_cu_seqlens, L.d_cu_pairs, L.d_cu_pad)
+  if (dtype == NT_BF16) { if (trans) NT_PACK(bf16, true); else NT_PACK(bf16, false); }
+  else { if (trans) NT_PACK(float, true); else NT_PACK(float, false); }
+#undef NT_PACK
+  return hipGetLastError();
+}
+
+// z[cell(x, y)] += sum_k PA[x, k] PB[y, k] over pair-tiled planes (channel stride ld_ab).
+hipError_t contract(const nt_layout& L, int C, const void* a, const void* b, int64_t ld_ab, void* z, int64_t ld_z,
+                    nt_dtype dtype, hipStream_t s) {
   const int64_t items = L.tri_items();
   if (items == 0) return hipSuccess;
-  if (operands == NT_TRI_PACKED) {
-    // re-tile a and b into the workspace in the variant the direction needs
-    const int64_t ldp = (L.sum_pad + 7) / 8 * 8;
-    const size_t es = dtype == NT_BF16 ? 2 : 4;
-    char* wa = static_cast<char*>(workspace);
-    char* wb = wa + (size_t)C * ldp * es;
-    const dim3 grid((unsigned)(L.sum_pad / 512));
-#define NT_PACK(T, TR)                                                                                       \
-    do {                                                                                                     \
-      pack_tiled_kernel<T, TR><<<grid, dim3(256), 0, s>>>((const T*)a, ld_ab, C, (T*)wa, ldp, L.batch,        \
-                                                          L.d_cu_seqlens, L.d_cu_pairs, L.d_cu_pad);           \
-      pack_tiled_kernel<T, TR><<<grid, dim3(256), 0, s>>>((const T*)b, ld_ab, C, (T*)wb, ldp, L.batch,        \
-                                                          L.d_cu_seqlens, L.d_cu_pairs, L.d_cu_pad);           \
-    } while (0)
-    if (dtype == NT_BF16) { if (direction == 0) NT_PACK(bf16, false); else NT_PACK(bf16, true); }
-    else { if (direction == 0) NT_PACK(float, false); else NT_PACK(float, true); }
-#undef NT_PACK
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    a = wa;
-    b = wb;
-    ld_ab = ldp;
-  }
   if (dtype == NT_F32) {
     TriF32Args t{C, (const float*)a, (const float*)b, ld_ab, (float*)z, ld_z, L.d_tri_work, L.d_cu_seqlens,
                  L.d_cu_pairs, L.d_cu_pad};
@@ -311,6 +303,53 @@ hipError_t launch_triangle(const nt_layout& L, int direction, int C, const void*
   // items is a multiple of 8, so the grid splits evenly over the XCDs
   triangle_mfma_kernel<<<dim3((unsigned)(items * groups * 4)), dim3(kTriThreads), 0, s>>>(t);
   return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_triangle(const nt_layout& L, int direction, int C, const void* a, const void* b, int64_t ld_ab,
+                           nt_tri_operands operands, void* z, int64_t ld_z, nt_dtype dtype, void* workspace,
+                           hipStream_t s) {
+  if (L.tri_items() == 0) return hipSuccess;
+  if (operands == NT_TRI_PACKED) {
+    // re-tile a and b into the workspace in the variant the direction needs
+    const int64_t ldp = (L.sum_pad + 7) / 8 * 8;
+    char* wa = static_cast<char*>(workspace);
+    char* wb = wa + (size_t)C * ldp * (dtype == NT_BF16 ? 2 : 4);
+    hipError_t e = pack_planes(L, a, ld_ab, direction == 1, C, wa, ldp, dtype, s);
+    if (e == hipSuccess) e = pack_planes(L, b, ld_ab, direction == 1, C, wb, ldp, dtype, s);
+    if (e != hipSuccess) return e;
+    return contract(L, C, wa, wb, ldp, z, ld_z, dtype, s);
+  }
+  return contract(L, C, a, b, ld_ab, z, ld_z, dtype, s);
+}
+
+// Backward, per sample and channel c (T = A B^T outgoing, T = A^T B incoming):
+//   outgoing  dA = dT B      = contraction of (dT, B^T) rows;  dB = dT^T A = (dT^T, A^T)
+//   incoming  dA = B dT^T    = contraction of (B, dT);         dB = A dT   = (A, dT^T)
+// where the contraction computes out[x, y] = sum_k PA[x, k] PB[y, k] and a
+// transposed operand is re-tiled in the transposed variant.  Each pair of
+// operands is re-tiled into the workspace, then contracted into da or db.
+hipError_t launch_triangle_backward(const nt_layout& L, int direction, int C, const void* a, const void* b,
+                                    int64_t ld_ab, const void* dt, int64_t ld_dt, void* da, void* db,
+                                    int64_t ld_dab, nt_dtype dtype, void* workspace, hipStream_t s) {
+  if (L.tri_items() == 0) return hipSuccess;
+  const int64_t ldp = (L.sum_pad + 7) / 8 * 8;
+  char* wa = static_cast<char*>(workspace);
+  char* wb = wa + (size_t)C * ldp * (dtype == NT_BF16 ? 2 : 4);
+  struct Pass { const void* pa; int64_t lda; bool ta; const void* pb; int64_t ldb; bool tb; void* out; };
+  const Pass first = direction == 0 ? Pass{dt, ld_dt, false, b, ld_ab, true, da}
+                                    : Pass{b, ld_ab, false, dt, ld_dt, false, da};
+  const Pass second = direction == 0 ? Pass{dt, ld_dt, true, a, ld_ab, true, db}
+                                     : Pass{a, ld_ab, false, dt, ld_dt, true, db};
+  for (const Pass& p : {first, second}) {
+    if (!p.out) continue;
+    hipError_t e = pack_planes(L, p.pa, p.lda, p.ta, C, wa, ldp, dtype, s);
+    if (e == hipSuccess) e = pack_planes(L, p.pb, p.ldb, p.tb, C, wb, ldp, dtype, s);
+    if (e == hipSuccess) e = contract(L, C, wa, wb, ldp, p.out, ld_dab, dtype, s);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace nt

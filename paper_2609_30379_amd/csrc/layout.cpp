@@ -129,6 +129,10 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L) {
     }
   }
 
+  // 16-query blocks of every sample (bias gradient of the pair attention)
+  L->cu_qblk.assign(batch + 1, 0);
+  for (int32_t i = 0; i < batch; ++i) L->cu_qblk[i + 1] = L->cu_qblk[i] + (lengths[i] + 15) / 16;
+
   // pair-row attention: one item per (sample, pair row), cost N_i^2
   {
     std::vector<std::array<int32_t, 2>> items;

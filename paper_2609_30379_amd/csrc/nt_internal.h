@@ -49,6 +49,7 @@ struct nt_layout {
   std::vector<int32_t> sattn_work;   // 1-D attention: quads (sample, first 16-query tile, 0, tile count)
   std::vector<int32_t> blk_prow;     // [ceil(sum N^2 / kLinRows)] pair row holding cell kLinRows*b
   std::vector<int32_t> bc_cu_tiles;  // [B+1] prefix of N_i * ceil(N_i/16): broadcast tiles (16 cells of one pair row)
+  std::vector<int32_t> cu_qblk;      // [B+1] prefix of ceil(N_i/16): 16-query blocks (attention bias gradient)
 
   bool has_device = false;
   int device = -1;
@@ -67,6 +68,7 @@ struct nt_layout {
   const int32_t* d_bias_tiles = nullptr;
   const int32_t* d_sattn_work = nullptr;
   const int32_t* d_bc_cu_tiles = nullptr;
+  const int32_t* d_cu_qblk = nullptr;
 
   int64_t attn_items() const { return (int64_t)attn_work.size() / 2; }
   int64_t tri_items() const { return (int64_t)tri_work.size() / 4; }
@@ -140,7 +142,11 @@ hipError_t launch_pair_broadcast(const nt_layout& L, int C, const void* u, int64
 
 hipError_t launch_segment_reduce(const nt_layout& L, nt_level level, int op, int C,
                                  const void* x, int64_t ld_x, nt_dtype x_dtype,
-                                 float* y, int64_t ld_y, hipStream_t s);
+                                 float* y, int64_t ld_y, hipStream_t s, int accumulate = 0);
+
+hipError_t launch_segment_reduce_backward(const nt_layout& L, nt_level level, int op, int C, const float* dy,
+                                          int64_t ld_dy, void* dx, int64_t ld_dx, nt_dtype dtype, int accumulate,
+                                          hipStream_t s);
 
 // Tail output modes of the projection (columns routed to y_tail).
 enum TailMode { kTailChannelMajor = 0, kTailPairTiled = 1, kTailPairTiledT = 2 };
@@ -163,6 +169,21 @@ constexpr size_t kNoAllocScratchBytes = size_t(16) << 20;
 // once per device).
 hipError_t noalloc_scratch(void** ptr);
 
+// LayerNorm+Linear backward (k_backward.hip): workspace bytes and launch.
+size_t linear_backward_workspace_bytes(const nt_linear_bwd_args& a);
+hipError_t launch_linear_backward(const nt_linear_bwd_args& a, void* ws, hipStream_t s);
+
+// Attention backward (k_attention_backward.hip): bf16, head_dim 32, axes 0
+// and 1, N_i <= 512.  Workspace: the softmax statistics of every query
+// element, attention_backward_workspace_bytes(L, H) bytes.
+size_t attention_backward_workspace_bytes(const nt_layout& L, int H);
+hipError_t launch_attention_backward(const nt_layout& L, int axis, int H, const void* q, const void* k,
+                                     const void* v, int64_t ld_qkv, const void* bias, int64_t ld_bias,
+                                     int64_t ld_bias_head, const void* dout,
+                                     int64_t ld_dout, float scale, void* dq, void* dk, void* dv, int64_t ld_dqkv,
+                                     float* dbias, int64_t ld_dbias, int64_t ld_dbias_head, void* workspace,
+                                     hipStream_t s);
+
 // Bias-image bytes of a pair attention call (0: none).
 size_t attention_workspace_bytes(const nt_layout& L, int axis, int H, int D, nt_dtype dtype, bool has_bias);
 // bias element (cell c, head h) at bias[c * ld_bias + h * ld_bias_head];
@@ -180,6 +201,12 @@ size_t triangle_workspace_bytes(const nt_layout& L, int C, nt_tri_operands opera
 hipError_t launch_triangle(const nt_layout& L, int direction, int C, const void* a, const void* b,
                            int64_t ld_ab, nt_tri_operands operands, void* z, int64_t ld_z, nt_dtype dtype,
                            void* workspace, hipStream_t s);
+// Backward of the triangle update on packed operands: da, db (row stride
+// ld_dab; either may be NULL) accumulate the gradients; the workspace is
+// triangle_workspace_bytes(L, C, NT_TRI_PACKED, dtype).
+hipError_t launch_triangle_backward(const nt_layout& L, int direction, int C, const void* a, const void* b,
+                                    int64_t ld_ab, const void* dt, int64_t ld_dt, void* da, void* db,
+                                    int64_t ld_dab, nt_dtype dtype, void* workspace, hipStream_t s);
 
 // Host-side planner (pure C++; no HIP calls).  Fills every host array of the
 // layout from the lengths, or returns an error status.

@@ -131,6 +131,19 @@ def test_attention_backward_finite_differences(axis, with_bias):
                        ("dq", "dk", "dv", "dbias"))
 
 
+@pytest.mark.parametrize("axis", [0, 1])
+def test_attention_backward_from_the_exact_output_is_unchanged(axis):
+    """D taken from the forward output equals D from the softmax when the
+    output is exact (rowsum(dO * O) = rowsum(dP * P))."""
+    L, H, d = [4, 2, 0, 3], 2, 3
+    q, k, v, bias, G = _attn_inputs(L, H, d)
+    o = ops.pair_row_attention(q, k, v, bias, L, H, d, axis=axis)
+    a = grads.pair_row_attention_backward(q, k, v, bias, G, L, H, d, axis=axis)
+    b = grads.pair_row_attention_backward(q, k, v, bias, G, L, H, d, axis=axis, o=o)
+    for x, y in zip(a, b):
+        np.testing.assert_allclose(x, y, rtol=1e-11, atol=1e-12)
+
+
 def test_attention_backward_matches_torch_autograd_on_a_padded_batch(torch_cpu):
     """Masked padded row attention in torch (valid keys only), differentiated
     by autograd; the packed gradients equal its valid cells."""

@@ -426,3 +426,20 @@ def test_triangle_masked_padded_and_brute_force():
                 for c in range(C):
                     s = sum(a[off + x * n + kk, c] * b[off + y * n + kk, c] for kk in range(n))
                     assert t[off + x * n + y, c] == pytest.approx(s, rel=1e-12, abs=1e-12)
+
+
+def test_pair_row_sum_is_the_column_sum_of_the_transposes():
+    """Sum over the first pair axis: for lengths (2, 3) and cells numbered in
+    packed order, sample 0 gives [0+2, 1+3] and sample 1 gives the column sums
+    of [[4,5,6],[7,8,9],[10,11,12]]; in general it equals the Eq. pair-reduction
+    of each sample's transpose."""
+    x = np.arange(13, dtype=np.float64)[:, None]
+    y = ops.segment_reduce(x, [2, 3], "pair_rows", "sum")
+    assert y[:, 0].tolist() == [2, 4, 21, 24, 27]
+    L, C = [4, 0, 3, 1], 3
+    x = np.random.default_rng(3).standard_normal((sum(n * n for n in L), C))
+    t = np.concatenate([b.transpose(1, 0, 2).reshape(-1, C)
+                        for b in layout.unpack(x, layout.pair_offsets(L), [(n, n) for n in L])])
+    for op in ("sum", "mean"):
+        np.testing.assert_allclose(ops.segment_reduce(x, L, "pair_rows", op), ops.segment_reduce(t, L, "pair_cols", op),
+                                   rtol=1e-13, atol=1e-13)
