@@ -166,3 +166,76 @@ def encoder_layer(x, lengths, p, heads, head_dim, dtype="bf16", round_last=True)
     x = st(x_exact)
     pooled = ops.segment_reduce(x, lengths, "samples", "mean")
     return (x if round_last else x_exact), pooled, {"qkv": qkv, "o": o, "h": h}
+
+
+def mechanism_weights(B):
+    """Sample weights of Eq. joint-diagnostic-loss: alpha_i = 1 + i/B, beta_i = 1.5 - i/(2B)."""
+    return (np.array([1.0 + i / B for i in range(B)]), np.array([1.5 - i / (2.0 * B) for i in range(B)]))
+
+
+def mechanism_step(x, lengths, p, dtype="bf16", y=None, cols=None, S=1):
+    """One training step of the measured single-pair-single program (Eq.
+    running-block; App. A "Measured single-pair-single program"): forward,
+    the joint diagnostic loss, and the backward of every parameter and input.
+
+    Square (y, cols None): X_i [N_i, C] gives both pair operands,
+      P_i[a,b] = u(X_i[a]) + v(X_i[b]).
+    Rectangular: rows from x (N_i) and columns from y (M_i = cols[i]),
+      P_i[a,b] = u(X_i[a]) + v(Y_i[b]), and the column mean divides by M_i.
+    Then  Pt = P + SwiGLU(LN(P)),  Xt[a] = X[a] + g(mean_b Pt[a, b]),
+      L = sum_i alpha_i ||Xt_i||^2 / (S C sum N) + sum_i beta_i ||Pt_i||^2 / (S C_p sum N M).
+    p: u.w/u.b, v.w/v.b ([C_p, C]), trans.* (as the pair block), g.w/g.b ([C, C_p]).
+    bf16: every tensor that one kernel stores and another reads is rounded
+    (u, v, P, LN(P), the gated hidden, Pt, the column mean as consumed, Xt, and
+    the gradients handed between kernels as bf16: dXt, dPt, dP, du, dv); all
+    arithmetic between them is float64.
+    Returns dict: xt, pt, loss (total), loss_s, loss_p (per sample), and
+    gradients d_<param> and dx (and dy for rectangular)."""
+    from . import grads as G
+    from .numerics import round_bf16
+    keep = (lambda t: round_bf16(t)) if dtype == "bf16" else (lambda t: np.asarray(t, np.float64))  # noqa: E731
+    rect = y is not None
+    cols = lengths if cols is None else cols
+    x = np.asarray(x, np.float64)
+    yy = np.asarray(y, np.float64) if rect else x
+    B = len(lengths)
+    C, Cp = x.shape[1], p["u.w"].shape[0]
+    alpha, beta = mechanism_weights(B)
+    sum_n = int(np.sum(lengths))
+    cells = int(sum(int(n) * int(m) for n, m in zip(lengths, cols)))
+    # forward
+    u = keep(linear(x, p["u.w"], p["u.b"]))
+    v = keep(linear(yy, p["v.w"], p["v.b"]))
+    P = keep(ops.pair_broadcast(u, v, lengths, cols=cols))
+    Pt = keep(ref_transition(P, p, keep))
+    m = ops.segment_reduce(Pt, lengths, "pair_cols", "mean", cols=cols)
+    mk = keep(m)
+    xt = keep(x + linear(mk, p["g.w"], p["g.b"]))
+    ls, dxt = ops.weighted_square_loss(xt, lengths, alpha, 1.0 / (S * C * sum_n))
+    lp, dpt = ops.weighted_square_loss(Pt, [int(n) * int(mm) for n, mm in zip(lengths, cols)], beta,
+                                       1.0 / (S * Cp * cells))
+    out = {"xt": xt, "pt": Pt, "loss_s": ls, "loss_p": lp, "loss": float(ls.sum() + lp.sum())}
+    # backward
+    gs = G.layernorm_linear_backward(mk, p["g.w"], p["g.b"], keep(dxt), epilogue="residual")
+    out["d_g.w"], out["d_g.b"] = gs["dw"], gs["db"]
+    dm = gs["dx"]                                           # fp32 on the GPU, kept exact
+    dpt_total = keep(keep(dpt) + G.segment_reduce_backward(dm, lengths, "pair_cols", "mean", cols=cols))
+    gt = G.layernorm_linear_backward(P, p["trans.w"], p["trans.b"], dpt_total, ln=(p["trans.ln_g"], p["trans.ln_b"]),
+                                     epilogue="swiglu_residual", w2=p["trans.w2"], b2=p["trans.b2"],
+                                     xn_store=keep, h_store=keep)
+    for k_out, k_in in (("d_trans.w", "dw"), ("d_trans.b", "db"), ("d_trans.w2", "dw2"), ("d_trans.b2", "db2"),
+                        ("d_trans.ln_g", "dgamma"), ("d_trans.ln_b", "dbeta")):
+        out[k_out] = gt[k_in]
+    dP = keep(gt["dx"])
+    du, dv = G.pair_broadcast_backward(dP, lengths, cols)
+    du, dv = keep(du), keep(dv)
+    gu = G.layernorm_linear_backward(x, p["u.w"], p["u.b"], du)
+    gv = G.layernorm_linear_backward(yy, p["v.w"], p["v.b"], dv)
+    out["d_u.w"], out["d_u.b"], out["d_v.w"], out["d_v.b"] = gu["dw"], gu["db"], gv["dw"], gv["db"]
+    dx = dxt + gu["dx"]                                     # the residual path, then the u projection
+    if rect:
+        out["dy"] = gv["dx"]
+    else:
+        dx = dx + gv["dx"]
+    out["dx"] = dx
+    return out

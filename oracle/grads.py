@@ -32,34 +32,38 @@ def _f64(x):
 
 
 # ----------------------------------------------------------------- broadcast
-def pair_broadcast_backward(dz, lengths):
-    """z[o_i + a N_i + b] = u[eta_i + a] + v[eta_i + b] (Eq. running-block,
-    first line).  du[eta_i + a] = sum_b dz[a, b] (the column sum of Eq.
-    pair-reduction), dv[eta_i + b] = sum_a dz[a, b] (the sum over the first
-    pair axis).  Returns (du, dv), each [sum N, C]."""
+def pair_broadcast_backward(dz, lengths, cols=None):
+    """z[o_i + a M_i + b] = u[eta_i + a] + v[kappa_i + b] (Eq. running-block,
+    first line; M_i = N_i for square pairs).  du[eta_i + a] = sum_b dz[a, b]
+    (the column sum of Eq. pair-reduction), dv[kappa_i + b] = sum_a dz[a, b]
+    (the sum over the first pair axis).  Returns (du [sum N, C], dv [sum M, C])."""
     C = _f64(dz).shape[1]
     du, dv = [], []
-    for P in _pair_elements(dz, lengths):
+    for P in _pair_elements(dz, lengths, cols):
         du.append(P.sum(axis=1))
         dv.append(P.sum(axis=0))
     return layout.pack(du, (C,)), layout.pack(dv, (C,))
 
 
 # ----------------------------------------------------------------- reduce
-def segment_reduce_backward(dy, lengths, level="pair_cols", op="sum"):
+def segment_reduce_backward(dy, lengths, level="pair_cols", op="sum", cols=None):
     """Backward of segment_reduce: the gradient of every reduced position is
     the gradient of its group, divided by the group size for the mean.
-      pair_cols  dx[o_i + a N_i + b] = dy[eta_i + a] (/ N_i)
-      pair_rows  dx[o_i + a N_i + b] = dy[eta_i + b] (/ N_i)   (sum over the first pair axis)
-      samples    dx[eta_i + t] = dy[i] (/ N_i)"""
+      pair_cols  dx[o_i + a M_i + b] = dy[eta_i + a]   (/ M_i)
+      pair_rows  dx[o_i + a M_i + b] = dy[kappa_i + b] (/ N_i)   (sum over the first pair axis)
+      samples    dx[eta_i + t] = dy[i] (/ N_i)
+    (square pairs: M_i = N_i, kappa = eta)."""
     dy = _f64(dy)
     C = dy.shape[1]
     outs = []
     if level in ("pair_cols", "pair_rows"):
-        for Y, n in zip(_single_elements(dy, lengths), lengths):
-            n = int(n)
-            g = Y / n if (op == "mean" and n) else Y
-            P = np.repeat(g[:, None, :], n, axis=1) if level == "pair_cols" else np.repeat(g[None, :, :], n, axis=0)
+        cols = lengths if cols is None else cols
+        group = lengths if level == "pair_cols" else cols
+        for Y, n, m in zip(_single_elements(dy, group), lengths, cols):
+            n, m = int(n), int(m)
+            cnt = m if level == "pair_cols" else n
+            g = Y / cnt if (op == "mean" and cnt) else Y
+            P = np.repeat(g[:, None, :], m, axis=1) if level == "pair_cols" else np.repeat(g[None, :, :], n, axis=0)
             outs.append(P)
         return layout.pack(outs, (C,))
     if level == "samples":

@@ -21,10 +21,13 @@ def _f64(x):
     return np.asarray(x, dtype=np.float64)
 
 
-def _pair_elements(x, lengths):
-    """Logical view of a square pair tensor: list of [N_i, N_i, C...] arrays."""
-    o = layout.pair_offsets(lengths)
-    return layout.unpack(_f64(x), o, [(int(n), int(n)) for n in lengths])
+def _pair_elements(x, lengths, cols=None):
+    """Logical view of a pair tensor: list of [N_i, M_i, C...] arrays (square
+    pairs: M_i = N_i; rectangular pairs pack (N_i, M_i, C) as N_i M_i rows,
+    Eq. packing)."""
+    cols = lengths if cols is None else cols
+    o = layout.rect_pair_offsets(lengths, cols)
+    return layout.unpack(_f64(x), o, [(int(n), int(m)) for n, m in zip(lengths, cols)])
 
 
 def _single_elements(x, lengths):
@@ -33,15 +36,19 @@ def _single_elements(x, lengths):
 
 
 # --------------------------------------------------------------------------- A2
-def pair_broadcast(u, v, lengths, z_in=None):
+def pair_broadcast(u, v, lengths, z_in=None, cols=None):
     """Pair construction by broadcasting (Eq. running-block, first line; Sec. 3.2
-    "Creating axes through broadcasting"): element shapes (N_i,1,C) + (1,N_i,C)
-    give (N_i,N_i,C) with P_i[a,b,:] = U_i[a,:] + V_i[b,:].  No activation is
+    "Creating axes through broadcasting"): element shapes (N_i,1,C) + (1,M_i,C)
+    give (N_i,M_i,C) with P_i[a,b,:] = U_i[a,:] + V_i[b,:].  Square pairs take
+    M_i = N_i and both operands from one single track; rectangular pairs take
+    v from a column track of M_i rows per sample (cols).  No activation is
     applied (Appendix A.1).  With z_in the result is added to an existing pair
     state of the same layout.
     Pins: worked example (2,3), gather form of Fig. "program", numpy
-    broadcasting for equal lengths, fp32 exactness."""
-    U, V = _single_elements(u, lengths), _single_elements(v, lengths)
+    broadcasting for equal lengths, fp32 exactness, a rectangular worked
+    example."""
+    cols = lengths if cols is None else cols
+    U, V = _single_elements(u, lengths), _single_elements(v, cols)
     elems = [Ui[:, None, :] + Vi[None, :, :] for Ui, Vi in zip(U, V)]
     C = _f64(u).shape[1]
     P = layout.pack(elems, (C,))
@@ -205,14 +212,16 @@ def triangle_mul(a, b, lengths, direction="outgoing"):
 
 
 # --------------------------------------------------------------------------- A6
-def segment_reduce(x, lengths, level="pair_cols", op="sum"):
+def segment_reduce(x, lengths, level="pair_cols", op="sum", cols=None):
     """Reductions that consume a ragged axis.
 
-    level "pair_cols": Eq. pair-reduction, V_Y[eta_i + a] = sum_b V_P[o_i + a N_i + b];
-        "mean" divides each group by N_i (Eq. running-block, third line).
+    level "pair_cols": Eq. pair-reduction, V_Y[eta_i + a] = sum_b V_P[o_i + a M_i + b];
+        "mean" divides each group by M_i (N_i for square pairs: Eq.
+        running-block, third line; the rectangular variant divides by M_i).
     level "pair_rows": the same over the other pair axis,
-        V_Y[eta_i + b] = sum_a V_P[o_i + a N_i + b] (the broadcast's gradient
-        with respect to its column operand).
+        V_Y[kappa_i + b] = sum_a V_P[o_i + a M_i + b], mean over N_i (the
+        broadcast's gradient with respect to its column operand).
+    cols: M_i of rectangular pairs (None: square).
     level "samples":   complete reduction within each single-axis element,
         y_i = sum_t X_i[t] (Appendix A: sum(dim=0) of [1,2] and [3,4] is [3,7]);
         "mean" divides by N_i.  An empty element sums to 0 and its mean is NaN,
@@ -222,10 +231,11 @@ def segment_reduce(x, lengths, level="pair_cols", op="sum"):
         raise ValueError(op)
     outs = []
     if level in ("pair_cols", "pair_rows"):
-        for P in _pair_elements(x, lengths):
-            N = P.shape[0]
-            Y = P.sum(axis=1 if level == "pair_cols" else 0)
-            outs.append(Y / N if (op == "mean" and N) else Y)
+        for P in _pair_elements(x, lengths, cols):
+            ax = 1 if level == "pair_cols" else 0
+            cnt = P.shape[ax]
+            Y = P.sum(axis=ax)
+            outs.append(Y / cnt if (op == "mean" and cnt) else Y)
         C = _f64(x).shape[1]
         return layout.pack(outs, (C,))
     if level == "samples":
@@ -237,3 +247,16 @@ def segment_reduce(x, lengths, level="pair_cols", op="sum"):
             outs.append(y)
         return np.stack(outs, 0) if outs else np.zeros((0, _f64(x).shape[1]))
     raise ValueError(level)
+
+
+# --------------------------------------------------------------------------- loss
+def weighted_square_loss(x, counts, weights, scale):
+    """The diagnostic loss of the measured single-pair-single program (App. A,
+    Eq. joint-diagnostic-loss), one term: sample i owns the next counts[i]
+    packed rows of x, and contributes scale * weights[i] * ||x_i||_F^2.
+    Returns (per-sample losses [B], gradient dL/dx = 2 scale w_i x)."""
+    x = _f64(x)
+    o = layout.offsets(counts)
+    loss = np.array([scale * w * float(np.sum(x[o[i]:o[i + 1]] ** 2)) for i, w in enumerate(weights)])
+    g = np.concatenate([2.0 * scale * w * x[o[i]:o[i + 1]] for i, w in enumerate(weights)]) if len(x) else x
+    return loss, g

@@ -20,7 +20,7 @@ import numpy as np
 
 __all__ = [
     "Workload", "WORKLOADS", "lengths_for", "tensor_rng", "snap_bf16",
-    "pair_block_params", "encoder_layer_params", "normal",
+    "pair_block_params", "encoder_layer_params", "normal", "cols_for", "mechanism_params", "mechanism_gains",
 ]
 
 
@@ -46,6 +46,7 @@ class Workload:
     gains: dict = field(default_factory=dict, compare=False, hash=False)
     steps: tuple = ()          # ordered steps of one block (pair workloads)
     s_scale: float = 1.0       # std of the initial single track
+    col_dist: tuple = ()       # rectangular pairs: distribution of the column lengths M_i
 
 
 def _pair_gains(n_max: int, blocks: int = 1) -> dict:
@@ -75,6 +76,12 @@ _TINY = ("bcast", "lin", "att_row", "tri_out", "single")
 _BLOCK = ("bcast", "lin", "att_row", "tri_out", "trans", "single")
 _STACK = ("bcast", "tri_out", "tri_in", "att_row", "att_col", "trans", "single")
 
+def mechanism_gains() -> dict:
+    """Gains of the single-pair-single program: pair state std ~0.5, the
+    SwiGLU update and the single update of the same order as their inputs."""
+    return {"uv": 0.35, "gu": 1.0, "d": 0.25, "g": 0.5}
+
+
 WORKLOADS = {
     w.name: w for w in [
         Workload("pair_tiny_f32_b4", "pair", 4, ("uniform", 4, 16), 0, "f32",
@@ -91,6 +98,13 @@ WORKLOADS = {
                  c_s=384, c_z=128, heads=4, head_dim=32, hidden=512, blocks=4,
                  tri_incoming=True, col_attention=True,
                  gains=_pair_gains(768, blocks=4), steps=_STACK),
+        # the measured single-pair-single program (App. A): B=8, C=384,
+        # C_p=128, expansion 4; square lengths 66..317, rectangular
+        # 66..307 x 66..309 (Table "regimes")
+        Workload("mechanism_square_b8_n66_317_bf16", "mechanism", 8, ("uniform", 66, 317), 2, "bf16",
+                 c_s=384, c_z=128, hidden=512, gains=mechanism_gains()),
+        Workload("mechanism_rect_b8_n66_307_m66_309_bf16", "mechanism", 8, ("uniform", 66, 307), 3, "bf16",
+                 c_s=384, c_z=128, hidden=512, gains=mechanism_gains(), col_dist=("uniform", 66, 309)),
         Workload("tokens_b64_lognormal230_bf16", "tokens", 64,
                  ("lognormal", 230.0, 0.5, 16, 512), 0, "bf16",
                  c_s=768, heads=12, head_dim=64, hidden=3072,
@@ -99,18 +113,31 @@ WORKLOADS = {
 }
 
 
+def _draw(rng, dist, batch):
+    if dist[0] == "uniform":
+        _, lo, hi = dist
+        n = rng.integers(lo, hi, size=batch, endpoint=True)
+    elif dist[0] == "lognormal":
+        _, mu, sigma, lo, hi = dist
+        n = np.clip(np.rint(rng.lognormal(np.log(mu), sigma, size=batch)), lo, hi)
+    else:
+        raise ValueError(f"unknown length distribution {dist[0]!r}")
+    return np.asarray(n, dtype=np.int32)
+
+
 def lengths_for(w: Workload) -> np.ndarray:
     """Per-sample lengths N_i (int32) of a workload, from its own seed."""
+    return _draw(np.random.default_rng(w.seed), w.dist, w.batch)
+
+
+def cols_for(w: Workload):
+    """Column lengths M_i of a rectangular-pair workload (drawn after the row
+    lengths from the same generator), or None for square pairs."""
+    if not w.col_dist:
+        return None
     rng = np.random.default_rng(w.seed)
-    if w.dist[0] == "uniform":
-        _, lo, hi = w.dist
-        n = rng.integers(lo, hi, size=w.batch, endpoint=True)
-    elif w.dist[0] == "lognormal":
-        _, mu, sigma, lo, hi = w.dist
-        n = np.clip(np.rint(rng.lognormal(np.log(mu), sigma, size=w.batch)), lo, hi)
-    else:
-        raise ValueError(f"unknown length distribution {w.dist[0]!r}")
-    return np.asarray(n, dtype=np.int32)
+    _draw(rng, w.dist, w.batch)
+    return _draw(rng, w.col_dist, w.batch)
 
 
 def tensor_rng(seed: int, name: str) -> np.random.Generator:
@@ -189,4 +216,20 @@ def encoder_layer_params(w: Workload, seed: int | None = None) -> dict:
     p["ln2_g"], p["ln2_b"] = _ln(seed, "enc.ln2", c)
     p["ffn1.w"], p["ffn1.b"] = _linear(seed, "enc.ffn1", w.hidden, c, g["ffn1"], dt)
     p["ffn2.w"], p["ffn2.b"] = _linear(seed, "enc.ffn2", c, w.hidden, g["ffn2"], dt)
+    return p
+
+
+def mechanism_params(w: Workload, seed: int | None = None) -> dict:
+    """Random-init weights of the single-pair-single program: u, v (C -> C_p),
+    the pre-normalised SwiGLU transition of width C_p with expansion
+    hidden / C_p, and g (C_p -> C).  Matrices in the workload dtype, vectors fp32."""
+    seed = w.seed if seed is None else seed
+    g, dt, C, Cp = w.gains, w.dtype, w.c_s, w.c_z
+    p = {}
+    p["u.w"], p["u.b"] = _linear(seed, "mech.u", Cp, C, g["uv"], dt)
+    p["v.w"], p["v.b"] = _linear(seed, "mech.v", Cp, C, g["uv"], dt)
+    p["trans.ln_g"], p["trans.ln_b"] = _ln(seed, "mech.trans", Cp)
+    p["trans.w"], p["trans.b"] = _linear(seed, "mech.trans.gu", 2 * w.hidden, Cp, g["gu"], dt)
+    p["trans.w2"], p["trans.b2"] = _linear(seed, "mech.trans.d", Cp, w.hidden, g["d"], dt)
+    p["g.w"], p["g.b"] = _linear(seed, "mech.g", C, Cp, g["g"], dt)
     return p

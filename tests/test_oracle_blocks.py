@@ -148,3 +148,59 @@ def test_encoder_layer_matches_torch_encoder_layer(torch_cpu):
     ref_packed = np.concatenate([ref[i, :n] for i, n in enumerate(L)])
     np.testing.assert_allclose(xo, ref_packed, rtol=1e-10, atol=1e-10)
     np.testing.assert_allclose(pooled, np.stack([ref[i, :n].mean(0) for i, n in enumerate(L)]), rtol=1e-10, atol=1e-10)
+
+
+def _mech_params(C, Cp, seed):
+    from paper_2609_30379_amd import synth as S
+    w = S.Workload("m", "mechanism", 1, ("uniform", 1, 1), seed, "f32", c_s=C, c_z=Cp, hidden=4 * Cp,
+                   gains=S.mechanism_gains())
+    return S.mechanism_params(w)
+
+
+@pytest.mark.parametrize("rect", [False, True])
+def test_mechanism_step_gradients_are_the_derivative_of_its_loss(rect):
+    """The composed backward of the single-pair-single step equals central
+    finite differences of its own forward loss (fp32 mode: no rounding), for
+    every parameter and input; square and rectangular."""
+    L, M, C, Cp = [3, 1, 4], [2, 3, 1], 6, 4
+    p = _mech_params(C, Cp, 5)
+    rng = np.random.default_rng(9)
+    x = rng.standard_normal((sum(L), C))
+    y = rng.standard_normal((sum(M), C)) if rect else None
+    cols = M if rect else None
+    out = blocks.mechanism_step(x, L, p, dtype="f32", y=y, cols=cols)
+
+    def loss_with(name, val):
+        pp = dict(p)
+        xx, yy = x, y
+        if name == "x":
+            xx = val
+        elif name == "y":
+            yy = val
+        else:
+            pp[name] = val
+        return blocks.mechanism_step(xx, L, pp, dtype="f32", y=yy, cols=cols)["loss"]
+
+    names = [k for k in p] + ["x"] + (["y"] if rect else [])
+    for name in names:
+        base = {"x": x, "y": y}.get(name, p.get(name))
+        g = out["dx"] if name == "x" else (out["dy"] if name == "y" else out["d_" + name])
+        d = rng.standard_normal(np.shape(base))
+        eps = 1e-6
+        fd = (loss_with(name, base + eps * d) - loss_with(name, base - eps * d)) / (2 * eps)
+        got = float(np.sum(g * d))
+        assert abs(got - fd) <= 1e-6 * max(1.0, abs(fd)), (name, got, fd)
+
+
+def test_mechanism_loss_closed_form():
+    """Eq. joint-diagnostic-loss on the stored outputs: weights 1 + i/B and
+    1.5 - i/(2B), normalised by C sum N and C_p sum N M."""
+    L, M, C, Cp = [2, 3], [4, 1], 6, 4
+    p = _mech_params(C, Cp, 6)
+    x = np.random.default_rng(1).standard_normal((5, C))
+    y = np.random.default_rng(2).standard_normal((5, C))
+    out = blocks.mechanism_step(x, L, p, dtype="f32", y=y, cols=M)
+    xt, pt = out["xt"], out["pt"]
+    want = (1.0 * np.sum(xt[:2] ** 2) + 1.5 * np.sum(xt[2:] ** 2)) / (C * 5) + \
+        (1.5 * np.sum(pt[:8] ** 2) + 1.25 * np.sum(pt[8:] ** 2)) / (Cp * 11)
+    assert abs(out["loss"] - want) < 1e-12 * max(1.0, want)

@@ -108,3 +108,5 @@ def test_generator_lengths_fixture():
     g = _gold("workload_lengths.json")
     for name, w in synth.WORKLOADS.items():
         assert synth.lengths_for(w).tolist() == g[name], name
+        if w.col_dist:
+            assert synth.cols_for(w).tolist() == g[name + ".cols"], name

@@ -443,3 +443,29 @@ def test_pair_row_sum_is_the_column_sum_of_the_transposes():
     for op in ("sum", "mean"):
         np.testing.assert_allclose(ops.segment_reduce(x, L, "pair_rows", op), ops.segment_reduce(t, L, "pair_cols", op),
                                    rtol=1e-13, atol=1e-13)
+
+
+def test_rectangular_broadcast_and_column_mean_worked_example():
+    """Rows (2, 1) and columns (3, 2): sample 0 holds u0+v0 .. u1+v2 in row-major
+    cell order (o = [0, 6, 8]), sample 1 holds u2+v3, u2+v4; the column mean
+    of a pair row divides by its M_i (Eq. pair-reduction, rectangular variant)."""
+    u = np.array([[1.0], [2.0], [3.0]])
+    v = np.array([[10.0], [20.0], [30.0], [40.0], [50.0]])
+    z = ops.pair_broadcast(u, v, [2, 1], cols=[3, 2])
+    assert z[:, 0].tolist() == [11, 21, 31, 12, 22, 32, 43, 53]
+    assert layout.rect_pair_offsets([2, 1], [3, 2]).tolist() == [0, 6, 8]
+    m = ops.segment_reduce(z, [2, 1], "pair_cols", "mean", cols=[3, 2])
+    assert m[:, 0].tolist() == [21.0, 22.0, 48.0]
+    r = ops.segment_reduce(z, [2, 1], "pair_rows", "sum", cols=[3, 2])
+    assert r[:, 0].tolist() == [23.0, 43.0, 63.0, 43.0, 53.0]
+    # square pairs are the special case cols = lengths
+    L = [3, 0, 2]
+    uu = np.random.default_rng(4).standard_normal((5, 2))
+    np.testing.assert_array_equal(ops.pair_broadcast(uu, uu, L, cols=L), ops.pair_broadcast(uu, uu, L))
+
+
+def test_weighted_square_loss_is_its_definition():
+    x = np.arange(10.0).reshape(5, 2)
+    loss, g = ops.weighted_square_loss(x, [2, 3], [1.0, 2.0], 0.5)
+    assert loss.tolist() == [0.5 * (0 + 1 + 4 + 9), 0.5 * 2.0 * (16 + 25 + 36 + 49 + 64 + 81)]
+    np.testing.assert_array_equal(g, np.concatenate([x[:2], 2.0 * x[2:]]))
