@@ -11,8 +11,10 @@ back to the single track.  value = blocks x sum N^2 / step time (valid pair
 positions per second per pair block).
 
 The same JSON line nests the near-uniform (B=8, 208..224) and high-variation
-(B=8, 32..512) single pair blocks and the packed-token encoder layer (tokens
-per second), each timed the same way.  Step times are reported warm (steps
+(B=8, 32..512) single pair blocks, the packed-token encoder layer (tokens per
+second) and the training step (forward, joint diagnostic loss, backward) of
+the single-pair-single program on square and rectangular pairs, each timed
+the same way.  Step times are reported warm (steps
 back to back) and cold (a 512 MB write flushes the memory-side cache before
 each step), as median, p10 and p90.
 
@@ -129,6 +131,31 @@ def token_op_costs(w, L):
         "ffn_up_gelu": (T * (c + F) * e, 2 * T * c * F),
         "ffn_down_residual": (T * (F + 2 * c) * e, 2 * T * F * c),
         "sample_mean": (T * c * e + len(L) * c * 4, T * c),
+    }
+
+
+def mechanism_op_costs(w, L, M):
+    """Algorithmic HBM bytes and flops per launch of the ops of one training
+    step of the single-pair-single program (forward, loss, backward); M is
+    None for square pairs.  bf16 tensors 2 bytes, fp32 4."""
+    S = sum(L)
+    Mc = S if M is None else sum(M)
+    cells = sum(n * n for n in L) if M is None else sum(n * m for n, m in zip(L, M))
+    C, Cp, F = w.c_s, w.c_z, w.hidden
+    xin = (S + (0 if M is None else Mc)) * C * 2
+    return {
+        "mech_proj": (xin + (S + Mc) * Cp * 2, 2 * (S + Mc) * C * Cp),
+        "mech_broadcast": (cells * Cp * 2 + (S + Mc) * Cp * 2, cells * Cp),
+        "mech_transition": (cells * Cp * 2 * 2, 2 * cells * (Cp * 2 * F + F * Cp)),
+        "mech_column_mean": (cells * Cp * 2 + S * Cp * 4, cells * Cp),
+        "mech_single_update": (S * (Cp * 4 + 2 * C * 2), 2 * S * Cp * C),
+        "mech_loss": (2 * S * C * 2 + cells * Cp * 2 + S * C * (2 + 4) + cells * Cp * 2, 3 * (2 * S * C) + 3 * cells * Cp),
+        "mech_single_update_bwd": (S * Cp * 4 * 2 + S * C * 2, 2 * 2 * S * C * Cp),
+        "mech_column_mean_bwd": (S * Cp * 4 + cells * Cp * 2 * 2, cells * Cp),
+        "mech_transition_bwd": (cells * Cp * 2 * 3, 2 * cells * Cp * 8 * F),
+        "mech_broadcast_bwd": (cells * Cp * 2 * 2 + (S + Mc) * Cp * 2, 2 * cells * Cp),
+        "mech_proj_bwd": (xin + (S + Mc) * Cp * 2 + S * C * 4 * 2 + (0 if M is None else Mc * C * 4),
+                          2 * 2 * (S + Mc) * C * Cp),
     }
 
 
@@ -278,10 +305,13 @@ def measure(w, steps: int, warmup: int, graph: bool = False, cpu: bool = False):
     """Times `steps` steps of workload w; returns the result dict."""
     import torch
     from paper_2609_30379_amd import blocks
-    tokens = w.kind != "pair"
-    run = blocks.TokenRun(w) if tokens else blocks.PairRun(w)
+    tokens = w.kind == "tokens"
+    mech = w.kind == "mechanism"
+    run = blocks.TokenRun(w) if tokens else (blocks.MechanismRun(w) if mech else blocks.PairRun(w))
     L = run.lengths
     R, S = sum(n * n for n in L), sum(L)
+    if mech and run.rect:
+        R = sum(n * m for n, m in zip(L, run.cols))
     stream = torch.cuda.current_stream()          # the stream every nt_* call launches on
 
     for _ in range(max(1, warmup)):
@@ -347,7 +377,7 @@ def measure(w, steps: int, warmup: int, graph: bool = False, cpu: bool = False):
     blocks.timer = None
     per_op = tm.summary()                            # {op: (launches, mean us)}
 
-    costs = token_op_costs(w, L) if tokens else op_costs(w, L)
+    costs = token_op_costs(w, L) if tokens else (mechanism_op_costs(w, L, run.cols) if mech else op_costs(w, L))
     total_us = {k: n * us / steps for k, (n, us) in per_op.items()}
     dominant = max(total_us, key=total_us.get)
     n_launch, us_launch = per_op[dominant]
@@ -367,7 +397,15 @@ def measure(w, steps: int, warmup: int, graph: bool = False, cpu: bool = False):
               "cold_ms": {"median": _pct(cold, 50), "p10": _pct(cold, 10), "p90": _pct(cold, 90),
                           "reps": len(cold)},
               "op_sum_ms": round(sum(total_us.values()) / 1e3, 4)}
-    if tokens:
+    if mech:
+        out = {"metric": "valid pair positions/sec per training step (forward + loss + backward) of the "
+                         "single-pair-single program (1 MI355X)",
+               "value": round(R / (ms * 1e-3), 1), "unit": "pair positions/s",
+               "tokens_per_s": round(S / (ms * 1e-3), 1),
+               "config": {"workload": w.name, "batch": w.batch, "lengths": L, "cols": run.cols, "sum_n": S,
+                          "pair_cells": R, "c": w.c_s, "c_p": w.c_z, "hidden": w.hidden,
+                          "step": "forward, joint diagnostic loss, backward of every parameter and input"}}
+    elif tokens:
         out = {"metric": "packed tokens/sec per encoder layer (1 MI355X)", "value": round(S / (ms * 1e-3), 1),
                "unit": "tokens/s",
                "config": {"workload": w.name, "batch": w.batch, "lengths": L, "sum_n": S, "sum_n2": R,
@@ -385,7 +423,8 @@ def measure(w, steps: int, warmup: int, graph: bool = False, cpu: bool = False):
     return out
 
 
-NESTED = ("pair_b8_n208_224_bf16", "pair_b8_n32_512_bf16", "tokens_b64_lognormal230_bf16")
+NESTED = ("pair_b8_n208_224_bf16", "pair_b8_n32_512_bf16", "tokens_b64_lognormal230_bf16",
+          "mechanism_square_b8_n66_317_bf16", "mechanism_rect_b8_n66_307_m66_309_bf16")
 
 
 def main():
@@ -438,7 +477,8 @@ def main():
             if name == w.name:
                 continue
             r = measure(synth.WORKLOADS[name], args.steps, args.warmup, args.graph, cpu=False)
-            r.pop("kernels")
+            if synth.WORKLOADS[name].kind != "mechanism":
+                r.pop("kernels")
             nested[name] = r
         out["other_workloads"] = nested
     if args.kernels:

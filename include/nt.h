@@ -117,7 +117,9 @@ typedef enum {
   NT_ARR_ATTN_WORK = 5,        /* pair-row work map (sample, row) pairs, XCD-ordered */
   NT_ARR_TRI_WORK = 6,         /* triangle tile map (sample, x-tile, y-tile, first tile of the sample) quads */
   NT_ARR_SEQ_WORK = 7,         /* 1-D attention map (sample, query block) pairs */
-  NT_ARR_CU_PAD = 8            /* P_i offsets of pair-tiled operands, [B+1]     */
+  NT_ARR_CU_PAD = 8,           /* P_i offsets of pair-tiled operands, [B+1]     */
+  NT_ARR_COLS = 9,             /* M_i, [B] (= N_i for square pairs)             */
+  NT_ARR_CU_COLS = 10          /* column offsets kappa, [B+1]                   */
 } nt_array;
 
 typedef struct {
@@ -130,6 +132,9 @@ typedef struct {
   const int32_t* d_cu_seqlens; /* device mirrors (NULL for host-only layouts)   */
   const int32_t* d_cu_pairs;
   const int32_t* d_row_splits2;
+  int64_t sum_m;               /* sum_i M_i (columns; = sum_n for square pairs)  */
+  int32_t rect;                /* 1 for rectangular pairs N_i x M_i             */
+  const int32_t* d_cu_cols;    /* column offsets kappa (device)                 */
 } nt_layout_info_t;
 
 /* ---------------------------------------------------------------- layouts
@@ -150,6 +155,18 @@ typedef struct {
  *         NT_ERR_OOM / NT_ERR_HIP (device mirrors).                          */
 nt_status nt_from_lengths(const int32_t* lengths, int32_t batch, uint32_t flags,
                           void* stream, nt_layout** out);
+
+/* Rectangular pairs (Eq. packing with p_i = N_i M_i; Eq. pair-reduction):
+ * element i is an N_i x M_i pair state from a row track of N_i singles
+ * (offsets eta) and a column track of M_i singles (offsets kappa); cell
+ * (i, a, b) is packed row o_i + a M_i + b.  rows = N_i, cols = M_i (host,
+ * [batch], each >= 0).  The sum_n2 field of nt_layout_info counts the cells
+ * (sum_i N_i M_i).  Broadcast, segment reductions, their backward, and the
+ * row-wise ops accept rectangular layouts; attention over pair axes and the
+ * triangle update need square pairs (NT_ERR_UNSUPPORTED).
+ * Errors: as nt_from_lengths.                                                */
+nt_status nt_from_rect_lengths(const int32_t* rows, const int32_t* cols, int32_t batch, uint32_t flags,
+                               void* stream, nt_layout** out);
 
 /* Same from single offsets (cu_seqlens, host, [batch+1]); they must satisfy
  * o_0 = 0 and be non-decreasing (Appendix A, "Structural invariants"),
@@ -175,11 +192,13 @@ int32_t nt_layouts_compatible(const nt_layout* a, const nt_layout* b);
 
 /* ---------------------------------------------------------------- broadcast
  * Pair construction by broadcasting (Eq. running-block, first line; Sec. 3.2
- * "Creating axes through broadcasting"): for every sample i and a, b < N_i
- *     z[o_i + a N_i + b, c] (+)= u[eta_i + a, c] + v[eta_i + b, c]
- * computed in fp32 and rounded once to the storage dtype.
+ * "Creating axes through broadcasting"): for every sample i, a < N_i, b < M_i
+ *     z[o_i + a M_i + b, c] (+)= u[eta_i + a, c] + v[kappa_i + b, c]
+ * (square pairs: M_i = N_i, kappa = eta) computed in fp32 and rounded once to
+ * the storage dtype.
  *   C          channels (> 0).
- *   u, v       singles [sum N, C] with row strides ld_u, ld_v (may alias).
+ *   u, v       row singles [sum N, C] and column singles [sum M, C] with row
+ *              strides ld_u, ld_v (may alias for square pairs).
  *   z          pairs [sum N^2, C] with row stride ld_z (must not alias u/v).
  *   accumulate 0: z is overwritten; 1: z is read and the sum added to it.
  *   dtype      NT_F32 or NT_BF16 for u, v and z.
@@ -364,12 +383,13 @@ nt_status nt_triangle_mul_workspace(const nt_layout* layout, int32_t C, nt_tri_o
 
 /* ---------------------------------------------------------------- reduce
  * Reductions that consume a ragged axis, with fp32 accumulation and fp32
- * output, one launch, no atomics:
+ * output, one launch, no atomics (rectangular pairs: cell (a, b) at
+ * o_i + a M_i + b, square: M_i = N_i, kappa = eta):
  *   level NT_LEVEL_PAIRS   (pair columns, Eq. pair-reduction)
- *       y[eta_i + a, c] = sum_b x[o_i + a N_i + b, c]     (op 1: / N_i)
+ *       y[eta_i + a, c] = sum_b x[o_i + a M_i + b, c]     (op 1: / M_i)
  *   level NT_LEVEL_PAIRS_FIRST (the other pair axis; the broadcast's
  *       gradient with respect to its column operand)
- *       y[eta_i + b, c] = sum_a x[o_i + a N_i + b, c]     (op 1: / N_i)
+ *       y[kappa_i + b, c] = sum_a x[o_i + a M_i + b, c]   (op 1: / N_i)
  *   level NT_LEVEL_SINGLES (complete reduction within each element, Appendix A)
  *       y[i, c] = sum_t x[eta_i + t, c]                    (op 1: / N_i;
  *       an empty sample gives 0 for the sum and NaN for the mean)
@@ -386,21 +406,37 @@ nt_status nt_segment_reduce(const nt_layout* layout, nt_level level, int32_t op,
  * representations"): every gradient has the packed layout of its value.    */
 
 /* Backward of nt_pair_broadcast (z = u_a + v_b):
- *   du[eta_i + a, c] (+)= sum_b dz[o_i + a N_i + b, c]
- *   dv[eta_i + b, c] (+)= sum_a dz[o_i + a N_i + b, c]
- * dz [sum N^2, C] (dtype, row stride ld_dz); du, dv fp32 [sum N, C] with row
- * strides ld_du, ld_dv (multiples of 4); accumulate 0 overwrites, 1 adds.
- * Either of du, dv may be NULL (not computed).  fp32 accumulation, no atomics.
+ *   du[eta_i + a, c]   (+)= sum_b dz[o_i + a M_i + b, c]
+ *   dv[kappa_i + b, c] (+)= sum_a dz[o_i + a M_i + b, c]
+ * dz [cells, C] (dtype, row stride ld_dz); du [sum N, C] and dv [sum M, C] in
+ * out_dtype (fp32, or bf16 rounded once from the fp32 sums) with row strides
+ * ld_du, ld_dv; accumulate 0 overwrites, 1 adds.  Either of du, dv may be
+ * NULL (not computed).  fp32 accumulation, no atomics.
  * Errors: NT_ERR_INVALID_ARG.                                                */
 nt_status nt_pair_broadcast_backward(const nt_layout* layout, int32_t C, const void* dz, int64_t ld_dz,
-                                     nt_dtype dtype, float* du, int64_t ld_du, float* dv, int64_t ld_dv,
-                                     int32_t accumulate, void* stream);
+                                     nt_dtype dtype, void* du, int64_t ld_du, void* dv, int64_t ld_dv,
+                                     nt_dtype out_dtype, int32_t accumulate, void* stream);
+
+/* Sample-weighted squared norm and its gradient, the diagnostic loss of the
+ * measured single-pair-single program (App. A, Eq. joint-diagnostic-loss):
+ *   loss[i] = scale * weights[i] * sum over sample i's rows r, channels c of x[r, c]^2
+ *   dx[r, c] = 2 * scale * weights[i] * x[r, c]          (dx NULL: not written)
+ * level NT_LEVEL_SINGLES: rows eta_i .. eta_{i+1}; NT_LEVEL_PAIRS: the pair
+ * cells o_i .. o_{i+1}.  weights, loss: device fp32 [B]; x in dtype, dx in
+ * dx_dtype.  The per-sample sums are fp32 partials reduced in a fixed order.
+ * Workspace: nt_weighted_square_loss_workspace (B * 256 bytes).
+ * Errors: NT_ERR_INVALID_ARG.                                                */
+nt_status nt_weighted_square_loss(const nt_layout* layout, nt_level level, int32_t C, const void* x, int64_t ld_x,
+                                  nt_dtype dtype, const float* weights, float scale, float* loss, void* dx,
+                                  int64_t ld_dx, nt_dtype dx_dtype, void* workspace, uint64_t workspace_bytes,
+                                  void* stream);
+nt_status nt_weighted_square_loss_workspace(const nt_layout* layout, uint64_t* bytes);
 
 /* Backward of nt_segment_reduce: every reduced position receives its group's
  * gradient dy (fp32, the reduce's output layout, row stride ld_dy), divided
  * by N_i for op 1 (mean):
- *   NT_LEVEL_PAIRS        dx[o_i + a N_i + b] (+)= dy[eta_i + a] (/ N_i)
- *   NT_LEVEL_PAIRS_FIRST  dx[o_i + a N_i + b] (+)= dy[eta_i + b] (/ N_i)
+ *   NT_LEVEL_PAIRS        dx[o_i + a M_i + b] (+)= dy[eta_i + a]   (/ M_i)
+ *   NT_LEVEL_PAIRS_FIRST  dx[o_i + a M_i + b] (+)= dy[kappa_i + b] (/ N_i)
  *   NT_LEVEL_SINGLES      dx[eta_i + t]       (+)= dy[i]        (/ N_i)
  * dx in dtype with row stride ld_dx; accumulate 0 overwrites, 1 adds.
  * Errors: NT_ERR_INVALID_ARG.                                                */
@@ -464,8 +500,8 @@ nt_status nt_pair_row_attention_backward_workspace(const nt_layout* layout, int3
  * bf16 weights and dy; products on matrix cores with fp32 accumulation; the
  * normalised rows and the recomputed hidden are rounded to bf16 as the
  * forward consumed them.  Weight gradients (dw, db, dgamma, dbeta, dw2, db2:
- * fp32, contiguous, NULL = not wanted) are accumulated; dx (x_dtype or fp32)
- * is overwritten unless accumulate_dx.  Partial sums are reduced in a fixed
+ * fp32, contiguous, NULL = not wanted) are accumulated (overwritten with
+ * overwrite_weights); dx (x_dtype or fp32) is overwritten unless accumulate_dx.  Partial sums are reduced in a fixed
  * order: the result is deterministic.                                        */
 typedef struct {
   int64_t rows;                /* R                                              */
@@ -489,6 +525,7 @@ typedef struct {
   int64_t ld_dx;
   nt_dtype dx_dtype;
   int32_t accumulate_dx;
+  int32_t overwrite_weights;   /* 1: dw .. db2 are overwritten instead of accumulated */
   float* dw;                   /* [N_w, K]  */
   float* db;                   /* [N_w]     */
   float* dgamma;               /* [K]       */

@@ -235,7 +235,9 @@ def segment_reduce(x, lengths, level="pair_cols", op="sum", cols=None):
             ax = 1 if level == "pair_cols" else 0
             cnt = P.shape[ax]
             Y = P.sum(axis=ax)
-            outs.append(Y / cnt if (op == "mean" and cnt) else Y)
+            if op == "mean":                   # an empty group's mean is NaN, as the dense mean of nothing
+                Y = Y / cnt if cnt else np.full_like(Y, np.nan)
+            outs.append(Y)
         C = _f64(x).shape[1]
         return layout.pack(outs, (C,))
     if level == "samples":

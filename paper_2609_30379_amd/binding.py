@@ -23,7 +23,7 @@ LEVELS = {"singles": 0, "pairs": 1, "pairs_first": 2}
 TAILS = {"channel_major": 0, "pair_tiled": 1, "pair_tiled_t": 2}
 TRI_OPERANDS = {"packed": 0, "pair_tiled": 1, "pair_tiled_t": 2}
 ARRAYS = {"lengths": 0, "cu_seqlens": 1, "cu_pairs": 2, "row_splits2": 3, "row_sample": 4,
-          "attn_work": 5, "tri_work": 6, "seq_work": 7, "cu_pad": 8}
+          "attn_work": 5, "tri_work": 6, "seq_work": 7, "cu_pad": 8, "cols": 9, "cu_cols": 10}
 NT_LAYOUT_HOST_ONLY = 1
 
 
@@ -36,7 +36,8 @@ class NtError(RuntimeError):
 class LayoutInfo(C.Structure):
     _fields_ = [("batch", C.c_int32), ("max_len", C.c_int32), ("sum_n", C.c_int64), ("sum_n2", C.c_int64),
                 ("sum_n3", C.c_int64), ("sum_pad", C.c_int64), ("d_cu_seqlens", C.c_void_p),
-                ("d_cu_pairs", C.c_void_p), ("d_row_splits2", C.c_void_p)]
+                ("d_cu_pairs", C.c_void_p), ("d_row_splits2", C.c_void_p), ("sum_m", C.c_int64),
+                ("rect", C.c_int32), ("d_cu_cols", C.c_void_p)]
 
 
 class LinearBwdArgs(C.Structure):
@@ -47,6 +48,7 @@ class LinearBwdArgs(C.Structure):
                 ("hidden", C.c_int32), ("w2", C.c_void_p), ("residual_is_x", C.c_int32),
                 ("dy", C.c_void_p), ("ld_dy", C.c_int64),
                 ("dx", C.c_void_p), ("ld_dx", C.c_int64), ("dx_dtype", C.c_int), ("accumulate_dx", C.c_int32),
+                ("overwrite_weights", C.c_int32),
                 ("dw", C.c_void_p), ("db", C.c_void_p), ("dgamma", C.c_void_p), ("dbeta", C.c_void_p),
                 ("dw2", C.c_void_p), ("db2", C.c_void_p),
                 ("workspace", C.c_void_p), ("workspace_bytes", C.c_uint64)]
@@ -94,7 +96,10 @@ def load(path: str = LIB_PATH):
         "nt_triangle_mul": [vp, i32, i32, vp, vp, i64, C.c_int, vp, i64, C.c_int, vp, u64, vp],
         "nt_triangle_mul_workspace": [vp, i32, C.c_int, C.c_int, C.POINTER(u64)],
         "nt_segment_reduce": [vp, C.c_int, i32, i32, vp, i64, C.c_int, vp, i64, vp],
-        "nt_pair_broadcast_backward": [vp, i32, vp, i64, C.c_int, vp, i64, vp, i64, i32, vp],
+        "nt_pair_broadcast_backward": [vp, i32, vp, i64, C.c_int, vp, i64, vp, i64, C.c_int, i32, vp],
+        "nt_from_rect_lengths": [vp, vp, i32, C.c_uint32, vp, C.POINTER(vp)],
+        "nt_weighted_square_loss": [vp, C.c_int, i32, vp, i64, C.c_int, vp, f32, vp, vp, i64, C.c_int, vp, u64, vp],
+        "nt_weighted_square_loss_workspace": [vp, C.POINTER(u64)],
         "nt_segment_reduce_backward": [vp, C.c_int, i32, i32, vp, i64, vp, i64, C.c_int, i32, vp],
         "nt_triangle_mul_backward": [vp, i32, i32, vp, vp, i64, vp, i64, vp, vp, i64, C.c_int, vp, u64, vp],
         "nt_layernorm_linear_backward": [C.POINTER(LinearBwdArgs), vp],
@@ -162,9 +167,10 @@ def _ws(ws):
 
 
 class NestedLayout:
-    """Partitions of a batch of square pair states (nt_from_lengths)."""
+    """Partitions of a batch of pair states: square (nt_from_lengths /
+    nt_from_offsets) or, with cols, rectangular N_i x M_i (nt_from_rect_lengths)."""
 
-    def __init__(self, lengths, host_only: bool = False, offsets: bool = False):
+    def __init__(self, lengths, host_only: bool = False, offsets: bool = False, cols=None):
         lib = load()
         arr = np.ascontiguousarray(np.asarray(lengths, dtype=np.int32))
         self._arr = arr
@@ -172,13 +178,22 @@ class NestedLayout:
         flags = NT_LAYOUT_HOST_ONLY if host_only else 0
         stream = None if host_only else _stream()
         batch = len(arr) - 1 if offsets else len(arr)
-        fn = lib.nt_from_offsets if offsets else lib.nt_from_lengths
-        _check(fn(arr.ctypes.data_as(C.c_void_p), batch, flags, stream, C.byref(handle)))
+        if cols is not None:
+            carr = np.ascontiguousarray(np.asarray(cols, dtype=np.int32))
+            if len(carr) != len(arr) or offsets:
+                raise ValueError("cols needs one entry per sample (lengths, not offsets)")
+            self._carr = carr
+            _check(lib.nt_from_rect_lengths(arr.ctypes.data_as(C.c_void_p), carr.ctypes.data_as(C.c_void_p), batch,
+                                            flags, stream, C.byref(handle)))
+        else:
+            fn = lib.nt_from_offsets if offsets else lib.nt_from_lengths
+            _check(fn(arr.ctypes.data_as(C.c_void_p), batch, flags, stream, C.byref(handle)))
         self.handle = handle
         info = LayoutInfo()
         _check(lib.nt_layout_info(handle, C.byref(info)))
         self.batch, self.max_len = info.batch, info.max_len
         self.sum_n, self.sum_n2, self.sum_n3, self.sum_pad = info.sum_n, info.sum_n2, info.sum_n3, info.sum_pad
+        self.sum_m, self.rect = info.sum_m, bool(info.rect)
 
     def host_array(self, name: str) -> np.ndarray:
         ptr, count = C.POINTER(C.c_int32)(), C.c_int64()
@@ -376,13 +391,38 @@ def nt_segment_reduce(layout: NestedLayout, level: str, op: str, x, y):
 
 # ---------------------------------------------------------------- backward
 def nt_pair_broadcast_backward(layout: NestedLayout, dz, du=None, dv=None, accumulate: bool = False):
-    """du[eta_i + a] = sum_b dz[a, b], dv[eta_i + b] = sum_a dz[a, b] (fp32 outputs)."""
+    """du[eta_i + a] = sum_b dz[a, b], dv[kappa_i + b] = sum_a dz[a, b]; du and
+    dv share one dtype (fp32 or bf16)."""
     pz, ldz = _mat(dz, "dz")
     pu, ldu = _mat(du, "du") if du is not None else (None, int(dz.size(1)))
     pv, ldv = _mat(dv, "dv") if dv is not None else (None, int(dz.size(1)))
+    outs = [t for t in (du, dv) if t is not None]
+    if len(outs) == 2 and du.dtype != dv.dtype:
+        raise ValueError("du and dv must share one dtype")
+    out_dt = _dtype(outs[0]) if outs else NT_F32
     _check(load().nt_pair_broadcast_backward(layout.handle, int(dz.size(1)), pz, ldz, _dtype(dz), pu, ldu, pv, ldv,
-                                             int(accumulate), _stream()))
+                                             out_dt, int(accumulate), _stream()))
     return du, dv
+
+
+def loss_workspace_bytes(layout: NestedLayout) -> int:
+    n = C.c_uint64()
+    _check(load().nt_weighted_square_loss_workspace(layout.handle, C.byref(n)))
+    return int(n.value)
+
+
+def nt_weighted_square_loss(layout: NestedLayout, level: str, x, weights, scale: float, loss, dx=None,
+                            workspace=None):
+    """loss[i] = scale * weights[i] * ||x_i||^2 (device fp32 [B]); dx = 2 scale w_i x."""
+    px, ldx = _mat(x, "x")
+    pdx, lddx = _mat(dx, "dx") if dx is not None else (None, int(x.size(1)))
+    if workspace is None:
+        workspace = workspace_tensor(loss_workspace_bytes(layout))
+    pw, nw = _ws(workspace)
+    _check(load().nt_weighted_square_loss(layout.handle, LEVELS[level], int(x.size(1)), px, ldx, _dtype(x),
+                                          _ptr(weights), float(scale), _ptr(loss), pdx, lddx,
+                                          _dtype(dx) if dx is not None else NT_F32, pw, nw, _stream()))
+    return loss
 
 
 def nt_segment_reduce_backward(layout: NestedLayout, level: str, op: str, dy, dx, accumulate: bool = False):
@@ -418,7 +458,7 @@ def nt_triangle_mul_backward(layout: NestedLayout, direction: int, a, b, dt, da=
 def nt_layernorm_linear_backward(x, w, dy, ln=None, eps: float = 1e-5, bias=None, epilogue: str = "none",
                                  w2=None, hidden: int = 0, residual_is_x: bool = True, dx=None,
                                  accumulate_dx: bool = False, dw=None, db=None, dgamma=None, dbeta=None, dw2=None,
-                                 db2=None, workspace=None):
+                                 db2=None, workspace=None, overwrite_weights: bool = False):
     """Gradients of y = epilogue(LN(x) W^T + b) given dy; weight gradients (fp32)
     accumulate, dx is overwritten unless accumulate_dx."""
     a = LinearBwdArgs()
@@ -438,6 +478,7 @@ def nt_layernorm_linear_backward(x, w, dy, ln=None, eps: float = 1e-5, bias=None
     else:
         a.dx, a.ld_dx, a.dx_dtype = None, a.c_in, NT_BF16
     a.accumulate_dx = int(bool(accumulate_dx))
+    a.overwrite_weights = int(bool(overwrite_weights))
     a.dw, a.db, a.dgamma, a.dbeta = _ptr(dw), _ptr(db), _ptr(dgamma), _ptr(dbeta)
     a.dw2, a.db2 = _ptr(dw2), _ptr(db2)
     if workspace is None:

@@ -294,3 +294,138 @@ class TokenRun:
         self.x.copy_(self.x0)
         pooled = encoder_layer(self.layout, self.x, self.W, self.w.heads, self.w.head_dim, self.ws)
         return self.x, pooled
+
+
+class MechanismRun:
+    """The measured single-pair-single program as one training step on the
+    device: forward (Eq. running-block), the joint diagnostic loss, and the
+    backward of every parameter and input, one C-ABI call per op.
+
+    Square pairs take both pair operands from x; rectangular pairs take the
+    column operand from y (M_i rows per sample).  Weight gradients are
+    overwritten every step (fp32); the loss stays on the device as per-sample
+    terms.  Every buffer, scratch included, is allocated here: a step
+    allocates nothing."""
+
+    def __init__(self, w, lengths=None, cols=None, device="cuda"):
+        from . import synth
+        td = torch.bfloat16
+        self.w = w
+        self.lengths = [int(n) for n in (synth.lengths_for(w) if lengths is None else lengths)]
+        c = synth.cols_for(w) if cols is None else cols
+        self.cols = None if c is None else [int(m) for m in c]
+        self.rect = self.cols is not None
+        self.layout = B.NestedLayout(self.lengths, cols=self.cols)
+        lay = self.layout
+        S, Mr, cells = lay.sum_n, lay.sum_m, lay.sum_n2
+        Cx, Cp, F = w.c_s, w.c_z, w.hidden
+        self.params = synth.mechanism_params(w)
+        self.W = to_device(self.params, w.dtype, device)
+        if not self.rect:        # one projection computes u and v from the same rows
+            self.W["uv.w"] = torch.cat([self.W["u.w"], self.W["v.w"]], 0).contiguous()
+            self.W["uv.b"] = torch.cat([self.W["u.b"], self.W["v.b"]], 0).contiguous()
+        self.x_init = synth.normal(w.seed, "mech.x", (S, Cx), 1.0, w.dtype)
+        self.y_init = synth.normal(w.seed, "mech.y", (Mr, Cx), 1.0, w.dtype) if self.rect else None
+        self.x = torch.from_numpy(self.x_init).to(device=device, dtype=td)
+        self.y = torch.from_numpy(self.y_init).to(device=device, dtype=td) if self.rect else None
+        Bn = lay.batch
+        self.alpha = torch.tensor([1.0 + i / Bn for i in range(Bn)], dtype=torch.float32, device=device)
+        self.beta = torch.tensor([1.5 - i / (2.0 * Bn) for i in range(Bn)], dtype=torch.float32, device=device)
+        self.scale_s = 1.0 / (Cx * S)
+        self.scale_p = 1.0 / (Cp * cells)
+        e = lambda *shape, dt=td: torch.empty(shape, dtype=dt, device=device)   # noqa: E731
+        f32 = torch.float32
+        self.uv = e(S, 2 * Cp) if not self.rect else None
+        self.u, self.v = (self.uv[:, :Cp], self.uv[:, Cp:]) if not self.rect else (e(S, Cp), e(Mr, Cp))
+        self.P, self.Pt = e(cells, Cp), e(cells, Cp)
+        self.m = e(S, Cp, dt=f32)
+        self.xt = e(S, Cx)
+        self.loss_s, self.loss_p, self.loss_tmp = e(Bn, dt=f32), e(Bn, dt=f32), e(Bn, dt=f32)
+        self.dxt = e(S, Cx)
+        self.dx = e(S, Cx, dt=f32)
+        self.dy = e(Mr, Cx, dt=f32) if self.rect else None
+        self.dpt, self.dP = e(cells, Cp), e(cells, Cp)
+        self.dm = e(S, Cp, dt=f32)
+        self.duv = e(S, 2 * Cp) if not self.rect else None
+        self.du, self.dv = (self.duv[:, :Cp], self.duv[:, Cp:]) if not self.rect else (e(S, Cp), e(Mr, Cp))
+        self.grads = {k: torch.empty(v.shape, dtype=f32, device=device) for k, v in self.W.items()
+                      if k not in ("uv.w", "uv.b")}
+        if not self.rect:
+            self.grads["uv.w"] = torch.empty((2 * Cp, Cx), dtype=f32, device=device)
+            self.grads["uv.b"] = torch.empty((2 * Cp,), dtype=f32, device=device)
+        # op scratch, used one op at a time on one stream
+        need = [B.layernorm_linear_workspace_bytes(cells, Cp, Cp, w.dtype, epilogue="swiglu_residual", hidden=F),
+                B.loss_workspace_bytes(lay)]
+        need += [self._bwd_ws(cells, Cp, Cp, True, "swiglu_residual", F), self._bwd_ws(S, Cp, Cx, False, "residual", 0),
+                 self._bwd_ws(S, Cx, Cp if self.rect else 2 * Cp, False, "none", 0)]
+        if self.rect:
+            need.append(self._bwd_ws(Mr, Cx, Cp, False, "none", 0))
+        self.scratch = B.workspace_tensor(max(need), device)
+
+    @staticmethod
+    def _bwd_ws(rows, K, N, ln, epi, F):
+        import ctypes
+        a = B.LinearBwdArgs()
+        a.rows, a.c_in, a.c_out = int(rows), int(K), int(N)
+        a.ldx, a.ld_dy, a.ld_dx = K, N, K
+        a.x_dtype = a.dx_dtype = B.NT_BF16
+        a.ln_gamma = ctypes.c_void_p(16) if ln else None
+        a.epilogue, a.hidden = B.EPILOGUES[epi], int(F)
+        n = ctypes.c_uint64()
+        B._check(B.load().nt_layernorm_linear_backward_workspace(ctypes.byref(a), ctypes.byref(n)))
+        return int(n.value)
+
+    def step(self):
+        """Forward, loss and backward; returns (loss terms, xt, pt, grads)."""
+        lay, W, G, ws = self.layout, self.W, self.grads, self.scratch
+        Cp, F = self.w.c_z, self.w.hidden
+        # forward
+        with _op("mech_proj"):
+            if self.rect:
+                B.nt_layernorm_linear(self.x, W["u.w"], W["u.b"], self.u, layout=lay, level="singles")
+                B.nt_layernorm_linear(self.y, W["v.w"], W["v.b"], self.v)
+            else:
+                B.nt_layernorm_linear(self.x, W["uv.w"], W["uv.b"], self.uv, layout=lay, level="singles")
+        with _op("mech_broadcast"):
+            B.nt_pair_broadcast(lay, self.u, self.v, self.P)
+        with _op("mech_transition"):
+            B.nt_layernorm_linear(self.P, W["trans.w"], W["trans.b"], self.Pt, ln=(W["trans.ln_g"], W["trans.ln_b"]),
+                                  epilogue="swiglu_residual", w2=W["trans.w2"], bias2=W["trans.b2"], hidden=F,
+                                  residual=self.P, layout=lay, level="pairs", workspace=ws)
+        with _op("mech_column_mean"):
+            B.nt_segment_reduce(lay, "pairs", "mean", self.Pt, self.m)
+        with _op("mech_single_update"):
+            B.nt_layernorm_linear(self.m, W["g.w"], W["g.b"], self.xt, epilogue="residual", residual=self.x,
+                                  layout=lay, level="singles")
+        # loss (Eq. joint-diagnostic-loss) and its gradient
+        with _op("mech_loss"):
+            B.nt_weighted_square_loss(lay, "singles", self.xt, self.alpha, self.scale_s, self.loss_s, dx=self.dxt,
+                                      workspace=ws)
+            B.nt_weighted_square_loss(lay, "singles", self.xt, self.alpha, self.scale_s, self.loss_tmp, dx=self.dx,
+                                      workspace=ws)
+            B.nt_weighted_square_loss(lay, "pairs", self.Pt, self.beta, self.scale_p, self.loss_p, dx=self.dpt,
+                                      workspace=ws)
+        # backward
+        with _op("mech_single_update_bwd"):
+            B.nt_layernorm_linear_backward(self.m, W["g.w"], self.dxt, epilogue="residual", dx=self.dm, dw=G["g.w"],
+                                           db=G["g.b"], overwrite_weights=True, workspace=ws)
+        with _op("mech_column_mean_bwd"):
+            B.nt_segment_reduce_backward(lay, "pairs", "mean", self.dm, self.dpt, accumulate=True)
+        with _op("mech_transition_bwd"):
+            B.nt_layernorm_linear_backward(self.P, W["trans.w"], self.dpt, ln=(W["trans.ln_g"], W["trans.ln_b"]),
+                                           bias=W["trans.b"], epilogue="swiglu_residual", w2=W["trans.w2"], hidden=F,
+                                           dx=self.dP, dw=G["trans.w"], db=G["trans.b"], dgamma=G["trans.ln_g"],
+                                           dbeta=G["trans.ln_b"], dw2=G["trans.w2"], db2=G["trans.b2"],
+                                           overwrite_weights=True, workspace=ws)
+        with _op("mech_broadcast_bwd"):
+            B.nt_pair_broadcast_backward(lay, self.dP, self.du, self.dv)
+        with _op("mech_proj_bwd"):
+            if self.rect:
+                B.nt_layernorm_linear_backward(self.x, W["u.w"], self.du, dx=self.dx, accumulate_dx=True, dw=G["u.w"],
+                                               db=G["u.b"], overwrite_weights=True, workspace=ws)
+                B.nt_layernorm_linear_backward(self.y, W["v.w"], self.dv, dx=self.dy, dw=G["v.w"], db=G["v.b"],
+                                               overwrite_weights=True, workspace=ws)
+            else:
+                B.nt_layernorm_linear_backward(self.x, W["uv.w"], self.duv, dx=self.dx, accumulate_dx=True,
+                                               dw=G["uv.w"], db=G["uv.b"], overwrite_weights=True, workspace=ws)
+        return self.loss_s, self.loss_p, self.xt, self.Pt

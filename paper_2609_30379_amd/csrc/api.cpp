@@ -30,6 +30,11 @@ nt_status need_device(const nt_layout* L) {
   return NT_OK;
 }
 
+nt_status need_square(const nt_layout* L, const char* op) {
+  if (L && L->rect) return nt::fail(NT_ERR_UNSUPPORTED, std::string(op) + " needs square pairs (N_i x N_i)");
+  return NT_OK;
+}
+
 nt_status need_workspace(size_t need, const void* ws, uint64_t bytes, const char* query) {
   if (need == 0) return NT_OK;
   if (!ws || bytes < need)
@@ -40,7 +45,7 @@ nt_status need_workspace(size_t need, const void* ws, uint64_t bytes, const char
 }
 
 bool same_partition(const nt_layout* a, const nt_layout* b) {
-  return a == b || (a && b && a->lengths == b->lengths);
+  return a == b || (a && b && a->lengths == b->lengths && a->cols == b->cols);
 }
 
 nt_status upload(nt_layout* L, hipStream_t s) {
@@ -56,6 +61,7 @@ nt_status upload(nt_layout* L, hipStream_t s) {
       {&L->sattn_work, &L->d_sattn_work},
       {&L->bc_cu_tiles, &L->d_bc_cu_tiles},
       {&L->cu_qblk, &L->d_cu_qblk},
+      {&L->cu_cols, &L->d_cu_cols},       {&L->col_sample, &L->d_col_sample},
   };
   size_t total = 0;
   for (auto& p : parts) total += (p.v->size() * sizeof(int32_t) + 255) / 256 * 256;
@@ -80,13 +86,14 @@ nt_status upload(nt_layout* L, hipStream_t s) {
   return NT_OK;
 }
 
-nt_status build(const int32_t* lengths, int32_t batch, uint32_t flags, void* stream, nt_layout** out) {
+nt_status build(const int32_t* lengths, int32_t batch, uint32_t flags, void* stream, nt_layout** out,
+                const int32_t* cols = nullptr) {
   if (!out) return nt::fail(NT_ERR_INVALID_ARG, "out is NULL");
   *out = nullptr;
   if (flags & ~(uint32_t)NT_LAYOUT_HOST_ONLY) return nt::fail(NT_ERR_INVALID_ARG, "unknown flags");
   nt_layout* L = new (std::nothrow) nt_layout();
   if (!L) return nt::fail(NT_ERR_OOM, "host allocation failed");
-  nt_status st = nt::plan_layout(lengths, batch, L);
+  nt_status st = nt::plan_layout(lengths, batch, L, cols);
   if (st == NT_OK && !(flags & NT_LAYOUT_HOST_ONLY)) st = upload(L, static_cast<hipStream_t>(stream));
   if (st != NT_OK) {
     nt_layout_destroy(L);
@@ -116,6 +123,13 @@ nt_status nt_from_lengths(const int32_t* lengths, int32_t batch, uint32_t flags,
                           nt_layout** out) {
   g_last_error.clear();
   return build(lengths, batch, flags, stream, out);
+}
+
+nt_status nt_from_rect_lengths(const int32_t* rows, const int32_t* cols, int32_t batch, uint32_t flags, void* stream,
+                               nt_layout** out) {
+  g_last_error.clear();
+  if (!cols) return nt::fail(NT_ERR_INVALID_ARG, "cols is NULL");
+  return build(rows, batch, flags, stream, out, cols);
 }
 
 nt_status nt_from_offsets(const int32_t* cu_seqlens, int32_t batch, uint32_t flags, void* stream,
@@ -155,6 +169,9 @@ nt_status nt_layout_info(const nt_layout* L, nt_layout_info_t* info) {
   info->d_cu_seqlens = L->d_cu_seqlens;
   info->d_cu_pairs = L->d_cu_pairs;
   info->d_row_splits2 = L->d_row_splits2;
+  info->sum_m = L->sum_m;
+  info->rect = L->rect ? 1 : 0;
+  info->d_cu_cols = L->d_cu_cols;
   return NT_OK;
 }
 
@@ -172,6 +189,8 @@ nt_status nt_layout_host_array(const nt_layout* L, nt_array which, const int32_t
     case NT_ARR_TRI_WORK: v = &L->tri_work; break;
     case NT_ARR_SEQ_WORK: v = &L->seq_work; break;
     case NT_ARR_CU_PAD: v = &L->cu_pad; break;
+    case NT_ARR_COLS: v = &L->cols; break;
+    case NT_ARR_CU_COLS: v = &L->cu_cols; break;
     default: return nt::fail(NT_ERR_INVALID_ARG, "unknown array id");
   }
   *data = v->data();
@@ -180,6 +199,7 @@ nt_status nt_layout_host_array(const nt_layout* L, nt_array which, const int32_t
 }
 
 int32_t nt_layouts_compatible(const nt_layout* a, const nt_layout* b) {
+  if (a && b && a != b && (a->rect || b->rect) && a->cols != b->cols) return 0;
   return (a && b && same_partition(a, b)) ? 1 : 0;
 }
 
@@ -215,7 +235,7 @@ nt_status nt_segment_reduce(const nt_layout* L, nt_level level, int32_t op, int3
   const int ve = vec_elems(x_dtype);
   if (C % ve || ld_x % ve || ld_x < C) return nt::fail(NT_ERR_INVALID_ARG, "C and ld_x must be multiples of the vector width, ld_x >= C");
   if (ld_y < C || ld_y % 4) return nt::fail(NT_ERR_INVALID_ARG, "ld_y must be >= C and a multiple of 4");
-  const int64_t out_rows = level != NT_LEVEL_SINGLES ? L->sum_n : L->batch;
+  const int64_t out_rows = level == NT_LEVEL_PAIRS ? L->sum_n : (level == NT_LEVEL_PAIRS_FIRST ? L->sum_m : L->batch);
   if (out_rows == 0) return NT_OK;
   if (!y) return nt::fail(NT_ERR_INVALID_ARG, "y is NULL");
   if (!x && (level != NT_LEVEL_SINGLES ? L->sum_n2 : L->sum_n) > 0) return nt::fail(NT_ERR_INVALID_ARG, "x is NULL");
@@ -226,33 +246,64 @@ nt_status nt_segment_reduce(const nt_layout* L, nt_level level, int32_t op, int3
 }
 
 nt_status nt_pair_broadcast_backward(const nt_layout* L, int32_t C, const void* dz, int64_t ld_dz, nt_dtype dtype,
-                                     float* du, int64_t ld_du, float* dv, int64_t ld_dv, int32_t accumulate,
-                                     void* stream) {
+                                     void* du, int64_t ld_du, void* dv, int64_t ld_dv, nt_dtype out_dtype,
+                                     int32_t accumulate, void* stream) {
   g_last_error.clear();
   if (nt_status st = need_device(L)) return st;
-  if (!valid_dtype(dtype)) return nt::fail(NT_ERR_INVALID_ARG, "bad dtype");
+  if (!valid_dtype(dtype) || !valid_dtype(out_dtype)) return nt::fail(NT_ERR_INVALID_ARG, "bad dtype");
   if (C <= 0 || C % vec_elems(dtype)) return nt::fail(NT_ERR_INVALID_ARG, "C must be > 0 and a multiple of the vector width");
   if (accumulate != 0 && accumulate != 1) return nt::fail(NT_ERR_INVALID_ARG, "accumulate must be 0 or 1");
   if (ld_dz < C || ld_dz % vec_elems(dtype)) return nt::fail(NT_ERR_INVALID_ARG, "bad ld_dz");
-  if ((du && (ld_du < C || ld_du % 4)) || (dv && (ld_dv < C || ld_dv % 4)))
-    return nt::fail(NT_ERR_INVALID_ARG, "ld_du / ld_dv must be >= C and multiples of 4");
-  if (L->sum_n == 0 || (!du && !dv)) return NT_OK;
+  if ((du && ld_du < C) || (dv && ld_dv < C)) return nt::fail(NT_ERR_INVALID_ARG, "ld_du / ld_dv must be >= C");
+  if (L->sum_n2 == 0 || (!du && !dv)) return NT_OK;
   if (!dz) return nt::fail(NT_ERR_INVALID_ARG, "dz is NULL");
-  if (!aligned16(dz) || (du && !aligned16(du)) || (dv && !aligned16(dv)))
-    return nt::fail(NT_ERR_INVALID_ARG, "pointers must be 16-byte aligned");
+  if (!aligned16(dz) || (du && (reinterpret_cast<uintptr_t>(du) & 3u)) || (dv && (reinterpret_cast<uintptr_t>(dv) & 3u)))
+    return nt::fail(NT_ERR_INVALID_ARG, "misaligned pointer");
   const hipStream_t s = static_cast<hipStream_t>(stream);
   if (du) {
-    if (nt_status st = check_hip(nt::launch_segment_reduce(*L, NT_LEVEL_PAIRS, 0, C, dz, ld_dz, dtype, du, ld_du, s, accumulate),
+    if (nt_status st = check_hip(nt::launch_segment_reduce(*L, NT_LEVEL_PAIRS, 0, C, dz, ld_dz, dtype, du, ld_du, s,
+                                                           accumulate, out_dtype),
                                  "nt_pair_broadcast_backward launch"))
       return st;
   }
   if (dv) {
     if (nt_status st = check_hip(nt::launch_segment_reduce(*L, NT_LEVEL_PAIRS_FIRST, 0, C, dz, ld_dz, dtype, dv, ld_dv,
-                                                           s, accumulate),
+                                                           s, accumulate, out_dtype),
                                  "nt_pair_broadcast_backward launch"))
       return st;
   }
   return NT_OK;
+}
+
+nt_status nt_weighted_square_loss_workspace(const nt_layout* L, uint64_t* bytes) {
+  g_last_error.clear();
+  if (!L || !bytes) return nt::fail(NT_ERR_INVALID_ARG, "NULL argument");
+  *bytes = nt::loss_workspace_bytes(*L);
+  return NT_OK;
+}
+
+nt_status nt_weighted_square_loss(const nt_layout* L, nt_level level, int32_t C, const void* x, int64_t ld_x,
+                                  nt_dtype dtype, const float* weights, float scale, float* loss, void* dx,
+                                  int64_t ld_dx, nt_dtype dx_dtype, void* workspace, uint64_t workspace_bytes,
+                                  void* stream) {
+  g_last_error.clear();
+  if (!L) return nt::fail(NT_ERR_INVALID_ARG, "layout is NULL");
+  if (level != NT_LEVEL_SINGLES && level != NT_LEVEL_PAIRS) return nt::fail(NT_ERR_INVALID_ARG, "level must be singles or pairs");
+  if (!valid_dtype(dtype) || !valid_dtype(dx_dtype)) return nt::fail(NT_ERR_INVALID_ARG, "bad dtype");
+  const int ve = vec_elems(dtype);
+  if (C <= 0 || C % ve || ld_x < C || ld_x % ve) return nt::fail(NT_ERR_INVALID_ARG, "C and ld_x must be multiples of the vector width, ld_x >= C");
+  if (dx && ld_dx < C) return nt::fail(NT_ERR_INVALID_ARG, "ld_dx must be >= C");
+  if (!(scale == scale)) return nt::fail(NT_ERR_INVALID_ARG, "scale is NaN");
+  if (nt_status st = need_workspace(nt::loss_workspace_bytes(*L), workspace, workspace_bytes,
+                                    "nt_weighted_square_loss_workspace"))
+    return st;
+  if (nt_status st = need_device(L)) return st;
+  if (!weights || !loss) return nt::fail(NT_ERR_INVALID_ARG, "weights and loss must be non-NULL");
+  if ((L->sum_n > 0 && !x) || (x && !aligned16(x))) return nt::fail(NT_ERR_INVALID_ARG, "x is NULL or misaligned");
+  if (dx && (reinterpret_cast<uintptr_t>(dx) & 3u)) return nt::fail(NT_ERR_INVALID_ARG, "dx misaligned");
+  return check_hip(nt::launch_weighted_square_loss(*L, level, C, x, ld_x, dtype, weights, scale, loss, dx, ld_dx,
+                                                   dx_dtype, workspace, static_cast<hipStream_t>(stream)),
+                   "nt_weighted_square_loss launch");
 }
 
 nt_status nt_segment_reduce_backward(const nt_layout* L, nt_level level, int32_t op, int32_t C, const float* dy,
@@ -295,6 +346,7 @@ nt_status nt_layernorm_linear(const nt_linear_args* a, void* stream) {
     if (a->x) return nt::fail(NT_ERR_INVALID_ARG, "x must be NULL with broadcast rows");
     if (!a->layout || a->level != NT_LEVEL_PAIRS) return nt::fail(NT_ERR_INVALID_ARG, "broadcast rows need a pair-level layout");
     if (!a->layout->has_device) return nt::fail(NT_ERR_INVALID_ARG, "broadcast rows need a layout with device mirrors");
+    if (nt_status st = need_square(a->layout, "broadcast rows")) return st;
     if (a->dtype != NT_BF16 || a->x_dtype != NT_BF16 || (a->c_in != 64 && a->c_in != 128) || a->c_out > 512 ||
         a->c_out % 8 || (a->epilogue != NT_EPI_NONE && a->epilogue != NT_EPI_GELU) || a->n_tail || a->residual)
       return nt::fail(NT_ERR_UNSUPPORTED, "broadcast rows: bf16, c_in in {64, 128}, c_out <= 512 (multiple of 8), "
@@ -319,8 +371,8 @@ nt_status nt_layernorm_linear(const nt_linear_args* a, void* stream) {
   if (a->residual_layout && !same_partition(a->layout, a->residual_layout))
     return nt::fail(NT_ERR_LAYOUT_MISMATCH, "residual has a different logical partition than x");
   if (a->n_tail && a->tail_layout != NT_TAIL_CHANNEL_MAJOR &&
-      (!a->layout || a->level != NT_LEVEL_PAIRS))
-    return nt::fail(NT_ERR_UNSUPPORTED, "pair-tiled tail output needs a pair-level layout");
+      (!a->layout || a->level != NT_LEVEL_PAIRS || a->layout->rect))
+    return nt::fail(NT_ERR_UNSUPPORTED, "pair-tiled tail output needs a square pair-level layout");
   if (swiglu) {
     if (a->dtype == NT_BF16 && (a->c_in != a->c_out || (a->c_in != 64 && a->c_in != 128 && a->c_in != 256) ||
                                 a->hidden <= 0 || a->hidden % 32 || a->x_dtype != NT_BF16))
@@ -410,6 +462,7 @@ nt_status nt_pair_row_attention(const nt_layout* L, int32_t axis, int32_t H, int
   g_last_error.clear();
   if (!L) return nt::fail(NT_ERR_INVALID_ARG, "layout is NULL");
   if (axis < 0 || axis > 3) return nt::fail(NT_ERR_INVALID_ARG, "axis must be 0, 1, 2 or 3");
+  if (axis != 2) if (nt_status st = need_square(L, "pair attention")) return st;
   if (axis == 3 && (dtype != NT_BF16 || D != 32 || L->max_len > nt::kAttnLongLen))
     return nt::fail(NT_ERR_UNSUPPORTED, "single attention with pair bias supports bf16, head_dim 32, N_i <= " +
                                             std::to_string(nt::kAttnLongLen));
@@ -458,6 +511,7 @@ nt_status nt_pair_row_attention_backward(const nt_layout* L, int32_t axis, int32
                                          nt_dtype dtype, void* workspace, uint64_t workspace_bytes, void* stream) {
   g_last_error.clear();
   if (!L) return nt::fail(NT_ERR_INVALID_ARG, "layout is NULL");
+  if (nt_status st = need_square(L, "pair attention")) return st;
   if (axis != 0 && axis != 1) return nt::fail(NT_ERR_UNSUPPORTED, "the attention backward covers axes 0 and 1");
   if (dtype != NT_BF16 || D != 32) return nt::fail(NT_ERR_UNSUPPORTED, "the attention backward needs bf16 and head_dim 32");
   if (H <= 0) return nt::fail(NT_ERR_INVALID_ARG, "heads must be > 0");
@@ -522,6 +576,7 @@ nt_status nt_triangle_mul(const nt_layout* L, int32_t direction, int32_t C, cons
                           void* workspace, uint64_t workspace_bytes, void* stream) {
   g_last_error.clear();
   if (!L) return nt::fail(NT_ERR_INVALID_ARG, "layout is NULL");
+  if (nt_status st = need_square(L, "the triangle update")) return st;
   if (direction != 0 && direction != 1) return nt::fail(NT_ERR_INVALID_ARG, "direction must be 0 or 1");
   if (operands != NT_TRI_PACKED && operands != NT_TRI_PAIR_TILED && operands != NT_TRI_PAIR_TILED_T)
     return nt::fail(NT_ERR_INVALID_ARG, "bad operand layout");
@@ -557,6 +612,7 @@ nt_status nt_triangle_mul_backward(const nt_layout* L, int32_t direction, int32_
                                    nt_dtype dtype, void* workspace, uint64_t workspace_bytes, void* stream) {
   g_last_error.clear();
   if (!L) return nt::fail(NT_ERR_INVALID_ARG, "layout is NULL");
+  if (nt_status st = need_square(L, "the triangle update")) return st;
   if (direction != 0 && direction != 1) return nt::fail(NT_ERR_INVALID_ARG, "direction must be 0 or 1");
   if (!valid_dtype(dtype)) return nt::fail(NT_ERR_INVALID_ARG, "bad dtype");
   if (C <= 0) return nt::fail(NT_ERR_INVALID_ARG, "C must be > 0");

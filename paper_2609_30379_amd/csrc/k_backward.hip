@@ -332,6 +332,7 @@ hipError_t run_linear_backward(const nt_linear_bwd_args& a, void* ws, size_t* by
 
   const bf16* W = (const bf16*)a.w;
   const bf16* dy = (const bf16*)a.dy;
+  const int acc_w = a.overwrite_weights ? 0 : 1;
   const dim3 b256(256);
   // LN(x) (or x) in bf16 as the forward product consumed it, with the row statistics
   const bf16* xin = (const bf16*)a.x;
@@ -372,11 +373,11 @@ hipError_t run_linear_backward(const nt_linear_bwd_args& a, void* ws, size_t* by
         gemm_bf16_kernel<true, false><<<dim3((a.c_out + kBM - 1) / kBM, (F + kBN - 1) / kBN, sw2), b256, 0, s>>>(
             a.c_out, F, R, dy, a.ld_dy, h, F, part_w2, F, 1.f, 0, kc, (int64_t)a.c_out * F);
         reduce_partials_kernel<<<blocks_for((int64_t)a.c_out * F), b256, 0, s>>>(part_w2, sw2, (int64_t)a.c_out * F,
-                                                                                (int64_t)a.c_out * F, a.dw2, 1);
+                                                                                (int64_t)a.c_out * F, a.dw2, acc_w);
       }
       if (a.db2) {
         column_partials_kernel<bf16><<<dim3(groups), b256, 0, s>>>(dy, a.ld_dy, R, a.c_out, kRowsPerGroup, part_col);
-        reduce_partials_kernel<<<blocks_for(a.c_out), b256, 0, s>>>(part_col, groups, a.c_out, a.c_out, a.db2, 1);
+        reduce_partials_kernel<<<blocks_for(a.c_out), b256, 0, s>>>(part_col, groups, a.c_out, a.c_out, a.db2, acc_w);
       }
     }
     g = dp;
@@ -388,11 +389,11 @@ hipError_t run_linear_backward(const nt_linear_bwd_args& a, void* ws, size_t* by
     gemm_bf16_kernel<true, false><<<dim3((Nw + kBM - 1) / kBM, (K + kBN - 1) / kBN, sw), b256, 0, s>>>(
         Nw, K, R, g, ld_g, xin, ld_xin, part_w, K, 1.f, 0, kc, (int64_t)Nw * K);
     reduce_partials_kernel<<<blocks_for((int64_t)Nw * K), b256, 0, s>>>(part_w, sw, (int64_t)Nw * K, (int64_t)Nw * K,
-                                                                        a.dw, 1);
+                                                                        a.dw, acc_w);
   }
   if (a.db) {
     column_partials_kernel<bf16><<<dim3(groups), b256, 0, s>>>(g, ld_g, R, Nw, kRowsPerGroup, part_col);
-    reduce_partials_kernel<<<blocks_for(Nw), b256, 0, s>>>(part_col, groups, Nw, Nw, a.db, 1);
+    reduce_partials_kernel<<<blocks_for(Nw), b256, 0, s>>>(part_col, groups, Nw, Nw, a.db, acc_w);
   }
   const bf16* res = swiglu && a.residual_is_x ? dy : nullptr;
   if (direct_dx) {
@@ -417,9 +418,9 @@ hipError_t run_linear_backward(const nt_linear_bwd_args& a, void* ws, size_t* by
     else { if (dxf) NT_LNB(bf16, float); else NT_LNB(bf16, bf16); }
 #undef NT_LNB
     if (a.dgamma)
-      reduce_partials_kernel<<<blocks_for(K), b256, 0, s>>>(part_g, groups, K, K, a.dgamma, 1);
+      reduce_partials_kernel<<<blocks_for(K), b256, 0, s>>>(part_g, groups, K, K, a.dgamma, acc_w);
     if (a.dbeta)
-      reduce_partials_kernel<<<blocks_for(K), b256, 0, s>>>(part_b, groups, K, K, a.dbeta, 1);
+      reduce_partials_kernel<<<blocks_for(K), b256, 0, s>>>(part_b, groups, K, K, a.dbeta, acc_w);
   } else if (a.dx) {
     // no LayerNorm, bf16 dx = d(LN x)
     if (a.accumulate_dx || res) return hipErrorInvalidValue;

@@ -61,11 +61,62 @@ std::vector<int32_t> xcd_order(const std::vector<std::array<int32_t, W>>& items,
   return out;
 }
 
+// Rectangular pairs (N_i x M_i; Eq. packing with p_i = N_i M_i): row offsets
+// eta over N_i, column offsets kappa over M_i, cell (i, a, b) at
+// o_i + a M_i + b, level-2 splits o_i + a M_i.  The square-only work maps
+// (attention, triangle, pair-tiled operands) are left empty: calls that need
+// them reject rectangular layouts.
+nt_status plan_rect_layout(const int32_t* rows, const int32_t* cols, int32_t batch, nt_layout* L) {
+  L->batch = batch;
+  L->rect = true;
+  L->lengths.assign(rows, rows + batch);
+  L->cols.assign(cols, cols + batch);
+  L->cu_seqlens.assign(batch + 1, 0);
+  L->cu_cols.assign(batch + 1, 0);
+  L->cu_pairs.assign(batch + 1, 0);
+  L->cu_pad.assign(batch + 1, 0);
+  int64_t sn = 0, sm = 0, cells = 0;
+  int32_t mx = 0;
+  for (int32_t i = 0; i < batch; ++i) {
+    const int64_t n = rows[i], m = cols[i];
+    if (n < 0 || m < 0) return fail(NT_ERR_INVALID_ARG, "negative length at sample " + std::to_string(i));
+    sn += n;
+    sm += m;
+    cells += n * m;
+    if (sn > INT32_MAX || sm > INT32_MAX || cells > INT32_MAX)
+      return fail(NT_ERR_OVERFLOW, "packed pair extent exceeds int32 at sample " + std::to_string(i));
+    L->cu_seqlens[i + 1] = (int32_t)sn;
+    L->cu_cols[i + 1] = (int32_t)sm;
+    L->cu_pairs[i + 1] = (int32_t)cells;
+    mx = std::max<int32_t>(mx, (int32_t)std::max(n, m));
+  }
+  L->sum_n = sn;
+  L->sum_m = sm;
+  L->sum_n2 = cells;
+  L->sum_n3 = 0;
+  L->sum_pad = 0;
+  L->max_len = mx;
+  L->row_splits2.assign(sn + 1, 0);
+  L->row_sample.assign(sn, 0);
+  L->col_sample.assign(sm, 0);
+  for (int32_t i = 0; i < batch; ++i) {
+    for (int32_t a = 0; a < rows[i]; ++a) {
+      const int64_t eta = (int64_t)L->cu_seqlens[i] + a;
+      L->row_splits2[eta] = L->cu_pairs[i] + a * cols[i];
+      L->row_sample[eta] = i;
+    }
+    for (int32_t b = 0; b < cols[i]; ++b) L->col_sample[L->cu_cols[i] + b] = i;
+  }
+  L->row_splits2[sn] = (int32_t)cells;
+  return NT_OK;
+}
+
 }  // namespace
 
-nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L) {
+nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L, const int32_t* cols) {
   if (!lengths) return fail(NT_ERR_INVALID_ARG, "lengths is NULL");
   if (batch < 1) return fail(NT_ERR_INVALID_ARG, "batch must be >= 1");
+  if (cols) return plan_rect_layout(lengths, cols, batch, L);
   L->batch = batch;
   L->lengths.assign(lengths, lengths + batch);
   L->cu_seqlens.assign(batch + 1, 0);
@@ -105,6 +156,11 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L) {
     }
   }
   L->row_splits2[sn] = (int32_t)sn2;
+  // square pairs: the column partition is the row partition
+  L->cols = L->lengths;
+  L->cu_cols = L->cu_seqlens;
+  L->col_sample = L->row_sample;
+  L->sum_m = sn;
 
   // first pair row of every kLinRows-cell block of the pair tensor (row tiles
   // of the projections that write pair-tiled outputs)

@@ -34,6 +34,11 @@ struct nt_layout {
   int32_t max_len = 0;
   int64_t sum_n = 0, sum_n2 = 0, sum_n3 = 0;
   int64_t sum_pad = 0;             // sum_i round_up(N_i,16) * round_up(N_i,32): pair-tiled plane extent
+  bool rect = false;               // rectangular pairs N_i x M_i (cols differ from lengths)
+  int64_t sum_m = 0;               // sum_i M_i (= sum_n for square pairs)
+  std::vector<int32_t> cols;         // [B] M_i
+  std::vector<int32_t> cu_cols;      // [B+1] column offsets kappa
+  std::vector<int32_t> col_sample;   // [sum M] sample id of every column
 
   std::vector<int32_t> lengths;      // [B]
   std::vector<int32_t> cu_seqlens;   // [B+1]
@@ -69,6 +74,8 @@ struct nt_layout {
   const int32_t* d_sattn_work = nullptr;
   const int32_t* d_bc_cu_tiles = nullptr;
   const int32_t* d_cu_qblk = nullptr;
+  const int32_t* d_cu_cols = nullptr;
+  const int32_t* d_col_sample = nullptr;
 
   int64_t attn_items() const { return (int64_t)attn_work.size() / 2; }
   int64_t tri_items() const { return (int64_t)tri_work.size() / 4; }
@@ -140,9 +147,16 @@ hipError_t launch_pair_broadcast(const nt_layout& L, int C, const void* u, int64
                                  const void* v, int64_t ld_v, void* z, int64_t ld_z,
                                  int accumulate, nt_dtype dtype, hipStream_t s);
 
+// y in y_dtype (fp32 for the public reduce; bf16 for gradients handed to a product)
 hipError_t launch_segment_reduce(const nt_layout& L, nt_level level, int op, int C,
                                  const void* x, int64_t ld_x, nt_dtype x_dtype,
-                                 float* y, int64_t ld_y, hipStream_t s, int accumulate = 0);
+                                 void* y, int64_t ld_y, hipStream_t s, int accumulate = 0,
+                                 nt_dtype y_dtype = NT_F32);
+
+size_t loss_workspace_bytes(const nt_layout& L);
+hipError_t launch_weighted_square_loss(const nt_layout& L, nt_level level, int C, const void* x, int64_t ld_x,
+                                       nt_dtype dtype, const float* w, float scale, float* loss, void* dx,
+                                       int64_t ld_dx, nt_dtype dx_dtype, void* workspace, hipStream_t s);
 
 hipError_t launch_segment_reduce_backward(const nt_layout& L, nt_level level, int op, int C, const float* dy,
                                           int64_t ld_dy, void* dx, int64_t ld_dx, nt_dtype dtype, int accumulate,
@@ -210,6 +224,7 @@ hipError_t launch_triangle_backward(const nt_layout& L, int direction, int C, co
 
 // Host-side planner (pure C++; no HIP calls).  Fills every host array of the
 // layout from the lengths, or returns an error status.
-nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L);
+// cols non-NULL: rectangular pairs N_i x M_i (M_i = cols[i]).
+nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L, const int32_t* cols = nullptr);
 
 }  // namespace nt

@@ -237,3 +237,41 @@ def test_pair_attention_backward(B, axis, L, H, bias_layout):
     if bias_layout:
         got = host(dbias)
         check_grad(got.T if bias_layout == "heads" else got, rb, what + " dbias")
+
+
+# ------------------------------------------------------------------ rectangular pairs
+@pytest.mark.parametrize("dtype,C", [("bf16", 128), ("f32", 16)])
+def test_rectangular_pair_ops(B, dtype, C):
+    """Broadcast, both pair reductions and their backward on N_i x M_i pairs
+    (ragged rows and columns, an empty row track and an empty column track)."""
+    import torch
+    rows, cols = [5, 0, 37, 64, 3, 7, 1], [9, 4, 1, 70, 0, 13, 2]
+    lay = B.NestedLayout(rows, cols=cols)
+    assert lay.rect and lay.sum_m == sum(cols) and lay.sum_n2 == sum(n * m for n, m in zip(rows, cols))
+    S, M, R = sum(rows), sum(cols), lay.sum_n2
+    u, v = _n(90, "u", (S, C), 0.7, dtype), _n(91, "v", (M, C), 0.7, dtype)
+    z = torch.full((R, C), float("nan"), dtype=torch.bfloat16 if dtype == "bf16" else torch.float32, device="cuda")
+    B.nt_pair_broadcast(lay, dev(u, dtype), dev(v, dtype), z)
+    check(host(z), O.pair_broadcast(u, v, rows, cols=cols), dtype, f"rect broadcast {dtype}")
+    x = _n(92, "x", (R, C), 0.7, dtype)
+    for level, olevel, out_rows in (("pairs", "pair_cols", S), ("pairs_first", "pair_rows", M)):
+        for op in ("sum", "mean"):
+            y = torch.full((out_rows, C), 7.0, dtype=torch.float32, device="cuda")
+            B.nt_segment_reduce(lay, level, op, dev(x, dtype), y)
+            check(host(y), O.segment_reduce(x, rows, olevel, op, cols=cols), "f32", f"rect reduce {level} {op}",
+                  equal_nan=True)
+            dy = _n(93, "dy", (out_rows, C), 1.0, "f32")
+            dx = torch.full((R, C), float("nan"), dtype=z.dtype, device="cuda")
+            B.nt_segment_reduce_backward(lay, level, op, dev(dy, "f32"), dx)
+            check(host(dx), G.segment_reduce_backward(dy, rows, olevel, op, cols=cols), dtype,
+                  f"rect reduce backward {level} {op}")
+    dz = _n(94, "dz", (R, C), 1.0, dtype)
+    du = torch.full((S, C), float("nan"), device="cuda")
+    dv = torch.full((M, C), float("nan"), device="cuda")
+    B.nt_pair_broadcast_backward(lay, dev(dz, dtype), du, dv)
+    ru, rv = G.pair_broadcast_backward(dz, rows, cols)
+    check(host(du), ru, "f32", f"rect broadcast backward du {dtype}")
+    check(host(dv), rv, "f32", f"rect broadcast backward dv {dtype}")
+    # square-only calls reject rectangular layouts
+    with pytest.raises(B.NtError):
+        B.nt_triangle_mul(lay, 0, z, z, z)

@@ -469,3 +469,12 @@ def test_weighted_square_loss_is_its_definition():
     loss, g = ops.weighted_square_loss(x, [2, 3], [1.0, 2.0], 0.5)
     assert loss.tolist() == [0.5 * (0 + 1 + 4 + 9), 0.5 * 2.0 * (16 + 25 + 36 + 49 + 64 + 81)]
     np.testing.assert_array_equal(g, np.concatenate([x[:2], 2.0 * x[2:]]))
+
+
+def test_rectangular_mean_of_an_empty_group_is_nan():
+    """A pair row with no columns (M_i = 0) has an empty column mean: NaN, the
+    dense mean of an empty array; its sum is 0."""
+    x = np.ones((2, 1))
+    m = ops.segment_reduce(x, [2, 3], "pair_cols", "mean", cols=[1, 0])
+    assert m[:2, 0].tolist() == [1.0, 1.0] and np.all(np.isnan(m[2:]))
+    assert ops.segment_reduce(x, [2, 3], "pair_cols", "sum", cols=[1, 0])[2:, 0].tolist() == [0.0, 0.0, 0.0]
