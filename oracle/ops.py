@@ -163,21 +163,28 @@ def single_attention_pair_bias(q, k, v, bias, lengths, heads, head_dim, scale=No
     return layout.pack(outs, (H * d,))
 
 
-def attention_1d(q, k, v, lengths, heads, head_dim, scale=None):
-    """Variable-length self-attention on packed token-major [T, H*d] buffers with
+def attention_1d(q, k, v, lengths, heads, head_dim, scale=None, kv_lengths=None):
+    """Variable-length attention on packed token-major [T, H*d] buffers with
     cumulative lengths (Sec. 3.3 "Attention through packed blocks"): queries
-    of sample i attend to the keys of sample i only; no mask otherwise."""
+    of sample i attend to the keys of sample i only; no mask otherwise.
+    kv_lengths: cross-attention, where sample i has its own number of keys and
+    values (k, v packed by kv_lengths) and the output adopts the query
+    structure; a query with no keys gets 0 (the empty sum)."""
     H, d = int(heads), int(head_dim)
     scale = 1.0 / np.sqrt(d) if scale is None else float(scale)
-    Qs, Ks, Vs = (_single_elements(t, lengths) for t in (q, k, v))
+    kv_lengths = lengths if kv_lengths is None else kv_lengths
+    Qs = _single_elements(q, lengths)
+    Ks, Vs = (_single_elements(t, kv_lengths) for t in (k, v))
     outs = []
     for Q, K, V in zip(Qs, Ks, Vs):
-        N = Q.shape[0]
-        Q, K, V = (t.reshape(N, H, d) for t in (Q, K, V))
+        N, M = Q.shape[0], K.shape[0]
+        Q = Q.reshape(N, H, d)
+        K, V = K.reshape(M, H, d), V.reshape(M, H, d)
         O = np.zeros_like(Q)
         for h in range(H):
-            s = scale * (Q[:, h, :] @ K[:, h, :].T)
-            O[:, h, :] = softmax(s, axis=-1) @ V[:, h, :] if N else O[:, h, :]
+            if N and M:
+                s = scale * (Q[:, h, :] @ K[:, h, :].T)
+                O[:, h, :] = softmax(s, axis=-1) @ V[:, h, :]
         outs.append(O.reshape(N, H * d))
     return layout.pack(outs, (H * d,))
 

@@ -478,3 +478,30 @@ def test_rectangular_mean_of_an_empty_group_is_nan():
     m = ops.segment_reduce(x, [2, 3], "pair_cols", "mean", cols=[1, 0])
     assert m[:2, 0].tolist() == [1.0, 1.0] and np.all(np.isnan(m[2:]))
     assert ops.segment_reduce(x, [2, 3], "pair_cols", "sum", cols=[1, 0])[2:, 0].tolist() == [0.0, 0.0, 0.0]
+
+
+def test_cross_attention_equals_masked_padded_sdpa(torch_cpu):
+    """Cross-attention with different query and key lengths per sample equals
+    padded SDPA with the padded keys masked, on the valid queries; the
+    self-attention case kv_lengths = lengths is attention_1d itself; a sample
+    with queries but no keys gives 0."""
+    Lq, Lk, H, d = [3, 5, 1, 2], [4, 1, 6, 0], 2, 3
+    rng = np.random.default_rng(12)
+    q = rng.standard_normal((sum(Lq), H * d))
+    k, v = rng.standard_normal((sum(Lk), H * d)), rng.standard_normal((sum(Lk), H * d))
+    o = ops.attention_1d(q, k, v, Lq, H, d, kv_lengths=Lk)
+    B, Nq, Nk = len(Lq), max(Lq), max(Lk)
+    qo, ko = layout.single_offsets(Lq), layout.single_offsets(Lk)
+
+    def pad(x, off, n_max):
+        return torch.from_numpy(np.stack([np.pad(x[a:b], ((0, n_max - (b - a)), (0, 0)))
+                                          for a, b in zip(off[:-1], off[1:])]).reshape(B, n_max, H, d)).transpose(1, 2)
+    mask = torch.from_numpy(np.array([[kk < m for kk in range(Nk)] for m in Lk]))[:, None, None, :]
+    ref = torch.nn.functional.scaled_dot_product_attention(pad(q, qo, Nq), pad(k, ko, Nk), pad(v, ko, Nk),
+                                                           attn_mask=mask.expand(B, H, Nq, Nk))
+    ref = ref.transpose(1, 2).reshape(B, Nq, H * d).numpy()
+    for i, n in enumerate(Lq):
+        want = ref[i, :n] if Lk[i] else np.zeros((n, H * d))
+        np.testing.assert_allclose(o[qo[i]:qo[i + 1]], want, rtol=1e-11, atol=1e-11)
+    np.testing.assert_allclose(ops.attention_1d(q, q, q, Lq, H, d, kv_lengths=Lq), ops.attention_1d(q, q, q, Lq, H, d),
+                               rtol=0, atol=0)
