@@ -296,6 +296,72 @@ def bench_single_attention(args, w):
     print(json.dumps(line), flush=True)
 
 
+def bench_cross_attention(args, w):
+    """Cross-attention alone (queries and keys ragged differently): queries on
+    the packed-token workload's lengths, keys and values on lengths from the
+    same distribution drawn with the next seed, hidden 768 as 12 heads of 64.
+    value = query-key scores per second (H * sum N_i M_i / t)."""
+    import numpy as np
+    import torch
+    from paper_2609_30379_amd import binding, synth
+    wt = synth.WORKLOADS["tokens_b64_lognormal230_bf16"]
+    Lq = [int(n) for n in synth.lengths_for(wt)]
+    Lk = [int(n) for n in synth.lengths_for(wt, seed=wt.seed + 1)]
+    H, d = wt.heads, wt.head_dim
+    c = H * d
+    Tq, Tk, NM = sum(Lq), sum(Lk), sum(n * m for n, m in zip(Lq, Lk))
+    lq, lk = binding.NestedLayout(Lq), binding.NestedLayout(Lk)
+    q = torch.from_numpy(synth.normal(wt.seed, "cross_q", (Tq, c), dtype="bf16")).to("cuda", torch.bfloat16)
+    kv = torch.from_numpy(synth.normal(wt.seed, "cross_kv", (Tk, 2 * c), dtype="bf16")).to("cuda", torch.bfloat16)
+    o = torch.empty((Tq, c), dtype=torch.bfloat16, device="cuda")
+    call = lambda: binding.nt_cross_attention(lq, lk, H, d, q, kv[:, :c], kv[:, c:], o)  # noqa: E731
+    ms, us = _time_call(call, args)
+    nbytes = (2 * Tq * c + 2 * Tk * c) * 2
+    flops = 4 * H * d * NM
+    line = {"metric": "query-key scores/sec, cross-attention with different query and key lengths (1 MI355X)",
+            "value": round(H * NM / (ms * 1e-3), 1), "unit": "scores/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": "cross_attention_b64_lognormal230_bf16", "q_lengths": Lq, "kv_lengths": Lk,
+                       "heads": H, "head_dim": d},
+            "roofline": {"bound": "hbm", "achieved": round(nbytes / (us * 1e-6) / 1e9, 2), "peak": HBM_PEAK_GBS,
+                         "unit": "GB/s", "frac": round(nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                         "traffic": None, "algorithmic_bytes": nbytes, "us_per_launch": round(us, 2),
+                         "mfma_frac": round(flops / (us * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 4)}}
+    if not args.no_cpu_baseline:
+        from oracle import ops as oracle_ops
+        i = int(np.argmin([n * m for n, m in zip(Lq, Lk)]))
+        q1 = q[sum(Lq[:i]):sum(Lq[:i + 1])].float().cpu().numpy()
+        kv1 = kv[sum(Lk[:i]):sum(Lk[:i + 1])].float().cpu().numpy()
+        t0, reps = time.perf_counter(), 0
+        while time.perf_counter() - t0 < 1.0:
+            oracle_ops.attention_1d(q1, kv1[:, :c], kv1[:, c:], [Lq[i]], H, d, kv_lengths=[Lk[i]])
+            reps += 1
+        dt = (time.perf_counter() - t0) / reps
+        line["cpu_baseline"] = {"value": round(H * Lq[i] * Lk[i] / dt, 1), "unit": "scores/s",
+                                "cores": torch.get_num_threads(), "kind": "oracle",
+                                "sample": f"sample {i} alone (N={Lq[i]} queries, M={Lk[i]} keys), {reps} runs"}
+    print(json.dumps(line), flush=True)
+
+
+def _time_call(call, args):
+    """(host ms, device us) per call over args.steps calls after args.warmup,
+    HIP events on the launch stream."""
+    import torch
+    for _ in range(max(1, args.warmup)):
+        call()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        call()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / args.steps, ev0.elapsed_time(ev1) * 1e3 / args.steps
+
+
 def _pct(xs, q):
     import numpy as np
     return round(float(np.percentile(np.asarray(xs), q)), 4)
@@ -438,7 +504,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--graph", action="store_true", help="time replays of the step captured into a HIP graph")
     ap.add_argument("--kernels", action="store_true", help="also print the per-op breakdown to stderr")
-    ap.add_argument("--op", choices=["single_attention"], default=None,
+    ap.add_argument("--op", choices=["single_attention", "cross_attention"], default=None,
                     help="time one widened op alone instead of the pair block (its own JSON line)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device-to-device copy (scale reference for HBM counters)")
@@ -464,6 +530,9 @@ def main():
     torch.cuda.set_device(0)
     if args.op == "single_attention":
         bench_single_attention(args, w)
+        return
+    if args.op == "cross_attention":
+        bench_cross_attention(args, w)
         return
     head = measure(w, args.steps, args.warmup, args.graph, cpu=not args.no_cpu_baseline)
     out = {"metric": head.pop("metric"), "value": head.pop("value"), "unit": head.pop("unit"),

@@ -324,6 +324,26 @@ nt_status nt_pair_row_attention(const nt_layout* layout, int32_t axis,
                                 void* o, int64_t ld_o, nt_dtype dtype,
                                 void* workspace, uint64_t workspace_bytes, void* stream);
 
+/* Cross-attention over singles with different query and key lengths (Sec.
+ * 3.3 "Attention through packed blocks": the output takes the query
+ * structure, so queries and keys may be ragged differently).  Sample i has
+ * N_i queries (q_layout) and M_i keys and values (kv_layout); per head h
+ *   o[eta_i + t, h] = sum_k softmax_k(scale q[eta_i + t, h].k[kappa_i + k, h]) v[kappa_i + k, h]
+ * with eta the query offsets and kappa the key offsets.  A query whose sample
+ * has no keys (M_i = 0) gets the empty sum, 0.  Self-attention is
+ * nt_pair_row_attention with axis 2 (the same operation with kv = q layout).
+ *   q_layout, kv_layout  single-level layouts of one batch (equal batch size,
+ *            else NT_ERR_LAYOUT_MISMATCH); only their lengths are used.
+ *   q, o     [sum N, H*d], row strides ld_q, ld_o.
+ *   k, v     [sum M, H*d], common row stride ld_kv (may be NULL when sum M = 0).
+ *   dtype    bf16 (matrix cores, fp32 softmax; head_dim 32 or 64, M_i <= 512)
+ *            or f32 (exact two-pass softmax; head_dim 8, 16, 32, 64; M_i <= 4096).
+ * No workspace.  Errors: NT_ERR_INVALID_ARG, NT_ERR_LAYOUT_MISMATCH,
+ * NT_ERR_UNSUPPORTED (head_dim or key length beyond the limits), NT_ERR_HIP. */
+nt_status nt_cross_attention(const nt_layout* q_layout, const nt_layout* kv_layout, int32_t heads, int32_t head_dim,
+                             const void* q, int64_t ld_q, const void* k, const void* v, int64_t ld_kv,
+                             float scale, void* o, int64_t ld_o, nt_dtype dtype, void* stream);
+
 /* For callers that cannot allocate device memory (code under graph capture,
  * tight serving loops, harnesses that forbid allocation): the same operation
  * and arguments as nt_pair_row_attention without a workspace.  The bias image

@@ -92,6 +92,7 @@ def load(path: str = LIB_PATH):
         "nt_layernorm_linear_workspace": [C.POINTER(LinearArgs), C.POINTER(u64)],
         "nt_pair_row_attention": [vp, i32, i32, i32, vp, vp, vp, i64, vp, i64, i64, f32, vp, i64, C.c_int, vp, u64, vp],
         "nt_pair_row_attention_workspace": [vp, i32, i32, i32, C.c_int, i32, C.POINTER(u64)],
+        "nt_cross_attention": [vp, vp, i32, i32, vp, i64, vp, vp, i64, f32, vp, i64, C.c_int, vp],
         "nt_pair_row_attention_noalloc": [vp, i32, i32, i32, vp, vp, vp, i64, vp, i64, i64, f32, vp, i64, C.c_int, vp],
         "nt_triangle_mul": [vp, i32, i32, vp, vp, i64, C.c_int, vp, i64, C.c_int, vp, u64, vp],
         "nt_triangle_mul_workspace": [vp, i32, C.c_int, C.c_int, C.POINTER(u64)],
@@ -350,6 +351,21 @@ def nt_pair_row_attention(layout: NestedLayout, axis: int, heads: int, head_dim:
     pw, nw = _ws(workspace)
     _check(load().nt_pair_row_attention(layout.handle, int(axis), int(heads), int(head_dim), pq, pk, pv, ld,
                                         pb, ldb, ldbh, scale, po, ldo, dt, pw, nw, _stream()))
+    return o
+
+
+def nt_cross_attention(q_layout: NestedLayout, kv_layout: NestedLayout, heads: int, head_dim: int, q, k, v, o,
+                       scale: float | None = None):
+    """q, o: [sum N, H*d] by q_layout; k, v: [sum M, H*d] by kv_layout (one row stride)."""
+    pq, ldq = _mat(q, "q")
+    pk, ldk = _mat(k, "k")
+    pv, ldv = _mat(v, "v")
+    if ldk != ldv:
+        raise ValueError("k and v must share one row stride")
+    po, ldo = _mat(o, "o")
+    scale = 1.0 / float(np.sqrt(head_dim)) if scale is None else float(scale)
+    _check(load().nt_cross_attention(q_layout.handle, kv_layout.handle, int(heads), int(head_dim), pq, ldq, pk, pv,
+                                     ldk, scale, po, ldo, _dtype(q), _stream()))
     return o
 
 

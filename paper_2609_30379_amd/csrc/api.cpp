@@ -493,6 +493,41 @@ nt_status nt_pair_row_attention(const nt_layout* L, int32_t axis, int32_t H, int
                    "nt_pair_row_attention launch");
 }
 
+nt_status nt_cross_attention(const nt_layout* Lq, const nt_layout* Lkv, int32_t H, int32_t D, const void* q,
+                             int64_t ld_q, const void* k, const void* v, int64_t ld_kv, float scale, void* o,
+                             int64_t ld_o, nt_dtype dtype, void* stream) {
+  g_last_error.clear();
+  if (!Lq || !Lkv) return nt::fail(NT_ERR_INVALID_ARG, "layout is NULL");
+  if (Lq->batch != Lkv->batch)
+    return nt::fail(NT_ERR_LAYOUT_MISMATCH, "query and key layouts hold different batch sizes (" +
+                                                std::to_string(Lq->batch) + " vs " + std::to_string(Lkv->batch) + ")");
+  if (!valid_dtype(dtype)) return nt::fail(NT_ERR_INVALID_ARG, "bad dtype");
+  if (H <= 0 || D <= 0) return nt::fail(NT_ERR_INVALID_ARG, "heads and head_dim must be > 0");
+  if (dtype == NT_BF16 && D != 32 && D != 64)
+    return nt::fail(NT_ERR_UNSUPPORTED, "bf16 cross-attention supports head_dim 32 or 64");
+  if (dtype == NT_F32 && D != 8 && D != 16 && D != 32 && D != 64)
+    return nt::fail(NT_ERR_UNSUPPORTED, "f32 cross-attention supports head_dim 8, 16, 32 or 64");
+  if (dtype == NT_BF16 && Lkv->max_len > nt::kAttnLongLen)
+    return nt::fail(NT_ERR_UNSUPPORTED, "bf16 cross-attention supports at most " + std::to_string(nt::kAttnLongLen) +
+                                            " keys per sample");
+  if (dtype == NT_F32 && Lkv->max_len > 4096)
+    return nt::fail(NT_ERR_UNSUPPORTED, "f32 cross-attention supports at most 4096 keys per sample");
+  const int ve = vec_elems(dtype);
+  const int64_t c = (int64_t)H * D;
+  if (c > ld_q || c > ld_kv || c > ld_o || ld_q % ve || ld_kv % ve || ld_o % ve)
+    return nt::fail(NT_ERR_INVALID_ARG, "row strides must hold H*head_dim and be multiples of the vector width");
+  if (!(scale == scale)) return nt::fail(NT_ERR_INVALID_ARG, "scale is NaN");
+  if (nt_status st = need_device(Lq)) return st;
+  if (nt_status st = need_device(Lkv)) return st;
+  if (Lq->sum_n == 0) return NT_OK;
+  if (!q || !o || (Lkv->sum_n > 0 && (!k || !v))) return nt::fail(NT_ERR_INVALID_ARG, "q, k, v and o must be non-NULL");
+  if (!aligned16(q) || !aligned16(o) || (k && !aligned16(k)) || (v && !aligned16(v)))
+    return nt::fail(NT_ERR_INVALID_ARG, "q, k, v, o must be 16-byte aligned");
+  return check_hip(nt::launch_cross_attention(*Lq, *Lkv, H, D, q, ld_q, k, v, ld_kv, scale, o, ld_o, dtype,
+                                              static_cast<hipStream_t>(stream)),
+                   "nt_cross_attention launch");
+}
+
 nt_status nt_pair_row_attention_backward_workspace(const nt_layout* L, int32_t axis, int32_t H, int32_t D,
                                                    nt_dtype dtype, uint64_t* bytes) {
   g_last_error.clear();

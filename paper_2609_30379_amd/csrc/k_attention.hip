@@ -44,12 +44,14 @@ struct Seg {
   int64_t base, step;    // packed row of element t: base + t * step
   int q_begin, q_end;
   int64_t cu;            // pair offset of the sample (bias addressing)
+  int sample;
 };
 
 template <typename A>
 __device__ __forceinline__ bool segment_of(const A& p, Seg& s) {
   const int i = p.work[2 * blockIdx.x], r = p.work[2 * blockIdx.x + 1];
   if (i < 0) return false;
+  s.sample = i;
   if (p.axis == 2) {
     s.n = p.cu_seqlens[i + 1] - p.cu_seqlens[i];
     s.base = p.cu_seqlens[i];
@@ -636,33 +638,40 @@ __global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_k
   }
 }
 
-// ---------------------------------------------------------------- 1-D attention, head_dim 64
-// Variable-length self-attention over each sample's tokens (Sec. 3.3
-// "Attention through packed blocks"), head_dim 64, N_i <= kAttnLongLen.  A
-// workgroup of 8 waves takes (sample, block of up to 128 queries, head): all
-// keys and values of the sample are copied global -> LDS once (64-dim rows as
-// two 32-dim halves: keys as fragment images, values row-major with the
-// swizzle of the value reads), then each wave runs its 16 queries over 128-key
-// super-chunks -- score products of both halves, one maximum per query, the
-// exponentials and the value products -- with the lazily rescaled running
-// maximum of the pair kernel.  Keys past N repeat key N-1 in LDS and get
+// ---------------------------------------------------------------- 1-D attention, head_dim 32 / 64
+// Variable-length attention over each sample's tokens (Sec. 3.3 "Attention
+// through packed blocks"), head_dim D in {32, 64}, at most NMAX keys per
+// sample.  Queries of sample i are rows cu_q[i] .. cu_q[i+1] and its keys and
+// values rows cu_kv[i] .. cu_kv[i+1]: self-attention passes the same offsets
+// twice; cross-attention passes the key structure separately, and the output
+// takes the query structure (a query whose sample has no keys gets the empty
+// sum, 0).  A workgroup of 8 waves takes (sample, block of up to 128 queries,
+// head): all keys and values of the sample are copied global -> LDS once
+// (32-dim halves: keys as fragment images, values row-major with the swizzle
+// of the value reads), then each wave runs its 16 queries over 128-key
+// super-chunks -- score products, one maximum per query, the exponentials and
+// the value products -- with the lazily rescaled running maximum of the pair
+// kernel.  Keys past the key count repeat the last key in LDS and get
 // probability zero.
 struct SeqAttnArgs {
   const bf16* q;
+  int64_t ld_q;
   const bf16* k;
   const bf16* v;
-  int64_t ld_qkv;
+  int64_t ld_kv;
   float scale_log2;
   bf16* o;
   int64_t ld_o;
-  const int32_t* work;   // quads (sample, first 16-query tile, 0, tile count)
-  const int32_t* cu_seqlens;
+  const int32_t* work;   // quads (sample, first 16-query tile, 0, tile count) over the query layout
+  const int32_t* cu_q;   // query offsets
+  const int32_t* cu_kv;  // key / value offsets (= cu_q for self-attention)
   int H;
 };
 
-template <int NMAX>
+template <int NMAX, int D>
 __global__ void __launch_bounds__(512, NMAX <= 256 ? 4 : 2) attention_seq_kernel(SeqAttnArgs p) {
-  constexpr int D = 64;
+  static_assert(D == 32 || D == 64, "head_dim 32 or 64");
+  constexpr int HV = D / 32;                      // 32-dim halves
   constexpr int KT16 = NMAX / 16;
   extern __shared__ __attribute__((aligned(16))) bf16 lds[];
   const int x = blockIdx.x % kXcds, t = blockIdx.x / kXcds;
@@ -671,38 +680,50 @@ __global__ void __launch_bounds__(512, NMAX <= 256 ? 4 : 2) attention_seq_kernel
   const int i = w4.x;
   if (i < 0) return;
   const int qt0 = w4.y, nqt = w4.w;
-  const int64_t base = p.cu_seqlens[i];
-  const int n = p.cu_seqlens[i + 1] - (int)base;
-  const int npad = (n + 63) & ~63;
-  bf16* Kh0 = lds;                                // key images, dims 0-31: tile of 16 keys -> 512 elements
-  bf16* Kh1 = Kh0 + NMAX * 32;                    // dims 32-63
-  bf16* Vh0 = Kh1 + NMAX * 32;                    // values, row-major [key][32], dims 0-31
-  bf16* Vh1 = Vh0 + NMAX * 32;                    // dims 32-63
+  const int64_t qbase = p.cu_q[i];
+  const int n = p.cu_q[i + 1] - (int)qbase;       // queries of the sample
+  const int64_t kbase = p.cu_kv[i];
+  const int m = p.cu_kv[i + 1] - (int)kbase;      // keys of the sample
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l16 = lane & 15, g = lane >> 4;
-
-  // ---- stage keys and values of the whole sample (tiles below npad)
-  for (int kt = wave; kt < KT16; kt += 8) {
-    if (kt * 16 >= npad) break;
-    const int key_k = min(kt * 16 + l16, n - 1);
-    const int kv = kt * 16 + (lane >> 2), key_v = min(kv, n - 1);
-    const int dgv = (lane & 3) ^ ((kv >> 2) & 3);
-    const bf16* sk = p.k + (base + key_k) * p.ld_qkv + h * D + g * 8;
-    const bf16* sv = p.v + (base + key_v) * p.ld_qkv + h * D + dgv * 8;
-    __builtin_amdgcn_global_load_lds((const void*)sk, (__attribute__((address_space(3))) void*)(Kh0 + kt * 512), 16, 0, 0);
-    __builtin_amdgcn_global_load_lds((const void*)(sk + 32), (__attribute__((address_space(3))) void*)(Kh1 + kt * 512), 16, 0, 0);
-    __builtin_amdgcn_global_load_lds((const void*)sv, (__attribute__((address_space(3))) void*)(Vh0 + kt * 512), 16, 0, 0);
-    __builtin_amdgcn_global_load_lds((const void*)(sv + 32), (__attribute__((address_space(3))) void*)(Vh1 + kt * 512), 16, 0, 0);
-  }
   const int j0 = qt0 * 16;
   const int jw = j0 + 16 * wave + l16;            // this lane's query
   const bool wave_has_queries = wave < nqt && j0 + 16 * wave < n;
   const bool qvalid = jw < n;
-  bf16x8 qf0 = bf16x8{}, qf1 = bf16x8{};
+  if (m == 0) {
+    // no keys: the empty sum
+    if (wave_has_queries && qvalid) {
+      bf16* orow = p.o + (qbase + jw) * p.ld_o + h * D;
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt) *reinterpret_cast<bf16x4*>(orow + dt * 16 + 4 * g) = bf16x4{};
+    }
+    return;
+  }
+  const int npad = (m + 63) & ~63;
+  bf16* Kh[2] = {lds, lds + NMAX * 32};           // key images per 32-dim half: tile of 16 keys -> 512 elements
+  bf16* Vh[2] = {lds + HV * NMAX * 32, lds + (HV + 1) * NMAX * 32};   // values, row-major [key][32] per half
+
+  // ---- stage keys and values of the whole sample (tiles below npad)
+  for (int kt = wave; kt < KT16; kt += 8) {
+    if (kt * 16 >= npad) break;
+    const int key_k = min(kt * 16 + l16, m - 1);
+    const int kv = kt * 16 + (lane >> 2), key_v = min(kv, m - 1);
+    const int dgv = (lane & 3) ^ ((kv >> 2) & 3);
+    const bf16* sk = p.k + (kbase + key_k) * p.ld_kv + h * D + g * 8;
+    const bf16* sv = p.v + (kbase + key_v) * p.ld_kv + h * D + dgv * 8;
+#pragma unroll
+    for (int hv = 0; hv < HV; ++hv) {
+      __builtin_amdgcn_global_load_lds((const void*)(sk + 32 * hv), (__attribute__((address_space(3))) void*)(Kh[hv] + kt * 512), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((const void*)(sv + 32 * hv), (__attribute__((address_space(3))) void*)(Vh[hv] + kt * 512), 16, 0, 0);
+    }
+  }
+  bf16x8 qf[HV];
+#pragma unroll
+  for (int hv = 0; hv < HV; ++hv) qf[hv] = bf16x8{};
   if (qvalid) {
-    const bf16* qr = p.q + (base + jw) * p.ld_qkv + h * D + g * 8;
-    qf0 = *reinterpret_cast<const bf16x8*>(qr);
-    qf1 = *reinterpret_cast<const bf16x8*>(qr + 32);
+    const bf16* qr = p.q + (qbase + jw) * p.ld_q + h * D + g * 8;
+#pragma unroll
+    for (int hv = 0; hv < HV; ++hv) qf[hv] = *reinterpret_cast<const bf16x8*>(qr + 32 * hv);
   }
   __builtin_amdgcn_s_waitcnt(0);                  // this wave's copies have landed
   __syncthreads();
@@ -714,9 +735,10 @@ __global__ void __launch_bounds__(512, NMAX <= 256 ? 4 : 2) attention_seq_kernel
   for (int e = 0; e < 8; ++e) ones[e] = (bf16)1.f;
   const float c = p.scale_log2;
   float m_s = -INFINITY;
-  f32x4 O[5];                                     // dims 0-15, 16-31, 32-47, 48-63, row sum
+  constexpr int NO = D / 16;                      // output accumulators; O[NO] is the row sum
+  f32x4 O[NO + 1];
 #pragma unroll
-  for (int u = 0; u < 5; ++u) O[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int u = 0; u <= NO; ++u) O[u] = f32x4{0.f, 0.f, 0.f, 0.f};
   auto super_chunk = [&](auto sc_c, auto nt_c) {
     constexpr int SC = decltype(sc_c)::value, NT = decltype(nt_c)::value;
     constexpr int T0 = SC * 8;
@@ -724,18 +746,20 @@ __global__ void __launch_bounds__(512, NMAX <= 256 ? 4 : 2) attention_seq_kernel
     f32x4 S[NT];
 #pragma unroll
     for (int kt = 0; kt < NT; ++kt) {
-      const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(&Kh0[(T0 + kt) * 512 + lane * 8]);
-      const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(&Kh1[(T0 + kt) * 512 + lane * 8]);
-      S[kt] = mfma16(k0, qf0, f32x4{0.f, 0.f, 0.f, 0.f});
-      S[kt] = mfma16(k1, qf1, S[kt]);
+      S[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int hv = 0; hv < HV; ++hv) {
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Kh[hv][(T0 + kt) * 512 + lane * 8]);
+        S[kt] = mfma16(kf, qf[hv], S[kt]);
+      }
       if (kt % 4 == 3) __builtin_amdgcn_sched_barrier(0);   // bounded key fragments in flight
     }
-    if (kc + NT * 16 > n) {
+    if (kc + NT * 16 > m) {
 #pragma unroll
       for (int kt = 0; kt < NT; ++kt)
 #pragma unroll
         for (int ii = 0; ii < 4; ++ii)
-          if (kc + kt * 16 + 4 * g + ii >= n) S[kt][ii] = -INFINITY;
+          if (kc + kt * 16 + 4 * g + ii >= m) S[kt][ii] = -INFINITY;
     }
     float mloc = S[0][0];
 #pragma unroll
@@ -748,7 +772,7 @@ __global__ void __launch_bounds__(512, NMAX <= 256 ? 4 : 2) attention_seq_kernel
       const float alpha = __builtin_amdgcn_exp2f((m_s - m_new) * c);
       m_s = m_new;
 #pragma unroll
-      for (int u = 0; u < 5; ++u) O[u] *= alpha;
+      for (int u = 0; u <= NO; ++u) O[u] *= alpha;
     }
     const float nm = -m_s * c;
     bf16x8 P[NT / 2];
@@ -759,32 +783,34 @@ __global__ void __launch_bounds__(512, NMAX <= 256 ? 4 : 2) attention_seq_kernel
         P[kt >> 1][(kt & 1) * 4 + ii] = (bf16)__builtin_amdgcn_exp2f(fmaf(S[kt][ii], c, nm));
 #pragma unroll
     for (int pp = 0; pp + 1 < NT / 2; pp += 2) {
-      bf16x8 va[4], vb[4];
-      vt_frags2(Vh0, SC * 4 + pp, vl, va);
-      vt_frags2(Vh1, SC * 4 + pp, vl, vb);
+      bf16x8 vf[HV][4];
+#pragma unroll
+      for (int hv = 0; hv < HV; ++hv) vt_frags2(Vh[hv], SC * 4 + pp, vl, vf[hv]);
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
-        O[0] = mfma16(va[2 * u], P[pp + u], O[0]);
-        O[1] = mfma16(va[2 * u + 1], P[pp + u], O[1]);
-        O[2] = mfma16(vb[2 * u], P[pp + u], O[2]);
-        O[3] = mfma16(vb[2 * u + 1], P[pp + u], O[3]);
-        O[4] = mfma16(ones, P[pp + u], O[4]);
+#pragma unroll
+        for (int hv = 0; hv < HV; ++hv) {
+          O[2 * hv] = mfma16(vf[hv][2 * u], P[pp + u], O[2 * hv]);
+          O[2 * hv + 1] = mfma16(vf[hv][2 * u + 1], P[pp + u], O[2 * hv + 1]);
+        }
+        O[NO] = mfma16(ones, P[pp + u], O[NO]);
       }
     }
     if constexpr ((NT / 2) % 2 == 1) {
-      bf16x8 va[2], vb[2];
-      vt_frags1(Vh0, SC * 4 + NT / 2 - 1, vl, va);
-      vt_frags1(Vh1, SC * 4 + NT / 2 - 1, vl, vb);
-      O[0] = mfma16(va[0], P[NT / 2 - 1], O[0]);
-      O[1] = mfma16(va[1], P[NT / 2 - 1], O[1]);
-      O[2] = mfma16(vb[0], P[NT / 2 - 1], O[2]);
-      O[3] = mfma16(vb[1], P[NT / 2 - 1], O[3]);
-      O[4] = mfma16(ones, P[NT / 2 - 1], O[4]);
+      bf16x8 vf[HV][2];
+#pragma unroll
+      for (int hv = 0; hv < HV; ++hv) vt_frags1(Vh[hv], SC * 4 + NT / 2 - 1, vl, vf[hv]);
+#pragma unroll
+      for (int hv = 0; hv < HV; ++hv) {
+        O[2 * hv] = mfma16(vf[hv][0], P[NT / 2 - 1], O[2 * hv]);
+        O[2 * hv + 1] = mfma16(vf[hv][1], P[NT / 2 - 1], O[2 * hv + 1]);
+      }
+      O[NO] = mfma16(ones, P[NT / 2 - 1], O[NO]);
     }
   };
   auto run_sc = [&](auto sc_c) {
     constexpr int SC = decltype(sc_c)::value;
-    const int rem = n - SC * 128;
+    const int rem = m - SC * 128;
     if (rem <= 0) return;
     if (rem > 96) super_chunk(sc_c, std::integral_constant<int, 8>{});
     else if (rem > 64) super_chunk(sc_c, std::integral_constant<int, 6>{});
@@ -798,10 +824,10 @@ __global__ void __launch_bounds__(512, NMAX <= 256 ? 4 : 2) attention_seq_kernel
     run_sc(std::integral_constant<int, 3>{});
   }
   if (qvalid) {
-    const float inv = 1.f / O[4][0];
-    bf16* orow = p.o + (base + jw) * p.ld_o + h * D;
+    const float inv = 1.f / O[NO][0];
+    bf16* orow = p.o + (qbase + jw) * p.ld_o + h * D;
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt) {
+    for (int dt = 0; dt < NO; ++dt) {
       bf16x4 ov;
 #pragma unroll
       for (int ii = 0; ii < 4; ++ii) ov[ii] = (bf16)(O[dt][ii] * inv);
@@ -825,23 +851,38 @@ struct AttnF32Args {
   const int32_t* work;
   const int32_t* cu_seqlens;
   const int32_t* cu_pairs;
+  const int32_t* cu_kv;  // axis 2: key / value offsets (= cu_seqlens for self-attention)
+  int64_t ld_q;          // row stride of q (ld_qkv is that of k and v)
 };
 
-// Exact two-pass softmax per query in fp32: one thread per query.
+// Exact two-pass softmax per query in fp32: one thread per query.  On axis 2
+// the keys of sample i are rows cu_kv[i] .. cu_kv[i+1]; a query with no keys
+// gets the empty sum, 0.
 template <int D>
 __global__ void __launch_bounds__(256) attention_f32_kernel(AttnF32Args p) {
   Seg sg;
   if (!segment_of(p, sg)) return;
-  const int h = blockIdx.y, n = sg.n;
+  const int h = blockIdx.y;
+  int n = sg.n;                                   // keys
+  int64_t kbase = sg.base;
+  if (p.axis == 2) {
+    kbase = p.cu_kv[sg.sample];
+    n = p.cu_kv[sg.sample + 1] - (int)kbase;
+  }
   for (int qi = sg.q_begin + (int)threadIdx.x; qi < sg.q_end; qi += 256) {
     const int64_t qrow = sg.base + (int64_t)qi * sg.step;
+    if (n == 0) {
+#pragma unroll
+      for (int d = 0; d < D; ++d) p.o[qrow * p.ld_o + h * D + d] = 0.f;
+      continue;
+    }
     float qv[D];
 #pragma unroll
-    for (int d = 0; d < D; ++d) qv[d] = p.q[qrow * p.ld_qkv + h * D + d];
+    for (int d = 0; d < D; ++d) qv[d] = p.q[qrow * p.ld_q + h * D + d];
     const float* brow = p.bias ? p.bias + (int64_t)h * p.ld_bias_head + (sg.cu + (p.axis == 0 ? (int64_t)qi * n : qi)) * p.ld_bias
                                : nullptr;
     auto logit = [&](int key) {
-      const int64_t krow = sg.base + (int64_t)key * sg.step;
+      const int64_t krow = kbase + (int64_t)key * sg.step;
       float s = 0.f;
 #pragma unroll
       for (int d = 0; d < D; ++d) s = fmaf(qv[d], p.k[krow * p.ld_qkv + h * D + d], s);
@@ -857,7 +898,7 @@ __global__ void __launch_bounds__(256) attention_f32_kernel(AttnF32Args p) {
     for (int key = 0; key < n; ++key) {
       const float e = expf(logit(key) - mx);
       sum += e;
-      const int64_t krow = sg.base + (int64_t)key * sg.step;
+      const int64_t krow = kbase + (int64_t)key * sg.step;
 #pragma unroll
       for (int d = 0; d < D; ++d) acc[d] = fmaf(e, p.v[krow * p.ld_qkv + h * D + d], acc[d]);
     }
@@ -899,6 +940,61 @@ size_t attention_workspace_bytes(const nt_layout& L, int axis, int H, int D, nt_
   return (size_t)H * (size_t)L.bias_tiles_total() * 512;
 }
 
+namespace {
+// 1-D attention on bf16 rows, head_dim 32 or 64: queries by Lq's offsets,
+// keys and values by cu_kv (device) whose longest segment is kv_max_len
+// (<= kAttnLongLen).
+hipError_t launch_seq_attention(const nt_layout& Lq, const int32_t* cu_kv, int kv_max_len, int H, int D,
+                                const void* q, int64_t ld_q, const void* k, const void* v, int64_t ld_kv,
+                                float scale, void* o, int64_t ld_o, hipStream_t s) {
+  if (Lq.sattn_items() == 0) return hipSuccess;
+  if (D != 32 && D != 64) return hipErrorInvalidValue;
+  const bool shortk = kv_max_len <= kAttnShortLen;
+  const int nmax = shortk ? kAttnShortLen : kAttnLongLen;
+  SeqAttnArgs a{(const bf16*)q, ld_q, (const bf16*)k, (const bf16*)v, ld_kv, scale * kLog2e, (bf16*)o, ld_o,
+                Lq.d_sattn_work, Lq.d_cu_seqlens, cu_kv, H};
+  const size_t smem = sizeof(bf16) * 2 * (size_t)(D / 32) * (size_t)nmax * 32;
+  const dim3 grid((unsigned)(Lq.sattn_items() * H)), block(512);
+  const void* fn = D == 64 ? (shortk ? (const void*)attention_seq_kernel<kAttnShortLen, 64>
+                                     : (const void*)attention_seq_kernel<kAttnLongLen, 64>)
+                           : (shortk ? (const void*)attention_seq_kernel<kAttnShortLen, 32>
+                                     : (const void*)attention_seq_kernel<kAttnLongLen, 32>);
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+  if (e != hipSuccess) return e;
+  if (D == 64) {
+    if (shortk) attention_seq_kernel<kAttnShortLen, 64><<<grid, block, smem, s>>>(a);
+    else attention_seq_kernel<kAttnLongLen, 64><<<grid, block, smem, s>>>(a);
+  } else {
+    if (shortk) attention_seq_kernel<kAttnShortLen, 32><<<grid, block, smem, s>>>(a);
+    else attention_seq_kernel<kAttnLongLen, 32><<<grid, block, smem, s>>>(a);
+  }
+  return hipGetLastError();
+}
+}  // namespace
+
+hipError_t launch_cross_attention(const nt_layout& Lq, const nt_layout& Lkv, int H, int D, const void* q,
+                                  int64_t ld_q, const void* k, const void* v, int64_t ld_kv, float scale, void* o,
+                                  int64_t ld_o, nt_dtype dtype, hipStream_t s) {
+  if (Lq.sum_n == 0) return hipSuccess;
+  if (dtype == NT_BF16) {
+    if (Lkv.max_len > kAttnLongLen) return hipErrorInvalidValue;
+    return launch_seq_attention(Lq, Lkv.d_cu_seqlens, Lkv.max_len, H, D, q, ld_q, k, v, ld_kv, scale, o, ld_o, s);
+  }
+  // fp32: the exact kernel, one workgroup per (sample, query block)
+  if (Lq.seq_items() == 0) return hipSuccess;
+  AttnF32Args a{2, H, (const float*)q, (const float*)k, (const float*)v, ld_kv, nullptr, 1, 1, scale, (float*)o,
+                ld_o, Lq.d_seq_work, Lq.d_cu_seqlens, Lq.d_cu_pairs, Lkv.d_cu_seqlens, ld_q};
+  const dim3 grid((unsigned)Lq.seq_items(), (unsigned)H), block(256);
+  switch (D) {
+    case 8: attention_f32_kernel<8><<<grid, block, 0, s>>>(a); break;
+    case 16: attention_f32_kernel<16><<<grid, block, 0, s>>>(a); break;
+    case 32: attention_f32_kernel<32><<<grid, block, 0, s>>>(a); break;
+    case 64: attention_f32_kernel<64><<<grid, block, 0, s>>>(a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_attention(const nt_layout& L, int axis, int H, int D, const void* q, const void* k,
                             const void* v, int64_t ld_qkv, const void* bias, int64_t ld_bias, int64_t ld_bias_head,
                             float scale, void* o, int64_t ld_o, nt_dtype dtype, void* workspace, hipStream_t s) {
@@ -908,7 +1004,8 @@ hipError_t launch_attention(const nt_layout& L, int axis, int H, int D, const vo
   const dim3 grid((unsigned)items, (unsigned)H), block(256);
   if (dtype == NT_F32) {
     AttnF32Args a{axis, H, (const float*)q, (const float*)k, (const float*)v, ld_qkv, (const float*)bias,
-                  ld_bias, ld_bias_head, scale, (float*)o, ld_o, work, L.d_cu_seqlens, L.d_cu_pairs};
+                  ld_bias, ld_bias_head, scale, (float*)o, ld_o, work, L.d_cu_seqlens, L.d_cu_pairs,
+                  L.d_cu_seqlens, ld_qkv};
     switch (D) {
       case 8: attention_f32_kernel<8><<<grid, block, 0, s>>>(a); break;
       case 16: attention_f32_kernel<16><<<grid, block, 0, s>>>(a); break;
@@ -919,22 +1016,8 @@ hipError_t launch_attention(const nt_layout& L, int axis, int H, int D, const vo
     return hipGetLastError();
   }
   const int npad = (L.max_len + 63) & ~63;
-  if (D == 64 && axis == 2 && L.max_len <= kAttnLongLen) {
-    if (L.sattn_items() == 0) return hipSuccess;
-    const int nmax = L.max_len <= kAttnShortLen ? kAttnShortLen : kAttnLongLen;
-    SeqAttnArgs a{(const bf16*)q, (const bf16*)k, (const bf16*)v, ld_qkv, scale * kLog2e, (bf16*)o, ld_o,
-                  L.d_sattn_work, L.d_cu_seqlens, H};
-    const size_t smem = sizeof(bf16) * 4 * (size_t)nmax * 32;
-    const dim3 grid((unsigned)(L.sattn_items() * H));
-    const void* fn = nmax == kAttnShortLen ? (const void*)attention_seq_kernel<kAttnShortLen>
-                                          : (const void*)attention_seq_kernel<kAttnLongLen>;
-    hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-    if (nmax == kAttnShortLen)
-      attention_seq_kernel<kAttnShortLen><<<grid, dim3(512), smem, s>>>(a);
-    else
-      attention_seq_kernel<kAttnLongLen><<<grid, dim3(512), smem, s>>>(a);
-    return hipGetLastError();
-  }
+  if (axis == 2 && L.max_len <= kAttnLongLen)
+    return launch_seq_attention(L, L.d_cu_seqlens, L.max_len, H, D, q, ld_qkv, k, v, ld_qkv, scale, o, ld_o, s);
   if (D == 32 && axis != 2 && L.max_len <= kAttnLongLen) {
     if (L.pattn_items() == 0) return hipSuccess;
     const int nmax = L.max_len <= kAttnShortLen ? kAttnShortLen : kAttnLongLen;

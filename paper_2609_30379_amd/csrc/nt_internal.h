@@ -207,6 +207,13 @@ hipError_t launch_attention(const nt_layout& L, int axis, int H, int D,
                             const void* bias, int64_t ld_bias, int64_t ld_bias_head, float scale,
                             void* o, int64_t ld_o, nt_dtype dtype, void* workspace, hipStream_t s);
 
+// Cross-attention over singles: queries by Lq's offsets, keys and values by
+// Lkv's (same batch); bf16 head_dim 32 / 64 with every key segment at most
+// kAttnLongLen long, or fp32 head_dim 8 / 16 / 32 / 64.
+hipError_t launch_cross_attention(const nt_layout& Lq, const nt_layout& Lkv, int H, int D, const void* q,
+                                  int64_t ld_q, const void* k, const void* v, int64_t ld_kv, float scale, void* o,
+                                  int64_t ld_o, nt_dtype dtype, hipStream_t s);
+
 // Workspace bytes of a triangle call: the re-tiled a and b for packed
 // operands, 0 for pair-tiled ones.
 size_t triangle_workspace_bytes(const nt_layout& L, int C, nt_tri_operands operands, nt_dtype dtype);

@@ -125,9 +125,10 @@ def _draw(rng, dist, batch):
     return np.asarray(n, dtype=np.int32)
 
 
-def lengths_for(w: Workload) -> np.ndarray:
-    """Per-sample lengths N_i (int32) of a workload, from its own seed."""
-    return _draw(np.random.default_rng(w.seed), w.dist, w.batch)
+def lengths_for(w: Workload, seed: int | None = None) -> np.ndarray:
+    """Per-sample lengths N_i (int32) of a workload, from its own seed (or the
+    given one, for a second ragged axis drawn from the same distribution)."""
+    return _draw(np.random.default_rng(w.seed if seed is None else seed), w.dist, w.batch)
 
 
 def cols_for(w: Workload):

@@ -166,6 +166,16 @@ def test_op_argument_errors_need_no_device(lib):
     dev = B.NestedLayout([2, 3], host_only=True)
     assert lib.nt_pair_row_attention(dev.handle, 0, 4, 32, None, None, None, 384, None, 0, 0, 1.0, None, 128,
                                      B.NT_BF16, None, 0, None) == B.NT_ERR_INVALID_ARG    # host-only layout
+    # cross-attention validation: batch mismatch, head_dim, key length, host-only layouts
+    lq, lk = B.NestedLayout([2, 3], host_only=True), B.NestedLayout([4, 0, 1], host_only=True)
+    lk2 = B.NestedLayout([4, 600], host_only=True)
+    ca = lambda a, b, H, D, dt: lib.nt_cross_attention(a.handle, b.handle, H, D, C.c_void_p(16), 64, C.c_void_p(16),  # noqa: E731
+                                                        C.c_void_p(16), 64, 1.0, C.c_void_p(16), 64, dt, None)
+    assert ca(lq, lk, 2, 32, B.NT_BF16) == B.NT_ERR_LAYOUT_MISMATCH
+    assert ca(lq, lk2, 2, 32, B.NT_BF16) == B.NT_ERR_UNSUPPORTED          # more than 512 keys in bf16
+    assert ca(lq, lq, 2, 16, B.NT_BF16) == B.NT_ERR_UNSUPPORTED           # head_dim 16 in bf16
+    assert ca(lq, lq, 4, 32, B.NT_BF16) == B.NT_ERR_INVALID_ARG           # H*d beyond the row strides
+    assert ca(lq, lk2, 2, 32, B.NT_F32) == B.NT_ERR_INVALID_ARG           # fp32 allows it; host-only layout
 
 
 def _q(fn, *args):

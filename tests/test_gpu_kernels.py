@@ -334,6 +334,62 @@ def test_attention_1d(B, dtype, H, D, L):
     check(host(o), ref, dtype, f"1-D attention {dtype}")
 
 
+CROSS_CASES = [("bf16", 3, 64, [1, 5, 64, 130, 0, 200, 77], [3, 0, 64, 512, 10, 1, 256]),
+               ("bf16", 2, 32, [33, 1, 97, 300], [100, 7, 0, 256]),
+               ("bf16", 4, 32, [130, 16, 2], [257, 511, 33]),
+               ("f32", 2, 8, [15, 12, 10, 7, 0, 1], [3, 20, 0, 7, 5, 1]),
+               ("f32", 1, 64, [65, 3], [0, 130])]
+
+
+@pytest.mark.parametrize("dtype,H,D,Lq,Lk", CROSS_CASES)
+def test_cross_attention(B, dtype, H, D, Lq, Lk):
+    """Queries and keys ragged differently (the output takes the query
+    structure); samples with keys but no queries, queries but no keys (the
+    empty sum, 0), up to 512 keys; a second call repeats bit for bit."""
+    import torch
+    lq, lk = _layout(B, Lq), _layout(B, Lk)
+    c = H * D
+    q = _n(26, "q", (sum(Lq), c), 1.0, dtype)
+    kv = _n(27, "kv", (sum(Lk), 2 * c), 1.0, dtype)
+    qd, kvd = dev(q, dtype), dev(kv, dtype)
+    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    o = torch.full((sum(Lq), c), float("nan"), dtype=td, device="cuda")
+    B.nt_cross_attention(lq, lk, H, D, qd, kvd[:, :c], kvd[:, c:], o)
+    ref = O.attention_1d(q, kv[:, :c], kv[:, c:], Lq, H, D, kv_lengths=Lk)
+    check(host(o), ref, dtype, f"cross-attention {dtype} H={H} d={D} Lq={Lq} Lk={Lk}")
+    o2 = torch.full_like(o, float("nan"))
+    B.nt_cross_attention(lq, lk, H, D, qd, kvd[:, :c], kvd[:, c:], o2)
+    assert torch.equal(o, o2)
+
+
+def test_cross_attention_with_equal_lengths_is_self_attention(B):
+    """kv layout = q layout gives the bits of the 1-D self-attention call."""
+    import torch
+    L, H, D = [1, 64, 65, 300, 0, 17], 2, 64
+    lay, lay2 = _layout(B, L), _layout(B, L)
+    c = H * D
+    qkv = dev(_n(28, "qkv", (sum(L), 3 * c)), "bf16")
+    o1 = torch.empty((sum(L), c), dtype=torch.bfloat16, device="cuda")
+    o2 = torch.empty_like(o1)
+    B.nt_pair_row_attention(lay, 2, H, D, qkv[:, :c], qkv[:, c:2 * c], qkv[:, 2 * c:], o1)
+    B.nt_cross_attention(lay, lay2, H, D, qkv[:, :c], qkv[:, c:2 * c], qkv[:, 2 * c:], o2)
+    assert torch.equal(o1, o2)
+
+
+def test_cross_attention_rejects_mismatched_batches_and_long_keys(B):
+    import torch
+    H, D = 2, 32
+    q = torch.zeros((10, H * D), dtype=torch.bfloat16, device="cuda")
+    kv = torch.zeros((600, 2 * H * D), dtype=torch.bfloat16, device="cuda")
+    o = torch.zeros_like(q)
+    with pytest.raises(B.NtError) as e:
+        B.nt_cross_attention(_layout(B, [4, 6]), _layout(B, [600]), H, D, q, kv[:, :64], kv[:, 64:], o)
+    assert e.value.status == B.NT_ERR_LAYOUT_MISMATCH
+    with pytest.raises(B.NtError) as e:
+        B.nt_cross_attention(_layout(B, [4, 6]), _layout(B, [0, 600]), H, D, q, kv[:, :64], kv[:, 64:], o)
+    assert e.value.status == B.NT_ERR_UNSUPPORTED
+
+
 # ------------------------------------------------------------------ triangle
 @pytest.mark.parametrize("direction", [0, 1])
 @pytest.mark.parametrize("dtype,C,lname", [("bf16", 64, "ragged"), ("bf16", 32, "tiny"), ("f32", 16, "tiny"),
