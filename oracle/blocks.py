@@ -18,7 +18,7 @@ from __future__ import annotations
 import numpy as np
 
 from . import ops
-from .numerics import gelu, layernorm, linear, silu, store
+from .numerics import gelu, layernorm, linear, sigmoid, silu, store
 
 
 def _ln_linear(x, w, b, ln, st):
@@ -72,6 +72,32 @@ def ref_triangle(ab, z, C, lengths, direction):
     return z + ops.triangle_mul(ab[:, :C], ab[:, C:], lengths, direction)
 
 
+def ref_attention_gated(qkvg, beta, lengths, C, H, d, axis):
+    """Gated attention (the AlphaFold 3 form of the cited method): on stored
+    [q|k|v|g] ([R, 4C]) and bias, o = sigmoid(g) * attention(q, k, v, bias)."""
+    return ops.pair_row_attention(qkvg[:, :C], qkvg[:, C:2 * C], qkvg[:, 2 * C:3 * C], beta, lengths, H, d,
+                                  axis=axis, gate=qkvg[:, 3 * C:4 * C])
+
+
+def ref_gated_operands(proj, C):
+    """a = sigmoid(a_g) * a_p, b = sigmoid(b_g) * b_p from the stored
+    projection [a_p | a_g | b_p | b_g | g] ([R, 5C])."""
+    return (ops.gated_operand(proj[:, :C], proj[:, C:2 * C]),
+            ops.gated_operand(proj[:, 2 * C:3 * C], proj[:, 3 * C:4 * C]))
+
+
+def ref_triangle_t(a, b, lengths, direction):
+    """t = triangle(a, b) alone (the gated update normalises t before adding it)."""
+    return ops.triangle_mul(a, b, lengths, direction)
+
+
+def ref_gated_out(t, g, z, p, key, st):
+    """z + sigmoid(g) * (LN(t) W_o^T + b_o) with LN(t) stored: the output of
+    the gated triangle update."""
+    return ops.layernorm_linear(st(layernorm(t, *_ln(p, key + ".out"))), p[key + ".wo"], p[key + ".bo"],
+                                epilogue="gated_residual", residual=z, gate=g)
+
+
 def ref_transition(z, p, st):
     """z + SwiGLU(LN(z)) with LN(z) and the gated hidden stored (Eq.
     running-block, second line)."""
@@ -93,6 +119,7 @@ def ref_single_update(m, s, p, st):
 
 PAIR_ORDER_BLOCK = ("bcast", "lin", "att_row", "tri_out", "trans", "single")
 PAIR_ORDER_STACK = ("bcast", "tri_out", "tri_in", "att_row", "att_col", "trans", "single")
+PAIR_ORDER_STACK_GATED = ("bcast", "tri_out_g", "tri_in_g", "att_row_g", "att_col_g", "trans", "single")
 
 
 def pair_block(s, lengths, p, dims, order, z=None, dtype="bf16", round_last=True):
@@ -108,6 +135,12 @@ def pair_block(s, lengths, p, dims, order, z=None, dtype="bf16", round_last=True
       att_col  the same around the ending node (axis 1)
       tri_out  [a|b] = LN(z) W^T + b; z += triangle_outgoing(a, b)
       tri_in   [a|b] = LN(z) W^T + b; z += triangle_incoming(a, b)
+      tri_out_g, tri_in_g   the gated update of AlphaFold 3 (the method Sec.
+               4.3 cites): [a_p|a_g|b_p|b_g|g] = LN(z) W^T + b,
+               a = sigmoid(a_g) a_p, b = sigmoid(b_g) b_p, t = triangle(a, b),
+               z += sigmoid(g) * (LN(t) W_o^T + b_o)
+      att_row_g, att_col_g  gated attention: [q|k|v|g|beta] = LN(z) W^T + b,
+               o = sigmoid(g) * attention, z += o W_o^T + b_o
       trans    z = z + SwiGLU(LN(z))                                (Eq. running-block l.2)
       single   m = mean_b z[.,b];  s = s + m W_s^T + b_s            (Eq. running-block l.3)
     round_last=False returns the output of the final step unrounded (the
@@ -134,6 +167,18 @@ def pair_block(s, lengths, p, dims, order, z=None, dtype="bf16", round_last=True
             o = keep(ref_attention(qkv, beta, lengths, C, H, d, 0 if step == "att_row" else 1))
             trace[step + ".o"] = o
             z = st(ref_attn_out(o, z, p, step))
+        elif step in ("att_row_g", "att_col_g"):
+            proj = keep(ref_ln_linear(z, p, step, keep))
+            qkvg, beta = proj[:, :4 * C], proj[:, 4 * C:4 * C + H]
+            o = keep(ref_attention_gated(qkvg, beta, lengths, C, H, d, 0 if step == "att_row_g" else 1))
+            trace[step + ".o"] = o
+            z = st(ref_attn_out(o, z, p, step))
+        elif step in ("tri_out_g", "tri_in_g"):
+            proj = keep(ref_ln_linear(z, p, step, keep))
+            a, b = (keep(t) for t in ref_gated_operands(proj, C))
+            t = keep(ref_triangle_t(a, b, lengths, "outgoing" if step == "tri_out_g" else "incoming"))
+            trace[step + ".t"] = t
+            z = st(ref_gated_out(t, proj[:, 4 * C:5 * C], z, p, step, keep))
         elif step in ("tri_out", "tri_in"):
             ab = keep(ref_ln_linear(z, p, step, keep))
             z = st(ref_triangle(ab, z, C, lengths, "outgoing" if step == "tri_out" else "incoming"))

@@ -57,6 +57,13 @@ def silu(x):
     return x / (1.0 + np.exp(-x))
 
 
+def sigmoid(x):
+    """1 / (1 + exp(-x)), evaluated without overflow for large |x|."""
+    x = np.asarray(x, np.float64)
+    e = np.exp(-np.abs(x))
+    return np.where(x >= 0, 1.0 / (1.0 + e), e / (1.0 + e))
+
+
 def gelu(x):
     """Exact (erf) GELU."""
     x = np.asarray(x, np.float64)

@@ -14,7 +14,7 @@ from __future__ import annotations
 import numpy as np
 
 from . import layout
-from .numerics import layernorm, linear, silu, gelu, softmax, LN_EPS
+from .numerics import layernorm, linear, silu, gelu, sigmoid, softmax, LN_EPS
 
 
 def _f64(x):
@@ -59,7 +59,7 @@ def pair_broadcast(u, v, lengths, z_in=None, cols=None):
 
 # --------------------------------------------------------------------------- A3
 def layernorm_linear(x, w, b=None, ln=None, eps=LN_EPS, epilogue="none",
-                     w2=None, b2=None, residual=None):
+                     w2=None, b2=None, residual=None, gate=None):
     """Feature transform on packed rows (Sec. 3.3: V' = V W^T + b, normalisation
     on each row's feature tail; Sec. 3.2: feature transforms retain structure).
     Rows are independent, so the packed computation is the dense one on V.
@@ -68,6 +68,9 @@ def layernorm_linear(x, w, b=None, ln=None, eps=LN_EPS, epilogue="none",
     epilogue  "none"            y = LN(x) W^T + b
               "residual"        y = residual + LN(x) W^T + b
               "gelu"            y = gelu(LN(x) W^T + b)   (exact erf form)
+              "gated_residual"  y = residual + sigmoid(gate) * (LN(x) W^T + b),
+                                the output gate of the AlphaFold 3 triangle
+                                update that Sec. 4.3 cites (gate [rows, N])
               "swiglu_residual" the pre-normalised SwiGLU transition of
                                 Eq. running-block (second line, h_theta):
                                 W stacks [W_gate; W_up] (2F x C), then
@@ -81,6 +84,8 @@ def layernorm_linear(x, w, b=None, ln=None, eps=LN_EPS, epilogue="none",
         return y
     if epilogue == "residual":
         return _f64(residual) + y
+    if epilogue == "gated_residual":
+        return _f64(residual) + sigmoid(gate) * y
     if epilogue == "gelu":
         return gelu(y)
     if epilogue == "swiglu_residual":
@@ -106,13 +111,16 @@ def _row_attention_sample(Q, K, V, Bias, scale):
     return O
 
 
-def pair_row_attention(q, k, v, bias, lengths, heads, head_dim, axis=0, scale=None):
+def pair_row_attention(q, k, v, bias, lengths, heads, head_dim, axis=0, scale=None, gate=None):
     """Row (axis=0, around the starting node) or column (axis=1, around the
     ending node) attention with pair bias over a square pair state
     (Sec. 4.3 "A larger pair application", which cites the AlphaFold 3
     Pairformer; the paper gives no formula, see the design notes for this
     reading).  Axis 1 is axis 0 applied to every sample's transpose
     (P'[a,b] = P[b,a] for q, k, v and the bias), transposed back.
+    gate: [sum N^2, H*d] logits of the output gate of the AlphaFold 3 form
+    (the cited method), o <- sigmoid(gate) * o per cell and channel; None:
+    no gate.
     Parity: the formula is a reading; pinned by special cases (zero queries,
     one dominant bias entry, equal lengths = dense batch, masked padded
     attention) and brute force."""
@@ -131,7 +139,8 @@ def pair_row_attention(q, k, v, bias, lengths, heads, head_dim, axis=0, scale=No
         if axis == 1:
             O = O.transpose(1, 0, 2, 3)
         outs.append(O.reshape(N, N, H * d))
-    return layout.pack(outs, (H * d,))
+    out = layout.pack(outs, (H * d,))
+    return out if gate is None else sigmoid(gate) * out
 
 
 def single_attention_pair_bias(q, k, v, bias, lengths, heads, head_dim, scale=None):
@@ -216,6 +225,13 @@ def triangle_mul(a, b, lengths, direction="outgoing"):
         outs.append(np.moveaxis(Tc, 0, 2))
     C = _f64(a).shape[1]
     return layout.pack(outs, (C,))
+
+
+def gated_operand(proj, gate_logits):
+    """sigmoid(gate) * proj, elementwise: the gated projection that forms the
+    operands a and b of the AlphaFold 3 triangle multiplicative update cited
+    in Sec. 4.3 (gated variant; the plain update uses proj directly)."""
+    return sigmoid(gate_logits) * _f64(proj)
 
 
 # --------------------------------------------------------------------------- A6

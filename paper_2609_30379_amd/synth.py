@@ -65,6 +65,7 @@ def _pair_gains(n_max: int, blocks: int = 1) -> dict:
         "ab": float(np.sqrt(0.3 / n_max)) * np.sqrt(damp),
         "gu": 1.0, "d": 0.25 * damp,   # SwiGLU transition
         "s": 0.5,                 # single update from the column mean
+        "gate": 1.0,              # gate logits of the gated (AlphaFold 3 form) steps
     }
 
 
@@ -75,6 +76,8 @@ def _pair_gains(n_max: int, blocks: int = 1) -> dict:
 _TINY = ("bcast", "lin", "att_row", "tri_out", "single")
 _BLOCK = ("bcast", "lin", "att_row", "tri_out", "trans", "single")
 _STACK = ("bcast", "tri_out", "tri_in", "att_row", "att_col", "trans", "single")
+# the same stack with the gated triangle and attention steps of AlphaFold 3
+_STACK_GATED = ("bcast", "tri_out_g", "tri_in_g", "att_row_g", "att_col_g", "trans", "single")
 
 def mechanism_gains() -> dict:
     """Gains of the single-pair-single program: pair state std ~0.5, the
@@ -98,6 +101,11 @@ WORKLOADS = {
                  c_s=384, c_z=128, heads=4, head_dim=32, hidden=512, blocks=4,
                  tri_incoming=True, col_attention=True,
                  gains=_pair_gains(768, blocks=4), steps=_STACK),
+        Workload("pairformer4_gated_b16_lognormal192_bf16", "pair", 16,
+                 ("lognormal", 192.0, 0.6, 16, 768), 0, "bf16",
+                 c_s=384, c_z=128, heads=4, head_dim=32, hidden=512, blocks=4,
+                 tri_incoming=True, col_attention=True,
+                 gains=_pair_gains(768, blocks=4), steps=_STACK_GATED),
         # the measured single-pair-single program (App. A): B=8, C=384,
         # C_p=128, expansion 4; square lengths 66..317, rectangular
         # 66..307 x 66..309 (Table "regimes")
@@ -185,7 +193,8 @@ def pair_block_params(w: Workload, block: int = 0, seed: int | None = None) -> d
     if block == 0:
         p["lin.ln_g"], p["lin.ln_b"] = _ln(seed, pre + "lin", cz)
         p["lin.w"], p["lin.b"] = _linear(seed, pre + "lin", cz, cz, g["lin"], dt)
-    attn = ["row"] + (["col"] if w.col_attention else [])
+    gated = any(s.endswith("_g") for s in w.steps)
+    attn = [] if gated else ["row"] + (["col"] if w.col_attention else [])
     for a in attn:
         p[f"att_{a}.ln_g"], p[f"att_{a}.ln_b"] = _ln(seed, pre + "att_" + a, cz)
         wq, bq = _linear(seed, pre + f"att_{a}.qkv", 3 * cz, cz, g["qkv"], dt)
@@ -193,7 +202,25 @@ def pair_block_params(w: Workload, block: int = 0, seed: int | None = None) -> d
         p[f"att_{a}.w"] = np.concatenate([wq, wb], 0)
         p[f"att_{a}.b"] = np.concatenate([bq, bb], 0)
         p[f"att_{a}.wo"], p[f"att_{a}.bo"] = _linear(seed, pre + f"att_{a}.o", cz, cz, g["o"], dt)
-    tri = ["out"] + (["in"] if w.tri_incoming else [])
+    for key in [s for s in w.steps if s.startswith("att_") and s.endswith("_g")]:
+        # [q | k | v | g | bias]: the gate logits before the bias tail
+        p[f"{key}.ln_g"], p[f"{key}.ln_b"] = _ln(seed, pre + key, cz)
+        parts = [_linear(seed, pre + f"{key}.qkv", 3 * cz, cz, g["qkv"], dt),
+                 _linear(seed, pre + f"{key}.gate", cz, cz, g["gate"], dt),
+                 _linear(seed, pre + f"{key}.bias", H, cz, g["bias"], dt)]
+        p[f"{key}.w"] = np.concatenate([a for a, _ in parts], 0)
+        p[f"{key}.b"] = np.concatenate([b for _, b in parts], 0)
+        p[f"{key}.wo"], p[f"{key}.bo"] = _linear(seed, pre + f"{key}.o", cz, cz, g["o"], dt)
+    for key in [s for s in w.steps if s.startswith("tri_") and s.endswith("_g")]:
+        # [a_p | a_g | b_p | b_g | g], then LN(t) and the output projection
+        p[f"{key}.ln_g"], p[f"{key}.ln_b"] = _ln(seed, pre + key, cz)
+        parts = [_linear(seed, pre + f"{key}.{nm}", cz, cz, g["ab"] if nm in ("ap", "bp") else g["gate"], dt)
+                 for nm in ("ap", "ag", "bp", "bg", "g")]
+        p[f"{key}.w"] = np.concatenate([a for a, _ in parts], 0)
+        p[f"{key}.b"] = np.concatenate([b for _, b in parts], 0)
+        p[f"{key}.out.ln_g"], p[f"{key}.out.ln_b"] = _ln(seed, pre + key + ".out", cz)
+        p[f"{key}.wo"], p[f"{key}.bo"] = _linear(seed, pre + f"{key}.o", cz, cz, g["o"], dt)
+    tri = [] if gated else ["out"] + (["in"] if w.tri_incoming else [])
     for t in tri:
         p[f"tri_{t}.ln_g"], p[f"tri_{t}.ln_b"] = _ln(seed, pre + "tri_" + t, cz)
         p[f"tri_{t}.w"], p[f"tri_{t}.b"] = _linear(seed, pre + f"tri_{t}", 2 * cz, cz, g["ab"], dt)

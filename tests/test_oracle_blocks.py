@@ -11,10 +11,10 @@ from oracle import blocks, layout
 from paper_2609_30379_amd import synth
 
 
-def _params(c_s, c_z, H, hidden, seed, transition=True, cols=True, tri_in=True):
+def _params(c_s, c_z, H, hidden, seed, transition=True, cols=True, tri_in=True, steps=()):
     w = synth.Workload("t", "pair", 1, ("uniform", 1, 1), seed, "f32", c_s=c_s, c_z=c_z, heads=H,
                        head_dim=c_z // H, hidden=hidden, transition=transition,
-                       tri_incoming=tri_in, col_attention=cols, gains=synth._pair_gains(8))
+                       tri_incoming=tri_in, col_attention=cols, gains=synth._pair_gains(8), steps=steps)
     return synth.pair_block_params(w, block=0, seed=seed)
 
 
@@ -36,16 +36,29 @@ def _padded_pair_block(s, L, p, H, d, order, z=None):
         return F.linear(F.layer_norm(x, (x.shape[-1],), T(p[key + ".ln_g"]), T(p[key + ".ln_b"]), 1e-5),
                         T(p[key + ".w"]), T(p[key + ".b"]))
 
-    def att(zz, key):
+    def att(zz, key, gated=False):
         proj = lnlin(zz, key)
         q = proj[..., :C].reshape(B, N, N, H, d)
         k = proj[..., C:2 * C].reshape(B, N, N, H, d)
         v = proj[..., 2 * C:3 * C].reshape(B, N, N, H, d)
-        bias = proj[..., 3 * C:3 * C + H]                         # [B, j, k, H]
+        nb = 4 * C if gated else 3 * C                            # gated: [q|k|v|g|bias]
+        bias = proj[..., nb:nb + H]                               # [B, j, k, H]
         logits = torch.einsum("brjhd,brkhd->brhjk", q, k) / np.sqrt(d) + bias.permute(0, 3, 1, 2)[:, None]
         logits = logits.masked_fill(~valid[:, None, None, None, :], float("-inf"))
         o = torch.einsum("brhjk,brkhd->brjhd", torch.softmax(logits, -1), v).reshape(B, N, N, C)
+        if gated:
+            o = torch.sigmoid(proj[..., 3 * C:4 * C]) * o
         return zz + F.linear(o, T(p[key + ".wo"]), T(p[key + ".bo"]))
+
+    def tri_gated(zz, key):
+        # AlphaFold 3 form: gated operands, t, LayerNorm of t, output gate
+        proj = lnlin(zz, key)
+        a = torch.sigmoid(proj[..., C:2 * C]) * proj[..., :C] * cellmask[..., None]
+        b = torch.sigmoid(proj[..., 3 * C:4 * C]) * proj[..., 2 * C:3 * C] * cellmask[..., None]
+        eq = "bxkc,bykc->bxyc" if key == "tri_out_g" else "bkxc,bkyc->bxyc"
+        t = torch.einsum(eq, a, b)
+        tn = F.layer_norm(t, (C,), T(p[key + ".out.ln_g"]), T(p[key + ".out.ln_b"]), 1e-5)
+        return zz + torch.sigmoid(proj[..., 4 * C:5 * C]) * F.linear(tn, T(p[key + ".wo"]), T(p[key + ".bo"]))
 
     for step in order:
         if step == "bcast":
@@ -58,6 +71,12 @@ def _padded_pair_block(s, L, p, H, d, order, z=None):
             z = att(z, "att_row")
         elif step == "att_col":
             z = att(z.transpose(1, 2), "att_col").transpose(1, 2)
+        elif step == "att_row_g":
+            z = att(z, step, gated=True)
+        elif step == "att_col_g":
+            z = att(z.transpose(1, 2), step, gated=True).transpose(1, 2)
+        elif step in ("tri_out_g", "tri_in_g"):
+            z = tri_gated(z, step)
         elif step in ("tri_out", "tri_in"):
             ab = lnlin(z, step) * cellmask[..., None]
             a, b = ab[..., :C], ab[..., C:]
@@ -81,10 +100,12 @@ def _padded_pair_block(s, L, p, H, d, order, z=None):
     ([5, 3, 1, 4], blocks.PAIR_ORDER_BLOCK),
     ([4, 6, 2], blocks.PAIR_ORDER_STACK),
     ([3, 3, 3], blocks.PAIR_ORDER_BLOCK),     # all-equal lengths: ordinary dense batching
+    ([4, 6, 2, 1], blocks.PAIR_ORDER_STACK_GATED),
+    ([3, 3], blocks.PAIR_ORDER_STACK_GATED),
 ])
 def test_pair_block_equals_masked_padded(L, order):
     c_s, c_z, H = 12, 8, 2
-    p = _params(c_s, c_z, H, 16, seed=7)
+    p = _params(c_s, c_z, H, 16, seed=7, steps=order)
     s = synth.normal(7, "s", (sum(L), c_s))
     dims = dict(c_z=c_z, heads=H, head_dim=c_z // H)
     s_o, z_o, _ = blocks.pair_block(s, L, p, dims, order, dtype="f32")
@@ -204,3 +225,60 @@ def test_mechanism_loss_closed_form():
     want = (1.0 * np.sum(xt[:2] ** 2) + 1.5 * np.sum(xt[2:] ** 2)) / (C * 5) + \
         (1.5 * np.sum(pt[:8] ** 2) + 1.25 * np.sum(pt[8:] ** 2)) / (Cp * 11)
     assert abs(out["loss"] - want) < 1e-12 * max(1.0, want)
+
+
+def test_gated_steps_reduce_to_their_ungated_parts_when_the_gates_saturate():
+    """Gate logits driven to +inf (large gate biases) make every sigmoid 1:
+    the gated attention step is then the plain one with the same q, k, v and
+    bias, and the gated triangle step is z + LN(t) W_o + b_o with t the plain
+    contraction of a_p and b_p; logits driven to -inf leave z unchanged."""
+    from oracle import ops
+    from oracle.numerics import layernorm, linear
+    L, c_s, C, H = [4, 2, 5], 6, 8, 2
+    d = C // H
+    s = synth.normal(11, "s", (sum(L), c_s))
+    z0 = synth.normal(11, "z", (layout.pair_offsets(L)[-1], C))
+    dims = dict(c_z=C, heads=H, head_dim=d)
+    for sign in (1.0, -1.0):
+        p = _params(c_s, C, H, 16, seed=11, steps=blocks.PAIR_ORDER_STACK_GATED)
+        for key in ("att_row_g", "att_col_g"):
+            p[key + ".b"] = p[key + ".b"].copy()
+            p[key + ".b"][3 * C:4 * C] = 60.0 * sign
+        for key in ("tri_out_g", "tri_in_g"):
+            p[key + ".b"] = p[key + ".b"].copy()
+            p[key + ".b"][C:2 * C] = 60.0
+            p[key + ".b"][3 * C:4 * C] = 60.0
+            p[key + ".b"][4 * C:5 * C] = 60.0 * sign
+        for key, axis in (("att_row_g", 0), ("att_col_g", 1)):
+            _, z_g, _ = blocks.pair_block(s, L, p, dims, (key,), z=z0, dtype="f32")
+            if sign < 0:
+                np.testing.assert_allclose(z_g, z0 + linear(np.zeros((len(z0), C)), p[key + ".wo"], p[key + ".bo"]),
+                                           rtol=1e-12, atol=1e-12)
+                continue
+            proj = linear(layernorm(z0, p[key + ".ln_g"], p[key + ".ln_b"]), p[key + ".w"], p[key + ".b"])
+            o = ops.pair_row_attention(proj[:, :C], proj[:, C:2 * C], proj[:, 2 * C:3 * C], proj[:, 4 * C:4 * C + H],
+                                       L, H, d, axis=axis)
+            np.testing.assert_allclose(z_g, z0 + linear(o, p[key + ".wo"], p[key + ".bo"]), rtol=1e-12, atol=1e-12)
+        for key, direction in (("tri_out_g", "outgoing"), ("tri_in_g", "incoming")):
+            _, z_g, _ = blocks.pair_block(s, L, p, dims, (key,), z=z0, dtype="f32")
+            if sign < 0:
+                np.testing.assert_allclose(z_g, z0, rtol=0, atol=1e-20)
+                continue
+            proj = linear(layernorm(z0, p[key + ".ln_g"], p[key + ".ln_b"]), p[key + ".w"], p[key + ".b"])
+            t = ops.triangle_mul(proj[:, :C], proj[:, 2 * C:3 * C], L, direction)
+            want = z0 + linear(layernorm(t, p[key + ".out.ln_g"], p[key + ".out.ln_b"]), p[key + ".wo"], p[key + ".bo"])
+            np.testing.assert_allclose(z_g, want, rtol=1e-12, atol=1e-12)
+
+
+def test_gated_attention_gate_scales_the_output():
+    """o = sigmoid(g) * attention: g = 0 halves the plain attention output."""
+    from oracle import ops
+    L, H, d = [3, 5, 1], 2, 4
+    R = layout.pair_offsets(L)[-1]
+    rng = np.random.default_rng(4)
+    q, k, v = (rng.standard_normal((R, H * d)) for _ in range(3))
+    bias = rng.standard_normal((R, H))
+    for axis in (0, 1):
+        plain = ops.pair_row_attention(q, k, v, bias, L, H, d, axis=axis)
+        half = ops.pair_row_attention(q, k, v, bias, L, H, d, axis=axis, gate=np.zeros((R, H * d)))
+        np.testing.assert_allclose(half, 0.5 * plain, rtol=1e-14, atol=1e-14)

@@ -157,3 +157,32 @@ def test_padded_block_pin_catches_a_triangle_mistake(monkeypatch):
     monkeypatch.setattr(ops, "triangle_mul", _mut_triangle_transposed)
     from oracle import blocks
     assert _fails(T_blk.test_pair_block_equals_masked_padded, [4, 6, 2], blocks.PAIR_ORDER_STACK)
+
+
+def _mut_gated_operand_roles_swapped(proj, gate_logits):
+    return numerics.sigmoid(proj) * np.asarray(gate_logits, np.float64)
+
+
+def _mut_attention_gate_ignored(q, k, v, bias, lengths, heads, head_dim, axis=0, scale=None, gate=None):
+    return _orig["pair_row_attention"](q, k, v, bias, lengths, heads, head_dim, axis, scale)
+
+
+def _mut_gated_residual_ungated(x, w, b=None, ln=None, eps=1e-5, epilogue="none", w2=None, b2=None, residual=None,
+                                gate=None):
+    if epilogue == "gated_residual":
+        epilogue, gate = "residual", None
+    return _orig_lin(x, w, b, ln, eps, epilogue, w2, b2, residual, gate)
+
+
+_orig_lin = ops.layernorm_linear
+
+
+@pytest.mark.parametrize("attr,mutant", [("gated_operand", _mut_gated_operand_roles_swapped),
+                                         ("pair_row_attention", _mut_attention_gate_ignored),
+                                         ("layernorm_linear", _mut_gated_residual_ungated)])
+def test_padded_block_pin_catches_gated_step_mistakes(monkeypatch, attr, mutant):
+    """Swapped gate and projection roles, an ignored attention gate and an
+    ungated triangle output each fail the masked padded pin of the gated stack."""
+    monkeypatch.setattr(ops, attr, mutant)
+    from oracle import blocks
+    assert _fails(T_blk.test_pair_block_equals_masked_padded, [4, 6, 2, 1], blocks.PAIR_ORDER_STACK_GATED)
