@@ -113,6 +113,18 @@ def op_costs(w, L):
         "transition": (R * 2 * C * e, 2 * R * (C * 2 * F + F * C)),
         "segment_mean": (R * C * e + S * C * 4, R * C),
         "single_update": (S * (C * 4 + 2 * Cs * e), 2 * S * C * Cs),
+        # gated (AlphaFold 3 form) steps: [q|k|v|g] + bias projection; gated
+        # attention (q, k, v, g, bias read, o written); [a_p|a_g|b_p|b_g] and
+        # g projections (z read twice); the contraction on gated operands
+        # (a_p, a_g, b_p, b_g read, t written); LN(t) W_o gated residual (t,
+        # g, z read, z written)
+        "attn_proj_g": (R * (C + 4 * C + H) * e, 2 * R * C * (4 * C + H)),
+        "attention_row_g": (R * (5 * H * d + H) * e, 4 * H * d * N3),
+        "attention_col_g": (R * (5 * H * d + H) * e, 4 * H * d * N3),
+        "tri_proj_g": (R * (2 * C + 5 * C) * e, 2 * R * C * 5 * C),
+        "triangle_out_g": (R * 5 * C * e, 2 * C * N3),
+        "triangle_in_g": (R * 5 * C * e, 2 * C * N3),
+        "tri_out_gated_residual": (R * 4 * C * e, 2 * R * C * C),
     }
     return c
 
@@ -489,8 +501,9 @@ def measure(w, steps: int, warmup: int, graph: bool = False, cpu: bool = False):
     return out
 
 
-NESTED = ("pair_b8_n208_224_bf16", "pair_b8_n32_512_bf16", "tokens_b64_lognormal230_bf16",
-          "mechanism_square_b8_n66_317_bf16", "mechanism_rect_b8_n66_307_m66_309_bf16")
+NESTED = ("pair_b8_n208_224_bf16", "pair_b8_n32_512_bf16", "pairformer4_gated_b16_lognormal192_bf16",
+          "tokens_b64_lognormal230_bf16", "mechanism_square_b8_n66_317_bf16",
+          "mechanism_rect_b8_n66_307_m66_309_bf16")
 
 
 def main():
@@ -546,7 +559,7 @@ def main():
             if name == w.name:
                 continue
             r = measure(synth.WORKLOADS[name], args.steps, args.warmup, args.graph, cpu=False)
-            if synth.WORKLOADS[name].kind != "mechanism":
+            if synth.WORKLOADS[name].kind != "mechanism" and "gated" not in name:
                 r.pop("kernels")
             nested[name] = r
         out["other_workloads"] = nested

@@ -82,7 +82,14 @@ typedef enum {
   NT_EPI_RESIDUAL = 1,         /* y = residual + LN(x) W^T + b                       */
   NT_EPI_SWIGLU_RESIDUAL = 2,  /* y = residual + (silu(g) * u) W2^T + b2,
                                   [g|u] = LN(x) W^T + b (W stacks W_gate; W_up)       */
-  NT_EPI_GELU = 3              /* y = gelu(LN(x) W^T + b), exact erf form            */
+  NT_EPI_GELU = 3,             /* y = gelu(LN(x) W^T + b), exact erf form            */
+  NT_EPI_GATED_RESIDUAL = 4,   /* y = residual + sigmoid(gate) * (LN(x) W^T + b): the
+                                  output gate of the AlphaFold 3 triangle update
+                                  cited in Sec. 4.3 (gate: [R, N] logits)             */
+  NT_EPI_SIGMOID_GLU = 5       /* gated operands of that update: W has 2N rows in
+                                  blocks of 2G (G = hidden), [projection; gate];
+                                  y[:, G q + c] = sigmoid(p[:, 2G q + G + c]) *
+                                  p[:, 2G q + c] with p = LN(x) W^T + b            */
 } nt_epilogue;
 
 typedef enum {
@@ -260,6 +267,11 @@ typedef struct {
    * when the call needs none.                                              */
   void* workspace;
   uint64_t workspace_bytes;
+  /* NT_EPI_GATED_RESIDUAL: gate logits [R, N] in dtype, row stride ld_gate
+   * (>= N, a multiple of 8 for bf16 / 4 for f32, 16-byte aligned); NULL for
+   * every other epilogue.  No tail with this epilogue.                     */
+  const void* gate;
+  int64_t ld_gate;
 } nt_linear_args;
 
 /* Workspace (args->workspace, args->workspace_bytes): two kinds of bf16 call
@@ -273,7 +285,9 @@ typedef struct {
  * Errors: NT_ERR_INVALID_ARG (also a missing or too small workspace),
  * NT_ERR_LAYOUT_MISMATCH (residual_layout differs
  * from layout, or rows differ from the layout's count), NT_ERR_UNSUPPORTED
- * (bf16 SwiGLU unless x is bf16, K == N in {64, 128, 256} and F % 32 == 0;
+ * (NT_EPI_SIGMOID_GLU unless bf16, K == 128, hidden == 128, N == 256 and
+ * every output column in a pair-tiled tail (n_tail == N);
+ * bf16 SwiGLU unless x is bf16, K == N in {64, 128, 256} and F % 32 == 0;
  * f32 SwiGLU with K > 1024 or F > 4096; n_tail with SwiGLU; a pair-tiled
  * tail without a pair layout), NT_ERR_HIP (also when the workspace cannot be
  * allocated).  ln_gamma/ln_beta must be 16-byte aligned.                     */
@@ -323,6 +337,22 @@ nt_status nt_pair_row_attention(const nt_layout* layout, int32_t axis,
                                 const void* bias, int64_t ld_bias, int64_t ld_bias_head, float scale,
                                 void* o, int64_t ld_o, nt_dtype dtype,
                                 void* workspace, uint64_t workspace_bytes, void* stream);
+
+/* Gated pair attention (the AlphaFold 3 form of the triangle attention that
+ * Sec. 4.3 cites): nt_pair_row_attention on axis 0 or 1, with the output
+ * multiplied by the sigmoid of per-cell, per-channel gate logits:
+ *   o[cell, c] = sigmoid(gate[cell, c]) * attention[cell, c],  c < H*d
+ * gate: [sum N^2, >= H*d] in dtype, row stride ld_gate (a multiple of 8 for
+ * bf16 / 4 for f32, 16-byte aligned); it may be a column slice of the
+ * projection that produced q, k and v.  Other arguments, workspace and
+ * errors as nt_pair_row_attention (also NT_ERR_INVALID_ARG for axes 2 and 3
+ * or a NULL gate).                                                         */
+nt_status nt_pair_row_attention_gated(const nt_layout* layout, int32_t axis, int32_t heads, int32_t head_dim,
+                                      const void* q, const void* k, const void* v, int64_t ld_qkv,
+                                      const void* gate, int64_t ld_gate,
+                                      const void* bias, int64_t ld_bias, int64_t ld_bias_head, float scale,
+                                      void* o, int64_t ld_o, nt_dtype dtype,
+                                      void* workspace, uint64_t workspace_bytes, void* stream);
 
 /* Cross-attention over singles with different query and key lengths (Sec.
  * 3.3 "Attention through packed blocks": the output takes the query
@@ -395,6 +425,29 @@ nt_status nt_triangle_mul(const nt_layout* layout, int32_t direction, int32_t C,
                           const void* a, const void* b, int64_t ld_ab, nt_tri_operands operands,
                           void* z, int64_t ld_z, nt_dtype dtype,
                           void* workspace, uint64_t workspace_bytes, void* stream);
+
+/* Contraction of the gated triangle update (the AlphaFold 3 form of the
+ * update that Sec. 4.3 cites): the operands are gated projections,
+ *   a = sigmoid(a_g) * a_p,  b = sigmoid(b_g) * b_p   (elementwise, fp32, rounded once)
+ * and the contraction t (outgoing / incoming as nt_triangle_mul) is written
+ * to t, not added (the gated update normalises t before its own gated
+ * residual: nt_layernorm_linear with NT_EPI_GATED_RESIDUAL).
+ *   operands  NT_TRI_PACKED: a, b are packed pair rows [sum N^2, >= 2C] with
+ *             row stride ld_ab, channels [0, C) the projection and [C, 2C)
+ *             the gate logits (a and b may be column slices of one
+ *             projection output); they are gated while re-tiled into the
+ *             workspace (as nt_triangle_mul with NT_TRI_PACKED).
+ *             NT_TRI_PAIR_TILED / NT_TRI_PAIR_TILED_T: a, b are gated
+ *             operands already in pair-tiled planes (channel stride ld_ab),
+ *             as nt_layernorm_linear with NT_EPI_SIGMOID_GLU writes them; the
+ *             variant must match the direction, as for nt_triangle_mul.  No
+ *             workspace.
+ *   t         [sum N^2, C], row stride ld_t, overwritten.
+ * Errors: as nt_triangle_mul.                                               */
+nt_status nt_triangle_mul_gated(const nt_layout* layout, int32_t direction, int32_t C,
+                                const void* a, const void* b, int64_t ld_ab, nt_tri_operands operands,
+                                void* t, int64_t ld_t, nt_dtype dtype,
+                                void* workspace, uint64_t workspace_bytes, void* stream);
 
 /* Minimum workspace of nt_triangle_mul in bytes (0: none).
  * Errors: NT_ERR_INVALID_ARG.                                               */

@@ -80,8 +80,8 @@ def ref_attention_gated(qkvg, beta, lengths, C, H, d, axis):
 
 
 def ref_gated_operands(proj, C):
-    """a = sigmoid(a_g) * a_p, b = sigmoid(b_g) * b_p from the stored
-    projection [a_p | a_g | b_p | b_g | g] ([R, 5C])."""
+    """a = sigmoid(a_g) * a_p, b = sigmoid(b_g) * b_p from the projection
+    [a_p | a_g | b_p | b_g | g] ([R, 5C])."""
     return (ops.gated_operand(proj[:, :C], proj[:, C:2 * C]),
             ops.gated_operand(proj[:, 2 * C:3 * C], proj[:, 3 * C:4 * C]))
 
@@ -174,8 +174,11 @@ def pair_block(s, lengths, p, dims, order, z=None, dtype="bf16", round_last=True
             trace[step + ".o"] = o
             z = st(ref_attn_out(o, z, p, step))
         elif step in ("tri_out_g", "tri_in_g"):
-            proj = keep(ref_ln_linear(z, p, step, keep))
+            # the gated operands are formed from the projection before it is
+            # stored; the output gate logits are stored
+            proj = ref_ln_linear(z, p, step, keep)
             a, b = (keep(t) for t in ref_gated_operands(proj, C))
+            proj = keep(proj)
             t = keep(ref_triangle_t(a, b, lengths, "outgoing" if step == "tri_out_g" else "incoming"))
             trace[step + ".t"] = t
             z = st(ref_gated_out(t, proj[:, 4 * C:5 * C], z, p, step, keep))

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_PKG, "libnt.so")
 NT_OK, NT_ERR_INVALID_ARG, NT_ERR_LAYOUT_MISMATCH, NT_ERR_OVERFLOW, NT_ERR_UNSUPPORTED, NT_ERR_HIP, NT_ERR_OOM = \
     0, -1, -2, -3, -4, -5, -6
 NT_F32, NT_BF16 = 0, 1
-EPILOGUES = {"none": 0, "residual": 1, "swiglu_residual": 2, "gelu": 3}
+EPILOGUES = {"none": 0, "residual": 1, "swiglu_residual": 2, "gelu": 3, "gated_residual": 4, "sigmoid_glu": 5}
 LEVELS = {"singles": 0, "pairs": 1, "pairs_first": 2}
 TAILS = {"channel_major": 0, "pair_tiled": 1, "pair_tiled_t": 2}
 TRI_OPERANDS = {"packed": 0, "pair_tiled": 1, "pair_tiled_t": 2}
@@ -65,7 +65,8 @@ class LinearArgs(C.Structure):
                 ("n_tail", C.c_int32), ("y_tail", C.c_void_p), ("ld_tail", C.c_int64), ("tail_layout", C.c_int),
                 ("layout", C.c_void_p), ("level", C.c_int), ("residual_layout", C.c_void_p),
                 ("bcast_u", C.c_void_p), ("ld_bcast_u", C.c_int64), ("bcast_v", C.c_void_p), ("ld_bcast_v", C.c_int64),
-                ("workspace", C.c_void_p), ("workspace_bytes", C.c_uint64)]
+                ("workspace", C.c_void_p), ("workspace_bytes", C.c_uint64),
+                ("gate", C.c_void_p), ("ld_gate", C.c_int64)]
 
 
 _lib = None
@@ -93,9 +94,12 @@ def load(path: str = LIB_PATH):
         "nt_pair_row_attention": [vp, i32, i32, i32, vp, vp, vp, i64, vp, i64, i64, f32, vp, i64, C.c_int, vp, u64, vp],
         "nt_pair_row_attention_workspace": [vp, i32, i32, i32, C.c_int, i32, C.POINTER(u64)],
         "nt_cross_attention": [vp, vp, i32, i32, vp, i64, vp, vp, i64, f32, vp, i64, C.c_int, vp],
+        "nt_pair_row_attention_gated": [vp, i32, i32, i32, vp, vp, vp, i64, vp, i64, vp, i64, i64, f32, vp, i64,
+                                        C.c_int, vp, u64, vp],
         "nt_pair_row_attention_noalloc": [vp, i32, i32, i32, vp, vp, vp, i64, vp, i64, i64, f32, vp, i64, C.c_int, vp],
         "nt_triangle_mul": [vp, i32, i32, vp, vp, i64, C.c_int, vp, i64, C.c_int, vp, u64, vp],
         "nt_triangle_mul_workspace": [vp, i32, C.c_int, C.c_int, C.POINTER(u64)],
+        "nt_triangle_mul_gated": [vp, i32, i32, vp, vp, i64, C.c_int, vp, i64, C.c_int, vp, u64, vp],
         "nt_segment_reduce": [vp, C.c_int, i32, i32, vp, i64, C.c_int, vp, i64, vp],
         "nt_pair_broadcast_backward": [vp, i32, vp, i64, C.c_int, vp, i64, vp, i64, C.c_int, i32, vp],
         "nt_from_rect_lengths": [vp, vp, i32, C.c_uint32, vp, C.POINTER(vp)],
@@ -229,9 +233,10 @@ def nt_layernorm_linear(x, w, bias, y, ln=None, eps: float = 1e-5, epilogue: str
                         hidden: int = 0, residual=None, n_tail: int = 0, y_tail=None,
                         tail_layout: str = "channel_major", layout: NestedLayout | None = None,
                         level: str = "pairs", residual_layout: NestedLayout | None = None, c_out: int | None = None,
-                        bcast=None, workspace=None):
+                        bcast=None, workspace=None, gate=None):
     """bcast=(u, v) with x=None: the rows are the pair broadcast u[eta_i+a] + v[eta_i+b] over `layout`.
-    workspace: a device buffer from workspace_tensor(), or None to allocate one of the queried size."""
+    workspace: a device buffer from workspace_tensor(), or None to allocate one of the queried size.
+    gate: gate logits [rows, c_out] of the "gated_residual" epilogue."""
     a = LinearArgs()
     if bcast is not None:
         if x is not None or layout is None:
@@ -260,6 +265,7 @@ def nt_layernorm_linear(x, w, bias, y, ln=None, eps: float = 1e-5, epilogue: str
     a.layout = layout.handle if layout is not None else None
     a.level = LEVELS[level]
     a.residual_layout = residual_layout.handle if residual_layout is not None else None
+    a.gate, a.ld_gate = _mat(gate, "gate")
     if workspace is None:
         workspace = workspace_tensor(_linear_ws_bytes(a))
     a.workspace, a.workspace_bytes = _ws(workspace)
@@ -322,9 +328,11 @@ def attention_workspace_bytes(layout: NestedLayout, axis: int, heads: int, head_
 
 
 def nt_pair_row_attention(layout: NestedLayout, axis: int, heads: int, head_dim: int, q, k, v, o,
-                          bias=None, scale: float | None = None, bias_layout: str = "cells", workspace=None):
+                          bias=None, scale: float | None = None, bias_layout: str = "cells", workspace=None,
+                          gate=None):
     """bias: [sum N^2, H] with a row stride (bias_layout "cells"), or head-major
-    [H, >= sum N^2] (bias_layout "heads")."""
+    [H, >= sum N^2] (bias_layout "heads").  gate: [sum N^2, H*d] logits of the
+    output gate (nt_pair_row_attention_gated), or None."""
     pq, ld = _mat(q, "q")
     pk, ldk = _mat(k, "k")
     pv, ldv = _mat(v, "v")
@@ -349,6 +357,11 @@ def nt_pair_row_attention(layout: NestedLayout, axis: int, heads: int, head_dim:
         workspace = workspace_tensor(attention_workspace_bytes(layout, axis, heads, head_dim,
                                                                "bf16" if dt == NT_BF16 else "f32", bias is not None))
     pw, nw = _ws(workspace)
+    if gate is not None:
+        pg, ldg = _mat(gate, "gate")
+        _check(load().nt_pair_row_attention_gated(layout.handle, int(axis), int(heads), int(head_dim), pq, pk, pv, ld,
+                                                  pg, ldg, pb, ldb, ldbh, scale, po, ldo, dt, pw, nw, _stream()))
+        return o
     _check(load().nt_pair_row_attention(layout.handle, int(axis), int(heads), int(head_dim), pq, pk, pv, ld,
                                         pb, ldb, ldbh, scale, po, ldo, dt, pw, nw, _stream()))
     return o
@@ -395,6 +408,29 @@ def nt_triangle_mul(layout: NestedLayout, direction: int, a, b, z, operands: str
     _check(load().nt_triangle_mul(layout.handle, int(direction), Cz, pa, pb, lda, TRI_OPERANDS[operands], pz, ldz,
                                   _dtype(z), pw, nw, _stream()))
     return z
+
+
+def nt_triangle_mul_gated(layout: NestedLayout, direction: int, a, b, t, operands: str = "packed", workspace=None):
+    """operands "packed": a, b are [sum N^2, >= 2C] rows of [projection | gate
+    logits] (one row stride); "pair_tiled" / "pair_tiled_t": gated operands in
+    pair-tiled planes [C, >= sum_pad].  t: [sum N^2, C], overwritten with the
+    contraction of the gated operands."""
+    pt, ldt = _mat(t, "t")
+    Ct = int(t.size(1))
+    if operands == "packed":
+        pa, lda = _mat(a, "a")
+        pb, ldb = _mat(b, "b")
+        if lda != ldb:
+            raise ValueError("a and b must share one row stride")
+    else:
+        pa, lda = _ptr(a), int(a.stride(0))
+        pb = _ptr(b)
+    if workspace is None:
+        workspace = workspace_tensor(triangle_workspace_bytes(layout, Ct, operands, "bf16" if _dtype(t) == NT_BF16 else "f32"))
+    pw, nw = _ws(workspace)
+    _check(load().nt_triangle_mul_gated(layout.handle, int(direction), Ct, pa, pb, lda, TRI_OPERANDS[operands], pt,
+                                        ldt, _dtype(t), pw, nw, _stream()))
+    return t
 
 
 def nt_segment_reduce(layout: NestedLayout, level: str, op: str, x, y):

@@ -90,7 +90,8 @@ def to_device(params: dict, dtype: str, device="cuda") -> dict:
 class PairWorkspace:
     """Device buffers of one pair block for a given layout and widths."""
 
-    def __init__(self, layout: B.NestedLayout, c_s: int, c_z: int, heads: int, dtype: str, device="cuda"):
+    def __init__(self, layout: B.NestedLayout, c_s: int, c_z: int, heads: int, dtype: str, device="cuda",
+                 gated: bool = False):
         td = torch.bfloat16 if dtype == "bf16" else torch.float32
         R, S = layout.sum_n2, layout.sum_n
         self.td = td
@@ -106,6 +107,14 @@ class PairWorkspace:
         need = max(B.attention_workspace_bytes(layout, ax, heads, c_z // heads, dtype, True) for ax in (0, 1))
         need = max(need, B.layernorm_linear_workspace_bytes(R, c_z, c_z, dtype, epilogue="swiglu_residual",
                                                             hidden=4 * c_z))
+        if gated:
+            # gated steps: [q|k|v|g] or [a_p|a_g|b_p|b_g] rows, the gate logits
+            # of the triangle output and the contraction t; the gated operands
+            # are re-tiled into the scratch
+            self.p4 = torch.empty((R, 4 * c_z), dtype=td, device=device)
+            self.g = torch.empty((R, c_z), dtype=td, device=device)
+            self.t = torch.empty((R, c_z), dtype=td, device=device)
+            need = max(need, B.triangle_workspace_bytes(layout, c_z, "packed", dtype))
         self.scratch = B.workspace_tensor(need, device)
         self.cur = 0
 
@@ -115,6 +124,12 @@ fuse_broadcast = True             # the pair block fuses broadcast -> LayerNorm+
 
 def fuse_bcast(ws: PairWorkspace, C: int) -> bool:
     return fuse_broadcast and ws.td == torch.bfloat16 and C in (64, 128)
+
+
+def glu_tiled(ws: PairWorkspace, C: int) -> bool:
+    """The gated triangle operands go straight into pair-tiled planes (bf16,
+    C = 128); otherwise the projection is stored and gated while re-tiled."""
+    return ws.td == torch.bfloat16 and C == 128
 
 
 def pair_block(layout: B.NestedLayout, s, W: dict, dims: dict, order, ws: PairWorkspace, z=None, tap=None):
@@ -173,6 +188,57 @@ def pair_block(layout: B.NestedLayout, s, W: dict, dims: dict, order, ws: PairWo
             with _op("attn_out_residual"):
                 B.nt_layernorm_linear(ws.o, W[step + ".wo"], W[step + ".bo"], z, epilogue="residual", residual=z,
                                       layout=layout, level="pairs", residual_layout=layout)
+            tap(step + ".out", z=z)
+        elif step in ("att_row_g", "att_col_g"):
+            ln = (W[step + ".ln_g"], W[step + ".ln_b"])
+            with _op("attn_proj_g"):
+                # [q|k|v] with the bias tail, then the gate logits: the weight
+                # rows [q; k; v; g; bias] regrouped once on the device
+                B.nt_layernorm_linear(z, W[step + ".w_qkvb"], W[step + ".b_qkvb"], ws.qkv, ln=ln, n_tail=H,
+                                      y_tail=ws.bias, tail_layout="channel_major", layout=layout, level="pairs")
+                B.nt_layernorm_linear(z, W[step + ".w"][3 * C:4 * C], W[step + ".b"][3 * C:4 * C], ws.g, ln=ln,
+                                      layout=layout, level="pairs")
+            tap(step + ".proj", qkv=ws.qkv, g=ws.g, bias=ws.bias)
+            with _op("attention_" + step[4:7] + "_g"):
+                B.nt_pair_row_attention(layout, 0 if step == "att_row_g" else 1, H, d, ws.qkv[:, :C],
+                                        ws.qkv[:, C:2 * C], ws.qkv[:, 2 * C:], ws.o, bias=ws.bias,
+                                        bias_layout="heads", workspace=ws.scratch, gate=ws.g)
+            tap(step + ".attention", o=ws.o)
+            with _op("attn_out_residual"):
+                B.nt_layernorm_linear(ws.o, W[step + ".wo"], W[step + ".bo"], z, epilogue="residual", residual=z,
+                                      layout=layout, level="pairs", residual_layout=layout)
+            tap(step + ".out", z=z)
+        elif step in ("tri_out_g", "tri_in_g"):
+            ln = (W[step + ".ln_g"], W[step + ".ln_b"])
+            tiled = "pair_tiled" if step == "tri_out_g" else "pair_tiled_t"
+            with _op("tri_proj_g"):
+                # gated operands sigmoid(a_g) a_p | sigmoid(b_g) b_p straight
+                # into pair-tiled planes, then the output gate logits g
+                if glu_tiled(ws, C):
+                    B.nt_layernorm_linear(z, W[step + ".w"][:4 * C], W[step + ".b"][:4 * C], None, ln=ln,
+                                          epilogue="sigmoid_glu", hidden=C, n_tail=2 * C, y_tail=ws.ab,
+                                          tail_layout=tiled, layout=layout, level="pairs", c_out=2 * C)
+                else:
+                    B.nt_layernorm_linear(z, W[step + ".w"][:4 * C], W[step + ".b"][:4 * C], ws.p4, ln=ln,
+                                          layout=layout, level="pairs")
+                B.nt_layernorm_linear(z, W[step + ".w"][4 * C:], W[step + ".b"][4 * C:], ws.g, ln=ln,
+                                      layout=layout, level="pairs")
+            if glu_tiled(ws, C):
+                tap(step + ".proj", ab=ws.ab, g=ws.g)
+            else:
+                tap(step + ".proj", p4=ws.p4, g=ws.g)
+            with _op("triangle_" + step[4:-2] + "_g"):
+                if glu_tiled(ws, C):
+                    B.nt_triangle_mul_gated(layout, 0 if step == "tri_out_g" else 1, ws.ab[:C], ws.ab[C:], ws.t,
+                                            operands=tiled)
+                else:
+                    B.nt_triangle_mul_gated(layout, 0 if step == "tri_out_g" else 1, ws.p4[:, :2 * C],
+                                            ws.p4[:, 2 * C:], ws.t, workspace=ws.scratch)
+            tap(step + ".triangle", t=ws.t)
+            with _op("tri_out_gated_residual"):
+                B.nt_layernorm_linear(ws.t, W[step + ".wo"], W[step + ".bo"], z,
+                                      ln=(W[step + ".out.ln_g"], W[step + ".out.ln_b"]), epilogue="gated_residual",
+                                      residual=z, gate=ws.g, layout=layout, level="pairs", residual_layout=layout)
             tap(step + ".out", z=z)
         elif step in ("tri_out", "tri_in"):
             with _op("tri_proj"):
@@ -254,11 +320,17 @@ class PairRun:
         self.dims = dict(c_z=w.c_z, heads=w.heads, head_dim=w.head_dim)
         self.params = [synth.pair_block_params(w, block=b) for b in range(w.blocks)]
         self.W = [to_device(p, w.dtype, device) for p in self.params]
+        C, H = w.c_z, w.heads
+        for Wb in self.W:                      # gated attention: [q; k; v; bias] regrouped for one projection
+            for key in [t for t in w.steps if t.startswith("att_") and t.endswith("_g")]:
+                Wb[key + ".w_qkvb"] = torch.cat([Wb[key + ".w"][:3 * C], Wb[key + ".w"][4 * C:4 * C + H]]).contiguous()
+                Wb[key + ".b_qkvb"] = torch.cat([Wb[key + ".b"][:3 * C], Wb[key + ".b"][4 * C:4 * C + H]]).contiguous()
         self.s_init = synth.normal(w.seed, "s", (sum(self.lengths), w.c_s), w.s_scale, w.dtype)
         td = torch.bfloat16 if w.dtype == "bf16" else torch.float32
         self.s0 = torch.from_numpy(self.s_init).to(device=device, dtype=td)
         self.s = self.s0.clone()
-        self.ws = PairWorkspace(self.layout, w.c_s, w.c_z, w.heads, w.dtype, device)
+        self.ws = PairWorkspace(self.layout, w.c_s, w.c_z, w.heads, w.dtype, device,
+                                gated=any(t.endswith("_g") for t in w.steps))
         self.z = None
 
     def step(self, tap=None):

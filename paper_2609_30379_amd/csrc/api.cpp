@@ -335,9 +335,10 @@ nt_status nt_layernorm_linear(const nt_linear_args* a, void* stream) {
   if (a->rows < 0 || a->c_in <= 0 || a->c_out <= 0) return nt::fail(NT_ERR_INVALID_ARG, "bad sizes");
   if (a->rows > INT32_MAX) return nt::fail(NT_ERR_OVERFLOW, "rows exceed int32");
   if (a->c_in % 8) return nt::fail(NT_ERR_INVALID_ARG, "c_in must be a multiple of 8");
-  if (a->epilogue < NT_EPI_NONE || a->epilogue > NT_EPI_GELU) return nt::fail(NT_ERR_INVALID_ARG, "bad epilogue");
+  if (a->epilogue < NT_EPI_NONE || a->epilogue > NT_EPI_SIGMOID_GLU) return nt::fail(NT_ERR_INVALID_ARG, "bad epilogue");
   if (a->ln_beta && !a->ln_gamma) return nt::fail(NT_ERR_INVALID_ARG, "ln_beta without ln_gamma");
   if (a->ln_gamma && !(a->ln_eps >= 0.f)) return nt::fail(NT_ERR_INVALID_ARG, "ln_eps must be >= 0");
+  const bool gated = a->epilogue == NT_EPI_GATED_RESIDUAL;
   const bool swiglu = a->epilogue == NT_EPI_SWIGLU_RESIDUAL;
   const int vx = vec_elems(a->x_dtype), vy = vec_elems(a->dtype);
   const bool bcast = a->bcast_u || a->bcast_v;
@@ -386,6 +387,15 @@ nt_status nt_layernorm_linear(const nt_linear_args* a, void* stream) {
   }
   if (a->dtype == NT_F32 && !swiglu && a->c_in > 4096) return nt::fail(NT_ERR_UNSUPPORTED, "f32 path needs c_in <= 4096");
   if (a->epilogue == NT_EPI_RESIDUAL && !a->residual) return nt::fail(NT_ERR_INVALID_ARG, "residual epilogue needs residual");
+  if (gated && (!a->residual || !a->gate)) return nt::fail(NT_ERR_INVALID_ARG, "gated residual epilogue needs residual and gate");
+  if (gated && a->n_tail) return nt::fail(NT_ERR_UNSUPPORTED, "the gated residual epilogue has no tail output");
+  if (!gated && a->gate) return nt::fail(NT_ERR_INVALID_ARG, "gate is only read by the gated residual epilogue");
+  if (a->epilogue == NT_EPI_SIGMOID_GLU &&
+      (a->dtype != NT_BF16 || a->x_dtype != NT_BF16 || a->c_in != 128 || a->hidden != 128 || a->c_out != 256 ||
+       a->n_tail != a->c_out || a->tail_layout == NT_TAIL_CHANNEL_MAJOR || bcast || a->residual ||
+       !a->layout || a->layout->batch > nt::kPairTiledMaxSamples))
+    return nt::fail(NT_ERR_UNSUPPORTED, "the sigmoid GLU epilogue supports bf16, c_in = hidden = 128 and 256 outputs, "
+                                        "all in a pair-tiled tail");
   if (a->rows == 0) return NT_OK;
   if ((!a->x && !bcast) || !a->w) return nt::fail(NT_ERR_INVALID_ARG, "x and w must be non-NULL");
   if (n_main > 0 && !a->y) return nt::fail(NT_ERR_INVALID_ARG, "y is NULL");
@@ -397,6 +407,8 @@ nt_status nt_layernorm_linear(const nt_linear_args* a, void* stream) {
     return nt::fail(NT_ERR_INVALID_ARG, "pointers must be 16-byte aligned");
   if (n_main > 0 && (a->ldy < n_main || a->ldy % vy)) return nt::fail(NT_ERR_INVALID_ARG, "ldy must be >= the main width and a multiple of the vector width");
   if (a->residual && (a->ld_residual < n_main || a->ld_residual % vy)) return nt::fail(NT_ERR_INVALID_ARG, "bad ld_residual");
+  if (gated && (a->ld_gate < n_main || a->ld_gate % vy || !aligned16(a->gate)))
+    return nt::fail(NT_ERR_INVALID_ARG, "gate must be 16-byte aligned with ld_gate >= c_out, a multiple of the vector width");
   if (a->n_tail > 0) {
     const int64_t need = a->tail_layout == NT_TAIL_CHANNEL_MAJOR ? a->rows : a->layout->sum_pad;
     if (a->ld_tail < need) return nt::fail(NT_ERR_INVALID_ARG, "ld_tail is smaller than the tail's row extent");
@@ -455,11 +467,11 @@ nt_status nt_layernorm_linear_backward(const nt_linear_bwd_args* a, void* stream
                    "nt_layernorm_linear_backward launch");
 }
 
-nt_status nt_pair_row_attention(const nt_layout* L, int32_t axis, int32_t H, int32_t D, const void* q,
-                                const void* k, const void* v, int64_t ld_qkv, const void* bias,
-                                int64_t ld_bias, int64_t ld_bias_head, float scale, void* o, int64_t ld_o,
-                                nt_dtype dtype, void* workspace, uint64_t workspace_bytes, void* stream) {
-  g_last_error.clear();
+namespace {
+nt_status pair_row_attention(const nt_layout* L, int32_t axis, int32_t H, int32_t D, const void* q,
+                             const void* k, const void* v, int64_t ld_qkv, const void* gate, int64_t ld_gate,
+                             const void* bias, int64_t ld_bias, int64_t ld_bias_head, float scale, void* o,
+                             int64_t ld_o, nt_dtype dtype, void* workspace, uint64_t workspace_bytes, void* stream) {
   if (!L) return nt::fail(NT_ERR_INVALID_ARG, "layout is NULL");
   if (axis < 0 || axis > 3) return nt::fail(NT_ERR_INVALID_ARG, "axis must be 0, 1, 2 or 3");
   if (axis != 2) if (nt_status st = need_square(L, "pair attention")) return st;
@@ -488,9 +500,33 @@ nt_status nt_pair_row_attention(const nt_layout* L, int32_t axis, int32_t H, int
       (bias && (reinterpret_cast<uintptr_t>(bias) & (dtype == NT_BF16 ? 1u : 3u))))
     return nt::fail(NT_ERR_INVALID_ARG, "q, k, v, o must be 16-byte aligned, bias element-aligned");
   if (!(scale == scale)) return nt::fail(NT_ERR_INVALID_ARG, "scale is NaN");
+  if (gate && ((int64_t)H * D > ld_gate || ld_gate % ve || !aligned16(gate)))
+    return nt::fail(NT_ERR_INVALID_ARG, "gate must be 16-byte aligned with ld_gate >= H*head_dim, a multiple of the vector width");
   return check_hip(nt::launch_attention(*L, axis, H, D, q, k, v, ld_qkv, bias, ld_bias, ld_bias_head, scale, o, ld_o,
-                                        dtype, workspace, static_cast<hipStream_t>(stream)),
+                                        dtype, workspace, static_cast<hipStream_t>(stream), gate, ld_gate),
                    "nt_pair_row_attention launch");
+}
+}  // namespace
+
+nt_status nt_pair_row_attention(const nt_layout* L, int32_t axis, int32_t H, int32_t D, const void* q,
+                                const void* k, const void* v, int64_t ld_qkv, const void* bias,
+                                int64_t ld_bias, int64_t ld_bias_head, float scale, void* o, int64_t ld_o,
+                                nt_dtype dtype, void* workspace, uint64_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  return pair_row_attention(L, axis, H, D, q, k, v, ld_qkv, nullptr, 0, bias, ld_bias, ld_bias_head, scale, o, ld_o,
+                            dtype, workspace, workspace_bytes, stream);
+}
+
+nt_status nt_pair_row_attention_gated(const nt_layout* L, int32_t axis, int32_t H, int32_t D, const void* q,
+                                      const void* k, const void* v, int64_t ld_qkv, const void* gate,
+                                      int64_t ld_gate, const void* bias, int64_t ld_bias, int64_t ld_bias_head,
+                                      float scale, void* o, int64_t ld_o, nt_dtype dtype, void* workspace,
+                                      uint64_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  if (axis != 0 && axis != 1) return nt::fail(NT_ERR_INVALID_ARG, "the gated attention covers axes 0 and 1");
+  if (!gate && L && L->sum_n2 > 0) return nt::fail(NT_ERR_INVALID_ARG, "gate is NULL");
+  return pair_row_attention(L, axis, H, D, q, k, v, ld_qkv, gate, ld_gate, bias, ld_bias, ld_bias_head, scale, o,
+                            ld_o, dtype, workspace, workspace_bytes, stream);
 }
 
 nt_status nt_cross_attention(const nt_layout* Lq, const nt_layout* Lkv, int32_t H, int32_t D, const void* q,
@@ -640,6 +676,41 @@ nt_status nt_triangle_mul(const nt_layout* L, int32_t direction, int32_t C, cons
   return check_hip(nt::launch_triangle(*L, direction, C, a, b, ld_ab, operands, z, ld_z, dtype, workspace,
                                        static_cast<hipStream_t>(stream)),
                    "nt_triangle_mul launch");
+}
+
+nt_status nt_triangle_mul_gated(const nt_layout* L, int32_t direction, int32_t C, const void* a, const void* b,
+                                int64_t ld_ab, nt_tri_operands operands, void* t, int64_t ld_t, nt_dtype dtype,
+                                void* workspace, uint64_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  if (!L) return nt::fail(NT_ERR_INVALID_ARG, "layout is NULL");
+  if (nt_status st = need_square(L, "the triangle update")) return st;
+  if (direction != 0 && direction != 1) return nt::fail(NT_ERR_INVALID_ARG, "direction must be 0 or 1");
+  if (!valid_dtype(dtype)) return nt::fail(NT_ERR_INVALID_ARG, "bad dtype");
+  if (C <= 0) return nt::fail(NT_ERR_INVALID_ARG, "C must be > 0");
+  if (dtype == NT_BF16 && C % 32) return nt::fail(NT_ERR_INVALID_ARG, "bf16 triangle needs C % 32 == 0");
+  const int ve = vec_elems(dtype);
+  if (C % ve) return nt::fail(NT_ERR_INVALID_ARG, "C must be a multiple of the vector width");
+  if (operands != NT_TRI_PACKED && operands != NT_TRI_PAIR_TILED && operands != NT_TRI_PAIR_TILED_T)
+    return nt::fail(NT_ERR_INVALID_ARG, "bad operand layout");
+  if (ld_t < C || ld_t % ve) return nt::fail(NT_ERR_INVALID_ARG, "ld_t must be >= C and a multiple of the vector width");
+  if (operands == NT_TRI_PACKED) {
+    if (ld_ab < 2 * (int64_t)C || ld_ab % ve)
+      return nt::fail(NT_ERR_INVALID_ARG, "packed gated operands: ld_ab must be >= 2C and a multiple of the vector width");
+  } else {
+    if ((operands == NT_TRI_PAIR_TILED) != (direction == 0))
+      return nt::fail(NT_ERR_INVALID_ARG, "the pair-tiled operand variant does not match the direction");
+    if (ld_ab < L->sum_pad || ld_ab % 8) return nt::fail(NT_ERR_INVALID_ARG, "pair-tiled operands: ld_ab must be >= sum_pad and a multiple of 8");
+  }
+  if (nt_status st = need_workspace(nt::triangle_workspace_bytes(*L, C, operands, dtype), workspace,
+                                    workspace_bytes, "nt_triangle_mul_workspace"))
+    return st;
+  if (nt_status st = need_device(L)) return st;
+  if (L->sum_n2 == 0) return NT_OK;
+  if (!a || !b || !t) return nt::fail(NT_ERR_INVALID_ARG, "a, b and t must be non-NULL");
+  if (!aligned16(a) || !aligned16(b) || !aligned16(t)) return nt::fail(NT_ERR_INVALID_ARG, "pointers must be 16-byte aligned");
+  return check_hip(nt::launch_triangle_gated(*L, direction, C, a, b, ld_ab, operands, t, ld_t, dtype, workspace,
+                                             static_cast<hipStream_t>(stream)),
+                   "nt_triangle_mul_gated launch");
 }
 
 nt_status nt_triangle_mul_backward(const nt_layout* L, int32_t direction, int32_t C, const void* a, const void* b,

@@ -37,6 +37,8 @@ struct AttnArgs {
   const int32_t* cu_seqlens;
   const int32_t* cu_pairs;
   int vstride;           // LDS row stride of V^T (elements)
+  const bf16* gate;      // NULL, or o = sigmoid(gate) * attention (gate row stride ld_gate)
+  int64_t ld_gate;
 };
 
 struct Seg {
@@ -181,7 +183,14 @@ __global__ void __launch_bounds__(256) attention_mfma_kernel(AttnArgs p) {
       for (int dt = 0; dt < D / 16; ++dt) {
         bf16x4 ov;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) ov[i] = (bf16)(O[dt][i] * inv);
+        for (int i = 0; i < 4; ++i) {
+          float val = O[dt][i] * inv;
+          if (p.gate) {
+            const float gl = (float)p.gate[qrow * p.ld_gate + h * D + dt * 16 + 4 * g + i];
+            val *= __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-gl * kLog2e));
+          }
+          ov[i] = (bf16)val;
+        }
         *reinterpret_cast<bf16x4*>(orow + dt * 16 + 4 * g) = ov;
       }
     }
@@ -209,6 +218,8 @@ struct PairAttnArgs {
   const int32_t* bias_tiles;
   int batch;             // samples (persistent instance: rows are found from cu_seqlens)
   int64_t total_rows;    // sum of N_i (persistent instance)
+  const bf16* gate;      // gated output: o = sigmoid(gate) * attention, gate [rows, >= H*D] (GATE instances)
+  int64_t ld_gate;
 };
 
 // Pair bias image: for head h, sample i, 16-query tile qt and 16-key tile kt
@@ -359,7 +370,7 @@ __device__ __forceinline__ float query_max(float v) {
 // rows) and N <= 512 from a work list of (sample, query block, group of 16
 // rows) items with 8 waves (128 KB, twice the bias registers, two waves per
 // SIMD).
-template <int NMAX, int NW, bool PERSIST>
+template <int NMAX, int NW, bool PERSIST, bool GATE = false>
 __global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_kernel(PairAttnArgs p) {
   constexpr int D = 32;
   constexpr int KT16 = NMAX / 16;               // key tiles
@@ -512,6 +523,17 @@ __global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_k
     n2 = __builtin_amdgcn_readfirstlane(n2);
     cu2 = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(cu2 >> 32)) << 32) |
                     (uint32_t)__builtin_amdgcn_readfirstlane((int)cu2));
+    // gate of this lane's outputs (GATE): issued before the next row's
+    // copies, so waiting for it leaves those in flight; the query index is
+    // clamped into the row, so the load is unconditional
+    uint2 gt[2];
+    if constexpr (GATE) {
+      if (wave_has_queries) {
+        const bf16* gr = p.gate + (cu + (int64_t)r * sr + (int64_t)min(jw, n - 1) * st) * p.ld_gate + h * D + 4 * g;
+        gt[0] = *reinterpret_cast<const uint2*>(gr);
+        gt[1] = *reinterpret_cast<const uint2*>(gr + 16);
+      }
+    }
     bf16x8 qn = qf;
     if (more) {
       dma_kv(n2, cu2, r2, odd ? Kb0 : Kb1, odd ? Vb0 : Vb1);
@@ -616,9 +638,16 @@ __global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_k
         bf16* orow = p.o + (cu + (int64_t)r * sr + (int64_t)jw * st) * p.ld_o + h * D;
 #pragma unroll
         for (int dt = 0; dt < 2; ++dt) {
+          float gs[4] = {1.f, 1.f, 1.f, 1.f};
+          if constexpr (GATE) {
+            const float gl[4] = {__uint_as_float(gt[dt].x << 16), __uint_as_float(gt[dt].x & 0xffff0000u),
+                                 __uint_as_float(gt[dt].y << 16), __uint_as_float(gt[dt].y & 0xffff0000u)};
+#pragma unroll
+            for (int ii = 0; ii < 4; ++ii) gs[ii] = __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-gl[ii] * kLog2e));
+          }
           bf16x4 ov;
 #pragma unroll
-          for (int ii = 0; ii < 4; ++ii) ov[ii] = (bf16)(O[dt][ii] * inv);
+          for (int ii = 0; ii < 4; ++ii) ov[ii] = (bf16)(O[dt][ii] * inv * gs[ii]);
           *reinterpret_cast<bf16x4*>(orow + dt * 16 + 4 * g) = ov;
         }
       }
@@ -853,6 +882,8 @@ struct AttnF32Args {
   const int32_t* cu_pairs;
   const int32_t* cu_kv;  // axis 2: key / value offsets (= cu_seqlens for self-attention)
   int64_t ld_q;          // row stride of q (ld_qkv is that of k and v)
+  const float* gate;     // NULL, or o = sigmoid(gate) * attention
+  int64_t ld_gate;
 };
 
 // Exact two-pass softmax per query in fp32: one thread per query.  On axis 2
@@ -903,7 +934,11 @@ __global__ void __launch_bounds__(256) attention_f32_kernel(AttnF32Args p) {
       for (int d = 0; d < D; ++d) acc[d] = fmaf(e, p.v[krow * p.ld_qkv + h * D + d], acc[d]);
     }
 #pragma unroll
-    for (int d = 0; d < D; ++d) p.o[qrow * p.ld_o + h * D + d] = acc[d] / sum;
+    for (int d = 0; d < D; ++d) {
+      float val = acc[d] / sum;
+      if (p.gate) val /= 1.f + expf(-p.gate[qrow * p.ld_gate + h * D + d]);
+      p.o[qrow * p.ld_o + h * D + d] = val;
+    }
   }
 }
 
@@ -983,7 +1018,7 @@ hipError_t launch_cross_attention(const nt_layout& Lq, const nt_layout& Lkv, int
   // fp32: the exact kernel, one workgroup per (sample, query block)
   if (Lq.seq_items() == 0) return hipSuccess;
   AttnF32Args a{2, H, (const float*)q, (const float*)k, (const float*)v, ld_kv, nullptr, 1, 1, scale, (float*)o,
-                ld_o, Lq.d_seq_work, Lq.d_cu_seqlens, Lq.d_cu_pairs, Lkv.d_cu_seqlens, ld_q};
+                ld_o, Lq.d_seq_work, Lq.d_cu_seqlens, Lq.d_cu_pairs, Lkv.d_cu_seqlens, ld_q, nullptr, 0};
   const dim3 grid((unsigned)Lq.seq_items(), (unsigned)H), block(256);
   switch (D) {
     case 8: attention_f32_kernel<8><<<grid, block, 0, s>>>(a); break;
@@ -997,7 +1032,8 @@ hipError_t launch_cross_attention(const nt_layout& Lq, const nt_layout& Lkv, int
 
 hipError_t launch_attention(const nt_layout& L, int axis, int H, int D, const void* q, const void* k,
                             const void* v, int64_t ld_qkv, const void* bias, int64_t ld_bias, int64_t ld_bias_head,
-                            float scale, void* o, int64_t ld_o, nt_dtype dtype, void* workspace, hipStream_t s) {
+                            float scale, void* o, int64_t ld_o, nt_dtype dtype, void* workspace, hipStream_t s,
+                            const void* gate, int64_t ld_gate) {
   const int32_t* work = axis == 2 ? L.d_seq_work : L.d_attn_work;
   const int64_t items = axis == 2 ? L.seq_items() : L.attn_items();
   if (items == 0) return hipSuccess;
@@ -1005,7 +1041,7 @@ hipError_t launch_attention(const nt_layout& L, int axis, int H, int D, const vo
   if (dtype == NT_F32) {
     AttnF32Args a{axis, H, (const float*)q, (const float*)k, (const float*)v, ld_qkv, (const float*)bias,
                   ld_bias, ld_bias_head, scale, (float*)o, ld_o, work, L.d_cu_seqlens, L.d_cu_pairs,
-                  L.d_cu_seqlens, ld_qkv};
+                  L.d_cu_seqlens, ld_qkv, (const float*)gate, ld_gate};
     switch (D) {
       case 8: attention_f32_kernel<8><<<grid, block, 0, s>>>(a); break;
       case 16: attention_f32_kernel<16><<<grid, block, 0, s>>>(a); break;
@@ -1032,10 +1068,21 @@ hipError_t launch_attention(const nt_layout& L, int axis, int H, int D, const vo
     }
     PairAttnArgs a{axis, (const bf16*)q, (const bf16*)k, (const bf16*)v, ld_qkv, (const bf16*)bias, ld_bias,
                    ld_bias_head, scale * kLog2e, (bf16*)o, ld_o, L.d_pattn_work, L.d_cu_seqlens, L.d_cu_pairs, H,
-                   img, tiles * 64, L.d_bias_tiles, L.batch, L.sum_n};
+                   img, tiles * 64, L.d_bias_tiles, L.batch, L.sum_n, (const bf16*)gate, ld_gate};
     const size_t smem = sizeof(bf16) * 4 * (size_t)nmax * 32;
     const dim3 grid((unsigned)(L.pattn_items() * H));
-    if (axis == 3) {
+    if (gate) {
+      // gated output (axes 0 and 1): the GATE instances of the same kernel
+      if (nmax == kAttnShortLen) {
+        const int per_xcd = std::max(H, compute_units() / kXcds / H * H);
+        const dim3 gridp((unsigned)(per_xcd * kXcds));
+        hipFuncSetAttribute((const void*)attention_pair_kernel<kAttnShortLen, 16, true, true>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+        attention_pair_kernel<kAttnShortLen, 16, true, true><<<gridp, dim3(1024), smem, s>>>(a);
+      } else {
+        hipFuncSetAttribute((const void*)attention_pair_kernel<kAttnLongLen, 8, false, true>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+        attention_pair_kernel<kAttnLongLen, 8, false, true><<<grid, dim3(512), smem, s>>>(a);
+      }
+    } else if (axis == 3) {
       // single attention with pair bias: one row per sample, the 8-wave
       // instance over the 1-D attention's (sample, 128-query block) items
       if (L.sattn_items() == 0) return hipSuccess;
@@ -1059,7 +1106,8 @@ hipError_t launch_attention(const nt_layout& L, int axis, int H, int D, const vo
   }
   const int vstride = (npad + 127) / 128 * 128 + 4;
   AttnArgs a{axis, H, (const bf16*)q, (const bf16*)k, (const bf16*)v, ld_qkv, (const bf16*)bias, ld_bias,
-             ld_bias_head, scale * kLog2e, (bf16*)o, ld_o, work, L.d_cu_seqlens, L.d_cu_pairs, vstride};
+             ld_bias_head, scale * kLog2e, (bf16*)o, ld_o, work, L.d_cu_seqlens, L.d_cu_pairs, vstride,
+             (const bf16*)gate, ld_gate};
   const size_t smem = sizeof(bf16) * ((size_t)npad * (D + 8) + (size_t)D * vstride);
   if (D == 32) {
     if (smem > 65536) hipFuncSetAttribute((const void*)attention_mfma_kernel<32>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);

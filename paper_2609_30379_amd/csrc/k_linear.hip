@@ -51,7 +51,14 @@ struct LinArgs {
   int64_t ld_bc_u, ld_bc_v;
   const int32_t* bc_cu_tiles; // per sample: broadcast tiles (16 cells of one pair row) before it
   int bc_ntiles;              // all broadcast tiles
+  const bf16* gate;           // NT_EPI_GATED_RESIDUAL: gate logits [rows, n_main], row stride ld_gate
+  int64_t ld_gate;
 };
+
+// 1 / (1 + e^-v): the gate of the gated epilogues
+__device__ __forceinline__ float sigmoid_gate(float v) {
+  return __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-v * 1.4426950408889634f));
+}
 
 // Position of the pair cell (a, b) of sample i in its pair-tiled operand plane:
 // row a, column b, or row b, column a for the transposed (incoming) operand.
@@ -269,7 +276,11 @@ __global__ void __launch_bounds__(256) linear_mfma_kernel(LinArgs p) {
         if constexpr (EPI == NT_EPI_GELU) r[i] = gelu_erf(r[i]);
       }
       if (n + 4 <= p.n_main) {
-        if constexpr (EPI == NT_EPI_RESIDUAL) {
+        if constexpr (EPI == NT_EPI_GATED_RESIDUAL) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) r[i] *= sigmoid_gate((float)p.gate[(int64_t)m * p.ld_gate + n + i]);
+        }
+        if constexpr (EPI == NT_EPI_RESIDUAL || EPI == NT_EPI_GATED_RESIDUAL) {
           const uint2 rr = *reinterpret_cast<const uint2*>(p.res + (int64_t)m * p.ld_res + n);
           r[0] += __uint_as_float(rr.x << 16); r[1] += __uint_as_float(rr.x & 0xffff0000u);
           r[2] += __uint_as_float(rr.y << 16); r[3] += __uint_as_float(rr.y & 0xffff0000u);
@@ -285,7 +296,8 @@ __global__ void __launch_bounds__(256) linear_mfma_kernel(LinArgs p) {
           if (nn >= p.N) break;
           if (nn < p.n_main) {
             float v = r[i];
-            if constexpr (EPI == NT_EPI_RESIDUAL) v += (float)p.res[(int64_t)m * p.ld_res + nn];
+            if constexpr (EPI == NT_EPI_GATED_RESIDUAL) v *= sigmoid_gate((float)p.gate[(int64_t)m * p.ld_gate + nn]);
+            if constexpr (EPI == NT_EPI_RESIDUAL || EPI == NT_EPI_GATED_RESIDUAL) v += (float)p.res[(int64_t)m * p.ld_res + nn];
             p.y[(int64_t)m * p.ldy + nn] = (bf16)v;
           } else {
             p.y_tail[(int64_t)(nn - p.n_main) * p.ld_tail + tpos] = (bf16)r[i];
@@ -610,7 +622,7 @@ __global__ void __launch_bounds__(64 * kSmallWaves) linear_small_kernel(LinArgs 
 // scatter every store over 16 rows.
 constexpr int kStreamRows = 64;
 constexpr int kStreamThreads = 512;
-constexpr int kStreamMaxSamples = 1024;   // sample tables cached in LDS for pair-tiled tails
+constexpr int kStreamMaxSamples = kPairTiledMaxSamples;   // sample tables cached in LDS for pair-tiled tails
 
 // Pair-tiled position of packed pair cell m (Eq. coordinate inverted with the
 // sample tables): sample i by binary search over the pair offsets, then
@@ -900,9 +912,11 @@ constexpr int kWaveGroup = 8;                     // column tiles per product gr
 constexpr int kWaveMaxGroups = 4;                 // main columns up to 512
 constexpr int kWaveMaxTail = 2;                   // channel-major tail up to 32 channels
 
-template <int EPI> constexpr int wave_stage_stride() { return EPI == NT_EPI_RESIDUAL ? 132 : 144; }
+// residual epilogues stage fp32 values; the others bf16
+template <int EPI> constexpr bool wave_res() { return EPI == NT_EPI_RESIDUAL || EPI == NT_EPI_GATED_RESIDUAL; }
+template <int EPI> constexpr int wave_stage_stride() { return wave_res<EPI>() ? 132 : 144; }
 template <int EPI> constexpr int wave_stage_bytes() {
-  return 16 * wave_stage_stride<EPI>() * (EPI == NT_EPI_RESIDUAL ? 4 : 2);
+  return 16 * wave_stage_stride<EPI>() * (wave_res<EPI>() ? 4 : 2);
 }
 template <int K, int EPI> size_t wave_smem_bytes(int nt16) {
   return (size_t)nt16 * (K / 32) * 1024 + (size_t)nt16 * 16 * 4 + 2 * (size_t)K * 4 +
@@ -920,9 +934,10 @@ template <int K, int EPI> size_t wave_smem_bytes(int nt16) {
 // for the loads and defeats the prefetch.)
 template <int EPI, int K, bool BC, int G>
 __global__ void __launch_bounds__(kWaveThreads, 1) linear_wave_kernel(LinArgs p) {
-  static_assert(!BC || EPI != NT_EPI_RESIDUAL, "the broadcast rows use the residual buffers");
+  constexpr bool GATE = EPI == NT_EPI_GATED_RESIDUAL;  // residual + sigmoid(gate) * product
+  constexpr bool RES = wave_res<EPI>();
+  static_assert(!BC || !RES, "the broadcast rows use the residual buffers");
   constexpr int KT = K / 32;
-  constexpr bool RES = EPI == NT_EPI_RESIDUAL;
   constexpr int SS = wave_stage_stride<EPI>();
   extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
   const int nt16 = (p.N + 15) >> 4;
@@ -997,7 +1012,7 @@ __global__ void __launch_bounds__(kWaveThreads, 1) linear_wave_kernel(LinArgs p)
   // k = 32 kk + 8 g .. +7; residual rows in write-back order (4 chunks a lane);
   // broadcast sources: u in xr, v in rr (the walk is at the tile).  m0 and nv:
   // the tile's first output row and its rows
-  auto load_tile = [&](int t, uint4 (&xr)[KT], uint4 (&rr)[4], int64_t& m0, int& nv) {
+  auto load_tile = [&](int t, uint4 (&xr)[KT], uint4 (&rr)[4], uint4 (&gr)[4], int64_t& m0, int& nv) {
     if constexpr (BC) {
       static_assert(KT <= 4, "v rows fit the residual buffers");
       const bf16* su = p.bc_u + (int64_t)(w_vb + w_a) * p.ld_bc_u + g * 8;
@@ -1026,11 +1041,12 @@ __global__ void __launch_bounds__(kWaveThreads, 1) linear_wave_kernel(LinArgs p)
       for (int q = 0; q < 4; ++q) {
         const int row = q * 4 + (lane >> 4), cc = max(min(lane & 15, c8n - 1), 0), mm = min(t * 16 + row, p.rows - 1);
         rr[q] = *reinterpret_cast<const uint4*>(p.res + (int64_t)mm * p.ld_res + cc * 8);
+        if constexpr (GATE) gr[q] = *reinterpret_cast<const uint4*>(p.gate + (int64_t)mm * p.ld_gate + cc * 8);
       }
     }
   };
 
-  auto process = [&](int64_t m0, int nv, const uint4 (&xr_in)[KT], const uint4 (&rr)[4]) {
+  auto process = [&](int64_t m0, int nv, const uint4 (&xr_in)[KT], const uint4 (&rr)[4], const uint4 (&gr)[4]) {
     const int64_t m = m0 + l16;
     const bool mv = l16 < nv;
     uint4 xr[KT];
@@ -1137,8 +1153,15 @@ __global__ void __launch_bounds__(kWaveThreads, 1) linear_wave_kernel(LinArgs p)
           const float av[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
           float rv[8];
           XStage<bf16>::unpack(rr[q], rv);
+          if constexpr (GATE) {
+            float gv[8];
+            XStage<bf16>::unpack(gr[q], gv);
 #pragma unroll
-          for (int e = 0; e < 8; ++e) o[e] = (bf16)(av[e] + rv[e]);
+            for (int e = 0; e < 8; ++e) o[e] = (bf16)(av[e] * sigmoid_gate(gv[e]) + rv[e]);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) o[e] = (bf16)(av[e] + rv[e]);
+          }
         } else {
           o = *reinterpret_cast<const bf16x8*>(stage + (size_t)(row * SS + cc * 8) * 2);
         }
@@ -1186,16 +1209,16 @@ __global__ void __launch_bounds__(kWaveThreads, 1) linear_wave_kernel(LinArgs p)
   // after its loads would wait for everything in flight; loads issued in the
   // same step before the first use stay outstanding.  Past the end the
   // loads repeat valid rows and are never used.
-  uint4 xa[KT], ra[4], xb[KT], rb[4];
+  uint4 xa[KT], ra[4], ga[4], xb[KT], rb[4], gb[4];
   int64_t ma, mb;
   int na, nb;
-  load_tile(t0, xa, ra, ma, na);
+  load_tile(t0, xa, ra, ga, ma, na);
   for (int t = t0; t < t1; t += 2 * ts) {
-    load_tile(t + ts, xb, rb, mb, nb);
-    process(ma, na, xa, ra);
+    load_tile(t + ts, xb, rb, gb, mb, nb);
+    process(ma, na, xa, ra, ga);
     if (t + ts >= t1) break;
-    load_tile(t + 2 * ts, xa, ra, ma, na);
-    process(mb, nb, xb, rb);
+    load_tile(t + 2 * ts, xa, ra, ga, ma, na);
+    process(mb, nb, xb, rb, gb);
   }
 }
 
@@ -1210,10 +1233,17 @@ __global__ void __launch_bounds__(kWaveThreads, 1) linear_wave_kernel(LinArgs p)
 // for every channel it owns: one 16-byte store per channel, and the 16 lanes
 // of a channel write 256 contiguous bytes.  Chunk t of the planes is tile t,
 // so tiles run over [0, sum_pad/128) and padding cells get bias-only values.
+// GLU (K = 128, N = 512 product columns, 256 outputs): the weight rows are
+// [a_p; a_g; b_p; b_g] of 128 each, and output channel c of part q (a or b)
+// is sigmoid(g) * p of product columns 256 q + c and 256 q + 128 + c.  With
+// wave w owning column tiles w + 8 j, j = 0..3, a wave holds both columns of
+// every output it writes (j = 0, 1 for a; 2, 3 for b), so the gate is applied
+// in registers and only the gated operands are stored.
 constexpr int kTiledRows = 128;
 
-template <int K, int NTW>
+template <int K, int NTW, bool GLU = false>
 __global__ void __launch_bounds__(kStreamThreads, 1) linear_tiled_kernel(LinArgs p) {
+  static_assert(!GLU || (K == 128 && NTW == 4), "the gated-operand instance takes 4 x 128 product columns");
   constexpr int TR = kTiledRows;
   constexpr int SKR = frag_stride<K>();
   constexpr int KT = K / 32;
@@ -1339,29 +1369,46 @@ __global__ void __launch_bounds__(kStreamThreads, 1) linear_tiled_kernel(LinArgs
 
     // 8 subtiles (k-offsets); lane (r = l16, g) collects k-offsets 0..7 of
     // channels 4g..4g+3 of each owned column tile
-    bf16x8 hold[NTW][4];
+    constexpr int NH = GLU ? NTW / 2 : NTW;       // output column tiles held
+    bf16x8 hold[NH][4];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       bf16x8 xf[KT];
 #pragma unroll
       for (int kk = 0; kk < KT; ++kk) xf[kk] = *reinterpret_cast<const bf16x8*>(&xs[(u * 16 + l16) * SKR + kk * 32 + g * 8]);
+      if constexpr (GLU) {
 #pragma unroll
-      for (int j = 0; j < NTW; ++j) {
-        f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-        if (wave + 8 * j < nt16) {
+        for (int q = 0; q < 2; ++q) {
+          f32x4 ap = f32x4{0.f, 0.f, 0.f, 0.f}, ag = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int kk = 0; kk < KT; ++kk) acc = mfma16(wf[j][kk], xf[kk], acc);
+          for (int kk = 0; kk < KT; ++kk) {
+            ap = mfma16(wf[2 * q][kk], xf[kk], ap);
+            ag = mfma16(wf[2 * q + 1][kk], xf[kk], ag);
+          }
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            hold[q][i][u] = (bf16)((ap[i] + bv[2 * q][i]) * sigmoid_gate(ag[i] + bv[2 * q + 1][i]));
         }
+      } else {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) hold[j][i][u] = (bf16)(acc[i] + bv[j][i]);
+        for (int j = 0; j < NTW; ++j) {
+          f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+          if (wave + 8 * j < nt16) {
+#pragma unroll
+            for (int kk = 0; kk < KT; ++kk) acc = mfma16(wf[j][kk], xf[kk], acc);
+          }
+#pragma unroll
+          for (int i = 0; i < 4; ++i) hold[j][i][u] = (bf16)(acc[i] + bv[j][i]);
+        }
       }
     }
 #pragma unroll
-    for (int j = 0; j < NTW; ++j)
+    for (int j = 0; j < NH; ++j)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int c = (wave + 8 * j) * 16 + 4 * g + i;
-        if (c < p.N)
+        // GLU: output channel 128 q + 16 wave + 4 g + i of the two gated operands
+        const int c = GLU ? j * 128 + wave * 16 + 4 * g + i : (wave + 8 * j) * 16 + 4 * g + i;
+        if (GLU || c < p.N)
           *reinterpret_cast<bf16x8*>(p.y_tail + (int64_t)c * p.ld_tail + (int64_t)tile * TR + 8 * l16) = hold[j][i];
       }
     tile = next;
@@ -1597,6 +1644,8 @@ struct F32Args {
   float* y_tail;
   int64_t ld_tail;
   LinArgs pair;         // only the pair-tiled tail fields are used
+  const float* gate;    // NT_EPI_GATED_RESIDUAL
+  int64_t ld_gate;
 };
 
 __global__ void __launch_bounds__(256) linear_f32_kernel(F32Args p) {
@@ -1652,7 +1701,8 @@ __global__ void __launch_bounds__(256) linear_f32_kernel(F32Args p) {
     for (int k = 0; k < p.K; ++k) s = fmaf(xs[r * p.K + k], wr[k], s);
     if (p.epi == NT_EPI_GELU) s = 0.5f * s * (1.f + erff(s * 0.70710678118654752f));
     if (n < p.n_main) {
-      if (p.epi == NT_EPI_RESIDUAL) s += p.res[(int64_t)m * p.ld_res + n];
+      if (p.epi == NT_EPI_GATED_RESIDUAL) s /= 1.f + expf(-p.gate[(int64_t)m * p.ld_gate + n]);
+      if (p.epi == NT_EPI_RESIDUAL || p.epi == NT_EPI_GATED_RESIDUAL) s += p.res[(int64_t)m * p.ld_res + n];
       p.y[(int64_t)m * p.ldy + n] = s;
     } else {
       const int64_t pos = p.pair.tail_mode == kTailChannelMajor ? (int64_t)m : pair_tiled_pos(p.pair, m);
@@ -1692,21 +1742,22 @@ void launch_wave_g(const LinArgs& p, hipStream_t s) {
 template <int EPI, int K, bool BC = false>
 void launch_wave(const LinArgs& p, hipStream_t s) {
   if (p.n_main <= 16 * kWaveGroup) launch_wave_g<EPI, K, BC, 1>(p, s);
-  else if constexpr (EPI != NT_EPI_RESIDUAL) launch_wave_g<EPI, K, BC, kWaveMaxGroups>(p, s);
+  else if constexpr (!wave_res<EPI>()) launch_wave_g<EPI, K, BC, kWaveMaxGroups>(p, s);
 }
 
-template <int K>
+template <int K, bool GLU = false>
 void launch_tiled(const LinArgs& p, hipStream_t s) {
+  constexpr int NTW = GLU ? 4 : 2;
   static int per_cu = 0;
   if (per_cu == 0) {
     int nb = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, linear_tiled_kernel<K, 2>, kStreamThreads, 0) !=
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, linear_tiled_kernel<K, NTW, GLU>, kStreamThreads, 0) !=
             hipSuccess || nb < 1)
       nb = 1;
     per_cu = nb;
   }
   const int grid = std::min(p.ntiles, per_cu * compute_units());
-  if (grid > 0) linear_tiled_kernel<K, 2><<<dim3((unsigned)grid), dim3(kStreamThreads), 0, s>>>(p);
+  if (grid > 0) linear_tiled_kernel<K, NTW, GLU><<<dim3((unsigned)grid), dim3(kStreamThreads), 0, s>>>(p);
 }
 
 }  // namespace
@@ -1769,6 +1820,7 @@ hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
     p.blk_prow = plan.layout->d_blk_prow;
   }
   if (a.n_tail == 0) p.y_tail = nullptr;
+  p.gate = (const bf16*)a.gate; p.ld_gate = a.ld_gate;
 
   if (a.bcast_u) {
     // pair-broadcast rows: the wave-streamed kernel builds them from u and v
@@ -1798,6 +1850,7 @@ hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
     f.res = a.residual ? (const float*)a.residual : (const float*)a.x;
     f.ld_res = a.residual ? a.ld_residual : a.ldx;
     f.y = (float*)a.y; f.ldy = a.ldy; f.y_tail = (float*)a.y_tail; f.ld_tail = a.ld_tail; f.pair = p;
+    f.gate = (const float*)a.gate; f.ld_gate = a.ld_gate;
     const size_t smem = sizeof(float) * RB * ((size_t)a.c_in + (a.epilogue == NT_EPI_SWIGLU_RESIDUAL ? a.hidden : 0));
     linear_f32_kernel<<<dim3((rows + RB - 1) / RB), dim3(256), smem, s>>>(f);
     return hipGetLastError();
@@ -1836,6 +1889,35 @@ hipError_t launch_linear(const LinearPlan& plan, hipStream_t s) {
   p.mblocks = (rows + BM - 1) / BM;
   p.nblocks = (a.c_out + BN - 1) / BN;
   const bool xf = a.x_dtype == NT_F32;
+
+  if (a.epilogue == NT_EPI_SIGMOID_GLU) {
+    // gated operands straight into pair-tiled planes (checked by the caller:
+    // bf16, K = 128, hidden = 128, 256 outputs, all pair-tiled)
+    p.N = 2 * a.c_out;                            // product columns
+    p.n_main = 0;
+    p.cu_pairs = plan.layout->d_cu_pairs;
+    p.batch = plan.layout->batch;
+    p.ntiles = (int)(plan.layout->sum_pad / kTiledRows);
+    launch_tiled<128, true>(p, s);
+    return hipGetLastError();
+  }
+  if (a.epilogue == NT_EPI_GATED_RESIDUAL) {
+    // the wave-streamed kernel for bf16 rows of 64 or 128 features and at
+    // most 128 outputs, else the generic tile kernel
+    const int nt16 = (a.c_out + 15) / 16;
+    const size_t smem = a.c_in == 64 ? wave_smem_bytes<64, NT_EPI_GATED_RESIDUAL>(nt16)
+                                     : wave_smem_bytes<128, NT_EPI_GATED_RESIDUAL>(nt16);
+    if (!xf && a.n_tail == 0 && (a.c_in == 64 || a.c_in == 128) && p.n_main % 8 == 0 && p.n_main <= 128 &&
+        a.ldx % 8 == 0 && p.ldy % 8 == 0 && a.ld_residual % 8 == 0 && a.ld_gate % 8 == 0 && smem <= 150 * 1024) {
+      if (a.c_in == 64) launch_wave<NT_EPI_GATED_RESIDUAL, 64>(p, s);
+      else launch_wave<NT_EPI_GATED_RESIDUAL, 128>(p, s);
+      return hipGetLastError();
+    }
+    const unsigned grid = (unsigned)(((p.mblocks + kXcds - 1) / kXcds) * kXcds * p.nblocks);
+    if (xf) linear_mfma_kernel<float, NT_EPI_GATED_RESIDUAL><<<dim3(grid), dim3(256), 0, s>>>(p);
+    else linear_mfma_kernel<bf16, NT_EPI_GATED_RESIDUAL><<<dim3(grid), dim3(256), 0, s>>>(p);
+    return hipGetLastError();
+  }
 
   const bool tiled = p.y_tail && p.tail_mode != kTailChannelMajor;
   if (!a.ln_gamma && a.n_tail == 0 && a.c_in % 32 == 0 && rows <= kSmallRows) {

@@ -37,6 +37,7 @@ struct TriArgs {
   const int32_t* cu_pairs;
   const int32_t* cu_pad;
   int items, groups;     // tiles, and line groups of four channel blocks
+  int accumulate;        // 1: z += t;  0: z = t (z is not read)
 };
 
 __global__ void __launch_bounds__(kTriThreads, 1) triangle_mfma_kernel(TriArgs p) {
@@ -85,8 +86,10 @@ __global__ void __launch_bounds__(kTriThreads, 1) triangle_mfma_kernel(TriArgs p
       __builtin_amdgcn_global_load_lds((const void*)src, (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
     }
   };
-  z_copy(0, 0);
-  if (x0 + 16 < n) z_copy(1, 1);
+  if (p.accumulate) {
+    z_copy(0, 0);
+    if (x0 + 16 < n) z_copy(1, 1);
+  }
 
   // row tiles of the output tile that hold rows of the sample (uniform)
   bool xv[4], yv[4];
@@ -147,13 +150,18 @@ __global__ void __launch_bounds__(kTriThreads, 1) triangle_mfma_kernel(TriArgs p
       const float* st = &stage[(row * kTriRS + col) * kTriSC + half * 8];
       const float4 t0 = *reinterpret_cast<const float4*>(st);
       const float4 t1 = *reinterpret_cast<const float4*>(st + 4);
-      const uint4 zq = *reinterpret_cast<const uint4*>(&zbuf[xs & 1][(row * kTriTile + col) * kTriCB + half * 8]);
-      const uint32_t w4[4] = {zq.x, zq.y, zq.z, zq.w};
       float v[8];
+      if (p.accumulate) {
+        const uint4 zq = *reinterpret_cast<const uint4*>(&zbuf[xs & 1][(row * kTriTile + col) * kTriCB + half * 8]);
+        const uint32_t w4[4] = {zq.x, zq.y, zq.z, zq.w};
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        v[2 * j] = __uint_as_float(w4[j] << 16);
-        v[2 * j + 1] = __uint_as_float(w4[j] & 0xffff0000u);
+        for (int j = 0; j < 4; ++j) {
+          v[2 * j] = __uint_as_float(w4[j] << 16);
+          v[2 * j + 1] = __uint_as_float(w4[j] & 0xffff0000u);
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = 0.f;
       }
       v[0] += t0.x; v[1] += t0.y; v[2] += t0.z; v[3] += t0.w;
       v[4] += t1.x; v[5] += t1.y; v[6] += t1.z; v[7] += t1.w;
@@ -163,7 +171,7 @@ __global__ void __launch_bounds__(kTriThreads, 1) triangle_mfma_kernel(TriArgs p
       *reinterpret_cast<bf16x8*>(p.z + (cu + (int64_t)x * n + y) * p.ld_z + cb * kTriCB + half * 8) = o;
     }
     __syncthreads();                                  // stage and this band's z copy are free
-    if (xs + 2 < 4 && xv[xs + 2]) z_copy(xs + 2, xs & 1);
+    if (p.accumulate && xs + 2 < 4 && xv[xs + 2]) z_copy(xs + 2, xs & 1);
   }
 }
 
@@ -179,6 +187,7 @@ struct TriF32Args {
   const int32_t* cu_seqlens;
   const int32_t* cu_pairs;
   const int32_t* cu_pad;
+  int accumulate;
 };
 
 // One thread per (cell, channel) of the tile; exact fp32 dot over k.
@@ -199,7 +208,8 @@ __global__ void __launch_bounds__(256) triangle_f32_kernel(TriF32Args p) {
     const float* bp = p.b + (int64_t)c * p.ld_ab + P;
     float s = 0.f;
     for (int k = 0; k < n; ++k) s = fmaf(ap[tiled_offset(x, k, nkt)], bp[tiled_offset(y, k, nkt)], s);
-    p.z[(cu + (int64_t)x * n + y) * p.ld_z + c] += s;
+    float* zc = p.z + (cu + (int64_t)x * n + y) * p.ld_z + c;
+    *zc = p.accumulate ? *zc + s : s;
   }
 }
 
@@ -211,8 +221,11 @@ __global__ void __launch_bounds__(256) triangle_f32_kernel(TriF32Args p) {
 // (512 positions in fragment order, two per thread); channels are taken 16
 // bytes at a time: each thread loads that piece of its two source cells,
 // parks it in LDS, and the workgroup writes the chunk's channel slices of the
-// tile as contiguous 16-byte pieces.
-template <typename T, bool TRANS>
+// tile as contiguous 16-byte pieces.  GATED: each source row holds the
+// projection in channels [0, C) and the gate logits in [C, 2C), and the
+// plane receives sigmoid(gate) * projection (the gated operands of the
+// AlphaFold 3 form of the update), computed in fp32 and rounded once.
+template <typename T, bool TRANS, bool GATED = false>
 __global__ void __launch_bounds__(256) pack_tiled_kernel(const T* __restrict__ src, int64_t ld_src, int C,
                                                          T* __restrict__ dst, int64_t ld_dst, int batch,
                                                          const int32_t* __restrict__ cu_seqlens,
@@ -247,8 +260,19 @@ __global__ void __launch_bounds__(256) pack_tiled_kernel(const T* __restrict__ s
       uint4 piece = make_uint4(0u, 0u, 0u, 0u);
       if (row[h] >= 0) piece = *reinterpret_cast<const uint4*>(src + row[h] * ld_src + c0);
       const T* e = reinterpret_cast<const T*>(&piece);
+      if constexpr (GATED) {
+        uint4 gp = make_uint4(0u, 0u, 0u, 0u);
+        if (row[h] >= 0) gp = *reinterpret_cast<const uint4*>(src + row[h] * ld_src + C + c0);
+        const T* ge = reinterpret_cast<const T*>(&gp);
 #pragma unroll
-      for (int j = 0; j < V; ++j) park[j * 512 + q] = e[j];
+        for (int j = 0; j < V; ++j) {
+          const float gl = (float)ge[j];
+          park[j * 512 + q] = (T)((float)e[j] * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-gl * 1.4426950408889634f)));
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < V; ++j) park[j * 512 + q] = e[j];
+      }
     }
     __syncthreads();
 #pragma unroll
@@ -273,33 +297,36 @@ size_t triangle_workspace_bytes(const nt_layout& L, int C, nt_tri_operands opera
 
 namespace {
 
-// Re-tiles one packed operand (row stride ld_src) into planes at dst.
+// Re-tiles one packed operand (row stride ld_src) into planes at dst; gated:
+// sigmoid(src[:, C:2C]) * src[:, 0:C].
 hipError_t pack_planes(const nt_layout& L, const void* src, int64_t ld_src, bool trans, int C, void* dst,
-                       int64_t ldp, nt_dtype dtype, hipStream_t s) {
+                       int64_t ldp, nt_dtype dtype, hipStream_t s, bool gated = false) {
   const dim3 grid((unsigned)(L.sum_pad / 512));
   if (grid.x == 0) return hipSuccess;
-#define NT_PACK(T, TR) pack_tiled_kernel<T, TR><<<grid, dim3(256), 0, s>>>((const T*)src, ld_src, C, (T*)dst, ldp, \
-                                                                        L.batch, L.d_cu_seqlens, L.d_cu_pairs, L.d_cu_pad)
-  if (dtype == NT_BF16) { if (trans) NT_PACK(bf16, true); else NT_PACK(bf16, false); }
-  else { if (trans) NT_PACK(float, true); else NT_PACK(float, false); }
+#define NT_PACK(T, TR, G) pack_tiled_kernel<T, TR, G><<<grid, dim3(256), 0, s>>>((const T*)src, ld_src, C, (T*)dst, \
+                                                                        ldp, L.batch, L.d_cu_seqlens, L.d_cu_pairs, L.d_cu_pad)
+#define NT_PACK_G(T, TR) do { if (gated) NT_PACK(T, TR, true); else NT_PACK(T, TR, false); } while (0)
+  if (dtype == NT_BF16) { if (trans) NT_PACK_G(bf16, true); else NT_PACK_G(bf16, false); }
+  else { if (trans) NT_PACK_G(float, true); else NT_PACK_G(float, false); }
+#undef NT_PACK_G
 #undef NT_PACK
   return hipGetLastError();
 }
 
-// z[cell(x, y)] += sum_k PA[x, k] PB[y, k] over pair-tiled planes (channel stride ld_ab).
+// z[cell(x, y)] (+)= sum_k PA[x, k] PB[y, k] over pair-tiled planes (channel stride ld_ab).
 hipError_t contract(const nt_layout& L, int C, const void* a, const void* b, int64_t ld_ab, void* z, int64_t ld_z,
-                    nt_dtype dtype, hipStream_t s) {
+                    nt_dtype dtype, hipStream_t s, int accumulate = 1) {
   const int64_t items = L.tri_items();
   if (items == 0) return hipSuccess;
   if (dtype == NT_F32) {
     TriF32Args t{C, (const float*)a, (const float*)b, ld_ab, (float*)z, ld_z, L.d_tri_work, L.d_cu_seqlens,
-                 L.d_cu_pairs, L.d_cu_pad};
+                 L.d_cu_pairs, L.d_cu_pad, accumulate};
     triangle_f32_kernel<<<dim3((unsigned)items), dim3(256), 0, s>>>(t);
     return hipGetLastError();
   }
   const int nblk = C / kTriCB, groups = (nblk + 3) / 4;
   TriArgs t{C, nblk, (const bf16*)a, (const bf16*)b, ld_ab, (bf16*)z, ld_z, L.d_tri_work, L.d_cu_seqlens,
-            L.d_cu_pairs, L.d_cu_pad, (int)items, groups};
+            L.d_cu_pairs, L.d_cu_pad, (int)items, groups, accumulate};
   // items is a multiple of 8, so the grid splits evenly over the XCDs
   triangle_mfma_kernel<<<dim3((unsigned)(items * groups * 4)), dim3(kTriThreads), 0, s>>>(t);
   return hipGetLastError();
@@ -322,6 +349,22 @@ hipError_t launch_triangle(const nt_layout& L, int direction, int C, const void*
     return contract(L, C, wa, wb, ldp, z, ld_z, dtype, s);
   }
   return contract(L, C, a, b, ld_ab, z, ld_z, dtype, s);
+}
+
+hipError_t launch_triangle_gated(const nt_layout& L, int direction, int C, const void* a, const void* b,
+                                 int64_t ld_ab, nt_tri_operands operands, void* t, int64_t ld_t, nt_dtype dtype,
+                                 void* workspace, hipStream_t s) {
+  if (L.tri_items() == 0) return hipSuccess;
+  if (operands != NT_TRI_PACKED) return contract(L, C, a, b, ld_ab, t, ld_t, dtype, s, 0);
+  // gated operands re-tiled into the workspace in the direction's variant,
+  // then contracted into t (overwritten)
+  const int64_t ldp = (L.sum_pad + 7) / 8 * 8;
+  char* wa = static_cast<char*>(workspace);
+  char* wb = wa + (size_t)C * ldp * (dtype == NT_BF16 ? 2 : 4);
+  hipError_t e = pack_planes(L, a, ld_ab, direction == 1, C, wa, ldp, dtype, s, true);
+  if (e == hipSuccess) e = pack_planes(L, b, ld_ab, direction == 1, C, wb, ldp, dtype, s, true);
+  if (e != hipSuccess) return e;
+  return contract(L, C, wa, wb, ldp, t, ld_t, dtype, s, 0);
 }
 
 // Backward, per sample and channel c (T = A B^T outgoing, T = A^T B incoming):

@@ -21,6 +21,9 @@ constexpr int kAttnRG = 16;       // pair attention (head_dim 32): pair rows per
 constexpr int kAttnShortLen = 256;  // its instance with two workgroups per CU: longest sample
 constexpr int kAttnLongLen = 512;   // its instance with one workgroup per CU: longest sample
 
+// Samples whose tables the pair-tiled projection kernels cache in LDS.
+constexpr int kPairTiledMaxSamples = 1024;
+
 // Attention limits imposed by staging a whole key segment in LDS.
 constexpr int kAttnMaxLenD32 = 1024;
 constexpr int kAttnMaxLenD64 = 512;
@@ -202,10 +205,13 @@ hipError_t launch_attention_backward(const nt_layout& L, int axis, int H, const 
 size_t attention_workspace_bytes(const nt_layout& L, int axis, int H, int D, nt_dtype dtype, bool has_bias);
 // bias element (cell c, head h) at bias[c * ld_bias + h * ld_bias_head];
 // workspace: attention_workspace_bytes(...) bytes.
+// gate (axes 0 and 1, or NULL): o = sigmoid(gate) * attention, gate element
+// (cell, channel) at gate[cell * ld_gate + channel].
 hipError_t launch_attention(const nt_layout& L, int axis, int H, int D,
                             const void* q, const void* k, const void* v, int64_t ld_qkv,
                             const void* bias, int64_t ld_bias, int64_t ld_bias_head, float scale,
-                            void* o, int64_t ld_o, nt_dtype dtype, void* workspace, hipStream_t s);
+                            void* o, int64_t ld_o, nt_dtype dtype, void* workspace, hipStream_t s,
+                            const void* gate = nullptr, int64_t ld_gate = 0);
 
 // Cross-attention over singles: queries by Lq's offsets, keys and values by
 // Lkv's (same batch); bf16 head_dim 32 / 64 with every key segment at most
@@ -222,6 +228,12 @@ size_t triangle_workspace_bytes(const nt_layout& L, int C, nt_tri_operands opera
 hipError_t launch_triangle(const nt_layout& L, int direction, int C, const void* a, const void* b,
                            int64_t ld_ab, nt_tri_operands operands, void* z, int64_t ld_z, nt_dtype dtype,
                            void* workspace, hipStream_t s);
+// Gated operands: packed (a, b: [sum N^2, 2C] rows of [projection | gate
+// logits], row stride ld_ab, gated while re-tiled into the workspace) or
+// already-gated pair-tiled planes; t = triangle(a, b), overwritten.
+hipError_t launch_triangle_gated(const nt_layout& L, int direction, int C, const void* a, const void* b,
+                                 int64_t ld_ab, nt_tri_operands operands, void* t, int64_t ld_t, nt_dtype dtype,
+                                 void* workspace, hipStream_t s);
 // Backward of the triangle update on packed operands: da, db (row stride
 // ld_dab; either may be NULL) accumulate the gradients; the workspace is
 // triangle_workspace_bytes(L, C, NT_TRI_PACKED, dtype).

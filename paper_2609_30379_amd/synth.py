@@ -66,6 +66,9 @@ def _pair_gains(n_max: int, blocks: int = 1) -> dict:
         "gu": 1.0, "d": 0.25 * damp,   # SwiGLU transition
         "s": 0.5,                 # single update from the column mean
         "gate": 1.0,              # gate logits of the gated (AlphaFold 3 form) steps
+        # gated triangle: t is normalised before use, so a_p, b_p are scaled
+        # to give t of order 0.3 (sigmoid gates halve each operand)
+        "ab_g": float(np.sqrt(0.3 / n_max)) * 4.0 * np.sqrt(damp),
     }
 
 
@@ -214,7 +217,7 @@ def pair_block_params(w: Workload, block: int = 0, seed: int | None = None) -> d
     for key in [s for s in w.steps if s.startswith("tri_") and s.endswith("_g")]:
         # [a_p | a_g | b_p | b_g | g], then LN(t) and the output projection
         p[f"{key}.ln_g"], p[f"{key}.ln_b"] = _ln(seed, pre + key, cz)
-        parts = [_linear(seed, pre + f"{key}.{nm}", cz, cz, g["ab"] if nm in ("ap", "bp") else g["gate"], dt)
+        parts = [_linear(seed, pre + f"{key}.{nm}", cz, cz, g["ab_g"] if nm in ("ap", "bp") else g["gate"], dt)
                  for nm in ("ap", "ag", "bp", "bg", "g")]
         p[f"{key}.w"] = np.concatenate([a for a, _ in parts], 0)
         p[f"{key}.b"] = np.concatenate([b for _, b in parts], 0)

@@ -81,9 +81,16 @@ def ulp_bf16(x) -> np.ndarray:
 CHAIN_ULPS = 2.0
 
 
-def check_chained(got: np.ndarray, ref: np.ndarray, what: str = ""):
-    """Chained bf16 comparison: every element within 2e-2, or within two bf16
-    ulps of the larger of the two values where that is wider."""
+# The gated triangle update normalises its contraction t before the output
+# projection, so a one-ulp rounding difference of t moves the update by
+# ulp(t) / std(t) of a unit-variance value: chains through it flip further.
+CHAIN_ULPS_GATED = 4.0
+
+
+def check_chained(got: np.ndarray, ref: np.ndarray, what: str = "", ulps: float = CHAIN_ULPS):
+    """Chained bf16 comparison: every element within 2e-2, or within `ulps`
+    bf16 ulps (two by default) of the larger of the two values where that is
+    wider."""
     got = np.asarray(got, np.float64)
     ref = np.asarray(ref, np.float64)
     assert got.shape == ref.shape, (what, got.shape, ref.shape)
@@ -91,14 +98,14 @@ def check_chained(got: np.ndarray, ref: np.ndarray, what: str = ""):
     if got.size == 0:
         return 0.0
     d = np.abs(got - ref)
-    bound = np.maximum(BF16_MAX_ABS, CHAIN_ULPS * ulp_bf16(np.maximum(np.abs(got), np.abs(ref))))
+    bound = np.maximum(BF16_MAX_ABS, ulps * ulp_bf16(np.maximum(np.abs(got), np.abs(ref))))
     err = float(np.max(d))
     ratio = float(np.max(d / bound))
     amax = float(np.max(np.abs(ref)))
-    PARITY_LOG.append((what + f" [chained; {ratio:.2f} of max(2e-2, 2 ulp)]", err, BF16_MAX_ABS, amax))
+    PARITY_LOG.append((what + f" [chained; {ratio:.2f} of max(2e-2, {ulps:g} ulp)]", err, BF16_MAX_ABS, amax))
     worst = int(np.argmax(d / bound))
     assert ratio <= 1.0, (f"{what}: chained error {d.flat[worst]:.4g} at |ref| {abs(ref.flat[worst]):.3g} "
-                          f"exceeds max(2e-2, {CHAIN_ULPS:g} ulp)")
+                          f"exceeds max(2e-2, {ulps:g} ulp)")
     assert amax < BF16_MAX_MAGNITUDE, f"{what}: reference magnitude {amax:.3g} beyond the bf16 range of the bar"
     return err
 

@@ -158,6 +158,16 @@ def test_op_argument_errors_need_no_device(lib):
          B.NT_ERR_INVALID_ARG),                                          # x set
         (dict(x=None, bcast_u=C.c_void_p(0x7000), bcast_v=C.c_void_p(0x8000), ld_bcast_u=16, ld_bcast_v=16,
               rows=25, layout=host.handle, level=1), B.NT_ERR_INVALID_ARG),   # host-only layout
+        # gated residual: needs residual and gate, no tail; a gate needs that epilogue
+        (dict(epilogue=4, residual=C.c_void_p(0x6000), ld_residual=16), B.NT_ERR_INVALID_ARG),
+        (dict(epilogue=4, gate=C.c_void_p(0x6000), ld_gate=16), B.NT_ERR_INVALID_ARG),
+        (dict(epilogue=4, residual=C.c_void_p(0x6000), ld_residual=16, gate=C.c_void_p(0x9000), ld_gate=12),
+         B.NT_ERR_INVALID_ARG),                                          # ld_gate not a multiple of 8
+        (dict(epilogue=4, residual=C.c_void_p(0x6000), ld_residual=16, gate=C.c_void_p(0x9000), ld_gate=16,
+              n_tail=4, y_tail=C.c_void_p(0x5000), ld_tail=16), B.NT_ERR_UNSUPPORTED),
+        (dict(gate=C.c_void_p(0x9000), ld_gate=16), B.NT_ERR_INVALID_ARG),
+        (dict(epilogue=5), B.NT_ERR_UNSUPPORTED),                        # sigmoid GLU outside its one shape
+        (dict(epilogue=6), B.NT_ERR_INVALID_ARG),
     ]
     for kw, want in cases:
         a = _linear_args(**kw)

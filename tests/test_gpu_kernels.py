@@ -142,6 +142,40 @@ def test_layernorm_linear(B, R, K, N, ln, epi, xdt, dtype, n_tail):
         check(host(yt)[:, :R].T, ref[:, N - n_tail:], dtype, "linear tail")
 
 
+GATED_LIN_CASES = [
+    # rows, K, N, ln, x dtype, dtype: the output of the gated triangle update
+    (1000, 128, 128, True, "bf16", "bf16"),     # wave kernel
+    (777, 64, 64, True, "bf16", "bf16"),        # wave kernel, K = 64, last tile of 9 rows
+    (5000, 128, 128, False, "bf16", "bf16"),    # wave kernel without LayerNorm
+    (300, 136, 40, True, "bf16", "bf16"),       # generic tile kernel
+    (129, 128, 256, True, "bf16", "bf16"),      # more than 128 outputs: generic tile kernel
+    (100, 16, 16, True, "f32", "f32"),
+]
+
+
+@pytest.mark.parametrize("R,K,N,ln,xdt,dtype", GATED_LIN_CASES)
+def test_layernorm_linear_gated_residual(B, R, K, N, ln, xdt, dtype):
+    """y = residual + sigmoid(gate) * (LN(x) W^T + b); the gate and the
+    residual are column slices of wider buffers."""
+    import torch
+    x = _n(40, "x", (R, K), 0.5, xdt)
+    w = _n(41, "w", (N, K), 1.0 / np.sqrt(K), dtype)
+    b = _n(42, "b", (N,), 0.1, "f32")
+    g = _n(43, "g", (K,), 0.1, "f32") + 1.0
+    be = _n(44, "be", (K,), 0.1, "f32")
+    wide = _n(45, "gate_res", (R, 2 * N + 8), 0.5, dtype)
+    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    wd = dev(wide, dtype)
+    gate, res = wd[:, :N], wd[:, N + 8:]
+    y = torch.full((R, N), float("nan"), dtype=td, device="cuda")
+    B.nt_layernorm_linear(dev(x, xdt), dev(w, dtype), dev(b, "f32"), y,
+                          ln=(dev(g, "f32"), dev(be, "f32")) if ln else None, epilogue="gated_residual",
+                          residual=res, gate=gate)
+    ref = O.layernorm_linear(x, w, b, ln=(g, be) if ln else None, epilogue="gated_residual",
+                             residual=wide[:, N + 8:], gate=wide[:, :N])
+    check(host(y), ref, dtype, f"linear gated residual {R}x{K}->{N} ln={ln}")
+
+
 @pytest.mark.parametrize("lname,C,N,epi", [("ragged", 128, 128, "none"), ("tiny", 64, 64, "none"),
                                            ("ragged", 64, 96, "gelu"), ("one", 128, 128, "none"),
                                            ("small_mix", 128, 256, "none"), ("wide", 128, 128, "none")])
@@ -193,6 +227,41 @@ def test_layernorm_linear_pair_tiled_tail(B, transposed, dtype, C):
                           layout=lay, level="pairs", c_out=2 * C)
     ref = O.layernorm_linear(x, w, b, ln=(g, be))
     check(untile_pair(host(yt), L, transposed), ref, dtype, "pair-tiled tail")
+
+
+@pytest.mark.parametrize("transposed", [False, True])
+@pytest.mark.parametrize("lname", ["ragged", "tiny", "one"])
+def test_layernorm_linear_sigmoid_glu_pair_tiled(B, transposed, lname):
+    """Gated operands sigmoid(a_g) a_p | sigmoid(b_g) b_p of [a_p; a_g; b_p; b_g]
+    rows written straight into pair-tiled planes (C = 128), and contracted by
+    the gated triangle call on those planes."""
+    import torch
+    from oracle import blocks as OB
+    from oracle.numerics import store
+    L, C = LENGTHS[lname], 128
+    lay = _layout(B, L)
+    R = sum(n * n for n in L)
+    x = _n(50, "x", (R, C), 0.5, "bf16")
+    w = _n(51, "w", (4 * C, C), 1.0 / np.sqrt(C), "bf16")
+    w[:C] = synth.snap_bf16(0.3 * w[:C])                 # projections a_p, b_p scaled so |t| stays below 8
+    w[2 * C:3 * C] = synth.snap_bf16(0.3 * w[2 * C:3 * C])
+    b = _n(52, "b", (4 * C,), 0.1, "f32")
+    g, be = _n(53, "g", (C,), 0.1, "f32") + 1, _n(54, "be", (C,), 0.1, "f32")
+    ld = (lay.sum_pad + 7) // 8 * 8
+    yt = torch.full((2 * C, ld), float("nan"), dtype=torch.bfloat16, device="cuda")
+    variant = "pair_tiled_t" if transposed else "pair_tiled"
+    B.nt_layernorm_linear(dev(x, "bf16"), dev(w, "bf16"), dev(b, "f32"), None, ln=(dev(g, "f32"), dev(be, "f32")),
+                          epilogue="sigmoid_glu", hidden=C, n_tail=2 * C, y_tail=yt, tail_layout=variant,
+                          layout=lay, level="pairs", c_out=2 * C)
+    proj = O.layernorm_linear(x, w, b, ln=(g, be))
+    a_ref, b_ref = OB.ref_gated_operands(np.concatenate([proj, np.zeros((R, C))], 1), C)
+    got = untile_pair(host(yt), L, transposed)
+    check(got, np.concatenate([a_ref, b_ref], 1), "bf16", f"sigmoid GLU pair-tiled {lname} transposed={transposed}")
+    t = torch.full((R, C), float("nan"), dtype=torch.bfloat16, device="cuda")
+    B.nt_triangle_mul_gated(lay, 1 if transposed else 0, yt[:C], yt[C:], t, operands=variant)
+    ref = O.triangle_mul(store(got[:, :C], "bf16"), store(got[:, C:], "bf16"), L,
+                         "incoming" if transposed else "outgoing")
+    check(host(t), ref, "bf16", f"gated triangle on GLU planes {lname} transposed={transposed}")
 
 
 @pytest.mark.parametrize("R,K,F,dtype", [(1000, 128, 512, "bf16"), (333, 64, 256, "bf16"), (65, 256, 96, "bf16"),
@@ -277,6 +346,40 @@ def test_pair_attention(B, axis, dtype, H, D, lset, bias_layout):
     assert np.array_equal(host(o), first, equal_nan=True), "pair attention is not deterministic"
     ref = O.pair_row_attention(qkv[:, :c], qkv[:, c:2 * c], qkv[:, 2 * c:], bias, L, H, D, axis=axis)
     check(first, ref, dtype, f"pair attention axis {axis} {dtype} {lset} H={H} d={D} bias {bias_layout}")
+
+
+@pytest.mark.parametrize("axis", [0, 1])
+@pytest.mark.parametrize("dtype,H,D,lset", [("bf16", 4, 32, "att"), ("bf16", 2, 32, "mid512"),
+                                            ("bf16", 2, 32, "long"), ("bf16", 2, 64, "tiny"),
+                                            ("f32", 2, 8, "tiny")])
+def test_pair_attention_gated(B, axis, dtype, H, D, lset):
+    """o = sigmoid(g) * attention with the gate a column slice of the q|k|v|g
+    projection: the persistent and work-list instances of the head_dim 32
+    kernel (N <= 256, <= 512), the per-row path (N > 512, head_dim 64) and
+    fp32; a second call repeats bit for bit."""
+    import torch
+    L = {"att": ATT_LENGTHS, "tiny": LENGTHS["tiny"], "long": [530, 7, 64], "mid512": [512, 257, 1, 100]}[lset]
+    lay = _layout(B, L)
+    R = sum(n * n for n in L)
+    c = H * D
+    qkvg = _n(46, "qkvg", (R, 4 * c), 1.0, dtype)
+    qkvg[:, 2 * c:3 * c] *= 0.5
+    if dtype == "bf16":
+        qkvg = synth.snap_bf16(qkvg)
+    bias = _n(47, "bias", (R, H), 1.0, dtype)
+    qd = dev(qkvg, dtype)
+    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    o = torch.full((R, c), float("nan"), dtype=td, device="cuda")
+    bd = dev(_head_major(bias), dtype)
+    call = lambda: B.nt_pair_row_attention(lay, axis, H, D, qd[:, :c], qd[:, c:2 * c], qd[:, 2 * c:3 * c], o,  # noqa: E731
+                                           bias=bd, bias_layout="heads", gate=qd[:, 3 * c:])
+    call()
+    first = host(o)
+    call()
+    assert np.array_equal(host(o), first, equal_nan=True), "gated pair attention is not deterministic"
+    ref = O.pair_row_attention(qkvg[:, :c], qkvg[:, c:2 * c], qkvg[:, 2 * c:3 * c], bias, L, H, D, axis=axis,
+                               gate=qkvg[:, 3 * c:])
+    check(first, ref, dtype, f"gated pair attention axis {axis} {dtype} {lset} H={H} d={D}")
 
 
 @pytest.mark.parametrize("H,lset", [(4, "att"), (12, "att"), (12, "mid512"), (4, "one")])
@@ -448,3 +551,31 @@ def test_triangle_packed(B, direction, dtype, C, L):
         sl = slice(int(cu[i]), int(cu[i + 1]))
         ref = z0[sl] + O.triangle_mul(ab[sl, :C], ab[sl, C:], [n], direc)
         check(got[sl], ref, dtype, f"triangle packed dir {direction} {dtype} C={C} sample N={n}")
+
+TRI_GATED = [("bf16", 64, [5, 0, 1, 37, 64, 3, 70], 0.5), ("bf16", 128, [257, 130, 1], 0.35),
+             ("f32", 16, [15, 12, 10, 7], 0.5)]
+
+
+@pytest.mark.parametrize("direction", [0, 1])
+@pytest.mark.parametrize("dtype,C,L,gain", TRI_GATED)
+def test_triangle_gated(B, direction, dtype, C, L, gain):
+    """t = triangle(sigmoid(a_g) a_p, sigmoid(b_g) b_p) from one [a_p|a_g|b_p|b_g]
+    projection; t is overwritten (NaN before the call), never read."""
+    import torch
+    from oracle.numerics import store
+    lay = _layout(B, L)
+    R = sum(n * n for n in L)
+    p4 = _n(48, "p4", (R, 4 * C), 1.0, dtype)
+    p4[:, 0:C] *= gain
+    p4[:, 2 * C:3 * C] *= gain
+    if dtype == "bf16":
+        p4 = synth.snap_bf16(p4)
+    pd = dev(p4, dtype)
+    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    t = torch.full((R, C), float("nan"), dtype=td, device="cuda")
+    B.nt_triangle_mul_gated(lay, direction, pd[:, :2 * C], pd[:, 2 * C:], t)
+    a = store(O.gated_operand(p4[:, :C], p4[:, C:2 * C]), dtype)
+    b = store(O.gated_operand(p4[:, 2 * C:3 * C], p4[:, 3 * C:]), dtype)
+    ref = O.triangle_mul(a, b, L, "outgoing" if direction == 0 else "incoming")
+    check(host(t), ref, dtype, f"gated triangle {dtype} C={C} L={L} direction {direction}")
+

@@ -23,7 +23,8 @@ import pytest
 from oracle import blocks as OB
 from oracle.numerics import store
 from paper_2609_30379_amd import synth
-from tests.gpu_util import PARITY_LOG, check, check_chained, ulp_bf16, tiled_offsets, _tiled_plane_index
+from tests.gpu_util import (CHAIN_ULPS, CHAIN_ULPS_GATED, PARITY_LOG, check, check_chained, ulp_bf16,
+                             tiled_offsets, _tiled_plane_index)
 
 pytestmark = pytest.mark.gpu
 
@@ -93,6 +94,41 @@ class SampleTap:
             z = self._rows(t["z"], self.rp)
             self._cmp(z, OB.ref_ln_linear(self.z, p, "lin", keep), op)
             self.z = z
+        elif op.endswith(".proj") and op.startswith("att") and op[:-5].endswith("_g"):
+            step = op[:-5]
+            qkvg = np.concatenate([self._rows(t["qkv"], self.rp), self._rows(t["g"], self.rp)], 1)
+            beta = t["bias"][:, self.rp[0]:self.rp[1]].float().cpu().numpy().astype(np.float64).T
+            self._cmp(np.concatenate([qkvg, beta], 1), OB.ref_ln_linear(self.z, p, step, keep), op)
+            self.qkvg, self.beta = qkvg, beta
+        elif op.endswith(".attention") and op[:-10].endswith("_g"):
+            o = self._rows(t["o"], self.rp)
+            axis = 0 if op.startswith("att_row") else 1
+            self._cmp(o, OB.ref_attention_gated(self.qkvg, self.beta, L, C, H, d, axis), op)
+            self.o = o
+        elif op.endswith(".proj") and op.startswith("tri") and op[:-5].endswith("_g"):
+            # gated operands in pair-tiled planes, and the output gate logits
+            step = op[:-5]
+            g = self._rows(t["g"], self.rp)
+            proj = OB.ref_ln_linear(self.z, p, step, keep)
+            if "ab" in t:                             # gated operands written as pair-tiled planes
+                planes = t["ab"][:, self.tp[0]:self.tp[1]].float().cpu().numpy().astype(np.float64)
+                ab = planes[:, _tiled_plane_index(self.n, step == "tri_in_g")].T
+                self._cmp(np.concatenate([ab, g], 1),
+                          np.concatenate([*OB.ref_gated_operands(proj, C), proj[:, 4 * C:]], 1), op)
+            else:                                     # the projection stored, gated while re-tiled
+                p4 = self._rows(t["p4"], self.rp)
+                self._cmp(np.concatenate([p4, g], 1), proj, op)
+                ab = np.concatenate([keep(x) for x in OB.ref_gated_operands(p4, C)], 1)
+            self.ab, self.g = ab, g
+        elif op.endswith(".triangle") and op[:-9].endswith("_g"):
+            tt = self._rows(t["t"], self.rp)
+            direction = "outgoing" if op.startswith("tri_out") else "incoming"
+            self._cmp(tt, OB.ref_triangle_t(self.ab[:, :C], self.ab[:, C:], L, direction), op)
+            self.t = tt
+        elif op.endswith(".out") and op.startswith("tri") and op[:-4].endswith("_g"):
+            z = self._rows(t["z"], self.rp)
+            self._cmp(z, OB.ref_gated_out(self.t, self.g, self.z, p, op[:-4], keep), op)
+            self.z = z
         elif op.endswith(".proj") and op.startswith("att"):
             step = op[:-5]
             qkv = self._rows(t["qkv"], self.rp)
@@ -143,8 +179,9 @@ class SampleTap:
         s_ref, z_ref, _ = OB.pair_block(s_in, [self.n], self.run.params[block], self.dims, steps, z=z_in,
                                         dtype=w.dtype, round_last=False)
         what = f"{w.name} sample {self.i} N={self.n} block {block} (from the GPU's block input)"
-        check_chained(self.z, z_ref, what + " z")
-        check_chained(self.s, s_ref, what + " s")
+        ulps = CHAIN_ULPS_GATED if any(t.endswith("_g") for t in steps) else CHAIN_ULPS
+        check_chained(self.z, z_ref, what + " z", ulps=ulps)
+        check_chained(self.s, s_ref, what + " s", ulps=ulps)
 
 
 # (workload, sample): each workload's longest sample and a short one; the
@@ -158,6 +195,8 @@ KERNEL_CASES = [
     ("pairformer4_b16_lognormal192_bf16", 6),   # N = 420
     ("pairformer4_b16_lognormal192_bf16", 7),   # N = 339
     ("pairformer4_b16_lognormal192_bf16", 12),  # N = 48
+    ("pairformer4_gated_b16_lognormal192_bf16", 7),   # N = 339
+    ("pairformer4_gated_b16_lognormal192_bf16", 12),  # N = 48
 ]
 
 
@@ -167,7 +206,7 @@ def test_every_kernel_on_gpu_inputs(wname, i):
     print(f"per-kernel gating: {wname} sample {i} N={run.lengths[i]}", flush=True)
     tap = SampleTap(run, i, gate_kernels=True, gate_blocks=True)
     run.step(tap=tap)
-    per_block = 10 if wname.startswith("pair_b8") else 15
+    per_block = 10 if wname.startswith("pair_b8") else (17 if "gated" in wname else 15)
     assert tap.ops == per_block * run.w.blocks
 
 
