@@ -287,3 +287,28 @@ def mechanism_step(x, lengths, p, dtype="bf16", y=None, cols=None, S=1):
         dx = dx + gv["dx"]
     out["dx"] = dx
     return out
+
+
+def mechanism_step_nonleading(x, lengths, p, S, dtype="bf16"):
+    """The single-pair-single training step in the non-leading layout (Eq.
+    packing: an element (S, N_i, C) packs as (N_i, S, C), so x is
+    [sum N, S*C] with X_i[s] = x[eta_i:eta_{i+1}, s*C:(s+1)*C]; App. A runs
+    the program with S = 3).  Every op acts on the feature axis or on the
+    ragged axes of one s, so the program on X_i is the leading program on
+    each X_i[s] with shared weights: the pair state is (S, N_i, N_i, C_p),
+    packed [sum N^2, S*C_p]; the loss of Eq. joint-diagnostic-loss sums over
+    all S slices with S in both denominators; weight gradients sum over s.
+    Returns the keys of mechanism_step, with xt, pt, dx in the packed
+    non-leading layout."""
+    x = np.asarray(x, np.float64)
+    C = x.shape[1] // S
+    outs = [mechanism_step(x[:, s * C:(s + 1) * C], lengths, p, dtype=dtype, S=S) for s in range(S)]
+    res = {"xt": np.concatenate([o["xt"] for o in outs], 1),
+           "pt": np.concatenate([o["pt"] for o in outs], 1),
+           "dx": np.concatenate([o["dx"] for o in outs], 1),
+           "loss_s": sum(o["loss_s"] for o in outs), "loss_p": sum(o["loss_p"] for o in outs),
+           "loss": float(sum(o["loss"] for o in outs))}
+    for k in outs[0]:
+        if k.startswith("d_"):
+            res[k] = sum(o[k] for o in outs)
+    return res

@@ -282,3 +282,54 @@ def test_gated_attention_gate_scales_the_output():
         plain = ops.pair_row_attention(q, k, v, bias, L, H, d, axis=axis)
         half = ops.pair_row_attention(q, k, v, bias, L, H, d, axis=axis, gate=np.zeros((R, H * d)))
         np.testing.assert_allclose(half, 0.5 * plain, rtol=1e-14, atol=1e-14)
+
+
+def test_nonleading_mechanism_equals_dense_torch_autograd(torch_cpu):
+    """The non-leading program (elements (S, N_i, C), packed (N_i, S, C))
+    equals a dense padded torch program on [B, S, N, C] with masks, and its
+    gradients equal torch autograd of that program's loss (fp32 mode)."""
+    torch = torch_cpu
+    L, S, C, Cp = [3, 1, 4], 3, 6, 4
+    p = _mech_params(C, Cp, 8)
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((sum(L), S * C))
+    out = blocks.mechanism_step_nonleading(x, L, p, S, dtype="f32")
+
+    B, N = len(L), max(L)
+    T = {k: torch.tensor(np.asarray(v, np.float64), requires_grad=True) for k, v in p.items()}
+    X = torch.zeros(B, S, N, C, dtype=torch.float64)
+    o = layout.single_offsets(L)
+    for i, n in enumerate(L):                      # unpack (N_i, S, C) -> (S, N_i, C)
+        X[i, :, :n] = torch.from_numpy(x[o[i]:o[i + 1]].reshape(n, S, C).transpose(1, 0, 2))
+    X.requires_grad_(True)
+    valid = torch.zeros(B, N, dtype=torch.bool)
+    for i, n in enumerate(L):
+        valid[i, :n] = True
+    cell = (valid[:, :, None] & valid[:, None, :])[:, None, :, :, None]       # [B, 1, N, N, 1]
+    u = F.linear(X, T["u.w"], T["u.b"])
+    v = F.linear(X, T["v.w"], T["v.b"])
+    P = (u[:, :, :, None, :] + v[:, :, None, :, :]) * cell                    # [B, S, N, N, Cp]
+    xn = F.layer_norm(P, (Cp,), T["trans.ln_g"], T["trans.ln_b"], 1e-5)
+    gu = F.linear(xn, T["trans.w"], T["trans.b"])
+    Fh = gu.shape[-1] // 2
+    Pt = (P + F.linear(F.silu(gu[..., :Fh]) * gu[..., Fh:], T["trans.w2"], T["trans.b2"])) * cell
+    n_i = torch.tensor(L, dtype=torch.float64).clamp(min=1)[:, None, None, None]
+    m = Pt.sum(3) / n_i                                                          # mean over b
+    Xt = (X + F.linear(m, T["g.w"], T["g.b"])) * valid[:, None, :, None]
+    alpha = torch.tensor([1.0 + i / B for i in range(B)], dtype=torch.float64)
+    beta = torch.tensor([1.5 - i / (2.0 * B) for i in range(B)], dtype=torch.float64)
+    loss = (alpha * (Xt ** 2).sum((1, 2, 3))).sum() / (S * C * sum(L)) + \
+        (beta * (Pt ** 2).sum((1, 2, 3, 4))).sum() / (S * Cp * sum(n * n for n in L))
+    loss.backward()
+    lv = float(loss.detach())
+    assert abs(out["loss"] - lv) <= 1e-12 * lv
+    xt_ref = np.concatenate([Xt[i, :, :n].detach().numpy().transpose(1, 0, 2).reshape(n, S * C)
+                             for i, n in enumerate(L)])
+    np.testing.assert_allclose(out["xt"], xt_ref, rtol=1e-11, atol=1e-11)
+    pt_ref = np.concatenate([Pt[i, :, :n, :n].detach().numpy().transpose(1, 2, 0, 3).reshape(n * n, S * Cp)
+                             for i, n in enumerate(L)])
+    np.testing.assert_allclose(out["pt"], pt_ref, rtol=1e-11, atol=1e-11)
+    dx_ref = np.concatenate([X.grad[i, :, :n].numpy().transpose(1, 0, 2).reshape(n, S * C) for i, n in enumerate(L)])
+    np.testing.assert_allclose(out["dx"], dx_ref, rtol=1e-9, atol=1e-12)
+    for k in p:
+        np.testing.assert_allclose(out["d_" + k], T[k].grad.numpy(), rtol=1e-9, atol=1e-12, err_msg=k)
