@@ -150,9 +150,12 @@ def mechanism_op_costs(w, L, M):
     """Algorithmic HBM bytes and flops per launch of the ops of one training
     step of the single-pair-single program (forward, loss, backward); M is
     None for square pairs.  bf16 tensors 2 bytes, fp32 4."""
-    S = sum(L)
+    # non-leading layout: every packed position holds s_axis feature vectors,
+    # so each count of positions below is s_axis times larger
+    Sx = w.s_axis
+    S = sum(L) * Sx
     Mc = S if M is None else sum(M)
-    cells = sum(n * n for n in L) if M is None else sum(n * m for n, m in zip(L, M))
+    cells = (sum(n * n for n in L) if M is None else sum(n * m for n, m in zip(L, M))) * Sx
     C, Cp, F = w.c_s, w.c_z, w.hidden
     xin = (S + (0 if M is None else Mc)) * C * 2
     return {
@@ -390,6 +393,8 @@ def measure(w, steps: int, warmup: int, graph: bool = False, cpu: bool = False):
     R, S = sum(n * n for n in L), sum(L)
     if mech and run.rect:
         R = sum(n * m for n, m in zip(L, run.cols))
+    if mech:                                      # non-leading: s_axis pair positions per packed cell
+        R, S = R * w.s_axis, S * w.s_axis
     stream = torch.cuda.current_stream()          # the stream every nt_* call launches on
 
     for _ in range(max(1, warmup)):
@@ -481,7 +486,7 @@ def measure(w, steps: int, warmup: int, graph: bool = False, cpu: bool = False):
                "value": round(R / (ms * 1e-3), 1), "unit": "pair positions/s",
                "tokens_per_s": round(S / (ms * 1e-3), 1),
                "config": {"workload": w.name, "batch": w.batch, "lengths": L, "cols": run.cols, "sum_n": S,
-                          "pair_cells": R, "c": w.c_s, "c_p": w.c_z, "hidden": w.hidden,
+                          "pair_cells": R, "s_axis": w.s_axis, "c": w.c_s, "c_p": w.c_z, "hidden": w.hidden,
                           "step": "forward, joint diagnostic loss, backward of every parameter and input"}}
     elif tokens:
         out = {"metric": "packed tokens/sec per encoder layer (1 MI355X)", "value": round(S / (ms * 1e-3), 1),
@@ -503,7 +508,7 @@ def measure(w, steps: int, warmup: int, graph: bool = False, cpu: bool = False):
 
 NESTED = ("pair_b8_n208_224_bf16", "pair_b8_n32_512_bf16", "pairformer4_gated_b16_lognormal192_bf16",
           "tokens_b64_lognormal230_bf16", "mechanism_square_b8_n66_317_bf16",
-          "mechanism_rect_b8_n66_307_m66_309_bf16")
+          "mechanism_rect_b8_n66_307_m66_309_bf16", "mechanism_nonleading_s3_b8_n40_182_bf16")
 
 
 def main():

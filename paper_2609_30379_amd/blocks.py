@@ -391,45 +391,52 @@ class MechanismRun:
         lay = self.layout
         S, Mr, cells = lay.sum_n, lay.sum_m, lay.sum_n2
         Cx, Cp, F = w.c_s, w.c_z, w.hidden
+        # non-leading layout: elements (Sx, N_i, C) pack as (N_i, Sx, C), so
+        # every packed row holds Sx feature vectors; row-wise ops see Sx times
+        # the rows, ragged ops (broadcast, reductions, loss) Sx times the width
+        self.Sx = Sx = w.s_axis
+        self.sep = self.rect or Sx > 1          # u and v from separate projections
         self.params = synth.mechanism_params(w)
         self.W = to_device(self.params, w.dtype, device)
-        if not self.rect:        # one projection computes u and v from the same rows
+        if not self.sep:         # one projection computes u and v from the same rows
             self.W["uv.w"] = torch.cat([self.W["u.w"], self.W["v.w"]], 0).contiguous()
             self.W["uv.b"] = torch.cat([self.W["u.b"], self.W["v.b"]], 0).contiguous()
-        self.x_init = synth.normal(w.seed, "mech.x", (S, Cx), 1.0, w.dtype)
+        self.x_init = synth.normal(w.seed, "mech.x", (S, Sx * Cx), 1.0, w.dtype)
         self.y_init = synth.normal(w.seed, "mech.y", (Mr, Cx), 1.0, w.dtype) if self.rect else None
         self.x = torch.from_numpy(self.x_init).to(device=device, dtype=td)
         self.y = torch.from_numpy(self.y_init).to(device=device, dtype=td) if self.rect else None
         Bn = lay.batch
         self.alpha = torch.tensor([1.0 + i / Bn for i in range(Bn)], dtype=torch.float32, device=device)
         self.beta = torch.tensor([1.5 - i / (2.0 * Bn) for i in range(Bn)], dtype=torch.float32, device=device)
-        self.scale_s = 1.0 / (Cx * S)
-        self.scale_p = 1.0 / (Cp * cells)
+        self.scale_s = 1.0 / (Sx * Cx * S)
+        self.scale_p = 1.0 / (Sx * Cp * cells)
         e = lambda *shape, dt=td: torch.empty(shape, dtype=dt, device=device)   # noqa: E731
         f32 = torch.float32
-        self.uv = e(S, 2 * Cp) if not self.rect else None
-        self.u, self.v = (self.uv[:, :Cp], self.uv[:, Cp:]) if not self.rect else (e(S, Cp), e(Mr, Cp))
-        self.P, self.Pt = e(cells, Cp), e(cells, Cp)
-        self.m = e(S, Cp, dt=f32)
-        self.xt = e(S, Cx)
+        self.uv = e(S, 2 * Cp) if not self.sep else None
+        self.u, self.v = (self.uv[:, :Cp], self.uv[:, Cp:]) if not self.sep else (e(S, Sx * Cp), e(Mr, Sx * Cp))
+        self.P, self.Pt = e(cells, Sx * Cp), e(cells, Sx * Cp)
+        self.m = e(S, Sx * Cp, dt=f32)
+        self.xt = e(S, Sx * Cx)
         self.loss_s, self.loss_p, self.loss_tmp = e(Bn, dt=f32), e(Bn, dt=f32), e(Bn, dt=f32)
-        self.dxt = e(S, Cx)
-        self.dx = e(S, Cx, dt=f32)
+        self.dxt = e(S, Sx * Cx)
+        self.dx = e(S, Sx * Cx, dt=f32)
         self.dy = e(Mr, Cx, dt=f32) if self.rect else None
-        self.dpt, self.dP = e(cells, Cp), e(cells, Cp)
-        self.dm = e(S, Cp, dt=f32)
-        self.duv = e(S, 2 * Cp) if not self.rect else None
-        self.du, self.dv = (self.duv[:, :Cp], self.duv[:, Cp:]) if not self.rect else (e(S, Cp), e(Mr, Cp))
+        self.dpt, self.dP = e(cells, Sx * Cp), e(cells, Sx * Cp)
+        self.dm = e(S, Sx * Cp, dt=f32)
+        self.duv = e(S, 2 * Cp) if not self.sep else None
+        self.du, self.dv = (self.duv[:, :Cp], self.duv[:, Cp:]) if not self.sep else (e(S, Sx * Cp), e(Mr, Sx * Cp))
         self.grads = {k: torch.empty(v.shape, dtype=f32, device=device) for k, v in self.W.items()
                       if k not in ("uv.w", "uv.b")}
-        if not self.rect:
+        if not self.sep:
             self.grads["uv.w"] = torch.empty((2 * Cp, Cx), dtype=f32, device=device)
             self.grads["uv.b"] = torch.empty((2 * Cp,), dtype=f32, device=device)
         # op scratch, used one op at a time on one stream
-        need = [B.layernorm_linear_workspace_bytes(cells, Cp, Cp, w.dtype, epilogue="swiglu_residual", hidden=F),
+        need = [B.layernorm_linear_workspace_bytes(Sx * cells, Cp, Cp, w.dtype, epilogue="swiglu_residual",
+                                                   hidden=F),
                 B.loss_workspace_bytes(lay)]
-        need += [self._bwd_ws(cells, Cp, Cp, True, "swiglu_residual", F), self._bwd_ws(S, Cp, Cx, False, "residual", 0),
-                 self._bwd_ws(S, Cx, Cp if self.rect else 2 * Cp, False, "none", 0)]
+        need += [self._bwd_ws(Sx * cells, Cp, Cp, True, "swiglu_residual", F),
+                 self._bwd_ws(Sx * S, Cp, Cx, False, "residual", 0),
+                 self._bwd_ws(Sx * S, Cx, Cp if self.sep else 2 * Cp, False, "none", 0)]
         if self.rect:
             need.append(self._bwd_ws(Mr, Cx, Cp, False, "none", 0))
         self.scratch = B.workspace_tensor(max(need), device)
@@ -450,25 +457,32 @@ class MechanismRun:
     def step(self):
         """Forward, loss and backward; returns (loss terms, xt, pt, grads)."""
         lay, W, G, ws = self.layout, self.W, self.grads, self.scratch
-        Cp, F = self.w.c_z, self.w.hidden
+        Cx, Cp, F, Sx = self.w.c_s, self.w.c_z, self.w.hidden, self.Sx
+        # row views of the non-leading layout ([rows, Sx * C] as [rows * Sx, C]);
+        # the identity for Sx = 1 (row-wise calls then also check the layout)
+        rv = (lambda t: t.view(-1, t.shape[1] // Sx)) if Sx > 1 else (lambda t: t)   # noqa: E731
+        rl = dict(layout=lay) if Sx == 1 else {}
         # forward
         with _op("mech_proj"):
             if self.rect:
                 B.nt_layernorm_linear(self.x, W["u.w"], W["u.b"], self.u, layout=lay, level="singles")
                 B.nt_layernorm_linear(self.y, W["v.w"], W["v.b"], self.v)
+            elif self.sep:
+                B.nt_layernorm_linear(rv(self.x), W["u.w"], W["u.b"], rv(self.u))
+                B.nt_layernorm_linear(rv(self.x), W["v.w"], W["v.b"], rv(self.v))
             else:
                 B.nt_layernorm_linear(self.x, W["uv.w"], W["uv.b"], self.uv, layout=lay, level="singles")
         with _op("mech_broadcast"):
             B.nt_pair_broadcast(lay, self.u, self.v, self.P)
         with _op("mech_transition"):
-            B.nt_layernorm_linear(self.P, W["trans.w"], W["trans.b"], self.Pt, ln=(W["trans.ln_g"], W["trans.ln_b"]),
-                                  epilogue="swiglu_residual", w2=W["trans.w2"], bias2=W["trans.b2"], hidden=F,
-                                  residual=self.P, layout=lay, level="pairs", workspace=ws)
+            B.nt_layernorm_linear(rv(self.P), W["trans.w"], W["trans.b"], rv(self.Pt),
+                                  ln=(W["trans.ln_g"], W["trans.ln_b"]), epilogue="swiglu_residual", w2=W["trans.w2"],
+                                  bias2=W["trans.b2"], hidden=F, residual=rv(self.P), level="pairs", workspace=ws, **rl)
         with _op("mech_column_mean"):
             B.nt_segment_reduce(lay, "pairs", "mean", self.Pt, self.m)
         with _op("mech_single_update"):
-            B.nt_layernorm_linear(self.m, W["g.w"], W["g.b"], self.xt, epilogue="residual", residual=self.x,
-                                  layout=lay, level="singles")
+            B.nt_layernorm_linear(rv(self.m), W["g.w"], W["g.b"], rv(self.xt), epilogue="residual",
+                                  residual=rv(self.x), level="singles", **rl)
         # loss (Eq. joint-diagnostic-loss) and its gradient
         with _op("mech_loss"):
             B.nt_weighted_square_loss(lay, "singles", self.xt, self.alpha, self.scale_s, self.loss_s, dx=self.dxt,
@@ -479,14 +493,14 @@ class MechanismRun:
                                       workspace=ws)
         # backward
         with _op("mech_single_update_bwd"):
-            B.nt_layernorm_linear_backward(self.m, W["g.w"], self.dxt, epilogue="residual", dx=self.dm, dw=G["g.w"],
-                                           db=G["g.b"], overwrite_weights=True, workspace=ws)
+            B.nt_layernorm_linear_backward(rv(self.m), W["g.w"], rv(self.dxt), epilogue="residual", dx=rv(self.dm),
+                                           dw=G["g.w"], db=G["g.b"], overwrite_weights=True, workspace=ws)
         with _op("mech_column_mean_bwd"):
             B.nt_segment_reduce_backward(lay, "pairs", "mean", self.dm, self.dpt, accumulate=True)
         with _op("mech_transition_bwd"):
-            B.nt_layernorm_linear_backward(self.P, W["trans.w"], self.dpt, ln=(W["trans.ln_g"], W["trans.ln_b"]),
+            B.nt_layernorm_linear_backward(rv(self.P), W["trans.w"], rv(self.dpt), ln=(W["trans.ln_g"], W["trans.ln_b"]),
                                            bias=W["trans.b"], epilogue="swiglu_residual", w2=W["trans.w2"], hidden=F,
-                                           dx=self.dP, dw=G["trans.w"], db=G["trans.b"], dgamma=G["trans.ln_g"],
+                                           dx=rv(self.dP), dw=G["trans.w"], db=G["trans.b"], dgamma=G["trans.ln_g"],
                                            dbeta=G["trans.ln_b"], dw2=G["trans.w2"], db2=G["trans.b2"],
                                            overwrite_weights=True, workspace=ws)
         with _op("mech_broadcast_bwd"):
@@ -497,6 +511,11 @@ class MechanismRun:
                                                db=G["u.b"], overwrite_weights=True, workspace=ws)
                 B.nt_layernorm_linear_backward(self.y, W["v.w"], self.dv, dx=self.dy, dw=G["v.w"], db=G["v.b"],
                                                overwrite_weights=True, workspace=ws)
+            elif self.sep:
+                B.nt_layernorm_linear_backward(rv(self.x), W["u.w"], rv(self.du), dx=rv(self.dx), accumulate_dx=True,
+                                               dw=G["u.w"], db=G["u.b"], overwrite_weights=True, workspace=ws)
+                B.nt_layernorm_linear_backward(rv(self.x), W["v.w"], rv(self.dv), dx=rv(self.dx), accumulate_dx=True,
+                                               dw=G["v.w"], db=G["v.b"], overwrite_weights=True, workspace=ws)
             else:
                 B.nt_layernorm_linear_backward(self.x, W["uv.w"], self.duv, dx=self.dx, accumulate_dx=True,
                                                dw=G["uv.w"], db=G["uv.b"], overwrite_weights=True, workspace=ws)

@@ -47,6 +47,7 @@ class Workload:
     steps: tuple = ()          # ordered steps of one block (pair workloads)
     s_scale: float = 1.0       # std of the initial single track
     col_dist: tuple = ()       # rectangular pairs: distribution of the column lengths M_i
+    s_axis: int = 1            # non-leading layout: static axis S of elements (S, N_i, C), packed (N_i, S, C)
 
 
 def _pair_gains(n_max: int, blocks: int = 1) -> dict:
@@ -116,6 +117,10 @@ WORKLOADS = {
                  c_s=384, c_z=128, hidden=512, gains=mechanism_gains()),
         Workload("mechanism_rect_b8_n66_307_m66_309_bf16", "mechanism", 8, ("uniform", 66, 307), 3, "bf16",
                  c_s=384, c_z=128, hidden=512, gains=mechanism_gains(), col_dist=("uniform", 66, 309)),
+        # the non-leading layout of the same program: elements (S=3, N_i, C),
+        # lengths 40..182 (Table "regimes")
+        Workload("mechanism_nonleading_s3_b8_n40_182_bf16", "mechanism", 8, ("uniform", 40, 182), 4, "bf16",
+                 c_s=384, c_z=128, hidden=512, gains=mechanism_gains(), s_axis=3),
         Workload("tokens_b64_lognormal230_bf16", "tokens", 64,
                  ("lognormal", 230.0, 0.5, 16, 512), 0, "bf16",
                  c_s=768, heads=12, head_dim=64, hidden=3072,
