@@ -72,25 +72,44 @@ def ulp_bf16(x) -> np.ndarray:
     return np.ldexp(1.0, np.floor(np.log2(a)).astype(np.int64) - 7)
 
 
-# A chain of bf16-stored steps can round one intermediate differently on the
-# two sides (the fp32 and float64 values straddle a rounding boundary); the
-# one-ulp difference then travels down the residual stream and meets the
-# final rounding.  Chained comparisons therefore allow two bf16 ulps of the
-# value where that exceeds the per-kernel bar; each kernel on its own stored
-# inputs is held to the bar itself.
-CHAIN_ULPS = 2.0
+# Chained comparisons (several bf16-stored steps run from the same input on
+# both sides).  Every stored update rounds on both sides, the GPU from its
+# fp32 value and the oracle from the exact one; where the two straddle a
+# rounding boundary the stored values land one ulp apart, and the residual
+# stream carries that ulp into every later step.  After R stored updates of
+# a tensor the two can therefore differ by R ulps without any step being
+# wrong (each step on its own stored inputs is held to the 2e-2 bar by the
+# per-kernel checks).  A gated triangle update counts twice: its LayerNorm
+# over t turns a one-ulp flip of t into up to one more ulp of the update.
+# Flips are rare events (the fp32 and exact values must straddle a boundary),
+# so besides the R-ulp bound at most CHAIN_FRACTION of the elements may
+# differ by more than one ulp (or 2e-2): a mistake that shifts many elements
+# by a little fails that even where it stays inside the bound.
+CHAIN_FRACTION = 1e-4
 
 
-# The gated triangle update normalises its contraction t before the output
-# projection, so a one-ulp rounding difference of t moves the update by
-# ulp(t) / std(t) of a unit-variance value: chains through it flip further.
-CHAIN_ULPS_GATED = 4.0
+def chain_updates(steps, blocks: int = 1) -> int:
+    """Stored updates of the pair state along `blocks` blocks of `steps`
+    (every step but the single update writes z; "lin" only in the first
+    block)."""
+    total = 0
+    for b in range(blocks):
+        for t in steps:
+            if t == "single" or (t == "lin" and b > 0):
+                continue
+            total += 2 if t in ("tri_out_g", "tri_in_g") else 1
+    return total
 
 
-def check_chained(got: np.ndarray, ref: np.ndarray, what: str = "", ulps: float = CHAIN_ULPS):
-    """Chained bf16 comparison: every element within 2e-2, or within `ulps`
-    bf16 ulps (two by default) of the larger of the two values where that is
-    wider."""
+# the single state: the stored column mean entering the single update, and
+# the update itself, per block
+SINGLE_UPDATES = 2
+
+
+def check_chained(got: np.ndarray, ref: np.ndarray, what: str = "", updates: int = 2):
+    """Chained bf16 comparison after `updates` stored updates: every element
+    within max(2e-2, updates ulps of the larger of the two values), and at
+    most CHAIN_FRACTION of them beyond max(2e-2, one ulp)."""
     got = np.asarray(got, np.float64)
     ref = np.asarray(ref, np.float64)
     assert got.shape == ref.shape, (what, got.shape, ref.shape)
@@ -98,14 +117,18 @@ def check_chained(got: np.ndarray, ref: np.ndarray, what: str = "", ulps: float 
     if got.size == 0:
         return 0.0
     d = np.abs(got - ref)
-    bound = np.maximum(BF16_MAX_ABS, ulps * ulp_bf16(np.maximum(np.abs(got), np.abs(ref))))
+    ulp = ulp_bf16(np.maximum(np.abs(got), np.abs(ref)))
+    bound = np.maximum(BF16_MAX_ABS, updates * ulp)
     err = float(np.max(d))
     ratio = float(np.max(d / bound))
+    frac = float(np.mean(d > np.maximum(BF16_MAX_ABS, ulp)))
     amax = float(np.max(np.abs(ref)))
-    PARITY_LOG.append((what + f" [chained; {ratio:.2f} of max(2e-2, {ulps:g} ulp)]", err, BF16_MAX_ABS, amax))
+    PARITY_LOG.append((what + f" [chained; {ratio:.2f} of max(2e-2, {updates} ulp); beyond 1 ulp {frac:.1e}]",
+                       err, BF16_MAX_ABS, amax))
     worst = int(np.argmax(d / bound))
     assert ratio <= 1.0, (f"{what}: chained error {d.flat[worst]:.4g} at |ref| {abs(ref.flat[worst]):.3g} "
-                          f"exceeds max(2e-2, {ulps:g} ulp)")
+                          f"exceeds max(2e-2, {updates} ulp)")
+    assert frac <= CHAIN_FRACTION, f"{what}: {frac:.2e} of the elements are more than one ulp (and 2e-2) off"
     assert amax < BF16_MAX_MAGNITUDE, f"{what}: reference magnitude {amax:.3g} beyond the bf16 range of the bar"
     return err
 

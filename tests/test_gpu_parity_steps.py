@@ -23,7 +23,7 @@ import pytest
 from oracle import blocks as OB
 from oracle.numerics import store
 from paper_2609_30379_amd import synth
-from tests.gpu_util import (CHAIN_ULPS, CHAIN_ULPS_GATED, PARITY_LOG, check, check_chained, ulp_bf16,
+from tests.gpu_util import (SINGLE_UPDATES, PARITY_LOG, chain_updates, check, check_chained, ulp_bf16,
                              tiled_offsets, _tiled_plane_index)
 
 pytestmark = pytest.mark.gpu
@@ -179,9 +179,8 @@ class SampleTap:
         s_ref, z_ref, _ = OB.pair_block(s_in, [self.n], self.run.params[block], self.dims, steps, z=z_in,
                                         dtype=w.dtype, round_last=False)
         what = f"{w.name} sample {self.i} N={self.n} block {block} (from the GPU's block input)"
-        ulps = CHAIN_ULPS_GATED if any(t.endswith("_g") for t in steps) else CHAIN_ULPS
-        check_chained(self.z, z_ref, what + " z", ulps=ulps)
-        check_chained(self.s, s_ref, what + " s", ulps=ulps)
+        check_chained(self.z, z_ref, what + " z", updates=chain_updates(steps))
+        check_chained(self.s, s_ref, what + " s", updates=SINGLE_UPDATES)
 
 
 # (workload, sample): each workload's longest sample and a short one; the
