@@ -364,17 +364,30 @@ __device__ __forceinline__ float query_max(float v) {
 //     ones operand, on the same bf16 probabilities as the numerator.
 // Scores are kept transposed (S^T = K Q^T), so a lane holds 16 keys of one
 // query per 64-key chunk and the running max is mostly lane-local.
-// Two instances: N <= 256, persistent, with 16 waves (all queries of a row in
-// one workgroup, so a row's keys and values are copied once per CU; 64 KB of
-// LDS, four waves per SIMD, one workgroup per CU with an equal share of the
-// rows) and N <= 512 from a work list of (sample, query block, group of 16
-// rows) items with 8 waves (128 KB, twice the bias registers, two waves per
-// SIMD).
-template <int NMAX, int NW, bool PERSIST, bool GATE = false>
-__global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_kernel(PairAttnArgs p) {
+// Instances:
+//   * N <= 256, persistent, with 16 waves (all queries of a row in one
+//     workgroup, so a row's keys and values are copied once per CU; 64 KB of
+//     LDS, four waves per SIMD, one workgroup per CU with an equal share of
+//     the rows);
+//   * N <= 512, key split (KS): 16 waves from a work list of (sample, query
+//     block, group of 16 rows) items.  A sample longer than 256 splits its
+//     keys between wave pairs: waves w and w + 8 hold the same 16 queries,
+//     one the keys below 256 and the other the rest, each with the bias
+//     registers of 16 key tiles (as the N <= 256 instance), and the second
+//     hands its running maximum and accumulators to the first through LDS,
+//     which merges them (rescaled to the larger maximum) and stores the row;
+//     a block then holds 8 query tiles.  Shorter samples use all 16 waves as
+//     query tiles.  128 KB of key/value buffers and 26 KB for the hand-over
+//     keep one workgroup per CU at four waves per SIMD;
+//   * N <= 512, 8 waves, each wave all keys (the single attention of axis 3,
+//     one row per sample).
+template <int NMAX, int NW, bool PERSIST, bool GATE = false, bool KS = false>
+__global__ void __launch_bounds__(64 * NW, (NMAX <= 256 || KS) ? 4 : 2) attention_pair_kernel(PairAttnArgs p) {
   constexpr int D = 32;
   constexpr int KT16 = NMAX / 16;               // key tiles
+  constexpr int BT = KS ? 16 : KT16;            // key tiles of bias kept per lane
   static_assert(!PERSIST || NW * 16 >= NMAX, "the persistent instance covers all queries of a row");
+  static_assert(!KS || (NMAX == 512 && NW == 16 && !PERSIST), "the key-split instance: 16 waves, N <= 512");
   extern __shared__ __attribute__((aligned(16))) bf16 lds[];
   bf16* Kb0 = lds;                                         // key images: tile of 16 keys -> 512 elements
   bf16* Kb1 = Kb0 + NMAX * D;
@@ -397,6 +410,7 @@ __global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_k
   //     XCD together.
   int h, i, qt0, nqt_w = 0;
   int64_t row, row_end;
+  bool split = false;                           // key split between wave pairs (KS, N > 256)
   if constexpr (PERSIST) {
     const int x = blockIdx.x % kXcds, k = blockIdx.x / kXcds, per = (int)(gridDim.x / kXcds);
     h = k % p.H;
@@ -426,9 +440,13 @@ __global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_k
     row = p.cu_seqlens[i] + r0;
     row_end = p.axis == 3 ? row + 1 : p.cu_seqlens[i] + min(nn, r0 + kAttnRG);   // axis 3: one row per sample
     nqt_w = w4.w;
+    if constexpr (KS) split = nn > 256;
   }
+  // query slot and key half of this wave (key split: waves w, w + 8 share slot w % 8)
+  const int qs = __builtin_amdgcn_readfirstlane(KS && split ? wave & 7 : wave);
+  const int kh = __builtin_amdgcn_readfirstlane(KS && split ? wave >> 3 : 0);
   const int j0 = qt0 * 16;
-  const int jw = j0 + 16 * wave + l16;          // this lane's query
+  const int jw = j0 + 16 * qs + l16;            // this lane's query
 
   // ---- per-row staging: straight global -> LDS copies ---------------------
   // Each wave copies its key tiles (wave, wave + NW, ...; 16 keys each) with
@@ -473,20 +491,23 @@ __global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_k
   bool wave_has_queries = false, qvalid = false;
   // lane's bias: query 16*wave + l16, keys 16*kt + 4g .. +3 of every key
   // tile, read from the bias image (one contiguous 512 bytes per wave and tile)
-  uint2 bias_r[KT16];
+  uint2 bias_r[BT];
   auto set_sample = [&](int si, int sn, int64_t scu) {
     n = sn;
     cu = scu;
     sr = p.axis == 0 ? n : (p.axis == 1 ? 1 : 0);
     st = p.axis == 1 ? n : 1;
-    wave_has_queries = wave < (PERSIST ? (n + 15) / 16 : nqt_w) && j0 + 16 * wave < n;
+    wave_has_queries = qs < (PERSIST ? (n + 15) / 16 : nqt_w) && j0 + 16 * qs < n;
     qvalid = jw < n;
     const int kti = ((n + 63) & ~63) / 16;
     const uint2* img = p.bias_img && wave_has_queries
-                           ? p.bias_img + h * p.img_head + ((int64_t)p.bias_tiles[si] + (int64_t)(qt0 + wave) * kti) * 64 + lane
+                           ? p.bias_img + h * p.img_head + ((int64_t)p.bias_tiles[si] + (int64_t)(qt0 + qs) * kti) * 64 + lane
                            : nullptr;
 #pragma unroll
-    for (int kt = 0; kt < KT16; ++kt) bias_r[kt] = img && kt < kti ? img[kt * 64] : make_uint2(0u, 0u);
+    for (int kt = 0; kt < BT; ++kt) {
+      const int kk = kh * 16 + kt;              // key tile of this wave's half
+      bias_r[kt] = img && kk < kti ? img[kk * 64] : make_uint2(0u, 0u);
+    }
   };
   // first cell of the sample: pair offset, or for axis 3 its first token
   set_sample(i, __builtin_amdgcn_readfirstlane(p.cu_seqlens[i + 1] - p.cu_seqlens[i]),
@@ -528,7 +549,7 @@ __global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_k
     // clamped into the row, so the load is unconditional
     uint2 gt[2];
     if constexpr (GATE) {
-      if (wave_has_queries) {
+      if (wave_has_queries && kh == 0) {
         const bf16* gr = p.gate + (cu + (int64_t)r * sr + (int64_t)min(jw, n - 1) * st) * p.ld_gate + h * D + 4 * g;
         gt[0] = *reinterpret_cast<const uint2*>(gr);
         gt[1] = *reinterpret_cast<const uint2*>(gr + 16);
@@ -542,27 +563,31 @@ __global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_k
     // keep the bias packed: converting it once outside the row loop would
     // double its registers
 #pragma unroll
-    for (int kt = 0; kt < KT16; ++kt) asm volatile("" : "+v"(bias_r[kt].x), "+v"(bias_r[kt].y));
-    if (wave_has_queries) {
-      float m_s = -INFINITY;                      // running max of bias/scale + q.k
-      f32x4 O[3];                                 // dims 0-15, 16-31, row sum
+    for (int kt = 0; kt < BT; ++kt) asm volatile("" : "+v"(bias_r[kt].x), "+v"(bias_r[kt].y));
+    float m_s = -INFINITY;                        // running max of bias/scale + q.k
+    f32x4 O[3];                                   // dims 0-15, 16-31, row sum
 #pragma unroll
-      for (int u = 0; u < 3; ++u) O[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int u = 0; u < 3; ++u) O[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (wave_has_queries) {
       // Keys in super-chunks of 128 (8 key tiles), the last one cut to the
       // 2, 4 or 6 tiles that hold keys: all score products of a super-chunk
       // are issued together, one maximum per query, then the exponentials
       // and the value products.  Tiles read stay below the staged length.
+      // key tile offset of this wave's half (key split), uniform
+      const int kto = kh * 16;
+      const bf16* Kh = Kb + kto * 512;
+      const bf16* Vh = Vb + kto * 512;
       auto super_chunk = [&](auto sc_c, auto nt_c) {
         constexpr int SC = decltype(sc_c)::value, NT = decltype(nt_c)::value;
-        constexpr int T0 = SC * 8;                // first key tile
-        const int kc = SC * 128;
+        constexpr int T0 = SC * 8;                // first key tile (of this wave's half)
+        const int kc = kto * 16 + SC * 128;
         f32x4 S[NT];
 #pragma unroll
         for (int kt = 0; kt < NT; ++kt) {
           const uint2 bb = bias_r[T0 + kt];
           S[kt] = f32x4{__uint_as_float(bb.x << 16), __uint_as_float(bb.x & 0xffff0000u),
                         __uint_as_float(bb.y << 16), __uint_as_float(bb.y & 0xffff0000u)};
-          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Kb[(T0 + kt) * 512 + lane * 8]);
+          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Kh[(T0 + kt) * 512 + lane * 8]);
           S[kt] = mfma16(kf, qf, S[kt]);
           // at most four key fragments in flight (registers)
           if (kt % 4 == 3) __builtin_amdgcn_sched_barrier(0);
@@ -600,7 +625,7 @@ __global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_k
 #pragma unroll
         for (int pp = 0; pp + 1 < NT / 2; pp += 2) {
           bf16x8 vf[4];
-          v_frags2(Vb, SC * 4 + pp, vf);
+          v_frags2(Vh, SC * 4 + pp, vf);
           O[0] = mfma16(vf[0], P[pp], O[0]);
           O[1] = mfma16(vf[1], P[pp], O[1]);
           O[2] = mfma16(ones, P[pp], O[2]);
@@ -610,7 +635,7 @@ __global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_k
         }
         if constexpr ((NT / 2) % 2 == 1) {
           bf16x8 vf[2];
-          v_frags1(Vb, SC * 4 + NT / 2 - 1, vf);
+          v_frags1(Vh, SC * 4 + NT / 2 - 1, vf);
           O[0] = mfma16(vf[0], P[NT / 2 - 1], O[0]);
           O[1] = mfma16(vf[1], P[NT / 2 - 1], O[1]);
           O[2] = mfma16(ones, P[NT / 2 - 1], O[2]);
@@ -620,7 +645,7 @@ __global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_k
       // staged length, a multiple of 64, then reaches 128 past kc)
       auto run_sc = [&](auto sc_c) {
         constexpr int SC = decltype(sc_c)::value;
-        const int rem = n - SC * 128;
+        const int rem = n - kto * 16 - SC * 128;
         if (rem <= 0) return;
         if (rem > 96) super_chunk(sc_c, std::integral_constant<int, 8>{});
         else if (rem > 64) super_chunk(sc_c, std::integral_constant<int, 6>{});
@@ -629,10 +654,37 @@ __global__ void __launch_bounds__(64 * NW, NMAX <= 256 ? 4 : 2) attention_pair_k
       };
       run_sc(std::integral_constant<int, 0>{});
       run_sc(std::integral_constant<int, 1>{});
-      if constexpr (NMAX > 256) {
+      if constexpr (NMAX > 256 && !KS) {
         run_sc(std::integral_constant<int, 2>{});
         run_sc(std::integral_constant<int, 3>{});
       }
+    }
+    if constexpr (KS) {
+      if (split) {
+        // the upper key half hands (max, accumulators) to its partner, which
+        // merges the two partial softmax sums rescaled to the larger maximum
+        float* xf = reinterpret_cast<float*>(lds + 4 * NMAX * D);   // [13][8 slots][64 lanes]
+        if (kh == 1 && wave_has_queries) {
+          xf[(0 * 8 + qs) * 64 + lane] = m_s;
+#pragma unroll
+          for (int u = 0; u < 3; ++u)
+#pragma unroll
+            for (int ii = 0; ii < 4; ++ii) xf[((1 + 4 * u + ii) * 8 + qs) * 64 + lane] = O[u][ii];
+        }
+        __builtin_amdgcn_s_waitcnt(0xC07F);     // lgkmcnt(0): the hand-over is written (copies stay in flight)
+        __builtin_amdgcn_s_barrier();
+        if (kh == 0 && wave_has_queries) {
+          const float m1 = xf[(0 * 8 + qs) * 64 + lane];
+          const float mm = fmaxf(m_s, m1);
+          const float a0 = __builtin_amdgcn_exp2f((m_s - mm) * c), a1 = __builtin_amdgcn_exp2f((m1 - mm) * c);
+#pragma unroll
+          for (int u = 0; u < 3; ++u)
+#pragma unroll
+            for (int ii = 0; ii < 4; ++ii) O[u][ii] = O[u][ii] * a0 + xf[((1 + 4 * u + ii) * 8 + qs) * 64 + lane] * a1;
+        }
+      }
+    }
+    if (wave_has_queries && kh == 0) {
       if (qvalid) {
         const float inv = 1.f / O[2][0];
         bf16* orow = p.o + (cu + (int64_t)r * sr + (int64_t)jw * st) * p.ld_o + h * D;
@@ -1071,16 +1123,18 @@ hipError_t launch_attention(const nt_layout& L, int axis, int H, int D, const vo
                    img, tiles * 64, L.d_bias_tiles, L.batch, L.sum_n, (const bf16*)gate, ld_gate};
     const size_t smem = sizeof(bf16) * 4 * (size_t)nmax * 32;
     const dim3 grid((unsigned)(L.pattn_items() * H));
+    // the key-split instance also holds the hand-over of the upper key halves
+    const size_t smem_ks = sizeof(bf16) * 4 * (size_t)kAttnLongLen * 32 + sizeof(float) * 13 * 8 * 64;
     if (gate) {
-      // gated output (axes 0 and 1): the GATE instances of the same kernel
+      // gated output (axes 0 and 1): the GATE instances of the same kernels
       if (nmax == kAttnShortLen) {
         const int per_xcd = std::max(H, compute_units() / kXcds / H * H);
         const dim3 gridp((unsigned)(per_xcd * kXcds));
         hipFuncSetAttribute((const void*)attention_pair_kernel<kAttnShortLen, 16, true, true>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
         attention_pair_kernel<kAttnShortLen, 16, true, true><<<gridp, dim3(1024), smem, s>>>(a);
       } else {
-        hipFuncSetAttribute((const void*)attention_pair_kernel<kAttnLongLen, 8, false, true>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-        attention_pair_kernel<kAttnLongLen, 8, false, true><<<grid, dim3(512), smem, s>>>(a);
+        hipFuncSetAttribute((const void*)attention_pair_kernel<kAttnLongLen, 16, false, true, true>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem_ks);
+        attention_pair_kernel<kAttnLongLen, 16, false, true, true><<<grid, dim3(1024), smem_ks, s>>>(a);
       }
     } else if (axis == 3) {
       // single attention with pair bias: one row per sample, the 8-wave
@@ -1099,8 +1153,8 @@ hipError_t launch_attention(const nt_layout& L, int axis, int H, int D, const vo
       hipFuncSetAttribute((const void*)attention_pair_kernel<kAttnShortLen, 16, true>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
       attention_pair_kernel<kAttnShortLen, 16, true><<<gridp, dim3(1024), smem, s>>>(a);
     } else {
-      hipFuncSetAttribute((const void*)attention_pair_kernel<kAttnLongLen, 8, false>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-      attention_pair_kernel<kAttnLongLen, 8, false><<<grid, dim3(512), smem, s>>>(a);
+      hipFuncSetAttribute((const void*)attention_pair_kernel<kAttnLongLen, 16, false, false, true>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem_ks);
+      attention_pair_kernel<kAttnLongLen, 16, false, false, true><<<grid, dim3(1024), smem_ks, s>>>(a);
     }
     return hipGetLastError();
   }

@@ -205,14 +205,16 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L, const
   // ceil(tiles / W) blocks of at most W tiles (items: sample, first tile, row
   // group, tile count), so no block leaves most of its waves idle; generation
   // order is kept in each XCD's queue so the blocks of a row group stay
-  // adjacent and share keys and values.  W = 8, for the N <= 512 instance
-  // (the N <= 256 instance needs no list: its workgroups find their rows
-  // from the prefix sums).
-  auto pair_attn_items = [&](int32_t W) {
+  // adjacent and share keys and values.  For the 16-wave key-split instance
+  // (N <= 512) W is 16 for samples up to 256 long (a wave per query tile) and
+  // 8 for longer ones (a wave pair per query tile); the N <= 256 persistent
+  // instance needs no list (its workgroups find their rows from the prefix
+  // sums).
+  auto pair_attn_items = [&](auto W_of) {
     std::vector<std::array<int32_t, 4>> items;
     std::vector<double> cost;
     for (int32_t i = 0; i < batch; ++i) {
-      const int32_t n = lengths[i], tiles = (n + 15) / 16;
+      const int32_t n = lengths[i], tiles = (n + 15) / 16, W = W_of(n);
       const int32_t blocks = (tiles + W - 1) / W;
       for (int32_t rg = 0; rg * kAttnRG < n; ++rg)
         for (int32_t b = 0; b < blocks; ++b) {
@@ -223,7 +225,7 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L, const
     }
     return xcd_order<4>(items, cost, false);
   };
-  L->pattn_work = pair_attn_items(kAttnQB / 16);
+  L->pattn_work = pair_attn_items([](int32_t n) { return n <= kAttnShortLen ? 16 : 8; });
   // 1-D attention: the same even split of a sample's 16-query tiles over
   // blocks of at most kAttnQB queries, one item per block
   {
