@@ -126,7 +126,8 @@ typedef enum {
   NT_ARR_SEQ_WORK = 7,         /* 1-D attention map (sample, query block) pairs */
   NT_ARR_CU_PAD = 8,           /* P_i offsets of pair-tiled operands, [B+1]     */
   NT_ARR_COLS = 9,             /* M_i, [B] (= N_i for square pairs)             */
-  NT_ARR_CU_COLS = 10          /* column offsets kappa, [B+1]                   */
+  NT_ARR_CU_COLS = 10,         /* column offsets kappa, [B+1]                   */
+  NT_ARR_TRI_SPLIT = 11        /* triangle tile map cut into 8 XCD ranges, [9]  */
 } nt_array;
 
 typedef struct {

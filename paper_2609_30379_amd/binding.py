@@ -23,7 +23,8 @@ LEVELS = {"singles": 0, "pairs": 1, "pairs_first": 2}
 TAILS = {"channel_major": 0, "pair_tiled": 1, "pair_tiled_t": 2}
 TRI_OPERANDS = {"packed": 0, "pair_tiled": 1, "pair_tiled_t": 2}
 ARRAYS = {"lengths": 0, "cu_seqlens": 1, "cu_pairs": 2, "row_splits2": 3, "row_sample": 4,
-          "attn_work": 5, "tri_work": 6, "seq_work": 7, "cu_pad": 8, "cols": 9, "cu_cols": 10}
+          "attn_work": 5, "tri_work": 6, "seq_work": 7, "cu_pad": 8, "cols": 9, "cu_cols": 10,
+          "tri_split": 11}
 NT_LAYOUT_HOST_ONLY = 1
 
 

@@ -60,7 +60,7 @@ nt_status upload(nt_layout* L, hipStream_t s) {
       {&L->pattn_work, &L->d_pattn_work}, {&L->bias_tiles, &L->d_bias_tiles},
       {&L->sattn_work, &L->d_sattn_work},
       {&L->bc_cu_tiles, &L->d_bc_cu_tiles},
-      {&L->cu_qblk, &L->d_cu_qblk},
+      {&L->cu_qblk, &L->d_cu_qblk},       {&L->tri_split, &L->d_tri_split},
       {&L->cu_cols, &L->d_cu_cols},       {&L->col_sample, &L->d_col_sample},
   };
   size_t total = 0;
@@ -191,6 +191,7 @@ nt_status nt_layout_host_array(const nt_layout* L, nt_array which, const int32_t
     case NT_ARR_CU_PAD: v = &L->cu_pad; break;
     case NT_ARR_COLS: v = &L->cols; break;
     case NT_ARR_CU_COLS: v = &L->cu_cols; break;
+    case NT_ARR_TRI_SPLIT: v = &L->tri_split; break;
     default: return nt::fail(NT_ERR_INVALID_ARG, "unknown array id");
   }
   *data = v->data();

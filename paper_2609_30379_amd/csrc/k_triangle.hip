@@ -38,20 +38,23 @@ struct TriArgs {
   const int32_t* cu_pad;
   int items, groups;     // tiles, and line groups of four channel blocks
   int accumulate;        // 1: z += t;  0: z = t (z is not read)
+  const int32_t* split;  // [9] item ranges of the XCDs
 };
 
 __global__ void __launch_bounds__(kTriThreads, 1) triangle_mfma_kernel(TriArgs p) {
   __shared__ __attribute__((aligned(16))) float stage[16 * kTriRS * kTriSC];
   __shared__ __attribute__((aligned(16))) bf16 zbuf[2][16 * kTriTile * kTriCB];   // z of two bands, [row][col][16]
-  // Workgroup id runs on XCD id % 8, which takes the contiguous range
-  // [x W / 8, (x + 1) W / 8) of the sequence u = 4 v + j, where v runs over
-  // (sample, line group, tile) with the sample's tiles innermost and j is the
-  // channel block inside the line group.  The 32 workgroups an XCD holds at
-  // once then cover 8 tiles x 4 channel blocks of one sample and line group:
-  // an operand row block is fetched into that L2 for all tiles that use it,
-  // and each z line by the four blocks that share it.
-  const int id = blockIdx.x;
-  const int u = (id % kXcds) * (int)(gridDim.x / kXcds) + id / kXcds;
+  // Workgroup id runs on XCD x = id % 8, which takes the contiguous range
+  // [4 G split[x], 4 G split[x + 1]) of the sequence u = 4 v + j, where v runs
+  // over (sample, line group, tile) with the sample's tiles innermost, j is
+  // the channel block inside the line group and G the line groups; the item
+  // cuts split[] balance the k-steps over the XCDs.  The 32 workgroups an XCD
+  // holds at once then cover 8 tiles x 4 channel blocks of one sample and
+  // line group: an operand row block is fetched into that L2 for all tiles
+  // that use it, and each z line by the four blocks that share it.
+  const int id = blockIdx.x, xcd = id % kXcds;
+  const int u = 4 * p.groups * p.split[xcd] + id / kXcds;
+  if (u >= 4 * p.groups * p.split[xcd + 1]) return;
   const int v = u >> 2;
   const int e = v / p.groups;                         // an item of the same sample
   if (e >= p.items) return;
@@ -326,9 +329,10 @@ hipError_t contract(const nt_layout& L, int C, const void* a, const void* b, int
   }
   const int nblk = C / kTriCB, groups = (nblk + 3) / 4;
   TriArgs t{C, nblk, (const bf16*)a, (const bf16*)b, ld_ab, (bf16*)z, ld_z, L.d_tri_work, L.d_cu_seqlens,
-            L.d_cu_pairs, L.d_cu_pad, (int)items, groups, accumulate};
-  // items is a multiple of 8, so the grid splits evenly over the XCDs
-  triangle_mfma_kernel<<<dim3((unsigned)(items * groups * 4)), dim3(kTriThreads), 0, s>>>(t);
+            L.d_cu_pairs, L.d_cu_pad, (int)items, groups, accumulate, L.d_tri_split};
+  // every XCD gets as many workgroups as the widest of the item ranges needs
+  triangle_mfma_kernel<<<dim3((unsigned)((int64_t)L.tri_xcd_items * groups * 4 * kXcds)), dim3(kTriThreads), 0,
+                         s>>>(t);
   return hipGetLastError();
 }
 

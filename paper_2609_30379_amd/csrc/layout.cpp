@@ -254,8 +254,8 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L, const
   // triangle: one item per (sample, 64x64 output tile), largest samples first,
   // a sample's tiles contiguous and each carrying the index of the sample's
   // first item (the launch walks (sample, channel line group, tile) in this
-  // order, one contiguous stretch per XCD); the list is padded to a multiple
-  // of 8 with idle items.
+  // order, one cost-balanced stretch per XCD); the list is padded to a
+  // multiple of 8 with idle items.
   {
     std::vector<int32_t> order(batch);
     std::iota(order.begin(), order.end(), 0);
@@ -273,6 +273,30 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L, const
         }
     }
     while ((L->tri_work.size() / 4) % kXcds) L->tri_work.insert(L->tri_work.end(), {-1, -1, -1, -1});
+    // XCD x takes the items [tri_split[x], tri_split[x + 1]) (times the channel
+    // line groups of a call).  A tile costs its sample's 32-wide k-steps plus
+    // about two for reading and writing its z block; the cuts balance that
+    // cost, since equal item counts would leave the XCD with the largest
+    // samples doing most of the work.
+    const int64_t nitems = (int64_t)L->tri_work.size() / 4;
+    std::vector<double> pre(nitems + 1, 0.0);
+    for (int64_t e = 0; e < nitems; ++e) {
+      const int32_t i = L->tri_work[4 * e];
+      pre[e + 1] = pre[e] + (i < 0 ? 0.0 : (double)((lengths[i] + 31) / 32 + 2));
+    }
+    L->tri_split.assign(kXcds + 1, 0);
+    int64_t e = 0;
+    for (int x = 1; x < kXcds; ++x) {
+      const double target = pre[nitems] * x / kXcds;
+      while (e < nitems && pre[e + 1] <= target) ++e;
+      // the cut nearest the target
+      if (e < nitems && target - pre[e] > pre[e + 1] - target) ++e;
+      L->tri_split[x] = (int32_t)e;
+    }
+    L->tri_split[kXcds] = (int32_t)nitems;
+    int32_t widest = 0;
+    for (int x = 0; x < kXcds; ++x) widest = std::max(widest, L->tri_split[x + 1] - L->tri_split[x]);
+    L->tri_xcd_items = widest;
   }
   // 1-D attention: one item per (sample, block of kSeqQBlock queries), cost = queries * N_i
   {

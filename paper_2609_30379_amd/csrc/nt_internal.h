@@ -50,7 +50,9 @@ struct nt_layout {
   std::vector<int32_t> row_splits2;  // [sum N + 1]
   std::vector<int32_t> row_sample;   // [sum N]
   std::vector<int32_t> attn_work;    // pairs (sample, row); count multiple of 8; (-1,-1) = idle
-  std::vector<int32_t> tri_work;     // quads (sample, xt, yt, 0); count multiple of 8
+  std::vector<int32_t> tri_work;     // quads (sample, xt, yt, first item of the sample); count multiple of 8
+  std::vector<int32_t> tri_split;    // [9] cost-balanced item ranges of the 8 XCDs
+  int32_t tri_xcd_items = 0;         // largest item count of one XCD
   std::vector<int32_t> seq_work;     // pairs (sample, query block); count multiple of 8
   std::vector<int32_t> pattn_work;  // quads (sample, first 16-query tile, row group, tile count)
   std::vector<int32_t> bias_tiles;   // [B+1] prefix of ceil(N_i/16) * round_up(N_i,64)/16: bias image tiles
@@ -77,6 +79,7 @@ struct nt_layout {
   const int32_t* d_sattn_work = nullptr;
   const int32_t* d_bc_cu_tiles = nullptr;
   const int32_t* d_cu_qblk = nullptr;
+  const int32_t* d_tri_split = nullptr;
   const int32_t* d_cu_cols = nullptr;
   const int32_t* d_col_sample = nullptr;
 

@@ -81,6 +81,14 @@ def test_work_maps_cover_each_item_once(L):
     # balanced XCD loads: no XCD above the mean by more than one sample's largest item
     loads = _xcd_loads(att.tolist(), lambda it: L[it[0]] ** 2)
     assert loads.max() - loads.mean() <= max(L) ** 2 + 1e-9
+    # the triangle tile map is cut into 8 contiguous XCD ranges whose costs
+    # (32-wide k-steps + 2 per tile) are within one tile of the mean
+    split = lay.host_array("tri_split")
+    assert len(split) == 9 and split[0] == 0 and split[-1] == len(tri) and np.all(np.diff(split) >= 0)
+    cost = np.array([0 if i < 0 else -(-L[i] // 32) + 2 for i in tri[:, 0].tolist()], float)
+    pre = np.concatenate([[0.0], np.cumsum(cost)])
+    per = np.diff(pre[split])
+    assert np.all(np.abs(per - pre[-1] / 8) <= cost.max() + 1e-9)
 
 
 def test_uniform_batch_puts_each_sample_on_its_own_xcd():
