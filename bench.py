@@ -48,18 +48,18 @@ F32_PEAK_TFLOPS = 157.3        # fp32 vector
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 COUNTERS = {  # workload: {op: (kernel source, source hash, FETCH_SIZE KiB, WRITE_SIZE KiB)}
     "pairformer4_b16_lognormal192_bf16": {
-        "attention_row": ("k_attention.hip", "1c8befb2fe5cd30a", 337377 + 8060, 174369 + 6472),
-        "attention_col": ("k_attention.hip", "1c8befb2fe5cd30a", 337377 + 8060, 174369 + 6472),
-        "triangle_out": ("k_triangle.hip", "d6c9a1770a0bb33e", 686568, 177255),
-        "triangle_in": ("k_triangle.hip", "d6c9a1770a0bb33e", 686568, 177255),
-        "transition": ("k_transition.hip", "e2f701d5925d7f6e", 100348 + 268, 174431 + 384),
-        "attn_proj": ("k_linear.hip", "ab0523789d210285", 87689, 528956),
-        "tri_proj": ("k_linear.hip", "ab0523789d210285", 87863, 386304),
-        "attn_out_residual": ("k_linear.hip", "ab0523789d210285", 174594, 174373),
-        "pair_broadcast": ("k_segment.hip", "c95eabc6d4c62896", 68901, 174369),
-        "segment_mean": ("k_segment.hip", "c95eabc6d4c62896", 87296, 1492),
-        "single_proj": ("k_linear.hip", "ab0523789d210285", 5276, 1492),
-        "single_update": ("k_linear.hip", "ab0523789d210285", 6018, 2237),
+        "attention_row": ("k_attention.hip", "fb1580cc3df1ec1d", 324779 + 8058, 216030 + 6472),
+        "attention_col": ("k_attention.hip", "fb1580cc3df1ec1d", 324779 + 8058, 216030 + 6472),
+        "triangle_out": ("k_triangle.hip", "78ed89d0163e3191", 696154, 177229),
+        "triangle_in": ("k_triangle.hip", "78ed89d0163e3191", 696154, 177229),
+        "transition": ("k_transition.hip", "e2f701d5925d7f6e", 100338 + 268, 174430 + 384),
+        "attn_proj": ("k_linear.hip", "4daf048772e304da", 87689, 528972),
+        "tri_proj": ("k_linear.hip", "4daf048772e304da", 87863, 386304),
+        "attn_out_residual": ("k_linear.hip", "4daf048772e304da", 174596, 174371),
+        "pair_broadcast": ("k_segment.hip", "8d348b78ad1740b0", 68898, 174369),
+        "segment_mean": ("k_segment.hip", "8d348b78ad1740b0", 87298, 1492),
+        "single_proj": ("k_linear.hip", "4daf048772e304da", 5281, 1492),
+        "single_update": ("k_linear.hip", "4daf048772e304da", 6024, 2237),
     },
     "pair_b8_n208_224_bf16": {
         "transition": ("k_transition.hip", "e2f701d5925d7f6e", 53091, 91003),
@@ -458,7 +458,7 @@ def measure(w, steps: int, warmup: int, graph: bool = False, cpu: bool = False):
         run.step()
     torch.cuda.synchronize()
     blocks.timer = None
-    per_op = tm.summary()                            # {op: (launches, mean us)}
+    per_op = tm.summary()                            # {op: (launches, median us per launch)}
 
     costs = token_op_costs(w, L) if tokens else (mechanism_op_costs(w, L, run.cols) if mech else op_costs(w, L))
     total_us = {k: n * us / steps for k, (n, us) in per_op.items()}

@@ -38,13 +38,15 @@ class OpTimer:
         return _OpSpan(self, name)
 
     def summary(self):
-        """{op: (launches, mean microseconds)} after a device synchronisation."""
+        """{op: (launches, median microseconds per launch)} after a device
+        synchronisation.  An event span also holds any time the device waits
+        for the host to issue the op's launches; the median over launches
+        keeps an occasional host stall out of the op's figure."""
         torch.cuda.synchronize()
         acc = {}
         for name, a, b in self.events:
-            n, t = acc.get(name, (0, 0.0))
-            acc[name] = (n + 1, t + a.elapsed_time(b) * 1e3)
-        return {k: (n, t / n) for k, (n, t) in acc.items()}
+            acc.setdefault(name, []).append(a.elapsed_time(b) * 1e3)
+        return {k: (len(v), float(np.median(v))) for k, v in acc.items()}
 
 
 class _OpSpan:
