@@ -295,6 +295,22 @@ __device__ __forceinline__ VtLane vt_lane(int l16, int g) {
 __device__ __forceinline__ uint32_t lds_addr(const bf16* ptr) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) bf16*)ptr;
 }
+// bf16 ones as an MFMA operand, materialised where it is used: kept live
+// across the row loop it is one of the first values the register allocator
+// spills, and its reload waits for every copy in flight.
+__device__ __forceinline__ bf16x8 ones_bf16x8() {
+  uint32_t w;
+  asm volatile("v_mov_b32 %0, 0x3f803f80" : "=v"(w));
+  const uint32_t q[4] = {w, w, w, w};
+  return __builtin_bit_cast(bf16x8, q);
+}
+// an opaque copy of a lane-dependent value: what is derived from it is
+// recomputed at each use instead of being hoisted out of the row loop and
+// kept live (or spilled) across it
+__device__ __forceinline__ int opaque(int v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
 __device__ __forceinline__ bf16x8 pack_u2(uint2 lo, uint2 hi) {
   const uint32_t w[4] = {lo.x, lo.y, hi.x, hi.y};
   return __builtin_bit_cast(bf16x8, w);
@@ -372,8 +388,9 @@ __device__ __forceinline__ float query_max(float v) {
 //   * N <= 512, key split (KS): 16 waves from a work list of (sample, query
 //     block, group of 16 rows) items.  A sample longer than 256 splits its
 //     keys between wave pairs: waves w and w + 8 hold the same 16 queries,
-//     one the keys below 256 and the other the rest, each with the bias
-//     registers of 16 key tiles (as the N <= 256 instance), and the second
+//     one the keys below the cut (half the row rounded up to 32 keys) and
+//     the other the rest, each with the bias registers of at most 16 key
+//     tiles (as the N <= 256 instance), and the second
 //     hands its running maximum and accumulators to the first through LDS,
 //     which merges them (rescaled to the larger maximum) and stores the row;
 //     a block then holds 8 query tiles.  Shorter samples use all 16 waves as
@@ -456,20 +473,29 @@ __global__ void __launch_bounds__(64 * NW, (NMAX <= 256 || KS) ? 4 : 2) attentio
   // Every tile below the 64-key padded length is written (the last chunk
   // reads up to there): keys past N repeat key N-1, so the padding holds
   // finite values whose probabilities are masked to zero.
+  // this head's queries, keys, values, outputs (and gates): the head offset
+  // as a scalar, so the bases stay in scalar registers (global pointers)
+  const int hD = __builtin_amdgcn_readfirstlane(h * D);
+  const bf16* kbase = p.k + hD;
+  const bf16* vbase = p.v + hD;
+  const bf16* qbase = p.q + hD;
+  bf16* obase = p.o + hD;
+  const bf16* gbase = GATE ? p.gate + hD : nullptr;
   auto dma_kv = [&](int sn, int64_t scu, int r, bf16* Kb, bf16* Vr) {
     const int snpad = (sn + 63) & ~63;
     const int64_t ssr = p.axis == 0 ? sn : (p.axis == 1 ? 1 : 0), sst = p.axis == 1 ? sn : 1;
+    const int ln = opaque(lane);
 #pragma unroll
     for (int kt = wave; kt < KT16; kt += NW) {
       if (kt * 16 >= snpad) break;
       // values: the 16-byte chunk at column c of key row kv holds dim group
       // c ^ ((kv >> 2) & 3), so the four key groups of a transpose read fall
       // on different banks
-      const int kv = kt * 16 + (lane >> 2);
-      const int key_k = min(kt * 16 + l16, sn - 1), key_v = min(kv, sn - 1);
-      const int dgv = (lane & 3) ^ ((kv >> 2) & 3);
-      const bf16* sk = p.k + (scu + (int64_t)r * ssr + (int64_t)key_k * sst) * p.ld_qkv + h * D + g * 8;
-      const bf16* sv = p.v + (scu + (int64_t)r * ssr + (int64_t)key_v * sst) * p.ld_qkv + h * D + dgv * 8;
+      const int kv = kt * 16 + (ln >> 2);
+      const int key_k = min(kt * 16 + (ln & 15), sn - 1), key_v = min(kv, sn - 1);
+      const int dgv = (ln & 3) ^ ((kv >> 2) & 3);
+      const bf16* sk = kbase + (scu + (int64_t)r * ssr + (int64_t)key_k * sst) * p.ld_qkv + (ln >> 4) * 8;
+      const bf16* sv = vbase + (scu + (int64_t)r * ssr + (int64_t)key_v * sst) * p.ld_qkv + dgv * 8;
       __builtin_amdgcn_global_load_lds((const void*)sk, (__attribute__((address_space(3))) void*)(Kb + kt * 512), 16, 0, 0);
       __builtin_amdgcn_global_load_lds((const void*)sv, (__attribute__((address_space(3))) void*)(Vr + kt * 512), 16, 0, 0);
     }
@@ -479,7 +505,7 @@ __global__ void __launch_bounds__(64 * NW, (NMAX <= 256 || KS) ? 4 : 2) attentio
   auto load_q = [&](int sn, int64_t scu, int r) -> bf16x8 {
     if (jw >= sn) return bf16x8{};
     const int64_t ssr = p.axis == 0 ? sn : (p.axis == 1 ? 1 : 0), sst = p.axis == 1 ? sn : 1;
-    return *reinterpret_cast<const bf16x8*>(p.q + (scu + (int64_t)r * ssr + (int64_t)jw * sst) * p.ld_qkv + h * D + g * 8);
+    return *reinterpret_cast<const bf16x8*>(qbase + (scu + (int64_t)r * ssr + (int64_t)jw * sst) * p.ld_qkv + g * 8);
   };
   const VtLane vl = vt_lane(l16, g);
   auto v_frags1 = [&](const bf16* Vr, int kb, bf16x8 (&f)[2]) { vt_frags1(Vr, kb, vl, f); };
@@ -489,6 +515,10 @@ __global__ void __launch_bounds__(64 * NW, (NMAX <= 256 || KS) ? 4 : 2) attentio
   int n = 0;
   int64_t cu = 0, sr = 0, st = 0;               // cell(r, t) = cu + r*sr + t*st
   bool wave_has_queries = false, qvalid = false;
+  // keys of this wave: [16 kto, kend).  A split row is cut at half its
+  // length rounded up to 32 keys (at most 256 on either side), so both waves
+  // of a pair run about the same number of key tiles.
+  int kto = 0, kend = 0;
   // lane's bias: query 16*wave + l16, keys 16*kt + 4g .. +3 of every key
   // tile, read from the bias image (one contiguous 512 bytes per wave and tile)
   uint2 bias_r[BT];
@@ -499,13 +529,21 @@ __global__ void __launch_bounds__(64 * NW, (NMAX <= 256 || KS) ? 4 : 2) attentio
     st = p.axis == 1 ? n : 1;
     wave_has_queries = qs < (PERSIST ? (n + 15) / 16 : nqt_w) && j0 + 16 * qs < n;
     qvalid = jw < n;
+    if (KS && split) {
+      const int cut = __builtin_amdgcn_readfirstlane(min(n, ((n + 1) / 2 + 31) & ~31));
+      kto = kh ? cut / 16 : 0;
+      kend = kh ? n : cut;
+    } else {
+      kto = 0;
+      kend = n;
+    }
     const int kti = ((n + 63) & ~63) / 16;
     const uint2* img = p.bias_img && wave_has_queries
                            ? p.bias_img + h * p.img_head + ((int64_t)p.bias_tiles[si] + (int64_t)(qt0 + qs) * kti) * 64 + lane
                            : nullptr;
 #pragma unroll
     for (int kt = 0; kt < BT; ++kt) {
-      const int kk = kh * 16 + kt;              // key tile of this wave's half
+      const int kk = kto + kt;                  // key tile of this wave's half
       bias_r[kt] = img && kk < kti ? img[kk * 64] : make_uint2(0u, 0u);
     }
   };
@@ -518,9 +556,6 @@ __global__ void __launch_bounds__(64 * NW, (NMAX <= 256 || KS) ? 4 : 2) attentio
   __builtin_amdgcn_s_waitcnt(0);                // this wave's copies have landed
   __syncthreads();
 
-  bf16x8 ones;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) ones[e] = (bf16)1.f;
   const float c = p.scale_log2;                 // scale * log2(e)
   bool odd = false;
   for (; row < row_end; ++row) {
@@ -550,7 +585,7 @@ __global__ void __launch_bounds__(64 * NW, (NMAX <= 256 || KS) ? 4 : 2) attentio
     uint2 gt[2];
     if constexpr (GATE) {
       if (wave_has_queries && kh == 0) {
-        const bf16* gr = p.gate + (cu + (int64_t)r * sr + (int64_t)min(jw, n - 1) * st) * p.ld_gate + h * D + 4 * g;
+        const bf16* gr = gbase + (cu + (int64_t)r * sr + (int64_t)min(jw, n - 1) * st) * p.ld_gate + 4 * g;
         gt[0] = *reinterpret_cast<const uint2*>(gr);
         gt[1] = *reinterpret_cast<const uint2*>(gr + 16);
       }
@@ -573,8 +608,7 @@ __global__ void __launch_bounds__(64 * NW, (NMAX <= 256 || KS) ? 4 : 2) attentio
       // 2, 4 or 6 tiles that hold keys: all score products of a super-chunk
       // are issued together, one maximum per query, then the exponentials
       // and the value products.  Tiles read stay below the staged length.
-      // key tile offset of this wave's half (key split), uniform
-      const int kto = kh * 16;
+      // first key tile of this wave's half (key split), uniform
       const bf16* Kh = Kb + kto * 512;
       const bf16* Vh = Vb + kto * 512;
       auto super_chunk = [&](auto sc_c, auto nt_c) {
@@ -622,6 +656,7 @@ __global__ void __launch_bounds__(64 * NW, (NMAX <= 256 || KS) ? 4 : 2) attentio
 #pragma unroll
           for (int ii = 0; ii < 4; ++ii)
             P[kt >> 1][(kt & 1) * 4 + ii] = (bf16)__builtin_amdgcn_exp2f(fmaf(S[kt][ii], c, nm));
+        const bf16x8 ones = ones_bf16x8();
 #pragma unroll
         for (int pp = 0; pp + 1 < NT / 2; pp += 2) {
           bf16x8 vf[4];
@@ -645,7 +680,7 @@ __global__ void __launch_bounds__(64 * NW, (NMAX <= 256 || KS) ? 4 : 2) attentio
       // staged length, a multiple of 64, then reaches 128 past kc)
       auto run_sc = [&](auto sc_c) {
         constexpr int SC = decltype(sc_c)::value;
-        const int rem = n - kto * 16 - SC * 128;
+        const int rem = kend - kto * 16 - SC * 128;
         if (rem <= 0) return;
         if (rem > 96) super_chunk(sc_c, std::integral_constant<int, 8>{});
         else if (rem > 64) super_chunk(sc_c, std::integral_constant<int, 6>{});
@@ -687,7 +722,7 @@ __global__ void __launch_bounds__(64 * NW, (NMAX <= 256 || KS) ? 4 : 2) attentio
     if (wave_has_queries && kh == 0) {
       if (qvalid) {
         const float inv = 1.f / O[2][0];
-        bf16* orow = p.o + (cu + (int64_t)r * sr + (int64_t)jw * st) * p.ld_o + h * D;
+        bf16* orow = obase + (cu + (int64_t)r * sr + (int64_t)jw * st) * p.ld_o;
 #pragma unroll
         for (int dt = 0; dt < 2; ++dt) {
           float gs[4] = {1.f, 1.f, 1.f, 1.f};

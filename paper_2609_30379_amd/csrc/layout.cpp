@@ -264,13 +264,17 @@ nt_status plan_layout(const int32_t* lengths, int32_t batch, nt_layout* L, const
     for (int32_t i : order) {
       const int32_t n = lengths[i], nt = (n + kTriTile - 1) / kTriTile;
       const int32_t first = (int32_t)(L->tri_work.size() / 4);
-      for (int32_t xt = 0; xt < nt; ++xt)
-        for (int32_t yt = 0; yt < nt; ++yt) {
-          L->tri_work.push_back(i);
-          L->tri_work.push_back(xt);
-          L->tri_work.push_back(yt);
-          L->tri_work.push_back(first);
-        }
+      // bands of two tile rows, walked column by column: eight consecutive
+      // tiles (what an XCD holds at once, with the four channel blocks of a
+      // z line) read two row blocks of a and four of b
+      for (int32_t xb = 0; xb < nt; xb += 2)
+        for (int32_t yt = 0; yt < nt; ++yt)
+          for (int32_t xt = xb; xt < std::min(xb + 2, nt); ++xt) {
+            L->tri_work.push_back(i);
+            L->tri_work.push_back(xt);
+            L->tri_work.push_back(yt);
+            L->tri_work.push_back(first);
+          }
     }
     while ((L->tri_work.size() / 4) % kXcds) L->tri_work.insert(L->tri_work.end(), {-1, -1, -1, -1});
     // XCD x takes the items [tri_split[x], tri_split[x + 1]) (times the channel

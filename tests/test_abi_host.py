@@ -69,12 +69,15 @@ def test_work_maps_cover_each_item_once(L):
     got = sorted(map(tuple, tri[tri[:, 0] >= 0, :3].tolist()))
     T = 64
     assert got == sorted((i, x, y) for i, n in enumerate(L) for x in range(-(-n // T)) for y in range(-(-n // T)))
-    # a sample's tiles are contiguous, row-major, and carry the index of its first tile
+    # a sample's tiles are contiguous, in bands of two tile rows walked column
+    # by column, and carry the index of its first tile
     for j, (i, x, y, first) in enumerate(tri.tolist()):
         if i < 0:
             continue
         nt = -(-L[i] // T)
-        assert first == j - (x * nt + y) and tri[first, 0] == i and tri[first, 1] == 0 and tri[first, 2] == 0
+        xb = x - x % 2
+        pos = xb * nt + y * min(2, nt - xb) + (x - xb)
+        assert first == j - pos and tri[first, 0] == i and tri[first, 1] == 0 and tri[first, 2] == 0
     seq = lay.host_array("seq_work").reshape(-1, 2)
     got = sorted(map(tuple, seq[seq[:, 0] >= 0].tolist()))
     assert got == sorted((i, q) for i, n in enumerate(L) for q in range(-(-n // 64)))
