@@ -720,23 +720,40 @@ __global__ void __launch_bounds__(64 * NW, (NMAX <= 256 || KS) ? 4 : 2) attentio
       }
     }
     if (wave_has_queries && kh == 0) {
-      if (qvalid) {
-        const float inv = 1.f / O[2][0];
-        bf16* orow = obase + (cu + (int64_t)r * sr + (int64_t)jw * st) * p.ld_o;
+      // lane (l16, g) holds dims 4g .. 4g+3 and 16 + 4g .. +3 of its query;
+      // the rows g, g ^ 1 trade halves so that an even row holds dims
+      // 4g .. 4g+7 and an odd one 16 + 4(g-1) .. +7: one 16-byte store per
+      // lane instead of two 8-byte ones (each store instruction gathers 16
+      // cells and holds the texture-address unit the copies also need)
+      const float inv = 1.f / O[2][0];
+      uint32_t ow[2][2];
 #pragma unroll
-        for (int dt = 0; dt < 2; ++dt) {
-          float gs[4] = {1.f, 1.f, 1.f, 1.f};
-          if constexpr (GATE) {
-            const float gl[4] = {__uint_as_float(gt[dt].x << 16), __uint_as_float(gt[dt].x & 0xffff0000u),
-                                 __uint_as_float(gt[dt].y << 16), __uint_as_float(gt[dt].y & 0xffff0000u)};
+      for (int dt = 0; dt < 2; ++dt) {
+        float gs[4] = {1.f, 1.f, 1.f, 1.f};
+        if constexpr (GATE) {
+          const float gl[4] = {__uint_as_float(gt[dt].x << 16), __uint_as_float(gt[dt].x & 0xffff0000u),
+                               __uint_as_float(gt[dt].y << 16), __uint_as_float(gt[dt].y & 0xffff0000u)};
 #pragma unroll
-            for (int ii = 0; ii < 4; ++ii) gs[ii] = __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-gl[ii] * kLog2e));
-          }
-          bf16x4 ov;
-#pragma unroll
-          for (int ii = 0; ii < 4; ++ii) ov[ii] = (bf16)(O[dt][ii] * inv * gs[ii]);
-          *reinterpret_cast<bf16x4*>(orow + dt * 16 + 4 * g) = ov;
+          for (int ii = 0; ii < 4; ++ii) gs[ii] = __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-gl[ii] * kLog2e));
         }
+        bf16x4 ov;
+#pragma unroll
+        for (int ii = 0; ii < 4; ++ii) ov[ii] = (bf16)(O[dt][ii] * inv * gs[ii]);
+        const uint2 u = __builtin_bit_cast(uint2, ov);
+        ow[dt][0] = u.x;
+        ow[dt][1] = u.y;
+      }
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        // odd rows of the first operand trade with even rows of the second
+        const auto sw = __builtin_amdgcn_permlane16_swap(ow[0][e], ow[1][e], false, false);
+        ow[0][e] = sw[0];
+        ow[1][e] = sw[1];
+      }
+      if (qvalid) {
+        bf16* orow = obase + (cu + (int64_t)r * sr + (int64_t)jw * st) * p.ld_o;
+        const int d0 = (g & 1) ? 16 + 4 * (g - 1) : 4 * g;
+        *reinterpret_cast<uint4*>(orow + d0) = make_uint4(ow[0][0], ow[0][1], ow[1][0], ow[1][1]);
       }
     }
     __builtin_amdgcn_s_waitcnt(0);              // copies for the next row have landed
