@@ -576,7 +576,8 @@ nt_status nt_pair_row_attention_backward_workspace(const nt_layout* layout, int3
  * forward consumed them.  Weight gradients (dw, db, dgamma, dbeta, dw2, db2:
  * fp32, contiguous, NULL = not wanted) are accumulated (overwritten with
  * overwrite_weights); dx (x_dtype or fp32) is overwritten unless accumulate_dx.  Partial sums are reduced in a fixed
- * order: the result is deterministic.                                        */
+ * order: the result is deterministic.  Every pointer, the LayerNorm affine
+ * and the bias included, must be 16-byte aligned.                            */
 typedef struct {
   int64_t rows;                /* R                                              */
   int32_t c_in;                /* K (multiple of 8, <= 1024)                      */

@@ -459,7 +459,8 @@ nt_status nt_layernorm_linear_backward(const nt_linear_bwd_args* a, void* stream
   if (a->rows == 0) return NT_OK;
   if (!a->x || !a->w || !a->dy) return nt::fail(NT_ERR_INVALID_ARG, "x, w and dy must be non-NULL");
   if (!aligned16(a->x) || !aligned16(a->w) || !aligned16(a->dy) || (a->dx && !aligned16(a->dx)) ||
-      (a->w2 && !aligned16(a->w2)))
+      (a->w2 && !aligned16(a->w2)) || (a->ln_gamma && !aligned16(a->ln_gamma)) ||
+      (a->ln_beta && !aligned16(a->ln_beta)) || (a->bias && !aligned16(a->bias)))
     return nt::fail(NT_ERR_INVALID_ARG, "pointers must be 16-byte aligned");
   if (nt_status st = need_workspace(nt::linear_backward_workspace_bytes(*a), a->workspace, a->workspace_bytes,
                                     "nt_layernorm_linear_backward_workspace"))

@@ -285,3 +285,19 @@ def test_workspace_tensor_holds_the_requested_bytes(n):
     t = B.workspace_tensor(n, device="cpu")
     assert t.numel() * t.element_size() == n and t.data_ptr() % 16 == 0
     assert B.workspace_tensor(0, device="cpu") is None
+
+
+def test_linear_backward_rejects_misaligned_parameters(lib):
+    """The backward reads the LayerNorm affine and the bias in 16-byte pieces:
+    misaligned pointers are rejected before any device work."""
+    base = dict(rows=64, c_in=128, c_out=128, x=C.c_void_p(0x1000), ldx=128, x_dtype=B.NT_BF16,
+                w=C.c_void_p(0x2000), dy=C.c_void_p(0x3000), ld_dy=128, dx=C.c_void_p(0x4000), ld_dx=128,
+                dx_dtype=B.NT_BF16, ln_gamma=C.c_void_p(0x5000), ln_beta=C.c_void_p(0x6000), ln_eps=1e-5,
+                workspace=C.c_void_p(0x10000), workspace_bytes=1 << 30)
+    for field in ("ln_gamma", "ln_beta", "bias"):
+        a = B.LinearBwdArgs()
+        for k, v in base.items():
+            setattr(a, k, v)
+        setattr(a, field, C.c_void_p(0x7004))
+        st = lib.nt_layernorm_linear_backward(C.byref(a), None)
+        assert st == B.NT_ERR_INVALID_ARG and b"aligned" in lib.nt_last_error(), field
