@@ -112,6 +112,197 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(int M, int N, int K, con
       }
 }
 
+// ---------------------------------------------------------------- weight gradients
+// C[M, N] = sum over rows r of a range: A[r, m] B[r, n] (the weight gradient
+// g^T x of a linear layer, the contraction running over all packed rows).
+// Both operands are read row-major, as stored: per 32-row step a workgroup
+// copies a 32 x 128 slice of each into LDS (global -> LDS, 256 contiguous
+// bytes per row), and the fragments, which need 8 rows of one column, come
+// from transpose reads.  Four stages of copies are in flight.  Inside a row
+// of the LDS slice the 16-byte chunks are XOR-permuted by 2 (r % 8), so the
+// four rows a 16-lane group reads land on different banks.
+// Workgroup b runs on XCD b % 8: the column tiles of one row range are
+// consecutive workgroups of one XCD, so an operand slice that several tiles
+// read is fetched into that L2 once.
+// Requires M and N multiples of 128, lda and ldb multiples of 8 and 16-byte
+// aligned bases; row range z covers [z kchunk, min(R, (z + 1) kchunk)) with
+// kchunk a multiple of 32, and its partial goes to C + z split_stride.
+// With colsum, the column sums of A over the range (a bias gradient) go to
+// colsum[z M + m]: the waves of the first column tile that hold no B columns
+// past 64 add one more product per fragment, with a ones operand.
+constexpr int kWgT = 128, kWgStages = 4;
+
+__device__ __forceinline__ uint32_t lds_addr_wg(const bf16* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) bf16*)p;
+}
+// Fragments of columns from row-major LDS slices with rows kWgT apart: per
+// fragment two transpose reads 16 rows apart.  Lane (l16, grp) of a read at
+// address a (its piece: row 4 grp + l16 / 4, columns 4 (l16 % 4) .. + 3 of a
+// 16-column group) receives column l16 of rows 4 grp .. 4 grp + 3, and of
+// rows 16 + 4 grp .. + 3 from the second read.  Written as one block with its
+// own LDS wait: the compiler would otherwise make these reads wait for the
+// global -> LDS copies still in flight into other stages.
+__device__ __forceinline__ void tr_read_frags(const uint32_t (&a)[8], bf16x8 (&f)[8]) {
+  uint2 r[16];
+  asm volatile(
+      "ds_read_b64_tr_b16 %0, %16\n"
+      "ds_read_b64_tr_b16 %1, %16 offset:4096\n"
+      "ds_read_b64_tr_b16 %2, %17\n"
+      "ds_read_b64_tr_b16 %3, %17 offset:4096\n"
+      "ds_read_b64_tr_b16 %4, %18\n"
+      "ds_read_b64_tr_b16 %5, %18 offset:4096\n"
+      "ds_read_b64_tr_b16 %6, %19\n"
+      "ds_read_b64_tr_b16 %7, %19 offset:4096\n"
+      "ds_read_b64_tr_b16 %8, %20\n"
+      "ds_read_b64_tr_b16 %9, %20 offset:4096\n"
+      "ds_read_b64_tr_b16 %10, %21\n"
+      "ds_read_b64_tr_b16 %11, %21 offset:4096\n"
+      "ds_read_b64_tr_b16 %12, %22\n"
+      "ds_read_b64_tr_b16 %13, %22 offset:4096\n"
+      "ds_read_b64_tr_b16 %14, %23\n"
+      "ds_read_b64_tr_b16 %15, %23 offset:4096\n"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]), "=&v"(r[6]), "=&v"(r[7]),
+        "=&v"(r[8]), "=&v"(r[9]), "=&v"(r[10]), "=&v"(r[11]), "=&v"(r[12]), "=&v"(r[13]), "=&v"(r[14]), "=&v"(r[15])
+      : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(a[5]), "v"(a[6]), "v"(a[7])
+      : "memory");
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const uint32_t w[4] = {r[2 * i].x, r[2 * i].y, r[2 * i + 1].x, r[2 * i + 1].y};
+    f[i] = __builtin_bit_cast(bf16x8, w);
+  }
+}
+static_assert(16 * 128 * 2 == 4096, "second transpose read: 16 rows of a 128-column slice further");
+constexpr int kWgStage = 2 * 32 * kWgT;              // bf16 per stage (A and B slices)
+
+__global__ void __launch_bounds__(256, 2) wgrad_kernel(int M, int N, int R, const bf16* __restrict__ A, int64_t lda,
+                                                       const bf16* __restrict__ B, int64_t ldb, float* __restrict__ C,
+                                                       int kchunk, int splits, int64_t split_stride,
+                                                       float* __restrict__ colsum) {
+  extern __shared__ __attribute__((aligned(16))) bf16 wg_lds[];
+  const int mt = M / kWgT, T = mt * (N / kWgT);
+  const int xcd = blockIdx.x % kXcds, q = blockIdx.x / kXcds;
+  const int z = (q / T) * kXcds + xcd, t = q % T;
+  if (z >= splits) return;
+  const int m0 = (t % mt) * kWgT, n0 = (t / mt) * kWgT;
+  const int rbeg = z * kchunk, rend = min(R, rbeg + kchunk);
+  if (rbeg >= rend) return;
+  const int nsteps = (rend - rbeg + 31) / 32;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int l16 = lane & 15, grp = lane >> 4;
+
+  // copies of step s into stage s % kWgStages: wave w copies rows 8 w .. 8 w + 7
+  // of both slices (two 1 KB instructions each); lane i of an instruction
+  // writes LDS chunk i % 16 of row i / 16, which holds column chunk
+  // (i % 16) ^ 2 (row % 8) of the operand row (clamped into the matrix)
+  const int crow = lane >> 4, cpos = lane & 15;
+  auto copy_step = [&](int s) {
+    bf16* st = wg_lds + (s % kWgStages) * kWgStage;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int r = wave * 8 + h * 4 + crow;
+      const int gr = min(rbeg + s * 32 + r, R - 1);
+      const int ch = cpos ^ (2 * (r & 7));
+      const bf16* sa = A + (int64_t)gr * lda + m0 + ch * 8;
+      const bf16* sb = B + (int64_t)gr * ldb + n0 + ch * 8;
+      bf16* da = st + (wave * 8 + h * 4) * kWgT;
+      __builtin_amdgcn_global_load_lds((const void*)sa, (__attribute__((address_space(3))) void*)da, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((const void*)sb, (__attribute__((address_space(3))) void*)(da + 32 * kWgT), 16, 0,
+                                       0);
+    }
+  };
+  // transpose-read byte offset of this lane inside a slice for the 16
+  // columns at c0 (a multiple of 16): row 4 grp + l16 / 4 (the second read is
+  // 16 rows further), columns c0 + 4 (l16 % 4) .. + 3
+  const int trow = 4 * grp + (l16 >> 2);
+  auto tr_off = [&](int c0) -> uint32_t {
+    const int col = c0 + 4 * (l16 & 3);
+    return (uint32_t)((trow * kWgT + (((col >> 3) ^ (2 * (trow & 7))) << 3) + (col & 7)) * 2);
+  };
+  uint32_t offa[4], offb[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    offa[i] = tr_off(wm * 64 + 16 * i);
+    offb[i] = tr_off(wn * 64 + 16 * i) + 32 * kWgT * 2;
+  }
+  f32x4 acc[4][4], accs[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    accs[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  const bool do_cs = colsum != nullptr && n0 == 0 && wn == 0;     // uniform
+
+#pragma unroll
+  for (int s = 0; s < kWgStages - 1; ++s)
+    if (s < nsteps) copy_step(s);
+  for (int s = 0; s < nsteps; ++s) {
+    // step s has landed once at most the newer stages' copies (4 per stage
+    // per wave) are outstanding
+    const int newer = min(kWgStages - 2, nsteps - 1 - s);
+    if (newer >= 2) __builtin_amdgcn_s_waitcnt(0x3F70 | 8);        // vmcnt(8)
+    else if (newer == 1) __builtin_amdgcn_s_waitcnt(0x3F70 | 4);   // vmcnt(4)
+    else __builtin_amdgcn_s_waitcnt(0x3F70);                       // vmcnt(0)
+    // every wave's copies of step s have landed and its reads of step s - 1
+    // are done (they end in an LDS wait): the stage of step s - 1 is free
+    __builtin_amdgcn_s_barrier();
+    if (s + kWgStages - 1 < nsteps) copy_step(s + kWgStages - 1);
+    const uint32_t base = lds_addr_wg(wg_lds + (s % kWgStages) * kWgStage);
+    uint32_t ad[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      ad[i] = base + offa[i];
+      ad[4 + i] = base + offb[i];
+    }
+    bf16x8 fr[8];
+    tr_read_frags(ad, fr);
+    bf16x8 fa[4], fb[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      fa[i] = fr[i];
+      fb[i] = fr[4 + i];
+    }
+    // rows past the range (last step only) contribute zero
+    if (rbeg + s * 32 + 32 > rend) {
+      const int lim = rend - rbeg - s * 32;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int rr = (e < 4 ? 0 : 16) + 4 * grp + (e & 3);
+        if (rr >= lim)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) fa[i][e] = (bf16)0.f;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = mfma16(fa[i], fb[j], acc[i][j]);
+    if (do_cs) {
+      const bf16x8 ones = {(bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f, (bf16)1.f};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) accs[i] = mfma16(fa[i], ones, accs[i]);
+    }
+  }
+  // accs[i][e] (every column l16 alike) = sum of A column m0 + 64 wm + 16 i + 4 grp + e
+  if (do_cs && l16 == 0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) colsum[(int64_t)z * M + m0 + 64 * wm + 16 * i + 4 * grp + e] = accs[i][e];
+  }
+  // acc[i][j][e] = C[m0 + 64 wm + 16 i + 4 grp + e][n0 + 64 wn + 16 j + l16]
+  float* Cz = C + (int64_t)z * split_stride;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        Cz[(int64_t)(m0 + 64 * wm + 16 * i + 4 * grp + e) * N + n0 + 64 * wn + 16 * j + l16] = acc[i][j][e];
+}
+
 // out[i] (+)= sum_s part[s * stride + i], i < n: fixed order over s.
 __global__ void __launch_bounds__(256) reduce_partials_kernel(const float* __restrict__ part, int splits,
                                                               int64_t stride, int64_t n, float* __restrict__ out,
@@ -339,7 +530,7 @@ __global__ void __launch_bounds__(256) ln_backward_vec_kernel(const float* __res
     }
     s1 /= (float)K;
     s2 /= (float)K;
-    if (!ok) continue;
+    if (!ok || !dx) continue;                   // (dx == NULL: only dgamma / dbeta wanted)
     float v[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) v[e] = rs * (gv[e] - s1 - xh[e] * s2);
@@ -368,6 +559,149 @@ __global__ void __launch_bounds__(256) ln_backward_vec_kernel(const float* __res
   for (int c = threadIdx.x; c < K; c += 256) {
     part_g[(int64_t)blockIdx.x * K + c] = (sg[0][c] + sg[1][c]) + (sg[2][c] + sg[3][c]);
     part_b[(int64_t)blockIdx.x * K + c] = (sb[0][c] + sb[1][c]) + (sb[2][c] + sb[3][c]);
+  }
+}
+
+// d(LN x) = g W and the LayerNorm backward in one pass (K = 64 or 128
+// channels): g [R, Nw] bf16 (row stride ld_g), W given transposed, wt [K, Nw].
+// A wave owns 64 rows and computes d(LN x)^T = W^T g^T on matrix cores, so a
+// lane ends with 32 (K = 128) channels 16 j + 4 grp + e of row 16 i + l16 of
+// each of its four row tiles: a row's sums are in-lane sums plus two lane-row
+// swaps.  Then, as ln_backward_vec_kernel,
+//   gv = d(LN x) gamma,  xhat = (x - mean) rstd,
+//   dx = rstd (gv - mean(gv) - xhat mean(gv xhat))  (+ res, + dx if accumulating),
+// and the wave's sums of d(LN x) xhat and d(LN x) go to part_g / part_b row
+// (64-row group) blockIdx.x * 4 + wave.  Requires Nw a multiple of 32,
+// ld_g, ldx and the bases 16-byte aligned.
+template <int K, typename TO>
+__global__ void __launch_bounds__(256, 2) dgrad_ln_kernel(const bf16* __restrict__ g, int64_t ld_g, int Nw,
+                                                          const bf16* __restrict__ wt, const bf16* __restrict__ x,
+                                                          int64_t ldx, int R, const float* __restrict__ gamma,
+                                                          const float* __restrict__ mean,
+                                                          const float* __restrict__ rstd, const TO* __restrict__ res,
+                                                          int64_t ld_res, TO* __restrict__ dx, int64_t ld_dx,
+                                                          int accumulate, float* __restrict__ part_g,
+                                                          float* __restrict__ part_b) {
+  constexpr int KT = K / 16;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int l16 = lane & 15, grp = lane >> 4;
+  const int wg = blockIdx.x * 4 + wave;
+  const int r0 = wg * 64;
+  if (r0 >= R) return;
+  // this lane's g rows (clamped: a row past R only feeds its own discarded output)
+  const bf16* gp[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) gp[i] = g + (int64_t)min(r0 + 16 * i + l16, R - 1) * ld_g + 8 * grp;
+  const bf16* wp = wt + (int64_t)l16 * Nw + 8 * grp;
+  f32x4 acc[KT][4];
+#pragma unroll
+  for (int j = 0; j < KT; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int nks = Nw / 32;
+  bf16x8 gf[4], gn[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) gf[i] = *reinterpret_cast<const bf16x8*>(gp[i]);
+  for (int ks = 0; ks < nks; ++ks) {
+    bf16x8 wf[KT];
+#pragma unroll
+    for (int j = 0; j < KT; ++j) wf[j] = *reinterpret_cast<const bf16x8*>(wp + (int64_t)16 * j * Nw + ks * 32);
+    if (ks + 1 < nks) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) gn[i] = *reinterpret_cast<const bf16x8*>(gp[i] + (ks + 1) * 32);
+    }
+#pragma unroll
+    for (int j = 0; j < KT; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[j][i] = mfma16(wf[j], gf[i], acc[j][i]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) gf[i] = gn[i];
+  }
+  // acc[j][i][e] = d(LN x)[r0 + 16 i + l16][16 j + 4 grp + e]
+  float pg[KT][4], pb[KT][4];
+#pragma unroll
+  for (int j = 0; j < KT; ++j)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) pg[j][e] = pb[j][e] = 0.f;
+  // two passes over the lane's channels per row tile: the row sums, then dx;
+  // x and gamma are read again in the second pass (cache hits) rather than
+  // held in registers next to the accumulators
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = r0 + 16 * i + l16;
+    const bool ok = row < R;
+    const int rr = min(row, R - 1);
+    const float mu = mean[rr], rs = rstd[rr];
+    const bf16* xr = x + (int64_t)rr * ldx + 4 * grp;
+    auto xhat_gamma = [&](int j, float (&xh)[4], float (&gg)[4]) {
+      const uint2 q = *reinterpret_cast<const uint2*>(xr + 16 * j);
+      const float4 gm = *reinterpret_cast<const float4*>(gamma + 16 * j + 4 * grp);
+      xh[0] = (__uint_as_float(q.x << 16) - mu) * rs;
+      xh[1] = (__uint_as_float(q.x & 0xffff0000u) - mu) * rs;
+      xh[2] = (__uint_as_float(q.y << 16) - mu) * rs;
+      xh[3] = (__uint_as_float(q.y & 0xffff0000u) - mu) * rs;
+      gg[0] = gm.x; gg[1] = gm.y; gg[2] = gm.z; gg[3] = gm.w;
+    };
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int j = 0; j < KT; ++j) {
+      float xh[4], gg[4];
+      xhat_gamma(j, xh, gg);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float d = ok ? acc[j][i][e] : 0.f;
+        const float gv = d * gg[e];
+        s1 += gv;
+        s2 += gv * xh[e];
+        pg[j][e] += d * xh[e];
+        pb[j][e] += d;
+      }
+    }
+    s1 = sum_over_kgroups(s1) / (float)K;
+    s2 = sum_over_kgroups(s2) / (float)K;
+    if (!ok || !dx) continue;                   // (dx == NULL: only dgamma / dbeta wanted)
+#pragma unroll
+    for (int j = 0; j < KT; ++j) {
+      float xh[4], gg[4];
+      xhat_gamma(j, xh, gg);
+      float v[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = rs * (acc[j][i][e] * gg[e] - s1 - xh[e] * s2);
+      const int64_t c = 16 * j + 4 * grp;
+      if (res) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] += to_f32(res[(int64_t)row * ld_res + c + e]);
+      }
+      TO* o = dx + (int64_t)row * ld_dx + c;
+      if (accumulate) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] += to_f32(o[e]);
+      }
+      if constexpr (sizeof(TO) == 4) {
+        *reinterpret_cast<float4*>(o) = make_float4(v[0], v[1], v[2], v[3]);
+      } else {
+        bf16x4 ov;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) ov[e] = (bf16)v[e];
+        *reinterpret_cast<bf16x4*>(o) = ov;
+      }
+    }
+  }
+  // the 16 lanes l16 of a row group hold the same channels: sum them
+#pragma unroll
+  for (int j = 0; j < KT; ++j)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      pg[j][e] = group_sum<16>(pg[j][e]);
+      pb[j][e] = group_sum<16>(pb[j][e]);
+    }
+  if (l16 == 0) {
+#pragma unroll
+    for (int j = 0; j < KT; ++j) {
+      const int64_t c = (int64_t)wg * K + 16 * j + 4 * grp;
+      *reinterpret_cast<float4*>(part_g + c) = make_float4(pg[j][0], pg[j][1], pg[j][2], pg[j][3]);
+      *reinterpret_cast<float4*>(part_b + c) = make_float4(pb[j][0], pb[j][1], pb[j][2], pb[j][3]);
+    }
   }
 }
 
@@ -414,6 +748,7 @@ __global__ void __launch_bounds__(256) ln_backward_kernel(const float* __restric
     }
     s1 /= (float)K;
     s2 /= (float)K;
+    if (!dx) continue;                          // only dgamma / dbeta wanted
 #pragma unroll
     for (int j = 0; j < kMaxPer; ++j) {
       const int c = lane + 64 * j;
@@ -648,6 +983,29 @@ struct Carve {
 
 constexpr int kRowsPerGroup = 256;   // rows per partial group of the LayerNorm and column sums
 
+// Row ranges of a weight gradient C[M, N] = sum_r A[r, m] B[r, n] on
+// wgrad_kernel: about two workgroups per CU in all, ranges a multiple of 32
+// rows and at least 128.  splits == 0: the shape does not fit the kernel.
+struct WgPlan {
+  int splits = 0, kchunk = 0;
+  unsigned grid = 0;
+};
+WgPlan wgrad_plan(int M, int N, int R, int64_t lda, int64_t ldb) {
+  WgPlan w;
+  if (M % kWgT || N % kWgT || lda % 8 || ldb % 8 || R <= 0 || M <= 0 || N <= 0) return w;
+  const int T = (M / kWgT) * (N / kWgT);
+  const int want = std::max(1, 512 / T);
+  w.kchunk = std::max(128, ((R + want - 1) / want + 31) / 32 * 32);
+  w.splits = (R + w.kchunk - 1) / w.kchunk;
+  w.grid = (unsigned)((w.splits + kXcds - 1) / kXcds * kXcds * T);
+  return w;
+}
+void launch_wgrad(const WgPlan& w, int M, int N, int R, const bf16* A, int64_t lda, const bf16* B, int64_t ldb,
+                  float* part, float* colsum, hipStream_t s) {
+  wgrad_kernel<<<dim3(w.grid), dim3(256), kWgStages * kWgStage * sizeof(bf16), s>>>(
+      M, N, R, A, lda, B, ldb, part, w.kchunk, w.splits, (int64_t)M * N, colsum);
+}
+
 // Plans (and, with launch, runs) the backward; with ws == nullptr it only
 // counts the workspace bytes.
 hipError_t run_linear_backward(const nt_linear_bwd_args& a, void* ws, size_t* bytes, hipStream_t s, bool launch) {
@@ -677,18 +1035,35 @@ hipError_t run_linear_backward(const nt_linear_bwd_args& a, void* ws, size_t* by
   bf16* h = swiglu ? c.take<bf16>((size_t)R * F) : nullptr;
   bf16* dp = (gelu || swiglu) ? c.take<bf16>((size_t)R * Nw) : nullptr;        // d(pre-activation), bf16
   const bool direct_dx = !ln && dxf;                                      // the product writes dx itself
-  float* dxn = direct_dx ? nullptr : c.take<float>((size_t)R * K);
+  // LayerNorm on bf16 rows of 64 or 128: d(LN x) = g W and the LayerNorm
+  // backward in one kernel (no fp32 d(LN x) in memory)
+  const int64_t ld_g_dx = (gelu || swiglu) ? Nw : a.ld_dy;
+  const bool dgrad_fused = ln && vec_ln && (K == 64 || K == 128) && Nw % 32 == 0 && ld_g_dx % 8 == 0 &&
+                           (a.dx || a.dgamma || a.dbeta);
+  bf16* wt1 = dgrad_fused ? c.take<bf16>((size_t)K * Nw) : nullptr;         // W^T [K, Nw]
+  float* dxn = (direct_dx || dgrad_fused) ? nullptr : c.take<float>((size_t)R * K);
   const int groups = (R + rpg - 1) / rpg;
   float* part_g = c.take<float>((size_t)groups * K);
   float* part_b = c.take<float>((size_t)groups * K);
   float* part_col = c.take<float>((size_t)groups * std::max(Nw, a.c_out));
 
+  // weight gradients: dW = g^T LN(x) [Nw, K] and (SwiGLU) dW2 = dy^T h [N, F],
+  // on wgrad_kernel where the shape allows, else on the general product
+  const int64_t ld_g_plan = (gelu || swiglu) ? Nw : a.ld_dy;
+  const int64_t ld_x_plan = (ln || xf) ? K : a.ldx;
+  const WgPlan wp = wgrad_plan(Nw, K, R, ld_g_plan, ld_x_plan);
   const int64_t tiles_w = (int64_t)((Nw + kBM - 1) / kBM) * ((K + kBN - 1) / kBN);
-  const int sw = splits_for(tiles_w, R);
+  const int sw = wp.splits ? wp.splits : splits_for(tiles_w, R);
   float* part_w = c.take<float>((size_t)sw * Nw * K);
+  const WgPlan wp2 = swiglu ? wgrad_plan(a.c_out, F, R, a.ld_dy, F) : WgPlan{};
   const int64_t tiles_w2 = (int64_t)((a.c_out + kBM - 1) / kBM) * ((F + kBN - 1) / kBN);
-  const int sw2 = swiglu ? splits_for(tiles_w2, R) : 0;
+  const int sw2 = swiglu ? (wp2.splits ? wp2.splits : splits_for(tiles_w2, R)) : 0;
   float* part_w2 = swiglu ? c.take<float>((size_t)sw2 * a.c_out * F) : nullptr;
+  // bias gradients as column sums inside the weight-gradient kernel (per row range)
+  const bool cs_fused = wp.splits && a.dw && a.db;
+  const bool cs2_fused = wp2.splits && a.dw2 && a.db2;
+  float* part_cs = cs_fused ? c.take<float>((size_t)wp.splits * Nw) : nullptr;
+  float* part_cs2 = cs2_fused ? c.take<float>((size_t)wp2.splits * a.c_out) : nullptr;
   // second level of the reductions with more than 64 partials
   auto slices = [](int64_t splits) -> size_t { return splits > 64 ? (size_t)((splits + 63) / 64) : 0; };
   const size_t n2 = std::max({slices(groups) * (size_t)std::max(std::max(Nw, a.c_out), K),
@@ -772,11 +1147,16 @@ hipError_t run_linear_backward(const nt_linear_bwd_args& a, void* ws, size_t* by
       // dW2 += dy^T h,  db2 += sum_rows dy
       if (a.dw2) {
         const int kc = (R + sw2 - 1) / sw2;
-        gemm_bf16_kernel<true, false><<<dim3((a.c_out + kBM - 1) / kBM, (F + kBN - 1) / kBN, sw2), b256, 0, s>>>(
-            a.c_out, F, R, dy, a.ld_dy, h, F, part_w2, F, 1.f, 0, kc, (int64_t)a.c_out * F);
+        if (wp2.splits)
+          launch_wgrad(wp2, a.c_out, F, R, dy, a.ld_dy, h, F, part_w2, part_cs2, s);
+        else
+          gemm_bf16_kernel<true, false><<<dim3((a.c_out + kBM - 1) / kBM, (F + kBN - 1) / kBN, sw2), b256, 0, s>>>(
+              a.c_out, F, R, dy, a.ld_dy, h, F, part_w2, F, 1.f, 0, kc, (int64_t)a.c_out * F);
         reduce_parts(part_w2, sw2, (int64_t)a.c_out * F, (int64_t)a.c_out * F, a.dw2);
       }
-      if (a.db2) {
+      if (cs2_fused) {
+        reduce_parts(part_cs2, wp2.splits, a.c_out, a.c_out, a.db2);
+      } else if (a.db2) {
         column_parts(dy, a.ld_dy, a.c_out);
         reduce_parts(part_col, groups, a.c_out, a.c_out, a.db2);
       }
@@ -787,11 +1167,17 @@ hipError_t run_linear_backward(const nt_linear_bwd_args& a, void* ws, size_t* by
   // weight and bias gradients: dW += g^T LN(x),  db += sum_rows g
   if (a.dw) {
     const int kc = (R + sw - 1) / sw;
-    gemm_bf16_kernel<true, false><<<dim3((Nw + kBM - 1) / kBM, (K + kBN - 1) / kBN, sw), b256, 0, s>>>(
-        Nw, K, R, g, ld_g, xin, ld_xin, part_w, K, 1.f, 0, kc, (int64_t)Nw * K);
+    if (ld_g != ld_g_plan || ld_xin != ld_x_plan) return hipErrorInvalidValue;   // the plan saw these strides
+    if (wp.splits)
+      launch_wgrad(wp, Nw, K, R, g, ld_g, xin, ld_xin, part_w, part_cs, s);
+    else
+      gemm_bf16_kernel<true, false><<<dim3((Nw + kBM - 1) / kBM, (K + kBN - 1) / kBN, sw), b256, 0, s>>>(
+          Nw, K, R, g, ld_g, xin, ld_xin, part_w, K, 1.f, 0, kc, (int64_t)Nw * K);
     reduce_parts(part_w, sw, (int64_t)Nw * K, (int64_t)Nw * K, a.dw);
   }
-  if (a.db) {
+  if (cs_fused) {
+    reduce_parts(part_cs, wp.splits, Nw, Nw, a.db);
+  } else if (a.db) {
     column_parts(g, ld_g, Nw);
     reduce_parts(part_col, groups, Nw, Nw, a.db);
   }
@@ -801,6 +1187,22 @@ hipError_t run_linear_backward(const nt_linear_bwd_args& a, void* ws, size_t* by
     if (a.dx)
       gemm_bf16_kernel<false, false><<<dim3((R + kBM - 1) / kBM, (K + kBN - 1) / kBN, 1), b256, 0, s>>>(
           R, K, Nw, g, ld_g, W, K, (float*)a.dx, a.ld_dx, 1.f, a.accumulate_dx, Nw, 0);
+    return hipGetLastError();
+  }
+  if (dgrad_fused) {
+    if (ld_g != ld_g_dx) return hipErrorInvalidValue;                       // the plan saw this stride
+    if (res && dxf) return hipErrorInvalidValue;                            // the SwiGLU residual is bf16
+    transpose_bf16_kernel<<<blocks_for((int64_t)Nw * K), b256, 0, s>>>(W, Nw, K, wt1);
+    const dim3 grid((unsigned)((R + 255) / 256));
+#define NT_DGLN(KK, TO)                                                                                        \
+    dgrad_ln_kernel<KK, TO><<<grid, b256, 0, s>>>(g, ld_g, Nw, wt1, (const bf16*)a.x, a.ldx, R, a.ln_gamma, mean, \
+                                                  rstd, (const TO*)res, a.ld_dy, (TO*)a.dx, a.ld_dx,            \
+                                                  a.accumulate_dx, part_g, part_b)
+    if (K == 64) { if (dxf) NT_DGLN(64, float); else NT_DGLN(64, bf16); }
+    else { if (dxf) NT_DGLN(128, float); else NT_DGLN(128, bf16); }
+#undef NT_DGLN
+    if (a.dgamma) reduce_parts(part_g, groups, K, K, a.dgamma);
+    if (a.dbeta) reduce_parts(part_b, groups, K, K, a.dbeta);
     return hipGetLastError();
   }
   // d(LN x) = g W  (W stored [Nw, K])

@@ -129,6 +129,7 @@ LIN_BWD = [
     (300, 384, 256, False, "none", "bf16", "f32"),      # single projection u|v (no LayerNorm)
     (300, 128, 384, False, "residual", "f32", "f32"),   # single update from an fp32 column mean
     (130, 136, 40, True, "none", "f32", "bf16"),
+    (70001, 128, 256, True, "none", "bf16", "bf16"),   # weight gradient over 244 row ranges, 17-row tail
 ]
 
 
