@@ -564,15 +564,82 @@ __global__ void __launch_bounds__(256) ln_backward_vec_kernel(const float* __res
 
 // d(LN x) = g W and the LayerNorm backward in one pass (K = 64 or 128
 // channels): g [R, Nw] bf16 (row stride ld_g), W given transposed, wt [K, Nw].
-// A wave owns 64 rows and computes d(LN x)^T = W^T g^T on matrix cores, so a
-// lane ends with 32 (K = 128) channels 16 j + 4 grp + e of row 16 i + l16 of
-// each of its four row tiles: a row's sums are in-lane sums plus two lane-row
-// swaps.  Then, as ln_backward_vec_kernel,
+// A workgroup of four waves owns 128 rows, a wave 32 of them, and computes
+// d(LN x)^T = W^T g^T on matrix cores: per 32-wide step of the contraction
+// it copies the g slice of its rows and the W^T slice into LDS (global ->
+// LDS, in fragment order: each fragment is one contiguous 1 KB read),
+// three stages deep.  A lane ends with K / 4 channels 16 j + 4 grp + e of row
+// 16 i + l16 of each of its wave's two row tiles, so a row's sums are in-lane
+// sums plus two lane-row swaps.  Then, as ln_backward_vec_kernel,
 //   gv = d(LN x) gamma,  xhat = (x - mean) rstd,
 //   dx = rstd (gv - mean(gv) - xhat mean(gv xhat))  (+ res, + dx if accumulating),
 // and the wave's sums of d(LN x) xhat and d(LN x) go to part_g / part_b row
-// (64-row group) blockIdx.x * 4 + wave.  Requires Nw a multiple of 32,
+// (32-row group) blockIdx.x * 4 + wave.  Requires Nw a multiple of 32,
 // ld_g, ldx and the bases 16-byte aligned.
+constexpr int kDgStages = 3, kDgRT = 2;        // stages; row tiles per wave
+constexpr int kDgRows = 4 * 16 * kDgRT;        // rows per workgroup
+template <int K> constexpr int dg_stage_elems() { return kDgRows * 32 + K * 32; }   // g slice + W^T slice
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+// Sum over the 16 lanes of a DPP row (lanes 16 r .. 16 r + 15): four
+// rotate-and-add steps within the row; lane 16 r holds the whole sum.
+__device__ __forceinline__ float row16_sum(float v) {
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x128, 0xf, 0xf, false));   // row_ror:8
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x124, 0xf, 0xf, false));   // row_ror:4
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x122, 0xf, 0xf, false));   // row_ror:2
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x121, 0xf, 0xf, false));   // row_ror:1
+  return v;
+}
+// the fragments of one step: KT W^T fragments at aw + 1 KB j, two g
+// fragments at ag, ag + 1 KB; one block with its own LDS wait (the compiler
+// would make plain reads wait for the copies in flight into other stages)
+template <int KT>
+__device__ __forceinline__ void dg_read(uint32_t aw, uint32_t ag, bf16x8 (&wf)[KT], bf16x8 (&gf)[kDgRT]);
+template <>
+__device__ __forceinline__ void dg_read<8>(uint32_t aw, uint32_t ag, bf16x8 (&wf)[8], bf16x8 (&gf)[kDgRT]) {
+  u32x4 r[10];
+  asm volatile(
+      "ds_read_b128 %0, %10\n"
+      "ds_read_b128 %1, %10 offset:1024\n"
+      "ds_read_b128 %2, %10 offset:2048\n"
+      "ds_read_b128 %3, %10 offset:3072\n"
+      "ds_read_b128 %4, %10 offset:4096\n"
+      "ds_read_b128 %5, %10 offset:5120\n"
+      "ds_read_b128 %6, %10 offset:6144\n"
+      "ds_read_b128 %7, %10 offset:7168\n"
+      "ds_read_b128 %8, %11\n"
+      "ds_read_b128 %9, %11 offset:1024\n"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]), "=&v"(r[6]), "=&v"(r[7]),
+        "=&v"(r[8]), "=&v"(r[9])
+      : "v"(aw), "v"(ag)
+      : "memory");
+#pragma unroll
+  for (int j = 0; j < 8; ++j) wf[j] = __builtin_bit_cast(bf16x8, r[j]);
+#pragma unroll
+  for (int i = 0; i < kDgRT; ++i) gf[i] = __builtin_bit_cast(bf16x8, r[8 + i]);
+}
+template <>
+__device__ __forceinline__ void dg_read<4>(uint32_t aw, uint32_t ag, bf16x8 (&wf)[4], bf16x8 (&gf)[kDgRT]) {
+  u32x4 r[6];
+  asm volatile(
+      "ds_read_b128 %0, %6\n"
+      "ds_read_b128 %1, %6 offset:1024\n"
+      "ds_read_b128 %2, %6 offset:2048\n"
+      "ds_read_b128 %3, %6 offset:3072\n"
+      "ds_read_b128 %4, %7\n"
+      "ds_read_b128 %5, %7 offset:1024\n"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5])
+      : "v"(aw), "v"(ag)
+      : "memory");
+#pragma unroll
+  for (int j = 0; j < 4; ++j) wf[j] = __builtin_bit_cast(bf16x8, r[j]);
+#pragma unroll
+  for (int i = 0; i < kDgRT; ++i) gf[i] = __builtin_bit_cast(bf16x8, r[4 + i]);
+}
+static_assert(kDgRT == 2, "dg_read reads two g fragments");
+
 template <int K, typename TO>
 __global__ void __launch_bounds__(256, 2) dgrad_ln_kernel(const bf16* __restrict__ g, int64_t ld_g, int Nw,
                                                           const bf16* __restrict__ wt, const bf16* __restrict__ x,
@@ -583,96 +650,186 @@ __global__ void __launch_bounds__(256, 2) dgrad_ln_kernel(const bf16* __restrict
                                                           int accumulate, float* __restrict__ part_g,
                                                           float* __restrict__ part_b) {
   constexpr int KT = K / 16;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int SE = dg_stage_elems<K>();
+  constexpr int NOPS = kDgRT + KT / 4;          // copy instructions per wave per step
+  extern __shared__ __attribute__((aligned(16))) bf16 dg_lds[];
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l16 = lane & 15, grp = lane >> 4;
+  const int rb = blockIdx.x * kDgRows;
   const int wg = blockIdx.x * 4 + wave;
-  const int r0 = wg * 64;
-  if (r0 >= R) return;
-  // this lane's g rows (clamped: a row past R only feeds its own discarded output)
-  const bf16* gp[4];
+  const int r0 = wg * 16 * kDgRT;
+  const int nks = Nw / 32;
+
+  // copies of step s: the wave's g tiles u (rows 16 u .. of the workgroup)
+  // and W^T tiles v = wave, wave + 4: lane i fetches row (or channel) i % 16,
+  // k-chunk i / 16, so the tile lands in fragment order.  Rows past R are
+  // clamped (they only feed their own discarded outputs).
+  auto copy_step = [&](int s) {
+    bf16* st = dg_lds + (s % kDgStages) * SE;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) gp[i] = g + (int64_t)min(r0 + 16 * i + l16, R - 1) * ld_g + 8 * grp;
-  const bf16* wp = wt + (int64_t)l16 * Nw + 8 * grp;
-  f32x4 acc[KT][4];
+    for (int t = 0; t < kDgRT; ++t) {
+      const int u = kDgRT * wave + t;
+      const bf16* src = g + (int64_t)min(rb + 16 * u + l16, R - 1) * ld_g + 32 * s + 8 * grp;
+      __builtin_amdgcn_global_load_lds((const void*)src, (__attribute__((address_space(3))) void*)(st + u * 512), 16,
+                                       0, 0);
+    }
+#pragma unroll
+    for (int t = 0; t < KT / 4; ++t) {
+      const int v = wave + 4 * t;
+      const bf16* src = wt + (int64_t)(16 * v + l16) * Nw + 32 * s + 8 * grp;
+      __builtin_amdgcn_global_load_lds((const void*)src,
+                                       (__attribute__((address_space(3))) void*)(st + kDgRows * 32 + v * 512), 16, 0, 0);
+    }
+  };
+  f32x4 acc[KT][kDgRT];
 #pragma unroll
   for (int j = 0; j < KT; ++j)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int nks = Nw / 32;
-  bf16x8 gf[4], gn[4];
+    for (int i = 0; i < kDgRT; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int i = 0; i < 4; ++i) gf[i] = *reinterpret_cast<const bf16x8*>(gp[i]);
+  for (int s = 0; s < kDgStages - 1; ++s)
+    if (s < nks) copy_step(s);
   for (int ks = 0; ks < nks; ++ks) {
-    bf16x8 wf[KT];
-#pragma unroll
-    for (int j = 0; j < KT; ++j) wf[j] = *reinterpret_cast<const bf16x8*>(wp + (int64_t)16 * j * Nw + ks * 32);
-    if (ks + 1 < nks) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) gn[i] = *reinterpret_cast<const bf16x8*>(gp[i] + (ks + 1) * 32);
-    }
+    // step ks has landed once at most the next step's copies are outstanding
+    static_assert(kDgStages == 3, "the wait below covers one later step");
+    if (ks + 1 < nks) __builtin_amdgcn_s_waitcnt(0x3F70 | NOPS);
+    else __builtin_amdgcn_s_waitcnt(0x3F70);
+    __builtin_amdgcn_s_barrier();               // all copies of step ks; step ks - 1 read everywhere
+    if (ks + kDgStages - 1 < nks) copy_step(ks + kDgStages - 1);
+    const uint32_t base =
+        (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) bf16*)(dg_lds + (ks % kDgStages) * SE);
+    bf16x8 wf[KT], gf[kDgRT];
+    dg_read<KT>(base + kDgRows * 32 * 2 + lane * 16, base + wave * kDgRT * 1024 + lane * 16, wf, gf);
 #pragma unroll
     for (int j = 0; j < KT; ++j)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) acc[j][i] = mfma16(wf[j], gf[i], acc[j][i]);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) gf[i] = gn[i];
+      for (int i = 0; i < kDgRT; ++i) acc[j][i] = mfma16(wf[j], gf[i], acc[j][i]);
   }
-  // acc[j][i][e] = d(LN x)[r0 + 16 i + l16][16 j + 4 grp + e]
-  float pg[KT][4], pb[KT][4];
+  // The ring is free once every wave is past its last read: it now takes
+  // the workgroup's x rows and gamma, copied in one burst (global -> LDS).
+  // x row r (of the workgroup) holds its 16-byte chunk c at slot
+  // (r % RW) CR + (c ^ f(r)), CR = K / 8 chunks per row, RW = 256 / (2 K)
+  // rows per 256 bytes, f(r) = (r / RW) % CR: the 16 consecutive rows a
+  // read spans land on 16 different 16-byte slots of the banks.
+  constexpr int CR = K / 8, RW = 256 / (2 * K);
+  __builtin_amdgcn_s_waitcnt(0xC07F);           // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  {
+    constexpr int XI = kDgRows * CR / 64 / 4;   // 1 KB copies of x per wave
 #pragma unroll
-  for (int j = 0; j < KT; ++j)
+    for (int t = 0; t < XI; ++t) {
+      const int u = wave * XI + t;              // copy u: LDS bytes [1024 u, 1024 u + 1024)
+      const int slot = u * 64 + lane;           // 16-byte slot of the x tile
+      const int r = (slot / (RW * CR)) * RW + (slot % (RW * CR)) / CR;   // row owning the slot
+      const int c = (slot % CR) ^ ((r / RW) % CR);
+      const bf16* src = x + (int64_t)min(rb + r, R - 1) * ldx + 8 * c;
+      __builtin_amdgcn_global_load_lds((const void*)src, (__attribute__((address_space(3))) void*)(dg_lds + u * 512),
+                                       16, 0, 0);
+    }
+    if (wave == 0) {                            // gamma after the x tile (lanes past K / 4 repeat its last piece)
+      const float* src = gamma + 4 * min(lane, K / 4 - 1);
+      __builtin_amdgcn_global_load_lds((const void*)src,
+                                       (__attribute__((address_space(3))) void*)(dg_lds + kDgRows * K), 16, 0, 0);
+    }
+  }
+  static_assert(kDgRows * K * 2 + 1024 <= kDgStages * dg_stage_elems<K>() * 2, "x tile and gamma fit in the ring");
+  __builtin_amdgcn_s_waitcnt(0x3F70);           // vmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  if (r0 >= R) return;
+  const bf16* xs = dg_lds;
+  const float* gs = reinterpret_cast<const float*>(dg_lds + kDgRows * K);
+  // acc[j][i][e] = d(LN x)[r0 + 16 i + l16][16 j + 4 grp + e].
+  // First pass, channel tiles outer: the row sums of gv and gv xhat, and per
+  // channel tile the wave's sums of d(LN x) xhat and d(LN x) over its rows
+  // (lane sums over the row tiles, then over the 16 lanes of a row group),
+  // written at once.  Second pass: dx.  x and gamma are read from LDS in
+  // both passes rather than held in registers next to the accumulators.
+  // Rows past R (their g rows were clamped, so their values are finite)
+  // enter the channel sums with weight okf = 0.
+  float mu[kDgRT], rs[kDgRT], s1[kDgRT], s2[kDgRT], okf[kDgRT];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) pg[j][e] = pb[j][e] = 0.f;
-  // two passes over the lane's channels per row tile: the row sums, then dx;
-  // x and gamma are read again in the second pass (cache hits) rather than
-  // held in registers next to the accumulators
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < kDgRT; ++i) {
     const int row = r0 + 16 * i + l16;
-    const bool ok = row < R;
+    okf[i] = row < R ? 1.f : 0.f;
     const int rr = min(row, R - 1);
-    const float mu = mean[rr], rs = rstd[rr];
-    const bf16* xr = x + (int64_t)rr * ldx + 4 * grp;
-    auto xhat_gamma = [&](int j, float (&xh)[4], float (&gg)[4]) {
-      const uint2 q = *reinterpret_cast<const uint2*>(xr + 16 * j);
-      const float4 gm = *reinterpret_cast<const float4*>(gamma + 16 * j + 4 * grp);
-      xh[0] = (__uint_as_float(q.x << 16) - mu) * rs;
-      xh[1] = (__uint_as_float(q.x & 0xffff0000u) - mu) * rs;
-      xh[2] = (__uint_as_float(q.y << 16) - mu) * rs;
-      xh[3] = (__uint_as_float(q.y & 0xffff0000u) - mu) * rs;
-      gg[0] = gm.x; gg[1] = gm.y; gg[2] = gm.z; gg[3] = gm.w;
-    };
-    float s1 = 0.f, s2 = 0.f;
+    mu[i] = mean[rr];
+    rs[i] = rstd[rr];
+    s1[i] = s2[i] = 0.f;
+  }
+  // this lane's x piece (channels 16 j + 4 grp ..) of row tile i, from LDS
+  auto xhat4 = [&](int i, int j, float (&xh)[4]) {
+    const int r = wave * 16 * kDgRT + 16 * i + l16;        // row of the workgroup
+    const int c = 2 * j + (grp >> 1);
+    const int slot = (r / RW) * RW * CR + (r % RW) * CR + (c ^ ((r / RW) % CR));
+    const uint2 q = *reinterpret_cast<const uint2*>(xs + slot * 8 + (grp & 1) * 4);
+    xh[0] = (__uint_as_float(q.x << 16) - mu[i]) * rs[i];
+    xh[1] = (__uint_as_float(q.x & 0xffff0000u) - mu[i]) * rs[i];
+    xh[2] = (__uint_as_float(q.y << 16) - mu[i]) * rs[i];
+    xh[3] = (__uint_as_float(q.y & 0xffff0000u) - mu[i]) * rs[i];
+  };
 #pragma unroll
-    for (int j = 0; j < KT; ++j) {
-      float xh[4], gg[4];
-      xhat_gamma(j, xh, gg);
+  for (int j = 0; j < KT; ++j) {
+    const float4 gm = *reinterpret_cast<const float4*>(gs + 16 * j + 4 * grp);
+    const float gg[4] = {gm.x, gm.y, gm.z, gm.w};
+    float pg[4] = {0.f, 0.f, 0.f, 0.f}, pb[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < kDgRT; ++i) {
+      float xh[4];
+      xhat4(i, j, xh);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float d = ok ? acc[j][i][e] : 0.f;
+        const float d = acc[j][i][e];
         const float gv = d * gg[e];
-        s1 += gv;
-        s2 += gv * xh[e];
-        pg[j][e] += d * xh[e];
-        pb[j][e] += d;
+        s1[i] += gv;
+        s2[i] += gv * xh[e];
+        const float dm = d * okf[i];
+        pg[e] += dm * xh[e];
+        pb[e] += dm;
       }
     }
-    s1 = sum_over_kgroups(s1) / (float)K;
-    s2 = sum_over_kgroups(s2) / (float)K;
-    if (!ok || !dx) continue;                   // (dx == NULL: only dgamma / dbeta wanted)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      pg[e] = row16_sum(pg[e]);
+      pb[e] = row16_sum(pb[e]);
+    }
+    if (l16 == 0) {
+      const int64_t c = (int64_t)wg * K + 16 * j + 4 * grp;
+      *reinterpret_cast<float4*>(part_g + c) = make_float4(pg[0], pg[1], pg[2], pg[3]);
+      *reinterpret_cast<float4*>(part_b + c) = make_float4(pb[0], pb[1], pb[2], pb[3]);
+    }
+    // keep each channel tile's loads inside its iteration: hoisted, they
+    // would sit in registers next to the accumulators
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  if (!dx) return;                              // only dgamma / dbeta wanted
+#pragma unroll
+  for (int i = 0; i < kDgRT; ++i) {
+    s1[i] = sum_over_kgroups(s1[i]) / (float)K;
+    s2[i] = sum_over_kgroups(s2[i]) / (float)K;
+  }
+  // an offset the compiler cannot see through: the second pass reads x and
+  // gamma from LDS again instead of keeping the first pass's values live
+  int z0 = 0;
+  asm volatile("" : "+v"(z0));
+#pragma unroll
+  for (int i = 0; i < kDgRT; ++i) {
+    if (okf[i] == 0.f) continue;
+    const int64_t row = r0 + 16 * i + l16;
 #pragma unroll
     for (int j = 0; j < KT; ++j) {
-      float xh[4], gg[4];
-      xhat_gamma(j, xh, gg);
+      const float4 gm = *reinterpret_cast<const float4*>(gs + z0 + 16 * j + 4 * grp);
+      const float gg[4] = {gm.x, gm.y, gm.z, gm.w};
+      float xh[4];
+      xhat4(i, j + z0, xh);
       float v[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = rs * (acc[j][i][e] * gg[e] - s1 - xh[e] * s2);
+      for (int e = 0; e < 4; ++e) v[e] = rs[i] * (acc[j][i][e] * gg[e] - s1[i] - xh[e] * s2[i]);
       const int64_t c = 16 * j + 4 * grp;
       if (res) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] += to_f32(res[(int64_t)row * ld_res + c + e]);
+        for (int e = 0; e < 4; ++e) v[e] += to_f32(res[row * ld_res + c + e]);
       }
-      TO* o = dx + (int64_t)row * ld_dx + c;
+      TO* o = dx + row * ld_dx + c;
       if (accumulate) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[e] += to_f32(o[e]);
@@ -685,22 +842,7 @@ __global__ void __launch_bounds__(256, 2) dgrad_ln_kernel(const bf16* __restrict
         for (int e = 0; e < 4; ++e) ov[e] = (bf16)v[e];
         *reinterpret_cast<bf16x4*>(o) = ov;
       }
-    }
-  }
-  // the 16 lanes l16 of a row group hold the same channels: sum them
-#pragma unroll
-  for (int j = 0; j < KT; ++j)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      pg[j][e] = group_sum<16>(pg[j][e]);
-      pb[j][e] = group_sum<16>(pb[j][e]);
-    }
-  if (l16 == 0) {
-#pragma unroll
-    for (int j = 0; j < KT; ++j) {
-      const int64_t c = (int64_t)wg * K + 16 * j + 4 * grp;
-      *reinterpret_cast<float4*>(part_g + c) = make_float4(pg[j][0], pg[j][1], pg[j][2], pg[j][3]);
-      *reinterpret_cast<float4*>(part_b + c) = make_float4(pb[j][0], pb[j][1], pb[j][2], pb[j][3]);
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
 }
@@ -1020,7 +1162,6 @@ hipError_t run_linear_backward(const nt_linear_bwd_args& a, void* ws, size_t* by
   // bf16 rows of K in {64, 128, 256, 512}: the LayerNorm passes read 16-byte
   // pieces, K / 8 lanes per row, and partial groups are 64 rows
   const bool vec_ln = !xf && (K == 64 || K == 128 || K == 256 || K == 512) && a.ldx % 8 == 0;
-  const int rpg = vec_ln ? 64 : kRowsPerGroup;
   Carve c{static_cast<char*>(ws)};
   bf16* xn = (ln || xf) ? c.take<bf16>((size_t)R * K) : nullptr;       // LN(x), or x in bf16
   float* mean = ln ? c.take<float>(R) : nullptr;
@@ -1042,10 +1183,12 @@ hipError_t run_linear_backward(const nt_linear_bwd_args& a, void* ws, size_t* by
                            (a.dx || a.dgamma || a.dbeta);
   bf16* wt1 = dgrad_fused ? c.take<bf16>((size_t)K * Nw) : nullptr;         // W^T [K, Nw]
   float* dxn = (direct_dx || dgrad_fused) ? nullptr : c.take<float>((size_t)R * K);
+  // rows per partial group of the LayerNorm and column sums: one wave's rows
+  // in the fused kernel, 64 on the 16-byte LayerNorm passes, else 256
+  const int rpg = dgrad_fused ? 16 * kDgRT : (vec_ln ? 64 : kRowsPerGroup);
   const int groups = (R + rpg - 1) / rpg;
   float* part_g = c.take<float>((size_t)groups * K);
   float* part_b = c.take<float>((size_t)groups * K);
-  float* part_col = c.take<float>((size_t)groups * std::max(Nw, a.c_out));
 
   // weight gradients: dW = g^T LN(x) [Nw, K] and (SwiGLU) dW2 = dy^T h [N, F],
   // on wgrad_kernel where the shape allows, else on the general product
@@ -1064,6 +1207,9 @@ hipError_t run_linear_backward(const nt_linear_bwd_args& a, void* ws, size_t* by
   const bool cs2_fused = wp2.splits && a.dw2 && a.db2;
   float* part_cs = cs_fused ? c.take<float>((size_t)wp.splits * Nw) : nullptr;
   float* part_cs2 = cs2_fused ? c.take<float>((size_t)wp2.splits * a.c_out) : nullptr;
+  // column sums of the bias gradients that the weight-gradient kernel does not give
+  const bool need_col = (a.db && !cs_fused) || (swiglu && a.db2 && !cs2_fused);
+  float* part_col = need_col ? c.take<float>((size_t)groups * std::max(Nw, a.c_out)) : nullptr;
   // second level of the reductions with more than 64 partials
   auto slices = [](int64_t splits) -> size_t { return splits > 64 ? (size_t)((splits + 63) / 64) : 0; };
   const size_t n2 = std::max({slices(groups) * (size_t)std::max(std::max(Nw, a.c_out), K),
@@ -1193,11 +1339,15 @@ hipError_t run_linear_backward(const nt_linear_bwd_args& a, void* ws, size_t* by
     if (ld_g != ld_g_dx) return hipErrorInvalidValue;                       // the plan saw this stride
     if (res && dxf) return hipErrorInvalidValue;                            // the SwiGLU residual is bf16
     transpose_bf16_kernel<<<blocks_for((int64_t)Nw * K), b256, 0, s>>>(W, Nw, K, wt1);
-    const dim3 grid((unsigned)((R + 255) / 256));
+    const dim3 grid((unsigned)((R + kDgRows - 1) / kDgRows));
 #define NT_DGLN(KK, TO)                                                                                        \
-    dgrad_ln_kernel<KK, TO><<<grid, b256, 0, s>>>(g, ld_g, Nw, wt1, (const bf16*)a.x, a.ldx, R, a.ln_gamma, mean, \
+  do {                                                                                                         \
+    (void)hipFuncSetAttribute((const void*)dgrad_ln_kernel<KK, TO>, hipFuncAttributeMaxDynamicSharedMemorySize,   \
+                              (int)(kDgStages * dg_stage_elems<KK>() * sizeof(bf16)));                           \
+    dgrad_ln_kernel<KK, TO><<<grid, b256, kDgStages * dg_stage_elems<KK>() * sizeof(bf16), s>>>(g, ld_g, Nw, wt1, (const bf16*)a.x, a.ldx, R, a.ln_gamma, mean, \
                                                   rstd, (const TO*)res, a.ld_dy, (TO*)a.dx, a.ld_dx,            \
-                                                  a.accumulate_dx, part_g, part_b)
+                                                  a.accumulate_dx, part_g, part_b);                                     \
+  } while (0)
     if (K == 64) { if (dxf) NT_DGLN(64, float); else NT_DGLN(64, bf16); }
     else { if (dxf) NT_DGLN(128, float); else NT_DGLN(128, bf16); }
 #undef NT_DGLN

@@ -172,6 +172,31 @@ def test_layernorm_linear_backward(B, R, K, N, ln, epi, xdt, dxdt):
         check_grad(host(db2), ref["db2"], what + " db2")
 
 
+@pytest.mark.parametrize("K", [64, 128, 136])
+def test_layernorm_linear_backward_without_dx(B, K):
+    """dx not wanted (NULL): the LayerNorm and weight gradients alone, equal
+    to those of a call that also writes dx (fused and general LayerNorm paths)."""
+    import torch
+    R, N = 3001, 256
+    x = _n(83, "x", (R, K), 0.5, "bf16")
+    w = _n(84, "w", (N, K), 1.0 / np.sqrt(K), "bf16")
+    g, be = _n(85, "g", (K,), 0.1, "f32") + 1.0, _n(86, "be", (K,), 0.1, "f32")
+    dy = _n(87, "dy", (R, N), 1.0, "bf16")
+    outs = []
+    for with_dx in (False, True):
+        dw, dg, dbe = (torch.zeros((N, K), device="cuda"), torch.zeros((K,), device="cuda"),
+                       torch.zeros((K,), device="cuda"))
+        dx = torch.empty((R, K), dtype=torch.bfloat16, device="cuda") if with_dx else None
+        B.nt_layernorm_linear_backward(dev(x, "bf16"), dev(w, "bf16"), dev(dy, "bf16"),
+                                       ln=(dev(g, "f32"), dev(be, "f32")), dx=dx, dw=dw, dgamma=dg, dbeta=dbe)
+        outs.append((host(dw), host(dg), host(dbe)))
+    for a, b in zip(outs[0], outs[1]):
+        assert np.array_equal(a, b)
+    ref = G.layernorm_linear_backward(x, w, None, dy, ln=(g, be), xn_store=round_bf16)
+    check_grad(outs[0][1], ref["dgamma"], f"linear backward without dx K={K} dgamma")
+    check_grad(outs[0][2], ref["dbeta"], f"linear backward without dx K={K} dbeta")
+
+
 def test_layernorm_linear_backward_full_size(B):
     """The attention projection of the near-uniform block (364k rows,
     128 -> 388) and a second call that accumulates the weight gradients."""
