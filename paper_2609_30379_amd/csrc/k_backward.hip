@@ -564,21 +564,24 @@ __global__ void __launch_bounds__(256) ln_backward_vec_kernel(const float* __res
 
 // d(LN x) = g W and the LayerNorm backward in one pass (K = 64 or 128
 // channels): g [R, Nw] bf16 (row stride ld_g), W given transposed, wt [K, Nw].
-// A workgroup of four waves owns 128 rows, a wave 32 of them, and computes
-// d(LN x)^T = W^T g^T on matrix cores: per 32-wide step of the contraction
+// A workgroup of eight waves owns 256 rows, a wave 32 of them, and computes
+// d(LN x)^T = W^T g^T on matrix cores.  Per 64-wide step of the contraction
 // it copies the g slice of its rows and the W^T slice into LDS (global ->
-// LDS, in fragment order: each fragment is one contiguous 1 KB read),
-// three stages deep.  A lane ends with K / 4 channels 16 j + 4 grp + e of row
-// 16 i + l16 of each of its wave's two row tiles, so a row's sums are in-lane
-// sums plus two lane-row swaps.  Then, as ln_backward_vec_kernel,
+// LDS; each copy instruction covers whole 128-byte lines of 8 rows, the
+// address unit being the limit with shorter pieces), three stages deep.  In
+// a slice row r keeps its 16-byte chunk c at position c ^ ((r / 2) % 8), so
+// the 16 rows a fragment read spans land on different banks.  A lane ends
+// with K / 4 channels 16 j + 4 grp + e of row 16 i + l16 of each of its
+// wave's two row tiles, so a row's sums are in-lane sums plus two lane-row
+// swaps.  Then, as ln_backward_vec_kernel,
 //   gv = d(LN x) gamma,  xhat = (x - mean) rstd,
 //   dx = rstd (gv - mean(gv) - xhat mean(gv xhat))  (+ res, + dx if accumulating),
 // and the wave's sums of d(LN x) xhat and d(LN x) go to part_g / part_b row
-// (32-row group) blockIdx.x * 4 + wave.  Requires Nw a multiple of 32,
+// (32-row group) blockIdx.x * 8 + wave.  Requires Nw a multiple of 64,
 // ld_g, ldx and the bases 16-byte aligned.
-constexpr int kDgStages = 3, kDgRT = 2;        // stages; row tiles per wave
-constexpr int kDgRows = 4 * 16 * kDgRT;        // rows per workgroup
-template <int K> constexpr int dg_stage_elems() { return kDgRows * 32 + K * 32; }   // g slice + W^T slice
+constexpr int kDgStages = 3, kDgRT = 2, kDgWaves = 8;   // stages; row tiles per wave; waves
+constexpr int kDgRows = kDgWaves * 16 * kDgRT;           // rows per workgroup
+template <int K> constexpr int dg_stage_elems() { return kDgRows * 64 + K * 64; }   // g slice + W^T slice
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 // Sum over the 16 lanes of a DPP row (lanes 16 r .. 16 r + 15): four
@@ -590,9 +593,10 @@ __device__ __forceinline__ float row16_sum(float v) {
   v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x121, 0xf, 0xf, false));   // row_ror:1
   return v;
 }
-// the fragments of one step: KT W^T fragments at aw + 1 KB j, two g
-// fragments at ag, ag + 1 KB; one block with its own LDS wait (the compiler
-// would make plain reads wait for the copies in flight into other stages)
+// the fragments of one 32-wide half step: KT W^T fragments at aw + 2 KB j,
+// two g fragments at ag, ag + 2 KB (16 slice rows of 128 bytes apart); one
+// block with its own LDS wait (the compiler would make plain reads wait for
+// the copies in flight into other stages)
 template <int KT>
 __device__ __forceinline__ void dg_read(uint32_t aw, uint32_t ag, bf16x8 (&wf)[KT], bf16x8 (&gf)[kDgRT]);
 template <>
@@ -600,15 +604,15 @@ __device__ __forceinline__ void dg_read<8>(uint32_t aw, uint32_t ag, bf16x8 (&wf
   u32x4 r[10];
   asm volatile(
       "ds_read_b128 %0, %10\n"
-      "ds_read_b128 %1, %10 offset:1024\n"
-      "ds_read_b128 %2, %10 offset:2048\n"
-      "ds_read_b128 %3, %10 offset:3072\n"
-      "ds_read_b128 %4, %10 offset:4096\n"
-      "ds_read_b128 %5, %10 offset:5120\n"
-      "ds_read_b128 %6, %10 offset:6144\n"
-      "ds_read_b128 %7, %10 offset:7168\n"
+      "ds_read_b128 %1, %10 offset:2048\n"
+      "ds_read_b128 %2, %10 offset:4096\n"
+      "ds_read_b128 %3, %10 offset:6144\n"
+      "ds_read_b128 %4, %10 offset:8192\n"
+      "ds_read_b128 %5, %10 offset:10240\n"
+      "ds_read_b128 %6, %10 offset:12288\n"
+      "ds_read_b128 %7, %10 offset:14336\n"
       "ds_read_b128 %8, %11\n"
-      "ds_read_b128 %9, %11 offset:1024\n"
+      "ds_read_b128 %9, %11 offset:2048\n"
       "s_waitcnt lgkmcnt(0)"
       : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]), "=&v"(r[6]), "=&v"(r[7]),
         "=&v"(r[8]), "=&v"(r[9])
@@ -624,11 +628,11 @@ __device__ __forceinline__ void dg_read<4>(uint32_t aw, uint32_t ag, bf16x8 (&wf
   u32x4 r[6];
   asm volatile(
       "ds_read_b128 %0, %6\n"
-      "ds_read_b128 %1, %6 offset:1024\n"
-      "ds_read_b128 %2, %6 offset:2048\n"
-      "ds_read_b128 %3, %6 offset:3072\n"
+      "ds_read_b128 %1, %6 offset:2048\n"
+      "ds_read_b128 %2, %6 offset:4096\n"
+      "ds_read_b128 %3, %6 offset:6144\n"
       "ds_read_b128 %4, %7\n"
-      "ds_read_b128 %5, %7 offset:1024\n"
+      "ds_read_b128 %5, %7 offset:2048\n"
       "s_waitcnt lgkmcnt(0)"
       : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5])
       : "v"(aw), "v"(ag)
@@ -641,45 +645,53 @@ __device__ __forceinline__ void dg_read<4>(uint32_t aw, uint32_t ag, bf16x8 (&wf
 static_assert(kDgRT == 2, "dg_read reads two g fragments");
 
 template <int K, typename TO>
-__global__ void __launch_bounds__(256, 2) dgrad_ln_kernel(const bf16* __restrict__ g, int64_t ld_g, int Nw,
-                                                          const bf16* __restrict__ wt, const bf16* __restrict__ x,
-                                                          int64_t ldx, int R, const float* __restrict__ gamma,
-                                                          const float* __restrict__ mean,
-                                                          const float* __restrict__ rstd, const TO* __restrict__ res,
-                                                          int64_t ld_res, TO* __restrict__ dx, int64_t ld_dx,
-                                                          int accumulate, float* __restrict__ part_g,
-                                                          float* __restrict__ part_b) {
+__global__ void __launch_bounds__(64 * kDgWaves, 1) dgrad_ln_kernel(
+    const bf16* __restrict__ g, int64_t ld_g, int Nw, const bf16* __restrict__ wt, const bf16* __restrict__ x,
+    int64_t ldx, int R, const float* __restrict__ gamma, const float* __restrict__ mean,
+    const float* __restrict__ rstd, const TO* __restrict__ res, int64_t ld_res, TO* __restrict__ dx, int64_t ld_dx,
+    int accumulate, float* __restrict__ part_g, float* __restrict__ part_b) {
   constexpr int KT = K / 16;
   constexpr int SE = dg_stage_elems<K>();
-  constexpr int NOPS = kDgRT + KT / 4;          // copy instructions per wave per step
+  constexpr int GI = kDgRows / 8 / kDgWaves;    // g copy instructions per wave per step (8 rows each)
+  constexpr int WI = K / 8 / kDgWaves;          // W^T copy instructions per wave per step
+  constexpr int NOPS = GI + WI;
+  static_assert(GI >= 1 && WI >= 1 && K / 8 == WI * kDgWaves, "copies cover the slices");
   extern __shared__ __attribute__((aligned(16))) bf16 dg_lds[];
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l16 = lane & 15, grp = lane >> 4;
   const int rb = blockIdx.x * kDgRows;
-  const int wg = blockIdx.x * 4 + wave;
+  const int wg = blockIdx.x * kDgWaves + wave;
   const int r0 = wg * 16 * kDgRT;
-  const int nks = Nw / 32;
+  const int nks = Nw / 64;
 
-  // copies of step s: the wave's g tiles u (rows 16 u .. of the workgroup)
-  // and W^T tiles v = wave, wave + 4: lane i fetches row (or channel) i % 16,
-  // k-chunk i / 16, so the tile lands in fragment order.  Rows past R are
-  // clamped (they only feed their own discarded outputs).
+  // copies of step s: instruction u covers slice rows 8 u .. 8 u + 7; lane i
+  // fetches row 8 u + i / 8, LDS position i % 8, which holds the row's chunk
+  // (i % 8) ^ ((row / 2) % 8).  Rows past R are clamped (they only feed
+  // their own discarded outputs).
+  const int crow = lane >> 3, cpos = lane & 7;
   auto copy_step = [&](int s) {
     bf16* st = dg_lds + (s % kDgStages) * SE;
 #pragma unroll
-    for (int t = 0; t < kDgRT; ++t) {
-      const int u = kDgRT * wave + t;
-      const bf16* src = g + (int64_t)min(rb + 16 * u + l16, R - 1) * ld_g + 32 * s + 8 * grp;
+    for (int t = 0; t < GI; ++t) {
+      const int u = GI * wave + t, r = 8 * u + crow;
+      const int c = cpos ^ ((r >> 1) & 7);
+      const bf16* src = g + (int64_t)min(rb + r, R - 1) * ld_g + 64 * s + 8 * c;
       __builtin_amdgcn_global_load_lds((const void*)src, (__attribute__((address_space(3))) void*)(st + u * 512), 16,
                                        0, 0);
     }
 #pragma unroll
-    for (int t = 0; t < KT / 4; ++t) {
-      const int v = wave + 4 * t;
-      const bf16* src = wt + (int64_t)(16 * v + l16) * Nw + 32 * s + 8 * grp;
+    for (int t = 0; t < WI; ++t) {
+      const int v = wave + kDgWaves * t, n = 8 * v + crow;
+      const int c = cpos ^ ((n >> 1) & 7);
+      const bf16* src = wt + (int64_t)n * Nw + 64 * s + 8 * c;
       __builtin_amdgcn_global_load_lds((const void*)src,
-                                       (__attribute__((address_space(3))) void*)(st + kDgRows * 32 + v * 512), 16, 0, 0);
+                                       (__attribute__((address_space(3))) void*)(st + kDgRows * 64 + v * 512), 16, 0, 0);
     }
+  };
+  // this lane's fragment offset in a slice for half step h: row (or channel)
+  // l16 of a 16-row tile, chunk 4 h + grp, permuted as stored
+  auto frag_off = [&](int h) -> uint32_t {
+    return (uint32_t)(l16 * 128 + (((4 * h + grp) ^ ((l16 >> 1) & 7)) << 4));
   };
   f32x4 acc[KT][kDgRT];
 #pragma unroll
@@ -691,19 +703,23 @@ __global__ void __launch_bounds__(256, 2) dgrad_ln_kernel(const bf16* __restrict
     if (s < nks) copy_step(s);
   for (int ks = 0; ks < nks; ++ks) {
     // step ks has landed once at most the next step's copies are outstanding
-    static_assert(kDgStages == 3, "the wait below covers one later step");
+    static_assert(kDgStages == 3 && NOPS < 16, "the wait below covers one later step");
     if (ks + 1 < nks) __builtin_amdgcn_s_waitcnt(0x3F70 | NOPS);
     else __builtin_amdgcn_s_waitcnt(0x3F70);
     __builtin_amdgcn_s_barrier();               // all copies of step ks; step ks - 1 read everywhere
     if (ks + kDgStages - 1 < nks) copy_step(ks + kDgStages - 1);
     const uint32_t base =
         (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) bf16*)(dg_lds + (ks % kDgStages) * SE);
-    bf16x8 wf[KT], gf[kDgRT];
-    dg_read<KT>(base + kDgRows * 32 * 2 + lane * 16, base + wave * kDgRT * 1024 + lane * 16, wf, gf);
 #pragma unroll
-    for (int j = 0; j < KT; ++j)
+    for (int h = 0; h < 2; ++h) {
+      const uint32_t off = frag_off(h);
+      bf16x8 wf[KT], gf[kDgRT];
+      dg_read<KT>(base + kDgRows * 128 + off, base + wave * 16 * kDgRT * 128 + off, wf, gf);
 #pragma unroll
-      for (int i = 0; i < kDgRT; ++i) acc[j][i] = mfma16(wf[j], gf[i], acc[j][i]);
+      for (int j = 0; j < KT; ++j)
+#pragma unroll
+        for (int i = 0; i < kDgRT; ++i) acc[j][i] = mfma16(wf[j], gf[i], acc[j][i]);
+    }
   }
   // The ring is free once every wave is past its last read: it now takes
   // the workgroup's x rows and gamma, copied in one burst (global -> LDS).
@@ -715,7 +731,7 @@ __global__ void __launch_bounds__(256, 2) dgrad_ln_kernel(const bf16* __restrict
   __builtin_amdgcn_s_waitcnt(0xC07F);           // lgkmcnt(0)
   __builtin_amdgcn_s_barrier();
   {
-    constexpr int XI = kDgRows * CR / 64 / 4;   // 1 KB copies of x per wave
+    constexpr int XI = kDgRows * CR / 64 / kDgWaves;   // 1 KB copies of x per wave
 #pragma unroll
     for (int t = 0; t < XI; ++t) {
       const int u = wave * XI + t;              // copy u: LDS bytes [1024 u, 1024 u + 1024)
@@ -990,7 +1006,7 @@ __global__ void __launch_bounds__(256) swiglu_backward_kernel(const float* __res
 //   G = Wg LN(x)^T,  U = Wu LN(x)^T,  D = W2^T dy^T
 // so lane (l16, g) holds units 16 t + 4 g + i of row l16; the SwiGLU
 // derivative is applied in registers (the same fp32 formulas as the unfused
-// path) and h, d g, d u are stored as 8-byte pieces.  The workgroups of one
+// path) and h, d g, d u are stored as 16-byte pieces after a lane-row swap.  The workgroups of one
 // row block run on one XCD, so its rows are read from HBM once.
 constexpr int kSgRT = 64;                     // row tiles (of 16) per workgroup
 
@@ -1055,6 +1071,7 @@ __global__ void __launch_bounds__(256, 4) swiglu_backward_fused_kernel(const bf1
     // lane offset keeps the compiler from holding all of them in registers
     int lo = lane * 8;
     asm volatile("" : "+v"(lo));
+    uint32_t ow[3][4][2];                       // [h, d g, d u][unit tile t] as packed bf16 pairs
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       f32x4 G = {0.f, 0.f, 0.f, 0.f}, U = G, D = G;
@@ -1077,14 +1094,40 @@ __global__ void __launch_bounds__(256, 4) swiglu_backward_fused_kernel(const bf1
         go[i] = (bf16)(d * uv * sg * (1.f + gv * (1.f - sg)));
         uo[i] = (bf16)(d * silu);
       }
-      // a lane past R computed row R - 1 (its input row was clamped) and
-      // stores those same values there: no divergent branch, so the waits
-      // for the next tile's rows stay exact
-      const int f = u0 + 16 * t + 4 * g;
-      const int64_t ro = min(row, R - 1);
-      *reinterpret_cast<bf16x4*>(h + ro * F + f) = ho;
-      *reinterpret_cast<bf16x4*>(dp + ro * 2 * F + f) = go;
-      *reinterpret_cast<bf16x4*>(dp + ro * 2 * F + F + f) = uo;
+      const uint2 a = __builtin_bit_cast(uint2, ho), b = __builtin_bit_cast(uint2, go),
+                  c = __builtin_bit_cast(uint2, uo);
+      ow[0][t][0] = a.x; ow[0][t][1] = a.y;
+      ow[1][t][0] = b.x; ow[1][t][1] = b.y;
+      ow[2][t][0] = c.x; ow[2][t][1] = c.y;
+    }
+    // lane (l16, g) holds units 16 t + 4 g .. + 3 of row l16.  Lane-row
+    // groups g, g ^ 1 trade the pieces of tiles t, t + 1 (t even) so that an
+    // even g holds units 16 t + 4 g .. + 7 and an odd g units
+    // 16 (t + 1) + 4 (g - 1) .. + 7: one 16-byte store per lane and tile pair,
+    // the four lane groups of a row writing 64 contiguous bytes (the address
+    // unit is charged per line an instruction touches).
+#pragma unroll
+    for (int o = 0; o < 3; ++o)
+#pragma unroll
+      for (int t = 0; t < 4; t += 2)
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const auto sw = __builtin_amdgcn_permlane16_swap(ow[o][t][e], ow[o][t + 1][e], false, false);
+          ow[o][t][e] = sw[0];
+          ow[o][t + 1][e] = sw[1];
+        }
+    // a lane past R computed row R - 1 (its input row was clamped) and
+    // stores those same values there: no divergent branch, so the waits
+    // for the next tile's rows stay exact
+    const int64_t ro = min(row, R - 1);
+#pragma unroll
+    for (int t = 0; t < 4; t += 2) {
+      const int f = u0 + 16 * t + ((g & 1) ? 16 + 4 * (g - 1) : 4 * g);
+      *reinterpret_cast<uint4*>(h + ro * F + f) = make_uint4(ow[0][t][0], ow[0][t][1], ow[0][t + 1][0], ow[0][t + 1][1]);
+      *reinterpret_cast<uint4*>(dp + ro * 2 * F + f) =
+          make_uint4(ow[1][t][0], ow[1][t][1], ow[1][t + 1][0], ow[1][t + 1][1]);
+      *reinterpret_cast<uint4*>(dp + ro * 2 * F + F + f) =
+          make_uint4(ow[2][t][0], ow[2][t][1], ow[2][t + 1][0], ow[2][t + 1][1]);
     }
   }
 }
@@ -1179,7 +1222,7 @@ hipError_t run_linear_backward(const nt_linear_bwd_args& a, void* ws, size_t* by
   // LayerNorm on bf16 rows of 64 or 128: d(LN x) = g W and the LayerNorm
   // backward in one kernel (no fp32 d(LN x) in memory)
   const int64_t ld_g_dx = (gelu || swiglu) ? Nw : a.ld_dy;
-  const bool dgrad_fused = ln && vec_ln && (K == 64 || K == 128) && Nw % 32 == 0 && ld_g_dx % 8 == 0 &&
+  const bool dgrad_fused = ln && vec_ln && (K == 64 || K == 128) && Nw % 64 == 0 && ld_g_dx % 8 == 0 &&
                            (a.dx || a.dgamma || a.dbeta);
   bf16* wt1 = dgrad_fused ? c.take<bf16>((size_t)K * Nw) : nullptr;         // W^T [K, Nw]
   float* dxn = (direct_dx || dgrad_fused) ? nullptr : c.take<float>((size_t)R * K);
@@ -1339,12 +1382,12 @@ hipError_t run_linear_backward(const nt_linear_bwd_args& a, void* ws, size_t* by
     if (ld_g != ld_g_dx) return hipErrorInvalidValue;                       // the plan saw this stride
     if (res && dxf) return hipErrorInvalidValue;                            // the SwiGLU residual is bf16
     transpose_bf16_kernel<<<blocks_for((int64_t)Nw * K), b256, 0, s>>>(W, Nw, K, wt1);
-    const dim3 grid((unsigned)((R + kDgRows - 1) / kDgRows));
+    const dim3 grid((unsigned)((R + kDgRows - 1) / kDgRows)), bdg(64 * kDgWaves);
 #define NT_DGLN(KK, TO)                                                                                        \
   do {                                                                                                         \
     (void)hipFuncSetAttribute((const void*)dgrad_ln_kernel<KK, TO>, hipFuncAttributeMaxDynamicSharedMemorySize,   \
                               (int)(kDgStages * dg_stage_elems<KK>() * sizeof(bf16)));                           \
-    dgrad_ln_kernel<KK, TO><<<grid, b256, kDgStages * dg_stage_elems<KK>() * sizeof(bf16), s>>>(g, ld_g, Nw, wt1, (const bf16*)a.x, a.ldx, R, a.ln_gamma, mean, \
+    dgrad_ln_kernel<KK, TO><<<grid, bdg, kDgStages * dg_stage_elems<KK>() * sizeof(bf16), s>>>(g, ld_g, Nw, wt1, (const bf16*)a.x, a.ldx, R, a.ln_gamma, mean, \
                                                   rstd, (const TO*)res, a.ld_dy, (TO*)a.dx, a.ld_dx,            \
                                                   a.accumulate_dx, part_g, part_b);                                     \
   } while (0)
