@@ -48,10 +48,10 @@ F32_PEAK_TFLOPS = 157.3        # fp32 vector
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 COUNTERS = {  # workload: {op: (kernel source, source hash, FETCH_SIZE KiB, WRITE_SIZE KiB)}
     "pairformer4_b16_lognormal192_bf16": {
-        "attention_row": ("k_attention.hip", "fb1580cc3df1ec1d", 324779 + 8058, 216030 + 6472),
-        "attention_col": ("k_attention.hip", "fb1580cc3df1ec1d", 324779 + 8058, 216030 + 6472),
-        "triangle_out": ("k_triangle.hip", "78ed89d0163e3191", 696154, 177229),
-        "triangle_in": ("k_triangle.hip", "78ed89d0163e3191", 696154, 177229),
+        "attention_row": ("k_attention.hip", "1029ede52508d9db", 321692 + 8058, 174370 + 6472),
+        "attention_col": ("k_attention.hip", "1029ede52508d9db", 321692 + 8058, 174370 + 6472),
+        "triangle_out": ("k_triangle.hip", "78ed89d0163e3191", 640247, 175968),
+        "triangle_in": ("k_triangle.hip", "78ed89d0163e3191", 640247, 175968),
         "transition": ("k_transition.hip", "e2f701d5925d7f6e", 100338 + 268, 174430 + 384),
         "attn_proj": ("k_linear.hip", "4daf048772e304da", 87689, 528972),
         "tri_proj": ("k_linear.hip", "4daf048772e304da", 87863, 386304),

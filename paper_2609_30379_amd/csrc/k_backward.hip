@@ -2,18 +2,30 @@
 // LayerNorm on each row's features) for a training step (Sec. 3.4).
 //
 // Pieces, each one launch over all rows:
-//   * ln_rows_kernel          LN(x) in bf16 (what the forward product consumed)
+//   * ln_rows_kernel / ln_rows_vec_kernel
+//                             LN(x) in bf16 (what the forward product consumed)
 //                             and each row's mean and 1/std;
-//   * gemm_bf16_kernel        C (+)= op(A) op(B), bf16 operands from memory,
-//                             fp32 accumulation on matrix cores, 64 x 64 tiles,
-//                             optional split of the contraction into partial
-//                             sums (the weight gradients reduce over all rows);
-//   * gelu / swiglu backward  elementwise, on the recomputed pre-activations;
-//   * ln_backward_kernel      dx from d(LN(x)), with per-workgroup partial sums
-//                             of dgamma and dbeta;
-//   * column_sum / partials   bias gradients and the reduction of partials.
-// Partial sums are written per workgroup and reduced in a fixed order, so
-// every gradient is deterministic.
+//   * swiglu_backward_fused_kernel
+//                             (SwiGLU, K = N in {64, 128}) the recomputed gate
+//                             and up products, d h = dy W2 and the SwiGLU
+//                             derivative in one pass: h and d[g | u];
+//   * wgrad_kernel            weight gradients g^T LN(x) and dy^T h, summed
+//                             over row ranges (copy ring into LDS, transpose
+//                             reads), with the bias gradient as the column sums
+//                             of g from the same fragments;
+//   * dgrad_ln_kernel         (LayerNorm, K in {64, 128}) d(LN x) = g W and the
+//                             LayerNorm backward, with per-wave partial sums of
+//                             dgamma and dbeta;
+//   * gemm_bf16_kernel        the general product C (+)= op(A) op(B) (64 x 64
+//                             tiles, split contraction) for the other shapes;
+//   * gelu / swiglu backward  elementwise, on recomputed pre-activations
+//                             (shapes the fused kernels do not take);
+//   * ln_backward_kernel      dx from d(LN x) on the general path, with
+//                             per-group partial sums of dgamma and dbeta;
+//   * column partials         bias gradients the weight-gradient kernel does not
+//                             give; the reductions of all partial sums.
+// Partial sums are written per workgroup, wave or row range and reduced in a
+// fixed order, so every gradient is deterministic.
 #include <algorithm>
 
 #include "nt_device.h"
@@ -1258,6 +1270,11 @@ hipError_t run_linear_backward(const nt_linear_bwd_args& a, void* ws, size_t* by
   const size_t n2 = std::max({slices(groups) * (size_t)std::max(std::max(Nw, a.c_out), K),
                               slices(sw) * (size_t)Nw * K, slices(sw2) * (size_t)a.c_out * F});
   float* part2 = c.take<float>(std::max<size_t>(n2, 1));
+  // third level and beyond (ping-pong with part2): at most 1/64 of part2
+  auto slices2 = [&](int64_t splits) -> size_t { return slices((int64_t)slices(splits)); };
+  const size_t n3 = std::max({slices2(groups) * (size_t)std::max(std::max(Nw, a.c_out), K),
+                              slices2(sw) * (size_t)Nw * K, slices2(sw2) * (size_t)a.c_out * F});
+  float* part3 = c.take<float>(std::max<size_t>(n3, 1));
   *bytes = c.used;
   if (!launch) return hipSuccess;
 
@@ -1266,15 +1283,21 @@ hipError_t run_linear_backward(const nt_linear_bwd_args& a, void* ws, size_t* by
   const int acc_w = a.overwrite_weights ? 0 : 1;
   const dim3 b256(256);
   // out (+)= sum over `splits` partials (stride apart) of n values, in a fixed
-  // order: through part2 when there are more than 64 partials
+  // order: while more than 64 remain, each 64 of them are summed into one
+  // (reduce_level1_kernel, alternately into part2 and part3), then the rest
   auto reduce_parts = [&](const float* part, int splits, int64_t stride, int64_t n, float* out) {
-    if (splits > 64) {
+    float* bufs[2] = {part2, part3};
+    int b = 0;
+    while (splits > 64) {
       const int sl = (splits + 63) / 64;
-      reduce_level1_kernel<<<dim3((unsigned)((n + 63) / 64), (unsigned)sl), b256, 0, s>>>(part, splits, stride, n, part2);
-      reduce_partials_kernel<<<blocks_for(n), b256, 0, s>>>(part2, sl, n, n, out, acc_w);
-    } else {
-      reduce_partials_kernel<<<blocks_for(n), b256, 0, s>>>(part, splits, stride, n, out, acc_w);
+      reduce_level1_kernel<<<dim3((unsigned)((n + 63) / 64), (unsigned)sl), b256, 0, s>>>(part, splits, stride, n,
+                                                                                         bufs[b]);
+      part = bufs[b];
+      stride = n;
+      splits = sl;
+      b ^= 1;
     }
+    reduce_partials_kernel<<<blocks_for(n), b256, 0, s>>>(part, splits, stride, n, out, acc_w);
   };
   // column sums of a bf16 [R, N] matrix into part_col (groups of rpg rows)
   auto column_parts = [&](const bf16* X, int64_t ld, int N) {
