@@ -213,20 +213,43 @@ __global__ void __launch_bounds__(kTwThreads, 1) transition_wide_kernel(TransArg
                             b2.z + __uint_as_float(rr.y << 16), b2.w + __uint_as_float(rr.y & 0xffff0000u)};
       }
   };
+  // Lane (l16, g) holds channels 16 a + 4 g .. + 3 of row l16.  Lane-row
+  // groups g, g ^ 1 trade the pieces of tiles a, a + 1 (a even), so that an
+  // even g holds channels 16 a + 4 g .. + 7 and an odd g 16 (a + 1) +
+  // 4 (g - 1) .. + 7: one 16-byte store per lane and tile pair, the four lane
+  // groups of a row writing 64 contiguous bytes (the address unit is charged
+  // per line a store instruction touches).
   auto store_out = [&](int ps) __attribute__((always_inline)) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       const int64_t m = (int64_t)ps * kTwRows + (wave * MT + mt) * 16 + l16;
-      if (m >= p.rows) continue;
+      uint32_t ow[NT][2];
 #pragma unroll
       for (int a = 0; a < NT; ++a) {
         bf16x4 o;
 #pragma unroll
         for (int i = 0; i < 4; ++i) o[i] = (bf16)accY[a][mt][i];
-        *reinterpret_cast<bf16x4*>(p.y + m * p.ldy + a * 16 + 4 * g) = o;
+        const uint2 u = __builtin_bit_cast(uint2, o);
+        ow[a][0] = u.x;
+        ow[a][1] = u.y;
+      }
+#pragma unroll
+      for (int a = 0; a < NT; a += 2)
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const auto sw = __builtin_amdgcn_permlane16_swap(ow[a][e], ow[a + 1][e], false, false);
+          ow[a][e] = sw[0];
+          ow[a + 1][e] = sw[1];
+        }
+      if (m >= p.rows) continue;
+#pragma unroll
+      for (int a = 0; a < NT; a += 2) {
+        const int c = 16 * a + ((g & 1) ? 16 + 4 * (g - 1) : 4 * g);
+        *reinterpret_cast<uint4*>(p.y + m * p.ldy + c) = make_uint4(ow[a][0], ow[a][1], ow[a + 1][0], ow[a + 1][1]);
       }
     }
   };
+  static_assert(NT % 2 == 0, "tiles pair up for the 16-byte stores");
 
   // gate and up biases of the chunk at hidden offset f0: slot j = 4 ft + i of
   // lane group g is hidden unit f0 + 8g + j.  Read with inline assembly and
