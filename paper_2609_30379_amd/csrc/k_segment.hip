@@ -27,10 +27,13 @@ pair_broadcast_kernel(const int32_t* __restrict__ row_sample, const int32_t* __r
   const int cv = C / VE;                       // vector chunks per cell
   const T* urow = u + (int64_t)eta * ld_u;
   const T* vblk = v + (int64_t)k0 * ld_v;
-  if (256 % cv == 0) {
-    // every thread owns one fixed chunk of channels; u is loaded once
+  if (cv <= 256) {
+    // every thread owns one fixed chunk of channels (the first 256 / cv * cv
+    // threads take part); u is loaded once
+    const int bstep = 256 / cv;
+    if ((int)threadIdx.x >= bstep * cv) return;
     const int ch = (threadIdx.x % cv) * VE;
-    const int b0 = threadIdx.x / cv, bstep = 256 / cv;
+    const int b0 = threadIdx.x / cv;
     Vec<T> uu;
     uu.load(urow + ch);
     for (int b = b0; b < n; b += bstep) {
@@ -155,6 +158,25 @@ segment_reduce_backward_kernel(int level, const int32_t* __restrict__ row_sample
   }
   const int a = eta - s0;
   const int64_t cell0 = (int64_t)cu_pairs[i] + (int64_t)a * n;
+  if (level == NT_LEVEL_PAIRS && cv <= 256) {
+    // the whole pair row takes dy[eta]: every thread owns one fixed chunk of
+    // channels (the first 256 / cv * cv threads), loaded once
+    const int bstep = 256 / cv;
+    if ((int)threadIdx.x >= bstep * cv) return;
+    const int ch = (threadIdx.x % cv) * VE;
+    float gv[VE];
+#pragma unroll
+    for (int j = 0; j < VE; ++j) gv[j] = dy[(int64_t)(s0 + a) * ld_dy + ch + j] * scale;
+    for (int b = threadIdx.x / cv; b < n; b += bstep) {
+      T* dst = dx + (cell0 + b) * ld_dx + ch;
+      Vec<T> out;
+      if (accumulate) out.load(dst);
+#pragma unroll
+      for (int j = 0; j < VE; ++j) out.v[j] = (accumulate ? out.v[j] : 0.f) + gv[j];
+      out.store(dst);
+    }
+    return;
+  }
   const int total = n * cv;
   for (int t = threadIdx.x; t < total; t += 256) {
     const int b = t / cv, ch = (t - b * cv) * VE;
