@@ -197,13 +197,13 @@ segment_reduce_backward_kernel(int level, const int32_t* __restrict__ row_sample
 // Rows of sample i are [off[i], off[i+1]) (singles: eta, pairs: o).  Grid
 // (B, CH): chunk c takes an equal share of the sample's rows; partial sums are
 // reduced per sample in a fixed order by loss_finish_kernel.
-constexpr int kLossChunks = 64;
+constexpr int kLossChunks = 256;   // workgroups per sample: enough loads in flight on a batch of 8
 
 template <typename T, typename TO>
 __global__ void __launch_bounds__(256)
 weighted_sq_kernel(const int32_t* __restrict__ off, int C, const T* __restrict__ x, int64_t ld_x,
                    const float* __restrict__ w, float scale, float* __restrict__ part, TO* __restrict__ dx,
-                   int64_t ld_dx) {
+                   int64_t ld_dx, int dx_vec) {
   constexpr int VE = Vec<T>::N;
   __shared__ float red[4];
   const int i = blockIdx.x, c = blockIdx.y;
@@ -212,22 +212,37 @@ weighted_sq_kernel(const int32_t* __restrict__ off, int C, const T* __restrict__
   const int cv = C / VE;
   const float g = 2.f * scale * w[i];
   float acc = 0.f;
-  for (int64_t e = threadIdx.x; e < (b - a) * cv; e += 256) {
-    const int64_t r = a + e / cv;
-    const int ch = (int)(e % cv) * VE;
+  // one chunk of VE channels: its squares, and dx = g x (one vector store
+  // when dx_vec: dx and its row stride 16-byte aligned)
+  auto chunk = [&](int64_t r, int ch) {
     Vec<T> t;
     t.load(x + r * ld_x + ch);
-    Vec<TO> d;
 #pragma unroll
     for (int j = 0; j < VE; ++j) acc = fmaf(t.v[j], t.v[j], acc);
-    if (dx) {
+    if (!dx) return;
+    TO* o = dx + r * ld_dx + ch;
+    if (dx_vec) {
+      if constexpr (sizeof(TO) == 4) {
 #pragma unroll
-      for (int j = 0; j < VE; ++j) {
-        TO* o = dx + r * ld_dx + ch + j;
-        *o = from_f32<TO>(g * t.v[j]);
+        for (int j = 0; j < VE; j += 4)
+          *reinterpret_cast<float4*>(o + j) = make_float4(g * t.v[j], g * t.v[j + 1], g * t.v[j + 2], g * t.v[j + 3]);
+      } else if constexpr (VE == 8) {
+        bf16x8 v;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = (bf16)(g * t.v[j]);
+        *reinterpret_cast<bf16x8*>(o) = v;
+      } else {
+        bf16x4 v;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = (bf16)(g * t.v[j]);
+        *reinterpret_cast<bf16x4*>(o) = v;
       }
+    } else {
+#pragma unroll
+      for (int j = 0; j < VE; ++j) o[j] = from_f32<TO>(g * t.v[j]);
     }
-  }
+  };
+  for (int64_t e = threadIdx.x; e < (b - a) * cv; e += 256) chunk(a + e / cv, (int)(e % cv) * VE);
   for (int m = 32; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, 64);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
   __syncthreads();
@@ -253,8 +268,10 @@ hipError_t launch_weighted_square_loss(const nt_layout& L, nt_level level, int C
   const int32_t* off = level == NT_LEVEL_PAIRS ? L.d_cu_pairs : L.d_cu_seqlens;
   float* part = static_cast<float*>(workspace);
   const dim3 grid((unsigned)L.batch, kLossChunks);
+  const size_t eo = dx_dtype == NT_BF16 ? 2 : 4;
+  const int dx_vec = dx && (reinterpret_cast<uintptr_t>(dx) % 16 == 0) && ((size_t)ld_dx * eo) % 16 == 0;
 #define NT_LOSS(T, TO) weighted_sq_kernel<T, TO><<<grid, dim3(256), 0, s>>>(off, C, (const T*)x, ld_x, w, scale, part, \
-                                                                            (TO*)dx, ld_dx)
+                                                                            (TO*)dx, ld_dx, dx_vec)
   if (dtype == NT_BF16) { if (dx_dtype == NT_BF16) NT_LOSS(bf16, bf16); else NT_LOSS(bf16, float); }
   else { if (dx_dtype == NT_BF16) NT_LOSS(float, bf16); else NT_LOSS(float, float); }
 #undef NT_LOSS

@@ -301,3 +301,35 @@ def test_rectangular_pair_ops(B, dtype, C):
     # square-only calls reject rectangular layouts
     with pytest.raises(B.NtError):
         B.nt_triangle_mul(lay, 0, z, z, z)
+
+
+# ------------------------------------------------------------------ diagnostic loss
+@pytest.mark.parametrize("level", ["pairs", "singles"])
+@pytest.mark.parametrize("xdt,dxdt,C,pad", [("bf16", "bf16", 128, 0), ("bf16", "f32", 384, 0), ("f32", "f32", 128, 0),
+                                            ("f32", "bf16", 64, 0), ("bf16", "bf16", 384, 2), ("f32", "f32", 16, 1),
+                                            ("bf16", "bf16", 2056, 0)])
+def test_weighted_square_loss(B, level, xdt, dxdt, C, pad):
+    """One term of the joint diagnostic loss and its gradient (App. A), on
+    16-byte aligned gradient rows (vector stores) and on padded rows (element
+    stores), for narrow and wide rows."""
+    import torch
+    L = LSETS["ragged"] if C <= 384 else [5, 0, 1, 37, 3]
+    lay = B.NestedLayout(L)
+    rows = sum(n * n for n in L) if level == "pairs" else sum(L)
+    x = _n(90, "x", (rows, C), 0.7, xdt)
+    w = np.linspace(0.5, 2.0, len(L))
+    loss = torch.full((len(L),), float("nan"), device="cuda")
+    tdt = torch.bfloat16 if dxdt == "bf16" else torch.float32
+    dx_full = torch.full((rows, C + pad), float("nan"), dtype=tdt, device="cuda")
+    dx = dx_full[:, :C]
+    B.nt_weighted_square_loss(lay, level, dev(x, xdt), torch.tensor(w, dtype=torch.float32, device="cuda"), 0.25,
+                              loss, dx=dx)
+    counts = [n * n for n in L] if level == "pairs" else L
+    ref_loss, ref_g = O.weighted_square_loss(x, counts, w, 0.25)
+    what = f"loss {level} x={xdt} dx={dxdt} C={C} pad={pad}"
+    got = host(loss)
+    assert np.allclose(got, ref_loss, rtol=1e-4, atol=1e-6), (what, got, ref_loss)
+    # dx = 2 scale w x: one rounding to dx's dtype
+    check(host(dx), ref_g, dxdt, what + " dx")
+    if pad:
+        assert torch.isnan(dx_full[:, C:]).all(), what + ": padding written"
