@@ -912,9 +912,12 @@ constexpr int kWaveGroup = 8;                     // column tiles per product gr
 constexpr int kWaveMaxGroups = 4;                 // main columns up to 512
 constexpr int kWaveMaxTail = 2;                   // channel-major tail up to 32 channels
 
-// residual epilogues stage fp32 values; the others bf16
+// residual epilogues stage fp32 values; the others bf16.  Row strides of
+// 132 floats and 136 bf16 put rows 4 banks apart (mod 64): the 8-byte writes
+// of 16 rows x 2 lane groups and the 16-byte write-back reads of a row both
+// fall on distinct banks
 template <int EPI> constexpr bool wave_res() { return EPI == NT_EPI_RESIDUAL || EPI == NT_EPI_GATED_RESIDUAL; }
-template <int EPI> constexpr int wave_stage_stride() { return wave_res<EPI>() ? 132 : 144; }
+template <int EPI> constexpr int wave_stage_stride() { return wave_res<EPI>() ? 132 : 136; }
 template <int EPI> constexpr int wave_stage_bytes() {
   return 16 * wave_stage_stride<EPI>() * (wave_res<EPI>() ? 4 : 2);
 }
