@@ -1153,6 +1153,15 @@ __global__ void __launch_bounds__(256) transpose_bf16_kernel(const bf16* __restr
   at[(int64_t)c * rows + r] = a[e];
 }
 
+// fp32 rows [R, K] (contiguous) -> bf16 rows ld apart, one thread per element.
+__global__ void __launch_bounds__(256) to_bf16_rows_kernel(const float* __restrict__ x, int R, int K,
+                                                           bf16* __restrict__ y, int64_t ld) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e >= (int64_t)R * K) return;
+  const int64_t r = e / K, c = e % K;
+  y[r * ld + c] = (bf16)x[e];
+}
+
 // fp32 matrix [R, N] -> bf16 (row stride N).
 __global__ void __launch_bounds__(256) to_bf16_kernel(const float* __restrict__ x, int64_t n, bf16* __restrict__ y) {
   const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -1447,9 +1456,9 @@ hipError_t run_linear_backward(const nt_linear_bwd_args& a, void* ws, size_t* by
     if (a.dgamma) reduce_parts(part_g, groups, K, K, a.dgamma);
     if (a.dbeta) reduce_parts(part_b, groups, K, K, a.dbeta);
   } else if (a.dx) {
-    // no LayerNorm, bf16 dx = d(LN x)
+    // no LayerNorm, bf16 dx = d(LN x), rows ld_dx apart
     if (a.accumulate_dx || res) return hipErrorInvalidValue;
-    to_bf16_kernel<<<blocks_for((int64_t)R * K), b256, 0, s>>>(dxn, (int64_t)R * K, (bf16*)a.dx);
+    to_bf16_rows_kernel<<<blocks_for((int64_t)R * K), b256, 0, s>>>(dxn, R, K, (bf16*)a.dx, a.ld_dx);
   }
   return hipGetLastError();
 }

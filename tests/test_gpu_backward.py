@@ -197,6 +197,50 @@ def test_layernorm_linear_backward_without_dx(B, K):
     check_grad(outs[0][2], ref["dbeta"], f"linear backward without dx K={K} dbeta")
 
 
+@pytest.mark.parametrize("epi,K,N,ln", [("swiglu_residual", 128, 128, True), ("none", 128, 256, True),
+                                        ("none", 64, 128, True), ("gelu", 128, 384, False)])
+def test_layernorm_linear_backward_strided(B, epi, K, N, ln):
+    """x, dy and dx as column views of wider buffers (row strides K + 8, N + 16,
+    K + 24): the weight-gradient kernel reads strided operands, the fused
+    SwiGLU and d(LN x) kernels strided rows; padding is never written."""
+    import torch
+    R = 4099
+    F = 4 * K if epi == "swiglu_residual" else 0
+    Nw = 2 * F if F else N
+    x = _n(100, "x", (R, K), 0.5, "bf16")
+    w = _n(101, "w", (Nw, K), 1.0 / np.sqrt(K), "bf16")
+    b = _n(102, "b", (Nw,), 0.1, "f32")
+    g, be = _n(103, "g", (K,), 0.1, "f32") + 1.0, _n(104, "be", (K,), 0.1, "f32")
+    w2 = _n(105, "w2", (N, F), 0.5 / np.sqrt(F), "bf16") if F else None
+    dy = _n(106, "dy", (R, N), 1.0, "bf16")
+    xw = torch.zeros((R, K + 8), dtype=torch.bfloat16, device="cuda")
+    xw[:, :K] = dev(x, "bf16")
+    dyw = torch.zeros((R, N + 16), dtype=torch.bfloat16, device="cuda")
+    dyw[:, :N] = dev(dy, "bf16")
+    dxw = torch.full((R, K + 24), float("nan"), dtype=torch.bfloat16, device="cuda")
+    dw, db = torch.zeros((Nw, K), device="cuda"), torch.zeros((Nw,), device="cuda")
+    dg, dbe = torch.zeros((K,), device="cuda"), torch.zeros((K,), device="cuda")
+    dw2 = torch.zeros((N, F), device="cuda") if F else None
+    db2 = torch.zeros((N,), device="cuda") if F else None
+    B.nt_layernorm_linear_backward(xw[:, :K], dev(w, "bf16"), dyw[:, :N],
+                                   ln=(dev(g, "f32"), dev(be, "f32")) if ln else None, bias=dev(b, "f32"),
+                                   epilogue=epi, w2=dev(w2, "bf16") if F else None, hidden=F, dx=dxw[:, :K], dw=dw,
+                                   db=db, dgamma=dg if ln else None, dbeta=dbe if ln else None, dw2=dw2, db2=db2)
+    ref = G.layernorm_linear_backward(x, w, b, dy, ln=(g, be) if ln else None, epilogue=epi, w2=w2,
+                                      xn_store=round_bf16, h_store=round_bf16)
+    what = f"strided linear backward {R}x{K}->{N} {epi}"
+    check_grad(host(dxw[:, :K]), ref["dx"], what + " dx")
+    check_grad(host(dw), ref["dw"], what + " dw")
+    check_grad(host(db), ref["db"], what + " db")
+    if ln:
+        check_grad(host(dg), ref["dgamma"], what + " dgamma")
+        check_grad(host(dbe), ref["dbeta"], what + " dbeta")
+    if F:
+        check_grad(host(dw2), ref["dw2"], what + " dw2")
+        check_grad(host(db2), ref["db2"], what + " db2")
+    assert torch.isnan(dxw[:, K:]).all(), what + ": padding of dx written"
+
+
 def test_layernorm_linear_backward_full_size(B):
     """The attention projection of the near-uniform block (364k rows,
     128 -> 388) and a second call that accumulates the weight gradients."""
