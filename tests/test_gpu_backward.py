@@ -130,6 +130,9 @@ LIN_BWD = [
     (300, 128, 384, False, "residual", "f32", "f32"),   # single update from an fp32 column mean
     (130, 136, 40, True, "none", "f32", "bf16"),
     (70001, 128, 256, True, "none", "bf16", "bf16"),   # weight gradient over 244 row ranges, 17-row tail
+    (7, 128, 128, True, "swiglu_residual", "bf16", "bf16"),   # fewer rows than one tile / one 32-row step
+    (9, 128, 256, True, "none", "bf16", "f32"),
+    (5, 64, 128, True, "none", "bf16", "bf16"),
 ]
 
 
