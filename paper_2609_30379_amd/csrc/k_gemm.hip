@@ -39,6 +39,37 @@ __device__ __forceinline__ int swz(int row, int piece) { return piece ^ ((row >>
 
 __device__ __forceinline__ float gelu_exact(float v) { return 0.5f * v * (1.f + erff(v * 0.70710678118654752f)); }
 
+typedef uint32_t g_u32x4 __attribute__((ext_vector_type(4)));
+// The fragments of one k-step: eight weight fragments at aw + 1 KB i and four
+// row fragments at ax + 1 KB j (16 staged rows of 64 bytes apart), in one
+// block with its own LDS wait: as plain loads the compiler would make them
+// wait for the copies still in flight into the other stages.
+__device__ __forceinline__ void gemm_frags(uint32_t aw, uint32_t ax, bf16x8 (&w)[8], bf16x8 (&x)[4]) {
+  g_u32x4 r[12];
+  asm volatile(
+      "ds_read_b128 %0, %12\n"
+      "ds_read_b128 %1, %12 offset:1024\n"
+      "ds_read_b128 %2, %12 offset:2048\n"
+      "ds_read_b128 %3, %12 offset:3072\n"
+      "ds_read_b128 %4, %12 offset:4096\n"
+      "ds_read_b128 %5, %12 offset:5120\n"
+      "ds_read_b128 %6, %12 offset:6144\n"
+      "ds_read_b128 %7, %12 offset:7168\n"
+      "ds_read_b128 %8, %13\n"
+      "ds_read_b128 %9, %13 offset:1024\n"
+      "ds_read_b128 %10, %13 offset:2048\n"
+      "ds_read_b128 %11, %13 offset:3072\n"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]), "=&v"(r[6]), "=&v"(r[7]),
+        "=&v"(r[8]), "=&v"(r[9]), "=&v"(r[10]), "=&v"(r[11])
+      : "v"(aw), "v"(ax)
+      : "memory");
+#pragma unroll
+  for (int i = 0; i < 8; ++i) w[i] = __builtin_bit_cast(bf16x8, r[i]);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) x[j] = __builtin_bit_cast(bf16x8, r[8 + j]);
+}
+
 __global__ void __launch_bounds__(kGThreads, 1) gemm_kernel(GemmArgs p) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   bf16* ring = reinterpret_cast<bf16*>(smem);
@@ -83,30 +114,29 @@ __global__ void __launch_bounds__(kGThreads, 1) gemm_kernel(GemmArgs p) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // this lane's byte offset inside a 16-row fragment block: row l16, piece g
+  // at its swizzled place (the swizzle depends only on l16, since fragment
+  // blocks start at multiples of 16 rows)
+  const uint32_t lofs = (uint32_t)(l16 * kGBK * 2 + (swz(l16, g) << 4));
   for (int kt = 0; kt < nk; ++kt) {
     // stage kt has landed for this wave (later stages may still be in flight)
     if (kt + 2 < nk) __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8) | 8);   // vmcnt(8)
     else if (kt + 1 < nk) __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8) | 4);  // vmcnt(4)
     else __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8) | 0);
-    __syncthreads();                              // stage kt complete; slot (kt - 1) % 4 free
+    // stage kt complete everywhere and slot (kt - 1) % 4 free (every wave's
+    // reads of it ended in an LDS wait).  The plain barrier: __syncthreads
+    // would also wait for the copies still in flight, leaving no lookahead.
+    __builtin_amdgcn_s_barrier();
     if (kt + kGStages - 1 < nk) copy_stage(kt + kGStages - 1, (kt + kGStages - 1) % kGStages);
-    bf16* st = ring + (kt % kGStages) * kGStageElems;
-    bf16* sx = st + kGT * kGBK;
+    const uint32_t st = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) bf16*)(ring + (kt % kGStages) * kGStageElems);
     // fragments: weight rows wc*128 + 16 i + l16, tile rows wr*64 + 16 j + l16,
     // k = 8 g .. 8 g + 7 of the stage
-    bf16x8 bx[4];
+    bf16x8 aw[8], bx[4];
+    gemm_frags(st + wc * 128 * kGBK * 2 + lofs, st + (kGT + wr * 64) * kGBK * 2 + lofs, aw, bx);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int r = wr * 64 + j * 16 + l16;
-      bx[j] = *reinterpret_cast<const bf16x8*>(sx + r * kGBK + swz(r, g) * 8);
-    }
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int r = wc * 128 + i * 16 + l16;
-      const bf16x8 aw = *reinterpret_cast<const bf16x8*>(st + r * kGBK + swz(r, g) * 8);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = mfma16(aw, bx[j], acc[i][j]);
-    }
+      for (int j = 0; j < 4; ++j) acc[i][j] = mfma16(aw[i], bx[j], acc[i][j]);
   }
 
   // ---- epilogue, two rounds of 64 channels per wave through LDS: acc[i][j][ii]
