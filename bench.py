@@ -100,7 +100,10 @@ def op_costs(w, L):
     e = 2 if w.dtype == "bf16" else 4
     c = {
         "single_proj": (S * (Cs + 2 * C) * e, 2 * S * Cs * 2 * C),
-        "pair_broadcast": (R * C * e + 2 * S * C * e, R * C),
+        # the stacks' broadcast accumulates into the pair state (z read and
+        # written) in every block but the first, so the median launch is an
+        # accumulating one
+        "pair_broadcast": (2 * R * C * e + 2 * S * C * e, R * C),
         "ln_linear": (R * 2 * C * e, 2 * R * C * C),
         "bcast_ln_linear": (2 * S * C * e + R * C * e, R * C + 2 * R * C * C),
         "attn_proj": (R * (C + 3 * C + H) * e, 2 * R * C * (3 * C + H)),
