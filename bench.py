@@ -48,18 +48,18 @@ F32_PEAK_TFLOPS = 157.3        # fp32 vector
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 COUNTERS = {  # workload: {op: (kernel source, source hash, FETCH_SIZE KiB, WRITE_SIZE KiB)}
     "pairformer4_b16_lognormal192_bf16": {
-        "attention_row": ("k_attention.hip", "1029ede52508d9db", 321692 + 8058, 174370 + 6472),
-        "attention_col": ("k_attention.hip", "1029ede52508d9db", 321692 + 8058, 174370 + 6472),
-        "triangle_out": ("k_triangle.hip", "78ed89d0163e3191", 640247, 175968),
-        "triangle_in": ("k_triangle.hip", "78ed89d0163e3191", 640247, 175968),
-        "transition": ("k_transition.hip", "e2f701d5925d7f6e", 100338 + 268, 174430 + 384),
-        "attn_proj": ("k_linear.hip", "4daf048772e304da", 87689, 528972),
-        "tri_proj": ("k_linear.hip", "4daf048772e304da", 87863, 386304),
-        "attn_out_residual": ("k_linear.hip", "4daf048772e304da", 174596, 174371),
-        "pair_broadcast": ("k_segment.hip", "8d348b78ad1740b0", 68898, 174369),
-        "segment_mean": ("k_segment.hip", "8d348b78ad1740b0", 87298, 1492),
-        "single_proj": ("k_linear.hip", "4daf048772e304da", 5281, 1492),
-        "single_update": ("k_linear.hip", "4daf048772e304da", 6024, 2237),
+        "attention_row": ("k_attention.hip", "1029ede52508d9db", 321829 + 8058, 174370 + 6472),
+        "attention_col": ("k_attention.hip", "1029ede52508d9db", 321829 + 8058, 174370 + 6472),
+        "triangle_out": ("k_triangle.hip", "78ed89d0163e3191", 637979, 175997),
+        "triangle_in": ("k_triangle.hip", "78ed89d0163e3191", 637979, 175997),
+        "transition": ("k_transition.hip", "fc86ddcdca398fdb", 102020 + 268, 174369 + 384),
+        "attn_proj": ("k_linear.hip", "8c9d00dd2754951b", 87689, 528988),
+        "tri_proj": ("k_linear.hip", "8c9d00dd2754951b", 87748, 386304),
+        "attn_out_residual": ("k_linear.hip", "8c9d00dd2754951b", 174601, 174370),
+        "pair_broadcast": ("k_segment.hip", "28f1c83801f4cc17", 68891, 174369),
+        "segment_mean": ("k_segment.hip", "28f1c83801f4cc17", 87298, 1492),
+        "single_proj": ("k_linear.hip", "8c9d00dd2754951b", 5282, 1492),
+        "single_update": ("k_linear.hip", "8c9d00dd2754951b", 6023, 2237),
     },
     "pair_b8_n208_224_bf16": {
         "transition": ("k_transition.hip", "e2f701d5925d7f6e", 53091, 91003),
