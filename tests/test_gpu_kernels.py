@@ -349,6 +349,35 @@ def test_pair_attention(B, axis, dtype, H, D, lset, bias_layout):
 
 
 @pytest.mark.parametrize("axis", [0, 1])
+@pytest.mark.parametrize("L", [ATT_LENGTHS, [300, 64, 3], [512, 257, 1, 100]], ids=["att", "mid", "mid512"])
+def test_pair_attention_masking_bias(B, axis, L):
+    """A bias that masks keys with -inf (and with huge finite negatives) on
+    valid cells: the masked keys get probability zero exactly as in the
+    oracle.  Diagonal cells are never masked, so every query keeps a key."""
+    import torch
+    H, D = 2, 32
+    lay = _layout(B, L)
+    R = sum(n * n for n in L)
+    qkv = synth.snap_bf16(_n(25, "qkv", (R, 3 * H * D), 1.0, "bf16"))
+    bias = _n(26, "bias", (R, H), 1.0, "bf16")
+    u = np.random.default_rng(27).random((R, H))
+    diag = np.zeros(R, bool)
+    for off, n in zip(np.cumsum([0] + [n * n for n in L[:-1]]), L):
+        diag[off + np.arange(n) * (n + 1)] = True
+    bias[(u < 0.3) & ~diag[:, None]] = -np.inf
+    bias[(u > 0.97) & ~diag[:, None]] = -1e35
+    c = H * D
+    qd = dev(qkv, "bf16")
+    o = torch.full((R, c), float("nan"), dtype=torch.bfloat16, device="cuda")
+    B.nt_pair_row_attention(lay, axis, H, D, qd[:, :c], qd[:, c:2 * c], qd[:, 2 * c:], o,
+                            bias=dev(_head_major(bias), "bf16"), bias_layout="heads")
+    got = host(o)
+    assert np.isfinite(got).all()
+    ref = O.pair_row_attention(qkv[:, :c], qkv[:, c:2 * c], qkv[:, 2 * c:], bias, L, H, D, axis=axis)
+    check(got, ref, "bf16", f"pair attention axis {axis} masking bias {L}")
+
+
+@pytest.mark.parametrize("axis", [0, 1])
 @pytest.mark.parametrize("dtype,H,D,lset", [("bf16", 4, 32, "att"), ("bf16", 2, 32, "mid512"),
                                             ("bf16", 2, 32, "long"), ("bf16", 2, 64, "tiny"),
                                             ("f32", 2, 8, "tiny")])
