@@ -362,6 +362,10 @@ __device__ __forceinline__ float query_max(float v) {
   return fmaxf(__uint_as_float(s32[0]), __uint_as_float(s32[1]));
 }
 
+// key-split hand-over: 10 floats per lane of 8 query slots
+constexpr int kAttnHandBytes = 10 * 8 * 64 * 4;
+constexpr int kAttnGateBytes = 16 * 1024;        // gate slots: 16 waves x 1 KB (8 when the keys are split)
+
 // ---------------------------------------------------------------- pair attention, head_dim 32
 // Pair attention for head_dim 32 and N_i <= kAttnLongLen, organised so that
 // the exponentials are nearly the only vector work.  A workgroup of NW waves
@@ -394,8 +398,9 @@ __device__ __forceinline__ float query_max(float v) {
 //     hands its running maximum and accumulators to the first through LDS,
 //     which merges them (rescaled to the larger maximum) and stores the row;
 //     a block then holds 8 query tiles.  Shorter samples use all 16 waves as
-//     query tiles.  128 KB of key/value buffers and 26 KB for the hand-over
-//     keep one workgroup per CU at four waves per SIMD;
+//     query tiles.  128 KB of key/value buffers and 20 KB for the hand-over
+//     (the gated instance adds 8 KB of gate rows) keep one workgroup per CU
+//     at four waves per SIMD;
 //   * N <= 512, 8 waves, each wave all keys (the single attention of axis 3,
 //     one row per sample).
 template <int NMAX, int NW, bool PERSIST, bool GATE = false, bool KS = false>
@@ -464,6 +469,9 @@ __global__ void __launch_bounds__(64 * NW, (NMAX <= 256 || KS) ? 4 : 2) attentio
   const int kh = __builtin_amdgcn_readfirstlane(KS && split ? wave >> 3 : 0);
   const int j0 = qt0 * 16;
   const int jw = j0 + 16 * qs + l16;            // this lane's query
+  // gate rows of this wave (gated key-split instance): 1 KB slots after the
+  // key/value buffers, past the hand-over when the keys are split
+  bf16* gslot = lds + 4 * NMAX * D + (split ? kAttnHandBytes / 2 : 0) + qs * 512;
 
   // ---- per-row staging: straight global -> LDS copies ---------------------
   // Each wave copies its key tiles (wave, wave + NW, ...; 16 keys each) with
@@ -582,8 +590,19 @@ __global__ void __launch_bounds__(64 * NW, (NMAX <= 256 || KS) ? 4 : 2) attentio
     // gate of this lane's outputs (GATE): issued before the next row's
     // copies, so waiting for it leaves those in flight; the query index is
     // clamped into the row, so the load is unconditional
+    // (key-split instance: the wave's 16 gate rows are copied into its LDS
+    // slot, lane l taking dims 8 (l % 4) .. +7 of query l / 4; held in
+    // registers across the row they were spilled, and each reload waited for
+    // the copies in flight mid-row)
     uint2 gt[2];
-    if constexpr (GATE) {
+    if constexpr (GATE && KS) {
+      if (wave_has_queries && kh == 0) {
+        const int lq = opaque(lane);
+        const int jq = min(j0 + 16 * qs + (lq >> 2), n - 1);
+        const bf16* gr = gbase + (cu + (int64_t)r * sr + (int64_t)jq * st) * p.ld_gate + 8 * (lq & 3);
+        __builtin_amdgcn_global_load_lds((const void*)gr, (__attribute__((address_space(3))) void*)gslot, 16, 0, 0);
+      }
+    } else if constexpr (GATE) {
       if (wave_has_queries && kh == 0) {
         const bf16* gr = gbase + (cu + (int64_t)r * sr + (int64_t)min(jw, n - 1) * st) * p.ld_gate + 4 * g;
         gt[0] = *reinterpret_cast<const uint2*>(gr);
@@ -698,13 +717,16 @@ __global__ void __launch_bounds__(64 * NW, (NMAX <= 256 || KS) ? 4 : 2) attentio
       if (split) {
         // the upper key half hands (max, accumulators) to its partner, which
         // merges the two partial softmax sums rescaled to the larger maximum
-        float* xf = reinterpret_cast<float*>(lds + 4 * NMAX * D);   // [13][8 slots][64 lanes]
+        // [10][8 slots][64 lanes]: the maximum, dims 4g .. +3 and 16 + 4g .. +3,
+        // and the denominator (the ones product gives it in all four elements)
+        float* xf = reinterpret_cast<float*>(lds + 4 * NMAX * D);
         if (kh == 1 && wave_has_queries) {
           xf[(0 * 8 + qs) * 64 + lane] = m_s;
 #pragma unroll
-          for (int u = 0; u < 3; ++u)
+          for (int u = 0; u < 2; ++u)
 #pragma unroll
             for (int ii = 0; ii < 4; ++ii) xf[((1 + 4 * u + ii) * 8 + qs) * 64 + lane] = O[u][ii];
+          xf[(9 * 8 + qs) * 64 + lane] = O[2][0];
         }
         __builtin_amdgcn_s_waitcnt(0xC07F);     // lgkmcnt(0): the hand-over is written (copies stay in flight)
         __builtin_amdgcn_s_barrier();
@@ -713,9 +735,10 @@ __global__ void __launch_bounds__(64 * NW, (NMAX <= 256 || KS) ? 4 : 2) attentio
           const float mm = fmaxf(m_s, m1);
           const float a0 = __builtin_amdgcn_exp2f((m_s - mm) * c), a1 = __builtin_amdgcn_exp2f((m1 - mm) * c);
 #pragma unroll
-          for (int u = 0; u < 3; ++u)
+          for (int u = 0; u < 2; ++u)
 #pragma unroll
             for (int ii = 0; ii < 4; ++ii) O[u][ii] = O[u][ii] * a0 + xf[((1 + 4 * u + ii) * 8 + qs) * 64 + lane] * a1;
+          O[2][0] = O[2][0] * a0 + xf[(9 * 8 + qs) * 64 + lane] * a1;
         }
       }
     }
@@ -725,6 +748,14 @@ __global__ void __launch_bounds__(64 * NW, (NMAX <= 256 || KS) ? 4 : 2) attentio
       // 4g .. 4g+7 and an odd one 16 + 4(g-1) .. +7: one 16-byte store per
       // lane instead of two 8-byte ones (each store instruction gathers 16
       // cells and holds the texture-address unit the copies also need)
+      if constexpr (GATE && KS) {
+        // the gate copy has landed (so have the next row's copies, which the
+        // row end waits for anyway); lane (l16, g): dims 4g .. +3, 16 + 4g .. +3
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        const bf16* gl = gslot + l16 * 32 + 4 * g;
+        gt[0] = *reinterpret_cast<const uint2*>(gl);
+        gt[1] = *reinterpret_cast<const uint2*>(gl + 16);
+      }
       const float inv = 1.f / O[2][0];
       uint32_t ow[2][2];
 #pragma unroll
@@ -1176,7 +1207,11 @@ hipError_t launch_attention(const nt_layout& L, int axis, int H, int D, const vo
     const size_t smem = sizeof(bf16) * 4 * (size_t)nmax * 32;
     const dim3 grid((unsigned)(L.pattn_items() * H));
     // the key-split instance also holds the hand-over of the upper key halves
-    const size_t smem_ks = sizeof(bf16) * 4 * (size_t)kAttnLongLen * 32 + sizeof(float) * 13 * 8 * 64;
+    const size_t smem_ks = sizeof(bf16) * 4 * (size_t)kAttnLongLen * 32 + kAttnHandBytes;
+    // gated: split rows add 8 gate slots past the hand-over, unsplit rows
+    // use 16 slots from its start
+    const size_t smem_ksg = sizeof(bf16) * 4 * (size_t)kAttnLongLen * 32 +
+                            std::max<size_t>(kAttnHandBytes + kAttnGateBytes / 2, kAttnGateBytes);
     if (gate) {
       // gated output (axes 0 and 1): the GATE instances of the same kernels
       if (nmax == kAttnShortLen) {
@@ -1185,8 +1220,8 @@ hipError_t launch_attention(const nt_layout& L, int axis, int H, int D, const vo
         hipFuncSetAttribute((const void*)attention_pair_kernel<kAttnShortLen, 16, true, true>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
         attention_pair_kernel<kAttnShortLen, 16, true, true><<<gridp, dim3(1024), smem, s>>>(a);
       } else {
-        hipFuncSetAttribute((const void*)attention_pair_kernel<kAttnLongLen, 16, false, true, true>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem_ks);
-        attention_pair_kernel<kAttnLongLen, 16, false, true, true><<<grid, dim3(1024), smem_ks, s>>>(a);
+        hipFuncSetAttribute((const void*)attention_pair_kernel<kAttnLongLen, 16, false, true, true>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem_ksg);
+        attention_pair_kernel<kAttnLongLen, 16, false, true, true><<<grid, dim3(1024), smem_ksg, s>>>(a);
       }
     } else if (axis == 3) {
       // single attention with pair bias: one row per sample, the 8-wave
