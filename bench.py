@@ -48,8 +48,8 @@ F32_PEAK_TFLOPS = 157.3        # fp32 vector
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 COUNTERS = {  # workload: {op: (kernel source, source hash, FETCH_SIZE KiB, WRITE_SIZE KiB)}
     "pairformer4_b16_lognormal192_bf16": {
-        "attention_row": ("k_attention.hip", "1029ede52508d9db", 321829 + 8058, 174370 + 6472),
-        "attention_col": ("k_attention.hip", "1029ede52508d9db", 321829 + 8058, 174370 + 6472),
+        "attention_row": ("k_attention.hip", "87a973263a55fff9", 321637 + 8058, 174371 + 6472),
+        "attention_col": ("k_attention.hip", "87a973263a55fff9", 321637 + 8058, 174371 + 6472),
         "triangle_out": ("k_triangle.hip", "78ed89d0163e3191", 637979, 175997),
         "triangle_in": ("k_triangle.hip", "78ed89d0163e3191", 637979, 175997),
         "transition": ("k_transition.hip", "fc86ddcdca398fdb", 102020 + 268, 174369 + 384),
